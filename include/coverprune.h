@@ -1,0 +1,168 @@
+/*
+ * coverprune.h -- C-ABI of the CoverPrune hot path for AMD Instinct MI355X (gfx950).
+ *
+ * CoverPrune (arXiv 2608.13226) prunes the N visual tokens of a video to K
+ * tokens that best cover the scene in an optimal-transport sense.  This
+ * library computes, on one GPU:
+ *
+ *   coverprune_fst_cost    the Feature-Spatial-Temporal transport cost between
+ *                          every pair of tokens (Sec. 3.3, Eq. 7-8);
+ *   coverprune_sgs_select  greedy selection of K tokens against that cost and
+ *                          the target capacities (Sec. 3.5, Eq. 11-16);
+ *   coverprune_lite_select CoverPrune-Lite: Morton ordering, capacity-guided
+ *                          grouping and per-group prototypes (Sec. 4, Eq. 17-20).
+ *
+ * Conventions shared by every entry point
+ *   - Token j has a feature row f_j (D values), a 3D position x_j (metres) and
+ *     the integer index tau_j of the frame it came from (problem setup, Sec. 3.2).
+ *   - Every array argument is DEVICE memory owned by the caller, row-major and
+ *     densely packed.  The library keeps no pointer after a call returns and
+ *     allocates no memory: scratch space is the caller's workspace, sized by
+ *     the matching *_workspace() query.  Workspace and array pointers must be
+ *     16-byte aligned.
+ *   - Calls are asynchronous: work is enqueued on `stream` (a hipStream_t; NULL
+ *     is the default stream) and results are valid once the stream has
+ *     completed it.  No call synchronises the host with the device.
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     failed check returns an error status and enqueues nothing.  Data values
+ *     are not checked (finite inputs, capacities >= 0 with a positive sum are
+ *     the caller's duty).  coverprune_last_error() describes the last failure
+ *     of the calling thread.
+ *   - Results are bitwise reproducible run to run on the same GPU.  Calls on
+ *     distinct workspaces and streams may run concurrently.
+ */
+#ifndef COVERPRUNE_H
+#define COVERPRUNE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CP_OK = 0,
+  CP_ERR_INVALID_ARG = 1, /* a scalar out of range or a required pointer is NULL */
+  CP_ERR_UNSUPPORTED = 2, /* a dtype, feature width or flag this build does not handle */
+  CP_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the query returned */
+  CP_ERR_HIP = 4          /* the HIP runtime reported an error while enqueuing */
+} cp_status;
+
+typedef enum { CP_F32 = 0, CP_BF16 = 1 } cp_dtype;
+
+/* Weights of Eq. 8.  lambda_* >= 0 weight the feature, spatial and temporal
+ * terms; kappa >= 0 shapes phi_kappa(z) = log(1 + kappa z) / log(1 + kappa),
+ * with kappa = 0 taken as the kappa -> 0 limit phi(z) = z.  The paper's
+ * experiments use lambda = 1 (Sec. 5.1) and give no kappa. */
+typedef struct {
+  float lambda_f;
+  float lambda_x;
+  float lambda_tau;
+  float kappa;
+} cp_fst_weights;
+
+/* SGS flags. */
+#define CP_SGS_DENSE 0u /* every step re-evaluates every candidate's gain over the whole cost matrix */
+
+/* ------------------------------------------------------------------------ */
+/* FST transport cost (Sec. 3.3, Eq. 7-8).
+ *
+ * For source (retained) token s and target token t:
+ *   d_f = 1 - cos(f_s, f_t),  d_x = |x_s - x_t|_2,  d_tau = max(0, tau_s - tau_t)
+ *   C(s, t) = lambda_f d_f / M_f + lambda_x phi_kappa(d_x / M_x) + lambda_tau d_tau / M_tau
+ * where each M is that discrepancy's maximum over all N^2 ordered pairs of the
+ * scene ("min-max normalised within the sample"; the minimum is 0 because
+ * d(t, t) = 0); a term whose M is 0 is 0.  cos with a zero-norm feature is 0,
+ * d_f is clamped to [0, 2] and d_f(t, t) = 0.
+ *
+ *   feats   [n, d] features, dtype CP_F32 (float) or CP_BF16 (bfloat16);
+ *           d % 8 == 0 for CP_BF16 and d % 4 == 0 for CP_F32
+ *   pos     [n, 3] float positions in metres
+ *   frame   [n] int32 frame indices
+ *   cost    [n, n] float output, TARGET-MAJOR: cost[t * n + s] = C(s, t), so
+ *           row t lists what every candidate s would pay to cover t
+ *   maxima  [3] float output (may be NULL): M_f, M_x, M_tau
+ *   Accumulation: features are multiplied in their storage type and summed in
+ *   float32 (bfloat16 products on the matrix cores).
+ */
+size_t coverprune_fst_cost_workspace(int64_t n, int64_t d, cp_dtype dtype);
+cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int64_t d,
+                              const float* pos, const int32_t* frame, cp_fst_weights w,
+                              float* cost, float* maxima, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Spatial-Guided Greedy Selection (Sec. 3.5, Eq. 11-16).
+ *
+ * Greedy over the coverage loss L(S) = sum_j v_j min(c0, min_{s in S} C(s, j)):
+ * each step adds the unselected candidate c with the largest gain
+ *   gain(c) = sum_j v_j max(0, b_j - C(c, j)),   b_j = min(c0, min_{s in S} C(s, j)),
+ * i.e. the largest decrease of L (the free-source, epsilon -> 0 limit of the
+ * semi-relaxed transport of Eq. 11-12, with every target as a neighbour,
+ * g = N in Eq. 13).  Equal gains go to the smaller index; exactly k tokens
+ * are selected even when gains reach 0.  Gains and L are summed in float64.
+ *
+ *   cost      [n, n] float, target-major as written by coverprune_fst_cost
+ *   capacity  [n] float target capacities v (Sec. 3.4), v >= 0
+ *   k         1 <= k <= n
+ *   c0        cost of leaving a target uncovered; lambda_f + lambda_x +
+ *             lambda_tau (the largest value C can take) is the usual choice
+ *   flags     CP_SGS_DENSE
+ *   selected        [k] int32 output: tokens in the order they were chosen
+ *   step_gain       [k] double output (may be NULL): gain of each step
+ *   step_objective  [k] double output (may be NULL): L(S) after each step
+ *   assign          [n] int32 output (may be NULL): for each target the chosen
+ *                   token that covers it most cheaply (the earliest chosen among
+ *                   equals), or -1 if no chosen token costs less than c0
+ */
+size_t coverprune_sgs_workspace(int64_t n, int64_t k);
+cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capacity, int64_t k,
+                                float c0, uint32_t flags, int32_t* selected, double* step_gain,
+                                double* step_objective, int32_t* assign, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* CoverPrune-Lite (Sec. 4, Eq. 17-20).
+ *
+ *  1. Morton order: per axis q = floor((x - min_x) * (256 / voxel_size)) in
+ *     float64, clamped to [0, 2^21 - 1]; key = bit interleave of (qx, qy, qz)
+ *     with x in bit 0; tokens sorted by (key, index).  A token's voxel is
+ *     q >> 8, so each voxel of edge voxel_size is a contiguous run.
+ *  2. Groups (Eq. 17): V_j = floor(v_j * 2^40) in exact integers, W = sum V.
+ *     Walking the order, the current group q closes before token p when
+ *     K * (sum of V before p) >= (q + 1) * W, or when the tokens left equal
+ *     the groups left; this yields exactly k non-empty contiguous groups of
+ *     about 1/k capacity each.
+ *  3. Costs: pairs in one group whose voxels are within one cell on every
+ *     axis (27 neighbouring cells) cost C of Eq. 8 with M_f, M_x, M_tau taken
+ *     over those pairs (diagonal included); other same-group pairs cost
+ *     c0 = lambda_f + lambda_x + lambda_tau.
+ *  4. Prototype of group q (Eq. 18): argmin over t in G_q of sum_{j in G_q}
+ *     v_j C(t, j); ties to the smaller token index.
+ *
+ *   feats, dtype, n, d, pos, frame, w: as for coverprune_fst_cost
+ *   capacity    [n] float target capacities, v >= 0, 0 < sum v < 2^20
+ *   k           1 <= k <= n, k < 2^23
+ *   voxel_size  voxel edge in metres, > 0
+ *   selected    [k] int32 output: selected[q] is the prototype of group q
+ *   group       [n] int32 output (may be NULL): group of every token
+ *   objective   [1] double output (may be NULL): sum over groups of the
+ *               prototype's cost, the block-plan transport cost of Eq. 20
+ */
+size_t coverprune_lite_workspace(int64_t n, int64_t d, int64_t k, cp_dtype dtype);
+cp_status coverprune_lite_select(const void* feats, cp_dtype dtype, int64_t n, int64_t d,
+                                 const float* pos, const int32_t* frame, const float* capacity,
+                                 int64_t k, cp_fst_weights w, float voxel_size, int32_t* selected,
+                                 int32_t* group, double* objective, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+const char* coverprune_status_string(cp_status status); /* static text, never NULL */
+const char* coverprune_last_error(void);                /* thread-local; "" if none */
+int coverprune_abi_version(void);                       /* 1 */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* COVERPRUNE_H */

@@ -1,0 +1,216 @@
+"""CoverPrune's hot path on AMD Instinct MI355X.
+
+Python binding of ``libcoverprune.so`` (C-ABI in include/coverprune.h).  The
+functions here only check and marshal torch tensors: every step runs in the
+library's HIP kernels.  Tensors must live on the current GPU; work is
+enqueued on torch's current stream and nothing synchronises the host.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+__all__ = ["fst_cost", "sgs_select", "lite_select", "library", "library_path", "CoverPruneError",
+           "DEFAULT_KAPPA"]
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_NAME = "libcoverprune.so"
+
+# The paper leaves kappa open (Sec. 3.3 only requires kappa > 0).
+DEFAULT_KAPPA = 10.0
+
+CP_F32, CP_BF16 = 0, 1
+CP_SGS_DENSE = 0
+
+
+class CoverPruneError(RuntimeError):
+    pass
+
+
+class _Weights(ctypes.Structure):
+    _fields_ = [("lambda_f", ctypes.c_float), ("lambda_x", ctypes.c_float),
+                ("lambda_tau", ctypes.c_float), ("kappa", ctypes.c_float)]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return os.path.join(HERE, _LIB_NAME)
+
+
+def library() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise CoverPruneError(f"{path} is missing: build it with `python -m paper_2608_13226_amd.build`")
+    lib = ctypes.CDLL(path)
+    i64, sz, vp, u32 = ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_uint32
+    st = ctypes.c_int
+    lib.coverprune_fst_cost_workspace.argtypes = [i64, i64, ctypes.c_int]
+    lib.coverprune_fst_cost_workspace.restype = sz
+    lib.coverprune_fst_cost.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, _Weights, vp, vp, vp, sz, vp]
+    lib.coverprune_fst_cost.restype = st
+    lib.coverprune_sgs_workspace.argtypes = [i64, i64]
+    lib.coverprune_sgs_workspace.restype = sz
+    lib.coverprune_sgs_select.argtypes = [vp, i64, vp, i64, ctypes.c_float, u32, vp, vp, vp, vp, vp, sz, vp]
+    lib.coverprune_sgs_select.restype = st
+    lib.coverprune_lite_workspace.argtypes = [i64, i64, i64, ctypes.c_int]
+    lib.coverprune_lite_workspace.restype = sz
+    lib.coverprune_lite_select.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, vp, i64, _Weights,
+                                           ctypes.c_float, vp, vp, vp, vp, sz, vp]
+    lib.coverprune_lite_select.restype = st
+    lib.coverprune_status_string.argtypes = [st]
+    lib.coverprune_status_string.restype = ctypes.c_char_p
+    lib.coverprune_last_error.argtypes = []
+    lib.coverprune_last_error.restype = ctypes.c_char_p
+    lib.coverprune_abi_version.argtypes = []
+    lib.coverprune_abi_version.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        lib = library()
+        raise CoverPruneError(f"{lib.coverprune_status_string(status).decode()}: "
+                              f"{lib.coverprune_last_error().decode()}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype, shape, device) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _feature_dtype(feats: torch.Tensor) -> int:
+    if feats.dtype == torch.bfloat16:
+        return CP_BF16
+    if feats.dtype == torch.float32:
+        return CP_F32
+    raise TypeError(f"features must be bfloat16 or float32, got {feats.dtype}")
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+
+
+def _weights(weights, kappa) -> _Weights:
+    lf, lx, lt = (float(w) for w in weights)
+    return _Weights(lf, lx, lt, float(kappa))
+
+
+def fst_cost(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor,
+             weights=(1.0, 1.0, 1.0), kappa: float = DEFAULT_KAPPA,
+             out: Optional[torch.Tensor] = None, maxima: Optional[torch.Tensor] = None,
+             workspace: Optional[torch.Tensor] = None, stream=None):
+    """FST transport cost (Sec. 3.3, Eq. 7-8), target-major: out[t, s] = C(s, t).
+
+    Returns (cost [n, n] float32, maxima [3] float32 = M_f, M_x, M_tau)."""
+    lib = library()
+    n, d = feats.shape
+    dev = feats.device
+    dt = _feature_dtype(feats)
+    _need(feats, "feats", feats.dtype, (n, d), dev)
+    _need(pos, "pos", torch.float32, (n, 3), dev)
+    _need(frame, "frame", torch.int32, (n,), dev)
+    if out is None:
+        out = torch.empty((n, n), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, (n, n), dev)
+    if maxima is None:
+        maxima = torch.empty(3, dtype=torch.float32, device=dev)
+    _need(maxima, "maxima", torch.float32, (3,), dev)
+    need = lib.coverprune_fst_cost_workspace(n, d, dt)
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    _check(lib.coverprune_fst_cost(_ptr(feats), dt, n, d, _ptr(pos), _ptr(frame), _weights(weights, kappa),
+                                   _ptr(out), _ptr(maxima), _ptr(workspace), workspace.numel(),
+                                   _stream(stream)))
+    return out, maxima
+
+
+@dataclass
+class SgsResult:
+    selected: torch.Tensor     # [k] int32, greedy order
+    gain: torch.Tensor         # [k] float64
+    objective: torch.Tensor    # [k] float64, L(S) after each step
+    assign: torch.Tensor       # [n] int32
+
+
+def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[float] = None,
+               weights=(1.0, 1.0, 1.0), workspace: Optional[torch.Tensor] = None,
+               stream=None) -> SgsResult:
+    """Greedy selection of k tokens over a target-major cost (Sec. 3.5, Eq. 11-16).
+    c0 defaults to the sum of the cost weights, the largest value C takes."""
+    lib = library()
+    n = cost.shape[0]
+    dev = cost.device
+    _need(cost, "cost", torch.float32, (n, n), dev)
+    _need(capacity, "capacity", torch.float32, (n,), dev)
+    if c0 is None:
+        c0 = float(sum(float(w) for w in weights))
+    sel = torch.empty(int(k), dtype=torch.int32, device=dev)
+    gain = torch.empty(int(k), dtype=torch.float64, device=dev)
+    obj = torch.empty(int(k), dtype=torch.float64, device=dev)
+    assign = torch.empty(n, dtype=torch.int32, device=dev)
+    need = lib.coverprune_sgs_workspace(n, int(k))
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    _check(lib.coverprune_sgs_select(_ptr(cost), n, _ptr(capacity), int(k), float(c0), CP_SGS_DENSE,
+                                     _ptr(sel), _ptr(gain), _ptr(obj), _ptr(assign), _ptr(workspace),
+                                     workspace.numel(), _stream(stream)))
+    return SgsResult(sel, gain, obj, assign)
+
+
+@dataclass
+class LiteResult:
+    selected: torch.Tensor     # [k] int32, prototype of group q at [q]
+    group: torch.Tensor        # [n] int32
+    objective: torch.Tensor    # [1] float64
+
+
+def lite_select(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor, capacity: torch.Tensor,
+                k: int, weights=(1.0, 1.0, 1.0), kappa: float = DEFAULT_KAPPA, voxel_size: float = 0.25,
+                workspace: Optional[torch.Tensor] = None, stream=None) -> LiteResult:
+    """CoverPrune-Lite (Sec. 4, Eq. 17-20)."""
+    lib = library()
+    n, d = feats.shape
+    dev = feats.device
+    dt = _feature_dtype(feats)
+    _need(feats, "feats", feats.dtype, (n, d), dev)
+    _need(pos, "pos", torch.float32, (n, 3), dev)
+    _need(frame, "frame", torch.int32, (n,), dev)
+    _need(capacity, "capacity", torch.float32, (n,), dev)
+    sel = torch.empty(int(k), dtype=torch.int32, device=dev)
+    group = torch.empty(n, dtype=torch.int32, device=dev)
+    obj = torch.empty(1, dtype=torch.float64, device=dev)
+    need = lib.coverprune_lite_workspace(n, d, int(k), dt)
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    _check(lib.coverprune_lite_select(_ptr(feats), dt, n, d, _ptr(pos), _ptr(frame), _ptr(capacity), int(k),
+                                      _weights(weights, kappa), float(voxel_size), _ptr(sel), _ptr(group),
+                                      _ptr(obj), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return LiteResult(sel, group, obj)

@@ -1,0 +1,228 @@
+// C-ABI entry points of the CoverPrune library: host-side argument checks,
+// workspace carving and kernel dispatch.  Nothing here touches device data.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/coverprune.h"
+#include "launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+cp_status fail(cp_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+cp_status ok() {
+  g_last_error.clear();
+  return CP_OK;
+}
+
+cp_status hip_fail(hipError_t e, const char* where) {
+  return fail(CP_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+constexpr int64_t kMaxDenseN = int64_t(1) << 18;   // cost matrix of 256 GiB
+constexpr int64_t kMaxLiteN = int64_t(1) << 24;
+constexpr int64_t kMaxD = int64_t(1) << 16;
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+cp_status check_features(const void* feats, cp_dtype dtype, int64_t n, int64_t d, int64_t max_n) {
+  if (n < 1 || n > max_n) return fail(CP_ERR_INVALID_ARG, "n = %lld outside [1, %lld]", (long long)n, (long long)max_n);
+  if (d < 1 || d > kMaxD) return fail(CP_ERR_INVALID_ARG, "d = %lld outside [1, %lld]", (long long)d, (long long)kMaxD);
+  if (dtype != CP_F32 && dtype != CP_BF16) return fail(CP_ERR_UNSUPPORTED, "unknown feature dtype %d", (int)dtype);
+  if (dtype == CP_BF16 && d % 8 != 0) return fail(CP_ERR_UNSUPPORTED, "bf16 features need d %% 8 == 0 (d = %lld)", (long long)d);
+  if (dtype == CP_F32 && d % 4 != 0) return fail(CP_ERR_UNSUPPORTED, "f32 features need d %% 4 == 0 (d = %lld)", (long long)d);
+  if (!feats) return fail(CP_ERR_INVALID_ARG, "feats is NULL");
+  if (!aligned16(feats)) return fail(CP_ERR_INVALID_ARG, "feats is not 16-byte aligned");
+  return CP_OK;
+}
+
+cp_status check_weights(const cp_fst_weights& w) {
+  const float v[4] = {w.lambda_f, w.lambda_x, w.lambda_tau, w.kappa};
+  for (float x : v)
+    if (!std::isfinite(x) || x < 0.f) return fail(CP_ERR_INVALID_ARG, "weights and kappa must be finite and >= 0");
+  return CP_OK;
+}
+
+cp_status check_workspace(void* ws, size_t have, size_t need) {
+  if (need == 0) return CP_OK;
+  if (!ws) return fail(CP_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (!aligned16(ws)) return fail(CP_ERR_WORKSPACE, "workspace is not 16-byte aligned");
+  if (have < need) return fail(CP_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return CP_OK;
+}
+
+float inv_log1p(float kappa) { return kappa > 0.f ? float(1.0 / std::log1p(double(kappa))) : 0.f; }
+
+}  // namespace
+
+extern "C" {
+
+const char* coverprune_status_string(cp_status s) {
+  switch (s) {
+    case CP_OK: return "ok";
+    case CP_ERR_INVALID_ARG: return "invalid argument";
+    case CP_ERR_UNSUPPORTED: return "unsupported";
+    case CP_ERR_WORKSPACE: return "workspace too small";
+    case CP_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* coverprune_last_error(void) { return g_last_error.c_str(); }
+
+int coverprune_abi_version(void) { return 1; }
+
+// ---------------------------------------------------------------------------
+size_t coverprune_fst_cost_workspace(int64_t n, int64_t d, cp_dtype dtype) {
+  (void)d;
+  (void)dtype;
+  if (n < 1) return 0;
+  return align_up(size_t(n) * sizeof(float)) + kAlign;
+}
+
+cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int64_t d,
+                              const float* pos, const int32_t* frame, cp_fst_weights w,
+                              float* cost, float* maxima, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  cp_status st = check_features(feats, dtype, n, d, kMaxDenseN);
+  if (st != CP_OK) return st;
+  if (!pos || !frame || !cost) return fail(CP_ERR_INVALID_ARG, "pos, frame and cost must be non-NULL");
+  if (!aligned16(cost)) return fail(CP_ERR_INVALID_ARG, "cost is not 16-byte aligned");
+  if ((st = check_weights(w)) != CP_OK) return st;
+  const size_t need = coverprune_fst_cost_workspace(n, d, dtype);
+  if ((st = check_workspace(workspace, workspace_bytes, need)) != CP_OK) return st;
+
+  char* base = static_cast<char*>(workspace);
+  cp::FstScratch s;
+  s.inv_norm = reinterpret_cast<float*>(base);
+  char* tail = base + align_up(size_t(n) * sizeof(float));
+  s.mf_bits = reinterpret_cast<unsigned int*>(tail);
+  s.tau_min = reinterpret_cast<int*>(tail + 4);
+  s.tau_max = reinterpret_cast<int*>(tail + 8);
+  s.mx2_bits = reinterpret_cast<unsigned long long*>(tail + 16);
+
+  cp::FstParams p;
+  p.feats = feats;
+  p.bf16 = dtype == CP_BF16;
+  p.n = int(n);
+  p.d = int(d);
+  p.pos = pos;
+  p.frame = frame;
+  p.lambda_f = w.lambda_f;
+  p.lambda_x = w.lambda_x;
+  p.lambda_tau = w.lambda_tau;
+  p.kappa = w.kappa;
+  p.inv_log1p_kappa = inv_log1p(w.kappa);
+  p.cost = cost;
+  p.maxima = maxima;
+
+  hipStream_t s_ = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if ((e = cp::launch_fst_prep(p, s, s_)) != hipSuccess) return hip_fail(e, "fst prep");
+  if ((e = cp::launch_gram(p, s, s_)) != hipSuccess) return hip_fail(e, "gram");
+  if ((e = cp::launch_fst_epilogue(p, s, s_)) != hipSuccess) return hip_fail(e, "fst epilogue");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+size_t coverprune_sgs_workspace(int64_t n, int64_t k) {
+  (void)k;
+  if (n < 1) return 0;
+  return cp::sgs_workspace_bytes(n);
+}
+
+cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capacity, int64_t k,
+                                float c0, uint32_t flags, int32_t* selected, double* step_gain,
+                                double* step_objective, int32_t* assign, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  if (n < 1 || n > kMaxDenseN) return fail(CP_ERR_INVALID_ARG, "n = %lld outside [1, %lld]", (long long)n, (long long)kMaxDenseN);
+  if (k < 1 || k > n) return fail(CP_ERR_INVALID_ARG, "k = %lld outside [1, n = %lld]", (long long)k, (long long)n);
+  if (!std::isfinite(c0)) return fail(CP_ERR_INVALID_ARG, "c0 must be finite");
+  if (flags != CP_SGS_DENSE) return fail(CP_ERR_UNSUPPORTED, "unknown flags 0x%x", flags);
+  if (!cost || !capacity || !selected) return fail(CP_ERR_INVALID_ARG, "cost, capacity and selected must be non-NULL");
+  if (!aligned16(cost)) return fail(CP_ERR_INVALID_ARG, "cost is not 16-byte aligned");
+  cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_workspace(n, k));
+  if (st != CP_OK) return st;
+
+  cp::SgsParams p;
+  p.cost = cost;
+  p.n = int(n);
+  p.capacity = capacity;
+  p.k = int(k);
+  p.c0 = c0;
+  p.selected = selected;
+  p.step_gain = step_gain;
+  p.step_objective = step_objective;
+  p.assign = assign;
+  p.workspace = workspace;
+  p.workspace_bytes = workspace_bytes;
+  hipError_t e = cp::launch_sgs_dense(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sgs");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+size_t coverprune_lite_workspace(int64_t n, int64_t d, int64_t k, cp_dtype dtype) {
+  (void)d;
+  (void)dtype;
+  if (n < 1 || k < 1) return 0;
+  return cp::lite_workspace_bytes(n, k);
+}
+
+cp_status coverprune_lite_select(const void* feats, cp_dtype dtype, int64_t n, int64_t d,
+                                 const float* pos, const int32_t* frame, const float* capacity,
+                                 int64_t k, cp_fst_weights w, float voxel_size, int32_t* selected,
+                                 int32_t* group, double* objective, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  cp_status st = check_features(feats, dtype, n, d, kMaxLiteN);
+  if (st != CP_OK) return st;
+  if (k < 1 || k > n) return fail(CP_ERR_INVALID_ARG, "k = %lld outside [1, n = %lld]", (long long)k, (long long)n);
+  if (k >= (int64_t(1) << 23)) return fail(CP_ERR_INVALID_ARG, "k = %lld must be below 2^23", (long long)k);
+  if (!pos || !frame || !capacity || !selected) return fail(CP_ERR_INVALID_ARG, "pos, frame, capacity and selected must be non-NULL");
+  if ((st = check_weights(w)) != CP_OK) return st;
+  if (!std::isfinite(voxel_size) || !(voxel_size > 0.f)) return fail(CP_ERR_INVALID_ARG, "voxel_size must be finite and > 0");
+  if ((st = check_workspace(workspace, workspace_bytes, coverprune_lite_workspace(n, d, k, dtype))) != CP_OK) return st;
+
+  cp::LiteParams p;
+  p.feats = feats;
+  p.bf16 = dtype == CP_BF16;
+  p.n = int(n);
+  p.d = int(d);
+  p.pos = pos;
+  p.frame = frame;
+  p.capacity = capacity;
+  p.k = int(k);
+  p.lambda_f = w.lambda_f;
+  p.lambda_x = w.lambda_x;
+  p.lambda_tau = w.lambda_tau;
+  p.kappa = w.kappa;
+  p.inv_log1p_kappa = w.kappa > 0.f ? 1.0 / std::log1p(double(w.kappa)) : 0.0;
+  p.grid_scale = 256.0 / double(voxel_size);
+  p.selected = selected;
+  p.group = group;
+  p.objective = objective;
+  p.workspace = workspace;
+  p.workspace_bytes = workspace_bytes;
+  hipError_t e = cp::launch_lite(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "lite");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,224 @@
+// FST transport cost, everything except the feature Gram (Sec. 3.3, Eq. 7-8).
+//
+//   prep      inverse feature norms, frame-index range (M_tau) and the exact
+//             maximum pairwise distance (M_x, over all N^2 pairs)
+//   epilogue  turns the Gram's raw d_f (upper tiles only) into the final
+//             target-major cost C_tm[t][s] = C(s, t), writing both triangles
+#include <hip/hip_runtime.h>
+
+#include <climits>
+
+#include "common.h"
+#include "launch.h"
+
+namespace cp {
+namespace {
+
+__global__ void fst_init_kernel(FstScratch s) {
+  *s.mf_bits = 0u;
+  *s.mx2_bits = 0ull;
+  *s.tau_min = INT_MAX;
+  *s.tau_max = INT_MIN;
+}
+
+// One wave per feature row: inverse norm.  The block also folds its rows'
+// frame indices into the global range.
+template <bool BF16>
+__global__ __launch_bounds__(256) void row_norm_kernel(const void* feats, int n, int d,
+                                                       const int32_t* frame, FstScratch s) {
+  const int lane = threadIdx.x & 63, wib = threadIdx.x >> 6;
+  const int row = blockIdx.x * 4 + wib;
+  float acc = 0.f;
+  if (row < n) {
+    if (BF16) {
+      const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(feats) + size_t(row) * d);
+      for (int i = lane; i < d / 8; i += 64) {
+        const uint4 q = p[i];
+        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const float lo = bf16_bits_to_float(w[h] & 0xffffu), hi = bf16_bits_to_float(w[h] >> 16);
+          acc = fmaf(lo, lo, acc);
+          acc = fmaf(hi, hi, acc);
+        }
+      }
+    } else {
+      const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(feats) + size_t(row) * d);
+      for (int i = lane; i < d / 4; i += 64) {
+        const float4 q = p[i];
+        acc = fmaf(q.x, q.x, acc);
+        acc = fmaf(q.y, q.y, acc);
+        acc = fmaf(q.z, q.z, acc);
+        acc = fmaf(q.w, q.w, acc);
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if (row < n && lane == 0) s.inv_norm[row] = acc > 0.f ? 1.0f / sqrtf(acc) : 0.f;
+
+  __shared__ int smin[4], smax[4];
+  const int f = row < n ? frame[row] : 0;
+  if (lane == 0) {
+    smin[wib] = row < n ? f : INT_MAX;
+    smax[wib] = row < n ? f : INT_MIN;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int lo = smin[0], hi = smax[0];
+    for (int w = 1; w < 4; ++w) {
+      lo = min(lo, smin[w]);
+      hi = max(hi, smax[w]);
+    }
+    if (lo != INT_MAX) {
+      atomicMin(s.tau_min, lo);
+      atomicMax(s.tau_max, hi);
+    }
+  }
+}
+
+// Upper-triangular tile index b -> (ti <= tj).
+__device__ __forceinline__ void upper_tile(int b, int& ti, int& tj) {
+  int j = int((sqrt(8.0 * double(b) + 1.0) - 1.0) * 0.5);
+  while (j * (j + 1) / 2 > b) --j;
+  while ((j + 1) * (j + 2) / 2 <= b) ++j;
+  tj = j;
+  ti = b - j * (j + 1) / 2;
+}
+
+// Squared distance in float64 with a fixed operation order and no fused
+// multiply-add, so the maximum is bitwise reproducible.
+__device__ __forceinline__ double sq_dist(double ax, double ay, double az, double bx, double by,
+                                          double bz) {
+#pragma clang fp contract(off)
+  const double dx = ax - bx, dy = ay - by, dz = az - bz;
+  return (dx * dx + dy * dy) + dz * dz;
+}
+
+constexpr int kPosTile = 256;
+
+__global__ __launch_bounds__(256) void pos_pairmax_kernel(const float* pos, int n, FstScratch s) {
+  int ti, tj;
+  upper_tile(blockIdx.x, ti, tj);
+  __shared__ double sx[kPosTile], sy[kPosTile], sz[kPosTile];
+  const int j = tj * kPosTile + threadIdx.x;
+  const int jn = min(kPosTile, n - tj * kPosTile);
+  if (threadIdx.x < jn) {
+    sx[threadIdx.x] = pos[3 * j];
+    sy[threadIdx.x] = pos[3 * j + 1];
+    sz[threadIdx.x] = pos[3 * j + 2];
+  }
+  __syncthreads();
+  const int i = ti * kPosTile + threadIdx.x;
+  double best = 0.0;
+  if (i < n) {
+    const double x = pos[3 * i], y = pos[3 * i + 1], z = pos[3 * i + 2];
+    for (int jj = 0; jj < jn; ++jj) best = fmax(best, sq_dist(x, y, z, sx[jj], sy[jj], sz[jj]));
+  }
+  best = wave_max(best);
+  if ((threadIdx.x & 63) == 0) atomic_max_nonneg(s.mx2_bits, best);
+}
+
+// ---------------------------------------------------------------------------
+constexpr int kEpiTile = 64;
+
+__device__ __forceinline__ float phi_kappa(float z, float kappa, float inv_log1p_kappa) {
+  return kappa > 0.f ? log1pf(kappa * z) * inv_log1p_kappa : z;
+}
+
+// Block = one upper tile pair (ti <= tj) of 64 x 64.  The upper tile holds
+// d_f(i, j) from the Gram (rows i in ti, columns j in tj).  It becomes
+// C_tm[i][j] = C(s = j, t = i) in place, and its mirror C_tm[j][i] = C(s = i, t = j)
+// is staged through LDS and written transposed.
+__global__ __launch_bounds__(256) void fst_epilogue_kernel(FstParams p, FstScratch s) {
+  int ti, tj;
+  upper_tile(blockIdx.x, ti, tj);
+  const int n = p.n;
+  __shared__ float rx[kEpiTile], ry[kEpiTile], rz[kEpiTile], cx[kEpiTile], cy[kEpiTile], cz[kEpiTile];
+  __shared__ int rf[kEpiTile], cf[kEpiTile];
+  __shared__ float tr[kEpiTile][kEpiTile + 1];
+
+  const int t = threadIdx.x;
+  if (t < kEpiTile) {
+    const int i = ti * kEpiTile + t;
+    if (i < n) {
+      rx[t] = p.pos[3 * i];
+      ry[t] = p.pos[3 * i + 1];
+      rz[t] = p.pos[3 * i + 2];
+      rf[t] = p.frame[i];
+    }
+  } else if (t < 2 * kEpiTile) {
+    const int c = t - kEpiTile, j = tj * kEpiTile + c;
+    if (j < n) {
+      cx[c] = p.pos[3 * j];
+      cy[c] = p.pos[3 * j + 1];
+      cz[c] = p.pos[3 * j + 2];
+      cf[c] = p.frame[j];
+    }
+  }
+
+  const float m_f = __uint_as_float(*s.mf_bits);
+  const float m_x = float(sqrt(__longlong_as_double((long long)*s.mx2_bits)));
+  const int m_t = *s.tau_max - *s.tau_min;
+  if (blockIdx.x == 0 && t == 0 && p.maxima) {
+    p.maxima[0] = m_f;
+    p.maxima[1] = m_x;
+    p.maxima[2] = float(m_t);
+  }
+  const float wf = m_f > 0.f ? p.lambda_f / m_f : 0.f;
+  const float inv_mx = m_x > 0.f ? 1.f / m_x : 0.f;
+  const float wt = m_t > 0 ? p.lambda_tau / float(m_t) : 0.f;
+  __syncthreads();
+
+  const int c = t & 63;
+  const int j = tj * kEpiTile + c;
+  const bool mirror = ti != tj;
+#pragma unroll 4
+  for (int r = t >> 6; r < kEpiTile; r += 4) {
+    const int i = ti * kEpiTile + r;
+    if (i < n && j < n) {
+      const size_t at = size_t(i) * n + j;
+      const float df = p.cost[at];
+      const float dx = rx[r] - cx[c], dy = ry[r] - cy[c], dz = rz[r] - cz[c];
+      const float dist = sqrtf(dx * dx + dy * dy + dz * dz);
+      const float base = wf * df + p.lambda_x * phi_kappa(dist * inv_mx, p.kappa, p.inv_log1p_kappa);
+      p.cost[at] = base + wt * float(max(0, cf[c] - rf[r]));
+      if (mirror) tr[c][r] = base + wt * float(max(0, rf[r] - cf[c]));
+    }
+  }
+  if (!mirror) return;
+  __syncthreads();
+  const int i = ti * kEpiTile + c;
+#pragma unroll 4
+  for (int r = t >> 6; r < kEpiTile; r += 4) {
+    const int jr = tj * kEpiTile + r;
+    if (jr < n && i < n) p.cost[size_t(jr) * n + i] = tr[r][c];
+  }
+}
+
+int tiles_of(int n, int tile) { return (n + tile - 1) / tile; }
+
+}  // namespace
+
+hipError_t launch_fst_prep(const FstParams& p, const FstScratch& s, hipStream_t stream) {
+  fst_init_kernel<<<1, 1, 0, stream>>>(s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int nb = (p.n + 3) / 4;
+  if (p.bf16)
+    row_norm_kernel<true><<<nb, 256, 0, stream>>>(p.feats, p.n, p.d, p.frame, s);
+  else
+    row_norm_kernel<false><<<nb, 256, 0, stream>>>(p.feats, p.n, p.d, p.frame, s);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int t = tiles_of(p.n, kPosTile);
+  pos_pairmax_kernel<<<t * (t + 1) / 2, 256, 0, stream>>>(p.pos, p.n, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_fst_epilogue(const FstParams& p, const FstScratch& s, hipStream_t stream) {
+  const int t = tiles_of(p.n, kEpiTile);
+  fst_epilogue_kernel<<<t * (t + 1) / 2, 256, 0, stream>>>(p, s);
+  return hipGetLastError();
+}
+
+}  // namespace cp

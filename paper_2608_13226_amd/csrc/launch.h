@@ -1,0 +1,78 @@
+// Host-side launchers: the only interface between the C-ABI layer (api.hip)
+// and the kernel translation units.  Every launcher enqueues on `stream`,
+// never synchronises, and returns the HIP status of its launches.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cp {
+
+// Workspace of coverprune_fst_cost.
+struct FstScratch {
+  float* inv_norm;                // [n] 1 / |f_i| (0 for a zero row)
+  unsigned int* mf_bits;          // max d_f as float bits
+  unsigned long long* mx2_bits;   // max squared distance as double bits
+  int* tau_min;                   // min frame index
+  int* tau_max;                   // max frame index
+};
+
+struct FstParams {
+  const void* feats;
+  bool bf16;
+  int n;
+  int d;
+  const float* pos;
+  const int32_t* frame;
+  float lambda_f, lambda_x, lambda_tau, kappa;
+  float inv_log1p_kappa;          // 1 / log1p(kappa), unused when kappa == 0
+  float* cost;                    // [n, n] target-major
+  float* maxima;                  // [3] or nullptr
+};
+
+hipError_t launch_fst_prep(const FstParams& p, const FstScratch& s, hipStream_t stream);
+hipError_t launch_gram(const FstParams& p, const FstScratch& s, hipStream_t stream);
+hipError_t launch_fst_epilogue(const FstParams& p, const FstScratch& s, hipStream_t stream);
+
+// Greedy selection.
+struct SgsParams {
+  const float* cost;              // [n, n] target-major
+  int n;
+  const float* capacity;          // [n]
+  int k;
+  float c0;
+  int32_t* selected;              // [k]
+  double* step_gain;              // [k] or nullptr
+  double* step_objective;         // [k] or nullptr
+  int32_t* assign;                // [n] or nullptr
+  void* workspace;
+  size_t workspace_bytes;
+};
+
+size_t sgs_workspace_bytes(int64_t n);
+hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream);
+
+// CoverPrune-Lite.
+struct LiteParams {
+  const void* feats;
+  bool bf16;
+  int n;
+  int d;
+  const float* pos;
+  const int32_t* frame;
+  const float* capacity;
+  int k;
+  float lambda_f, lambda_x, lambda_tau, kappa;
+  double inv_log1p_kappa;
+  double grid_scale;              // 256 / voxel_size, float64
+  int32_t* selected;              // [k]
+  int32_t* group;                 // [n] or nullptr
+  double* objective;              // [1] or nullptr
+  void* workspace;
+  size_t workspace_bytes;
+};
+
+size_t lite_workspace_bytes(int64_t n, int64_t k);
+hipError_t launch_lite(const LiteParams& p, hipStream_t stream);
+
+}  // namespace cp

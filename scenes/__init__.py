@@ -28,7 +28,7 @@ from typing import Optional, Tuple
 
 import numpy as np
 
-__all__ = ["SceneConfig", "Scene", "CONFIGS", "make_scene", "f32_to_bf16_bits",
+__all__ = ["SceneConfig", "Scene", "CONFIGS", "make_scene", "f32_to_bf16_bits", "to_device",
            "bf16_bits_to_f32", "subscene"]
 
 
@@ -263,3 +263,19 @@ def subscene(scene: Scene, idx, k: Optional[int] = None, renormalise: bool = Tru
                  np.ascontiguousarray(scene.pos[idx]), np.ascontiguousarray(scene.frame[idx]),
                  cap.astype(np.float32), scene.k if k is None else int(k),
                  np.ascontiguousarray(scene.obj[idx]))
+
+
+def to_device(scene: Scene, device="cuda"):
+    """The scene's arrays as torch tensors on ``device`` (features as
+    torch.bfloat16 or torch.float32).  Plain data movement."""
+    import torch
+    if scene.dtype == "bf16":
+        feats = torch.from_numpy(scene.feats.view(np.int16)).view(torch.bfloat16)
+    else:
+        feats = torch.from_numpy(scene.feats)
+    return dict(
+        feats=feats.to(device).contiguous(),
+        pos=torch.from_numpy(scene.pos).to(device).contiguous(),
+        frame=torch.from_numpy(scene.frame).to(device).contiguous(),
+        capacity=torch.from_numpy(scene.capacity).to(device).contiguous(),
+    )

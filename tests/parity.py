@@ -1,0 +1,135 @@
+"""Comparison helpers for the GPU parity tests.  Expected values always come
+from the oracle; GPU outputs are only ever the thing being checked."""
+from __future__ import annotations
+
+import numpy as np
+
+import functools
+
+from oracle import fst, lite, sgs
+from scenes import make_scene, subscene
+
+# Cost tolerance: bf16 inputs with float32 accumulation against float64.
+COST_RTOL = 1e-3
+COST_ATOL = 1e-5
+# Gains within this relative distance of the best count as ties.
+TIE_RTOL = 1e-6
+
+
+@functools.lru_cache(maxsize=8)
+def _scene(cfg, seed):
+    return make_scene(cfg, seed)
+
+
+def sample_scene(cfg, n, seed, salt=0):
+    """``n`` random tokens (sorted) of a generated scene; the whole scene for
+    n = None.  Always a fresh copy, so callers may modify it."""
+    s = _scene(cfg, seed)
+    if n is None or n >= s.n:
+        return subscene(s, np.arange(s.n), renormalise=False)
+    idx = np.sort(np.random.default_rng(salt + seed).choice(s.n, size=n, replace=False))
+    return subscene(s, idx)
+
+
+def oracle_cost(scene, weights=(1.0, 1.0, 1.0), kappa=10.0, rows=None, maxima=None):
+    F = fst.widen_features(scene.feats, scene.dtype)
+    return fst.fst_cost_ref(F, scene.pos, scene.frame, weights=weights, kappa=kappa, rows=rows,
+                            maxima=maxima)
+
+
+def oracle_cost_f32_target_major(scene, weights=(1.0, 1.0, 1.0), kappa=10.0, block=2048):
+    """The oracle's full cost rounded to float32, target-major, built in row
+    blocks so that large scenes fit in memory."""
+    F = fst.widen_features(scene.feats, scene.dtype)
+    maxima = fst.sample_maxima(F, scene.pos, scene.frame, block=block)
+    n = scene.n
+    out = np.empty((n, n), np.float32)
+    for lo in range(0, n, block):
+        rows = np.arange(lo, min(n, lo + block))
+        C, _ = fst.fst_cost_ref(F, scene.pos, scene.frame, weights=weights, kappa=kappa, rows=rows,
+                                maxima=maxima)
+        out[:, lo:lo + rows.size] = C.T.astype(np.float32)
+    return out, maxima
+
+
+def assert_cost_close(gpu_tm: np.ndarray, ref_source_major: np.ndarray):
+    """gpu_tm[t, s] = C(s, t) against the oracle's C[s, t]."""
+    ref_tm = ref_source_major.T
+    err = np.abs(gpu_tm.astype(np.float64) - ref_tm)
+    bound = COST_RTOL * np.abs(ref_tm) + COST_ATOL
+    bad = err > bound
+    if bad.any():
+        t, s = np.argwhere(bad)[0]
+        raise AssertionError(f"{int(bad.sum())} cost entries off; first at target {t}, source {s}: "
+                             f"gpu {gpu_tm[t, s]!r} oracle {ref_tm[t, s]!r}; max err {err.max():.3g}")
+    return float(err.max())
+
+
+def replay_greedy(C_src: np.ndarray, v: np.ndarray, c0: float, picks, tie_atol=0.0):
+    """Check that ``picks`` is a valid greedy trajectory on the oracle's cost.
+
+    At every step the pick must be unselected and its exact gain (oracle
+    arithmetic, on the trajectory so far) within TIE_RTOL * best + tie_atol of
+    the best gain.  Returns (steps where the pick was not the oracle's own
+    first choice, oracle gains of the picks, oracle objectives)."""
+    C = np.asarray(C_src, np.float64)
+    v = np.asarray(v, np.float64)
+    n = C.shape[0]
+    b = np.full(n, float(c0))
+    chosen = np.zeros(n, bool)
+    ties, gains, objs = [], [], []
+    for step, t in enumerate(int(x) for x in picks):
+        assert 0 <= t < n and not chosen[t], f"step {step}: pick {t} invalid or repeated"
+        g = (v[None, :] * np.maximum(0.0, b[None, :] - C)).sum(axis=1)
+        g[chosen] = -np.inf
+        best = int(np.argmax(g))
+        if t != best:
+            slack = TIE_RTOL * abs(g[best]) + tie_atol
+            assert g[t] >= g[best] - slack, (f"step {step}: picked {t} with gain {g[t]!r}, "
+                                             f"best is {best} with {g[best]!r}")
+            ties.append(step)
+        chosen[t] = True
+        gains.append(g[t])
+        b = np.minimum(b, C[t])
+        objs.append(float(np.sum(v * b)))
+    return ties, np.array(gains), np.array(objs)
+
+
+def check_trajectory_invariants(sel, gain, obj, v, c0, k, n):
+    sel = np.asarray(sel)
+    assert len(sel) == k and len(set(sel.tolist())) == k
+    assert sel.min() >= 0 and sel.max() < n
+    v = np.asarray(v, np.float64)
+    total = c0 * v.sum()
+    # L_k = c0 sum(v) - sum of gains, and L decreases by exactly each gain.
+    assert abs(obj[-1] - (total - gain.sum())) <= 1e-9 * total + 1e-12
+    prev = np.concatenate([[total], obj[:-1]])
+    assert np.allclose(prev - obj, gain, rtol=1e-7, atol=1e-12 * total)
+    # Gains of a monotone submodular function never grow along the greedy.
+    assert np.all(np.diff(gain) <= 1e-9 * max(gain[0], 1e-300))
+
+
+def lite_reference(scene, k, weights=(1.0, 1.0, 1.0), kappa=10.0, h=0.25, capacity=None):
+    F = fst.widen_features(scene.feats, scene.dtype)
+    v = scene.capacity if capacity is None else capacity
+    return lite.lite_ref(F, scene.pos, scene.frame, v, k, weights=weights, kappa=kappa, h=h)
+
+
+def assert_lite_close(gpu_sel, gpu_group, gpu_obj, ref, rtol=1e-5, atol=1e-9):
+    """Groups bit-exact; each GPU prototype's oracle cost within tolerance of
+    the group minimum; objective within rtol."""
+    gpu_group = np.asarray(gpu_group)
+    assert np.array_equal(gpu_group, ref["group"]), \
+        f"{int((gpu_group != ref['group']).sum())} tokens in a different group"
+    cost = ref["cost"]
+    gpu_sel = np.asarray(gpu_sel)
+    assert np.array_equal(ref["group"][gpu_sel], np.arange(len(gpu_sel))), "prototype outside its group"
+    c_gpu = cost[gpu_sel]
+    c_ref = cost[ref["selected"]]
+    slack = rtol * np.abs(c_ref) + atol
+    bad = c_gpu > c_ref + slack
+    assert not bad.any(), (f"{int(bad.sum())} groups pick a worse prototype; first group "
+                           f"{int(np.argmax(bad))}: {c_gpu[bad][0]!r} vs {c_ref[bad][0]!r}")
+    ties = int((gpu_sel != ref["selected"]).sum())
+    assert abs(gpu_obj - ref["objective"]) <= rtol * abs(ref["objective"]) + atol
+    return ties

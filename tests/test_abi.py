@@ -1,0 +1,125 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol the header
+declares, and rejects bad arguments on the host before launching anything.
+No call here reaches a kernel, so no GPU is needed."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "coverprune.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+FAKE = ctypes.c_void_p(0x1000)          # aligned, never dereferenced by the host checks
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2608_13226_amd as cp
+    if not os.path.exists(cp.library_path()):
+        from paper_2608_13226_amd import build
+        build.build()
+    return cp.library()
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(coverprune_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert {"coverprune_fst_cost", "coverprune_sgs_select", "coverprune_lite_select"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), f"{name} declared in the header but not exported"
+
+
+def test_version_and_status_strings(lib):
+    assert lib.coverprune_abi_version() == 1
+    for code, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported"),
+                       (3, b"workspace too small"), (4, b"HIP runtime error")]:
+        assert lib.coverprune_status_string(code) == text
+    assert lib.coverprune_status_string(99) == b"unknown status"
+
+
+def test_workspace_queries(lib):
+    assert lib.coverprune_fst_cost_workspace(0, 8, 1) == 0
+    assert lib.coverprune_fst_cost_workspace(16384, 3584, 1) >= 16384 * 4
+    a = lib.coverprune_sgs_workspace(1024, 102)
+    b = lib.coverprune_sgs_workspace(16384, 1638)
+    assert 0 < a < b
+    assert lib.coverprune_lite_workspace(32768, 3584, 3277, 1) >= 32768 * 64
+
+
+def _w(lf=1.0, lx=1.0, lt=1.0, kappa=10.0):
+    import paper_2608_13226_amd as cp
+    return cp._Weights(lf, lx, lt, kappa)
+
+
+def _fst(lib, **kw):
+    a = dict(feats=FAKE, dtype=1, n=64, d=64, pos=FAKE, frame=FAKE, w=_w(), cost=FAKE, maxima=None,
+             ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return lib.coverprune_fst_cost(a["feats"], a["dtype"], a["n"], a["d"], a["pos"], a["frame"], a["w"],
+                                   a["cost"], a["maxima"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), INVALID), (dict(n=-5), INVALID), (dict(n=1 << 19), INVALID),
+    (dict(d=0), INVALID), (dict(d=12), UNSUPPORTED), (dict(dtype=0, d=6), UNSUPPORTED),
+    (dict(dtype=7), UNSUPPORTED), (dict(feats=None), INVALID), (dict(pos=None), INVALID),
+    (dict(frame=None), INVALID), (dict(cost=None), INVALID),
+    (dict(feats=ctypes.c_void_p(0x1004)), INVALID),
+    (dict(w=_w(lf=-1.0)), INVALID), (dict(w=_w(kappa=float("nan"))), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(ws_bytes=16), WORKSPACE),
+])
+def test_fst_cost_rejects(lib, kw, code):
+    assert _fst(lib, **kw) == code
+    assert lib.coverprune_last_error() != b""
+
+
+def _sgs(lib, **kw):
+    a = dict(cost=FAKE, n=64, v=FAKE, k=8, c0=3.0, flags=0, sel=FAKE, gain=None, obj=None, assign=None,
+             ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return lib.coverprune_sgs_select(a["cost"], a["n"], a["v"], a["k"], a["c0"], a["flags"], a["sel"],
+                                     a["gain"], a["obj"], a["assign"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), INVALID), (dict(k=0), INVALID), (dict(k=65), INVALID), (dict(k=-1), INVALID),
+    (dict(c0=float("inf")), INVALID), (dict(flags=7), UNSUPPORTED), (dict(cost=None), INVALID),
+    (dict(v=None), INVALID), (dict(sel=None), INVALID), (dict(ws=None), WORKSPACE),
+    (dict(ws_bytes=100), WORKSPACE), (dict(ws=ctypes.c_void_p(0x1008)), WORKSPACE),
+])
+def test_sgs_rejects(lib, kw, code):
+    assert _sgs(lib, **kw) == code
+
+
+def _lite(lib, **kw):
+    a = dict(feats=FAKE, dtype=1, n=64, d=64, pos=FAKE, frame=FAKE, v=FAKE, k=8, w=_w(), h=0.25,
+             sel=FAKE, group=None, obj=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return lib.coverprune_lite_select(a["feats"], a["dtype"], a["n"], a["d"], a["pos"], a["frame"], a["v"],
+                                      a["k"], a["w"], a["h"], a["sel"], a["group"], a["obj"], a["ws"],
+                                      a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), INVALID), (dict(k=0), INVALID), (dict(k=65), INVALID), (dict(h=0.0), INVALID),
+    (dict(h=-1.0), INVALID), (dict(h=float("inf")), INVALID), (dict(d=4), UNSUPPORTED),
+    (dict(v=None), INVALID), (dict(sel=None), INVALID), (dict(pos=None), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(ws_bytes=64), WORKSPACE), (dict(w=_w(lt=-2.0)), INVALID),
+])
+def test_lite_rejects(lib, kw, code):
+    assert _lite(lib, **kw) == code
+
+
+def test_binding_needs_the_library(monkeypatch, tmp_path):
+    # The Python layer never falls back to anything else: a missing library is an error.
+    import paper_2608_13226_amd as cp
+    monkeypatch.setattr(cp, "_lib", None)
+    monkeypatch.setattr(cp, "library_path", lambda: str(tmp_path / "missing.so"))
+    with pytest.raises(cp.CoverPruneError):
+        cp.library()

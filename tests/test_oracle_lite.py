@@ -44,7 +44,10 @@ def _scan_groups(v, K):
     W = sum(V)
     out, cum, low = [], 0, None
     for p in range(n):
-        t = min(K - 1, (K * cum) // W) if W > 0 else K - 1
+        if p == 0:
+            t = 0
+        else:
+            t = min(K - 1, (K * cum) // W) if W > 0 else K - 1
         low = t - p if low is None else min(low, t - p)
         out.append(max(K - n + p, p + low))
         cum += V[p]
@@ -72,6 +75,15 @@ def test_walk_equals_scan(seed):
     # Exactly K non-empty contiguous groups, in order.
     assert g[0] == 0 and g[-1] == K - 1
     assert all(b - a in (0, 1) for a, b in zip(g, g[1:]))
+
+
+def test_all_capacity_below_resolution():
+    # Every V_j rounds to 0 (W = 0): each threshold counts as reached, so the
+    # walk opens a group at every token until the last group.
+    v = [np.float32(1e-15)] * 10
+    g = lite.capacity_groups(v, 4)
+    assert g == [0, 1, 2, 3, 3, 3, 3, 3, 3, 3]
+    assert g == _scan_groups(v, 4)
 
 
 def test_group_mass_near_one_over_k():
