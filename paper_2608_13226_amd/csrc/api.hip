@@ -143,9 +143,8 @@ cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int6
 
 // ---------------------------------------------------------------------------
 size_t coverprune_sgs_workspace(int64_t n, int64_t k) {
-  (void)k;
-  if (n < 1) return 0;
-  return cp::sgs_workspace_bytes(n);
+  if (n < 1 || k < 1) return 0;
+  return cp::sgs_workspace_bytes(n, k);
 }
 
 cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capacity, int64_t k,

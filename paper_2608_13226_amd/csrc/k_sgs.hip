@@ -1,21 +1,31 @@
 // Greedy coverage selection over the target-major cost (Sec. 3.5, Eq. 14-16).
 //
 // State: b_j, the best cost at which target j is covered so far (c0 while
-// uncovered), and the mask of chosen tokens.  One step:
-//   S  sweep    gain(c) = sum_j v_j max(0, b_j - C_tm[j][c]) for every c: a
-//               column reduction of the N x N matrix, streamed row by row
-//               (each row is one target; a wave reads 1 KB of it per load);
-//               waves own (row chunk, 256-column strip) items and write
-//               float64 partial gains per row chunk
-//   R  argmax   partials summed per column in a fixed order, masked, argmax
-//               with ties to the smaller index; the last block to finish
-//               publishes the step's winner t*
-//   U  update   b_j = min(b_j, C_tm[j][t*]); assign_j = t* on strict
-//               improvement; L = sum_j v_j b_j folded per block
-// The K steps run inside one cooperative launch; grid barriers separate the
-// phases, so the greedy never returns to the host.
+// uncovered), and the mask of chosen tokens.  Step l picks
+//   t_l = argmax_{c not chosen} gain(c),  gain(c) = sum_j v_j max(0, b_j - C_tm[j][c])
+// and then b_j <- min(b_j, C_tm[j][t_l]).
+//
+// One cooperative launch runs all K steps.  The matrix is cut into P row
+// panels x S column strips of 256 columns; the item (panel, strip) is owned by
+// one block for the whole launch.  Per step the block
+//   1. brings its private copy of b for the panel's rows up to date with the
+//      previous pick (b = min(b, C_tm[j][t])) and stages b and v in LDS; the
+//      strip-0 item of a panel also updates the assignment and folds the
+//      panel's share of the objective;
+//   2. streams the panel's rows of its strip (a wave reads 1 KB of a row per
+//      16-byte non-temporal load) accumulating float64 gains per column, and
+//      writes the panel's partial gains;
+//   3. arrives at its strip's counter.  The strip's last block sums the P
+//      partials of every column in panel order, masks chosen columns, takes
+//      the strip's exact argmax (ties to the smaller index), records it, folds
+//      it into the step's packed (gain, index) maximum with one 64-bit
+//      atomicMax, and arrives at the step counter;
+//   4. waits until every strip has arrived and reads the step's winner.
+// Only thread 0 of a block issues device-scope fences, once per arrival.
+// Across strips the packed key compares gains truncated to 44 bits (relative
+// resolution 2^-32) and breaks ties by the smaller index; within a strip the
+// comparison is exact.
 #include <hip/hip_runtime.h>
-#include <hip/hip_cooperative_groups.h>
 
 #include <algorithm>
 #include <climits>
@@ -23,16 +33,15 @@
 #include "common.h"
 #include "launch.h"
 
-namespace cg = cooperative_groups;
-
 namespace cp {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kStrip = 256;        // columns per wave item: 64 lanes x 4 floats
-constexpr int kMaxChunks = 64;     // row chunks (partial-gain rows)
-constexpr int kMaxBlocks = 4096;
-constexpr int kMinRowsPerChunk = 16;
+constexpr int kStrip = 256;        // columns per strip: 64 lanes x 4 floats
+constexpr int kMaxPanels = 64;
+constexpr int kMaxStrips = (1 << 18) / kStrip;
+constexpr int kMinPanelRows = 64;
+constexpr int kIndexBits = 20;     // packed key: [44-bit gain | 20-bit inverted index]
+constexpr unsigned long long kIndexMask = (1ull << kIndexBits) - 1ull;
 
 struct SgsDev {
   const float* C;
@@ -43,39 +52,66 @@ struct SgsDev {
   double* step_gain;
   double* step_obj;
   int32_t* assign;
-  float* b;
+  float* bpriv;              // [items][rows] private best costs
   uint8_t* mask;
-  double* partial;     // [nrc][n]
-  double* bbest_g;     // [grid]
-  int* bbest_i;        // [grid]
-  double* obj_part;    // [grid]
-  unsigned int* counter;
-  int* tstar;
-  int ncs, nrc, rows;  // column strips, row chunks, rows per chunk
+  double* partial;           // [P][n]
+  double* strip_g;           // [S]
+  int* strip_i;              // [S]
+  double* obj_part;          // [P]
+  unsigned long long* key;   // [k] packed step maxima
+  unsigned int* strip_cnt;   // [S]
+  unsigned int* step_cnt;
+  unsigned int* fin_cnt;
+  int P, S, rows;            // panels, strips, rows per panel
 };
 
 struct Layout {
-  size_t b, mask, partial, bbest_g, bbest_i, obj_part, ctrl, total;
+  size_t bpriv, mask, partial, strip_g, strip_i, obj_part, key, strip_cnt, ctrl, total;
 };
 
 size_t a256(size_t x) { return (x + 255) / 256 * 256; }
 
-Layout layout(int64_t n) {
+// Private best costs: items x rows = S x (P x rows) < S x (n + P) floats.
+Layout layout(int64_t n, int64_t k) {
   Layout L;
+  const size_t S = size_t((n + kStrip - 1) / kStrip);
   size_t o = 0;
-  L.b = o;        o += a256(size_t(n) * 4);
-  L.mask = o;     o += a256(size_t(n));
-  L.partial = o;  o += a256(size_t(kMaxChunks) * size_t(n) * 8);
-  L.bbest_g = o;  o += a256(size_t(kMaxBlocks) * 8);
-  L.bbest_i = o;  o += a256(size_t(kMaxBlocks) * 4);
-  L.obj_part = o; o += a256(size_t(kMaxBlocks) * 8);
-  L.ctrl = o;     o += 256;
+  L.bpriv = o;     o += a256(S * size_t(n + kMaxPanels) * 4);
+  L.mask = o;      o += a256(size_t(n));
+  L.partial = o;   o += a256(size_t(kMaxPanels) * size_t(n) * 8);
+  L.strip_g = o;   o += a256(size_t(kMaxStrips) * 8);
+  L.strip_i = o;   o += a256(size_t(kMaxStrips) * 4);
+  L.obj_part = o;  o += a256(size_t(kMaxPanels) * 8);
+  L.key = o;       o += a256(size_t(k) * 8);
+  L.strip_cnt = o; o += a256(size_t(kMaxStrips) * 4);
+  L.ctrl = o;      o += 256;
   L.total = o;
   return L;
 }
 
-// Block-wide reduction of per-thread (gain, index) to thread 0.
+// All threads' writes are complete at workgroup scope after the barrier;
+// thread 0 then publishes them device-wide and counts the block in.  Returns,
+// block-uniformly, the counter value before this block's increment; a block
+// that finds itself last has acquired every earlier arrival's writes.
+template <int BT>
+__device__ unsigned int block_arrive(unsigned int* counter, unsigned int* s_prev) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    *s_prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  return *s_prev;
+}
+
+__device__ __forceinline__ void acquire_once() {
+  if (threadIdx.x == 0) __threadfence();
+  __syncthreads();
+}
+
+template <int BT>
 __device__ void block_argmax(double& g, int& i, double* sg, int* si) {
+  constexpr int W = BT / 64;
   wave_argmax(g, i);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   __syncthreads();
@@ -84,17 +120,18 @@ __device__ void block_argmax(double& g, int& i, double* sg, int* si) {
     si[w] = i;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int x = 1; x < kThreads / 64; ++x)
+  if (threadIdx.x == 0)
+    for (int x = 1; x < W; ++x)
       if (better(sg[x], si[x], g, i)) {
         g = sg[x];
         i = si[x];
       }
-  }
 }
 
-// Block-wide float64 sum in a fixed order, result in thread 0.
+// Fixed-order block sum, result in thread 0.
+template <int BT>
 __device__ double block_sum(double x, double* sd) {
+  constexpr int W = BT / 64;
   x = wave_sum(x);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   __syncthreads();
@@ -102,217 +139,307 @@ __device__ double block_sum(double x, double* sd) {
   __syncthreads();
   double s = 0.0;
   if (threadIdx.x == 0)
-    for (int q = 0; q < kThreads / 64; ++q) s += sd[q];
+    for (int q = 0; q < W; ++q) s += sd[q];
   return s;
 }
 
-__device__ __forceinline__ void sweep_item(const SgsDev& a, int it, int lane) {
-  const int r = it / a.ncs, strip = it - r * a.ncs;
-  const int col = strip * kStrip + lane * 4;
-  const int j0 = r * a.rows, j1 = min(a.n, j0 + a.rows);
-  double g0 = 0.0, g1 = 0.0, g2 = 0.0, g3 = 0.0;
-  const bool full = (a.n & 3) == 0 && col + 3 < a.n;
-  if (full) {
-    const float* base = a.C + col;
-    int j = j0;
-    for (; j + 4 <= j1; j += 4) {
-      f32x4 x[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        x[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(base + size_t(j + u) * a.n));
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float bj = a.b[j + u];
-        const double vj = double(a.v[j + u]);
-        g0 = fma(vj, double(fmaxf(bj - x[u][0], 0.f)), g0);
-        g1 = fma(vj, double(fmaxf(bj - x[u][1], 0.f)), g1);
-        g2 = fma(vj, double(fmaxf(bj - x[u][2], 0.f)), g2);
-        g3 = fma(vj, double(fmaxf(bj - x[u][3], 0.f)), g3);
-      }
-    }
-    for (; j < j1; ++j) {
-      const f32x4 x = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(base + size_t(j) * a.n));
-      const float bj = a.b[j];
-      const double vj = double(a.v[j]);
-      g0 = fma(vj, double(fmaxf(bj - x[0], 0.f)), g0);
-      g1 = fma(vj, double(fmaxf(bj - x[1], 0.f)), g1);
-      g2 = fma(vj, double(fmaxf(bj - x[2], 0.f)), g2);
-      g3 = fma(vj, double(fmaxf(bj - x[3], 0.f)), g3);
-    }
-  } else {
-    double g[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int j = j0; j < j1; ++j) {
-      const float bj = a.b[j];
-      const double vj = double(a.v[j]);
-      const float* row = a.C + size_t(j) * a.n;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (col + q < a.n) g[q] = fma(vj, double(fmaxf(bj - row[col + q], 0.f)), g[q]);
-    }
-    g0 = g[0]; g1 = g[1]; g2 = g[2]; g3 = g[3];
-  }
-  double* out = a.partial + size_t(r) * a.n + col;
-  if (col < a.n) out[0] = g0;
-  if (col + 1 < a.n) out[1] = g1;
-  if (col + 2 < a.n) out[2] = g2;
-  if (col + 3 < a.n) out[3] = g3;
-}
-
-__global__ __launch_bounds__(kThreads) void sgs_dense_kernel(SgsDev a) {
-  cg::grid_group grid = cg::this_grid();
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int gw = blockIdx.x * (kThreads / 64) + (tid >> 6), nw = gridDim.x * (kThreads / 64);
-  const int gt = blockIdx.x * kThreads + tid, nt = gridDim.x * kThreads;
-  __shared__ double sg[kThreads / 64];
-  __shared__ int si[kThreads / 64];
-  __shared__ int s_last;
-
+__global__ void sgs_init_kernel(SgsDev a) {
+  const int gt = blockIdx.x * blockDim.x + threadIdx.x, nt = gridDim.x * blockDim.x;
   for (int j = gt; j < a.n; j += nt) {
-    a.b[j] = a.c0;
     a.mask[j] = 0;
     if (a.assign) a.assign[j] = -1;
   }
-  if (gt == 0) *a.counter = 0u;
-  grid.sync();
+  for (int s = gt; s < a.S; s += nt) a.strip_cnt[s] = 0u;
+  for (int s = gt; s < a.k; s += nt) a.key[s] = 0ull;
+  if (gt == 0) {
+    *a.step_cnt = 0u;
+    *a.fin_cnt = 0u;
+  }
+}
 
-  const int items = a.ncs * a.nrc;
-  for (int step = 0; step < a.k; ++step) {
-    // S: partial gains.
-    for (int it = gw; it < items; it += nw) sweep_item(a, it, lane);
-    grid.sync();
+__device__ __forceinline__ unsigned long long pack_key(double g, int idx) {
+  const unsigned long long gb = (unsigned long long)__double_as_longlong(g) >> kIndexBits;
+  return (gb << kIndexBits) | (kIndexMask - (unsigned long long)idx);
+}
 
-    // R: per-column totals, block argmax, last block -> global argmax.
-    double bg = -1.0;
-    int bi = INT_MAX;
-    for (int c = gt; c < a.n; c += nt) {
-      if (a.mask[c]) continue;
-      double g = 0.0;
-      for (int r = 0; r < a.nrc; ++r) g += a.partial[size_t(r) * a.n + c];
-      if (better(g, c, bg, bi)) {
-        bg = g;
-        bi = c;
+struct RowState {
+  float bo, cv, vj;
+};
+
+// Row j entering step `step`: previous best cost, cost of the previous pick.
+__device__ __forceinline__ RowState fetch_row(const SgsDev& a, const float* bp, int step, int tprev,
+                                              int j, int j1) {
+  RowState r{0.f, 0.f, 0.f};
+  if (j < j1) {
+    r.vj = a.v[j];
+    if (step == 0) {
+      r.bo = a.c0;
+      r.cv = a.c0;
+    } else {
+      r.bo = bp[j];
+      r.cv = a.C[size_t(j) * a.n + tprev];
+    }
+  }
+  return r;
+}
+
+// Sweep of one item for one step.  Returns the panel's objective share in
+// thread 0 for the strip-0 item.
+template <int BT, bool VEC4>
+__device__ double sweep_item(const SgsDev& a, int step, int tprev, int it, int panel, int strip,
+                             float* sb, float* sv, double* red, double* sd) {
+  constexpr int W = BT / 64;
+  constexpr int U = 16;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int j0 = panel * a.rows, j1 = min(a.n, j0 + a.rows);
+  float* bp = a.bpriv + size_t(it) * a.rows - j0;   // bp[j], j in [j0, j1)
+  const int col = strip * kStrip + lane * 4;
+  const bool owner = strip == 0;
+  double g0 = 0.0, g1 = 0.0, g2 = 0.0, g3 = 0.0;
+  double objp = 0.0;
+
+  RowState next = fetch_row(a, bp, step, tprev, j0 + tid, j1);
+  for (int c0 = j0; c0 < j1; c0 += BT) {
+    const RowState cur = next;
+    const int j = c0 + tid;
+    float bn = 0.f;
+    if (j < j1) {
+      bn = fminf(cur.bo, cur.cv);
+      bp[j] = bn;
+      if (owner) {
+        if (a.assign && step > 0 && cur.cv < cur.bo) a.assign[j] = tprev;
+        objp = fma(double(cur.vj), double(bn), objp);
       }
     }
-    block_argmax(bg, bi, sg, si);
-    if (tid == 0) {
-      a.bbest_g[blockIdx.x] = bg;
-      a.bbest_i[blockIdx.x] = bi;
-      __threadfence();
-      const unsigned int prev = atomicAdd(a.counter, 1u);
-      s_last = prev == unsigned(step + 1) * gridDim.x - 1u;
+    sb[tid] = bn;
+    sv[tid] = cur.vj;
+    __syncthreads();
+    if (c0 + BT < j1) next = fetch_row(a, bp, step, tprev, c0 + BT + tid, j1);
+
+    // Wave w streams rows c0 + 64 w .. + 63 of the chunk.
+    const int r0 = c0 + w * 64, r1 = min(j1, r0 + 64);
+    if (VEC4) {
+      if (col < a.n) {
+        const float* base = a.C + col;
+        int r = r0;
+        for (; r + U <= r1; r += U) {
+          f32x4 x[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            x[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(base + size_t(r + u) * a.n));
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const float bj = sb[r + u - c0];
+            const double vj = double(sv[r + u - c0]);
+            g0 = fma(vj, double(fmaxf(bj - x[u][0], 0.f)), g0);
+            g1 = fma(vj, double(fmaxf(bj - x[u][1], 0.f)), g1);
+            g2 = fma(vj, double(fmaxf(bj - x[u][2], 0.f)), g2);
+            g3 = fma(vj, double(fmaxf(bj - x[u][3], 0.f)), g3);
+          }
+        }
+        for (; r < r1; ++r) {
+          const f32x4 x = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(base + size_t(r) * a.n));
+          const float bj = sb[r - c0];
+          const double vj = double(sv[r - c0]);
+          g0 = fma(vj, double(fmaxf(bj - x[0], 0.f)), g0);
+          g1 = fma(vj, double(fmaxf(bj - x[1], 0.f)), g1);
+          g2 = fma(vj, double(fmaxf(bj - x[2], 0.f)), g2);
+          g3 = fma(vj, double(fmaxf(bj - x[3], 0.f)), g3);
+        }
+      }
+    } else {
+      for (int r = r0; r < r1; ++r) {
+        const float* row = a.C + size_t(r) * a.n;
+        const float bj = sb[r - c0];
+        const double vj = double(sv[r - c0]);
+        if (col < a.n) g0 = fma(vj, double(fmaxf(bj - row[col], 0.f)), g0);
+        if (col + 1 < a.n) g1 = fma(vj, double(fmaxf(bj - row[col + 1], 0.f)), g1);
+        if (col + 2 < a.n) g2 = fma(vj, double(fmaxf(bj - row[col + 2], 0.f)), g2);
+        if (col + 3 < a.n) g3 = fma(vj, double(fmaxf(bj - row[col + 3], 0.f)), g3);
+      }
     }
     __syncthreads();
-    if (s_last) {
-      __threadfence();
+  }
+
+  // The waves' partial gains, summed in wave order: thread c < 256 owns column c.
+  red[(w * 64 + lane) * 4 + 0] = g0;
+  red[(w * 64 + lane) * 4 + 1] = g1;
+  red[(w * 64 + lane) * 4 + 2] = g2;
+  red[(w * 64 + lane) * 4 + 3] = g3;
+  __syncthreads();
+  if (tid < kStrip) {
+    const int cc = strip * kStrip + tid;
+    if (cc < a.n) {
+      const int l = tid >> 2, q = tid & 3;
+      double s = 0.0;
+#pragma unroll
+      for (int x = 0; x < W; ++x) s += red[(x * 64 + l) * 4 + q];
+      a.partial[size_t(panel) * a.n + cc] = s;
+    }
+  }
+  return owner ? block_sum<BT>(objp, sd) : 0.0;
+}
+
+template <int BT, bool VEC4>
+__global__ __launch_bounds__(BT) void sgs_dense_kernel(SgsDev a) {
+  constexpr int W = BT / 64;
+  const int tid = threadIdx.x;
+  __shared__ float sb[BT], sv[BT];
+  __shared__ double red[BT * 4];
+  __shared__ double sd[W];
+  __shared__ int si[W];
+  __shared__ unsigned int s_prev;
+  __shared__ int s_t;
+
+  const int items = a.P * a.S;
+  int tprev = -1;
+  for (int step = 0; step < a.k; ++step) {
+    for (int it = blockIdx.x; it < items; it += gridDim.x) {
+      const int panel = it / a.S, strip = it - panel * a.S;
+      const double objp = sweep_item<BT, VEC4>(a, step, tprev, it, panel, strip, sb, sv, red, sd);
+      if (strip == 0 && tid == 0) a.obj_part[panel] = objp;
+
+      const unsigned int prev = block_arrive<BT>(a.strip_cnt + strip, &s_prev);
+      if (prev != unsigned(step + 1) * unsigned(a.P) - 1u) continue;
+      // Last block of the strip.
+      acquire_once();
       double g = -1.0;
-      int i = INT_MAX;
-      for (int x = tid; x < int(gridDim.x); x += kThreads)
-        if (better(a.bbest_g[x], a.bbest_i[x], g, i)) {
-          g = a.bbest_g[x];
-          i = a.bbest_i[x];
+      int gi = INT_MAX;
+      if (tid < kStrip) {
+        const int cc = strip * kStrip + tid;
+        if (cc < a.n && !a.mask[cc]) {
+          g = 0.0;
+          for (int p = 0; p < a.P; ++p) g += a.partial[size_t(p) * a.n + cc];
+          gi = cc;
         }
-      block_argmax(g, i, sg, si);
+      }
+      block_argmax<BT>(g, gi, sd, si);
       double prev_obj = 0.0;
-      if (step > 0 && a.step_obj) {
+      if (strip == 0 && step > 0) {
         double x = 0.0;
-        for (int q = tid; q < int(gridDim.x); q += kThreads) x += a.obj_part[q];
-        prev_obj = block_sum(x, sg);
+        for (int p = tid; p < a.P; p += BT) x += a.obj_part[p];
+        prev_obj = block_sum<BT>(x, sd);
       }
       if (tid == 0) {
-        *a.tstar = i;
-        a.selected[step] = i;
-        if (a.step_gain) a.step_gain[step] = g;
-        if (step > 0 && a.step_obj) a.step_obj[step - 1] = prev_obj;
-        a.mask[i] = 1;
+        a.strip_g[strip] = g;
+        a.strip_i[strip] = gi;
+        if (gi != INT_MAX)
+          __hip_atomic_fetch_max(a.key + step, pack_key(g, gi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (strip == 0 && step > 0 && a.step_obj) a.step_obj[step - 1] = prev_obj;
+      }
+      block_arrive<BT>(a.step_cnt, &s_prev);
+    }
+    // Wait until every strip has reported, then read the winner.
+    if (tid == 0) {
+      const unsigned int target = unsigned(step + 1) * unsigned(a.S);
+      while (__hip_atomic_load(a.step_cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target)
+        __builtin_amdgcn_s_sleep(1);
+      __threadfence();
+      const unsigned long long kk = __hip_atomic_load(a.key + step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int t = int(kIndexMask - (kk & kIndexMask));
+      s_t = t;
+      const int ts = t / kStrip;
+      if (int(blockIdx.x) == ts % int(gridDim.x)) a.mask[t] = 1;     // owner of item (0, ts)
+      if (blockIdx.x == 0) {
+        a.selected[step] = t;
+        if (a.step_gain) a.step_gain[step] = a.strip_g[ts];
       }
     }
-    grid.sync();
-
-    // U: best-cost update and this step's objective share.
-    const int t = *a.tstar;
-    double part = 0.0;
-    for (int j = gt; j < a.n; j += nt) {
-      const float c = a.C[size_t(j) * a.n + t];
-      float bj = a.b[j];
-      if (c < bj) {
-        bj = c;
-        a.b[j] = c;
-        if (a.assign) a.assign[j] = t;
-      }
-      part = fma(double(a.v[j]), double(bj), part);
-    }
-    const double bs = block_sum(part, sg);
-    if (tid == 0) a.obj_part[blockIdx.x] = bs;
-    grid.sync();
+    __syncthreads();
+    tprev = s_t;
   }
-  if (blockIdx.x == 0 && a.step_obj) {
+
+  // Apply the last pick: assignment and the final objective.
+  for (int it = blockIdx.x; it < items; it += gridDim.x) {
+    const int panel = it / a.S, strip = it - panel * a.S;
+    if (strip != 0) continue;
+    const int j0 = panel * a.rows, j1 = min(a.n, j0 + a.rows);
+    const float* bp = a.bpriv + size_t(it) * a.rows - j0;
+    double objp = 0.0;
+    for (int j = j0 + tid; j < j1; j += BT) {
+      const float bo = bp[j];
+      const float cv = a.C[size_t(j) * a.n + tprev];
+      if (a.assign && cv < bo) a.assign[j] = tprev;
+      objp = fma(double(a.v[j]), double(fminf(bo, cv)), objp);
+    }
+    const double s = block_sum<BT>(objp, sd);
+    if (tid == 0) a.obj_part[panel] = s;
+  }
+  const unsigned int fprev = block_arrive<BT>(a.fin_cnt, &s_prev);
+  if (fprev == gridDim.x - 1u && a.step_obj) {
+    acquire_once();
     double x = 0.0;
-    for (int q = tid; q < int(gridDim.x); q += kThreads) x += a.obj_part[q];
-    const double s = block_sum(x, sg);
+    for (int p = tid; p < a.P; p += BT) x += a.obj_part[p];
+    const double s = block_sum<BT>(x, sd);
     if (tid == 0) a.step_obj[a.k - 1] = s;
   }
 }
 
-struct DeviceInfo {
-  int cus = 0;
-  int blocks_per_cu = 0;
-};
+constexpr int kBlock = 256;
 
-hipError_t device_info(DeviceInfo& info) {
-  int dev = 0;
+template <bool VEC4>
+hipError_t max_coresident(int& blocks) {
+  int dev = 0, cus = 0, per_cu = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if ((e = hipDeviceGetAttribute(&info.cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(&info.blocks_per_cu,
-                                                      reinterpret_cast<const void*>(sgs_dense_kernel),
-                                                      kThreads, 0);
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+      &per_cu, reinterpret_cast<const void*>(sgs_dense_kernel<kBlock, VEC4>), kBlock, 0);
+  // Two blocks (8 waves) per CU: enough loads in flight to saturate HBM while
+  // keeping the per-step arrivals few.
+  blocks = std::max(1, cus * std::min(per_cu, 2));
+  return e;
 }
 
 }  // namespace
 
-size_t sgs_workspace_bytes(int64_t n) { return layout(n).total; }
+size_t sgs_workspace_bytes(int64_t n, int64_t k) { return layout(n, k).total; }
 
 hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream) {
-  DeviceInfo info;
-  hipError_t e = device_info(info);
+  const bool vec4 = (p.n % 4) == 0;
+  int max_blocks = 0;
+  hipError_t e = vec4 ? max_coresident<true>(max_blocks) : max_coresident<false>(max_blocks);
   if (e != hipSuccess) return e;
-  const int64_t n = p.n;
-  const int max_blocks = std::min(kMaxBlocks, info.cus * std::min(info.blocks_per_cu, 4));
-  // Aim for at least 64 KB of the matrix per wave per step.
-  const int64_t waves_wanted = std::max<int64_t>(1, (4 * n * n + 65535) / 65536);
-  const int grid = int(std::max<int64_t>(1, std::min<int64_t>(max_blocks, (waves_wanted + 3) / 4)));
-  const int ncs = int((n + kStrip - 1) / kStrip);
-  int nrc = std::max(1, (grid * (kThreads / 64)) / ncs);
-  nrc = std::min<int>(nrc, kMaxChunks);
-  nrc = std::min<int>(nrc, int(std::max<int64_t>(1, n / kMinRowsPerChunk)));
-  const int rows = int((n + nrc - 1) / nrc);
+  const int n = p.n;
+  const int S = (n + kStrip - 1) / kStrip;
+  int P = std::max(1, max_blocks / S);
+  P = std::min(P, kMaxPanels);
+  P = std::min(P, std::max(1, n / kMinPanelRows));
+  const int rows = (n + P - 1) / P;
+  const int grid = std::min(P * S, max_blocks);
 
-  const Layout L = layout(n);
+  const Layout L = layout(n, p.k);
   char* w = static_cast<char*>(p.workspace);
   SgsDev a;
   a.C = p.cost;
   a.v = p.capacity;
-  a.n = p.n;
+  a.n = n;
   a.k = p.k;
   a.c0 = p.c0;
   a.selected = p.selected;
   a.step_gain = p.step_gain;
   a.step_obj = p.step_objective;
   a.assign = p.assign;
-  a.b = reinterpret_cast<float*>(w + L.b);
+  a.bpriv = reinterpret_cast<float*>(w + L.bpriv);
   a.mask = reinterpret_cast<uint8_t*>(w + L.mask);
   a.partial = reinterpret_cast<double*>(w + L.partial);
-  a.bbest_g = reinterpret_cast<double*>(w + L.bbest_g);
-  a.bbest_i = reinterpret_cast<int*>(w + L.bbest_i);
+  a.strip_g = reinterpret_cast<double*>(w + L.strip_g);
+  a.strip_i = reinterpret_cast<int*>(w + L.strip_i);
   a.obj_part = reinterpret_cast<double*>(w + L.obj_part);
-  a.counter = reinterpret_cast<unsigned int*>(w + L.ctrl);
-  a.tstar = reinterpret_cast<int*>(w + L.ctrl + 4);
-  a.ncs = ncs;
-  a.nrc = nrc;
+  a.key = reinterpret_cast<unsigned long long*>(w + L.key);
+  a.strip_cnt = reinterpret_cast<unsigned int*>(w + L.strip_cnt);
+  a.step_cnt = reinterpret_cast<unsigned int*>(w + L.ctrl);
+  a.fin_cnt = reinterpret_cast<unsigned int*>(w + L.ctrl + 4);
+  a.P = P;
+  a.S = S;
   a.rows = rows;
+
+  sgs_init_kernel<<<std::min(1024, (std::max(n, p.k) + 255) / 256), 256, 0, stream>>>(a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   void* args[] = {&a};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_dense_kernel), dim3(grid),
-                                    dim3(kThreads), args, 0, stream);
+  const void* fn = vec4 ? reinterpret_cast<const void*>(sgs_dense_kernel<kBlock, true>)
+                        : reinterpret_cast<const void*>(sgs_dense_kernel<kBlock, false>);
+  return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(kBlock), args, 0, stream);
 }
 
 }  // namespace cp

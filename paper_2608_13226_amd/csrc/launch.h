@@ -49,7 +49,7 @@ struct SgsParams {
   size_t workspace_bytes;
 };
 
-size_t sgs_workspace_bytes(int64_t n);
+size_t sgs_workspace_bytes(int64_t n, int64_t k);
 hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream);
 
 // CoverPrune-Lite.

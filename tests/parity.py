@@ -102,9 +102,10 @@ def check_trajectory_invariants(sel, gain, obj, v, c0, k, n):
     v = np.asarray(v, np.float64)
     total = c0 * v.sum()
     # L_k = c0 sum(v) - sum of gains, and L decreases by exactly each gain.
-    assert abs(obj[-1] - (total - gain.sum())) <= 1e-9 * total + 1e-12
+    # The kernel forms b - C in float32 (relative rounding 2^-24 per term).
+    assert abs(obj[-1] - (total - gain.sum())) <= 1e-6 * total + 1e-12
     prev = np.concatenate([[total], obj[:-1]])
-    assert np.allclose(prev - obj, gain, rtol=1e-7, atol=1e-12 * total)
+    assert np.allclose(prev - obj, gain, rtol=1e-6, atol=1e-9 * total)
     # Gains of a monotone submodular function never grow along the greedy.
     assert np.all(np.diff(gain) <= 1e-9 * max(gain[0], 1e-300))
 
