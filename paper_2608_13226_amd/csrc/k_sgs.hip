@@ -21,7 +21,13 @@
 //      it into the step's packed (gain, index) maximum with one 64-bit
 //      atomicMax, and arrives at the step counter;
 //   4. waits until every strip has arrived and reads the step's winner.
-// Only thread 0 of a block issues device-scope fences, once per arrival.
+// Data that crosses blocks (partial gains, strip winners, objective shares,
+// the mask, the step's key and counters) is written and read only with
+// device-scope atomic operations, which are coherent across the chip's L2
+// caches without fences.  A block's writes are complete at the workgroup
+// barrier that precedes thread 0's counter update, so a block that observes
+// the counter also observes the data.  A device-scope fence would instead
+// write back the whole L2 and cost about as much as a step's tail.
 // Across strips the packed key compares gains truncated to 44 bits (relative
 // resolution 2^-32) and breaks ties by the smaller index; within a strip the
 // comparison is exact.
@@ -53,10 +59,9 @@ struct SgsDev {
   double* step_obj;
   int32_t* assign;
   float* bpriv;              // [items][rows] private best costs
-  uint8_t* mask;
+  unsigned int* mask;        // [n] 1 once chosen
   double* partial;           // [P][n]
-  double* strip_g;           // [S]
-  int* strip_i;              // [S]
+  double* strip_g;           // [S] exact gain of each strip's winner
   double* obj_part;          // [P]
   unsigned long long* key;   // [k] packed step maxima
   unsigned int* strip_cnt;   // [S]
@@ -66,7 +71,7 @@ struct SgsDev {
 };
 
 struct Layout {
-  size_t bpriv, mask, partial, strip_g, strip_i, obj_part, key, strip_cnt, ctrl, total;
+  size_t bpriv, mask, partial, strip_g, obj_part, key, strip_cnt, ctrl, total;
 };
 
 size_t a256(size_t x) { return (x + 255) / 256 * 256; }
@@ -77,10 +82,9 @@ Layout layout(int64_t n, int64_t k) {
   const size_t S = size_t((n + kStrip - 1) / kStrip);
   size_t o = 0;
   L.bpriv = o;     o += a256(S * size_t(n + kMaxPanels) * 4);
-  L.mask = o;      o += a256(size_t(n));
+  L.mask = o;      o += a256(size_t(n) * 4);
   L.partial = o;   o += a256(size_t(kMaxPanels) * size_t(n) * 8);
   L.strip_g = o;   o += a256(size_t(kMaxStrips) * 8);
-  L.strip_i = o;   o += a256(size_t(kMaxStrips) * 4);
   L.obj_part = o;  o += a256(size_t(kMaxPanels) * 8);
   L.key = o;       o += a256(size_t(k) * 8);
   L.strip_cnt = o; o += a256(size_t(kMaxStrips) * 4);
@@ -89,24 +93,31 @@ Layout layout(int64_t n, int64_t k) {
   return L;
 }
 
-// All threads' writes are complete at workgroup scope after the barrier;
-// thread 0 then publishes them device-wide and counts the block in.  Returns,
-// block-uniformly, the counter value before this block's increment; a block
-// that finds itself last has acquired every earlier arrival's writes.
+__device__ __forceinline__ void put(double* p, double x) {
+  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), (unsigned long long)__double_as_longlong(x),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double get(const double* p) {
+  return __longlong_as_double((long long)__hip_atomic_load(reinterpret_cast<const unsigned long long*>(p),
+                                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+__device__ __forceinline__ void put(unsigned int* p, unsigned int x) {
+  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned int get(const unsigned int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The barrier waits for every wave's outstanding memory operations, so the
+// block's device-scope stores are complete before thread 0 counts the block
+// in.  Returns, block-uniformly, the counter value before this increment.
 template <int BT>
 __device__ unsigned int block_arrive(unsigned int* counter, unsigned int* s_prev) {
   __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
+  if (threadIdx.x == 0)
     *s_prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
   __syncthreads();
   return *s_prev;
-}
-
-__device__ __forceinline__ void acquire_once() {
-  if (threadIdx.x == 0) __threadfence();
-  __syncthreads();
 }
 
 template <int BT>
@@ -146,7 +157,7 @@ __device__ double block_sum(double x, double* sd) {
 __global__ void sgs_init_kernel(SgsDev a) {
   const int gt = blockIdx.x * blockDim.x + threadIdx.x, nt = gridDim.x * blockDim.x;
   for (int j = gt; j < a.n; j += nt) {
-    a.mask[j] = 0;
+    a.mask[j] = 0u;
     if (a.assign) a.assign[j] = -1;
   }
   for (int s = gt; s < a.S; s += nt) a.strip_cnt[s] = 0u;
@@ -274,7 +285,7 @@ __device__ double sweep_item(const SgsDev& a, int step, int tprev, int it, int p
       double s = 0.0;
 #pragma unroll
       for (int x = 0; x < W; ++x) s += red[(x * 64 + l) * 4 + q];
-      a.partial[size_t(panel) * a.n + cc] = s;
+      put(a.partial + size_t(panel) * a.n + cc, s);
     }
   }
   return owner ? block_sum<BT>(objp, sd) : 0.0;
@@ -297,19 +308,18 @@ __global__ __launch_bounds__(BT) void sgs_dense_kernel(SgsDev a) {
     for (int it = blockIdx.x; it < items; it += gridDim.x) {
       const int panel = it / a.S, strip = it - panel * a.S;
       const double objp = sweep_item<BT, VEC4>(a, step, tprev, it, panel, strip, sb, sv, red, sd);
-      if (strip == 0 && tid == 0) a.obj_part[panel] = objp;
+      if (strip == 0 && tid == 0) put(a.obj_part + panel, objp);
 
       const unsigned int prev = block_arrive<BT>(a.strip_cnt + strip, &s_prev);
       if (prev != unsigned(step + 1) * unsigned(a.P) - 1u) continue;
       // Last block of the strip.
-      acquire_once();
       double g = -1.0;
       int gi = INT_MAX;
       if (tid < kStrip) {
         const int cc = strip * kStrip + tid;
-        if (cc < a.n && !a.mask[cc]) {
+        if (cc < a.n && !get(a.mask + cc)) {
           g = 0.0;
-          for (int p = 0; p < a.P; ++p) g += a.partial[size_t(p) * a.n + cc];
+          for (int p = 0; p < a.P; ++p) g += get(a.partial + size_t(p) * a.n + cc);
           gi = cc;
         }
       }
@@ -317,12 +327,11 @@ __global__ __launch_bounds__(BT) void sgs_dense_kernel(SgsDev a) {
       double prev_obj = 0.0;
       if (strip == 0 && step > 0) {
         double x = 0.0;
-        for (int p = tid; p < a.P; p += BT) x += a.obj_part[p];
+        for (int p = tid; p < a.P; p += BT) x += get(a.obj_part + p);
         prev_obj = block_sum<BT>(x, sd);
       }
       if (tid == 0) {
-        a.strip_g[strip] = g;
-        a.strip_i[strip] = gi;
+        put(a.strip_g + strip, g);
         if (gi != INT_MAX)
           __hip_atomic_fetch_max(a.key + step, pack_key(g, gi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (strip == 0 && step > 0 && a.step_obj) a.step_obj[step - 1] = prev_obj;
@@ -332,17 +341,15 @@ __global__ __launch_bounds__(BT) void sgs_dense_kernel(SgsDev a) {
     // Wait until every strip has reported, then read the winner.
     if (tid == 0) {
       const unsigned int target = unsigned(step + 1) * unsigned(a.S);
-      while (__hip_atomic_load(a.step_cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target)
-        __builtin_amdgcn_s_sleep(1);
-      __threadfence();
+      while (get(a.step_cnt) < target) __builtin_amdgcn_s_sleep(1);
       const unsigned long long kk = __hip_atomic_load(a.key + step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const int t = int(kIndexMask - (kk & kIndexMask));
       s_t = t;
       const int ts = t / kStrip;
-      if (int(blockIdx.x) == ts % int(gridDim.x)) a.mask[t] = 1;     // owner of item (0, ts)
+      if (int(blockIdx.x) == ts % int(gridDim.x)) put(a.mask + t, 1u);   // owner of item (0, ts)
       if (blockIdx.x == 0) {
         a.selected[step] = t;
-        if (a.step_gain) a.step_gain[step] = a.strip_g[ts];
+        if (a.step_gain) a.step_gain[step] = get(a.strip_g + ts);
       }
     }
     __syncthreads();
@@ -363,13 +370,12 @@ __global__ __launch_bounds__(BT) void sgs_dense_kernel(SgsDev a) {
       objp = fma(double(a.v[j]), double(fminf(bo, cv)), objp);
     }
     const double s = block_sum<BT>(objp, sd);
-    if (tid == 0) a.obj_part[panel] = s;
+    if (tid == 0) put(a.obj_part + panel, s);
   }
   const unsigned int fprev = block_arrive<BT>(a.fin_cnt, &s_prev);
   if (fprev == gridDim.x - 1u && a.step_obj) {
-    acquire_once();
     double x = 0.0;
-    for (int p = tid; p < a.P; p += BT) x += a.obj_part[p];
+    for (int p = tid; p < a.P; p += BT) x += get(a.obj_part + p);
     const double s = block_sum<BT>(x, sd);
     if (tid == 0) a.step_obj[a.k - 1] = s;
   }
@@ -421,10 +427,9 @@ hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream) {
   a.step_obj = p.step_objective;
   a.assign = p.assign;
   a.bpriv = reinterpret_cast<float*>(w + L.bpriv);
-  a.mask = reinterpret_cast<uint8_t*>(w + L.mask);
+  a.mask = reinterpret_cast<unsigned int*>(w + L.mask);
   a.partial = reinterpret_cast<double*>(w + L.partial);
   a.strip_g = reinterpret_cast<double*>(w + L.strip_g);
-  a.strip_i = reinterpret_cast<int*>(w + L.strip_i);
   a.obj_part = reinterpret_cast<double*>(w + L.obj_part);
   a.key = reinterpret_cast<unsigned long long*>(w + L.key);
   a.strip_cnt = reinterpret_cast<unsigned int*>(w + L.strip_cnt);
