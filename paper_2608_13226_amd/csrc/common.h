@@ -67,6 +67,50 @@ __device__ __forceinline__ float float_from_order_key(unsigned int k) {
   return __uint_as_float(u);
 }
 
+// Device-scope relaxed atomic loads and stores.  Data that one block writes
+// and another block reads inside the same launch goes through these: they are
+// coherent across the chip's per-XCD L2 caches without device-scope fences
+// (each of which writes back a whole L2).  A block's stores are complete at
+// the workgroup barrier that precedes its arrival at a counter.
+__device__ __forceinline__ void put(unsigned int* p, unsigned int x) {
+  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned int get(const unsigned int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void put(int* p, int x) {
+  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int get(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void put(unsigned long long* p, unsigned long long x) {
+  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long get(const unsigned long long* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void put(double* p, double x) {
+  put(reinterpret_cast<unsigned long long*>(p), (unsigned long long)__double_as_longlong(x));
+}
+__device__ __forceinline__ double get(const double* p) {
+  return __longlong_as_double((long long)get(reinterpret_cast<const unsigned long long*>(p)));
+}
+
+// Grid barrier for a cooperative launch: every block counts itself in and
+// waits until all gridDim.x blocks have arrived `round` times.  `counter`
+// must be zero at launch.  Only data written with put() before the barrier
+// may be read with get() after it.
+__device__ __forceinline__ void grid_barrier(unsigned int* counter, unsigned int round) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned int target = round * gridDim.x;
+    while (get(counter) < target) __builtin_amdgcn_s_sleep(1);
+  }
+  __syncthreads();
+}
+
 // (gain, index) pair ordering used by every argmax: larger gain first, then
 // smaller index.
 __device__ __forceinline__ bool better(double g, int i, double bg, int bi) {

@@ -1,26 +1,27 @@
 // CoverPrune-Lite (Sec. 4, Eq. 17-20) on one GPU.
 //
-//   front (one cooperative launch, grid barriers between phases)
+//   front (one cooperative launch; phases separated by fence-free grid
+//          barriers, data between phases exchanged with device-scope atomics)
 //     bbox     per-axis minimum of the positions (the Morton origin)
 //     keys     q = floor((x - min) * 256 / h) in float64, clamped to 21 bits;
 //              key = 3-way bit interleave; voxel = q >> 8
-//     sort     stable LSD radix sort of (key, token) in 8-bit digits, only
-//              over the key bits in use; ties stay in token order
-//     groups   V = floor(v * 2^40) in exact integers; exclusive scan gives the
-//              mass before each position, t(p) = min(K-1, K * mass / W); a
-//              prefix-min scan of t(p) - p and the K - N + p floor give the
+//     sort     stable LSD radix sort of (key, token) in 8-bit digits over the
+//              key bits in use; equal keys stay in token order
+//     groups   V = floor(v * 2^40) in exact integers; an exclusive scan gives
+//              the mass before each position, t(p) = min(K-1, K * mass / W);
+//              a prefix-min scan of t(p) - p and the K - N + p floor give the
 //              group of every position (the walk of Eq. 17 in scan form)
+//     tiles    16-row tiles per group and their prefix (work units below)
 //     maxima   M_x, M_tau over same-group, 27-adjacent pairs
 //     B(p)     sum_j v_j (lam_x phi(d_x / M_x) + lam_tau d_tau / M_tau), or
 //              v_j c0 for a non-adjacent pair: every term of the group cost
 //              that does not involve features
-//   pairs    one wave per group: the group's Gram on the matrix cores
-//            (16 x 16 tiles over D), d_f, A(p) = sum_j v_j d_f over adjacent
-//            pairs, and the global M_f
+//   pairs    one wave per 16-row tile of a group: the tile's rows against the
+//            whole group on the matrix cores (16 x 16 tiles over D), d_f,
+//            A(p) = sum_j v_j d_f over adjacent pairs, and the global M_f
 //   select   cost(p) = (lam_f / M_f) A(p) + B(p); per-group argmin (Eq. 18)
 //   total    fixed-order sum of the K prototype costs (Eq. 20 objective)
 #include <hip/hip_runtime.h>
-#include <hip/hip_cooperative_groups.h>
 
 #include <algorithm>
 #include <climits>
@@ -28,16 +29,16 @@
 #include "common.h"
 #include "launch.h"
 
-namespace cg = cooperative_groups;
-
 namespace cp {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
 constexpr int kFrontBlocks = 64;
 constexpr int kBins = 256;
 constexpr int kAxisBits = 21;
 constexpr int kSubBits = 8;
+constexpr int kTileRows = 16;
 
 struct LiteDev {
   const void* feats;
@@ -53,29 +54,33 @@ struct LiteDev {
   // workspace
   unsigned long long* key[2];
   int* tok[2];
-  int4* vox_tok;        // [n] voxel of each token
-  int4* vox_pos;        // [n] voxel of each sorted position
-  unsigned int* hist;   // [grid][256]
-  unsigned long long* bsum;  // [grid]
-  int* bmin;            // [grid]
-  int* gid;             // [n] group of each sorted position
-  int* gstart;          // [k + 1]
-  double* A;            // [n]
-  double* B;            // [n]
-  double* gcost;        // [k]
-  unsigned int* ctrl;   // see kCtrl* offsets
+  unsigned long long* vox_tok;  // [n] packed voxel of each token
+  unsigned long long* vox_pos;  // [n] packed voxel of each sorted position
+  unsigned int* hist;           // [G][256]
+  unsigned long long* bsum;     // [G]
+  int* bmin;                    // [G]
+  int* gid;                     // [n] group of each sorted position
+  int* gstart;                  // [k + 1]
+  int* rt_start;                // [k + 1] first 16-row tile of each group
+  double* A;                    // [n]
+  double* B;                    // [n]
+  double* gcost;                // [k]
+  unsigned int* ctrl;           // see kCtrl* offsets
 };
 
 // ctrl words
 constexpr int kCtrlBbox = 0;       // 3 x order key of the per-axis minimum
-constexpr int kCtrlMaxKey = 4;     // u64 (2 words)
-constexpr int kCtrlMx2 = 6;        // u64 bits of max squared distance (2 words)
+constexpr int kCtrlMaxKey = 4;     // u64 (words 4, 5)
+constexpr int kCtrlMx2 = 6;        // u64 bits of max squared distance (words 6, 7)
 constexpr int kCtrlMt = 8;         // max |d tau| over evaluated pairs
 constexpr int kCtrlMf = 9;         // float bits of max d_f
 constexpr int kCtrlSorted = 10;    // which key/tok buffer holds the sorted order
+constexpr int kCtrlBarrier = 11;   // grid barrier counter
+constexpr int kCtrlTiles = 12;     // total number of 16-row tiles
 
 struct Layout {
-  size_t key0, key1, tok0, tok1, vox_tok, vox_pos, hist, bsum, bmin, gid, gstart, A, B, gcost, ctrl, total;
+  size_t key0, key1, tok0, tok1, vox_tok, vox_pos, hist, bsum, bmin, gid, gstart, rt_start, A, B, gcost,
+      ctrl, total;
 };
 
 size_t a256(size_t x) { return (x + 255) / 256 * 256; }
@@ -83,21 +88,22 @@ size_t a256(size_t x) { return (x + 255) / 256 * 256; }
 Layout layout(int64_t n, int64_t k) {
   Layout L;
   size_t o = 0;
-  L.key0 = o;    o += a256(size_t(n) * 8);
-  L.key1 = o;    o += a256(size_t(n) * 8);
-  L.tok0 = o;    o += a256(size_t(n) * 4);
-  L.tok1 = o;    o += a256(size_t(n) * 4);
-  L.vox_tok = o; o += a256(size_t(n) * 16);
-  L.vox_pos = o; o += a256(size_t(n) * 16);
-  L.hist = o;    o += a256(size_t(kFrontBlocks) * kBins * 4);
-  L.bsum = o;    o += a256(size_t(kFrontBlocks) * 8);
-  L.bmin = o;    o += a256(size_t(kFrontBlocks) * 4);
-  L.gid = o;     o += a256(size_t(n) * 4);
-  L.gstart = o;  o += a256(size_t(k + 1) * 4);
-  L.A = o;       o += a256(size_t(n) * 8);
-  L.B = o;       o += a256(size_t(n) * 8);
-  L.gcost = o;   o += a256(size_t(k) * 8);
-  L.ctrl = o;    o += 256;
+  L.key0 = o;     o += a256(size_t(n) * 8);
+  L.key1 = o;     o += a256(size_t(n) * 8);
+  L.tok0 = o;     o += a256(size_t(n) * 4);
+  L.tok1 = o;     o += a256(size_t(n) * 4);
+  L.vox_tok = o;  o += a256(size_t(n) * 8);
+  L.vox_pos = o;  o += a256(size_t(n) * 8);
+  L.hist = o;     o += a256(size_t(kFrontBlocks) * kBins * 4);
+  L.bsum = o;     o += a256(size_t(kFrontBlocks) * 8);
+  L.bmin = o;     o += a256(size_t(kFrontBlocks) * 4);
+  L.gid = o;      o += a256(size_t(n) * 4);
+  L.gstart = o;   o += a256(size_t(k + 1) * 4);
+  L.rt_start = o; o += a256(size_t(k + 1) * 4);
+  L.A = o;        o += a256(size_t(n) * 8);
+  L.B = o;        o += a256(size_t(n) * 8);
+  L.gcost = o;    o += a256(size_t(k) * 8);
+  L.ctrl = o;     o += 256;
   L.total = o;
   return L;
 }
@@ -106,6 +112,17 @@ __device__ __forceinline__ unsigned long long spread3(unsigned int x) {
   unsigned long long r = 0;
   for (int i = 0; i < kAxisBits; ++i) r |= (unsigned long long)((x >> i) & 1u) << (3 * i);
   return r;
+}
+
+// Voxel coordinates (q >> 8, at most 13 bits each) packed 21 bits apart.
+__device__ __forceinline__ unsigned long long pack_vox(unsigned int x, unsigned int y, unsigned int z) {
+  return (unsigned long long)x | ((unsigned long long)y << 21) | ((unsigned long long)z << 42);
+}
+
+__device__ __forceinline__ bool adjacent(unsigned long long a, unsigned long long b) {
+  const int ax = int(a & 0x1fffff), ay = int((a >> 21) & 0x1fffff), az = int(a >> 42);
+  const int bx = int(b & 0x1fffff), by = int((b >> 21) & 0x1fffff), bz = int(b >> 42);
+  return abs(ax - bx) <= 1 && abs(ay - by) <= 1 && abs(az - bz) <= 1;
 }
 
 __device__ __forceinline__ double sq_dist(double ax, double ay, double az, double bx, double by,
@@ -134,11 +151,11 @@ __device__ long long thresholds_crossed(unsigned long long K, unsigned long long
   return tq;
 }
 
-__device__ __forceinline__ bool adjacent(int4 a, int4 b) {
-  return abs(a.x - b.x) <= 1 && abs(a.y - b.y) <= 1 && abs(a.z - b.z) <= 1;
+__device__ __forceinline__ unsigned long long capacity_units(float v) {
+  return (unsigned long long)floor(double(v) * 1099511627776.0);   // v * 2^40
 }
 
-// Inclusive block scan helpers over 256 threads.
+// Block scans over 256 threads.
 __device__ unsigned long long block_excl_sum_u64(unsigned long long x, unsigned long long* sh,
                                                  unsigned long long& total) {
   const int t = threadIdx.x;
@@ -171,31 +188,38 @@ __device__ int block_incl_min(int x, int* sh) {
   return r;
 }
 
-__global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
-  cg::grid_group grid = cg::this_grid();
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int G = gridDim.x, blk = blockIdx.x;
-  const int n = a.n;
-  const int tile = (n + G - 1) / G;
-  const int p0 = min(n, blk * tile), p1 = min(n, p0 + tile);
+__device__ __forceinline__ int clamp_range(int x, int n) { return min(max(x, 0), n); }
 
-  __shared__ unsigned int s_u32[3][4];
-  __shared__ unsigned long long s_u64[kThreads];
-  __shared__ int s_i32[kThreads];
-  __shared__ unsigned int s_hist[kBins];
-  __shared__ unsigned int s_base[kBins];
-  __shared__ unsigned int s_wcnt[kThreads / 64][kBins];
-  __shared__ unsigned long long s_off;
-  __shared__ int s_minoff;
-
-  if (blk == 0 && t == 0) {
+__global__ void lite_init_kernel(LiteDev a) {
+  if (threadIdx.x == 0) {
     a.ctrl[kCtrlBbox + 0] = a.ctrl[kCtrlBbox + 1] = a.ctrl[kCtrlBbox + 2] = 0xffffffffu;
     *reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey) = 0ull;
     *reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2) = 0ull;
     a.ctrl[kCtrlMt] = 0u;
     a.ctrl[kCtrlMf] = 0u;
+    a.ctrl[kCtrlSorted] = 0u;
+    a.ctrl[kCtrlBarrier] = 0u;
+    a.ctrl[kCtrlTiles] = 0u;
   }
-  grid.sync();
+}
+
+__global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int G = gridDim.x, blk = blockIdx.x;
+  const int n = a.n, K = a.k;
+  const int tile = (n + G - 1) / G;
+  const int p0 = min(n, blk * tile), p1 = min(n, p0 + tile);
+  unsigned int* bar = a.ctrl + kCtrlBarrier;
+  unsigned int round = 0;
+
+  __shared__ unsigned int s_u32[3][kWaves];
+  __shared__ unsigned long long s_u64[kThreads];
+  __shared__ int s_i32[kThreads];
+  __shared__ unsigned int s_hist[kBins];
+  __shared__ unsigned int s_base[kBins];
+  __shared__ unsigned int s_wcnt[kWaves][kBins];
+  __shared__ unsigned long long s_off, s_w;
+  __shared__ int s_minoff;
 
   // ---- bbox minimum per axis
   {
@@ -210,21 +234,20 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     __syncthreads();
     if (t < 3) {
       unsigned int x = s_u32[t][0];
-      for (int q = 1; q < 4; ++q) x = min(x, s_u32[t][q]);
+      for (int q = 1; q < kWaves; ++q) x = min(x, s_u32[t][q]);
       atomicMin(a.ctrl + kCtrlBbox + t, x);
     }
   }
-  grid.sync();
+  grid_barrier(bar, ++round);
 
   // ---- Morton keys
   {
-    const double o0 = float_from_order_key(a.ctrl[kCtrlBbox + 0]);
-    const double o1 = float_from_order_key(a.ctrl[kCtrlBbox + 1]);
-    const double o2 = float_from_order_key(a.ctrl[kCtrlBbox + 2]);
+    const double org[3] = {double(float_from_order_key(get(a.ctrl + kCtrlBbox + 0))),
+                           double(float_from_order_key(get(a.ctrl + kCtrlBbox + 1))),
+                           double(float_from_order_key(get(a.ctrl + kCtrlBbox + 2)))};
     const double top = double((1 << kAxisBits) - 1);
     unsigned long long kmax = 0ull;
     for (int i = p0 + t; i < p1; i += kThreads) {
-      const double org[3] = {o0, o1, o2};
       unsigned int q[3];
       for (int ax = 0; ax < 3; ++ax) {
         double g = floor((double(a.pos[3 * i + ax]) - org[ax]) * a.grid_scale);
@@ -232,9 +255,9 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
         q[ax] = (unsigned int)g;
       }
       const unsigned long long key = spread3(q[0]) | (spread3(q[1]) << 1) | (spread3(q[2]) << 2);
-      a.key[0][i] = key;
-      a.tok[0][i] = i;
-      a.vox_tok[i] = make_int4(int(q[0] >> kSubBits), int(q[1] >> kSubBits), int(q[2] >> kSubBits), 0);
+      put(a.key[0] + i, key);
+      put(a.tok[0] + i, i);
+      put(a.vox_tok + i, pack_vox(q[0] >> kSubBits, q[1] >> kSubBits, q[2] >> kSubBits));
       kmax = max(kmax, key);
     }
     for (int o = 32; o > 0; o >>= 1) {
@@ -243,31 +266,31 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     }
     if (lane == 0) atomicMax(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey), kmax);
   }
-  grid.sync();
+  grid_barrier(bar, ++round);
 
   // ---- stable LSD radix sort of (key, token), 8 bits per pass
-  const unsigned long long maxkey = *reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey);
+  const unsigned long long maxkey = get(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey));
   const int bits = maxkey ? 64 - __clzll((long long)maxkey) : 0;
   const int passes = (bits + 7) / 8;
   for (int pass = 0; pass < passes; ++pass) {
-    const int src = pass & 1, dst = src ^ 1, sh = 8 * pass;
+    const int src = pass & 1, sh = 8 * pass;
     const unsigned long long* ks = src ? a.key[1] : a.key[0];
     const int* ts = src ? a.tok[1] : a.tok[0];
-    unsigned long long* kd = dst ? a.key[1] : a.key[0];
-    int* td = dst ? a.tok[1] : a.tok[0];
+    unsigned long long* kd = src ? a.key[0] : a.key[1];
+    int* td = src ? a.tok[0] : a.tok[1];
     s_hist[t] = 0u;
     __syncthreads();
-    for (int i = p0 + t; i < p1; i += kThreads) atomicAdd(&s_hist[(ks[i] >> sh) & 0xffu], 1u);
+    for (int i = p0 + t; i < p1; i += kThreads) atomicAdd(&s_hist[(get(ks + i) >> sh) & 0xffu], 1u);
     __syncthreads();
-    a.hist[blk * kBins + t] = s_hist[t];
-    grid.sync();
+    put(a.hist + blk * kBins + t, s_hist[t]);
+    grid_barrier(bar, ++round);
 
-    // Base offset of digit t for this block: all smaller digits everywhere,
+    // Base offset of digit t for this block: every smaller digit anywhere,
     // plus digit t in earlier blocks.
     {
       unsigned int tot = 0u, pre = 0u;
       for (int b = 0; b < G; ++b) {
-        const unsigned int h = a.hist[b * kBins + t];
+        const unsigned int h = get(a.hist + b * kBins + t);
         tot += h;
         if (b < blk) pre += h;
       }
@@ -282,7 +305,9 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     for (int c0 = p0; c0 < p1; c0 += kThreads) {
       const int i = c0 + t;
       const bool live = i < p1;
-      const unsigned int dig = live ? unsigned((ks[i] >> sh) & 0xffu) : 0u;
+      const unsigned long long kv = live ? get(ks + i) : 0ull;
+      const int tv = live ? get(ts + i) : 0;
+      const unsigned int dig = unsigned((kv >> sh) & 0xffu);
       unsigned long long same = __ballot(live);
       for (int bit = 0; bit < 8; ++bit) {
         const unsigned long long m = __ballot(live && ((dig >> bit) & 1u));
@@ -290,23 +315,23 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       }
       const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
       const int rank = __popcll(same & below);
-      for (int q = t; q < (kThreads / 64) * kBins; q += kThreads) (&s_wcnt[0][0])[q] = 0u;
+      for (int q = t; q < kWaves * kBins; q += kThreads) (&s_wcnt[0][0])[q] = 0u;
       __syncthreads();
       if (live && rank == 0) s_wcnt[w][dig] = unsigned(__popcll(same));
       __syncthreads();
       if (live) {
         unsigned int off = s_base[dig];
         for (int q = 0; q < w; ++q) off += s_wcnt[q][dig];
-        kd[off + rank] = ks[i];
-        td[off + rank] = ts[i];
+        put(kd + off + rank, kv);
+        put(td + off + rank, tv);
       }
       __syncthreads();
       unsigned int add = 0u;
-      for (int q = 0; q < kThreads / 64; ++q) add += s_wcnt[q][t];
+      for (int q = 0; q < kWaves; ++q) add += s_wcnt[q][t];
       s_base[t] += add;
       __syncthreads();
     }
-    grid.sync();
+    grid_barrier(bar, ++round);
   }
   const int sorted = passes & 1;
   const int* perm = sorted ? a.tok[1] : a.tok[0];
@@ -314,43 +339,40 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
   // ---- groups: exclusive scan of V over sorted positions
   {
     unsigned long long local = 0ull;
-    for (int i = p0 + t; i < p1; i += kThreads)
-      local += (unsigned long long)floor(double(a.v[perm[i]]) * 1099511627776.0);
+    for (int i = p0 + t; i < p1; i += kThreads) local += capacity_units(a.v[get(perm + i)]);
     unsigned long long tot;
     block_excl_sum_u64(local, s_u64, tot);
-    if (t == 0) a.bsum[blk] = tot;
+    if (t == 0) put(a.bsum + blk, tot);
   }
-  grid.sync();
+  grid_barrier(bar, ++round);
   {
     if (t == 0) {
       unsigned long long off = 0ull, W = 0ull;
       for (int b = 0; b < G; ++b) {
-        if (b < blk) off += a.bsum[b];
-        W += a.bsum[b];
+        const unsigned long long x = get(a.bsum + b);
+        if (b < blk) off += x;
+        W += x;
       }
       s_off = off;
-      s_u64[0] = W;  // consumed below before reuse
+      s_w = W;
     }
     __syncthreads();
-    const unsigned long long W = s_u64[0];
+    const unsigned long long W = s_w;
+    const unsigned long long KK = (unsigned long long)K;
     unsigned long long run = s_off;
-    __syncthreads();
-    const unsigned long long K = (unsigned long long)a.k;
     int bmin = INT_MAX;
     for (int c0 = p0; c0 < p1; c0 += kThreads) {
       const int i = c0 + t;
-      const unsigned long long V =
-          i < p1 ? (unsigned long long)floor(double(a.v[perm[i]]) * 1099511627776.0) : 0ull;
+      const unsigned long long V = i < p1 ? capacity_units(a.v[get(perm + i)]) : 0ull;
       unsigned long long chunk;
       const unsigned long long ex = block_excl_sum_u64(V, s_u64, chunk);
       if (i < p1) {
-        const unsigned long long before = run + ex;
         long long tp;
         if (i == 0) tp = 0;
-        else if (W == 0ull) tp = a.k - 1;
-        else tp = thresholds_crossed(K, before, W);
+        else if (W == 0ull) tp = K - 1;
+        else tp = thresholds_crossed(KK, run + ex, W);
         const int m = int(tp - i);
-        a.gid[i] = m;
+        put(a.gid + i, m);
         bmin = min(bmin, m);
       }
       run += chunk;
@@ -360,56 +382,68 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     __syncthreads();
     if (t == 0) {
       int m = s_i32[0];
-      for (int q = 1; q < 4; ++q) m = min(m, s_i32[q]);
-      a.bmin[blk] = m;
+      for (int q = 1; q < kWaves; ++q) m = min(m, s_i32[q]);
+      put(a.bmin + blk, m);
     }
   }
-  grid.sync();
+  grid_barrier(bar, ++round);
   {
     if (t == 0) {
       int m = INT_MAX;
-      for (int b = 0; b < blk; ++b) m = min(m, a.bmin[b]);
+      for (int b = 0; b < blk; ++b) m = min(m, get(a.bmin + b));
       s_minoff = m;
     }
     __syncthreads();
     int run = s_minoff;
     for (int c0 = p0; c0 < p1; c0 += kThreads) {
       const int i = c0 + t;
-      const int m = i < p1 ? a.gid[i] : INT_MAX;
+      const int m = i < p1 ? get(a.gid + i) : INT_MAX;
       const int inc = min(block_incl_min(m, s_i32), run);
-      if (i < p1) a.gid[i] = max(a.k - n + i, i + inc);
+      if (i < p1) put(a.gid + i, max(K - n + i, i + inc));
       s_i32[t] = inc;
       __syncthreads();
       run = s_i32[kThreads - 1];
       __syncthreads();
     }
   }
-  grid.sync();
+  grid_barrier(bar, ++round);
 
   // ---- group starts, voxels by sorted position, group output
   for (int i = p0 + t; i < p1; i += kThreads) {
-    const int q = a.gid[i];
-    if (i == 0 || a.gid[i - 1] != q) a.gstart[q] = i;
-    if (i == n - 1) a.gstart[a.k] = n;
-    const int tokn = perm[i];
-    a.vox_pos[i] = a.vox_tok[tokn];
+    const int q = get(a.gid + i);
+    if (i == 0 || get(a.gid + i - 1) != q) put(a.gstart + q, i);
+    if (i == n - 1) put(a.gstart + K, n);
+    const int tokn = get(perm + i);
+    put(a.vox_pos + i, get(a.vox_tok + tokn));
     if (a.group) a.group[tokn] = q;
   }
-  grid.sync();
+  grid_barrier(bar, ++round);
 
-  // ---- M_x, M_tau over same-group 27-adjacent pairs
+  // ---- tiles per group (block sums) and M_x, M_tau over evaluated pairs
+  const int gtile = (K + G - 1) / G;
+  const int q0 = min(K, blk * gtile), q1 = min(K, q0 + gtile);
   {
+    unsigned long long local = 0ull;
+    for (int q = q0 + t; q < q1; q += kThreads) {
+      const int g = max(0, get(a.gstart + q + 1) - get(a.gstart + q));
+      local += (unsigned long long)((g + kTileRows - 1) / kTileRows);
+    }
+    unsigned long long tot;
+    block_excl_sum_u64(local, s_u64, tot);
+    if (t == 0) put(a.bsum + blk, tot);
+
     double mx2 = 0.0;
     int mt = 0;
     for (int i = p0 + t; i < p1; i += kThreads) {
-      const int q = a.gid[i];
-      const int tokn = perm[i];
-      const int4 vi = a.vox_pos[i];
+      const int q = get(a.gid + i);
+      const int tokn = get(perm + i);
+      const unsigned long long vi = get(a.vox_pos + i);
       const double xi = a.pos[3 * tokn], yi = a.pos[3 * tokn + 1], zi = a.pos[3 * tokn + 2];
       const int fi = a.frame[tokn];
-      for (int j = a.gstart[q]; j < a.gstart[q + 1]; ++j) {
-        if (!adjacent(vi, a.vox_pos[j])) continue;
-        const int tj = perm[j];
+      const int j0 = clamp_range(get(a.gstart + q), n), j1 = clamp_range(get(a.gstart + q + 1), n);
+      for (int j = j0; j < j1; ++j) {
+        if (!adjacent(vi, get(a.vox_pos + j))) continue;
+        const int tj = get(perm + j);
         mx2 = fmax(mx2, sq_dist(xi, yi, zi, a.pos[3 * tj], a.pos[3 * tj + 1], a.pos[3 * tj + 2]));
         mt = max(mt, abs(fi - a.frame[tj]));
       }
@@ -421,24 +455,51 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       atomicMax(a.ctrl + kCtrlMt, unsigned(mt));
     }
   }
-  grid.sync();
+  grid_barrier(bar, ++round);
 
-  // ---- B(p): feature-free part of every group cost
+  // ---- tile prefix per group; B(p), the feature-free part of every group cost
   {
-    const double m_x = sqrt(__longlong_as_double(*reinterpret_cast<long long*>(a.ctrl + kCtrlMx2)));
-    const int m_t = int(a.ctrl[kCtrlMt]);
+    if (t == 0) {
+      unsigned long long off = 0ull, tot = 0ull;
+      for (int b = 0; b < G; ++b) {
+        const unsigned long long x = get(a.bsum + b);
+        if (b < blk) off += x;
+        tot += x;
+      }
+      s_off = off;
+      if (blk == 0) put(a.ctrl + kCtrlTiles, unsigned(tot));
+    }
+    __syncthreads();
+    unsigned long long run = s_off;
+    for (int c0 = q0; c0 < q1; c0 += kThreads) {
+      const int q = c0 + t;
+      unsigned long long nt = 0ull;
+      if (q < q1) {
+        const int g = max(0, get(a.gstart + q + 1) - get(a.gstart + q));
+        nt = (unsigned long long)((g + kTileRows - 1) / kTileRows);
+      }
+      unsigned long long chunk;
+      const unsigned long long ex = block_excl_sum_u64(nt, s_u64, chunk);
+      if (q < q1) a.rt_start[q] = int(run + ex);
+      if (q == K - 1) a.rt_start[K] = int(run + ex + nt);
+      run += chunk;
+    }
+
+    const double m_x = sqrt(__longlong_as_double((long long)get(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2))));
+    const int m_t = int(get(a.ctrl + kCtrlMt));
     const double c0 = double(a.lam_f) + double(a.lam_x) + double(a.lam_t);
     for (int i = p0 + t; i < p1; i += kThreads) {
-      const int q = a.gid[i];
-      const int tokn = perm[i];
-      const int4 vi = a.vox_pos[i];
+      const int q = get(a.gid + i);
+      const int tokn = get(perm + i);
+      const unsigned long long vi = get(a.vox_pos + i);
       const double xi = a.pos[3 * tokn], yi = a.pos[3 * tokn + 1], zi = a.pos[3 * tokn + 2];
       const int fi = a.frame[tokn];
       double acc = 0.0;
-      for (int j = a.gstart[q]; j < a.gstart[q + 1]; ++j) {
-        const int tj = perm[j];
+      const int j0 = clamp_range(get(a.gstart + q), n), j1 = clamp_range(get(a.gstart + q + 1), n);
+      for (int j = j0; j < j1; ++j) {
+        const int tj = get(perm + j);
         const double vj = double(a.v[tj]);
-        if (!adjacent(vi, a.vox_pos[j])) {
+        if (!adjacent(vi, get(a.vox_pos + j))) {
           acc += vj * c0;
           continue;
         }
@@ -455,105 +516,114 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
 }
 
 // ---------------------------------------------------------------------------
-// Within-group feature pass.  One wave per group; the group's sorted positions
-// [p0, p1) are cut into 16-row tiles and every tile pair is multiplied on the
-// matrix cores over the full feature width.  Lane l supplies row l % 16 and
+// Within-group feature pass.  Work unit: one 16-row tile of one group, taken
+// by one wave, multiplied on the matrix cores against every 16-row tile of the
+// same group over the full feature width.  Lane l supplies row l % 16 and
 // feature slice 8 (l / 16) .. +8 of each 32-wide K step (bf16), or 4 (l / 16)
 // .. +4 of each 16-wide step spread over four MFMAs (f32); the output element
 // (4 (l / 16) + r, l % 16) lands in register r of lane l.
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void lite_pair_kernel(LiteDev a) {
   const int lane = threadIdx.x & 63;
-  const int gw = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-  const int nw = gridDim.x * (kThreads / 64);
+  const int gw = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  const int nw = gridDim.x * kWaves;
   const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
+  const int units = int(a.ctrl[kCtrlTiles]);
   const int row = lane & 15, quad = lane >> 4;
   float lmax = 0.f;
 
-  for (int q = gw; q < a.k; q += nw) {
-    const int p0 = a.gstart[q], g = a.gstart[q + 1] - p0;
-    const int ntile = (g + 15) / 16;
-    for (int ta = 0; ta < ntile; ++ta) {
-      const int ra = ta * 16 + row;  // operand row of this lane in tile ta
-      double arow[4] = {0.0, 0.0, 0.0, 0.0};
-      for (int tb = 0; tb < ntile; ++tb) {
-        const int rb = tb * 16 + row;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        float na = 0.f, nb = 0.f;
-        if (BF16) {
-          const uint16_t* Fa = ra < g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[p0 + ra]) * a.d : nullptr;
-          const uint16_t* Fb = rb < g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[p0 + rb]) * a.d : nullptr;
-          for (int k0 = 0; k0 < a.d; k0 += 32) {
-            const int kk = k0 + quad * 8;
-            uint4 ua = {0u, 0u, 0u, 0u}, ub = {0u, 0u, 0u, 0u};
-            if (Fa && kk < a.d) ua = *reinterpret_cast<const uint4*>(Fa + kk);
-            if (tb == ta) ub = ua;
-            else if (Fb && kk < a.d) ub = *reinterpret_cast<const uint4*>(Fb + kk);
-            const uint32_t wa[4] = {ua.x, ua.y, ua.z, ua.w}, wb[4] = {ub.x, ub.y, ub.z, ub.w};
+  for (int u = gw; u < units; u += nw) {
+    // Group of unit u: the last q with rt_start[q] <= u.
+    int lo = 0, hi = a.k - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.rt_start[mid] <= u) lo = mid;
+      else hi = mid - 1;
+    }
+    const int q = lo;
+    const int p0 = clamp_range(a.gstart[q], a.n), g = max(0, clamp_range(a.gstart[q + 1], a.n) - p0);
+    const int ntile = (g + kTileRows - 1) / kTileRows;
+    const int ta = u - a.rt_start[q];
+    if (ta < 0 || ta >= ntile) continue;
+    const int ra = ta * kTileRows + row;  // operand row of this lane in tile ta
+    double arow[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int tb = 0; tb < ntile; ++tb) {
+      const int rb = tb * kTileRows + row;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      float na = 0.f, nb = 0.f;
+      if (BF16) {
+        const uint16_t* Fa = ra < g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[p0 + ra]) * a.d : nullptr;
+        const uint16_t* Fb = rb < g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[p0 + rb]) * a.d : nullptr;
+        for (int k0 = 0; k0 < a.d; k0 += 32) {
+          const int kk = k0 + quad * 8;
+          uint4 ua = {0u, 0u, 0u, 0u}, ub = {0u, 0u, 0u, 0u};
+          if (Fa && kk < a.d) ua = *reinterpret_cast<const uint4*>(Fa + kk);
+          if (tb == ta) ub = ua;
+          else if (Fb && kk < a.d) ub = *reinterpret_cast<const uint4*>(Fb + kk);
+          const uint32_t wa[4] = {ua.x, ua.y, ua.z, ua.w}, wb[4] = {ub.x, ub.y, ub.z, ub.w};
 #pragma unroll
-            for (int h = 0; h < 4; ++h) {
-              const float a0 = bf16_bits_to_float(wa[h] & 0xffffu), a1 = bf16_bits_to_float(wa[h] >> 16);
-              const float b0 = bf16_bits_to_float(wb[h] & 0xffffu), b1 = bf16_bits_to_float(wb[h] >> 16);
-              na = fmaf(a0, a0, fmaf(a1, a1, na));
-              nb = fmaf(b0, b0, fmaf(b1, b1, nb));
-            }
-            bf16x8 va, vb;
-            __builtin_memcpy(&va, &ua, sizeof va);
-            __builtin_memcpy(&vb, &ub, sizeof vb);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, vb, acc, 0, 0, 0);
+          for (int h = 0; h < 4; ++h) {
+            const float a0 = bf16_bits_to_float(wa[h] & 0xffffu), a1 = bf16_bits_to_float(wa[h] >> 16);
+            const float b0 = bf16_bits_to_float(wb[h] & 0xffffu), b1 = bf16_bits_to_float(wb[h] >> 16);
+            na = fmaf(a0, a0, fmaf(a1, a1, na));
+            nb = fmaf(b0, b0, fmaf(b1, b1, nb));
           }
-        } else {
-          const float* Fa = ra < g ? static_cast<const float*>(a.feats) + size_t(perm[p0 + ra]) * a.d : nullptr;
-          const float* Fb = rb < g ? static_cast<const float*>(a.feats) + size_t(perm[p0 + rb]) * a.d : nullptr;
-          for (int k0 = 0; k0 < a.d; k0 += 16) {
-            const int kk = k0 + quad * 4;
-            float4 fa = make_float4(0.f, 0.f, 0.f, 0.f), fb = fa;
-            if (Fa && kk < a.d) fa = *reinterpret_cast<const float4*>(Fa + kk);
-            if (tb == ta) fb = fa;
-            else if (Fb && kk < a.d) fb = *reinterpret_cast<const float4*>(Fb + kk);
-            na = fmaf(fa.x, fa.x, fmaf(fa.y, fa.y, fmaf(fa.z, fa.z, fmaf(fa.w, fa.w, na))));
-            nb = fmaf(fb.x, fb.x, fmaf(fb.y, fb.y, fmaf(fb.z, fb.z, fmaf(fb.w, fb.w, nb))));
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.x, fb.x, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.y, fb.y, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.z, fb.z, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.w, fb.w, acc, 0, 0, 0);
-          }
+          bf16x8 va, vb;
+          __builtin_memcpy(&va, &ua, sizeof va);
+          __builtin_memcpy(&vb, &ub, sizeof vb);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, vb, acc, 0, 0, 0);
         }
-        // Row sums of squares: the four lanes sharing l % 16 hold its slices.
-        na += __shfl_xor(na, 16);
-        na += __shfl_xor(na, 32);
-        nb += __shfl_xor(nb, 16);
-        nb += __shfl_xor(nb, 32);
-        const int cb = tb * 16 + row;          // output column of this lane
-        const bool cvalid = cb < g;
-        const int4 vb = cvalid ? a.vox_pos[p0 + cb] : make_int4(0, 0, 0, 0);
-        const double wv = cvalid ? double(a.v[perm[p0 + cb]]) : 0.0;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int oa = quad * 4 + r;         // output row within tile ta
-          const float nra = __shfl(na, oa);
-          const int ca = ta * 16 + oa;
-          if (cvalid && ca < g && adjacent(a.vox_pos[p0 + ca], vb)) {
-            const float den = sqrtf(nra) * sqrtf(nb);
-            const float cosv = den > 0.f ? acc[r] / den : 0.f;
-            float df = fminf(fmaxf(1.f - cosv, 0.f), 2.f);
-            if (ca == cb) df = 0.f;
-            arow[r] = fma(wv, double(df), arow[r]);
-            lmax = fmaxf(lmax, df);
-          }
+      } else {
+        const float* Fa = ra < g ? static_cast<const float*>(a.feats) + size_t(perm[p0 + ra]) * a.d : nullptr;
+        const float* Fb = rb < g ? static_cast<const float*>(a.feats) + size_t(perm[p0 + rb]) * a.d : nullptr;
+        for (int k0 = 0; k0 < a.d; k0 += 16) {
+          const int kk = k0 + quad * 4;
+          float4 fa = make_float4(0.f, 0.f, 0.f, 0.f), fb = fa;
+          if (Fa && kk < a.d) fa = *reinterpret_cast<const float4*>(Fa + kk);
+          if (tb == ta) fb = fa;
+          else if (Fb && kk < a.d) fb = *reinterpret_cast<const float4*>(Fb + kk);
+          na = fmaf(fa.x, fa.x, fmaf(fa.y, fa.y, fmaf(fa.z, fa.z, fmaf(fa.w, fa.w, na))));
+          nb = fmaf(fb.x, fb.x, fmaf(fb.y, fb.y, fmaf(fb.z, fb.z, fmaf(fb.w, fb.w, nb))));
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.x, fb.x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.y, fb.y, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.z, fb.z, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.w, fb.w, acc, 0, 0, 0);
         }
       }
-      // Sum each output row over the 16 lanes (columns) that share it.
+      // Row sums of squares: the four lanes sharing l % 16 hold its slices.
+      na += __shfl_xor(na, 16);
+      na += __shfl_xor(na, 32);
+      nb += __shfl_xor(nb, 16);
+      nb += __shfl_xor(nb, 32);
+      const int cb = tb * kTileRows + row;    // output column of this lane
+      const bool cvalid = cb < g;
+      const unsigned long long vb = cvalid ? a.vox_pos[p0 + cb] : 0ull;
+      const double wv = cvalid ? double(a.v[perm[p0 + cb]]) : 0.0;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        double x = arow[r];
-        x += __shfl_xor(x, 1);
-        x += __shfl_xor(x, 2);
-        x += __shfl_xor(x, 4);
-        x += __shfl_xor(x, 8);
-        const int ca = ta * 16 + quad * 4 + r;
-        if (row == 0 && ca < g) a.A[p0 + ca] = x;
+        const int oa = quad * 4 + r;           // output row within tile ta
+        const float nra = __shfl(na, oa);
+        const int ca = ta * kTileRows + oa;
+        if (cvalid && ca < g && adjacent(a.vox_pos[p0 + ca], vb)) {
+          const float den = sqrtf(nra) * sqrtf(nb);
+          const float cosv = den > 0.f ? acc[r] / den : 0.f;
+          float df = fminf(fmaxf(1.f - cosv, 0.f), 2.f);
+          if (ca == cb) df = 0.f;
+          arow[r] = fma(wv, double(df), arow[r]);
+          lmax = fmaxf(lmax, df);
+        }
       }
+    }
+    // Sum each output row over the 16 lanes (columns) that share it.
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      double x = arow[r];
+      x += __shfl_xor(x, 1);
+      x += __shfl_xor(x, 2);
+      x += __shfl_xor(x, 4);
+      x += __shfl_xor(x, 8);
+      const int ca = ta * kTileRows + quad * 4 + r;
+      if (row == 0 && ca < g) a.A[p0 + ca] = x;
     }
   }
   lmax = wave_max(lmax);
@@ -569,7 +639,8 @@ __global__ __launch_bounds__(kThreads) void lite_select_kernel(LiteDev a) {
   const double wf = m_f > 0.f ? double(a.lam_f) / double(m_f) : 0.0;
   double best = 0.0;
   int bt = INT_MAX;
-  for (int i = a.gstart[q]; i < a.gstart[q + 1]; ++i) {
+  const int i0 = clamp_range(a.gstart[q], a.n), i1 = clamp_range(a.gstart[q + 1], a.n);
+  for (int i = i0; i < i1; ++i) {
     const double c = fma(wf, a.A[i], a.B[i]);
     const int tk = perm[i];
     if (bt == INT_MAX || c < best || (c == best && tk < bt)) {
@@ -577,7 +648,7 @@ __global__ __launch_bounds__(kThreads) void lite_select_kernel(LiteDev a) {
       bt = tk;
     }
   }
-  a.selected[q] = bt;
+  a.selected[q] = bt == INT_MAX ? -1 : bt;
   a.gcost[q] = best;
 }
 
@@ -622,25 +693,31 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   a.key[1] = reinterpret_cast<unsigned long long*>(w + L.key1);
   a.tok[0] = reinterpret_cast<int*>(w + L.tok0);
   a.tok[1] = reinterpret_cast<int*>(w + L.tok1);
-  a.vox_tok = reinterpret_cast<int4*>(w + L.vox_tok);
-  a.vox_pos = reinterpret_cast<int4*>(w + L.vox_pos);
+  a.vox_tok = reinterpret_cast<unsigned long long*>(w + L.vox_tok);
+  a.vox_pos = reinterpret_cast<unsigned long long*>(w + L.vox_pos);
   a.hist = reinterpret_cast<unsigned int*>(w + L.hist);
   a.bsum = reinterpret_cast<unsigned long long*>(w + L.bsum);
   a.bmin = reinterpret_cast<int*>(w + L.bmin);
   a.gid = reinterpret_cast<int*>(w + L.gid);
   a.gstart = reinterpret_cast<int*>(w + L.gstart);
+  a.rt_start = reinterpret_cast<int*>(w + L.rt_start);
   a.A = reinterpret_cast<double*>(w + L.A);
   a.B = reinterpret_cast<double*>(w + L.B);
   a.gcost = reinterpret_cast<double*>(w + L.gcost);
   a.ctrl = reinterpret_cast<unsigned int*>(w + L.ctrl);
 
+  lite_init_kernel<<<1, 64, 0, stream>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const int G = std::max(1, std::min(kFrontBlocks, (p.n + kThreads - 1) / kThreads));
   void* args[] = {&a};
-  hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(lite_front_kernel), dim3(G),
-                                            dim3(kThreads), args, 0, stream);
+  e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(lite_front_kernel), dim3(G), dim3(kThreads),
+                                 args, 0, stream);
   if (e != hipSuccess) return e;
-  const int waves = p.k;
-  const int blocks = (waves + 3) / 4;
+  // One wave per 16-row tile; a group has at most n / 16 + 1 tiles in total
+  // over all groups, so n / 16 + k waves cover every tile.
+  const int units = p.n / kTileRows + p.k;
+  const int blocks = std::max(1, std::min((units + kWaves - 1) / kWaves, 65535));
   if (p.bf16)
     lite_pair_kernel<true><<<blocks, kThreads, 0, stream>>>(a);
   else
