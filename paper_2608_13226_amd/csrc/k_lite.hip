@@ -190,6 +190,28 @@ __device__ int block_incl_min(int x, int* sh) {
 
 __device__ __forceinline__ int clamp_range(int x, int n) { return min(max(x, 0), n); }
 
+// Sum of vals[0..G) and of vals[0..blk), read in parallel (one thread per
+// block, G <= 256) and reduced in LDS.  Result valid in every thread.
+__device__ void block_prefix_u64(const unsigned long long* vals, int G, int blk, unsigned long long* sh,
+                                 unsigned long long& before, unsigned long long& total) {
+  const int t = threadIdx.x;
+  sh[t] = t < G ? get(vals + t) : 0ull;
+  __syncthreads();
+  if (t == 0) {
+    unsigned long long b = 0ull, s = 0ull;
+    for (int x = 0; x < G; ++x) {
+      if (x < blk) b += sh[x];
+      s += sh[x];
+    }
+    sh[kThreads] = b;
+    sh[kThreads + 1] = s;
+  }
+  __syncthreads();
+  before = sh[kThreads];
+  total = sh[kThreads + 1];
+  __syncthreads();
+}
+
 __global__ void lite_init_kernel(LiteDev a) {
   if (threadIdx.x == 0) {
     a.ctrl[kCtrlBbox + 0] = a.ctrl[kCtrlBbox + 1] = a.ctrl[kCtrlBbox + 2] = 0xffffffffu;
@@ -213,12 +235,11 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
   unsigned int round = 0;
 
   __shared__ unsigned int s_u32[3][kWaves];
-  __shared__ unsigned long long s_u64[kThreads];
+  __shared__ unsigned long long s_u64[kThreads + 2];
   __shared__ int s_i32[kThreads];
   __shared__ unsigned int s_hist[kBins];
   __shared__ unsigned int s_base[kBins];
   __shared__ unsigned int s_wcnt[kWaves][kBins];
-  __shared__ unsigned long long s_off, s_w;
   __shared__ int s_minoff;
 
   // ---- bbox minimum per axis
@@ -289,10 +310,15 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     // plus digit t in earlier blocks.
     {
       unsigned int tot = 0u, pre = 0u;
-      for (int b = 0; b < G; ++b) {
-        const unsigned int h = get(a.hist + b * kBins + t);
-        tot += h;
-        if (b < blk) pre += h;
+      for (int b0 = 0; b0 < G; b0 += 16) {
+        unsigned int h[16];
+#pragma unroll
+        for (int x = 0; x < 16; ++x) h[x] = b0 + x < G ? get(a.hist + (b0 + x) * kBins + t) : 0u;
+#pragma unroll
+        for (int x = 0; x < 16; ++x) {
+          tot += h[x];
+          if (b0 + x < blk) pre += h[x];
+        }
       }
       unsigned long long total;
       const unsigned long long ex = block_excl_sum_u64(tot, s_u64, total);
@@ -346,20 +372,9 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
   }
   grid_barrier(bar, ++round);
   {
-    if (t == 0) {
-      unsigned long long off = 0ull, W = 0ull;
-      for (int b = 0; b < G; ++b) {
-        const unsigned long long x = get(a.bsum + b);
-        if (b < blk) off += x;
-        W += x;
-      }
-      s_off = off;
-      s_w = W;
-    }
-    __syncthreads();
-    const unsigned long long W = s_w;
+    unsigned long long run, W;
+    block_prefix_u64(a.bsum, G, blk, s_u64, run, W);
     const unsigned long long KK = (unsigned long long)K;
-    unsigned long long run = s_off;
     int bmin = INT_MAX;
     for (int c0 = p0; c0 < p1; c0 += kThreads) {
       const int i = c0 + t;
@@ -388,9 +403,11 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
   }
   grid_barrier(bar, ++round);
   {
+    s_i32[t] = t < blk ? get(a.bmin + t) : INT_MAX;
+    __syncthreads();
     if (t == 0) {
       int m = INT_MAX;
-      for (int b = 0; b < blk; ++b) m = min(m, get(a.bmin + b));
+      for (int b = 0; b < blk; ++b) m = min(m, s_i32[b]);
       s_minoff = m;
     }
     __syncthreads();
@@ -459,18 +476,9 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
 
   // ---- tile prefix per group; B(p), the feature-free part of every group cost
   {
-    if (t == 0) {
-      unsigned long long off = 0ull, tot = 0ull;
-      for (int b = 0; b < G; ++b) {
-        const unsigned long long x = get(a.bsum + b);
-        if (b < blk) off += x;
-        tot += x;
-      }
-      s_off = off;
-      if (blk == 0) put(a.ctrl + kCtrlTiles, unsigned(tot));
-    }
-    __syncthreads();
-    unsigned long long run = s_off;
+    unsigned long long run, tot;
+    block_prefix_u64(a.bsum, G, blk, s_u64, run, tot);
+    if (blk == 0 && t == 0) put(a.ctrl + kCtrlTiles, unsigned(tot));
     for (int c0 = q0; c0 < q1; c0 += kThreads) {
       const int q = c0 + t;
       unsigned long long nt = 0ull;
@@ -554,24 +562,35 @@ __global__ __launch_bounds__(kThreads) void lite_pair_kernel(LiteDev a) {
       if (BF16) {
         const uint16_t* Fa = ra < g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[p0 + ra]) * a.d : nullptr;
         const uint16_t* Fb = rb < g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[p0 + rb]) * a.d : nullptr;
-        for (int k0 = 0; k0 < a.d; k0 += 32) {
-          const int kk = k0 + quad * 8;
-          uint4 ua = {0u, 0u, 0u, 0u}, ub = {0u, 0u, 0u, 0u};
-          if (Fa && kk < a.d) ua = *reinterpret_cast<const uint4*>(Fa + kk);
-          if (tb == ta) ub = ua;
-          else if (Fb && kk < a.d) ub = *reinterpret_cast<const uint4*>(Fb + kk);
-          const uint32_t wa[4] = {ua.x, ua.y, ua.z, ua.w}, wb[4] = {ub.x, ub.y, ub.z, ub.w};
+        // Eight 32-wide K steps per round: all loads first, then the MFMAs.
+        constexpr int U = 8;
+        const bool same = tb == ta;
+        for (int k0 = 0; k0 < a.d; k0 += 32 * U) {
+          uint4 ua[U], ub[U];
 #pragma unroll
-          for (int h = 0; h < 4; ++h) {
-            const float a0 = bf16_bits_to_float(wa[h] & 0xffffu), a1 = bf16_bits_to_float(wa[h] >> 16);
-            const float b0 = bf16_bits_to_float(wb[h] & 0xffffu), b1 = bf16_bits_to_float(wb[h] >> 16);
-            na = fmaf(a0, a0, fmaf(a1, a1, na));
-            nb = fmaf(b0, b0, fmaf(b1, b1, nb));
+          for (int x = 0; x < U; ++x) {
+            const int kk = k0 + 32 * x + quad * 8;
+            ua[x] = uint4{0u, 0u, 0u, 0u};
+            ub[x] = uint4{0u, 0u, 0u, 0u};
+            if (Fa && kk < a.d) ua[x] = *reinterpret_cast<const uint4*>(Fa + kk);
+            if (!same && Fb && kk < a.d) ub[x] = *reinterpret_cast<const uint4*>(Fb + kk);
           }
-          bf16x8 va, vb;
-          __builtin_memcpy(&va, &ua, sizeof va);
-          __builtin_memcpy(&vb, &ub, sizeof vb);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, vb, acc, 0, 0, 0);
+#pragma unroll
+          for (int x = 0; x < U; ++x) {
+            if (same) ub[x] = ua[x];
+            const uint32_t wa[4] = {ua[x].x, ua[x].y, ua[x].z, ua[x].w}, wb[4] = {ub[x].x, ub[x].y, ub[x].z, ub[x].w};
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+              const float a0 = bf16_bits_to_float(wa[h] & 0xffffu), a1 = bf16_bits_to_float(wa[h] >> 16);
+              const float b0 = bf16_bits_to_float(wb[h] & 0xffffu), b1 = bf16_bits_to_float(wb[h] >> 16);
+              na = fmaf(a0, a0, fmaf(a1, a1, na));
+              nb = fmaf(b0, b0, fmaf(b1, b1, nb));
+            }
+            bf16x8 va, vb;
+            __builtin_memcpy(&va, &ua[x], sizeof va);
+            __builtin_memcpy(&vb, &ub[x], sizeof vb);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, vb, acc, 0, 0, 0);
+          }
         }
       } else {
         const float* Fa = ra < g ? static_cast<const float*>(a.feats) + size_t(perm[p0 + ra]) * a.d : nullptr;
