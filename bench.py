@@ -37,6 +37,8 @@ def _args():
     ap.add_argument("--workload", default="n16384_d3584")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lite-workload", default="lite_n32768_d3584",
+                    help="also time CoverPrune-Lite alone on this workload ('' to skip)")
     return ap.parse_args()
 
 
@@ -93,6 +95,40 @@ def cpu_baseline(scene, lite_h):
         "parts_ms": {"fst_cost": round(t_cost * 1e3, 1), "sgs_select": round(t_sgs * 1e3, 1),
                      "lite_select": round(t_lite * 1e3, 1)},
     }
+
+
+def time_lite(name, seed, reps, dev):
+    """CoverPrune-Lite alone on its own workload: HIP-event time per call and
+    the feature stream's share of HBM peak (features are read once)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_13226_amd as cp
+    from scenes import CONFIGS, make_scene, to_device
+
+    cfg = CONFIGS[name]
+    scene = make_scene(cfg, seed)
+    t = to_device(scene, dev)
+    lib = cp.library()
+    dt = cp.CP_BF16 if scene.dtype == "bf16" else cp.CP_F32
+    ws = torch.empty(lib.coverprune_lite_workspace(scene.n, scene.dim, scene.k, dt), dtype=torch.uint8, device=dev)
+    run = lambda: cp.lite_select(t["feats"], t["pos"], t["frame"], t["capacity"], scene.k,
+                                 voxel_size=cfg.voxel or 0.25, workspace=ws)
+    run()
+    torch.cuda.synchronize()
+    e0 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    e1 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    for i in range(reps):
+        e0[i].record()
+        run()
+        e1[i].record()
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(b) for a, b in zip(e0, e1)]))
+    feat_bytes = float(scene.n) * scene.dim * (2 if scene.dtype == "bf16" else 4)
+    return {"workload": name, "n": scene.n, "d": scene.dim, "k": scene.k, "voxel_m": cfg.voxel,
+            "ms_per_scene": round(ms, 4),
+            "hbm": {"achieved": round(feat_bytes / (ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "bytes": feat_bytes, "note": "features read once; whole call timed"}}
 
 
 def main():
@@ -206,6 +242,8 @@ def main():
         },
         "device": torch.cuda.get_device_name(0),
     }
+    if args.lite_workload:
+        out["lite_workload"] = time_lite(args.lite_workload, args.seed, max(K, 5), dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(scene, lite_h)
     print(json.dumps(out), flush=True)

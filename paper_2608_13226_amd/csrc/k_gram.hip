@@ -7,8 +7,9 @@
 // mirrors the lower triangle.
 //
 // bf16: v_mfma_f32_32x32x16_bf16, fp32 accumulation.  f32: v_mfma_f32_32x32x2f32.
-// Block tile 128 x 128, four waves in a 2 x 2 arrangement of 64 x 64 wave
-// tiles (2 x 2 MFMA 32 x 32 tiles each); K staged through LDS.
+// Large bf16 problems use 256 x 256 block tiles (gram_bf16_big_kernel); the
+// rest use 128 x 128 block tiles, four waves in a 2 x 2 arrangement of 64 x 64
+// wave tiles (2 x 2 MFMA 32 x 32 tiles each), K staged through LDS.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -29,25 +30,59 @@ __device__ __forceinline__ void upper_tile(int b, int& ti, int& tj) {
 
 // Accumulator element (mi, ni, r) of lane `lane` in a 32x32 MFMA output sits at
 // row 8*(r/4) + 4*(lane/32) + r%4 and column lane%32 of that 32x32 tile.
-__device__ __forceinline__ void store_df(const f32x16 (&acc)[2][2], int row0, int col0, int wm, int wn,
-                                         int lane, int n, const float* inv_norm, float* out,
-                                         unsigned int* mf_bits) {
+// (row0, col0) is the wave's corner.  The inverse norms of a 32-row group are
+// fetched before its first store.  A wave block that lies inside the matrix
+// and off the diagonal (the common case) stores through a buffer resource
+// based at its corner: per-lane 32-bit offsets, row steps in the scalar
+// offset, no per-element checks.
+template <int MT, int NT>
+__device__ __forceinline__ void store_df(const f32x16 (&acc)[MT][NT], int row0, int col0, int lane, int n,
+                                         const float* inv_norm, float* out, unsigned int* mf_bits) {
+  float rc[NT];
+#pragma unroll
+  for (int ni = 0; ni < NT; ++ni) rc[ni] = inv_norm[min(col0 + ni * 32 + (lane & 31), n - 1)];
   float lmax = 0.f;
+  const bool fast = row0 + MT * 32 <= n && col0 + NT * 32 <= n && (row0 >= col0 + NT * 32 || col0 >= row0 + MT * 32);
+  if (fast) {
+    float* base = out + size_t(row0) * n + col0;
+    const size_t left = (size_t(n) * n - (size_t(row0) * n + col0)) * 4;
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(base, 0, int(left < 0x7fffffffu ? left : 0x7fffffffu), 0x00020000);
+    const int voff = ((4 * (lane >> 5)) * n + (lane & 31)) * 4;
 #pragma unroll
-  for (int ni = 0; ni < 2; ++ni) {
-    const int col = col0 + wn * 64 + ni * 32 + (lane & 31);
-    const float rc = col < n ? inv_norm[col] : 0.f;
+    for (int mi = 0; mi < MT; ++mi) {
+      float rn[16];
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi) {
+      for (int r = 0; r < 16; ++r) rn[r] = inv_norm[row0 + mi * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = row0 + wm * 64 + mi * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < n && col < n) {
-          const float cosv = acc[mi][ni][r] * inv_norm[row] * rc;
-          float df = fminf(fmaxf(1.f - cosv, 0.f), 2.f);
-          if (row == col) df = 0.f;
-          out[size_t(row) * n + col] = df;
+      for (int ni = 0; ni < NT; ++ni)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float df = fminf(fmaxf(1.f - acc[mi][ni][r] * rn[r] * rc[ni], 0.f), 2.f);
           lmax = fmaxf(lmax, df);
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(df), rsrc, voff + ni * 128,
+                                                (mi * 32 + 8 * (r >> 2) + (r & 3)) * n * 4, 0);
+        }
+    }
+  } else {
+#pragma unroll
+    for (int mi = 0; mi < MT; ++mi) {
+      float rn[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        rn[r] = inv_norm[min(row0 + mi * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3), n - 1)];
+#pragma unroll
+      for (int ni = 0; ni < NT; ++ni) {
+        const int col = col0 + ni * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + mi * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          float df = fminf(fmaxf(1.f - acc[mi][ni][r] * rn[r] * rc[ni], 0.f), 2.f);
+          if (row == col) df = 0.f;
+          if (row < n && col < n) {
+            out[size_t(row) * n + col] = df;
+            lmax = fmaxf(lmax, df);
+          }
         }
       }
     }
@@ -70,7 +105,7 @@ __global__ __launch_bounds__(256) void gram_bf16_kernel(const uint16_t* __restri
   __shared__ __attribute__((aligned(16))) uint16_t As[kTile * kLdB];
   __shared__ __attribute__((aligned(16))) uint16_t Bs[kTile * kLdB];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   f32x16 acc[2][2];
 #pragma unroll
@@ -133,7 +168,222 @@ __global__ __launch_bounds__(256) void gram_bf16_kernel(const uint16_t* __restri
   }
 #undef CP_GLOAD_ALL_B
 #undef CP_GLOAD_B
-  store_df(acc, row0, col0, wm, wn, lane, n, inv_norm, out, mf_bits);
+  store_df(acc, row0 + wm * 64, col0 + wn * 64, lane, n, inv_norm, out, mf_bits);
+}
+
+// ---------------------------------------------------------------------------
+// Large-tile bf16 Gram for D % 128 == 0 and n d < 2^30: 256 x 256 block
+// tiles, eight waves (two per SIMD) of 128 x 64, K in slabs of 64 (128-byte
+// row segments, one cache line per row) with two LDS stages of 64 KB.  Slabs
+// go from global memory straight into LDS (buffer_load_dwordx4 ... lds: lane
+// l's 16 bytes land at base + 16 l), so the next slab streams in while the
+// current one is multiplied.
+constexpr int kBig = 256;
+constexpr int kBigK = 64;
+
+// LDS serves a 16-byte read for 16 lanes per cycle from 64 four-byte banks,
+// so one 256-byte bank row holds two 128-byte slab rows.  The 16-byte chunk
+// index is XOR-ed with (row / 2) mod 8: the 16 consecutive rows that one
+// operand read touches per cycle then cover all 16 (row mod 2, chunk) bank
+// groups.
+__device__ __forceinline__ int swz(int row, int chunk) { return row * 8 + (chunk ^ ((row >> 1) & 7)); }
+
+// Map a linear block index to an upper tile.  Blocks are dealt to the 8 XCDs
+// round-robin, so each XCD gets a contiguous range of the linear order; that
+// order walks the upper triangle in bands of kBand tile rows, column by
+// column, so the ~32 tiles resident on one XCD span about 4 row and 8 column
+// panels and share their K slabs through the XCD's L2.  Each band starts with
+// a triangle (column r0 + j holds j + 1 tiles, j < rows - 1) followed by full
+// columns of `rows` tiles.  Returns false for padding blocks.
+constexpr int kBand = 8;
+__device__ __forceinline__ bool big_tile(int b, int nb, int T, int& ti, int& tj) {
+  const int per = (nb + 7) / 8;
+  int lin = (b % 8) * per + b / 8;
+  if (lin >= nb) return false;
+  for (int r0 = 0; r0 < T; r0 += kBand) {
+    const int rows = min(kBand, T - r0);
+    const int tri = rows * (rows - 1) / 2;
+    const int size = tri + rows * (T - r0 - rows + 1);
+    if (lin < size) {
+      if (lin < tri) {
+        int j = 0;
+        while ((j + 1) * (j + 2) / 2 <= lin) ++j;
+        ti = r0 + lin - j * (j + 1) / 2;
+        tj = r0 + j;
+      } else {
+        const int q = lin - tri;
+        ti = r0 + q % rows;
+        tj = r0 + rows - 1 + q / rows;
+      }
+      return true;
+    }
+    lin -= size;
+  }
+  return false;
+}
+
+// Slab loader: instruction i of wave w (eight waves) fills LDS slots
+// (4 w + i) * 64 + lane of one operand (slot = row * 8 + physical chunk), i.e.
+// row 32 w + 8 i + lane / 8 at physical chunk lane % 8, holding logical chunk
+// (lane % 8) ^ (lane / 16) ^ (4 (i % 2)).  `voff_even` / `voff_odd` are the
+// lane's byte offsets for i = 0 / 1 at k = 0; rows past the feature matrix
+// read as zero (buffer range check).
+__device__ __forceinline__ void load_slab(uint4* dst, __amdgpu_buffer_rsrc_t rsrc, int voff_even, int voff_odd,
+                                          int row_step, int k0, int wave) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst + (wave * 4 + i) * 64, 16,
+                                             ((i & 1) ? voff_odd : voff_even) + (i >> 1) * row_step, k0 * 2, 0, 0);
+}
+
+// Operand fragments of one 16-wide K step: MT tiles of A and NT tiles of B
+// (32 rows each, 256 slots apart) from slot offsets `ia` / `ib` of the first.
+template <int MT, int NT>
+__device__ __forceinline__ void load_frags(bf16x8 (&a)[MT], bf16x8 (&b)[NT], const uint4* sa, const uint4* sb,
+                                           int ia, int ib) {
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const uint4 v = sa[ia + m * 256];
+    __builtin_memcpy(&a[m], &v, 16);
+  }
+#pragma unroll
+  for (int m = 0; m < NT; ++m) {
+    const uint4 v = sb[ib + m * 256];
+    __builtin_memcpy(&b[m], &v, 16);
+  }
+}
+
+template <int MT, int NT>
+__device__ __forceinline__ void mma_step(f32x16 (&acc)[MT][NT], const bf16x8 (&a)[MT], const bf16x8 (&b)[NT]) {
+#pragma unroll
+  for (int mi = 0; mi < MT; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < NT; ++ni)
+      acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
+}
+
+// Workgroup barrier for the slab pipeline.  Unlike __syncthreads() it does not
+// wait for all of this wave's loads: the caller has already waited for the
+// slab it is about to read, and the LDS reads of the previous slab have been
+// consumed by MFMAs.  The signal fences only keep the compiler from moving
+// memory operations across it.
+__device__ __forceinline__ void slab_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Issue order of K step 0 (8 MFMAs, the 6 fragment reads of step 1, all 8
+// loads of the next slab) and of steps 1-2 (8 MFMAs, the 6 reads of the next
+// step): memory instructions ride between MFMAs instead of arriving in bursts
+// that leave the matrix core idle, and the loads go out early in the slab so
+// they have most of it to land.
+__device__ __forceinline__ void interleave_first() {
+#pragma unroll
+  for (int i = 0; i < 6; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+  }
+}
+__device__ __forceinline__ void interleave_step() {
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 5, 0);
+}
+
+// One slab of the K loop in LDS stage ST: wait for this wave's loads of it,
+// barrier so every wave's part has landed and every wave is done with the
+// other stage, then run the four K steps, the reads of step kk + 1 issued
+// ahead of the MFMAs of step kk and the loads that refill the other stage
+// (NX) with slab LOAD (when LOAD >= 0) issued during step 0.  The steps carry
+// no branches, which keeps the compiler's per-object tracking of in-flight
+// LDS loads intact.
+#define CP_BIG_SLAB(ST, NX, LOAD)                                                        \
+  {                                                                                      \
+    __builtin_amdgcn_s_waitcnt(0xF70); /* vmcnt(0) */                                    \
+    slab_barrier();                                                                      \
+    load_frags(fa[0], fb[0], ST, ST + kBig * 8, offa[0], offb[0]);                       \
+    __builtin_amdgcn_sched_barrier(0);                                                   \
+    _Pragma("unroll") for (int kk = 0; kk < 4; ++kk) {                                   \
+      if (kk < 3) load_frags(fa[(kk + 1) & 1], fb[(kk + 1) & 1], ST, ST + kBig * 8,      \
+                             offa[kk + 1], offb[kk + 1]);                                \
+      if (kk == 0 && LOAD >= 0) {                                                        \
+        load_slab(NX, rsrc, voff_a0, voff_a1, row_step, (LOAD) * kBigK, wave);           \
+        load_slab(NX + kBig * 8, rsrc, voff_b0, voff_b1, row_step, (LOAD) * kBigK, wave); \
+      }                                                                                  \
+      mma_step(acc, fa[kk & 1], fb[kk & 1]);                                             \
+      if (kk == 0) interleave_first();                                                   \
+      else if (kk < 3) interleave_step();                                                \
+      __builtin_amdgcn_sched_barrier(0);                                                 \
+    }                                                                                    \
+  }
+
+// Eight waves in a 2 x 4 arrangement of 128 x 64 wave tiles (4 x 2 MFMA 32 x
+// 32 tiles, 128 accumulators per lane), two waves per SIMD: while one waits
+// on LDS or a barrier the other keeps the matrix core busy.  Loads into one
+// stage stay in flight while the other is read.  Requires d % (2 * kBigK) == 0.
+__global__ __launch_bounds__(512) void gram_bf16_big_kernel(const uint16_t* __restrict__ F, int n, int d,
+                                                            const float* __restrict__ inv_norm,
+                                                            float* __restrict__ out, unsigned int* mf_bits,
+                                                            int ntiles, int T) {
+  int ti, tj;
+  if (!big_tile(blockIdx.x, ntiles, T, ti, tj)) return;
+  const int row0 = ti * kBig, col0 = tj * kBig;
+  // One LDS object per stage (A rows, then B rows), so the compiler can tell
+  // which stage each in-flight load targets.
+  __shared__ uint4 st0[2 * kBig * 8], st1[2 * kBig * 8];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  // Raw buffer over the whole feature matrix (bytes); 0x00020000 selects
+  // plain 32-bit data for the descriptor's format field.
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(F), 0, n * d * 2, 0x00020000);
+  const int lrow = lane >> 3, lc_even = (lane & 7) ^ (lane >> 4), lc_odd = lc_even ^ 4;
+  const int ra = row0 + wave * 32 + lrow, rb = col0 + wave * 32 + lrow;
+  const int voff_a0 = (ra * d + lc_even * 8) * 2, voff_a1 = ((ra + 8) * d + lc_odd * 8) * 2;
+  const int voff_b0 = (rb * d + lc_even * 8) * 2, voff_b1 = ((rb + 8) * d + lc_odd * 8) * 2;
+  const int row_step = 32 * d;    // 16 rows, in bytes
+  // MFMA operand reads: lane l reads row l % 32 of each 32-row tile at logical
+  // chunk 2 kk + l / 32; every tile starts at a multiple of 32 rows, so the
+  // swizzle term depends on l only.
+  int offa[4], offb[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    offa[kk] = swz(wm * 128 + (lane & 31), kk * 2 + (lane >> 5));
+    offb[kk] = swz(wn * 64 + (lane & 31), kk * 2 + (lane >> 5));
+  }
+
+  bf16x8 fa[2][4], fb[2][2];
+  const int nslabs = d / kBigK;   // even, at least 2
+  load_slab(st0, rsrc, voff_a0, voff_a1, row_step, 0, wave);
+  load_slab(st0 + kBig * 8, rsrc, voff_b0, voff_b1, row_step, 0, wave);
+  int s = 0;
+  for (; s + 2 < nslabs; s += 2) {
+    CP_BIG_SLAB(st0, st1, s + 1)
+    CP_BIG_SLAB(st1, st0, s + 2)
+  }
+  CP_BIG_SLAB(st0, st1, s + 1)
+  CP_BIG_SLAB(st1, st0, -1)
+#undef CP_BIG_SLAB
+  store_df(acc, row0 + wm * 128, col0 + wn * 64, lane, n, inv_norm, out, mf_bits);
 }
 
 // ---------------------------------------------------------------------------
@@ -150,7 +400,7 @@ __global__ __launch_bounds__(256) void gram_f32_kernel(const float* __restrict__
   __shared__ __attribute__((aligned(16))) float As[kTile * kLdF];
   __shared__ __attribute__((aligned(16))) float Bs[kTile * kLdF];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   f32x16 acc[2][2];
 #pragma unroll
@@ -213,12 +463,20 @@ __global__ __launch_bounds__(256) void gram_f32_kernel(const float* __restrict__
   }
 #undef CP_GLOAD_ALL_F
 #undef CP_GLOAD_F
-  store_df(acc, row0, col0, wm, wn, lane, n, inv_norm, out, mf_bits);
+  store_df(acc, row0 + wm * 64, col0 + wn * 64, lane, n, inv_norm, out, mf_bits);
 }
 
 }  // namespace
 
 hipError_t launch_gram(const FstParams& p, const FstScratch& s, hipStream_t stream) {
+  if (p.bf16 && p.d % (2 * kBigK) == 0 && p.n >= 4096 && int64_t(p.n) * p.d < (int64_t(1) << 30)) {
+    const int t = (p.n + kBig - 1) / kBig;
+    const int tiles = t * (t + 1) / 2;
+    const int blocks = (tiles + 7) / 8 * 8;
+    gram_bf16_big_kernel<<<blocks, 512, 0, stream>>>(static_cast<const uint16_t*>(p.feats), p.n, p.d,
+                                                       s.inv_norm, p.cost, s.mf_bits, tiles, t);
+    return hipGetLastError();
+  }
   const int t = (p.n + kTile - 1) / kTile;
   const int blocks = t * (t + 1) / 2;
   if (p.bf16)

@@ -49,7 +49,8 @@ def test_workspace_queries(lib):
     a = lib.coverprune_sgs_workspace(1024, 102)
     b = lib.coverprune_sgs_workspace(16384, 1638)
     assert 0 < a < b
-    assert lib.coverprune_lite_workspace(32768, 3584, 3277, 1) >= 32768 * 64
+    # at least two radix key buffers, two token buffers and the packed voxel words
+    assert lib.coverprune_lite_workspace(32768, 3584, 3277, 1) >= 32768 * 40
 
 
 def _w(lf=1.0, lx=1.0, lt=1.0, kappa=10.0):

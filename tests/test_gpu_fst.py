@@ -26,7 +26,9 @@ def _run(scene, weights=(1.0, 1.0, 1.0), kappa=10.0):
 
 
 # (config, tokens or None for the whole scene, seed): several 128-tiles plus a
-# ragged tail, an odd count, and float32 and bfloat16 features.
+# ragged tail, an odd count, and float32 and bfloat16 features; from 4096
+# tokens up, bf16 problems take the 256 x 256 tile path (whole tiles, and a
+# ragged tail).
 CASES = [
     ("n1024_d256_f32", None, 0),
     ("n1024_d256_f32", None, 1),
@@ -35,6 +37,8 @@ CASES = [
     ("n4096_d1152", 997, 1),
     ("n8192_d3584", 700, 0),
     ("n16384_d3584", 520, 3),
+    ("n4096_d1152", None, 0),
+    ("n8192_d3584", 4357, 1),
 ]
 
 
