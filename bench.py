@@ -39,7 +39,68 @@ def _args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--lite-workload", default="lite_n32768_d3584",
                     help="also time CoverPrune-Lite alone on this workload ('' to skip)")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="only measure the achievable ceilings: a 1 GiB device-to-device copy (also the "
+                         "calibration kernel for the HBM byte counters) and a 16384 x 3584 x 16384 bf16 "
+                         "torch.matmul")
     return ap.parse_args()
+
+
+def ceilings():
+    """Plain copy and library GEMM on the same device, for the achievable
+    fractions of HBM and MFMA peak."""
+    import torch
+
+    dev = torch.device("cuda:0")
+    src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)   # 1 GiB
+    dst = torch.empty_like(src)
+    a = torch.randn(16384, 3584, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(3584, 16384, device=dev, dtype=torch.bfloat16)
+    out = {}
+    for name, fn, work in (("copy_1GiB", lambda: dst.copy_(src), 2.0 * src.numel() * 4),
+                           ("matmul_bf16_16384x3584x16384", lambda: a @ b, 2.0 * 16384 * 16384 * 3584)):
+        fn()
+        torch.cuda.synchronize()
+        e0 = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        e1 = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        for i in range(5):
+            e0[i].record()
+            fn()
+            e1[i].record()
+        torch.cuda.synchronize()
+        ms = min(x.elapsed_time(y) for x, y in zip(e0, e1))
+        if name.startswith("copy"):
+            out[name] = {"ms": round(ms, 4), "GB/s": round(work / ms / 1e6, 1),
+                         "frac_of_peak": round(work / ms / 1e6 / HBM_PEAK_GBS, 4)}
+        else:
+            out[name] = {"ms": round(ms, 4), "TFLOP/s": round(work / ms / 1e9, 1),
+                         "frac_of_peak": round(work / ms / 1e9 / BF16_PEAK_TFLOPS, 4)}
+    print(json.dumps({"ceilings": out, "device": torch.cuda.get_device_name(0)}), flush=True)
+
+
+def traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, calibrated against a
+    plain copy), or None when there is none or the kernel's source has changed
+    since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                key, val = line.split(":", 1)
+                rec[key.strip()] = val.strip()
+    src = os.path.join(ROOT, rec.get("source", ""))
+    if not os.path.isfile(src):
+        return None
+    with open(src, "rb") as fh:
+        if hashlib.sha256(fh.read()).hexdigest() != rec.get("source_sha256"):
+            return None
+    return float(rec["traffic_bytes_per_launch"])
 
 
 def _timed(fn, starts, ends, i):
@@ -137,6 +198,9 @@ def main():
         print("bench.py runs on exactly one GPU: the hot path is a single-GPU library "
               "(multi-GPU scaling is one scene per GPU with no communication).", file=sys.stderr)
         sys.exit(2)
+    if args.ceilings:
+        ceilings()
+        return
 
     import numpy as np
     import torch
@@ -203,7 +267,7 @@ def main():
     sgs_bytes = k * (4.0 * n * n + 12.0 * n)
     sgs_gbs = sgs_bytes / (s_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(sgs_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(sgs_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(sgs_gbs / HBM_PEAK_GBS, 4), "traffic": traffic("sgs_dense_kernel", cfg.name),
                 "kernel": "sgs_dense_kernel", "bytes_per_launch": sgs_bytes, "ms_per_launch": round(s_ms, 3)}
 
     # FST cost: symmetric Gram needs N (N + 1) D flops; the whole call (prep,
