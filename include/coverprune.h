@@ -62,8 +62,9 @@ typedef struct {
   float kappa;
 } cp_fst_weights;
 
-/* SGS flags. */
-#define CP_SGS_DENSE 0u /* every step re-evaluates every candidate's gain over the whole cost matrix */
+/* SGS flags (the same greedy either way; see coverprune_sgs_select). */
+#define CP_SGS_DENSE 0u       /* every step re-evaluates every candidate's gain over the whole cost matrix */
+#define CP_SGS_INCREMENTAL 1u /* gains computed once, then updated from the rows whose best cost drops */
 
 /* ------------------------------------------------------------------------ */
 /* FST transport cost (Sec. 3.3, Eq. 7-8).
@@ -108,7 +109,14 @@ cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int6
  *   k         1 <= k <= n
  *   c0        cost of leaving a target uncovered; lambda_f + lambda_x +
  *             lambda_tau (the largest value C can take) is the usual choice
- *   flags     CP_SGS_DENSE
+ *   flags     CP_SGS_DENSE: every step sums every candidate's gain over the
+ *             whole matrix (K full reads of the cost).
+ *             CP_SGS_INCREMENTAL: the gains are summed once at b = c0 and then
+ *             updated, step by step, from the rows of the targets whose best
+ *             cost the pick lowers (their old and new b); the terms are the
+ *             same float32 differences and float64 products, only the order
+ *             of the float64 additions differs, so picks can differ from the
+ *             dense sweep only between gains within rounding of each other.
  *   selected        [k] int32 output: tokens in the order they were chosen
  *   step_gain       [k] double output (may be NULL): gain of each step
  *   step_objective  [k] double output (may be NULL): L(S) after each step

@@ -25,6 +25,7 @@ DEFAULT_KAPPA = 10.0
 
 CP_F32, CP_BF16 = 0, 1
 CP_SGS_DENSE = 0
+CP_SGS_INCREMENTAL = 1
 
 
 class CoverPruneError(RuntimeError):
@@ -162,9 +163,11 @@ class SgsResult:
 
 def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[float] = None,
                weights=(1.0, 1.0, 1.0), workspace: Optional[torch.Tensor] = None,
-               stream=None) -> SgsResult:
+               stream=None, incremental: bool = False) -> SgsResult:
     """Greedy selection of k tokens over a target-major cost (Sec. 3.5, Eq. 11-16).
-    c0 defaults to the sum of the cost weights, the largest value C takes."""
+    c0 defaults to the sum of the cost weights, the largest value C takes.
+    incremental=True runs the same greedy with gains updated from the rows
+    whose best cost drops (CP_SGS_INCREMENTAL) instead of full sweeps."""
     lib = library()
     n = cost.shape[0]
     dev = cost.device
@@ -179,7 +182,8 @@ def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[
     need = lib.coverprune_sgs_workspace(n, int(k))
     if workspace is None:
         workspace = _workspace(need, dev)
-    _check(lib.coverprune_sgs_select(_ptr(cost), n, _ptr(capacity), int(k), float(c0), CP_SGS_DENSE,
+    flags = CP_SGS_INCREMENTAL if incremental else CP_SGS_DENSE
+    _check(lib.coverprune_sgs_select(_ptr(cost), n, _ptr(capacity), int(k), float(c0), flags,
                                      _ptr(sel), _ptr(gain), _ptr(obj), _ptr(assign), _ptr(workspace),
                                      workspace.numel(), _stream(stream)))
     return SgsResult(sel, gain, obj, assign)

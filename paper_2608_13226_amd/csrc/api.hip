@@ -2,6 +2,7 @@
 // workspace carving and kernel dispatch.  Nothing here touches device data.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -144,7 +145,7 @@ cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int6
 // ---------------------------------------------------------------------------
 size_t coverprune_sgs_workspace(int64_t n, int64_t k) {
   if (n < 1 || k < 1) return 0;
-  return cp::sgs_workspace_bytes(n, k);
+  return std::max(cp::sgs_workspace_bytes(n, k), cp::sgs_inc_workspace_bytes(n, k));
 }
 
 cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capacity, int64_t k,
@@ -154,7 +155,7 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
   if (n < 1 || n > kMaxDenseN) return fail(CP_ERR_INVALID_ARG, "n = %lld outside [1, %lld]", (long long)n, (long long)kMaxDenseN);
   if (k < 1 || k > n) return fail(CP_ERR_INVALID_ARG, "k = %lld outside [1, n = %lld]", (long long)k, (long long)n);
   if (!std::isfinite(c0)) return fail(CP_ERR_INVALID_ARG, "c0 must be finite");
-  if (flags != CP_SGS_DENSE) return fail(CP_ERR_UNSUPPORTED, "unknown flags 0x%x", flags);
+  if (flags != CP_SGS_DENSE && flags != CP_SGS_INCREMENTAL) return fail(CP_ERR_UNSUPPORTED, "unknown flags 0x%x", flags);
   if (!cost || !capacity || !selected) return fail(CP_ERR_INVALID_ARG, "cost, capacity and selected must be non-NULL");
   if (!aligned16(cost)) return fail(CP_ERR_INVALID_ARG, "cost is not 16-byte aligned");
   cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_workspace(n, k));
@@ -172,7 +173,8 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
   p.assign = assign;
   p.workspace = workspace;
   p.workspace_bytes = workspace_bytes;
-  hipError_t e = cp::launch_sgs_dense(p, static_cast<hipStream_t>(stream));
+  hipError_t e = flags == CP_SGS_INCREMENTAL ? cp::launch_sgs_incremental(p, static_cast<hipStream_t>(stream))
+                                             : cp::launch_sgs_dense(p, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "sgs");
   return ok();
 }

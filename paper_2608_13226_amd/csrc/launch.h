@@ -51,6 +51,8 @@ struct SgsParams {
 
 size_t sgs_workspace_bytes(int64_t n, int64_t k);
 hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream);
+size_t sgs_inc_workspace_bytes(int64_t n, int64_t k);
+hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream);
 
 // CoverPrune-Lite.
 struct LiteParams {

@@ -19,22 +19,27 @@ def _sub(cfg, n, seed):
     return parity.sample_scene(cfg, n, seed, salt=2000)
 
 
-def _gpu_select(C_tm_f32: np.ndarray, v: np.ndarray, k: int, c0: float):
+# Both forms of the greedy: full sweeps (dense) and running gains updated from
+# the targets whose best cost drops (incremental).
+MODES = [pytest.param(False, id="dense"), pytest.param(True, id="incremental")]
+
+
+def _gpu_select(C_tm_f32: np.ndarray, v: np.ndarray, k: int, c0: float, incremental=False):
     cost = torch.from_numpy(np.ascontiguousarray(C_tm_f32)).cuda()
     cap = torch.from_numpy(np.ascontiguousarray(v, dtype=np.float32)).cuda()
-    r = _cp().sgs_select(cost, cap, k, c0=c0)
+    r = _cp().sgs_select(cost, cap, k, c0=c0, incremental=incremental)
     torch.cuda.synchronize()
     return (r.selected.cpu().numpy(), r.gain.cpu().numpy(), r.objective.cpu().numpy(),
             r.assign.cpu().numpy())
 
 
-def _same_cost_case(s, k, c0=3.0, weights=(1.0, 1.0, 1.0), kappa=10.0):
+def _same_cost_case(s, k, c0=3.0, weights=(1.0, 1.0, 1.0), kappa=10.0, incremental=False):
     """The oracle's cost, rounded once to float32, drives both greedies."""
     C_ref, _ = parity.oracle_cost(s, weights, kappa)
     C32 = C_ref.astype(np.float32)                 # source-major, float32 values
     v = s.capacity
     ref = sgs.sgs_ref(C32.astype(np.float64), v.astype(np.float64), k, c0)
-    sel, gain, obj, assign = _gpu_select(np.ascontiguousarray(C32.T), v, k, c0)
+    sel, gain, obj, assign = _gpu_select(np.ascontiguousarray(C32.T), v, k, c0, incremental)
     ties, g_or, o_or = parity.replay_greedy(C32, v, c0, sel)
     assert np.allclose(gain, g_or, rtol=1e-6, atol=1e-12)
     assert np.allclose(obj, o_or, rtol=1e-9, atol=1e-12)
@@ -58,37 +63,41 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("incremental", MODES)
 @pytest.mark.parametrize("cfg,n,k,seed", CASES)
-def test_same_cost_parity(cfg, n, k, seed):
+def test_same_cost_parity(cfg, n, k, seed, incremental):
     s = _sub(cfg, n, seed)
-    print(f"sgs same-cost {cfg} n={s.n} k={k} seed={seed}", flush=True)
-    ties = _same_cost_case(s, k)
+    print(f"sgs same-cost {cfg} n={s.n} k={k} seed={seed} incremental={incremental}", flush=True)
+    ties = _same_cost_case(s, k, incremental=incremental)
     assert len(ties) <= 1, f"unexpected near-ties at steps {ties}"
 
 
-def test_single_token():
+@pytest.mark.parametrize("incremental", MODES)
+def test_single_token(incremental):
     s = _sub("n4096_d1152", 1, 0)
     s.capacity[:] = 1.0
-    print("sgs n=1", flush=True)
-    sel, gain, obj, assign = _gpu_select(np.zeros((1, 1), np.float32), s.capacity, 1, 3.0)
+    print(f"sgs n=1 incremental={incremental}", flush=True)
+    sel, gain, obj, assign = _gpu_select(np.zeros((1, 1), np.float32), s.capacity, 1, 3.0, incremental)
     assert sel.tolist() == [0] and assign.tolist() == [0]
     assert gain[0] == pytest.approx(3.0) and obj[0] == 0.0
 
 
-def test_exact_ties_go_to_smaller_index():
+@pytest.mark.parametrize("incremental", MODES)
+def test_exact_ties_go_to_smaller_index(incremental):
     # Duplicated tokens have identical gains at every step; the smaller index wins.
     s = _sub("n4096_d1152", 200, 5)
     idx = np.concatenate([np.arange(200), np.arange(0, 200, 7)])
     d = subscene(s, idx)
-    print("sgs exact ties", flush=True)
+    print(f"sgs exact ties incremental={incremental}", flush=True)
     C_ref, _ = parity.oracle_cost(d)
     C32 = C_ref.astype(np.float32)
     ref = sgs.sgs_ref(C32.astype(np.float64), d.capacity.astype(np.float64), 40, 3.0)
-    sel, _, _, _ = _gpu_select(np.ascontiguousarray(C32.T), d.capacity, 40, 3.0)
+    sel, _, _, _ = _gpu_select(np.ascontiguousarray(C32.T), d.capacity, 40, 3.0, incremental)
     assert np.array_equal(sel, ref["selected"])
 
 
-def test_zero_capacity_steps_still_select():
+@pytest.mark.parametrize("incremental", MODES)
+def test_zero_capacity_steps_still_select(incremental):
     # Only 3 targets carry capacity: after they are covered every gain is 0 and
     # the remaining picks go to the smallest unselected indices.
     s = _sub("n4096_d1152", 120, 6)
@@ -99,22 +108,23 @@ def test_zero_capacity_steps_still_select():
     C_ref, _ = parity.oracle_cost(s)
     C32 = C_ref.astype(np.float32)
     ref = sgs.sgs_ref(C32.astype(np.float64), v.astype(np.float64), 10, 3.0)
-    sel, gain, _, _ = _gpu_select(np.ascontiguousarray(C32.T), v, 10, 3.0)
+    sel, gain, _, _ = _gpu_select(np.ascontiguousarray(C32.T), v, 10, 3.0, incremental)
     assert np.array_equal(sel, ref["selected"])
     assert np.all(gain[3:] == 0.0)
 
 
-def test_end_to_end_parity():
+@pytest.mark.parametrize("incremental", MODES)
+def test_end_to_end_parity(incremental):
     # GPU cost and GPU greedy against the oracle's cost and greedy.  A pick may
     # differ from the oracle's only where two gains are closer than the cost
     # error can resolve.
     s = _sub("n4096_d1152", 1200, 7)
     k = 120
-    print(f"sgs end-to-end n={s.n} k={k}", flush=True)
+    print(f"sgs end-to-end n={s.n} k={k} incremental={incremental}", flush=True)
     t = to_device(s)
     cp = _cp()
     cost, _ = cp.fst_cost(t["feats"], t["pos"], t["frame"])
-    r = cp.sgs_select(cost, t["capacity"], k)
+    r = cp.sgs_select(cost, t["capacity"], k, incremental=incremental)
     torch.cuda.synchronize()
     sel = r.selected.cpu().numpy()
     C_ref, _ = parity.oracle_cost(s)
@@ -126,26 +136,28 @@ def test_end_to_end_parity():
     print(f"  {len(ties)} near-tie steps", flush=True)
 
 
-def test_deterministic():
+@pytest.mark.parametrize("incremental", MODES)
+def test_deterministic(incremental):
     s = _sub("n4096_d1152", 1000, 8)
     C_ref, _ = parity.oracle_cost(s)
     C_tm = np.ascontiguousarray(C_ref.T.astype(np.float32))
-    print("sgs determinism", flush=True)
-    a = _gpu_select(C_tm, s.capacity, 100, 3.0)
-    b = _gpu_select(C_tm, s.capacity, 100, 3.0)
+    print(f"sgs determinism incremental={incremental}", flush=True)
+    a = _gpu_select(C_tm, s.capacity, 100, 3.0, incremental)
+    b = _gpu_select(C_tm, s.capacity, 100, 3.0, incremental)
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
 
 
 @pytest.mark.slow
-def test_full_size_first_steps():
+@pytest.mark.parametrize("incremental", MODES)
+def test_full_size_first_steps(incremental):
     # 16384 tokens, the benchmark's launch shape, first 6 steps against the
     # oracle on the same float32 cost (narrow 16-d features keep the oracle fast).
     s = make_scene("n16384_d3584", 0, dim=16)
-    print(f"sgs full size n={s.n}", flush=True)
+    print(f"sgs full size n={s.n} incremental={incremental}", flush=True)
     C_tm, _ = parity.oracle_cost_f32_target_major(s)
     k = 6
-    sel, gain, obj, _ = _gpu_select(C_tm, s.capacity, k, 3.0)
+    sel, gain, obj, _ = _gpu_select(C_tm, s.capacity, k, 3.0, incremental)
     C32 = C_tm.T
     ties, g_or, o_or = parity.replay_greedy(C32, s.capacity, 3.0, sel)
     assert np.allclose(gain, g_or, rtol=1e-6)
@@ -154,14 +166,15 @@ def test_full_size_first_steps():
 
 
 @pytest.mark.slow
-def test_full_size_trajectory_invariants():
+@pytest.mark.parametrize("incremental", MODES)
+def test_full_size_trajectory_invariants(incremental):
     # The full 16384-token workload as the benchmark runs it (K = 1638).
     s = make_scene("n16384_d3584", 0)
-    print(f"sgs full workload n={s.n} k={s.k}", flush=True)
+    print(f"sgs full workload n={s.n} k={s.k} incremental={incremental}", flush=True)
     t = to_device(s)
     cp = _cp()
     cost, _ = cp.fst_cost(t["feats"], t["pos"], t["frame"])
-    r = cp.sgs_select(cost, t["capacity"], s.k)
+    r = cp.sgs_select(cost, t["capacity"], s.k, incremental=incremental)
     torch.cuda.synchronize()
     sel, gain, obj, assign = (r.selected.cpu().numpy(), r.gain.cpu().numpy(),
                               r.objective.cpu().numpy(), r.assign.cpu().numpy())
@@ -176,3 +189,27 @@ def test_full_size_trajectory_invariants():
         if best[a] < 3.0:
             assert assign[j] in set(sel.tolist())
             assert rows[a, list(sel).index(assign[j])] == best[a]
+
+
+@pytest.mark.slow
+def test_full_size_incremental_matches_dense():
+    # Both forms on the same full-size GPU cost: the trajectories agree until
+    # two gains fall within rounding of each other (the dense sweep sums in
+    # float64, the incremental form in exact fixed point).
+    s = make_scene("n16384_d3584", 0)
+    print(f"sgs dense vs incremental n={s.n} k={s.k}", flush=True)
+    t = to_device(s)
+    cp = _cp()
+    cost, _ = cp.fst_cost(t["feats"], t["pos"], t["frame"])
+    a = cp.sgs_select(cost, t["capacity"], s.k)
+    b = cp.sgs_select(cost, t["capacity"], s.k, incremental=True)
+    torch.cuda.synchronize()
+    sa, sb = a.selected.cpu().numpy(), b.selected.cpu().numpy()
+    ga, gb = a.gain.cpu().numpy(), b.gain.cpu().numpy()
+    diff = np.nonzero(sa != sb)[0]
+    first = int(diff[0]) if len(diff) else s.k
+    print(f"  trajectories agree on the first {first} of {s.k} steps", flush=True)
+    assert np.allclose(ga[:first], gb[:first], rtol=1e-9, atol=0.0)
+    if first < s.k:
+        assert abs(ga[first] - gb[first]) <= 1e-9 * ga[first]
+    assert np.allclose(a.objective.cpu().numpy()[-1], b.objective.cpu().numpy()[-1], rtol=1e-6)
