@@ -20,19 +20,29 @@
 // and the columns [b W, (b + 1) W): the best costs b_j and capacities of its
 // rows and the running gains of its columns stay in LDS for the whole launch.
 // Per step:
-//   1. every block reads the step's winner, and tests its own rows against
-//      the winner's column; the rows that improve are written, compacted, to
-//      the block's slice of the change list (row, v, old b, new b);
-//   2. grid barrier;
-//   3. every block walks the whole change list (all slices, in block order)
-//      and applies the changes to its columns' gains, reading each changed
-//      row's segment over its columns (one coalesced 256-byte read per row and
-//      64 columns); block 0 also folds the drop of the objective;
-//   4. every block takes the exact argmax of its unchosen columns and folds it
-//      into the next step's packed (gain, index) maximum; grid barrier.
-// Cross-block data (change lists, counts, the packed maxima, the barrier
-// counter) goes through device-scope atomic operations, coherent across the
-// chip's L2 caches without fences.
+//   1. every block reads all blocks' candidates for the step (each block's
+//      best unchosen column, published at the end of the previous step) and
+//      takes the same winner;
+//   2. it tests its own rows against the winner's column and writes the rows
+//      that improve, compacted, to its slice of the change list (row, v,
+//      old b, new b), then publishes the slice's length;
+//   3. it reads every block's length, walks the whole change list (slices
+//      in block order) and applies the changes to its columns' gains,
+//      reading each changed row's segment over its columns (one coalesced
+//      256-byte read per row and 64 columns); block 0 also applies them to the
+//      objective, kept in the same fixed point;
+//   4. it publishes the exact argmax of its unchosen columns.
+// The exchanges are per-block slots rather than counters: a slot holds the
+// value together with the step it belongs to, every block reads all slots in
+// parallel (one thread per slot), and no address takes more than one writer,
+// so a step costs two round trips through memory instead of two grid
+// barriers of serialized atomic increments.  Slots, lists and lengths are
+// written and read with device-scope atomic operations, coherent across the
+// chip's L2 caches without fences; a block's list writes are complete at the
+// workgroup barrier before its thread 0 publishes the length.  A slot is only
+// rewritten after every block has read it: a block can publish step l + 1's
+// values only after reading every block's step-l + 1 candidate, which each
+// block publishes only after it has consumed step l.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -47,10 +57,16 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / 64;
 constexpr int kMaxBlocks = 256;    // at most one block per compute unit
-constexpr int kBatch = 32;         // change-list entries a wave has in flight
+constexpr int kBatch = 64;         // change-list entries a wave has in flight
 constexpr int kInitRows = 16;      // rows a wave has in flight in the full pass
-constexpr int kIndexBits = 20;     // packed key: [44-bit gain | 20-bit inverted index]
+constexpr int kIndexBits = 20;     // candidate: [epoch | 43-bit gain | 20-bit inverted index]
 constexpr unsigned long long kIndexMask = (1ull << kIndexBits) - 1ull;
+constexpr unsigned long long kEpoch = 1ull << 63;
+constexpr unsigned long long kNoCandidate = 1ull;   // below every real candidate
+// Every wait in the kernel is bounded: about a second of polling (far beyond
+// any legitimate wait) raises the abort flag, after which every block leaves
+// its waits and returns, and selected[] is filled with -1.
+constexpr unsigned int kSpinLimit = 1u << 22;
 
 // Fixed-point value of a nonnegative term: floor(t 2^S) in 128 bits (t 2^S <
 // 2^102, so the high part stays below 2^38).
@@ -76,14 +92,14 @@ struct IncDev {
   double* step_obj;
   int32_t* assign;
   unsigned long long* list;   // [blocks][W][2]: (row | v << 32), (old b | new b << 32)
-  unsigned int* count;        // [blocks] entries in each slice
-  unsigned long long* key;    // [k] packed step maxima
-  unsigned int* bar;          // grid barrier counter
+  unsigned long long* lens;   // [blocks] (step + 1) << 32 | slice length
+  unsigned long long* cand;   // [2][blocks] packed candidate | epoch << 63
+  unsigned int* abort;        // set when a wait exceeds kSpinLimit polls
   int W;                      // rows and columns per block
 };
 
 struct Layout {
-  size_t list, count, key, ctrl, total;
+  size_t list, lens, cand, ctrl, total;
 };
 
 size_t a256(size_t x) { return (x + 255) / 256 * 256; }
@@ -94,42 +110,79 @@ int blocks_for(int64_t n, int cus) {
 
 // Sized for the largest grid (kMaxBlocks blocks of W = ceil(n / blocks) rows).
 Layout layout(int64_t n, int64_t k) {
+  (void)k;
   Layout L;
   size_t o = 0;
-  L.list = o;  o += a256(size_t(n + kMaxBlocks) * 16);
-  L.count = o; o += a256(size_t(kMaxBlocks) * 4);
-  L.key = o;   o += a256(size_t(k) * 8);
-  L.ctrl = o;  o += 256;
+  L.list = o; o += a256(size_t(n + kMaxBlocks) * 16);
+  L.lens = o; o += a256(size_t(kMaxBlocks) * 8);
+  L.cand = o; o += a256(size_t(2 * kMaxBlocks) * 8);
+  L.ctrl = o; o += 256;
   L.total = o;
   return L;
 }
 
+// Nonnegative gain truncated to its top 43 bits (relative resolution 2^-31),
+// then the inverted index: larger gain first, then smaller index.  Indices
+// are below 2^18, so every real candidate exceeds kNoCandidate.
 __device__ __forceinline__ unsigned long long pack_key(double g, int idx) {
-  const unsigned long long gb = (unsigned long long)__double_as_longlong(g) >> kIndexBits;
+  const unsigned long long gb = (unsigned long long)__double_as_longlong(g) >> (kIndexBits + 1);
   return (gb << kIndexBits) | (kIndexMask - (unsigned long long)idx);
 }
 
-__global__ void sgs_inc_init_kernel(IncDev a, int blocks) {
-  const int gt = blockIdx.x * blockDim.x + threadIdx.x, nt = gridDim.x * blockDim.x;
-  for (int s = gt; s < a.k; s += nt) a.key[s] = 0ull;
-  for (int s = gt; s < blocks; s += nt) a.count[s] = 0u;
-  for (int j = gt; j < a.n; j += nt)
-    if (a.assign) a.assign[j] = -1;
-  if (gt == 0) *a.bar = 0u;
+// Epoch bit of the candidates for step l, kept in slot set l % 2: it flips
+// between consecutive uses of a set and is never the zero of a fresh
+// workspace for steps 0 and 1.
+__device__ __forceinline__ unsigned long long epoch_of(int step) {
+  return ((step >> 1) & 1) ? 0ull : kEpoch;
 }
 
-// Fixed-order block sum, result in every thread.
-__device__ double block_sum_all(double x, double* sd) {
-  x = wave_sum(x);
+__global__ void sgs_inc_init_kernel(IncDev a) {
+  const int gt = blockIdx.x * blockDim.x + threadIdx.x, nt = gridDim.x * blockDim.x;
+  for (int s = gt; s < kMaxBlocks; s += nt) {
+    a.lens[s] = 0ull;
+    a.cand[s] = 0ull;
+    a.cand[kMaxBlocks + s] = 0ull;
+  }
+  for (int j = gt; j < a.n; j += nt)
+    if (a.assign) a.assign[j] = -1;
+  if (gt == 0) *a.abort = 0u;
+}
+
+// Sum over the block of 128-bit integers, result in every thread.
+__device__ __int128 block_sum_i128(__int128 x, __int128* sg) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const unsigned long long lo = __shfl_xor((unsigned long long)x, o);
+    const long long hi = __shfl_xor((long long)(x >> 64), o);
+    x += ((__int128)hi << 64) | (__int128)lo;
+  }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   __syncthreads();
-  if (lane == 0) sd[w] = x;
+  if (lane == 0) sg[w] = x;
   __syncthreads();
-  double s = 0.0;
+  __int128 s = 0;
 #pragma unroll
-  for (int q = 0; q < kWaves; ++q) s += sd[q];
+  for (int q = 0; q < kWaves; ++q) s += sg[q];
   __syncthreads();
   return s;
+}
+
+// Poll *p until pred(value) holds; false if the launch is aborting (this
+// wait timed out, or another one did).
+template <class Pred>
+__device__ bool wait_slot(const unsigned long long* p, unsigned int* abort, Pred pred, unsigned long long& x) {
+  for (unsigned int spins = 0;; ++spins) {
+    x = get(p);
+    if (pred(x)) return true;
+    if ((spins & 63u) == 63u) {
+      if (get(abort)) return false;
+      if (spins > kSpinLimit) {
+        put(abort, 1u);
+        return false;
+      }
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
 }
 
 // Inclusive prefix sum over the block (thread order), result in every thread.
@@ -149,11 +202,26 @@ __device__ int block_inclusive_scan(int x, int* swt) {
   return x;
 }
 
+// Fixed-order block sum, result in every thread.
+__device__ double block_sum_all(double x, double* sd) {
+  x = wave_sum(x);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sd[w] = x;
+  __syncthreads();
+  double s = 0.0;
+#pragma unroll
+  for (int q = 0; q < kWaves; ++q) s += sd[q];
+  __syncthreads();
+  return s;
+}
+
 // Exact argmax (ties to the smaller index) of the block's unchosen columns,
-// folded into *key; the cross-block key compares the gains as doubles
-// truncated to 44 bits.
+// published as the block's candidate for the step; across blocks the gains
+// compare as doubles truncated to 43 bits.
 __device__ void publish_argmax(const unsigned long long* sGlo, const long long* sGhi, const unsigned char* ssel,
-                               int lo, int cnt, int S, unsigned long long* key, __int128* sg, int* si) {
+                               int lo, int cnt, int S, unsigned long long* slot, unsigned long long epoch,
+                               __int128* sg, int* si) {
   __int128 g = -1;
   int gi = INT_MAX;
   for (int i = threadIdx.x; i < cnt; i += kBlock)
@@ -187,30 +255,62 @@ __device__ void publish_argmax(const unsigned long long* sGlo, const long long* 
         g = sg[q];
         gi = si[q];
       }
-    if (gi != INT_MAX)
-      __hip_atomic_fetch_max(key, pack_key(fx_to_double(g, S), gi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    put(slot, (gi != INT_MAX ? pack_key(fx_to_double(g, S), gi) : kNoCandidate) | epoch);
   }
   __syncthreads();
+}
+
+// The step's winner: thread i < nb waits for block i's candidate of this
+// epoch; the largest wins (the same in every block).  Returns -1 when the
+// launch is aborting.
+__device__ int read_winner(const unsigned long long* slots, unsigned long long epoch, int nb,
+                           unsigned int* abort, unsigned long long* su, int* sflag) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  unsigned long long best = 0ull;
+  if (tid == 0) *sflag = 0;
+  __syncthreads();
+  if (tid < nb) {
+    unsigned long long x;
+    if (wait_slot(slots + tid, abort, [epoch](unsigned long long v) { return (v & kEpoch) == epoch; }, x))
+      best = x & ~kEpoch;
+    else
+      *sflag = 1;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const unsigned long long y = __shfl_xor(best, o);
+    best = y > best ? y : best;
+  }
+  if (lane == 0) su[w] = best;
+  __syncthreads();
+  unsigned long long m = su[0];
+#pragma unroll
+  for (int q = 1; q < kWaves; ++q) m = su[q] > m ? su[q] : m;
+  const bool aborting = *sflag != 0;
+  __syncthreads();
+  return aborting ? -1 : int(kIndexMask - (m & kIndexMask));
 }
 
 __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
   extern __shared__ unsigned long long smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int nb = gridDim.x, blk = blockIdx.x;
+  const int blk = blockIdx.x;
   const int lo = blk * a.W;
   const int cnt = max(0, min(a.n, lo + a.W) - lo);
   unsigned long long* sGlo = smem;                                 // [W] running gains, low words
   long long* sGhi = reinterpret_cast<long long*>(sGlo + a.W);      // [W] high words
   float* sb = reinterpret_cast<float*>(sGhi + a.W);                // [W] best costs of own rows
   float* sv = sb + a.W;                                            // [W] capacities of own rows
-  int* spre = reinterpret_cast<int*>(sv + a.W);                    // [nb + 1] list offsets
-  unsigned char* ssel = reinterpret_cast<unsigned char*>(spre + nb + 1);   // [W] chosen columns
+  unsigned char* ssel = reinterpret_cast<unsigned char*>(sv + a.W);       // [W] chosen columns
   __shared__ __int128 red[kBlock];
   __shared__ __int128 sg[kWaves];
   __shared__ double sd[kWaves];
   __shared__ int si[kWaves];
   __shared__ int swt[kWaves];
-  __shared__ int s_t;
+  __shared__ unsigned long long su[kWaves];
+  const int nb = gridDim.x;
+  __shared__ int spre[kMaxBlocks + 1];        // slice offsets
+  __shared__ int sflag;
 
   for (int i = tid; i < cnt; i += kBlock) {
     sb[i] = a.c0;
@@ -266,22 +366,23 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
     __syncthreads();
   }
 
-  // Block 0 keeps the objective L = sum_j v_j b_j, starting from c0 sum v.
-  double L = double(a.c0) * vsum;
+  // Block 0 keeps the objective L = sum_j v_j b_j in the gains' fixed point,
+  // starting from b = c0.
+  __int128 L = 0;
+  if (blk == 0) {
+    __int128 x = 0;
+    for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
+    L = block_sum_i128(x, sg);
+  }
 
-  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.key, sg, si);
-  unsigned int round = 0;
-  grid_barrier(a.bar, ++round);
+  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + blk, epoch_of(0), sg, si);
 
   for (int step = 0; step < a.k; ++step) {
-    if (tid == 0) {
-      const unsigned long long kk = __hip_atomic_load(a.key + step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      // Some block always publishes while unchosen columns remain; the clamp
-      // only keeps a broken key from addressing past the matrix.
-      s_t = min(int(kIndexMask - (kk & kIndexMask)), a.n - 1);
-    }
-    __syncthreads();
-    const int t = s_t;
+    // Some block has a candidate while unchosen columns remain; the clamp
+    // only keeps a broken slot from addressing past the matrix.
+    const int tw = read_winner(a.cand + (step & 1) * kMaxBlocks, epoch_of(step), nb, a.abort, su, &sflag);
+    if (tw < 0) break;
+    const int t = min(tw, a.n - 1);
     if (t >= lo && t < lo + cnt && tid == 0) {
       ssel[t - lo] = 1;
       a.selected[step] = t;
@@ -322,34 +423,49 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
       base += tot;
       __syncthreads();
     }
-    if (tid == 0) put(a.count + blk, unsigned(base));
-    grid_barrier(a.bar, ++round);
+    // The barrier above completed this block's list writes.
+    if (tid == 0) put(a.lens + blk, ((unsigned long long)(step + 1) << 32) | unsigned(base));
 
     // The last step's changes only feed the objective, kept by block 0.
     if (step + 1 == a.k && blk != 0) break;
 
-    // 2. Offsets of every block's slice in the flattened change list.
+    // 2. Every block's slice length (thread i waits for block i), and the
+    // slices' offsets in the flattened change list.
     {
-      const int c = tid < nb ? int(get(a.count + tid)) : 0;
+      if (tid == 0) sflag = 0;
+      __syncthreads();
+      int c = 0;
+      if (tid < nb) {
+        unsigned long long x;
+        const unsigned int round = unsigned(step + 1);
+        if (wait_slot(a.lens + tid, a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
+          c = int(x & 0xffffffffull);
+        else
+          sflag = 1;
+      }
       const int incl = block_inclusive_scan(c, swt);
       if (tid < nb) spre[tid + 1] = incl;
       if (tid == 0) spre[0] = 0;
       __syncthreads();
     }
+    if (sflag) break;
     const int total = spre[nb];
 
-    // 3. Apply the changes to the own columns' gains.  Lanes < kBatch locate
-    // and fetch one entry each; the entries are then broadcast and every lane
-    // reads its column of the entry's row.
-    double dobj = 0.0;
+    // 3. Apply the changes to the own columns' gains.  Each lane of a round
+    // locates and fetches one entry; the entries are then broadcast and every
+    // lane reads its column of each entry's row.
+    __int128 dobj = 0;
     for (int cc = 0; cc < cnt; cc += 64) {
       const bool colok = cc + lane < cnt;
       const int col = lo + cc + lane;
       __int128 g = 0;
-      for (int e0 = w * kBatch; e0 < total; e0 += kWaves * kBatch) {
+      // Rounds of up to kBatch entries per wave, the list split evenly over
+      // the waves.
+      const int per = min(kBatch, (total + kWaves - 1) / kWaves);
+      for (int e0 = w * per; e0 < total; e0 += kWaves * per) {
         const int e = e0 + lane;
         unsigned long long h0 = 0ull, h1 = 0ull;
-        if (lane < kBatch && e < total) {
+        if (lane < per && e < total) {
           int s0 = 0, s1 = nb;   // spre[s0] <= e < spre[s1]
           while (s1 - s0 > 1) {
             const int mid = (s0 + s1) >> 1;
@@ -360,27 +476,34 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
           h0 = get(src);
           h1 = get(src + 1);
         }
-        const int m = min(kBatch, total - e0);
+        const int m = min(per, total - e0);
         float x[kBatch];
+        // Entry u is broadcast from lane u with readlane (u is uniform).
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-          const int j = int(__shfl(unsigned(h0 & 0xffffffffull), u));
-          x[u] = (u < m && colok) ? a.C[size_t(j) * a.n + col] : 0.f;
+          if (u < m) {
+            const int j = __builtin_amdgcn_readlane(int(h0 & 0xffffffffull), u);
+            x[u] = colok ? a.C[size_t(j) * a.n + col] : 0.f;
+          }
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
           if (u < m) {
-            const double vj = double(__uint_as_float(__shfl(unsigned(h0 >> 32), u)));
-            const float bo = __uint_as_float(__shfl(unsigned(h1 & 0xffffffffull), u));
-            const float bn = __uint_as_float(__shfl(unsigned(h1 >> 32), u));
-            g += fx(vj * double(fmaxf(bn - x[u], 0.f)), S) - fx(vj * double(fmaxf(bo - x[u], 0.f)), S);
+            // A column that cost at least the old best contributes 0 before
+            // and after (new best < old best).
+            const float bo = __uint_as_float(__builtin_amdgcn_readlane(unsigned(h1 & 0xffffffffull), u));
+            if (x[u] < bo) {
+              const float bn = __uint_as_float(__builtin_amdgcn_readlane(unsigned(h1 >> 32), u));
+              const double vj = double(__uint_as_float(__builtin_amdgcn_readlane(unsigned(h0 >> 32), u)));
+              g += fx(vj * double(fmaxf(bn - x[u], 0.f)), S) - fx(vj * double(bo - x[u]), S);
+            }
           }
         }
-        if (blk == 0 && cc == 0 && lane < kBatch && e < total) {
-          const float vj = __uint_as_float(unsigned(h0 >> 32));
+        if (blk == 0 && cc == 0 && lane < per && e < total) {
+          const double vj = double(__uint_as_float(unsigned(h0 >> 32)));
           const float bo = __uint_as_float(unsigned(h1 & 0xffffffffull));
           const float bn = __uint_as_float(unsigned(h1 >> 32));
-          dobj = fma(double(vj), double(bo) - double(bn), dobj);
+          dobj += fx(vj * double(bn), S) - fx(vj * double(bo), S);
         }
       }
       red[tid] = g;
@@ -395,16 +518,17 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
       __syncthreads();
     }
     if (blk == 0) {
-      L -= block_sum_all(dobj, sd);
-      if (tid == 0 && a.step_obj) a.step_obj[step] = L;
+      L += block_sum_i128(dobj, sg);
+      if (tid == 0 && a.step_obj) a.step_obj[step] = fx_to_double(L, S);
     }
 
-    // 4. Next step's winner.
-    if (step + 1 < a.k) {
-      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.key + step + 1, sg, si);
-      grid_barrier(a.bar, ++round);
-    }
+    // 4. This block's candidate for the next step.
+    if (step + 1 < a.k)
+      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + ((step + 1) & 1) * kMaxBlocks + blk,
+                     epoch_of(step + 1), sg, si);
   }
+  if (blk == 0 && get(a.abort))
+    for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
 }
 
 }  // namespace
@@ -418,7 +542,7 @@ hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream) {
   if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
   const int nb = blocks_for(p.n, cus);
   const int W = (p.n + nb - 1) / nb;
-  const size_t lds = size_t(W) * (16 + 4 + 4 + 1) + size_t(nb + 1) * 4 + 16;
+  const size_t lds = size_t(W) * (16 + 4 + 4 + 1) + 16;
   int per_cu = 0;
   if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(sgs_inc_kernel),
                                                         kBlock, lds)) != hipSuccess)
@@ -438,12 +562,12 @@ hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream) {
   a.step_obj = p.step_objective;
   a.assign = p.assign;
   a.list = reinterpret_cast<unsigned long long*>(w + L.list);
-  a.count = reinterpret_cast<unsigned int*>(w + L.count);
-  a.key = reinterpret_cast<unsigned long long*>(w + L.key);
-  a.bar = reinterpret_cast<unsigned int*>(w + L.ctrl);
+  a.lens = reinterpret_cast<unsigned long long*>(w + L.lens);
+  a.cand = reinterpret_cast<unsigned long long*>(w + L.cand);
+  a.abort = reinterpret_cast<unsigned int*>(w + L.ctrl);
   a.W = W;
 
-  sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a, nb);
+  sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   void* args[] = {&a};
   return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_inc_kernel), dim3(nb), dim3(kBlock), args,
