@@ -16,7 +16,7 @@
 // dropped to zero is exactly zero), the result does not depend on the grid,
 // and equal gains go to the smaller index.
 //
-// One cooperative launch, one block per compute unit.  Block b owns the rows
+// One cooperative launch, one block of eight waves per compute unit.  Block b owns the rows
 // and the columns [b W, (b + 1) W): the best costs b_j and capacities of its
 // rows and the running gains of its columns stay in LDS for the whole launch.
 // Per step:
@@ -54,10 +54,11 @@
 namespace cp {
 namespace {
 
-constexpr int kBlock = 256;
+constexpr int kBlock = 512;
 constexpr int kWaves = kBlock / 64;
 constexpr int kMaxBlocks = 256;    // at most one block per compute unit
-constexpr int kBatch = 64;         // change-list entries a wave has in flight
+constexpr int kBatch = 64;         // change-list entries a wave fetches per round
+constexpr int kChunk = 16;         // of which the rows read together
 constexpr int kInitRows = 16;      // rows a wave has in flight in the full pass
 constexpr int kIndexBits = 20;     // candidate: [epoch | 43-bit gain | 20-bit inverted index]
 constexpr unsigned long long kIndexMask = (1ull << kIndexBits) - 1ull;
@@ -68,13 +69,18 @@ constexpr unsigned long long kNoCandidate = 1ull;   // below every real candidat
 // its waits and returns, and selected[] is filled with -1.
 constexpr unsigned int kSpinLimit = 1u << 22;
 
-// Fixed-point value of a nonnegative term: floor(t 2^S) in 128 bits (t 2^S <
-// 2^102, so the high part stays below 2^38).
+// Fixed-point value of a nonnegative term: floor(t 2^S) in 128 bits, read
+// off the bits of the double t 2^S (exact: a power-of-two scaling) with one
+// 64-bit shift; t 2^S < 2^102.  Negative, zero and subnormal-range values
+// give 0.
 __device__ __forceinline__ __int128 fx(double t, int S) {
-  const double y = __builtin_ldexp(fmax(t, 0.0), S);
-  const double hi = __builtin_floor(y * 0x1p-64);
-  const double lo = __builtin_fma(-hi, 0x1p64, y);
-  return ((__int128)(unsigned long long)hi << 64) + (__int128)(unsigned long long)lo;
+  const unsigned long long b = (unsigned long long)__double_as_longlong(__builtin_ldexp(t, S));
+  const int E = int(b >> 52) & 0x7ff;
+  if ((b >> 63) || E < 1023) return 0;                       // negative, or below 1
+  const unsigned long long m = (b & ((1ull << 52) - 1ull)) | (1ull << 52);
+  const int sh = E - 1075;                                    // value = m 2^sh, sh <= 49
+  if (sh <= 0) return (__int128)(m >> -sh);
+  return ((__int128)(m >> (64 - sh)) << 64) | (__int128)(m << sh);
 }
 
 __device__ __forceinline__ double fx_to_double(__int128 g, int S) {
@@ -335,24 +341,21 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
   }
 
   // Step-0 gains of the own columns: every row at b = c0.  Wave w takes the
-  // 16-row chunks w, w + 4, ...; the waves' sums are added in wave order.
+  // 16-row chunks w, w + kWaves, ...; the waves' sums are added in wave order.
   for (int cc = 0; cc < cnt; cc += 64) {
     const bool colok = cc + lane < cnt;
     const int col = lo + cc + lane;
     __int128 g = 0;
     for (int j0 = w * kInitRows; j0 < a.n; j0 += kWaves * kInitRows) {
-      float x[kInitRows];
+      float x[kInitRows], vj[kInitRows];
 #pragma unroll
       for (int u = 0; u < kInitRows; ++u) {
         const int j = j0 + u;
         x[u] = (colok && j < a.n) ? __builtin_nontemporal_load(a.C + size_t(j) * a.n + col) : a.c0;
+        vj[u] = j < a.n ? a.v[j] : 0.f;
       }
 #pragma unroll
-      for (int u = 0; u < kInitRows; ++u) {
-        const int j = j0 + u;
-        const float vj = j < a.n ? a.v[j] : 0.f;
-        g += fx(double(vj) * double(fmaxf(a.c0 - x[u], 0.f)), S);
-      }
+      for (int u = 0; u < kInitRows; ++u) g += fx(double(vj[u]) * double(fmaxf(a.c0 - x[u], 0.f)), S);
     }
     red[tid] = g;
     __syncthreads();
@@ -477,25 +480,31 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
           h1 = get(src + 1);
         }
         const int m = min(per, total - e0);
-        float x[kBatch];
-        // Entry u is broadcast from lane u with readlane (u is uniform).
+        // Entry u is broadcast from lane u with readlane (u is uniform), in
+        // chunks of kChunk whose row reads are in flight together.
+        const int hj = int(h0 & 0xffffffffull), hv = int(h0 >> 32);
+        const int hbo = int(h1 & 0xffffffffull), hbn = int(h1 >> 32);
+        for (int u0 = 0; u0 < m; u0 += kChunk) {
+          float x[kChunk];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-          if (u < m) {
-            const int j = __builtin_amdgcn_readlane(int(h0 & 0xffffffffull), u);
-            x[u] = colok ? a.C[size_t(j) * a.n + col] : 0.f;
+          for (int i = 0; i < kChunk; ++i) {
+            x[i] = 0.f;
+            if (u0 + i < m && colok) {
+              const int j = __builtin_amdgcn_readlane(hj, u0 + i);
+              x[i] = a.C[size_t(j) * a.n + col];
+            }
           }
-        }
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-          if (u < m) {
-            // A column that cost at least the old best contributes 0 before
-            // and after (new best < old best).
-            const float bo = __uint_as_float(__builtin_amdgcn_readlane(unsigned(h1 & 0xffffffffull), u));
-            if (x[u] < bo) {
-              const float bn = __uint_as_float(__builtin_amdgcn_readlane(unsigned(h1 >> 32), u));
-              const double vj = double(__uint_as_float(__builtin_amdgcn_readlane(unsigned(h0 >> 32), u)));
-              g += fx(vj * double(fmaxf(bn - x[u], 0.f)), S) - fx(vj * double(bo - x[u]), S);
+          for (int i = 0; i < kChunk; ++i) {
+            if (u0 + i < m) {
+              // A column that cost at least the old best contributes 0 before
+              // and after (new best < old best).
+              const float bo = __int_as_float(__builtin_amdgcn_readlane(hbo, u0 + i));
+              if (x[i] < bo) {
+                const float bn = __int_as_float(__builtin_amdgcn_readlane(hbn, u0 + i));
+                const double vj = double(__int_as_float(__builtin_amdgcn_readlane(hv, u0 + i)));
+                g += fx(vj * double(fmaxf(bn - x[i], 0.f)), S) - fx(vj * double(bo - x[i]), S);
+              }
             }
           }
         }
