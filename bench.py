@@ -3,12 +3,14 @@
 
 One step = one pass of the whole hot path over one synthetic scene resident
 in HBM: the FST cost (coverprune_fst_cost), the greedy selection of K tokens
-(coverprune_sgs_select) and CoverPrune-Lite (coverprune_lite_select).  The
-default workload is the 16384-token, 3584-wide bfloat16 scene whose 1 GiB
-float32 cost matrix stays in HBM (K = 1638, Lite voxels of 0.25 m).
+(coverprune_sgs_select, incremental form by default) and CoverPrune-Lite
+(coverprune_lite_select).  The default workload is the 16384-token,
+3584-wide bfloat16 scene whose 1 GiB float32 cost matrix stays in HBM
+(K = 1638, Lite voxels of 0.25 m).
 
 Prints one JSON line: prune latency in ms per scene, the dominant kernel's
-roofline fraction, and the CPU oracle timed on the host for comparison.
+roofline fraction, the dense greedy sweep's HBM fraction, and the CPU oracle
+timed on the host for comparison.
 """
 from __future__ import annotations
 
@@ -39,6 +41,8 @@ def _args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--lite-workload", default="lite_n32768_d3584",
                     help="also time CoverPrune-Lite alone on this workload ('' to skip)")
+    ap.add_argument("--sgs", choices=("incremental", "dense"), default="incremental",
+                    help="form of the greedy inside the timed step (both give the same picks)")
     ap.add_argument("--ceilings", action="store_true",
                     help="only measure the achievable ceilings: a 1 GiB device-to-device copy (also the "
                          "calibration kernel for the HBM byte counters) and a 16384 x 3584 x 16384 bf16 "
@@ -227,7 +231,8 @@ def main():
 
     def step(i=None, ev=None):
         run_f = lambda: cp.fst_cost(t["feats"], t["pos"], t["frame"], out=cost, maxima=maxima, workspace=ws_f)
-        run_s = lambda: cp.sgs_select(cost, t["capacity"], k, workspace=ws_s)
+        run_s = lambda: cp.sgs_select(cost, t["capacity"], k, workspace=ws_s,
+                                      incremental=args.sgs == "incremental")
         run_l = lambda: cp.lite_select(t["feats"], t["pos"], t["frame"], t["capacity"], k,
                                        voxel_size=lite_h, workspace=ws_l)
         if ev is None:
@@ -261,14 +266,57 @@ def main():
     sel = r.selected.cpu().numpy()
     assert len(set(sel.tolist())) == k, "greedy returned repeated tokens"
 
-    # Dominant kernel: the greedy, one cooperative launch per call.  Algorithmic
-    # bytes per step: the N x N float32 cost read once, plus the per-target
-    # vectors (capacity and best cost read, best cost written).
-    sgs_bytes = k * (4.0 * n * n + 12.0 * n)
-    sgs_gbs = sgs_bytes / (s_ms * 1e-3) / 1e9
-    roofline = {"bound": "hbm", "achieved": round(sgs_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(sgs_gbs / HBM_PEAK_GBS, 4), "traffic": traffic("sgs_dense_kernel", cfg.name),
-                "kernel": "sgs_dense_kernel", "bytes_per_launch": sgs_bytes, "ms_per_launch": round(s_ms, 3)}
+    # The dense sweep, timed on its own outside the step: its HBM fraction is
+    # the greedy's streaming figure.  Algorithmic bytes per launch: the N x N
+    # float32 cost read once per step, plus the per-target vectors (capacity
+    # and best cost read, best cost written).
+    def time_sgs(incremental, reps):
+        e0 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+        e1 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+        out = None
+        for i in range(reps):
+            e0[i].record()
+            out = cp.sgs_select(cost, t["capacity"], k, workspace=ws_s, incremental=incremental)
+            e1[i].record()
+        torch.cuda.synchronize()
+        return float(np.mean([x.elapsed_time(y) for x, y in zip(e0, e1)])), out
+
+    dense_bytes = k * (4.0 * n * n + 12.0 * n)
+    if args.sgs == "dense":
+        dense_ms, rd = s_ms, r
+    else:
+        dense_ms, rd = time_sgs(False, 1)
+    dense_gbs = dense_bytes / (dense_ms * 1e-3) / 1e9
+    dense = {"kernel": "sgs_dense_kernel", "ms": round(dense_ms, 3), "bound": "hbm",
+             "achieved": round(dense_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+             "frac": round(dense_gbs / HBM_PEAK_GBS, 4), "bytes": dense_bytes,
+             "traffic": traffic("sgs_dense_kernel", cfg.name)}
+    same = bool(np.array_equal(rd.selected.cpu().numpy(), sel))
+
+    # Incremental form: algorithmic bytes are the step-0 pass over the whole
+    # cost, one cost element per target per step (the pick's column), and one
+    # row of N costs per target whose best cost the pick lowers.  The number of
+    # such (step, target) pairs is replayed on the host from the cost and the
+    # picks, outside the timed region.
+    if args.sgs == "incremental":
+        C = cost.cpu().numpy()                     # target-major: C[j, s]
+        b = np.full(n, np.float32(3.0), np.float32)       # c0: sgs_select's default, the sum of the unit weights
+        changed = 0
+        for tt in sel:
+            col = C[:, int(tt)]
+            hit = col < b
+            changed += int(hit.sum())
+            b = np.where(hit, col, b)
+        del C
+        sgs_bytes = 4.0 * n * n + 4.0 * n * k + 4.0 * n * changed
+        sgs_gbs = sgs_bytes / (s_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(sgs_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(sgs_gbs / HBM_PEAK_GBS, 4), "traffic": traffic("sgs_inc_kernel", cfg.name),
+                    "kernel": "sgs_inc_kernel", "bytes_per_launch": sgs_bytes, "ms_per_launch": round(s_ms, 3),
+                    "changed_targets": changed, "us_per_greedy_step": round(s_ms * 1e3 / k, 2)}
+    else:
+        roofline = {key: dense[key] for key in ("bound", "achieved", "peak", "unit", "frac", "traffic", "kernel")}
+        roofline.update({"bytes_per_launch": dense_bytes, "ms_per_launch": round(dense_ms, 3)})
 
     # FST cost: symmetric Gram needs N (N + 1) D flops; the whole call (prep,
     # Gram, epilogue) is timed, so this fraction is a lower bound for the Gram.
@@ -290,11 +338,13 @@ def main():
         "dtype": scene.dtype,
         "data": "synthetic",
         "config": {"workload": cfg.name, "n": n, "d": d, "k": k, "features": scene.dtype,
-                   "lite_voxel_m": lite_h, "seed": args.seed},
+                   "lite_voxel_m": lite_h, "seed": args.seed, "sgs": args.sgs},
         "roofline": roofline,
         "breakdown": {
             "fst_cost_ms": round(f_ms, 3),
             "sgs_select_ms": round(s_ms, 3),
+            "sgs_dense_sweep": dense,
+            "sgs_dense_same_picks": same,
             "lite_select_ms": round(l_ms, 3),
             "coverprune_ms_per_scene": round(f_ms + s_ms, 3),
             "coverprune_lite_ms_per_scene": round(l_ms, 3),
