@@ -226,7 +226,8 @@ def main():
     cost = torch.empty((n, n), dtype=torch.float32, device=dev)
     maxima = torch.empty(3, dtype=torch.float32, device=dev)
     ws_f = torch.empty(lib.coverprune_fst_cost_workspace(n, d, dt), dtype=torch.uint8, device=dev)
-    ws_s = torch.empty(lib.coverprune_sgs_workspace(n, k), dtype=torch.uint8, device=dev)
+    ws_s = torch.empty(max(lib.coverprune_sgs_workspace(n, k, f) for f in (cp.CP_SGS_DENSE, cp.CP_SGS_INCREMENTAL)),
+                       dtype=torch.uint8, device=dev)
     ws_l = torch.empty(lib.coverprune_lite_workspace(n, d, k, dt), dtype=torch.uint8, device=dev)
 
     def step(i=None, ev=None):

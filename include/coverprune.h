@@ -124,7 +124,10 @@ cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int6
  *                   token that covers it most cheaply (the earliest chosen among
  *                   equals), or -1 if no chosen token costs less than c0
  */
-size_t coverprune_sgs_workspace(int64_t n, int64_t k);
+/* Workspace for one form (flags as for coverprune_sgs_select): the dense form
+ * needs about 9 MB at n = 16384 (private best costs and float64 partial
+ * gains of up to 64 row panels), the incremental form about 16 B per token. */
+size_t coverprune_sgs_workspace(int64_t n, int64_t k, uint32_t flags);
 cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capacity, int64_t k,
                                 float c0, uint32_t flags, int32_t* selected, double* step_gain,
                                 double* step_objective, int32_t* assign, void* workspace,

@@ -59,7 +59,7 @@ def library() -> ctypes.CDLL:
     lib.coverprune_fst_cost_workspace.restype = sz
     lib.coverprune_fst_cost.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, _Weights, vp, vp, vp, sz, vp]
     lib.coverprune_fst_cost.restype = st
-    lib.coverprune_sgs_workspace.argtypes = [i64, i64]
+    lib.coverprune_sgs_workspace.argtypes = [i64, i64, ctypes.c_uint32]
     lib.coverprune_sgs_workspace.restype = sz
     lib.coverprune_sgs_select.argtypes = [vp, i64, vp, i64, ctypes.c_float, u32, vp, vp, vp, vp, vp, sz, vp]
     lib.coverprune_sgs_select.restype = st
@@ -179,10 +179,10 @@ def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[
     gain = torch.empty(int(k), dtype=torch.float64, device=dev)
     obj = torch.empty(int(k), dtype=torch.float64, device=dev)
     assign = torch.empty(n, dtype=torch.int32, device=dev)
-    need = lib.coverprune_sgs_workspace(n, int(k))
+    flags = CP_SGS_INCREMENTAL if incremental else CP_SGS_DENSE
+    need = lib.coverprune_sgs_workspace(n, int(k), flags)
     if workspace is None:
         workspace = _workspace(need, dev)
-    flags = CP_SGS_INCREMENTAL if incremental else CP_SGS_DENSE
     _check(lib.coverprune_sgs_select(_ptr(cost), n, _ptr(capacity), int(k), float(c0), flags,
                                      _ptr(sel), _ptr(gain), _ptr(obj), _ptr(assign), _ptr(workspace),
                                      workspace.numel(), _stream(stream)))

@@ -143,9 +143,10 @@ cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int6
 }
 
 // ---------------------------------------------------------------------------
-size_t coverprune_sgs_workspace(int64_t n, int64_t k) {
+size_t coverprune_sgs_workspace(int64_t n, int64_t k, uint32_t flags) {
   if (n < 1 || k < 1) return 0;
-  return std::max(cp::sgs_workspace_bytes(n, k), cp::sgs_inc_workspace_bytes(n, k));
+  if (flags == CP_SGS_INCREMENTAL) return cp::sgs_inc_workspace_bytes(n, k);
+  return cp::sgs_workspace_bytes(n, k);
 }
 
 cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capacity, int64_t k,
@@ -158,7 +159,7 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
   if (flags != CP_SGS_DENSE && flags != CP_SGS_INCREMENTAL) return fail(CP_ERR_UNSUPPORTED, "unknown flags 0x%x", flags);
   if (!cost || !capacity || !selected) return fail(CP_ERR_INVALID_ARG, "cost, capacity and selected must be non-NULL");
   if (!aligned16(cost)) return fail(CP_ERR_INVALID_ARG, "cost is not 16-byte aligned");
-  cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_workspace(n, k));
+  cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_workspace(n, k, flags));
   if (st != CP_OK) return st;
 
   cp::SgsParams p;

@@ -46,8 +46,11 @@ def test_version_and_status_strings(lib):
 def test_workspace_queries(lib):
     assert lib.coverprune_fst_cost_workspace(0, 8, 1) == 0
     assert lib.coverprune_fst_cost_workspace(16384, 3584, 1) >= 16384 * 4
-    a = lib.coverprune_sgs_workspace(1024, 102)
-    b = lib.coverprune_sgs_workspace(16384, 1638)
+    a = lib.coverprune_sgs_workspace(1024, 102, 0)
+    b = lib.coverprune_sgs_workspace(16384, 1638, 0)
+    # the incremental form needs far less than the dense form's partial gains
+    c = lib.coverprune_sgs_workspace(16384, 1638, 1)
+    assert 16384 * 16 <= c < b
     assert 0 < a < b
     # at least two radix key buffers, two token buffers and the packed voxel words
     assert lib.coverprune_lite_workspace(32768, 3584, 3277, 1) >= 32768 * 40

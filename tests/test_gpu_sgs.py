@@ -213,3 +213,23 @@ def test_full_size_incremental_matches_dense():
     if first < s.k:
         assert abs(ga[first] - gb[first]) <= 1e-9 * ga[first]
     assert np.allclose(a.objective.cpu().numpy()[-1], b.objective.cpu().numpy()[-1], rtol=1e-6)
+
+
+@pytest.mark.slow
+def test_incremental_general_form_matches_dense():
+    # Beyond the benchmark's size, on a random cost of 16900 tokens (W = 67
+    # rows and columns per block, two column chunks), against the dense sweep.
+    n, k = 16900, 24
+    print(f"sgs incremental general form n={n} k={k}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(11)
+    cost = torch.rand((n, n), generator=g, device="cuda", dtype=torch.float32) * 3.0
+    cost.fill_diagonal_(0.0)
+    cap = torch.full((n,), 1.0 / n, device="cuda", dtype=torch.float32)
+    cp = _cp()
+    a = cp.sgs_select(cost, cap, k, c0=3.0)
+    b = cp.sgs_select(cost, cap, k, c0=3.0, incremental=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(a.selected.cpu().numpy(), b.selected.cpu().numpy())
+    assert np.allclose(a.gain.cpu().numpy(), b.gain.cpu().numpy(), rtol=1e-9, atol=0.0)
+    assert np.allclose(a.objective.cpu().numpy(), b.objective.cpu().numpy(), rtol=1e-9, atol=0.0)
+    assert np.array_equal(a.assign.cpu().numpy(), b.assign.cpu().numpy())
