@@ -6,6 +6,7 @@
 //             target-major cost C_tm[t][s] = C(s, t), writing both triangles
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 
 #include "common.h"
@@ -21,52 +22,61 @@ __global__ void fst_init_kernel(FstScratch s) {
   *s.tau_max = INT_MIN;
 }
 
-// One wave per feature row: inverse norm.  The block also folds its rows'
-// frame indices into the global range.
+// Inverse feature norms: each wave walks rows blockIdx.x * 8 + w, + 8 *
+// gridDim.x, ..., with a row's 16-byte loads (up to 8 per lane) in flight
+// together.  Frame indices fold into a per-block range first, so the grid
+// issues only two atomics per block.
 template <bool BF16>
-__global__ __launch_bounds__(256) void row_norm_kernel(const void* feats, int n, int d,
+__global__ __launch_bounds__(512) void row_norm_kernel(const void* feats, int n, int d,
                                                        const int32_t* frame, FstScratch s) {
   const int lane = threadIdx.x & 63, wib = threadIdx.x >> 6;
-  const int row = blockIdx.x * 4 + wib;
-  float acc = 0.f;
-  if (row < n) {
-    if (BF16) {
-      const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(feats) + size_t(row) * d);
-      for (int i = lane; i < d / 8; i += 64) {
-        const uint4 q = p[i];
-        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+  int fmin = INT_MAX, fmax = INT_MIN;
+  const int m = BF16 ? d / 8 : d / 4;   // 16-byte chunks per row
+  for (int row = blockIdx.x * 8 + wib; row < n; row += gridDim.x * 8) {
+    const uint4* p = reinterpret_cast<const uint4*>(static_cast<const char*>(feats) +
+                                                    size_t(row) * d * (BF16 ? 2 : 4));
+    float acc = 0.f;
+    for (int i0 = 0; i0 < m; i0 += 8 * 64) {
+      uint4 q[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + u * 64 + lane;
+        q[u] = i < m ? p[i] : make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t w4[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
-          const float lo = bf16_bits_to_float(w[h] & 0xffffu), hi = bf16_bits_to_float(w[h] >> 16);
-          acc = fmaf(lo, lo, acc);
-          acc = fmaf(hi, hi, acc);
+          if (BF16) {
+            const float lo = bf16_bits_to_float(w4[h] & 0xffffu), hi = bf16_bits_to_float(w4[h] >> 16);
+            acc = fmaf(lo, lo, acc);
+            acc = fmaf(hi, hi, acc);
+          } else {
+            const float x = __uint_as_float(w4[h]);
+            acc = fmaf(x, x, acc);
+          }
         }
       }
-    } else {
-      const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(feats) + size_t(row) * d);
-      for (int i = lane; i < d / 4; i += 64) {
-        const float4 q = p[i];
-        acc = fmaf(q.x, q.x, acc);
-        acc = fmaf(q.y, q.y, acc);
-        acc = fmaf(q.z, q.z, acc);
-        acc = fmaf(q.w, q.w, acc);
-      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+    if (lane == 0) {
+      s.inv_norm[row] = acc > 0.f ? 1.0f / sqrtf(acc) : 0.f;
+      const int f = frame[row];
+      fmin = min(fmin, f);
+      fmax = max(fmax, f);
     }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
-  if (row < n && lane == 0) s.inv_norm[row] = acc > 0.f ? 1.0f / sqrtf(acc) : 0.f;
-
-  __shared__ int smin[4], smax[4];
-  const int f = row < n ? frame[row] : 0;
+  __shared__ int smin[8], smax[8];
   if (lane == 0) {
-    smin[wib] = row < n ? f : INT_MAX;
-    smax[wib] = row < n ? f : INT_MIN;
+    smin[wib] = fmin;
+    smax[wib] = fmax;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     int lo = smin[0], hi = smax[0];
-    for (int w = 1; w < 4; ++w) {
+    for (int w = 1; w < 8; ++w) {
       lo = min(lo, smin[w]);
       hi = max(hi, smax[w]);
     }
@@ -97,26 +107,36 @@ __device__ __forceinline__ double sq_dist(double ax, double ay, double az, doubl
 
 constexpr int kPosTile = 256;
 
-__global__ __launch_bounds__(256) void pos_pairmax_kernel(const float* pos, int n, FstScratch s) {
-  int ti, tj;
-  upper_tile(blockIdx.x, ti, tj);
+// Exact maximum squared distance over all pairs: blocks walk the upper
+// 256 x 256 tiles (grid-stride), a thread takes one row of the tile against
+// the tile's columns staged in LDS, and each block issues one atomic at the
+// end.
+__global__ __launch_bounds__(256) void pos_pairmax_kernel(const float* pos, int n, int ntiles, FstScratch s) {
   __shared__ double sx[kPosTile], sy[kPosTile], sz[kPosTile];
-  const int j = tj * kPosTile + threadIdx.x;
-  const int jn = min(kPosTile, n - tj * kPosTile);
-  if (threadIdx.x < jn) {
-    sx[threadIdx.x] = pos[3 * j];
-    sy[threadIdx.x] = pos[3 * j + 1];
-    sz[threadIdx.x] = pos[3 * j + 2];
-  }
-  __syncthreads();
-  const int i = ti * kPosTile + threadIdx.x;
+  __shared__ double sm[4];
   double best = 0.0;
-  if (i < n) {
-    const double x = pos[3 * i], y = pos[3 * i + 1], z = pos[3 * i + 2];
-    for (int jj = 0; jj < jn; ++jj) best = fmax(best, sq_dist(x, y, z, sx[jj], sy[jj], sz[jj]));
+  for (int b = blockIdx.x; b < ntiles; b += gridDim.x) {
+    int ti, tj;
+    upper_tile(b, ti, tj);
+    const int j = tj * kPosTile + threadIdx.x;
+    const int jn = min(kPosTile, n - tj * kPosTile);
+    __syncthreads();
+    if (threadIdx.x < jn) {
+      sx[threadIdx.x] = pos[3 * j];
+      sy[threadIdx.x] = pos[3 * j + 1];
+      sz[threadIdx.x] = pos[3 * j + 2];
+    }
+    __syncthreads();
+    const int i = ti * kPosTile + threadIdx.x;
+    if (i < n) {
+      const double x = pos[3 * i], y = pos[3 * i + 1], z = pos[3 * i + 2];
+      for (int jj = 0; jj < jn; ++jj) best = fmax(best, sq_dist(x, y, z, sx[jj], sy[jj], sz[jj]));
+    }
   }
   best = wave_max(best);
-  if ((threadIdx.x & 63) == 0) atomic_max_nonneg(s.mx2_bits, best);
+  if ((threadIdx.x & 63) == 0) sm[threadIdx.x >> 6] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) atomic_max_nonneg(s.mx2_bits, fmax(fmax(sm[0], sm[1]), fmax(sm[2], sm[3])));
 }
 
 // ---------------------------------------------------------------------------
@@ -129,7 +149,10 @@ __device__ __forceinline__ float phi_kappa(float z, float kappa, float inv_log1p
 // Block = one upper tile pair (ti <= tj) of 64 x 64.  The upper tile holds
 // d_f(i, j) from the Gram (rows i in ti, columns j in tj).  It becomes
 // C_tm[i][j] = C(s = j, t = i) in place, and its mirror C_tm[j][i] = C(s = i, t = j)
-// is staged through LDS and written transposed.
+// is staged through LDS and written transposed.  With VEC (n % 4 == 0) a
+// thread moves 4 consecutive columns per 16-byte load and store: 16 threads
+// cover a tile row of 256 bytes.
+template <bool VEC>
 __global__ __launch_bounds__(256) void fst_epilogue_kernel(FstParams p, FstScratch s) {
   int ti, tj;
   upper_tile(blockIdx.x, ti, tj);
@@ -170,20 +193,50 @@ __global__ __launch_bounds__(256) void fst_epilogue_kernel(FstParams p, FstScrat
   const float wt = m_t > 0 ? p.lambda_tau / float(m_t) : 0.f;
   __syncthreads();
 
+  const bool mirror = ti != tj;
+  // Both terms of an entry from its raw d_f; writes the mirror value to LDS.
+  auto cost_at = [&](int r, int c, float df) {
+    const float dx = rx[r] - cx[c], dy = ry[r] - cy[c], dz = rz[r] - cz[c];
+    const float dist = sqrtf(dx * dx + dy * dy + dz * dz);
+    const float base = wf * df + p.lambda_x * phi_kappa(dist * inv_mx, p.kappa, p.inv_log1p_kappa);
+    if (mirror) tr[c][r] = base + wt * float(max(0, rf[r] - cf[c]));
+    return base + wt * float(max(0, cf[c] - rf[r]));
+  };
+  const bool full = (ti + 1) * kEpiTile <= n && (tj + 1) * kEpiTile <= n;
+  if (VEC && full) {
+    const int c4 = (t & 15) * 4;
+#pragma unroll 2
+    for (int r = t >> 4; r < kEpiTile; r += 16) {
+      float4* at = reinterpret_cast<float4*>(p.cost + size_t(ti * kEpiTile + r) * n + tj * kEpiTile + c4);
+      const float4 df = *at;
+      float4 out;
+      out.x = cost_at(r, c4, df.x);
+      out.y = cost_at(r, c4 + 1, df.y);
+      out.z = cost_at(r, c4 + 2, df.z);
+      out.w = cost_at(r, c4 + 3, df.w);
+      *at = out;
+    }
+    if (!mirror) return;
+    __syncthreads();
+#pragma unroll 2
+    for (int r = t >> 4; r < kEpiTile; r += 16) {
+      float4 v;
+      v.x = tr[r][c4];
+      v.y = tr[r][c4 + 1];
+      v.z = tr[r][c4 + 2];
+      v.w = tr[r][c4 + 3];
+      *reinterpret_cast<float4*>(p.cost + size_t(tj * kEpiTile + r) * n + ti * kEpiTile + c4) = v;
+    }
+    return;
+  }
   const int c = t & 63;
   const int j = tj * kEpiTile + c;
-  const bool mirror = ti != tj;
 #pragma unroll 4
   for (int r = t >> 6; r < kEpiTile; r += 4) {
     const int i = ti * kEpiTile + r;
     if (i < n && j < n) {
       const size_t at = size_t(i) * n + j;
-      const float df = p.cost[at];
-      const float dx = rx[r] - cx[c], dy = ry[r] - cy[c], dz = rz[r] - cz[c];
-      const float dist = sqrtf(dx * dx + dy * dy + dz * dz);
-      const float base = wf * df + p.lambda_x * phi_kappa(dist * inv_mx, p.kappa, p.inv_log1p_kappa);
-      p.cost[at] = base + wt * float(max(0, cf[c] - rf[r]));
-      if (mirror) tr[c][r] = base + wt * float(max(0, rf[r] - cf[c]));
+      p.cost[at] = cost_at(r, c, p.cost[at]);
     }
   }
   if (!mirror) return;
@@ -204,20 +257,24 @@ hipError_t launch_fst_prep(const FstParams& p, const FstScratch& s, hipStream_t 
   fst_init_kernel<<<1, 1, 0, stream>>>(s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nb = (p.n + 3) / 4;
+  const int nb = std::min((p.n + 7) / 8, 512);
   if (p.bf16)
-    row_norm_kernel<true><<<nb, 256, 0, stream>>>(p.feats, p.n, p.d, p.frame, s);
+    row_norm_kernel<true><<<nb, 512, 0, stream>>>(p.feats, p.n, p.d, p.frame, s);
   else
-    row_norm_kernel<false><<<nb, 256, 0, stream>>>(p.feats, p.n, p.d, p.frame, s);
+    row_norm_kernel<false><<<nb, 512, 0, stream>>>(p.feats, p.n, p.d, p.frame, s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int t = tiles_of(p.n, kPosTile);
-  pos_pairmax_kernel<<<t * (t + 1) / 2, 256, 0, stream>>>(p.pos, p.n, s);
+  const int tiles = t * (t + 1) / 2;
+  pos_pairmax_kernel<<<std::min(tiles, 512), 256, 0, stream>>>(p.pos, p.n, tiles, s);
   return hipGetLastError();
 }
 
 hipError_t launch_fst_epilogue(const FstParams& p, const FstScratch& s, hipStream_t stream) {
   const int t = tiles_of(p.n, kEpiTile);
-  fst_epilogue_kernel<<<t * (t + 1) / 2, 256, 0, stream>>>(p, s);
+  if (p.n % 4 == 0)
+    fst_epilogue_kernel<true><<<t * (t + 1) / 2, 256, 0, stream>>>(p, s);
+  else
+    fst_epilogue_kernel<false><<<t * (t + 1) / 2, 256, 0, stream>>>(p, s);
   return hipGetLastError();
 }
 
