@@ -13,9 +13,10 @@ Modules
            prototypes (Sec. 4, Eq. 17-20)
   ot       exact transport linear programs (Sec. 3.1, Eq. 2, 5, 11, 19-20) used
            only to pin the readings above on tiny inputs
+  knn      3D nearest-neighbour tables M_g(t) for the local greedy (Eq. 13)
 
 Readings of passages the paper leaves open are stated in each function's
 docstring; every one is also listed with its justification in the design
 notes at the repository root.
 """
-from . import fst, sgs, lite, ot  # noqa: F401
+from . import fst, sgs, lite, ot, knn  # noqa: F401

@@ -125,3 +125,38 @@ def test_local_neighbourhood_restricts_gain():
     nb = np.arange(60)[:, None]
     out = sgs.sgs_ref(C, v, 1, 3.0, neighbours=nb)
     assert out["selected"][0] == int(np.argmax(v))
+
+
+def test_local_gains_bounded_by_dense_gains():
+    # A neighbourhood only drops nonnegative terms: at every step of the local
+    # trajectory the pick's local gain is at most its gain over all targets.
+    from oracle import knn
+    s = _sub(90, 6)
+    C = _cost(s)
+    v = s.capacity.astype(np.float64)
+    nb = knn.knn_ref(s.pos, 7)
+    out = sgs.sgs_ref(C, v, 15, 3.0, neighbours=nb)
+    b = np.full(90, 3.0)
+    for t, g in zip(out["selected"], out["gain"]):
+        full = float(np.sum(v * np.maximum(0.0, b - C[t])))
+        assert g <= full + 1e-15
+        b = np.minimum(b, C[t])
+    # L(S) still telescopes over the picks' full gains.
+    assert out["objective"][-1] == pytest.approx(float(np.sum(v * b)), rel=1e-12)
+
+
+def test_local_pick_lowers_best_cost_beyond_its_neighbourhood():
+    # Three tokens on a line; each candidate sees only itself (g = 1), but the
+    # residual of the transport over all targets (Eq. 14) drops everywhere.
+    C = np.array([[0.0, 0.5, 2.0],
+                  [0.5, 0.0, 1.0],
+                  [2.0, 1.0, 0.0]])
+    v = np.array([0.5, 0.3, 0.2])
+    nb = np.arange(3)[:, None]
+    out = sgs.sgs_ref(C, v, 2, 3.0, neighbours=nb)
+    # step 0: local gains are c0 v_c = 1.5, 0.9, 0.6 -> token 0
+    assert out["selected"][0] == 0 and out["gain"][0] == pytest.approx(1.5)
+    # b after step 0 = min(c0, C[0]) = [0, 0.5, 2.0]; step 1 local gains:
+    # token 1: 0.3 (0.5 - 0) = 0.15, token 2: 0.2 (2.0 - 0) = 0.4 -> token 2
+    assert out["selected"][1] == 2 and out["gain"][1] == pytest.approx(0.4)
+    assert out["objective"][1] == pytest.approx(0.3 * 0.5)
