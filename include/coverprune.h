@@ -9,6 +9,9 @@
  *                          every pair of tokens (Sec. 3.3, Eq. 7-8);
  *   coverprune_sgs_select  greedy selection of K tokens against that cost and
  *                          the target capacities (Sec. 3.5, Eq. 11-16);
+ *   coverprune_knn         the g nearest tokens of every token in 3D, and
+ *   coverprune_sgs_local_select  the greedy with gains over those neighbours
+ *                          only (Sec. 3.5, Eq. 13);
  *   coverprune_lite_select CoverPrune-Lite: Morton ordering, capacity-guided
  *                          grouping and per-group prototypes (Sec. 4, Eq. 17-20).
  *
@@ -132,6 +135,51 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
                                 float c0, uint32_t flags, int32_t* selected, double* step_gain,
                                 double* step_objective, int32_t* assign, void* workspace,
                                 size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Spatially local greedy (Sec. 3.5, Eq. 13).
+ *
+ * The same greedy with each candidate's gain restricted to its neighbour set
+ * M_g(c), the g targets nearest to it in 3D:
+ *   gain(c) = sum_{j in M_g(c)} v_j max(0, b_j - C(c, j)),
+ * while a pick still lowers b_j of every target it is cheaper for (the
+ * residual of Eq. 14 is over all targets) and L(S) is summed over all of
+ * them.  Each term takes the float64 difference of the two float32 costs and
+ * a float64 product; every gain is summed afresh each step in exact 128-bit
+ * fixed point at a scale of 2^-S, S set by c0 * sum v (so only terms below
+ * that resolution differ from a float64 sum).  Equal gains go to the smaller
+ * index; exactly k tokens are selected.
+ *
+ * coverprune_knn writes the tables: row t lists the g tokens nearest to t,
+ * ordered by (distance, index), t itself included.  Distances are compared as
+ * float64 squared distances (dx^2 + dy^2) + dz^2 of the float32 positions,
+ * formed without fused multiply-adds, so the tables are exact and
+ * reproducible.
+ *
+ *   pos         [n, 3] float token positions (as for coverprune_fst_cost)
+ *   g           1 <= g <= min(n, CP_KNN_MAX_G) for coverprune_knn,
+ *               1 <= g <= min(n, CP_SGS_LOCAL_MAX_G) for the greedy
+ *   neighbours  [n, g] int32, device memory: written by coverprune_knn, read
+ *               by coverprune_sgs_local_select (row c = M_g(c); entries are
+ *               clamped into [0, n); a target listed twice counts twice)
+ *   cost, capacity, k, c0, selected, step_gain, step_objective, assign:
+ *               as for coverprune_sgs_select (n <= CP_SGS_LOCAL_MAX_N)
+ *
+ * Both enqueue on `stream` and return before the work is done; bad sizes or
+ * NULL pointers return CP_ERR_INVALID_ARG before anything is enqueued.  The
+ * workspace of the greedy is about 16 B per token.
+ */
+#define CP_KNN_MAX_N 16384
+#define CP_KNN_MAX_G 1024
+#define CP_SGS_LOCAL_MAX_N 16384
+#define CP_SGS_LOCAL_MAX_G 128
+cp_status coverprune_knn(const float* pos, int64_t n, int64_t g, int32_t* neighbours, void* stream);
+size_t coverprune_sgs_local_workspace(int64_t n, int64_t k);
+cp_status coverprune_sgs_local_select(const float* cost, int64_t n, const float* capacity,
+                                      const int32_t* neighbours, int64_t g, int64_t k, float c0,
+                                      int32_t* selected, double* step_gain, double* step_objective,
+                                      int32_t* assign, void* workspace, size_t workspace_bytes,
+                                      void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* CoverPrune-Lite (Sec. 4, Eq. 17-20).

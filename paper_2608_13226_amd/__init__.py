@@ -14,7 +14,7 @@ from typing import Optional
 
 import torch
 
-__all__ = ["fst_cost", "sgs_select", "lite_select", "library", "library_path", "CoverPruneError",
+__all__ = ["fst_cost", "sgs_select", "knn", "sgs_local_select", "lite_select", "library", "library_path", "CoverPruneError",
            "DEFAULT_KAPPA"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -63,6 +63,13 @@ def library() -> ctypes.CDLL:
     lib.coverprune_sgs_workspace.restype = sz
     lib.coverprune_sgs_select.argtypes = [vp, i64, vp, i64, ctypes.c_float, u32, vp, vp, vp, vp, vp, sz, vp]
     lib.coverprune_sgs_select.restype = st
+    lib.coverprune_knn.argtypes = [vp, i64, i64, vp, vp]
+    lib.coverprune_knn.restype = st
+    lib.coverprune_sgs_local_workspace.argtypes = [i64, i64]
+    lib.coverprune_sgs_local_workspace.restype = sz
+    lib.coverprune_sgs_local_select.argtypes = [vp, i64, vp, vp, i64, i64, ctypes.c_float, vp, vp, vp, vp, vp,
+                                                sz, vp]
+    lib.coverprune_sgs_local_select.restype = st
     lib.coverprune_lite_workspace.argtypes = [i64, i64, i64, ctypes.c_int]
     lib.coverprune_lite_workspace.restype = sz
     lib.coverprune_lite_select.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, vp, i64, _Weights,
@@ -186,6 +193,50 @@ def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[
     _check(lib.coverprune_sgs_select(_ptr(cost), n, _ptr(capacity), int(k), float(c0), flags,
                                      _ptr(sel), _ptr(gain), _ptr(obj), _ptr(assign), _ptr(workspace),
                                      workspace.numel(), _stream(stream)))
+    return SgsResult(sel, gain, obj, assign)
+
+
+def knn(pos: torch.Tensor, g: int, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """The g tokens nearest to every token in 3D (Sec. 3.5, Eq. 13): row t of
+    the [n, g] int32 result lists them by (distance, index), t included."""
+    lib = library()
+    n = pos.shape[0]
+    dev = pos.device
+    _need(pos, "pos", torch.float32, (n, 3), dev)
+    if out is None:
+        out = torch.empty((n, int(g)), dtype=torch.int32, device=dev)
+    _need(out, "out", torch.int32, (n, int(g)), dev)
+    _check(lib.coverprune_knn(_ptr(pos), n, int(g), _ptr(out), _stream(stream)))
+    return out
+
+
+def sgs_local_select(cost: torch.Tensor, capacity: torch.Tensor, neighbours: torch.Tensor, k: int,
+                     c0: Optional[float] = None, weights=(1.0, 1.0, 1.0),
+                     workspace: Optional[torch.Tensor] = None, stream=None) -> SgsResult:
+    """Greedy selection with each candidate's gain over its neighbour row only
+    (Sec. 3.5, Eq. 13); neighbours is an [n, g] int32 table such as knn()
+    returns.  c0 as for sgs_select."""
+    lib = library()
+    n = cost.shape[0]
+    dev = cost.device
+    _need(cost, "cost", torch.float32, (n, n), dev)
+    _need(capacity, "capacity", torch.float32, (n,), dev)
+    if neighbours.dim() != 2:
+        raise ValueError("neighbours must be an [n, g] table")
+    g = neighbours.shape[1]
+    _need(neighbours, "neighbours", torch.int32, (n, g), dev)
+    if c0 is None:
+        c0 = float(sum(float(w) for w in weights))
+    sel = torch.empty(int(k), dtype=torch.int32, device=dev)
+    gain = torch.empty(int(k), dtype=torch.float64, device=dev)
+    obj = torch.empty(int(k), dtype=torch.float64, device=dev)
+    assign = torch.empty(n, dtype=torch.int32, device=dev)
+    need = lib.coverprune_sgs_local_workspace(n, int(k))
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    _check(lib.coverprune_sgs_local_select(_ptr(cost), n, _ptr(capacity), _ptr(neighbours), g, int(k), float(c0),
+                                           _ptr(sel), _ptr(gain), _ptr(obj), _ptr(assign), _ptr(workspace),
+                                           workspace.numel(), _stream(stream)))
     return SgsResult(sel, gain, obj, assign)
 
 

@@ -181,6 +181,56 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
 }
 
 // ---------------------------------------------------------------------------
+cp_status coverprune_knn(const float* pos, int64_t n, int64_t g, int32_t* neighbours, void* stream) {
+  if (n < 1 || n > CP_KNN_MAX_N) return fail(CP_ERR_INVALID_ARG, "n = %lld outside [1, %d]", (long long)n, CP_KNN_MAX_N);
+  if (g < 1 || g > std::min<int64_t>(n, CP_KNN_MAX_G))
+    return fail(CP_ERR_INVALID_ARG, "g = %lld outside [1, min(n, %d)]", (long long)g, CP_KNN_MAX_G);
+  if (!pos || !neighbours) return fail(CP_ERR_INVALID_ARG, "pos and neighbours must be non-NULL");
+  hipError_t e = cp::launch_knn(pos, int(n), int(g), neighbours, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "knn");
+  return ok();
+}
+
+size_t coverprune_sgs_local_workspace(int64_t n, int64_t k) {
+  if (n < 1 || k < 1) return 0;
+  return cp::sgs_local_workspace_bytes(n, k);
+}
+
+cp_status coverprune_sgs_local_select(const float* cost, int64_t n, const float* capacity,
+                                      const int32_t* neighbours, int64_t g, int64_t k, float c0,
+                                      int32_t* selected, double* step_gain, double* step_objective,
+                                      int32_t* assign, void* workspace, size_t workspace_bytes,
+                                      void* stream) {
+  if (n < 1 || n > CP_SGS_LOCAL_MAX_N)
+    return fail(CP_ERR_INVALID_ARG, "n = %lld outside [1, %d]", (long long)n, CP_SGS_LOCAL_MAX_N);
+  if (g < 1 || g > std::min<int64_t>(n, CP_SGS_LOCAL_MAX_G))
+    return fail(CP_ERR_INVALID_ARG, "g = %lld outside [1, min(n, %d)]", (long long)g, CP_SGS_LOCAL_MAX_G);
+  if (k < 1 || k > n) return fail(CP_ERR_INVALID_ARG, "k = %lld outside [1, n = %lld]", (long long)k, (long long)n);
+  if (!std::isfinite(c0)) return fail(CP_ERR_INVALID_ARG, "c0 must be finite");
+  if (!cost || !capacity || !neighbours || !selected)
+    return fail(CP_ERR_INVALID_ARG, "cost, capacity, neighbours and selected must be non-NULL");
+  if (!aligned16(cost)) return fail(CP_ERR_INVALID_ARG, "cost is not 16-byte aligned");
+  cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_local_workspace(n, k));
+  if (st != CP_OK) return st;
+
+  cp::SgsParams p;
+  p.cost = cost;
+  p.n = int(n);
+  p.capacity = capacity;
+  p.k = int(k);
+  p.c0 = c0;
+  p.selected = selected;
+  p.step_gain = step_gain;
+  p.step_objective = step_objective;
+  p.assign = assign;
+  p.workspace = workspace;
+  p.workspace_bytes = workspace_bytes;
+  hipError_t e = cp::launch_sgs_local(p, neighbours, int(g), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sgs local");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
 size_t coverprune_lite_workspace(int64_t n, int64_t d, int64_t k, cp_dtype dtype) {
   (void)d;
   (void)dtype;

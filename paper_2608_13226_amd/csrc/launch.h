@@ -53,6 +53,12 @@ size_t sgs_workspace_bytes(int64_t n, int64_t k);
 hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream);
 size_t sgs_inc_workspace_bytes(int64_t n, int64_t k);
 hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream);
+// Local form: gains over the neighbour table nbr [n, g] (g <= 128, n <= 16384).
+size_t sgs_local_workspace_bytes(int64_t n, int64_t k);
+hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipStream_t stream);
+
+// Nearest-neighbour tables: out [n, g], n <= 16384, g <= min(n, 1024).
+hipError_t launch_knn(const float* pos, int n, int g, int32_t* out, hipStream_t stream);
 
 // CoverPrune-Lite.
 struct LiteParams {

@@ -95,6 +95,38 @@ def replay_greedy(C_src: np.ndarray, v: np.ndarray, c0: float, picks, tie_atol=0
     return ties, np.array(gains), np.array(objs)
 
 
+def replay_greedy_local(C_tm: np.ndarray, v: np.ndarray, c0: float, neighbours, picks, tie_atol=0.0):
+    """replay_greedy for the local form (Eq. 13): each candidate's gain runs
+    over its neighbour row only, while b is lowered for every target.
+
+    C_tm is target-major (C_tm[j, c] = C(c, j)), so a full-size float32 cost
+    fits; gains are formed from the gathered [n, g] band in float64."""
+    v = np.asarray(v, np.float64)
+    nb = np.asarray(neighbours, np.int64)
+    n, g = nb.shape
+    rows = np.repeat(np.arange(n), g).reshape(n, g)
+    Cg = np.asarray(C_tm[nb, rows], np.float64)            # Cg[c, q] = C(c, nb[c, q])
+    vg = v[nb]
+    b = np.full(n, float(c0))
+    chosen = np.zeros(n, bool)
+    ties, gains, objs = [], [], []
+    for step, t in enumerate(int(x) for x in picks):
+        assert 0 <= t < n and not chosen[t], f"step {step}: pick {t} invalid or repeated"
+        gl = (vg * np.maximum(0.0, b[nb] - Cg)).sum(axis=1)
+        gl[chosen] = -np.inf
+        best = int(np.argmax(gl))
+        if t != best:
+            slack = TIE_RTOL * abs(gl[best]) + tie_atol
+            assert gl[t] >= gl[best] - slack, (f"step {step}: picked {t} with local gain {gl[t]!r}, "
+                                               f"best is {best} with {gl[best]!r}")
+            ties.append(step)
+        chosen[t] = True
+        gains.append(gl[t])
+        b = np.minimum(b, np.asarray(C_tm[:, t], np.float64))
+        objs.append(float(np.sum(v * b)))
+    return ties, np.array(gains), np.array(objs)
+
+
 def check_trajectory_invariants(sel, gain, obj, v, c0, k, n):
     sel = np.asarray(sel)
     assert len(sel) == k and len(set(sel.tolist())) == k

@@ -127,3 +127,42 @@ def test_binding_needs_the_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cp, "library_path", lambda: str(tmp_path / "missing.so"))
     with pytest.raises(cp.CoverPruneError):
         cp.library()
+
+
+def test_local_workspace_query(lib):
+    assert lib.coverprune_sgs_local_workspace(0, 8) == 0
+    assert 16384 * 16 <= lib.coverprune_sgs_local_workspace(16384, 1638) < lib.coverprune_sgs_workspace(16384, 1638, 0)
+
+
+def _knn(lib, **kw):
+    a = dict(pos=FAKE, n=64, g=8, out=FAKE, stream=None)
+    a.update(kw)
+    return lib.coverprune_knn(a["pos"], a["n"], a["g"], a["out"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), INVALID), (dict(n=16385, g=8), INVALID), (dict(g=0), INVALID), (dict(g=65), INVALID),
+    (dict(n=4096, g=1025), INVALID), (dict(pos=None), INVALID), (dict(out=None), INVALID),
+])
+def test_knn_rejects(lib, kw, code):
+    assert _knn(lib, **kw) == code
+    assert lib.coverprune_last_error() != b""
+
+
+def _local(lib, **kw):
+    a = dict(cost=FAKE, n=64, v=FAKE, nbr=FAKE, g=8, k=8, c0=3.0, sel=FAKE, gain=None, obj=None, assign=None,
+             ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return lib.coverprune_sgs_local_select(a["cost"], a["n"], a["v"], a["nbr"], a["g"], a["k"], a["c0"], a["sel"],
+                                           a["gain"], a["obj"], a["assign"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), INVALID), (dict(n=16385), INVALID), (dict(g=0), INVALID), (dict(g=65), INVALID),
+    (dict(n=1024, g=129), INVALID), (dict(k=0), INVALID), (dict(k=65), INVALID),
+    (dict(c0=float("nan")), INVALID), (dict(cost=None), INVALID), (dict(v=None), INVALID),
+    (dict(nbr=None), INVALID), (dict(sel=None), INVALID), (dict(cost=ctypes.c_void_p(0x1004)), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(ws_bytes=100), WORKSPACE),
+])
+def test_sgs_local_rejects(lib, kw, code):
+    assert _local(lib, **kw) == code

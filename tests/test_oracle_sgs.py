@@ -160,3 +160,28 @@ def test_local_pick_lowers_best_cost_beyond_its_neighbourhood():
     # token 1: 0.3 (0.5 - 0) = 0.15, token 2: 0.2 (2.0 - 0) = 0.4 -> token 2
     assert out["selected"][1] == 2 and out["gain"][1] == pytest.approx(0.4)
     assert out["objective"][1] == pytest.approx(0.3 * 0.5)
+
+
+def test_local_replay_agrees_with_local_oracle():
+    # The gather-form replay used against GPU trajectories accepts the oracle's
+    # own local trajectory with no ties and the same gains and objectives, and
+    # rejects a trajectory that swaps a clearly better pick for a worse one.
+    from oracle import knn
+    from tests import parity
+    rng = np.random.default_rng(31)
+    n, g, K = 60, 8, 15
+    pos = rng.standard_normal((n, 3)).astype(np.float32)
+    C = rng.uniform(0.0, 3.0, (n, n))
+    np.fill_diagonal(C, 0.0)
+    v = rng.uniform(0.5, 1.5, n)
+    v /= v.sum()
+    nb = knn.knn_ref(pos, g)
+    ref = sgs.sgs_ref(C, v, K, 3.0, neighbours=nb)
+    ties, gains, objs = parity.replay_greedy_local(np.ascontiguousarray(C.T), v, 3.0, nb, ref["selected"])
+    assert ties == []
+    assert np.allclose(gains, ref["gain"], rtol=1e-14, atol=0.0)
+    assert np.allclose(objs, ref["objective"], rtol=1e-14, atol=0.0)
+    worst = int(np.argmin(np.where(np.arange(n) == ref["selected"][0], np.inf,
+                                   [np.sum(v[nb[c]] * np.maximum(0.0, 3.0 - C[c, nb[c]])) for c in range(n)])))
+    with pytest.raises(AssertionError):
+        parity.replay_greedy_local(np.ascontiguousarray(C.T), v, 3.0, nb, [worst])
