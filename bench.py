@@ -319,6 +319,33 @@ def main():
         roofline = {key: dense[key] for key in ("bound", "achieved", "peak", "unit", "frac", "traffic", "kernel")}
         roofline.update({"bytes_per_launch": dense_bytes, "ms_per_launch": round(dense_ms, 3)})
 
+    # Local greedy (Eq. 13) on the same cost: the g-nearest tables, then the
+    # greedy with gains over each candidate's table row.  The paper leaves g
+    # open; 64 neighbours per token is the setting timed here.
+    local = None
+    if n <= 16384:
+        g_loc = 64
+        nbr = torch.empty((n, g_loc), dtype=torch.int32, device=dev)
+        ws_loc = torch.empty(lib.coverprune_sgs_local_workspace(n, k), dtype=torch.uint8, device=dev)
+        reps = 3
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3 * reps)]
+        for i in range(reps):
+            e[3 * i].record()
+            cp.knn(t["pos"], g_loc, out=nbr)
+            e[3 * i + 1].record()
+            rl = cp.sgs_local_select(cost, t["capacity"], nbr, k, workspace=ws_loc)
+            e[3 * i + 2].record()
+        torch.cuda.synchronize()
+        knn_ms = float(np.mean([e[3 * i].elapsed_time(e[3 * i + 1]) for i in range(reps)]))
+        loc_ms = float(np.mean([e[3 * i + 1].elapsed_time(e[3 * i + 2]) for i in range(reps)]))
+        lsel = rl.selected.cpu().numpy()
+        assert len(set(lsel.tolist())) == k, "local greedy returned repeated tokens"
+        local = {"g": g_loc, "knn_ms": round(knn_ms, 3), "sgs_local_ms": round(loc_ms, 3),
+                 "us_per_greedy_step": round(loc_ms * 1e3 / k, 2),
+                 "objective": float(rl.objective[-1].item()),
+                 "dense_objective": float(r.objective[-1].item()),
+                 "picks_shared_with_dense": int(len(set(lsel.tolist()) & set(sel.tolist())))}
+
     # FST cost: symmetric Gram needs N (N + 1) D flops; the whole call (prep,
     # Gram, epilogue) is timed, so this fraction is a lower bound for the Gram.
     gram_flops = float(n) * (n + 1) * d
@@ -346,6 +373,7 @@ def main():
             "sgs_select_ms": round(s_ms, 3),
             "sgs_dense_sweep": dense,
             "sgs_dense_same_picks": same,
+            "sgs_local": local,
             "lite_select_ms": round(l_ms, 3),
             "coverprune_ms_per_scene": round(f_ms + s_ms, 3),
             "coverprune_lite_ms_per_scene": round(l_ms, 3),

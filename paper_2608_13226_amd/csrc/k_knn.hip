@@ -6,13 +6,22 @@
 // the order is reproducible bit for bit.  A nonnegative double's bit pattern
 // orders like its value, so each distance is a 64-bit integer key.
 //
-// One block per query token (exact, brute force over all n tokens, n <=
-// kKnnMaxN): the n keys go to LDS; an 8-bit radix select over the key's eight
-// bytes finds the g-th smallest key T and how many keys equal to T belong to
-// the answer; the tokens with key < T, and the first of those with key == T in
-// index order, are collected and each is placed by counting the collected
-// (key, index) pairs that precede it.
+// Exact brute force over all n tokens, in two kernels.
+//  - knn_bound_kernel (g <= kBoundMaxG), kQ query tokens per block: every
+//    thread keeps the smallest key it sees for each query; the g-th smallest
+//    of those per-thread minima is an upper bound U on the g-th smallest key
+//    (g distinct tokens lie at or below it).  A second pass collects the keys
+//    <= U, which hold every member of M_g together with all keys tied with
+//    the g-th, and ranks them by (key, index).  A row whose collection
+//    overflows kCap is marked with -1 in its first entry.
+//  - knn_radix_kernel, one row at a time per block with all n keys in LDS: an
+//    8-bit radix select over the key's eight bytes finds the g-th smallest key
+//    T and how many keys equal to T belong to the answer; the tokens below T,
+//    and the first tokens equal to T in index order, are collected and ranked.
+//    It serves g > kBoundMaxG and the rows the first kernel marked.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "common.h"
 #include "launch.h"
@@ -24,6 +33,11 @@ constexpr int kKnnMaxN = 16384;   // n float64 keys fill 128 KiB of LDS
 constexpr int kKnnMaxG = 1024;
 constexpr int kKnnBlock = 256;
 constexpr int kKnnWaves = kKnnBlock / 64;
+constexpr int kBoundMaxG = 128;         // <= kKnnBlock: the bound needs g per-thread minima; beyond
+                                        // 128 it is loose enough that rows overflow kCap
+constexpr int kQ = 8;                   // query tokens per block of the bounding kernel
+constexpr int kCap = 256;               // collected keys per query
+constexpr unsigned long long kNoKey = ~0ull;
 
 __device__ __forceinline__ unsigned long long sq_dist_key(float ax, float ay, float az, float bx, float by, float bz) {
 #pragma clang fp contract(off)
@@ -53,17 +67,107 @@ __device__ int block_exclusive_scan(int x, int* swt, int& total) {
   return before + incl - x;
 }
 
-__global__ __launch_bounds__(kKnnBlock) void knn_kernel(const float* __restrict__ pos, int n, int g,
-                                                        int32_t* __restrict__ out) {
-  extern __shared__ unsigned long long keys[];          // [n], then the collected pairs
-  unsigned long long* ckey = keys + n;                  // [g]
-  int* cidx = reinterpret_cast<int*>(ckey + g);         // [g]
+__global__ __launch_bounds__(kKnnBlock) void knn_bound_kernel(const float* __restrict__ pos, int n, int g,
+                                                              int32_t* __restrict__ out) {
+  __shared__ unsigned long long smin[kQ][kKnnBlock];
+  __shared__ unsigned long long ck[kQ][kCap];
+  __shared__ int ci[kQ][kCap];
+  __shared__ unsigned long long sU[kQ];
+  __shared__ int scount[kQ];
+  const int tid = threadIdx.x;
+  const int q0 = blockIdx.x * kQ;
+  const int nq = min(kQ, n - q0);
+  float qx[kQ], qy[kQ], qz[kQ];
+#pragma unroll
+  for (int q = 0; q < kQ; ++q) {
+    const int c = q0 + min(q, nq - 1);
+    qx[q] = pos[3 * c];
+    qy[q] = pos[3 * c + 1];
+    qz[q] = pos[3 * c + 2];
+  }
+
+  // Pass 1: every thread's smallest key for each query.
+  unsigned long long m[kQ];
+#pragma unroll
+  for (int q = 0; q < kQ; ++q) m[q] = kNoKey;
+  for (int j = tid; j < n; j += kKnnBlock) {
+    const float px = pos[3 * j], py = pos[3 * j + 1], pz = pos[3 * j + 2];
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      const unsigned long long k = sq_dist_key(qx[q], qy[q], qz[q], px, py, pz);
+      m[q] = k < m[q] ? k : m[q];
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kQ; ++q) smin[q][tid] = m[q];
+  if (tid < kQ) scount[tid] = 0;
+  __syncthreads();
+
+  // U_q = the g-th smallest per-thread minimum, by (value, thread).  Threads
+  // that saw no token hold kNoKey; at least min(n, kKnnBlock) >= g did.
+#pragma unroll
+  for (int q = 0; q < kQ; ++q) {
+    int rank = 0;
+    for (int b = 0; b < kKnnBlock; ++b) {
+      const unsigned long long x = smin[q][b];
+      rank += x < m[q] || (x == m[q] && b < tid);
+    }
+    if (rank == g - 1) sU[q] = m[q];
+  }
+  __syncthreads();
+
+  // Pass 2: every key <= U_q.
+  unsigned long long U[kQ];
+#pragma unroll
+  for (int q = 0; q < kQ; ++q) U[q] = sU[q];
+  for (int j = tid; j < n; j += kKnnBlock) {
+    const float px = pos[3 * j], py = pos[3 * j + 1], pz = pos[3 * j + 2];
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      const unsigned long long k = sq_dist_key(qx[q], qy[q], qz[q], px, py, pz);
+      if (k <= U[q]) {
+        const int slot = atomicAdd(&scount[q], 1);
+        if (slot < kCap) {
+          ck[q][slot] = k;
+          ci[q][slot] = j;
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // Rank the collected keys; the first g by (key, index) form the row.
+  for (int q = 0; q < nq; ++q) {
+    const int mq = scount[q];
+    int32_t* row = out + size_t(q0 + q) * g;
+    if (mq > kCap) {
+      if (tid == 0) row[0] = -1;
+      continue;
+    }
+    for (int a = tid; a < mq; a += kKnnBlock) {
+      const unsigned long long ka = ck[q][a];
+      const int ia = ci[q][a];
+      int rank = 0;
+      for (int b = 0; b < mq; ++b) {
+        const unsigned long long kb = ck[q][b];
+        rank += kb < ka || (kb == ka && ci[q][b] < ia);
+      }
+      if (rank < g) row[rank] = ia;
+    }
+  }
+}
+
+// Row c by radix select; keys is the block's dynamic LDS: n keys, then g
+// collected keys and g indices.
+__device__ void knn_radix_row(const float* __restrict__ pos, int n, int g, int c, unsigned long long* keys,
+                              int32_t* __restrict__ out) {
+  unsigned long long* ckey = keys + n;
+  int* cidx = reinterpret_cast<int*>(ckey + g);
   __shared__ unsigned int hist[256];
   __shared__ int swt[kKnnWaves];
   __shared__ unsigned long long s_prefix;
   __shared__ int s_rank;
   const int tid = threadIdx.x;
-  const int c = blockIdx.x;
   const float qx = pos[3 * c], qy = pos[3 * c + 1], qz = pos[3 * c + 2];
   for (int j = tid; j < n; j += kKnnBlock)
     keys[j] = sq_dist_key(qx, qy, qz, pos[3 * j], pos[3 * j + 1], pos[3 * j + 2]);
@@ -85,15 +189,15 @@ __global__ __launch_bounds__(kKnnBlock) void knn_kernel(const float* __restrict_
       if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
     }
     __syncthreads();
-    if (tid == 0) {
-      int r = s_rank;
-      int bucket = 0;
-      while (bucket < 255 && r >= int(hist[bucket])) {
-        r -= int(hist[bucket]);
-        ++bucket;
-      }
-      s_rank = r;
-      s_prefix = prefix | ((unsigned long long)bucket << shift);
+    // The bucket holding rank r: its exclusive prefix count is <= r and its
+    // inclusive count exceeds r.
+    const int r = s_rank;
+    const int h = int(hist[tid]);
+    int total;
+    const int before = block_exclusive_scan(h, swt, total);
+    if (before <= r && r < before + h) {
+      s_rank = r - before;
+      s_prefix = prefix | ((unsigned long long)tid << shift);
     }
     mask |= 255ull << shift;
     __syncthreads();
@@ -143,6 +247,30 @@ __global__ __launch_bounds__(kKnnBlock) void knn_kernel(const float* __restrict_
     }
     out[size_t(c) * g + rank] = ia;
   }
+  __syncthreads();
+}
+
+// Rows handled by the radix select: every row (marked_only == 0) or the rows
+// whose first entry the bounding kernel set to -1.  Block b takes rows
+// b, b + gridDim.x, ...; it checks kKnnBlock of them at a time and selects the
+// ones it must redo one after another.
+__global__ __launch_bounds__(kKnnBlock) void knn_radix_kernel(const float* __restrict__ pos, int n, int g,
+                                                              int marked_only, int32_t* __restrict__ out) {
+  extern __shared__ unsigned long long keys[];
+  __shared__ int rows[kKnnBlock];
+  __shared__ int nrows;
+  const int tid = threadIdx.x;
+  const int stride = gridDim.x;
+  for (int base = blockIdx.x; base < n; base += stride * kKnnBlock) {
+    if (tid == 0) nrows = 0;
+    __syncthreads();
+    const int c = base + stride * tid;
+    if (c < n && (!marked_only || out[size_t(c) * g] == -1)) rows[atomicAdd(&nrows, 1)] = c;
+    __syncthreads();
+    const int cnt = nrows;
+    for (int r = 0; r < cnt; ++r) knn_radix_row(pos, n, g, rows[r], keys, out);
+    __syncthreads();
+  }
 }
 
 }  // namespace
@@ -151,11 +279,21 @@ static size_t knn_lds_bytes(int n, int g) { return size_t(n) * 8 + size_t(g) * 1
 
 hipError_t launch_knn(const float* pos, int n, int g, int32_t* out, hipStream_t stream) {
   if (n < 1 || n > kKnnMaxN || g < 1 || g > n || g > kKnnMaxG) return hipErrorInvalidValue;
+  hipError_t e;
+  const bool bound = g <= kBoundMaxG;
+  if (bound) {
+    knn_bound_kernel<<<(n + kQ - 1) / kQ, kKnnBlock, 0, stream>>>(pos, n, g, out);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   const size_t lds = knn_lds_bytes(n, g);
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(knn_kernel),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-  if (e != hipSuccess) return e;
-  knn_kernel<<<n, kKnnBlock, lds, stream>>>(pos, n, g, out);
+  if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(knn_radix_kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
+    return e;
+  int dev = 0, cus = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  const int grid = std::max(1, std::min(n, bound ? cus : 4 * cus));
+  knn_radix_kernel<<<grid, kKnnBlock, lds, stream>>>(pos, n, g, bound ? 1 : 0, out);
   return hipGetLastError();
 }
 

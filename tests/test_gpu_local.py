@@ -46,6 +46,8 @@ KNN_CASES = [
     ("n1024_d256_f32", None, 1, 0),        # g = 1: every token's own index
     ("n1024_d256_f32", None, 16, 1),
     ("n4096_d1152", 997, 64, 2),           # ragged: not a multiple of the block
+    ("n4096_d1152", 1000, 128, 6),         # largest g of the bounding pass
+    ("n4096_d1152", 1000, 129, 7),         # smallest g of the radix select
     ("n4096_d1152", 300, 300, 3),          # g = n: the whole scene, sorted
     ("n8192_d3584", 2048, 1024, 4),        # largest g
     ("n16384_d3584", 1, 1, 5),             # one token
@@ -81,13 +83,35 @@ def test_knn_duplicate_positions():
     assert np.array_equal(_gpu_knn(d.pos, 40), oknn.knn_ref(d.pos, 40))
 
 
+def test_knn_coincident_tokens_take_the_radix_path():
+    # Every token at one point: all distances are 0, every row is 0..g-1, and
+    # the bounding pass collects all n tokens per row, more than it keeps, so
+    # every row is redone by the radix select.
+    pos = np.full((600, 3), 1.25, np.float32)
+    print("knn coincident tokens", flush=True)
+    got = _gpu_knn(pos, 24)
+    assert np.array_equal(got, np.tile(np.arange(24), (600, 1)))
+    assert np.array_equal(got, oknn.knn_ref(pos, 24))
+
+
+def test_knn_half_coincident():
+    # Half the tokens share one point (rows there overflow the bounding pass),
+    # the rest are spread out (rows there do not).
+    s = _sub("n4096_d1152", 800, 20)
+    pos = s.pos.copy()
+    pos[::2] = pos[0]
+    print("knn half coincident", flush=True)
+    for g in (8, 64, 200):
+        assert np.array_equal(_gpu_knn(pos, g), oknn.knn_ref(pos, g))
+
+
 def test_knn_full_size_sampled_rows():
     # The 16384-token scene at the local greedy's g = 64 and at the largest g,
     # sampled rows against the oracle.
     s = make_scene("n16384_d3584", 0, dim=16)
     rng = np.random.default_rng(14)
     rows = np.sort(rng.choice(s.n, 256, replace=False))
-    for g in (64, 1024):
+    for g in (64, 128, 1024):
         print(f"knn full size n={s.n} g={g}", flush=True)
         got = _gpu_knn(s.pos, g)
         assert np.array_equal(got[rows], oknn.knn_ref(s.pos, g, rows=rows))
