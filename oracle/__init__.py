@@ -14,9 +14,11 @@ Modules
   ot       exact transport linear programs (Sec. 3.1, Eq. 2, 5, 11, 19-20) used
            only to pin the readings above on tiny inputs
   knn      3D nearest-neighbour tables M_g(t) for the local greedy (Eq. 13)
+  capacity FST capacity: neighbour discrepancy scores and their
+           normalisation (Sec. 3.4, Eq. 9-10)
 
 Readings of passages the paper leaves open are stated in each function's
 docstring; every one is also listed with its justification in the design
 notes at the repository root.
 """
-from . import fst, sgs, lite, ot, knn  # noqa: F401
+from . import fst, sgs, lite, ot, knn, capacity  # noqa: F401
