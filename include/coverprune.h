@@ -7,6 +7,8 @@
  *
  *   coverprune_fst_cost    the Feature-Spatial-Temporal transport cost between
  *                          every pair of tokens (Sec. 3.3, Eq. 7-8);
+ *   coverprune_fst_capacity the target capacities v from each token's 3D
+ *                          neighbours (Sec. 3.4, Eq. 9-10);
  *   coverprune_sgs_select  greedy selection of K tokens against that cost and
  *                          the target capacities (Sec. 3.5, Eq. 11-16);
  *   coverprune_knn         the g nearest tokens of every token in 3D, and
@@ -96,6 +98,42 @@ cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int6
                               float* cost, float* maxima, void* workspace,
                               size_t workspace_bytes, void* stream);
 
+/* Largest scene and neighbour count of the 3D nearest-neighbour tables
+ * (coverprune_knn, coverprune_fst_capacity). */
+#define CP_KNN_MAX_N 16384
+#define CP_KNN_MAX_G 1024
+
+/* ------------------------------------------------------------------------ */
+/* FST capacity (Sec. 3.4, Eq. 9-10).
+ *
+ *   r_j = (1/n) sum_{k in N_n(j)} ( alpha_f d_f(j,k)/M_f + alpha_x d_x(j,k)/M_x
+ *                                   + alpha_tau d_tau(j,k)/M_tau ),
+ *   v_j = r_j / sum_l r_l          (uniform 1/N when every r_j is 0).
+ *
+ * N_n(j) is the n tokens nearest to j in 3D other than j itself, in the
+ * (distance, index) order of coverprune_knn.  d_f = 1 - cos clamped to
+ * [0, 2] (cos = 0 for a zero-norm row), d_x the Euclidean distance,
+ * d_tau(j, k) = ReLU(tau_j - tau_k), as in the cost; each M is that term's
+ * maximum over the N * n scored pairs (a term whose maximum is 0 adds 0).
+ * phi of Eq. 10 is the identity.  Dot products, norms, scores and the sum are
+ * float64; the capacity is rounded once to float32.  Deterministic.
+ *
+ *   feats, dtype, n, d, pos, frame: as for coverprune_fst_cost, 2 <= n <= CP_KNN_MAX_N
+ *   n_nb      neighbours per token, 1 <= n_nb <= min(n - 1, CP_KNN_MAX_G - 1)
+ *   alpha     term weights, finite and >= 0 (the experiments use 1, Sec. 5.1)
+ *   capacity  [n] float output v, the input of the greedy and of Lite
+ *   score     [n] double output r (may be NULL)
+ *   workspace about (4 + 24 n_nb) bytes per token
+ */
+typedef struct {
+  float alpha_f, alpha_x, alpha_tau;
+} cp_capacity_weights;
+
+size_t coverprune_fst_capacity_workspace(int64_t n, int64_t n_nb);
+cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, int64_t d, const float* pos,
+                                  const int32_t* frame, int64_t n_nb, cp_capacity_weights alpha, float* capacity,
+                                  double* score, void* workspace, size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Spatial-Guided Greedy Selection (Sec. 3.5, Eq. 11-16).
  *
@@ -169,8 +207,6 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
  * NULL pointers return CP_ERR_INVALID_ARG before anything is enqueued.  The
  * workspace of the greedy is about 16 B per token.
  */
-#define CP_KNN_MAX_N 16384
-#define CP_KNN_MAX_G 1024
 #define CP_SGS_LOCAL_MAX_N 16384
 #define CP_SGS_LOCAL_MAX_G 128
 cp_status coverprune_knn(const float* pos, int64_t n, int64_t g, int32_t* neighbours, void* stream);

@@ -29,10 +29,12 @@ def neighbours_excluding_self(pos, n_nb: int) -> np.ndarray:
     N = np.asarray(pos).shape[0]
     if not 1 <= n_nb <= N - 1:
         raise ValueError("need 1 <= n <= N - 1")
-    table = knn.knn_ref(pos, n_nb + 1)
     out = np.empty((N, n_nb), np.int64)
-    for j in range(N):
-        out[j] = [k for k in table[j] if k != j][:n_nb]
+    for lo in range(0, N, 1024):            # row blocks only bound the memory of the distance table
+        rows = np.arange(lo, min(N, lo + 1024))
+        table = knn.knn_ref(pos, n_nb + 1, rows=rows)
+        for i, j in enumerate(rows):
+            out[j] = [k for k in table[i] if k != j][:n_nb]
     return out
 
 

@@ -14,7 +14,7 @@ from typing import Optional
 
 import torch
 
-__all__ = ["fst_cost", "sgs_select", "knn", "sgs_local_select", "lite_select", "library", "library_path", "CoverPruneError",
+__all__ = ["fst_cost", "fst_capacity", "sgs_select", "knn", "sgs_local_select", "lite_select", "library", "library_path", "CoverPruneError",
            "DEFAULT_KAPPA"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -35,6 +35,10 @@ class CoverPruneError(RuntimeError):
 class _Weights(ctypes.Structure):
     _fields_ = [("lambda_f", ctypes.c_float), ("lambda_x", ctypes.c_float),
                 ("lambda_tau", ctypes.c_float), ("kappa", ctypes.c_float)]
+
+
+class _CapWeights(ctypes.Structure):
+    _fields_ = [("alpha_f", ctypes.c_float), ("alpha_x", ctypes.c_float), ("alpha_tau", ctypes.c_float)]
 
 
 _lib = None
@@ -63,6 +67,11 @@ def library() -> ctypes.CDLL:
     lib.coverprune_sgs_workspace.restype = sz
     lib.coverprune_sgs_select.argtypes = [vp, i64, vp, i64, ctypes.c_float, u32, vp, vp, vp, vp, vp, sz, vp]
     lib.coverprune_sgs_select.restype = st
+    lib.coverprune_fst_capacity_workspace.argtypes = [i64, i64]
+    lib.coverprune_fst_capacity_workspace.restype = sz
+    lib.coverprune_fst_capacity.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, i64, _CapWeights, vp, vp, vp, sz,
+                                            vp]
+    lib.coverprune_fst_capacity.restype = st
     lib.coverprune_knn.argtypes = [vp, i64, i64, vp, vp]
     lib.coverprune_knn.restype = st
     lib.coverprune_sgs_local_workspace.argtypes = [i64, i64]
@@ -158,6 +167,34 @@ def fst_cost(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor,
                                    _ptr(out), _ptr(maxima), _ptr(workspace), workspace.numel(),
                                    _stream(stream)))
     return out, maxima
+
+
+def fst_capacity(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor, n_nb: int,
+                 alpha=(1.0, 1.0, 1.0), out: Optional[torch.Tensor] = None,
+                 score: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None, stream=None):
+    """FST capacity (Sec. 3.4, Eq. 9-10) from each token's n_nb nearest other
+    tokens.  Returns (v [n] float32 summing to 1, r [n] float64 scores)."""
+    lib = library()
+    n, d = feats.shape
+    dev = feats.device
+    dt = _feature_dtype(feats)
+    _need(feats, "feats", feats.dtype, (n, d), dev)
+    _need(pos, "pos", torch.float32, (n, 3), dev)
+    _need(frame, "frame", torch.int32, (n,), dev)
+    if out is None:
+        out = torch.empty(n, dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, (n,), dev)
+    if score is None:
+        score = torch.empty(n, dtype=torch.float64, device=dev)
+    _need(score, "score", torch.float64, (n,), dev)
+    need = lib.coverprune_fst_capacity_workspace(n, int(n_nb))
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    a_f, a_x, a_t = (float(a) for a in alpha)
+    _check(lib.coverprune_fst_capacity(_ptr(feats), dt, n, d, _ptr(pos), _ptr(frame), int(n_nb),
+                                       _CapWeights(a_f, a_x, a_t), _ptr(out), _ptr(score), _ptr(workspace),
+                                       workspace.numel(), _stream(stream)))
+    return out, score
 
 
 @dataclass

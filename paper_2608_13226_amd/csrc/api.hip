@@ -191,6 +191,46 @@ cp_status coverprune_knn(const float* pos, int64_t n, int64_t g, int32_t* neighb
   return ok();
 }
 
+size_t coverprune_fst_capacity_workspace(int64_t n, int64_t n_nb) {
+  if (n < 2 || n_nb < 1 || n_nb > n - 1) return 0;
+  return cp::capacity_workspace_bytes(n, n_nb);
+}
+
+cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, int64_t d, const float* pos,
+                                  const int32_t* frame, int64_t n_nb, cp_capacity_weights alpha, float* capacity,
+                                  double* score, void* workspace, size_t workspace_bytes, void* stream) {
+  cp_status st = check_features(feats, dtype, n, d, CP_KNN_MAX_N);
+  if (st != CP_OK) return st;
+  if (n < 2) return fail(CP_ERR_INVALID_ARG, "n = %lld: the capacity needs at least 2 tokens", (long long)n);
+  if (n_nb < 1 || n_nb > std::min<int64_t>(n - 1, CP_KNN_MAX_G - 1))
+    return fail(CP_ERR_INVALID_ARG, "n_nb = %lld outside [1, min(n - 1, %d)]", (long long)n_nb, CP_KNN_MAX_G - 1);
+  if (!pos || !frame || !capacity) return fail(CP_ERR_INVALID_ARG, "pos, frame and capacity must be non-NULL");
+  const float a[3] = {alpha.alpha_f, alpha.alpha_x, alpha.alpha_tau};
+  for (float x : a)
+    if (!std::isfinite(x) || x < 0.f) return fail(CP_ERR_INVALID_ARG, "capacity weights must be finite and >= 0");
+  if ((st = check_workspace(workspace, workspace_bytes, coverprune_fst_capacity_workspace(n, n_nb))) != CP_OK)
+    return st;
+
+  cp::CapacityParams p;
+  p.feats = feats;
+  p.bf16 = dtype == CP_BF16;
+  p.n = int(n);
+  p.d = int(d);
+  p.pos = pos;
+  p.frame = frame;
+  p.nn = int(n_nb);
+  p.alpha_f = alpha.alpha_f;
+  p.alpha_x = alpha.alpha_x;
+  p.alpha_tau = alpha.alpha_tau;
+  p.capacity = capacity;
+  p.score = score;
+  p.workspace = workspace;
+  p.workspace_bytes = workspace_bytes;
+  hipError_t e = cp::launch_capacity(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "capacity");
+  return ok();
+}
+
 size_t coverprune_sgs_local_workspace(int64_t n, int64_t k) {
   if (n < 1 || k < 1) return 0;
   return cp::sgs_local_workspace_bytes(n, k);

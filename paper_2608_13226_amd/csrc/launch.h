@@ -60,6 +60,25 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
 // Nearest-neighbour tables: out [n, g], n <= 16384, g <= min(n, 1024).
 hipError_t launch_knn(const float* pos, int n, int g, int32_t* out, hipStream_t stream);
 
+// FST capacity.
+struct CapacityParams {
+  const void* feats;
+  bool bf16;
+  int n;
+  int d;
+  const float* pos;
+  const int32_t* frame;
+  int nn;                         // neighbours per token, 1 <= nn <= n - 1
+  float alpha_f, alpha_x, alpha_tau;
+  float* capacity;                // [n]
+  double* score;                  // [n] or nullptr
+  void* workspace;
+  size_t workspace_bytes;
+};
+
+size_t capacity_workspace_bytes(int64_t n, int64_t nn);
+hipError_t launch_capacity(const CapacityParams& p, hipStream_t stream);
+
 // CoverPrune-Lite.
 struct LiteParams {
   const void* feats;

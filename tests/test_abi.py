@@ -166,3 +166,33 @@ def _local(lib, **kw):
 ])
 def test_sgs_local_rejects(lib, kw, code):
     assert _local(lib, **kw) == code
+
+
+def _cw(af=1.0, ax=1.0, at=1.0):
+    import paper_2608_13226_amd as cp
+    return cp._CapWeights(af, ax, at)
+
+
+def test_capacity_workspace_query(lib):
+    assert lib.coverprune_fst_capacity_workspace(1, 1) == 0
+    assert lib.coverprune_fst_capacity_workspace(64, 64) == 0
+    assert lib.coverprune_fst_capacity_workspace(16384, 16) >= 16384 * (4 * 17 + 24 * 16)
+
+
+def _cap(lib, **kw):
+    a = dict(feats=FAKE, dtype=1, n=64, d=64, pos=FAKE, frame=FAKE, nn=8, alpha=_cw(), v=FAKE, r=None,
+             ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return lib.coverprune_fst_capacity(a["feats"], a["dtype"], a["n"], a["d"], a["pos"], a["frame"], a["nn"],
+                                       a["alpha"], a["v"], a["r"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=1, nn=1), INVALID), (dict(n=16385), INVALID), (dict(nn=0), INVALID), (dict(nn=64), INVALID),
+    (dict(n=4096, nn=1024), INVALID), (dict(d=12), UNSUPPORTED), (dict(feats=None), INVALID),
+    (dict(pos=None), INVALID), (dict(frame=None), INVALID), (dict(v=None), INVALID),
+    (dict(alpha=_cw(af=-1.0)), INVALID), (dict(alpha=_cw(at=float("inf"))), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(ws_bytes=1000), WORKSPACE),
+])
+def test_capacity_rejects(lib, kw, code):
+    assert _cap(lib, **kw) == code
