@@ -346,6 +346,27 @@ def main():
                  "dense_objective": float(r.objective[-1].item()),
                  "picks_shared_with_dense": int(len(set(lsel.tolist()) & set(sel.tolist())))}
 
+    # FST capacity (Eq. 9-10) from 16 neighbours per token, timed on its own:
+    # the workload's capacities are an input of the step.
+    cap = None
+    if n <= 16384:
+        n_nb = 16
+        ws_c = torch.empty(lib.coverprune_fst_capacity_workspace(n, n_nb), dtype=torch.uint8, device=dev)
+        v_out = torch.empty(n, dtype=torch.float32, device=dev)
+        r_out = torch.empty(n, dtype=torch.float64, device=dev)
+        reps = 3
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+        for i in range(reps):
+            e[2 * i].record()
+            cp.fst_capacity(t["feats"], t["pos"], t["frame"], n_nb, out=v_out, score=r_out, workspace=ws_c)
+            e[2 * i + 1].record()
+        torch.cuda.synchronize()
+        cap_ms = float(np.mean([e[2 * i].elapsed_time(e[2 * i + 1]) for i in range(reps)]))
+        # Gathered feature rows: one neighbour row per scored pair.
+        gather = float(n) * n_nb * d * (2 if scene.dtype == "bf16" else 4)
+        cap = {"n_nb": n_nb, "ms": round(cap_ms, 3), "gathered_row_bytes": gather,
+               "gathered_gbs": round(gather / (cap_ms * 1e-3) / 1e9, 1)}
+
     # FST cost: symmetric Gram needs N (N + 1) D flops; the whole call (prep,
     # Gram, epilogue) is timed, so this fraction is a lower bound for the Gram.
     gram_flops = float(n) * (n + 1) * d
@@ -374,6 +395,7 @@ def main():
             "sgs_dense_sweep": dense,
             "sgs_dense_same_picks": same,
             "sgs_local": local,
+            "fst_capacity": cap,
             "lite_select_ms": round(l_ms, 3),
             "coverprune_ms_per_scene": round(f_ms + s_ms, 3),
             "coverprune_lite_ms_per_scene": round(l_ms, 3),
