@@ -98,12 +98,16 @@ def traffic(kernel, workload):
             if ":" in line and not line.startswith("#"):
                 key, val = line.split(":", 1)
                 rec[key.strip()] = val.strip()
-    src = os.path.join(ROOT, rec.get("source", ""))
-    if not os.path.isfile(src):
-        return None
-    with open(src, "rb") as fh:
-        if hashlib.sha256(fh.read()).hexdigest() != rec.get("source_sha256"):
+    # One source file, or several separated by commas (hashed in that order).
+    h = hashlib.sha256()
+    for name in rec.get("source", "").split(","):
+        src = os.path.join(ROOT, name.strip())
+        if not name.strip() or not os.path.isfile(src):
             return None
+        with open(src, "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != rec.get("source_sha256"):
+        return None
     return float(rec["traffic_bytes_per_launch"])
 
 

@@ -32,270 +32,20 @@
 //      256-byte read per row and 64 columns); block 0 also applies them to the
 //      objective, kept in the same fixed point;
 //   4. it publishes the exact argmax of its unchosen columns.
-// The exchanges are per-block slots rather than counters: a slot holds the
-// value together with the step it belongs to, every block reads all slots in
-// parallel (one thread per slot), and no address takes more than one writer,
-// so a step costs two round trips through memory instead of two grid
-// barriers of serialized atomic increments.  Slots, lists and lengths are
-// written and read with device-scope atomic operations, coherent across the
-// chip's L2 caches without fences; a block's list writes are complete at the
-// workgroup barrier before its thread 0 publishes the length.  A slot is only
-// rewritten after every block has read it: a block can publish step l + 1's
-// values only after reading every block's step-l + 1 candidate, which each
-// block publishes only after it has consumed step l.
+//
+// The exchanges and the fixed point are in sgs_exchange.h.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <climits>
 
-#include "common.h"
-#include "launch.h"
+#include "sgs_exchange.h"
 
 namespace cp {
 namespace {
 
-constexpr int kBlock = 512;
-constexpr int kWaves = kBlock / 64;
-constexpr int kMaxBlocks = 256;    // at most one block per compute unit
 constexpr int kBatch = 64;         // change-list entries a wave fetches per round
 constexpr int kChunk = 16;         // of which the rows read together
 constexpr int kInitRows = 16;      // rows a wave has in flight in the full pass
-constexpr int kIndexBits = 20;     // candidate: [epoch | 43-bit gain | 20-bit inverted index]
-constexpr unsigned long long kIndexMask = (1ull << kIndexBits) - 1ull;
-constexpr unsigned long long kEpoch = 1ull << 63;
-constexpr unsigned long long kNoCandidate = 1ull;   // below every real candidate
-// Every wait in the kernel is bounded: about a second of polling (far beyond
-// any legitimate wait) raises the abort flag, after which every block leaves
-// its waits and returns, and selected[] is filled with -1.
-constexpr unsigned int kSpinLimit = 1u << 22;
-
-// Fixed-point value of a nonnegative term: floor(t 2^S) in 128 bits, read
-// off the bits of the double t 2^S (exact: a power-of-two scaling) with one
-// 64-bit shift; t 2^S < 2^102.  Negative, zero and subnormal-range values
-// give 0.
-__device__ __forceinline__ __int128 fx(double t, int S) {
-  const unsigned long long b = (unsigned long long)__double_as_longlong(__builtin_ldexp(t, S));
-  const int E = int(b >> 52) & 0x7ff;
-  if ((b >> 63) || E < 1023) return 0;                       // negative, or below 1
-  const unsigned long long m = (b & ((1ull << 52) - 1ull)) | (1ull << 52);
-  const int sh = E - 1075;                                    // value = m 2^sh, sh <= 49
-  if (sh <= 0) return (__int128)(m >> -sh);
-  return ((__int128)(m >> (64 - sh)) << 64) | (__int128)(m << sh);
-}
-
-__device__ __forceinline__ double fx_to_double(__int128 g, int S) {
-  const double x = (double)(long long)(g >> 64) * 0x1p64 + (double)(unsigned long long)g;
-  return __builtin_ldexp(x, -S);
-}
-
-struct IncDev {
-  const float* C;
-  const float* v;
-  int n, k;
-  float c0;
-  int32_t* selected;
-  double* step_gain;
-  double* step_obj;
-  int32_t* assign;
-  unsigned long long* list;   // [blocks][W][2]: (row | v << 32), (old b | new b << 32)
-  unsigned long long* lens;   // [blocks] (step + 1) << 32 | slice length
-  unsigned long long* cand;   // [2][blocks] packed candidate | epoch << 63
-  unsigned int* abort;        // set when a wait exceeds kSpinLimit polls
-  int W;                      // rows and columns per block
-};
-
-struct Layout {
-  size_t list, lens, cand, ctrl, total;
-};
-
-size_t a256(size_t x) { return (x + 255) / 256 * 256; }
-
-int blocks_for(int64_t n, int cus) {
-  return int(std::max<int64_t>(1, std::min<int64_t>(std::min(cus, kMaxBlocks), (n + 63) / 64)));
-}
-
-// Sized for the largest grid (kMaxBlocks blocks of W = ceil(n / blocks) rows).
-Layout layout(int64_t n, int64_t k) {
-  (void)k;
-  Layout L;
-  size_t o = 0;
-  L.list = o; o += a256(size_t(n + kMaxBlocks) * 16);
-  L.lens = o; o += a256(size_t(kMaxBlocks) * 8);
-  L.cand = o; o += a256(size_t(2 * kMaxBlocks) * 8);
-  L.ctrl = o; o += 256;
-  L.total = o;
-  return L;
-}
-
-// Nonnegative gain truncated to its top 43 bits (relative resolution 2^-31),
-// then the inverted index: larger gain first, then smaller index.  Indices
-// are below 2^18, so every real candidate exceeds kNoCandidate.
-__device__ __forceinline__ unsigned long long pack_key(double g, int idx) {
-  const unsigned long long gb = (unsigned long long)__double_as_longlong(g) >> (kIndexBits + 1);
-  return (gb << kIndexBits) | (kIndexMask - (unsigned long long)idx);
-}
-
-// Epoch bit of the candidates for step l, kept in slot set l % 2: it flips
-// between consecutive uses of a set and is never the zero of a fresh
-// workspace for steps 0 and 1.
-__device__ __forceinline__ unsigned long long epoch_of(int step) {
-  return ((step >> 1) & 1) ? 0ull : kEpoch;
-}
-
-__global__ void sgs_inc_init_kernel(IncDev a) {
-  const int gt = blockIdx.x * blockDim.x + threadIdx.x, nt = gridDim.x * blockDim.x;
-  for (int s = gt; s < kMaxBlocks; s += nt) {
-    a.lens[s] = 0ull;
-    a.cand[s] = 0ull;
-    a.cand[kMaxBlocks + s] = 0ull;
-  }
-  for (int j = gt; j < a.n; j += nt)
-    if (a.assign) a.assign[j] = -1;
-  if (gt == 0) *a.abort = 0u;
-}
-
-// Sum over the block of 128-bit integers, result in every thread.
-__device__ __int128 block_sum_i128(__int128 x, __int128* sg) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const unsigned long long lo = __shfl_xor((unsigned long long)x, o);
-    const long long hi = __shfl_xor((long long)(x >> 64), o);
-    x += ((__int128)hi << 64) | (__int128)lo;
-  }
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) sg[w] = x;
-  __syncthreads();
-  __int128 s = 0;
-#pragma unroll
-  for (int q = 0; q < kWaves; ++q) s += sg[q];
-  __syncthreads();
-  return s;
-}
-
-// Poll *p until pred(value) holds; false if the launch is aborting (this
-// wait timed out, or another one did).
-template <class Pred>
-__device__ bool wait_slot(const unsigned long long* p, unsigned int* abort, Pred pred, unsigned long long& x) {
-  for (unsigned int spins = 0;; ++spins) {
-    x = get(p);
-    if (pred(x)) return true;
-    if ((spins & 63u) == 63u) {
-      if (get(abort)) return false;
-      if (spins > kSpinLimit) {
-        put(abort, 1u);
-        return false;
-      }
-    }
-    __builtin_amdgcn_s_sleep(1);
-  }
-}
-
-// Inclusive prefix sum over the block (thread order), result in every thread.
-__device__ int block_inclusive_scan(int x, int* swt) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) swt[w] = x;
-  __syncthreads();
-#pragma unroll
-  for (int q = 0; q < kWaves; ++q)
-    if (q < w) x += swt[q];
-  __syncthreads();
-  return x;
-}
-
-// Fixed-order block sum, result in every thread.
-__device__ double block_sum_all(double x, double* sd) {
-  x = wave_sum(x);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) sd[w] = x;
-  __syncthreads();
-  double s = 0.0;
-#pragma unroll
-  for (int q = 0; q < kWaves; ++q) s += sd[q];
-  __syncthreads();
-  return s;
-}
-
-// Exact argmax (ties to the smaller index) of the block's unchosen columns,
-// published as the block's candidate for the step; across blocks the gains
-// compare as doubles truncated to 43 bits.
-__device__ void publish_argmax(const unsigned long long* sGlo, const long long* sGhi, const unsigned char* ssel,
-                               int lo, int cnt, int S, unsigned long long* slot, unsigned long long epoch,
-                               __int128* sg, int* si) {
-  __int128 g = -1;
-  int gi = INT_MAX;
-  for (int i = threadIdx.x; i < cnt; i += kBlock)
-    if (!ssel[i]) {
-      const __int128 x = ((__int128)sGhi[i] << 64) | (__int128)sGlo[i];
-      if (x > g || (x == g && lo + i < gi)) {
-        g = x;
-        gi = lo + i;
-      }
-    }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const unsigned long long olo = __shfl_xor((unsigned long long)g, o);
-    const long long ohi = __shfl_xor((long long)(g >> 64), o);
-    const int oi = __shfl_xor(gi, o);
-    const __int128 og = ((__int128)ohi << 64) | (__int128)olo;
-    if (og > g || (og == g && oi < gi)) {
-      g = og;
-      gi = oi;
-    }
-  }
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (lane == 0) {
-    sg[w] = g;
-    si[w] = gi;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int q = 1; q < kWaves; ++q)
-      if (sg[q] > g || (sg[q] == g && si[q] < gi)) {
-        g = sg[q];
-        gi = si[q];
-      }
-    put(slot, (gi != INT_MAX ? pack_key(fx_to_double(g, S), gi) : kNoCandidate) | epoch);
-  }
-  __syncthreads();
-}
-
-// The step's winner: thread i < nb waits for block i's candidate of this
-// epoch; the largest wins (the same in every block).  Returns -1 when the
-// launch is aborting.
-__device__ int read_winner(const unsigned long long* slots, unsigned long long epoch, int nb,
-                           unsigned int* abort, unsigned long long* su, int* sflag) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  unsigned long long best = 0ull;
-  if (tid == 0) *sflag = 0;
-  __syncthreads();
-  if (tid < nb) {
-    unsigned long long x;
-    if (wait_slot(slots + tid, abort, [epoch](unsigned long long v) { return (v & kEpoch) == epoch; }, x))
-      best = x & ~kEpoch;
-    else
-      *sflag = 1;
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const unsigned long long y = __shfl_xor(best, o);
-    best = y > best ? y : best;
-  }
-  if (lane == 0) su[w] = best;
-  __syncthreads();
-  unsigned long long m = su[0];
-#pragma unroll
-  for (int q = 1; q < kWaves; ++q) m = su[q] > m ? su[q] : m;
-  const bool aborting = *sflag != 0;
-  __syncthreads();
-  return aborting ? -1 : int(kIndexMask - (m & kIndexMask));
-}
 
 __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
   extern __shared__ unsigned long long smem[];
@@ -540,204 +290,6 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
     for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
 }
 
-// ---------------------------------------------------------------------------
-// Local form (Eq. 13): a candidate's gain runs over its g nearest targets
-// only, gain(c) = sum_{j in M_g(c)} v_j max(0, b_j - C(c, j)), while a pick
-// still lowers the best cost of every target (the residual is over all
-// targets, Eq. 14).  Same exchanges as above; each block keeps every
-// target's best cost in LDS (updated from the whole change list each step),
-// its candidates' neighbour lists and costs C(c, j) for j in M_g(c) in LDS,
-// and sums its candidates' local gains afresh each step in the same fixed
-// point.  n <= kLocalMaxN, g <= kLocalMaxG.
-constexpr int kLocalMaxN = 16384;
-constexpr int kLocalMaxG = 128;
-
-__global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32_t* __restrict__ nbr, int g) {
-  extern __shared__ unsigned long long smem[];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int blk = blockIdx.x, nb = gridDim.x;
-  const int lo = blk * a.W;
-  const int cnt = max(0, min(a.n, lo + a.W) - lo);
-  unsigned long long* sGlo = smem;                                 // [W] gains, low words
-  long long* sGhi = reinterpret_cast<long long*>(sGlo + a.W);      // [W] high words
-  float* sball = reinterpret_cast<float*>(sGhi + a.W);             // [n] best cost of every target
-  float* scg = sball + a.n;                                        // [W][g] C(c, j), j in M_g(c)
-  int* snb = reinterpret_cast<int*>(scg + size_t(a.W) * g);        // [W][g] M_g(c)
-  unsigned char* ssel = reinterpret_cast<unsigned char*>(snb + size_t(a.W) * g);   // [W]
-  __shared__ __int128 red[kBlock];
-  __shared__ __int128 sg[kWaves];
-  __shared__ double sd[kWaves];
-  __shared__ int si[kWaves];
-  __shared__ int swt[kWaves];
-  __shared__ unsigned long long su[kWaves];
-  __shared__ int spre[kMaxBlocks + 1];
-  __shared__ int sflag;
-
-  for (int j = tid; j < a.n; j += kBlock) sball[j] = a.c0;
-  for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
-  // The band of the own candidates: neighbour lists and C(c, j) = C_tm[j][c]
-  // (indices clamped into range; the table is the caller's).
-  for (int e = tid; e < cnt * g; e += kBlock) {
-    const int i = e / g;
-    const int j = min(max(nbr[size_t(lo + i) * g + (e - i * g)], 0), a.n - 1);
-    snb[e] = j;
-    scg[e] = a.C[size_t(j) * a.n + lo + i];
-  }
-
-  double vsum;
-  {
-    double x = 0.0;
-    for (int j = tid; j < a.n; j += kBlock) x += double(a.v[j]);
-    vsum = block_sum_all(x, sd);
-  }
-  const double M = double(a.c0) * vsum;
-  int S = 0;
-  if (M > 0.0) {
-    int e = 0;
-    (void)__builtin_frexp(M, &e);
-    S = 101 - e;
-  }
-
-  __int128 L = 0;
-  if (blk == 0) {
-    __int128 x = 0;
-    for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
-    L = block_sum_i128(x, sg);
-  }
-
-  // Local gains of the own candidates from the current best costs: lane =
-  // candidate within a chunk of 64, waves split the neighbour list.
-  const int qper = (g + kWaves - 1) / kWaves;
-  auto local_gains = [&]() {
-    __syncthreads();
-    for (int cc = 0; cc < cnt; cc += 64) {
-      const int i = cc + lane;
-      __int128 gsum = 0;
-      if (i < cnt) {
-        const int q1 = min(g, (w + 1) * qper);
-        for (int q = w * qper; q < q1; ++q) {
-          const int j = snb[i * g + q];
-          const double d = double(sball[j]) - double(scg[i * g + q]);
-          if (d > 0.0) gsum += fx(double(a.v[j]) * d, S);
-        }
-      }
-      red[tid] = gsum;
-      __syncthreads();
-      if (tid < 64 && cc + tid < cnt) {
-        __int128 s = 0;
-#pragma unroll
-        for (int q = 0; q < kWaves; ++q) s += red[q * 64 + tid];
-        sGlo[cc + tid] = (unsigned long long)s;
-        sGhi[cc + tid] = (long long)(s >> 64);
-      }
-      __syncthreads();
-    }
-  };
-
-  local_gains();
-  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + blk, epoch_of(0), sg, si);
-
-  for (int step = 0; step < a.k; ++step) {
-    const int tw = read_winner(a.cand + (step & 1) * kMaxBlocks, epoch_of(step), nb, a.abort, su, &sflag);
-    if (tw < 0) break;
-    const int t = min(tw, a.n - 1);
-    if (t >= lo && t < lo + cnt && tid == 0) {
-      ssel[t - lo] = 1;
-      a.selected[step] = t;
-      if (a.step_gain) a.step_gain[step] = fx_to_double(((__int128)sGhi[t - lo] << 64) | (__int128)sGlo[t - lo], S);
-    }
-
-    // 1. Own targets that the pick improves, into the block's slice.
-    int base = 0;
-    unsigned long long* mine = a.list + size_t(blk) * a.W * 2;
-    for (int i0 = 0; i0 < cnt; i0 += kBlock) {
-      const int i = i0 + tid;
-      float cv = 0.f, bo = 0.f;
-      bool hit = false;
-      if (i < cnt) {
-        cv = a.C[size_t(lo + i) * a.n + t];
-        bo = sball[lo + i];
-        hit = cv < bo;
-      }
-      const unsigned long long m = __ballot(hit);
-      const int rank = __popcll(m & ((1ull << lane) - 1ull));
-      if (lane == 0) swt[w] = __popcll(m);
-      __syncthreads();
-      int off = base, tot = 0;
-#pragma unroll
-      for (int q = 0; q < kWaves; ++q) {
-        if (q < w) off += swt[q];
-        tot += swt[q];
-      }
-      if (hit) {
-        const int slot = off + rank;
-        put(mine + size_t(slot) * 2,
-            (unsigned long long)(unsigned int)(lo + i) | ((unsigned long long)__float_as_uint(a.v[lo + i]) << 32));
-        put(mine + size_t(slot) * 2 + 1,
-            (unsigned long long)__float_as_uint(bo) | ((unsigned long long)__float_as_uint(cv) << 32));
-        if (a.assign) a.assign[lo + i] = t;
-      }
-      base += tot;
-      __syncthreads();
-    }
-    if (tid == 0) put(a.lens + blk, ((unsigned long long)(step + 1) << 32) | unsigned(base));
-    if (step + 1 == a.k && blk != 0) break;
-
-    // 2. Every block's slice length, then every change applied to the
-    // replicated best costs (and, in block 0, to the objective).
-    {
-      if (tid == 0) sflag = 0;
-      __syncthreads();
-      int c = 0;
-      if (tid < nb) {
-        unsigned long long x;
-        const unsigned int round = unsigned(step + 1);
-        if (wait_slot(a.lens + tid, a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
-          c = int(x & 0xffffffffull);
-        else
-          sflag = 1;
-      }
-      const int incl = block_inclusive_scan(c, swt);
-      if (tid < nb) spre[tid + 1] = incl;
-      if (tid == 0) spre[0] = 0;
-      __syncthreads();
-    }
-    if (sflag) break;
-    const int total = spre[nb];
-    __int128 dobj = 0;
-    for (int e = tid; e < total; e += kBlock) {
-      int s0 = 0, s1 = nb;   // spre[s0] <= e < spre[s1]
-      while (s1 - s0 > 1) {
-        const int mid = (s0 + s1) >> 1;
-        if (spre[mid] <= e) s0 = mid;
-        else s1 = mid;
-      }
-      const unsigned long long* src = a.list + (size_t(s0) * a.W + size_t(e - spre[s0])) * 2;
-      const unsigned long long h0 = get(src), h1 = get(src + 1);
-      const int j = int(h0 & 0xffffffffull);
-      const float bn = __uint_as_float(unsigned(h1 >> 32));
-      sball[j] = bn;
-      if (blk == 0) {
-        const double vj = double(__uint_as_float(unsigned(h0 >> 32)));
-        dobj += fx(vj * double(bn), S) - fx(vj * double(__uint_as_float(unsigned(h1 & 0xffffffffull))), S);
-      }
-    }
-    if (blk == 0) {
-      L += block_sum_i128(dobj, sg);
-      if (tid == 0 && a.step_obj) a.step_obj[step] = fx_to_double(L, S);
-    }
-
-    // 3. Fresh local gains and this block's candidate for the next step.
-    if (step + 1 < a.k) {
-      local_gains();
-      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + ((step + 1) & 1) * kMaxBlocks + blk,
-                     epoch_of(step + 1), sg, si);
-    }
-  }
-  if (blk == 0 && get(a.abort))
-    for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
-}
-
 }  // namespace
 
 size_t sgs_inc_workspace_bytes(int64_t n, int64_t k) { return layout(n, k).total; }
@@ -778,55 +330,6 @@ hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream) {
   if ((e = hipGetLastError()) != hipSuccess) return e;
   void* args[] = {&a};
   return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_inc_kernel), dim3(nb), dim3(kBlock), args,
-                                    lds, stream);
-}
-
-}  // namespace cp
-
-namespace cp {
-
-size_t sgs_local_workspace_bytes(int64_t n, int64_t k) { return sgs_inc_workspace_bytes(n, k); }
-
-hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipStream_t stream) {
-  if (p.n < 1 || p.n > kLocalMaxN || g < 1 || g > p.n || g > kLocalMaxG) return hipErrorInvalidValue;
-  int dev = 0, cus = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-  const int nb = blocks_for(p.n, cus);
-  const int W = (p.n + nb - 1) / nb;
-  const size_t lds = size_t(W) * 16 + size_t(p.n) * 4 + size_t(W) * g * 8 + size_t(W) + 16;
-  if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(sgs_local_kernel),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
-    return e;
-  int per_cu = 0;
-  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(sgs_local_kernel),
-                                                        kBlock, lds)) != hipSuccess)
-    return e;
-  if (per_cu < 1) return hipErrorCooperativeLaunchTooLarge;
-
-  const Layout L = layout(p.n, p.k);
-  char* w = static_cast<char*>(p.workspace);
-  IncDev a;
-  a.C = p.cost;
-  a.v = p.capacity;
-  a.n = p.n;
-  a.k = p.k;
-  a.c0 = p.c0;
-  a.selected = p.selected;
-  a.step_gain = p.step_gain;
-  a.step_obj = p.step_objective;
-  a.assign = p.assign;
-  a.list = reinterpret_cast<unsigned long long*>(w + L.list);
-  a.lens = reinterpret_cast<unsigned long long*>(w + L.lens);
-  a.cand = reinterpret_cast<unsigned long long*>(w + L.cand);
-  a.abort = reinterpret_cast<unsigned int*>(w + L.ctrl);
-  a.W = W;
-
-  sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  void* args[] = {&a, const_cast<int32_t**>(&nbr), &g};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_local_kernel), dim3(nb), dim3(kBlock), args,
                                     lds, stream);
 }
 

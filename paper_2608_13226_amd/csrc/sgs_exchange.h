@@ -1,0 +1,270 @@
+// Shared parts of the persistent greedy kernels that keep their gains in
+// exact fixed point: the incremental form (k_sgs_inc.hip) and the local form
+// (k_sgs_local.hip), Sec. 3.5.  Both run one cooperative launch of one block
+// per compute unit; block b owns tokens [b W, (b + 1) W).
+//
+// The exchanges are per-block slots rather than counters: a slot holds the
+// value together with the step it belongs to, every block reads all slots in
+// parallel (one thread per slot), and no address takes more than one writer,
+// so a step costs two round trips through memory instead of two grid
+// barriers of serialized atomic increments.  Slots, lists and lengths are
+// written and read with device-scope atomic operations, coherent across the
+// chip's L2 caches without fences; a block's list writes are complete at the
+// workgroup barrier before its thread 0 publishes the length.  A slot is only
+// rewritten after every block has read it: a block can publish step l + 1's
+// values only after reading every block's step-l + 1 candidate, which each
+// block publishes only after it has consumed step l.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <climits>
+
+#include "common.h"
+#include "launch.h"
+
+namespace cp {
+namespace {
+
+constexpr int kBlock = 512;
+constexpr int kWaves = kBlock / 64;
+constexpr int kMaxBlocks = 256;    // at most one block per compute unit
+constexpr int kIndexBits = 20;     // candidate: [epoch | 43-bit gain | 20-bit inverted index]
+constexpr unsigned long long kIndexMask = (1ull << kIndexBits) - 1ull;
+constexpr unsigned long long kEpoch = 1ull << 63;
+constexpr unsigned long long kNoCandidate = 1ull;   // below every real candidate
+// Every wait in the kernel is bounded: about a second of polling (far beyond
+// any legitimate wait) raises the abort flag, after which every block leaves
+// its waits and returns, and selected[] is filled with -1.
+constexpr unsigned int kSpinLimit = 1u << 22;
+
+// Fixed-point value of a nonnegative term: floor(t 2^S) in 128 bits, read
+// off the bits of the double t 2^S (exact: a power-of-two scaling) with one
+// 64-bit shift; t 2^S < 2^102.  Negative, zero and subnormal-range values
+// give 0.
+__device__ __forceinline__ __int128 fx(double t, int S) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(__builtin_ldexp(t, S));
+  const int E = int(b >> 52) & 0x7ff;
+  if ((b >> 63) || E < 1023) return 0;                       // negative, or below 1
+  const unsigned long long m = (b & ((1ull << 52) - 1ull)) | (1ull << 52);
+  const int sh = E - 1075;                                    // value = m 2^sh, sh <= 49
+  if (sh <= 0) return (__int128)(m >> -sh);
+  return ((__int128)(m >> (64 - sh)) << 64) | (__int128)(m << sh);
+}
+
+__device__ __forceinline__ double fx_to_double(__int128 g, int S) {
+  const double x = (double)(long long)(g >> 64) * 0x1p64 + (double)(unsigned long long)g;
+  return __builtin_ldexp(x, -S);
+}
+
+struct IncDev {
+  const float* C;
+  const float* v;
+  int n, k;
+  float c0;
+  int32_t* selected;
+  double* step_gain;
+  double* step_obj;
+  int32_t* assign;
+  unsigned long long* list;   // [blocks][W][2]: (row | v << 32), (old b | new b << 32)
+  unsigned long long* lens;   // [blocks] (step + 1) << 32 | slice length
+  unsigned long long* cand;   // [2][blocks] packed candidate | epoch << 63
+  unsigned int* abort;        // set when a wait exceeds kSpinLimit polls
+  int W;                      // rows and columns per block
+};
+
+struct Layout {
+  size_t list, lens, cand, ctrl, total;
+};
+
+size_t a256(size_t x) { return (x + 255) / 256 * 256; }
+
+int blocks_for(int64_t n, int cus) {
+  return int(std::max<int64_t>(1, std::min<int64_t>(std::min(cus, kMaxBlocks), (n + 63) / 64)));
+}
+
+// Sized for the largest grid (kMaxBlocks blocks of W = ceil(n / blocks) rows).
+Layout layout(int64_t n, int64_t k) {
+  (void)k;
+  Layout L;
+  size_t o = 0;
+  L.list = o; o += a256(size_t(n + kMaxBlocks) * 16);
+  L.lens = o; o += a256(size_t(kMaxBlocks) * 8);
+  L.cand = o; o += a256(size_t(2 * kMaxBlocks) * 8);
+  L.ctrl = o; o += 256;
+  L.total = o;
+  return L;
+}
+
+// Nonnegative gain truncated to its top 43 bits (relative resolution 2^-31),
+// then the inverted index: larger gain first, then smaller index.  Indices
+// are below 2^18, so every real candidate exceeds kNoCandidate.
+__device__ __forceinline__ unsigned long long pack_key(double g, int idx) {
+  const unsigned long long gb = (unsigned long long)__double_as_longlong(g) >> (kIndexBits + 1);
+  return (gb << kIndexBits) | (kIndexMask - (unsigned long long)idx);
+}
+
+// Epoch bit of the candidates for step l, kept in slot set l % 2: it flips
+// between consecutive uses of a set and is never the zero of a fresh
+// workspace for steps 0 and 1.
+__device__ __forceinline__ unsigned long long epoch_of(int step) {
+  return ((step >> 1) & 1) ? 0ull : kEpoch;
+}
+
+__global__ void sgs_inc_init_kernel(IncDev a) {
+  const int gt = blockIdx.x * blockDim.x + threadIdx.x, nt = gridDim.x * blockDim.x;
+  for (int s = gt; s < kMaxBlocks; s += nt) {
+    a.lens[s] = 0ull;
+    a.cand[s] = 0ull;
+    a.cand[kMaxBlocks + s] = 0ull;
+  }
+  for (int j = gt; j < a.n; j += nt)
+    if (a.assign) a.assign[j] = -1;
+  if (gt == 0) *a.abort = 0u;
+}
+
+// Sum over the block of 128-bit integers, result in every thread.
+__device__ __int128 block_sum_i128(__int128 x, __int128* sg) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const unsigned long long lo = __shfl_xor((unsigned long long)x, o);
+    const long long hi = __shfl_xor((long long)(x >> 64), o);
+    x += ((__int128)hi << 64) | (__int128)lo;
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sg[w] = x;
+  __syncthreads();
+  __int128 s = 0;
+#pragma unroll
+  for (int q = 0; q < kWaves; ++q) s += sg[q];
+  __syncthreads();
+  return s;
+}
+
+// Poll *p until pred(value) holds; false if the launch is aborting (this
+// wait timed out, or another one did).
+template <class Pred>
+__device__ bool wait_slot(const unsigned long long* p, unsigned int* abort, Pred pred, unsigned long long& x) {
+  for (unsigned int spins = 0;; ++spins) {
+    x = get(p);
+    if (pred(x)) return true;
+    if ((spins & 63u) == 63u) {
+      if (get(abort)) return false;
+      if (spins > kSpinLimit) {
+        put(abort, 1u);
+        return false;
+      }
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+// Inclusive prefix sum over the block (thread order), result in every thread.
+__device__ int block_inclusive_scan(int x, int* swt) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) swt[w] = x;
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < kWaves; ++q)
+    if (q < w) x += swt[q];
+  __syncthreads();
+  return x;
+}
+
+// Fixed-order block sum, result in every thread.
+__device__ double block_sum_all(double x, double* sd) {
+  x = wave_sum(x);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sd[w] = x;
+  __syncthreads();
+  double s = 0.0;
+#pragma unroll
+  for (int q = 0; q < kWaves; ++q) s += sd[q];
+  __syncthreads();
+  return s;
+}
+
+// Exact argmax (ties to the smaller index) of the block's unchosen columns,
+// published as the block's candidate for the step; across blocks the gains
+// compare as doubles truncated to 43 bits.
+__device__ void publish_argmax(const unsigned long long* sGlo, const long long* sGhi, const unsigned char* ssel,
+                               int lo, int cnt, int S, unsigned long long* slot, unsigned long long epoch,
+                               __int128* sg, int* si) {
+  __int128 g = -1;
+  int gi = INT_MAX;
+  for (int i = threadIdx.x; i < cnt; i += kBlock)
+    if (!ssel[i]) {
+      const __int128 x = ((__int128)sGhi[i] << 64) | (__int128)sGlo[i];
+      if (x > g || (x == g && lo + i < gi)) {
+        g = x;
+        gi = lo + i;
+      }
+    }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const unsigned long long olo = __shfl_xor((unsigned long long)g, o);
+    const long long ohi = __shfl_xor((long long)(g >> 64), o);
+    const int oi = __shfl_xor(gi, o);
+    const __int128 og = ((__int128)ohi << 64) | (__int128)olo;
+    if (og > g || (og == g && oi < gi)) {
+      g = og;
+      gi = oi;
+    }
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) {
+    sg[w] = g;
+    si[w] = gi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < kWaves; ++q)
+      if (sg[q] > g || (sg[q] == g && si[q] < gi)) {
+        g = sg[q];
+        gi = si[q];
+      }
+    put(slot, (gi != INT_MAX ? pack_key(fx_to_double(g, S), gi) : kNoCandidate) | epoch);
+  }
+  __syncthreads();
+}
+
+// The step's winner: thread i < nb waits for block i's candidate of this
+// epoch; the largest wins (the same in every block).  Returns -1 when the
+// launch is aborting.
+__device__ int read_winner(const unsigned long long* slots, unsigned long long epoch, int nb,
+                           unsigned int* abort, unsigned long long* su, int* sflag) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  unsigned long long best = 0ull;
+  if (tid == 0) *sflag = 0;
+  __syncthreads();
+  if (tid < nb) {
+    unsigned long long x;
+    if (wait_slot(slots + tid, abort, [epoch](unsigned long long v) { return (v & kEpoch) == epoch; }, x))
+      best = x & ~kEpoch;
+    else
+      *sflag = 1;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const unsigned long long y = __shfl_xor(best, o);
+    best = y > best ? y : best;
+  }
+  if (lane == 0) su[w] = best;
+  __syncthreads();
+  unsigned long long m = su[0];
+#pragma unroll
+  for (int q = 1; q < kWaves; ++q) m = su[q] > m ? su[q] : m;
+  const bool aborting = *sflag != 0;
+  __syncthreads();
+  return aborting ? -1 : int(kIndexMask - (m & kIndexMask));
+}
+
+}  // namespace
+}  // namespace cp
