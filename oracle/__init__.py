@@ -16,9 +16,11 @@ Modules
   knn      3D nearest-neighbour tables M_g(t) for the local greedy (Eq. 13)
   capacity FST capacity: neighbour discrepancy scores and their
            normalisation (Sec. 3.4, Eq. 9-10)
+  literal  the greedy step as written: entropic semi-relaxed transport per
+           step, residual capacity, residual-weighted score (Sec. 3.5, Eq. 11-15)
 
 Readings of passages the paper leaves open are stated in each function's
 docstring; every one is also listed with its justification in the design
 notes at the repository root.
 """
-from . import fst, sgs, lite, ot, knn, capacity  # noqa: F401
+from . import fst, sgs, lite, ot, knn, capacity, literal  # noqa: F401
