@@ -14,6 +14,8 @@
  *   coverprune_knn         the g nearest tokens of every token in 3D, and
  *   coverprune_sgs_local_select  the greedy with gains over those neighbours
  *                          only (Sec. 3.5, Eq. 13);
+ *   coverprune_sgs_literal_select  the greedy with each step's transport
+ *                          solved as written (Sec. 3.5, Eq. 11-15);
  *   coverprune_lite_select CoverPrune-Lite: Morton ordering, capacity-guided
  *                          grouping and per-group prototypes (Sec. 4, Eq. 17-20).
  *
@@ -216,6 +218,50 @@ cp_status coverprune_sgs_local_select(const float* cost, int64_t n, const float*
                                       int32_t* selected, double* step_gain, double* step_objective,
                                       int32_t* assign, void* workspace, size_t workspace_bytes,
                                       void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* The greedy step solved as written (Sec. 3.5, Eq. 11-15).
+ *
+ * Where coverprune_sgs_select reads each step's transport in its
+ * epsilon -> 0, free-source limit, this call solves it: step l retains
+ * S_l = {s_0 .. s_{l-1}} with source mass u = 1/k each and solves the
+ * entropic semi-relaxed transport of Eq. 12 (P 1 = u, P^T 1 <= v) by
+ * alternating scalings P = diag(a) E diag(b), E = exp(-C_S / epsilon):
+ *   a <- u / (E b),   b <- min(1, v / (E^T a))   (b_j = 1 where E^T a is 0),
+ * from b = 1, for `rounds` rounds.  The residual r = [v - P^T 1]_+ (Eq. 14)
+ * weights the score sum_j r_j C(t, j) (Eq. 15, every target a neighbour; with
+ * a restricted neighbourhood a covered one would score 0), and the unselected
+ * token with the smallest score is retained (ties to the smaller index).
+ * Step 0 has r = v, so the first pick is the capacity-weighted medoid.  After
+ * k picks the same solve over the whole set gives the plan whose transport
+ * cost <P, C_S> is reported as `objective`.  E and every sum are float64,
+ * sums in a fixed order (deterministic); E underflows to 0 where
+ * C / epsilon exceeds about 708, so epsilon should stay above max C / 700.
+ * Each step costs `rounds` passes over an n x l matrix and one pass over the
+ * cost.
+ *
+ *   cost, n, capacity: as for coverprune_sgs_select (every retained token must
+ *             reach some target at finite E, e.g. C(s, s) = 0 as the FST cost has)
+ *   k         1 <= k <= min(n, CP_SGS_LITERAL_MAX_K)
+ *   epsilon   entropic regularisation, > 0, in the cost's units
+ *   rounds    scaling rounds per solve, 1 <= rounds <= CP_SGS_LITERAL_MAX_ROUNDS
+ *   follow    [k] int32 or NULL: picks to take instead of the argmin (a replay
+ *             of another trajectory, e.g. to price the coverage-loss greedy's
+ *             set); distinct indices in [0, n) are the caller's duty
+ *   selected       [k] int32 output: the picks in order
+ *   step_score     [k] double output (may be NULL): score of each pick
+ *   step_residual  [k] double output (may be NULL): sum_j r_j before each pick
+ *   objective      [1] double output (may be NULL): <P, C_S> of the final plan
+ * With `follow` set and both step outputs NULL only the final plan is solved.
+ * Workspace: about 8 k + 40 bytes per token plus 8 k per 64 tokens.
+ */
+#define CP_SGS_LITERAL_MAX_K 4096
+#define CP_SGS_LITERAL_MAX_ROUNDS 1000000
+size_t coverprune_sgs_literal_workspace(int64_t n, int64_t k);
+cp_status coverprune_sgs_literal_select(const float* cost, int64_t n, const float* capacity, int64_t k,
+                                        float epsilon, int32_t rounds, const int32_t* follow, int32_t* selected,
+                                        double* step_score, double* step_residual, double* objective,
+                                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* CoverPrune-Lite (Sec. 4, Eq. 17-20).

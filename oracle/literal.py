@@ -46,11 +46,13 @@ def sot_scaling(C_S, u, v, eps: float, rounds: int):
     return a, b, E
 
 
-def literal_sgs_ref(C, v, K: int, eps: float, rounds: int, follow=None):
+def literal_sgs_ref(C, v, K: int, eps: float, rounds: int, follow=None, steps=None):
     """K steps of the literal greedy (readings above) on the source-major cost C.
 
     follow: optional picks to take instead of the oracle's own (a replay of
     another trajectory); the oracle's scores are still reported for them.
+    steps: optionally stop after that many steps (the sources keep mass 1/K);
+    the objective is then None.
 
     Returns dict(selected, score, best, residual, objective): the picks; the
     score sum_j r_j C(t, j) of each pick; the smallest score among the
@@ -63,7 +65,7 @@ def literal_sgs_ref(C, v, K: int, eps: float, rounds: int, follow=None):
         raise ValueError("need 1 <= K <= N")
     chosen = np.zeros(n, bool)
     S, scores, bests, residual = [], [], [], []
-    for step in range(K):
+    for step in range(K if steps is None else min(K, steps)):
         if S:
             a, b, E = sot_scaling(C[S], np.full(len(S), 1.0 / K), v, eps, rounds)
             r = np.maximum(v - b * (E.T @ a), 0.0)
@@ -80,7 +82,10 @@ def literal_sgs_ref(C, v, K: int, eps: float, rounds: int, follow=None):
         residual.append(float(r.sum()))
         chosen[t] = True
         S.append(t)
-    a, b, E = sot_scaling(C[S], np.full(K, 1.0 / K), v, eps, rounds)
-    P = a[:, None] * E * b[None, :]
+    objective = None
+    if len(S) == K:
+        a, b, E = sot_scaling(C[S], np.full(K, 1.0 / K), v, eps, rounds)
+        P = a[:, None] * E * b[None, :]
+        objective = float(np.sum(P * C[S]))
     return dict(selected=np.array(S, np.int64), score=np.array(scores), best=np.array(bests),
-                residual=np.array(residual), objective=float(np.sum(P * C[S])))
+                residual=np.array(residual), objective=objective)

@@ -14,7 +14,7 @@ from typing import Optional
 
 import torch
 
-__all__ = ["fst_cost", "fst_capacity", "sgs_select", "knn", "sgs_local_select", "lite_select", "library", "library_path", "CoverPruneError",
+__all__ = ["fst_cost", "fst_capacity", "sgs_select", "sgs_literal_select", "knn", "sgs_local_select", "lite_select", "library", "library_path", "CoverPruneError",
            "DEFAULT_KAPPA"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -72,6 +72,11 @@ def library() -> ctypes.CDLL:
     lib.coverprune_fst_capacity.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, i64, _CapWeights, vp, vp, vp, sz,
                                             vp]
     lib.coverprune_fst_capacity.restype = st
+    lib.coverprune_sgs_literal_workspace.argtypes = [i64, i64]
+    lib.coverprune_sgs_literal_workspace.restype = sz
+    lib.coverprune_sgs_literal_select.argtypes = [vp, i64, vp, i64, ctypes.c_float, ctypes.c_int32, vp, vp, vp, vp,
+                                                  vp, vp, sz, vp]
+    lib.coverprune_sgs_literal_select.restype = st
     lib.coverprune_knn.argtypes = [vp, i64, i64, vp, vp]
     lib.coverprune_knn.restype = st
     lib.coverprune_sgs_local_workspace.argtypes = [i64, i64]
@@ -231,6 +236,43 @@ def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[
                                      _ptr(sel), _ptr(gain), _ptr(obj), _ptr(assign), _ptr(workspace),
                                      workspace.numel(), _stream(stream)))
     return SgsResult(sel, gain, obj, assign)
+
+
+@dataclass
+class LiteralResult:
+    selected: torch.Tensor     # [k] int32, greedy order
+    score: torch.Tensor        # [k] float64, score of each pick
+    residual: torch.Tensor     # [k] float64, residual mass before each pick
+    objective: torch.Tensor    # [1] float64, transport cost of the final plan
+
+
+def sgs_literal_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, epsilon: float = 0.05,
+                       rounds: int = 100, follow: Optional[torch.Tensor] = None, steps: bool = True,
+                       workspace: Optional[torch.Tensor] = None, stream=None) -> LiteralResult:
+    """The greedy with each step's entropic semi-relaxed transport solved as
+    written (Sec. 3.5, Eq. 11-15).  follow: [k] int32 picks to replay instead
+    of the argmin; with steps=False (and follow given) only the final plan is
+    solved and score/residual are left empty."""
+    lib = library()
+    n = cost.shape[0]
+    dev = cost.device
+    _need(cost, "cost", torch.float32, (n, n), dev)
+    _need(capacity, "capacity", torch.float32, (n,), dev)
+    if follow is not None:
+        _need(follow, "follow", torch.int32, (int(k),), dev)
+    sel = torch.empty(int(k), dtype=torch.int32, device=dev)
+    score = torch.empty(int(k), dtype=torch.float64, device=dev)
+    resid = torch.empty(int(k), dtype=torch.float64, device=dev)
+    obj = torch.empty(1, dtype=torch.float64, device=dev)
+    need = lib.coverprune_sgs_literal_workspace(n, int(k))
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    keep = steps or follow is None
+    _check(lib.coverprune_sgs_literal_select(_ptr(cost), n, _ptr(capacity), int(k), float(epsilon), int(rounds),
+                                             _ptr(follow), _ptr(sel), _ptr(score) if keep else None,
+                                             _ptr(resid) if keep else None, _ptr(obj), _ptr(workspace),
+                                             workspace.numel(), _stream(stream)))
+    return LiteralResult(sel, score, resid, obj)
 
 
 def knn(pos: torch.Tensor, g: int, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:

@@ -181,6 +181,46 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
 }
 
 // ---------------------------------------------------------------------------
+size_t coverprune_sgs_literal_workspace(int64_t n, int64_t k) {
+  if (n < 1 || k < 1 || k > n) return 0;
+  return cp::sgs_literal_workspace_bytes(n, k);
+}
+
+cp_status coverprune_sgs_literal_select(const float* cost, int64_t n, const float* capacity, int64_t k,
+                                        float epsilon, int32_t rounds, const int32_t* follow, int32_t* selected,
+                                        double* step_score, double* step_residual, double* objective,
+                                        void* workspace, size_t workspace_bytes, void* stream) {
+  if (n < 1 || n > kMaxDenseN) return fail(CP_ERR_INVALID_ARG, "n = %lld outside [1, %lld]", (long long)n, (long long)kMaxDenseN);
+  if (k < 1 || k > std::min<int64_t>(n, CP_SGS_LITERAL_MAX_K))
+    return fail(CP_ERR_INVALID_ARG, "k = %lld outside [1, min(n, %d)]", (long long)k, CP_SGS_LITERAL_MAX_K);
+  if (!std::isfinite(epsilon) || !(epsilon > 0.f)) return fail(CP_ERR_INVALID_ARG, "epsilon must be finite and > 0");
+  if (rounds < 1 || rounds > CP_SGS_LITERAL_MAX_ROUNDS)
+    return fail(CP_ERR_INVALID_ARG, "rounds = %d outside [1, %d]", (int)rounds, CP_SGS_LITERAL_MAX_ROUNDS);
+  if (!cost || !capacity || !selected) return fail(CP_ERR_INVALID_ARG, "cost, capacity and selected must be non-NULL");
+  if (!aligned16(cost)) return fail(CP_ERR_INVALID_ARG, "cost is not 16-byte aligned");
+  cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_literal_workspace(n, k));
+  if (st != CP_OK) return st;
+
+  cp::LiteralParams p;
+  p.cost = cost;
+  p.n = int(n);
+  p.capacity = capacity;
+  p.k = int(k);
+  p.epsilon = epsilon;
+  p.rounds = int(rounds);
+  p.follow = follow;
+  p.selected = selected;
+  p.step_score = step_score;
+  p.step_residual = step_residual;
+  p.objective = objective;
+  p.workspace = workspace;
+  p.workspace_bytes = workspace_bytes;
+  hipError_t e = cp::launch_sgs_literal(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sgs literal");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
 cp_status coverprune_knn(const float* pos, int64_t n, int64_t g, int32_t* neighbours, void* stream) {
   if (n < 1 || n > CP_KNN_MAX_N) return fail(CP_ERR_INVALID_ARG, "n = %lld outside [1, %d]", (long long)n, CP_KNN_MAX_N);
   if (g < 1 || g > std::min<int64_t>(n, CP_KNN_MAX_G))

@@ -60,6 +60,26 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
 // Nearest-neighbour tables: out [n, g], n <= 16384, g <= min(n, 1024).
 hipError_t launch_knn(const float* pos, int n, int g, int32_t* out, hipStream_t stream);
 
+// The greedy step solved as written: entropic semi-relaxed transport per step.
+struct LiteralParams {
+  const float* cost;              // [n, n] target-major
+  int n;
+  const float* capacity;          // [n]
+  int k;                          // 1 <= k <= min(n, 4096)
+  float epsilon;
+  int rounds;
+  const int32_t* follow;          // [k] or nullptr
+  int32_t* selected;              // [k]
+  double* step_score;             // [k] or nullptr
+  double* step_residual;          // [k] or nullptr
+  double* objective;              // [1] or nullptr
+  void* workspace;
+  size_t workspace_bytes;
+};
+
+size_t sgs_literal_workspace_bytes(int64_t n, int64_t k);
+hipError_t launch_sgs_literal(const LiteralParams& p, hipStream_t stream);
+
 // FST capacity.
 struct CapacityParams {
   const void* feats;

@@ -196,3 +196,28 @@ def _cap(lib, **kw):
 ])
 def test_capacity_rejects(lib, kw, code):
     assert _cap(lib, **kw) == code
+
+
+def test_literal_workspace_query(lib):
+    assert lib.coverprune_sgs_literal_workspace(0, 1) == 0
+    assert lib.coverprune_sgs_literal_workspace(10, 11) == 0
+    assert lib.coverprune_sgs_literal_workspace(16384, 1638) >= 16384 * 1640 * 8
+
+
+def _lit(lib, **kw):
+    a = dict(cost=FAKE, n=64, v=FAKE, k=8, eps=0.05, rounds=10, follow=None, sel=FAKE, score=None, resid=None,
+             obj=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return lib.coverprune_sgs_literal_select(a["cost"], a["n"], a["v"], a["k"], a["eps"], a["rounds"], a["follow"],
+                                             a["sel"], a["score"], a["resid"], a["obj"], a["ws"], a["ws_bytes"],
+                                             a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), INVALID), (dict(k=0), INVALID), (dict(k=65), INVALID), (dict(n=8192, k=4097), INVALID),
+    (dict(eps=0.0), INVALID), (dict(eps=-1.0), INVALID), (dict(eps=float("nan")), INVALID),
+    (dict(rounds=0), INVALID), (dict(rounds=1000001), INVALID), (dict(cost=None), INVALID),
+    (dict(v=None), INVALID), (dict(sel=None), INVALID), (dict(ws=None), WORKSPACE), (dict(ws_bytes=64), WORKSPACE),
+])
+def test_literal_rejects(lib, kw, code):
+    assert _lit(lib, **kw) == code

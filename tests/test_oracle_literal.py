@@ -131,3 +131,13 @@ def test_follow_replays_a_trajectory():
     assert rep["score"][4] >= rep["best"][4]
     with pytest.raises(ValueError):
         literal.literal_sgs_ref(C, v, 3, eps=0.1, rounds=5, follow=[1, 1, 2])
+
+
+def test_steps_limit_is_a_prefix():
+    C, v = _random(20, 20, 17)
+    np.fill_diagonal(C, 0.0)
+    full = literal.literal_sgs_ref(C, v, 6, eps=0.1, rounds=30)
+    part = literal.literal_sgs_ref(C, v, 6, eps=0.1, rounds=30, steps=3)
+    assert np.array_equal(part["selected"], full["selected"][:3])
+    assert np.array_equal(part["score"], full["score"][:3])
+    assert part["objective"] is None
