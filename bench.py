@@ -43,6 +43,10 @@ def _args():
                     help="also time CoverPrune-Lite alone on this workload ('' to skip)")
     ap.add_argument("--sgs", choices=("incremental", "dense"), default="incremental",
                     help="form of the greedy inside the timed step (both give the same picks)")
+    ap.add_argument("--literal-rounds", type=int, default=50,
+                    help="scaling rounds per step of the literal greedy timed beside the step (0 to skip)")
+    ap.add_argument("--literal-eps", type=float, default=0.05,
+                    help="entropic regularisation of the literal greedy, in cost units")
     ap.add_argument("--ceilings", action="store_true",
                     help="only measure the achievable ceilings: a 1 GiB device-to-device copy (also the "
                          "calibration kernel for the HBM byte counters) and a 16384 x 3584 x 16384 bf16 "
@@ -371,6 +375,34 @@ def main():
         cap = {"n_nb": n_nb, "ms": round(cap_ms, 3), "gathered_row_bytes": gather,
                "gathered_gbs": round(gather / (cap_ms * 1e-3) / 1e9, 1)}
 
+    # The greedy with each step's transport solved as written (Eq. 11-15),
+    # timed once on the same cost: its picks against the timed greedy's, and
+    # both sets priced by the same final transport solve.  Algorithmic bytes:
+    # per step l, every scaling round reads the n x l float64 matrix once and
+    # the score reads the cost once.
+    lit = None
+    if args.literal_rounds > 0 and k <= 4096:
+        rounds, eps = args.literal_rounds, args.literal_eps
+        ws_lit = torch.empty(lib.coverprune_sgs_literal_workspace(n, k), dtype=torch.uint8, device=dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        rl = cp.sgs_literal_select(cost, t["capacity"], k, epsilon=eps, rounds=rounds, workspace=ws_lit)
+        e1.record()
+        torch.cuda.synchronize()
+        lit_ms = e0.elapsed_time(e1)
+        hot = cp.sgs_literal_select(cost, t["capacity"], k, epsilon=eps, rounds=rounds, follow=r.selected,
+                                    steps=False, workspace=ws_lit)
+        torch.cuda.synchronize()
+        lsel = rl.selected.cpu().numpy()
+        lit_bytes = sum(rounds * 8.0 * n * l + 4.0 * n * n for l in range(k)) + rounds * 8.0 * n * k
+        lit = {"eps": eps, "rounds": rounds, "ms": round(lit_ms, 1),
+               "us_per_greedy_step": round(lit_ms * 1e3 / k, 1),
+               "achieved_gbs": round(lit_bytes / (lit_ms * 1e-3) / 1e9, 1), "bytes": lit_bytes,
+               "picks_shared_with_step": int(len(set(lsel.tolist()) & set(sel.tolist()))),
+               "transport_cost_literal": float(rl.objective[0].item()),
+               "transport_cost_step_picks": float(hot.objective[0].item())}
+        del ws_lit
+
     # FST cost: symmetric Gram needs N (N + 1) D flops; the whole call (prep,
     # Gram, epilogue) is timed, so this fraction is a lower bound for the Gram.
     gram_flops = float(n) * (n + 1) * d
@@ -400,6 +432,7 @@ def main():
             "sgs_dense_same_picks": same,
             "sgs_local": local,
             "fst_capacity": cap,
+            "sgs_literal": lit,
             "lite_select_ms": round(l_ms, 3),
             "coverprune_ms_per_scene": round(f_ms + s_ms, 3),
             "coverprune_lite_ms_per_scene": round(l_ms, 3),

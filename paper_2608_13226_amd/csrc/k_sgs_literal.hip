@@ -55,7 +55,7 @@ struct LitDev {
   double* a;               // [k]
   double* b;               // [n]
   double* r;               // [n]
-  double* colpart;         // [nrb, kp]
+  double* colpart;         // [kp, nrb]: column i's partial sums, one per row block
   double* scorepart;       // [panels, n]
   double* objpart;         // [nrb]
   unsigned char* chosen;   // [n]
@@ -100,6 +100,7 @@ __global__ __launch_bounds__(kLitBlock) void lit_rows_kernel(LitDev p, int l, in
       const int j = j0 + q;
       const double* e = p.E + size_t(j) * p.kp;
       double t = 0.0;
+#pragma unroll 4
       for (int i = lane; i < l; i += kWave) t = fma(e[i], sa[i], t);
       t = wave_sum(t);
       const double vj = double(p.v[j]);
@@ -115,17 +116,23 @@ __global__ __launch_bounds__(kLitBlock) void lit_rows_kernel(LitDev p, int l, in
   __syncthreads();
   for (int i = threadIdx.x; i < l; i += kLitBlock) {
     double s = 0.0;
+#pragma unroll 8
     for (int q = 0; q < rows; ++q) s = fma(p.E[size_t(j0 + q) * p.kp + i], sb[q], s);
-    p.colpart[size_t(blockIdx.x) * p.kp + i] = s;
+    p.colpart[size_t(i) * p.nrb + blockIdx.x] = s;
   }
 }
 
-__global__ void lit_a_kernel(LitDev p, int l) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+// One wave per column: its row-block partials, lane-strided then a fixed
+// butterfly, so the sum's order does not depend on timing.
+__global__ __launch_bounds__(kLitBlock) void lit_a_kernel(LitDev p, int l) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int i = blockIdx.x * kLitWaves + (threadIdx.x >> 6);
   if (i >= l) return;
+  const double* c = p.colpart + size_t(i) * p.nrb;
   double s = 0.0;
-  for (int rb = 0; rb < p.nrb; ++rb) s += p.colpart[size_t(rb) * p.kp + i];
-  p.a[i] = p.u / s;
+  for (int rb = lane; rb < p.nrb; rb += kWave) s += c[rb];
+  s = wave_sum(s);
+  if (lane == 0) p.a[i] = p.u / s;
 }
 
 // Partial scores: block (strip, panel) sums r_j C_tm[j][c] over the panel's
@@ -287,7 +294,7 @@ LitLayout lit_layout(int64_t n, int64_t k) {
 // One solve over the first l retained tokens: `rounds` scaling rounds, the
 // last one leaving b and the residual.
 hipError_t solve(const LitDev& p, int l, int rounds, hipStream_t stream) {
-  const int a_blocks = (l + kLitBlock - 1) / kLitBlock;
+  const int a_blocks = (l + kLitWaves - 1) / kLitWaves;
   lit_rows_kernel<<<p.nrb, kLitBlock, 0, stream>>>(p, l, 0);
   for (int it = 0; it < rounds; ++it) {
     lit_a_kernel<<<a_blocks, kLitBlock, 0, stream>>>(p, l);
