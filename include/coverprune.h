@@ -11,6 +11,7 @@
  *                          neighbours (Sec. 3.4, Eq. 9-10);
  *   coverprune_sgs_select  greedy selection of K tokens against that cost and
  *                          the target capacities (Sec. 3.5, Eq. 11-16);
+ *   coverprune_sgs_select_batch  up to 16 scenes' greedies in one launch;
  *   coverprune_knn         the g nearest tokens of every token in 3D, and
  *   coverprune_sgs_local_select  the greedy with gains over those neighbours
  *                          only (Sec. 3.5, Eq. 13);
@@ -175,6 +176,44 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
                                 float c0, uint32_t flags, int32_t* selected, double* step_gain,
                                 double* step_objective, int32_t* assign, void* workspace,
                                 size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Several scenes' greedies in one launch (the incremental form).
+ *
+ * Pruning runs once per request before the language model's prefill
+ * (Sec. 5.1), and one scene's greedy occupies at most one compute unit per 64
+ * tokens, so a few-thousand-token scene leaves most of the chip idle.  This
+ * call runs up to CP_SGS_MAX_BATCH scenes of any sizes side by side in one
+ * cooperative launch: scene s gets its own group of blocks (one block per
+ * compute unit in all, groups balanced by tokens per block) and its own
+ * exchanges, so each scene's result is what coverprune_sgs_select with
+ * CP_SGS_INCREMENTAL computes for it alone (its block partition can differ,
+ * which matters only for gains equal to 2^-31 relative in different blocks).
+ * The call takes as long as its slowest scene.
+ *
+ *   scenes    host array of `count` scene descriptions (read during the call
+ *             only); each field as for coverprune_sgs_select, all device memory
+ *   count     1 <= count <= CP_SGS_MAX_BATCH (and at most the number of
+ *             compute units)
+ *   workspace the sum of the scenes' incremental workspaces, laid out one
+ *             after another; size from coverprune_sgs_batch_workspace
+ */
+#define CP_SGS_MAX_BATCH 16
+typedef struct {
+  const float* cost;       /* [n, n] target-major */
+  const float* capacity;   /* [n] */
+  int64_t n;
+  int64_t k;
+  float c0;
+  int32_t* selected;       /* [k] */
+  double* step_gain;       /* [k] or NULL */
+  double* step_objective;  /* [k] or NULL */
+  int32_t* assign;         /* [n] or NULL */
+} cp_sgs_scene;
+
+size_t coverprune_sgs_batch_workspace(const cp_sgs_scene* scenes, int32_t count);
+cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count, void* workspace,
+                                      size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Spatially local greedy (Sec. 3.5, Eq. 13).

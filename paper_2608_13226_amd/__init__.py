@@ -14,7 +14,7 @@ from typing import Optional
 
 import torch
 
-__all__ = ["fst_cost", "fst_capacity", "sgs_select", "sgs_literal_select", "knn", "sgs_local_select", "lite_select", "library", "library_path", "CoverPruneError",
+__all__ = ["fst_cost", "fst_capacity", "sgs_select", "sgs_select_batch", "sgs_literal_select", "knn", "sgs_local_select", "lite_select", "library", "library_path", "CoverPruneError",
            "DEFAULT_KAPPA"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -35,6 +35,12 @@ class CoverPruneError(RuntimeError):
 class _Weights(ctypes.Structure):
     _fields_ = [("lambda_f", ctypes.c_float), ("lambda_x", ctypes.c_float),
                 ("lambda_tau", ctypes.c_float), ("kappa", ctypes.c_float)]
+
+
+class _SgsScene(ctypes.Structure):
+    _fields_ = [("cost", ctypes.c_void_p), ("capacity", ctypes.c_void_p), ("n", ctypes.c_int64),
+                ("k", ctypes.c_int64), ("c0", ctypes.c_float), ("selected", ctypes.c_void_p),
+                ("step_gain", ctypes.c_void_p), ("step_objective", ctypes.c_void_p), ("assign", ctypes.c_void_p)]
 
 
 class _CapWeights(ctypes.Structure):
@@ -72,6 +78,10 @@ def library() -> ctypes.CDLL:
     lib.coverprune_fst_capacity.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, i64, _CapWeights, vp, vp, vp, sz,
                                             vp]
     lib.coverprune_fst_capacity.restype = st
+    lib.coverprune_sgs_batch_workspace.argtypes = [ctypes.POINTER(_SgsScene), ctypes.c_int32]
+    lib.coverprune_sgs_batch_workspace.restype = sz
+    lib.coverprune_sgs_select_batch.argtypes = [ctypes.POINTER(_SgsScene), ctypes.c_int32, vp, sz, vp]
+    lib.coverprune_sgs_select_batch.restype = st
     lib.coverprune_sgs_literal_workspace.argtypes = [i64, i64]
     lib.coverprune_sgs_literal_workspace.restype = sz
     lib.coverprune_sgs_literal_select.argtypes = [vp, i64, vp, i64, ctypes.c_float, ctypes.c_int32, vp, vp, vp, vp,
@@ -236,6 +246,37 @@ def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[
                                      _ptr(sel), _ptr(gain), _ptr(obj), _ptr(assign), _ptr(workspace),
                                      workspace.numel(), _stream(stream)))
     return SgsResult(sel, gain, obj, assign)
+
+
+def sgs_select_batch(costs, capacities, ks, c0: Optional[float] = None, weights=(1.0, 1.0, 1.0),
+                     workspace: Optional[torch.Tensor] = None, stream=None):
+    """The incremental greedy of several scenes (lists of target-major costs,
+    capacities and budgets) in one launch.  Returns one SgsResult per scene."""
+    lib = library()
+    count = len(costs)
+    if not (len(capacities) == len(ks) == count):
+        raise ValueError("costs, capacities and ks must have the same length")
+    if c0 is None:
+        c0 = float(sum(float(w) for w in weights))
+    arr = (_SgsScene * max(count, 1))()
+    out = []
+    for s, (cost, cap, k) in enumerate(zip(costs, capacities, ks)):
+        n = cost.shape[0]
+        dev = cost.device
+        _need(cost, f"costs[{s}]", torch.float32, (n, n), dev)
+        _need(cap, f"capacities[{s}]", torch.float32, (n,), dev)
+        r = SgsResult(torch.empty(int(k), dtype=torch.int32, device=dev),
+                      torch.empty(int(k), dtype=torch.float64, device=dev),
+                      torch.empty(int(k), dtype=torch.float64, device=dev),
+                      torch.empty(n, dtype=torch.int32, device=dev))
+        arr[s] = _SgsScene(cost.data_ptr(), cap.data_ptr(), n, int(k), float(c0), r.selected.data_ptr(),
+                           r.gain.data_ptr(), r.objective.data_ptr(), r.assign.data_ptr())
+        out.append(r)
+    need = lib.coverprune_sgs_batch_workspace(arr, count)
+    if workspace is None:
+        workspace = _workspace(need, costs[0].device if count else None)
+    _check(lib.coverprune_sgs_select_batch(arr, count, _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out
 
 
 @dataclass

@@ -181,6 +181,53 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
 }
 
 // ---------------------------------------------------------------------------
+size_t coverprune_sgs_batch_workspace(const cp_sgs_scene* scenes, int32_t count) {
+  if (!scenes || count < 1 || count > CP_SGS_MAX_BATCH) return 0;
+  int64_t n[CP_SGS_MAX_BATCH], k[CP_SGS_MAX_BATCH];
+  for (int32_t s = 0; s < count; ++s) {
+    if (scenes[s].n < 1 || scenes[s].k < 1) return 0;
+    n[s] = scenes[s].n;
+    k[s] = scenes[s].k;
+  }
+  return cp::sgs_inc_batch_workspace_bytes(n, k, int(count));
+}
+
+cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  if (!scenes) return fail(CP_ERR_INVALID_ARG, "scenes is NULL");
+  if (count < 1 || count > CP_SGS_MAX_BATCH)
+    return fail(CP_ERR_INVALID_ARG, "count = %d outside [1, %d]", (int)count, CP_SGS_MAX_BATCH);
+  cp::SgsParams p[CP_SGS_MAX_BATCH];
+  for (int32_t s = 0; s < count; ++s) {
+    const cp_sgs_scene& c = scenes[s];
+    if (c.n < 1 || c.n > kMaxDenseN)
+      return fail(CP_ERR_INVALID_ARG, "scene %d: n = %lld outside [1, %lld]", (int)s, (long long)c.n, (long long)kMaxDenseN);
+    if (c.k < 1 || c.k > c.n)
+      return fail(CP_ERR_INVALID_ARG, "scene %d: k = %lld outside [1, n = %lld]", (int)s, (long long)c.k, (long long)c.n);
+    if (!std::isfinite(c.c0)) return fail(CP_ERR_INVALID_ARG, "scene %d: c0 must be finite", (int)s);
+    if (!c.cost || !c.capacity || !c.selected)
+      return fail(CP_ERR_INVALID_ARG, "scene %d: cost, capacity and selected must be non-NULL", (int)s);
+    if (!aligned16(c.cost)) return fail(CP_ERR_INVALID_ARG, "scene %d: cost is not 16-byte aligned", (int)s);
+    p[s].cost = c.cost;
+    p[s].n = int(c.n);
+    p[s].capacity = c.capacity;
+    p[s].k = int(c.k);
+    p[s].c0 = c.c0;
+    p[s].selected = c.selected;
+    p[s].step_gain = c.step_gain;
+    p[s].step_objective = c.step_objective;
+    p[s].assign = c.assign;
+    p[s].workspace = nullptr;
+    p[s].workspace_bytes = 0;
+  }
+  cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_batch_workspace(scenes, count));
+  if (st != CP_OK) return st;
+  hipError_t e = cp::launch_sgs_incremental_batch(p, int(count), workspace, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sgs batch");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
 size_t coverprune_sgs_literal_workspace(int64_t n, int64_t k) {
   if (n < 1 || k < 1 || k > n) return 0;
   return cp::sgs_literal_workspace_bytes(n, k);

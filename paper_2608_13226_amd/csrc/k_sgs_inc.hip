@@ -47,10 +47,10 @@ constexpr int kBatch = 64;         // change-list entries a wave fetches per rou
 constexpr int kChunk = 16;         // of which the rows read together
 constexpr int kInitRows = 16;      // rows a wave has in flight in the full pass
 
-__global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
+// The greedy of one scene as run by block `blk` of the scene's `nb` blocks.
+__device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   extern __shared__ unsigned long long smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int blk = blockIdx.x;
   const int lo = blk * a.W;
   const int cnt = max(0, min(a.n, lo + a.W) - lo);
   unsigned long long* sGlo = smem;                                 // [W] running gains, low words
@@ -64,7 +64,6 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
   __shared__ int si[kWaves];
   __shared__ int swt[kWaves];
   __shared__ unsigned long long su[kWaves];
-  const int nb = gridDim.x;
   __shared__ int spre[kMaxBlocks + 1];        // slice offsets
   __shared__ int sflag;
 
@@ -290,26 +289,27 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) {
     for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
 }
 
-}  // namespace
+__global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) { inc_body(a, blockIdx.x, gridDim.x); }
 
-size_t sgs_inc_workspace_bytes(int64_t n, int64_t k) { return layout(n, k).total; }
+// Several scenes in one launch: scene s runs on blocks [g0[s], g0[s + 1])
+// with its own slots, change lists and abort flag, so the scenes' greedies
+// proceed independently side by side.
+constexpr int kMaxBatch = 16;
 
-hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream) {
-  int dev = 0, cus = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-  const int nb = blocks_for(p.n, cus);
-  const int W = (p.n + nb - 1) / nb;
-  const size_t lds = size_t(W) * (16 + 4 + 4 + 1) + 16;
-  int per_cu = 0;
-  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(sgs_inc_kernel),
-                                                        kBlock, lds)) != hipSuccess)
-    return e;
-  if (per_cu < 1) return hipErrorCooperativeLaunchTooLarge;
+struct IncBatch {
+  int count;
+  int g0[kMaxBatch + 1];
+  IncDev scene[kMaxBatch];
+};
 
+__global__ __launch_bounds__(kBlock) void sgs_inc_batch_kernel(IncBatch b) {
+  int s = 0;
+  while (s + 1 < b.count && int(blockIdx.x) >= b.g0[s + 1]) ++s;
+  inc_body(b.scene[s], int(blockIdx.x) - b.g0[s], b.g0[s + 1] - b.g0[s]);
+}
+
+IncDev inc_dev(const SgsParams& p, char* w, int W) {
   const Layout L = layout(p.n, p.k);
-  char* w = static_cast<char*>(p.workspace);
   IncDev a;
   a.C = p.cost;
   a.v = p.capacity;
@@ -325,12 +325,98 @@ hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream) {
   a.cand = reinterpret_cast<unsigned long long*>(w + L.cand);
   a.abort = reinterpret_cast<unsigned int*>(w + L.ctrl);
   a.W = W;
+  return a;
+}
 
+size_t lds_for(int W) { return size_t(W) * (16 + 4 + 4 + 1) + 16; }
+
+}  // namespace
+
+size_t sgs_inc_workspace_bytes(int64_t n, int64_t k) { return layout(n, k).total; }
+
+hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream) {
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  const int nb = blocks_for(p.n, cus);
+  const int W = (p.n + nb - 1) / nb;
+  const size_t lds = lds_for(W);
+  int per_cu = 0;
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(sgs_inc_kernel),
+                                                        kBlock, lds)) != hipSuccess)
+    return e;
+  if (per_cu < 1) return hipErrorCooperativeLaunchTooLarge;
+
+  IncDev a = inc_dev(p, static_cast<char*>(p.workspace), W);
   sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   void* args[] = {&a};
   return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_inc_kernel), dim3(nb), dim3(kBlock), args,
                                     lds, stream);
+}
+
+size_t sgs_inc_batch_workspace_bytes(const int64_t* n, const int64_t* k, int count) {
+  size_t total = 0;
+  for (int s = 0; s < count; ++s) total += layout(n[s], k[s]).total;
+  return total;
+}
+
+hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, void* workspace, hipStream_t stream) {
+  if (count < 1 || count > kMaxBatch) return hipErrorInvalidValue;
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  if (count > cus) return hipErrorInvalidValue;
+  // One block per compute unit in all: every scene starts with one, then the
+  // scene with the most tokens per block gains one (up to its own cap of one
+  // block per 64 tokens, at most kMaxBlocks) until the units run out.
+  int nb[kMaxBatch], cap[kMaxBatch];
+  int used = count;
+  for (int s = 0; s < count; ++s) {
+    nb[s] = 1;
+    cap[s] = blocks_for(p[s].n, cus);
+  }
+  while (used < cus) {
+    int best = -1;
+    long long bw = 0;
+    for (int s = 0; s < count; ++s) {
+      if (nb[s] >= cap[s]) continue;
+      const long long w = (p[s].n + nb[s] - 1) / nb[s];
+      if (w > bw) {
+        bw = w;
+        best = s;
+      }
+    }
+    if (best < 0) break;
+    ++nb[best];
+    ++used;
+  }
+  IncBatch b;
+  b.count = count;
+  b.g0[0] = 0;
+  size_t lds = 0, off = 0;
+  char* w = static_cast<char*>(workspace);
+  for (int s = 0; s < count; ++s) {
+    const int W = (p[s].n + nb[s] - 1) / nb[s];
+    b.scene[s] = inc_dev(p[s], w + off, W);
+    b.g0[s + 1] = b.g0[s] + nb[s];
+    lds = std::max(lds, lds_for(W));
+    off += layout(p[s].n, p[s].k).total;
+  }
+  int per_cu = 0;
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(sgs_inc_batch_kernel),
+                                                        kBlock, lds)) != hipSuccess)
+    return e;
+  if (per_cu < 1) return hipErrorCooperativeLaunchTooLarge;
+  for (int s = 0; s < count; ++s) {
+    sgs_inc_init_kernel<<<std::min(1024, (std::max(p[s].n, p[s].k) + 255) / 256), 256, 0, stream>>>(b.scene[s]);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  void* args[] = {&b};
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_inc_batch_kernel), dim3(used), dim3(kBlock),
+                                    args, lds, stream);
 }
 
 }  // namespace cp

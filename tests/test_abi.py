@@ -221,3 +221,39 @@ def _lit(lib, **kw):
 ])
 def test_literal_rejects(lib, kw, code):
     assert _lit(lib, **kw) == code
+
+
+def _scenes(count, **kw):
+    import paper_2608_13226_amd as cp
+    arr = (cp._SgsScene * max(count, 1))()
+    for s in range(count):
+        a = dict(cost=0x1000, capacity=0x1000, n=64, k=8, c0=3.0, selected=0x1000, step_gain=None,
+                 step_objective=None, assign=None)
+        if s == count - 1:
+            a.update(kw)
+        arr[s] = cp._SgsScene(a["cost"], a["capacity"], a["n"], a["k"], a["c0"], a["selected"], a["step_gain"],
+                              a["step_objective"], a["assign"])
+    return arr
+
+
+def test_batch_workspace_is_the_sum_of_the_scenes(lib):
+    one = lib.coverprune_sgs_workspace(64, 8, 1)
+    assert lib.coverprune_sgs_batch_workspace(_scenes(3), 3) == 3 * one
+    assert lib.coverprune_sgs_batch_workspace(_scenes(3), 17) == 0
+
+
+@pytest.mark.parametrize("count,kw,code", [
+    (0, {}, INVALID), (17, {}, INVALID), (3, dict(n=0), INVALID), (3, dict(k=0), INVALID), (3, dict(k=65), INVALID),
+    (2, dict(c0=float("inf")), INVALID), (2, dict(cost=None), INVALID), (2, dict(capacity=None), INVALID),
+    (2, dict(selected=None), INVALID), (2, dict(cost=0x1004), INVALID),
+])
+def test_batch_rejects(lib, count, kw, code):
+    arr = _scenes(max(count, 1), **kw) if count <= 16 else _scenes(16)
+    assert lib.coverprune_sgs_select_batch(arr, count, FAKE, 1 << 30, None) == code
+    assert lib.coverprune_last_error() != b""
+
+
+def test_batch_rejects_small_workspace(lib):
+    assert lib.coverprune_sgs_select_batch(_scenes(2), 2, FAKE, 64, None) == WORKSPACE
+    assert lib.coverprune_sgs_select_batch(_scenes(2), 2, None, 1 << 30, None) == WORKSPACE
+    assert lib.coverprune_sgs_select_batch(None, 2, FAKE, 1 << 30, None) == INVALID
