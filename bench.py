@@ -47,6 +47,9 @@ def _args():
                     help="scaling rounds per step of the literal greedy timed beside the step (0 to skip)")
     ap.add_argument("--literal-eps", type=float, default=0.05,
                     help="entropic regularisation of the literal greedy, in cost units")
+    ap.add_argument("--batch-scenes", type=int, default=4,
+                    help="scenes of the paper's 6272-token shape whose greedies are timed one by one and "
+                         "batched (0 to skip)")
     ap.add_argument("--ceilings", action="store_true",
                     help="only measure the achievable ceilings: a 1 GiB device-to-device copy (also the "
                          "calibration kernel for the HBM byte counters) and a 16384 x 3584 x 16384 bf16 "
@@ -403,6 +406,47 @@ def main():
                "transport_cost_step_picks": float(hot.objective[0].item())}
         del ws_lit
 
+    # Serving shape: several scenes of the paper's 32 x 196 = 6272 tokens,
+    # K = 628, pruned before their prefills.  The greedies one after another
+    # against one batched launch (costs from the FST kernel, made beforehand).
+    batch = None
+    if args.batch_scenes > 0:
+        bcfg = CONFIGS["paper_n6272_d3584"]
+        bcosts, bcaps, bks = [], [], []
+        for i in range(args.batch_scenes):
+            bs = make_scene(bcfg, args.seed + 1 + i)
+            bt = to_device(bs, dev)
+            c, _ = cp.fst_cost(bt["feats"], bt["pos"], bt["frame"])
+            bcosts.append(c)
+            bcaps.append(bt["capacity"])
+            bks.append(bs.k)
+            del bt
+        ws_b = torch.empty(max(lib.coverprune_sgs_workspace(int(c.shape[0]), kk, cp.CP_SGS_INCREMENTAL)
+                               for c, kk in zip(bcosts, bks)), dtype=torch.uint8, device=dev)
+        ws_bb = torch.empty(lib.coverprune_sgs_batch_workspace(
+            (cp._SgsScene * len(bks))(*[cp._SgsScene(0, 0, int(c.shape[0]), kk, 3.0, 0, 0, 0, 0)
+                                        for c, kk in zip(bcosts, bks)]), len(bks)), dtype=torch.uint8, device=dev)
+        for _ in range(2):                      # warm-up of both forms
+            one = [cp.sgs_select(c, v, kk, workspace=ws_b, incremental=True).selected
+                   for c, v, kk in zip(bcosts, bcaps, bks)]
+            many = cp.sgs_select_batch(bcosts, bcaps, bks, workspace=ws_bb)
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record()
+        one = [cp.sgs_select(c, v, kk, workspace=ws_b, incremental=True).selected.clone()
+               for c, v, kk in zip(bcosts, bcaps, bks)]
+        e[1].record()
+        many = cp.sgs_select_batch(bcosts, bcaps, bks, workspace=ws_bb)
+        e[2].record()
+        torch.cuda.synchronize()
+        seq_ms, bat_ms = e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2])
+        same_b = all(bool(torch.equal(a, b.selected)) for a, b in zip(one, many))
+        batch = {"workload": bcfg.name, "scenes": len(bks), "n": int(bcosts[0].shape[0]), "k": bks[0],
+                 "sequential_ms": round(seq_ms, 3), "batched_ms": round(bat_ms, 3),
+                 "scenes_per_s_sequential": round(len(bks) / (seq_ms * 1e-3), 1),
+                 "scenes_per_s_batched": round(len(bks) / (bat_ms * 1e-3), 1), "same_picks": same_b}
+        del bcosts, bcaps, ws_b, ws_bb
+
     # FST cost: symmetric Gram needs N (N + 1) D flops; the whole call (prep,
     # Gram, epilogue) is timed, so this fraction is a lower bound for the Gram.
     gram_flops = float(n) * (n + 1) * d
@@ -433,6 +477,7 @@ def main():
             "sgs_local": local,
             "fst_capacity": cap,
             "sgs_literal": lit,
+            "sgs_batch": batch,
             "lite_select_ms": round(l_ms, 3),
             "coverprune_ms_per_scene": round(f_ms + s_ms, 3),
             "coverprune_lite_ms_per_scene": round(l_ms, 3),
