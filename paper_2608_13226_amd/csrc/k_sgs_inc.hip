@@ -65,7 +65,8 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   __shared__ int swt[kWaves];
   __shared__ unsigned long long su[kWaves];
   __shared__ int spre[kMaxBlocks + 1];        // slice offsets
-  __shared__ int sflag;
+  __shared__ int sflag;                       // abort seen while waiting for the winner
+  __shared__ int slflag;                      // ... or for the slice lengths
 
   for (int i = tid; i < cnt; i += kBlock) {
     sb[i] = a.c0;
@@ -184,7 +185,7 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
     // 2. Every block's slice length (thread i waits for block i), and the
     // slices' offsets in the flattened change list.
     {
-      if (tid == 0) sflag = 0;
+      if (tid == 0) slflag = 0;
       __syncthreads();
       int c = 0;
       if (tid < nb) {
@@ -193,14 +194,14 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
         if (wait_slot(a.lens + tid, a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
           c = int(x & 0xffffffffull);
         else
-          sflag = 1;
+          slflag = 1;
       }
       const int incl = block_inclusive_scan(c, swt);
       if (tid < nb) spre[tid + 1] = incl;
       if (tid == 0) spre[0] = 0;
       __syncthreads();
     }
-    if (sflag) break;
+    if (slflag) break;
     const int total = spre[nb];
 
     // 3. Apply the changes to the own columns' gains.  Each lane of a round

@@ -44,7 +44,8 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
   __shared__ int swt[kWaves];
   __shared__ unsigned long long su[kWaves];
   __shared__ int spre[kMaxBlocks + 1];
-  __shared__ int sflag;
+  __shared__ int sflag;                       // abort seen while waiting for the winner
+  __shared__ int slflag;                      // ... or for the slice lengths
 
   for (int j = tid; j < a.n; j += kBlock) sball[j] = a.c0;
   for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
@@ -159,7 +160,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
     // 2. Every block's slice length, then every change applied to the
     // replicated best costs (and, in block 0, to the objective).
     {
-      if (tid == 0) sflag = 0;
+      if (tid == 0) slflag = 0;
       __syncthreads();
       int c = 0;
       if (tid < nb) {
@@ -168,14 +169,14 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
         if (wait_slot(a.lens + tid, a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
           c = int(x & 0xffffffffull);
         else
-          sflag = 1;
+          slflag = 1;
       }
       const int incl = block_inclusive_scan(c, swt);
       if (tid < nb) spre[tid + 1] = incl;
       if (tid == 0) spre[0] = 0;
       __syncthreads();
     }
-    if (sflag) break;
+    if (slflag) break;
     const int total = spre[nb];
     __int128 dobj = 0;
     for (int e = tid; e < total; e += kBlock) {

@@ -193,10 +193,36 @@ __device__ double block_sum_all(double x, double* sd) {
 
 // Exact argmax (ties to the smaller index) of the block's unchosen columns,
 // published as the block's candidate for the step; across blocks the gains
-// compare as doubles truncated to 43 bits.
+// compare as doubles truncated to 43 bits.  With at most 64 columns wave 0
+// does it alone, one column per lane, and no barrier follows: the callers'
+// next step begins with one (read_winner), and the gains and chosen flags it
+// reads were last written by wave 0 itself.
 __device__ void publish_argmax(const unsigned long long* sGlo, const long long* sGhi, const unsigned char* ssel,
                                int lo, int cnt, int S, unsigned long long* slot, unsigned long long epoch,
                                __int128* sg, int* si) {
+  if (cnt <= 64) {
+    if (threadIdx.x >= 64) return;
+    const int i = threadIdx.x;
+    __int128 g = -1;
+    int gi = INT_MAX;
+    if (i < cnt && !ssel[i]) {
+      g = ((__int128)sGhi[i] << 64) | (__int128)sGlo[i];
+      gi = lo + i;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const unsigned long long olo = __shfl_xor((unsigned long long)g, o);
+      const long long ohi = __shfl_xor((long long)(g >> 64), o);
+      const int oi = __shfl_xor(gi, o);
+      const __int128 og = ((__int128)ohi << 64) | (__int128)olo;
+      if (og > g || (og == g && oi < gi)) {
+        g = og;
+        gi = oi;
+      }
+    }
+    if (i == 0) put(slot, (gi != INT_MAX ? pack_key(fx_to_double(g, S), gi) : kNoCandidate) | epoch);
+    return;
+  }
   __int128 g = -1;
   int gi = INT_MAX;
   for (int i = threadIdx.x; i < cnt; i += kBlock)
