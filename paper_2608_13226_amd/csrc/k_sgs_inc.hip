@@ -120,12 +120,16 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   }
 
   // Block 0 keeps the objective L = sum_j v_j b_j in the gains' fixed point,
-  // starting from b = c0.
-  __int128 L = 0;
+  // starting from b = c0, as one running part per wave: a wave adds its share
+  // of a step's changes without a barrier, and thread 0 totals the parts for
+  // step l after the next step's first barrier (after the loop for the last).
+  __shared__ __int128 sLw[kWaves];
+  int obj_step = -1;
   if (blk == 0) {
     __int128 x = 0;
     for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
-    L = block_sum_i128(x, sg);
+    const __int128 L0 = block_sum_i128(x, sg);
+    if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
   }
 
   publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + blk, epoch_of(0), sg, si);
@@ -135,6 +139,12 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
     // only keeps a broken slot from addressing past the matrix.
     const int tw = read_winner(a.cand + (step & 1) * kMaxBlocks, epoch_of(step), nb, a.abort, su, &sflag);
     if (tw < 0) break;
+    if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
+      __int128 L = 0;
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) L += sLw[q];
+      a.step_obj[obj_step] = fx_to_double(L, S);
+    }
     const int t = min(tw, a.n - 1);
     if (t >= lo && t < lo + cnt && tid == 0) {
       ssel[t - lo] = 1;
@@ -277,14 +287,27 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
       __syncthreads();
     }
     if (blk == 0) {
-      L += block_sum_i128(dobj, sg);
-      if (tid == 0 && a.step_obj) a.step_obj[step] = fx_to_double(L, S);
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long olo = __shfl_xor((unsigned long long)dobj, o);
+        const long long ohi = __shfl_xor((long long)(dobj >> 64), o);
+        dobj += ((__int128)ohi << 64) | (__int128)olo;
+      }
+      if (lane == 0) sLw[w] += dobj;
+      obj_step = step;
     }
 
     // 4. This block's candidate for the next step.
     if (step + 1 < a.k)
       publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + ((step + 1) & 1) * kMaxBlocks + blk,
                      epoch_of(step + 1), sg, si);
+  }
+  __syncthreads();
+  if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
+    __int128 L = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) L += sLw[q];
+    a.step_obj[obj_step] = fx_to_double(L, S);
   }
   if (blk == 0 && get(a.abort))
     for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;

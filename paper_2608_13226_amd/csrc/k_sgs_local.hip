@@ -72,11 +72,15 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
     S = 101 - e;
   }
 
-  __int128 L = 0;
+  // Objective in block 0, one running part per wave (as in the incremental
+  // form): step l's total is written after the next step's first barrier.
+  __shared__ __int128 sLw[kWaves];
+  int obj_step = -1;
   if (blk == 0) {
     __int128 x = 0;
     for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
-    L = block_sum_i128(x, sg);
+    const __int128 L0 = block_sum_i128(x, sg);
+    if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
   }
 
   // Local gains of the own candidates from the current best costs: lane =
@@ -114,6 +118,12 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
   for (int step = 0; step < a.k; ++step) {
     const int tw = read_winner(a.cand + (step & 1) * kMaxBlocks, epoch_of(step), nb, a.abort, su, &sflag);
     if (tw < 0) break;
+    if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
+      __int128 L = 0;
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) L += sLw[q];
+      a.step_obj[obj_step] = fx_to_double(L, S);
+    }
     const int t = min(tw, a.n - 1);
     if (t >= lo && t < lo + cnt && tid == 0) {
       ssel[t - lo] = 1;
@@ -197,8 +207,14 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
       }
     }
     if (blk == 0) {
-      L += block_sum_i128(dobj, sg);
-      if (tid == 0 && a.step_obj) a.step_obj[step] = fx_to_double(L, S);
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long olo = __shfl_xor((unsigned long long)dobj, o);
+        const long long ohi = __shfl_xor((long long)(dobj >> 64), o);
+        dobj += ((__int128)ohi << 64) | (__int128)olo;
+      }
+      if (lane == 0) sLw[w] += dobj;
+      obj_step = step;
     }
 
     // 3. Fresh local gains and this block's candidate for the next step.
@@ -207,6 +223,13 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
       publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + ((step + 1) & 1) * kMaxBlocks + blk,
                      epoch_of(step + 1), sg, si);
     }
+  }
+  __syncthreads();
+  if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
+    __int128 L = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) L += sLw[q];
+    a.step_obj[obj_step] = fx_to_double(L, S);
   }
   if (blk == 0 && get(a.abort))
     for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
