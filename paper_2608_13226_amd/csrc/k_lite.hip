@@ -12,18 +12,22 @@
 //              a prefix-min scan of t(p) - p and the K - N + p floor give the
 //              group of every position (the walk of Eq. 17 in scan form)
 //     tiles    16-row tiles per group and their prefix (work units below)
-//     maxima   M_x, M_tau over same-group, 27-adjacent pairs
-//     B(p)     sum_j v_j (lam_x phi(d_x / M_x) + lam_tau d_tau / M_tau), or
-//              v_j c0 for a non-adjacent pair: every term of the group cost
-//              that does not involve features
-//   pairs    one wave per 16-row tile of a group: the tile's rows against the
-//            whole group on the matrix cores (16 x 16 tiles over D), d_f,
-//            A(p) = sum_j v_j d_f over adjacent pairs, and the global M_f
+//   maxima   M_x, M_tau over same-group, 27-adjacent pairs (a wave per
+//            position, after the front)
+//   B(p)     sum_j v_j (lam_x phi(d_x / M_x) + lam_tau d_tau / M_tau), or
+//            v_j c0 for a non-adjacent pair: every term of the group cost that
+//            does not involve features (a wave per position, after the front)
+//   pairs    per 16-row tile of a group, the tile's rows against the whole
+//            group on the matrix cores (16 x 16 tiles over D), d_f,
+//            A(p) = sum_j v_j d_f over adjacent pairs, and the global M_f:
+//            one wave per tile for groups of at most two tiles, one block per
+//            tile (waves splitting the column tiles) for larger groups
 //   select   cost(p) = (lam_f / M_f) A(p) + B(p); per-group argmin (Eq. 18)
 //   total    fixed-order sum of the K prototype costs (Eq. 20 objective)
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cfloat>
 #include <climits>
 
 #include "common.h"
@@ -436,7 +440,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
   }
   grid_barrier(bar, ++round);
 
-  // ---- tiles per group (block sums) and M_x, M_tau over evaluated pairs
+  // ---- tiles per group (block sums)
   const int gtile = (K + G - 1) / G;
   const int q0 = min(K, blk * gtile), q1 = min(K, q0 + gtile);
   {
@@ -448,29 +452,6 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     unsigned long long tot;
     block_excl_sum_u64(local, s_u64, tot);
     if (t == 0) put(a.bsum + blk, tot);
-
-    double mx2 = 0.0;
-    int mt = 0;
-    for (int i = p0 + t; i < p1; i += kThreads) {
-      const int q = get(a.gid + i);
-      const int tokn = get(perm + i);
-      const unsigned long long vi = get(a.vox_pos + i);
-      const double xi = a.pos[3 * tokn], yi = a.pos[3 * tokn + 1], zi = a.pos[3 * tokn + 2];
-      const int fi = a.frame[tokn];
-      const int j0 = clamp_range(get(a.gstart + q), n), j1 = clamp_range(get(a.gstart + q + 1), n);
-      for (int j = j0; j < j1; ++j) {
-        if (!adjacent(vi, get(a.vox_pos + j))) continue;
-        const int tj = get(perm + j);
-        mx2 = fmax(mx2, sq_dist(xi, yi, zi, a.pos[3 * tj], a.pos[3 * tj + 1], a.pos[3 * tj + 2]));
-        mt = max(mt, abs(fi - a.frame[tj]));
-      }
-    }
-    mx2 = wave_max(mx2);
-    mt = wave_max(mt);
-    if (lane == 0) {
-      atomic_max_nonneg(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2), mx2);
-      atomicMax(a.ctrl + kCtrlMt, unsigned(mt));
-    }
   }
   grid_barrier(bar, ++round);
 
@@ -492,44 +473,233 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       if (q == K - 1) a.rt_start[K] = int(run + ex + nt);
       run += chunk;
     }
-
-    const double m_x = sqrt(__longlong_as_double((long long)get(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2))));
-    const int m_t = int(get(a.ctrl + kCtrlMt));
-    const double c0 = double(a.lam_f) + double(a.lam_x) + double(a.lam_t);
-    for (int i = p0 + t; i < p1; i += kThreads) {
-      const int q = get(a.gid + i);
-      const int tokn = get(perm + i);
-      const unsigned long long vi = get(a.vox_pos + i);
-      const double xi = a.pos[3 * tokn], yi = a.pos[3 * tokn + 1], zi = a.pos[3 * tokn + 2];
-      const int fi = a.frame[tokn];
-      double acc = 0.0;
-      const int j0 = clamp_range(get(a.gstart + q), n), j1 = clamp_range(get(a.gstart + q + 1), n);
-      for (int j = j0; j < j1; ++j) {
-        const int tj = get(perm + j);
-        const double vj = double(a.v[tj]);
-        if (!adjacent(vi, get(a.vox_pos + j))) {
-          acc += vj * c0;
-          continue;
-        }
-        const double dist = sqrt(sq_dist(xi, yi, zi, a.pos[3 * tj], a.pos[3 * tj + 1], a.pos[3 * tj + 2]));
-        const double z = m_x > 0.0 ? dist / m_x : 0.0;
-        const double ph = a.kappa > 0.f ? log1p(double(a.kappa) * z) * a.inv_log1p_kappa : z;
-        const double dt = m_t > 0 ? double(max(0, fi - a.frame[tj])) / double(m_t) : 0.0;
-        acc += vj * (double(a.lam_x) * ph + double(a.lam_t) * dt);
-      }
-      a.B[i] = acc;
-    }
   }
   if (blk == 0 && t == 0) a.ctrl[kCtrlSorted] = unsigned(sorted);
 }
 
+// Block-wide maximum of a nonnegative float, raised into *bits with one
+// atomic (same-address atomics from many blocks serialize).
+__device__ __forceinline__ void block_max_to(unsigned int* bits, float x) {
+  __shared__ float sm[kWaves];
+  x = wave_max(x);
+  if ((threadIdx.x & 63) == 0) sm[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < kWaves; ++q) x = fmaxf(x, sm[q]);
+    atomic_max_nonneg(bits, x);
+  }
+}
+
 // ---------------------------------------------------------------------------
-// Within-group feature pass.  Work unit: one 16-row tile of one group, taken
-// by one wave, multiplied on the matrix cores against every 16-row tile of the
-// same group over the full feature width.  Lane l supplies row l % 16 and
-// feature slice 8 (l / 16) .. +8 of each 32-wide K step (bf16), or 4 (l / 16)
-// .. +4 of each 16-wide step spread over four MFMAs (f32); the output element
-// (4 (l / 16) + r, l % 16) lands in register r of lane l.
+// M_x and M_tau over the evaluated pairs (same group, adjacent voxels): waves
+// stride over the sorted positions, lanes over each group's members; one
+// atomic maximum per block (few blocks: same-address atomics serialize).
+__global__ __launch_bounds__(kThreads) void lite_maxima_kernel(LiteDev a) {
+  __shared__ double smx[kWaves];
+  __shared__ int smt[kWaves];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
+  double mx2 = 0.0;
+  int mt = 0;
+  for (int i = blockIdx.x * kWaves + w; i < a.n; i += gridDim.x * kWaves) {
+    const int q = min(max(a.gid[i], 0), a.k - 1);
+    const int tokn = perm[i];
+    const unsigned long long vi = a.vox_pos[i];
+    const double xi = a.pos[3 * tokn], yi = a.pos[3 * tokn + 1], zi = a.pos[3 * tokn + 2];
+    const int fi = a.frame[tokn];
+    const int j0 = clamp_range(a.gstart[q], a.n), j1 = clamp_range(a.gstart[q + 1], a.n);
+    for (int j = j0 + lane; j < j1; j += 64) {
+      if (!adjacent(vi, a.vox_pos[j])) continue;
+      const int tj = perm[j];
+      mx2 = fmax(mx2, sq_dist(xi, yi, zi, a.pos[3 * tj], a.pos[3 * tj + 1], a.pos[3 * tj + 2]));
+      mt = max(mt, abs(fi - a.frame[tj]));
+    }
+  }
+  mx2 = wave_max(mx2);
+  mt = wave_max(mt);
+  if (lane == 0) {
+    smx[w] = mx2;
+    smt[w] = mt;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < kWaves; ++q) {
+      mx2 = fmax(mx2, smx[q]);
+      mt = max(mt, smt[q]);
+    }
+    atomic_max_nonneg(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2), mx2);
+    atomicMax(a.ctrl + kCtrlMt, unsigned(mt));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// B(p) = sum over the group of v_j (lam_x phi(d_x / M_x) + lam_tau d_tau / M_tau)
+// for adjacent pairs and v_j c0 otherwise: one wave per sorted position, lanes
+// over the group's members, summed lane-strided and then across the wave in a
+// fixed order.
+__global__ __launch_bounds__(kThreads) void lite_b_kernel(LiteDev a) {
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (i >= a.n) return;
+  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
+  const double m_x = sqrt(__longlong_as_double(*reinterpret_cast<const long long*>(a.ctrl + kCtrlMx2)));
+  const int m_t = int(a.ctrl[kCtrlMt]);
+  const double c0 = double(a.lam_f) + double(a.lam_x) + double(a.lam_t);
+  const int q = min(max(a.gid[i], 0), a.k - 1);
+  const int tokn = perm[i];
+  const unsigned long long vi = a.vox_pos[i];
+  const double xi = a.pos[3 * tokn], yi = a.pos[3 * tokn + 1], zi = a.pos[3 * tokn + 2];
+  const int fi = a.frame[tokn];
+  double acc = 0.0;
+  const int j0 = clamp_range(a.gstart[q], a.n), j1 = clamp_range(a.gstart[q + 1], a.n);
+  for (int j = j0 + lane; j < j1; j += 64) {
+    const int tj = perm[j];
+    const double vj = double(a.v[tj]);
+    if (!adjacent(vi, a.vox_pos[j])) {
+      acc += vj * c0;
+      continue;
+    }
+    const double dist = sqrt(sq_dist(xi, yi, zi, a.pos[3 * tj], a.pos[3 * tj + 1], a.pos[3 * tj + 2]));
+    const double z = m_x > 0.0 ? dist / m_x : 0.0;
+    const double ph = a.kappa > 0.f ? log1p(double(a.kappa) * z) * a.inv_log1p_kappa : z;
+    const double dt = m_t > 0 ? double(max(0, fi - a.frame[tj])) / double(m_t) : 0.0;
+    acc += vj * (double(a.lam_x) * ph + double(a.lam_t) * dt);
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) a.B[i] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// Within-group feature pass.  Work unit: one 16-row tile ta of one group,
+// multiplied on the matrix cores against every 16-row tile tb of the same
+// group over the full feature width.  Lane l supplies row l % 16 and feature
+// slice 8 (l / 16) .. +8 of each 32-wide K step (bf16), or 4 (l / 16) .. +4 of
+// each 16-wide step spread over four MFMAs (f32); the output element
+// (4 (l / 16) + r, l % 16) lands in register r of lane l.  A group of at most
+// kSplitTiles tiles takes one wave per unit (lite_pair_kernel); a larger one
+// takes one block per unit whose waves split the column tiles and add their
+// row sums in wave order (lite_pair_split_kernel), so a big group does not
+// leave one wave working through all its tiles alone.
+constexpr int kSplitTiles = 2;
+
+struct Unit {
+  int p0, g, ntile, ta;
+};
+
+// Group and row tile of unit u: the last q with rt_start[q] <= u.
+__device__ __forceinline__ bool unit_of(const LiteDev& a, int u, Unit& t) {
+  int lo = 0, hi = a.k - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.rt_start[mid] <= u) lo = mid;
+    else hi = mid - 1;
+  }
+  t.p0 = clamp_range(a.gstart[lo], a.n);
+  t.g = max(0, clamp_range(a.gstart[lo + 1], a.n) - t.p0);
+  t.ntile = (t.g + kTileRows - 1) / kTileRows;
+  t.ta = u - a.rt_start[lo];
+  return t.ta >= 0 && t.ta < t.ntile;
+}
+
+// Row tile t.ta against column tile tb: adds v_j d_f over adjacent pairs to
+// arow (the lane's four output rows) and raises lmax.
+template <bool BF16>
+__device__ __forceinline__ void pair_tile(const LiteDev& a, const int* perm, const Unit& t, int tb, double* arow,
+                                          float& lmax) {
+  const int lane = threadIdx.x & 63;
+  const int row = lane & 15, quad = lane >> 4;
+  const int ra = t.ta * kTileRows + row;  // operand row of this lane in tile ta
+  const int rb = tb * kTileRows + row;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float na = 0.f, nb = 0.f;
+  if (BF16) {
+    const uint16_t* Fa = ra < t.g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[t.p0 + ra]) * a.d : nullptr;
+    const uint16_t* Fb = rb < t.g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[t.p0 + rb]) * a.d : nullptr;
+    // Eight 32-wide K steps per round: all loads first, then the MFMAs.
+    constexpr int U = 8;
+    const bool same = tb == t.ta;
+    for (int k0 = 0; k0 < a.d; k0 += 32 * U) {
+      uint4 ua[U], ub[U];
+#pragma unroll
+      for (int x = 0; x < U; ++x) {
+        const int kk = k0 + 32 * x + quad * 8;
+        ua[x] = uint4{0u, 0u, 0u, 0u};
+        ub[x] = uint4{0u, 0u, 0u, 0u};
+        if (Fa && kk < a.d) ua[x] = *reinterpret_cast<const uint4*>(Fa + kk);
+        if (!same && Fb && kk < a.d) ub[x] = *reinterpret_cast<const uint4*>(Fb + kk);
+      }
+#pragma unroll
+      for (int x = 0; x < U; ++x) {
+        if (same) ub[x] = ua[x];
+        const uint32_t wa[4] = {ua[x].x, ua[x].y, ua[x].z, ua[x].w}, wb[4] = {ub[x].x, ub[x].y, ub[x].z, ub[x].w};
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const float a0 = bf16_bits_to_float(wa[h] & 0xffffu), a1 = bf16_bits_to_float(wa[h] >> 16);
+          const float b0 = bf16_bits_to_float(wb[h] & 0xffffu), b1 = bf16_bits_to_float(wb[h] >> 16);
+          na = fmaf(a0, a0, fmaf(a1, a1, na));
+          nb = fmaf(b0, b0, fmaf(b1, b1, nb));
+        }
+        bf16x8 va, vb;
+        __builtin_memcpy(&va, &ua[x], sizeof va);
+        __builtin_memcpy(&vb, &ub[x], sizeof vb);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, vb, acc, 0, 0, 0);
+      }
+    }
+  } else {
+    const float* Fa = ra < t.g ? static_cast<const float*>(a.feats) + size_t(perm[t.p0 + ra]) * a.d : nullptr;
+    const float* Fb = rb < t.g ? static_cast<const float*>(a.feats) + size_t(perm[t.p0 + rb]) * a.d : nullptr;
+    for (int k0 = 0; k0 < a.d; k0 += 16) {
+      const int kk = k0 + quad * 4;
+      float4 fa = make_float4(0.f, 0.f, 0.f, 0.f), fb = fa;
+      if (Fa && kk < a.d) fa = *reinterpret_cast<const float4*>(Fa + kk);
+      if (tb == t.ta) fb = fa;
+      else if (Fb && kk < a.d) fb = *reinterpret_cast<const float4*>(Fb + kk);
+      na = fmaf(fa.x, fa.x, fmaf(fa.y, fa.y, fmaf(fa.z, fa.z, fmaf(fa.w, fa.w, na))));
+      nb = fmaf(fb.x, fb.x, fmaf(fb.y, fb.y, fmaf(fb.z, fb.z, fmaf(fb.w, fb.w, nb))));
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.x, fb.x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.y, fb.y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.z, fb.z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.w, fb.w, acc, 0, 0, 0);
+    }
+  }
+  // Row sums of squares: the four lanes sharing l % 16 hold its slices.
+  na += __shfl_xor(na, 16);
+  na += __shfl_xor(na, 32);
+  nb += __shfl_xor(nb, 16);
+  nb += __shfl_xor(nb, 32);
+  const int cb = tb * kTileRows + row;    // output column of this lane
+  const bool cvalid = cb < t.g;
+  const unsigned long long vb = cvalid ? a.vox_pos[t.p0 + cb] : 0ull;
+  const double wv = cvalid ? double(a.v[perm[t.p0 + cb]]) : 0.0;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int oa = quad * 4 + r;           // output row within tile ta
+    const float nra = __shfl(na, oa);
+    const int ca = t.ta * kTileRows + oa;
+    if (cvalid && ca < t.g && adjacent(a.vox_pos[t.p0 + ca], vb)) {
+      const float den = sqrtf(nra) * sqrtf(nb);
+      const float cosv = den > 0.f ? acc[r] / den : 0.f;
+      float df = fminf(fmaxf(1.f - cosv, 0.f), 2.f);
+      if (ca == cb) df = 0.f;
+      arow[r] = fma(wv, double(df), arow[r]);
+      lmax = fmaxf(lmax, df);
+    }
+  }
+}
+
+// Sum each output row over the 16 lanes (columns) that share it.
+__device__ __forceinline__ void row_sums(double* arow) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    double x = arow[r];
+    x += __shfl_xor(x, 1);
+    x += __shfl_xor(x, 2);
+    x += __shfl_xor(x, 4);
+    x += __shfl_xor(x, 8);
+    arow[r] = x;
+  }
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void lite_pair_kernel(LiteDev a) {
   const int lane = threadIdx.x & 63;
@@ -539,136 +709,96 @@ __global__ __launch_bounds__(kThreads) void lite_pair_kernel(LiteDev a) {
   const int units = int(a.ctrl[kCtrlTiles]);
   const int row = lane & 15, quad = lane >> 4;
   float lmax = 0.f;
-
   for (int u = gw; u < units; u += nw) {
-    // Group of unit u: the last q with rt_start[q] <= u.
-    int lo = 0, hi = a.k - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (a.rt_start[mid] <= u) lo = mid;
-      else hi = mid - 1;
-    }
-    const int q = lo;
-    const int p0 = clamp_range(a.gstart[q], a.n), g = max(0, clamp_range(a.gstart[q + 1], a.n) - p0);
-    const int ntile = (g + kTileRows - 1) / kTileRows;
-    const int ta = u - a.rt_start[q];
-    if (ta < 0 || ta >= ntile) continue;
-    const int ra = ta * kTileRows + row;  // operand row of this lane in tile ta
+    Unit t;
+    if (!unit_of(a, u, t) || t.ntile > kSplitTiles) continue;
     double arow[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int tb = 0; tb < ntile; ++tb) {
-      const int rb = tb * kTileRows + row;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      float na = 0.f, nb = 0.f;
-      if (BF16) {
-        const uint16_t* Fa = ra < g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[p0 + ra]) * a.d : nullptr;
-        const uint16_t* Fb = rb < g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[p0 + rb]) * a.d : nullptr;
-        // Eight 32-wide K steps per round: all loads first, then the MFMAs.
-        constexpr int U = 8;
-        const bool same = tb == ta;
-        for (int k0 = 0; k0 < a.d; k0 += 32 * U) {
-          uint4 ua[U], ub[U];
-#pragma unroll
-          for (int x = 0; x < U; ++x) {
-            const int kk = k0 + 32 * x + quad * 8;
-            ua[x] = uint4{0u, 0u, 0u, 0u};
-            ub[x] = uint4{0u, 0u, 0u, 0u};
-            if (Fa && kk < a.d) ua[x] = *reinterpret_cast<const uint4*>(Fa + kk);
-            if (!same && Fb && kk < a.d) ub[x] = *reinterpret_cast<const uint4*>(Fb + kk);
-          }
-#pragma unroll
-          for (int x = 0; x < U; ++x) {
-            if (same) ub[x] = ua[x];
-            const uint32_t wa[4] = {ua[x].x, ua[x].y, ua[x].z, ua[x].w}, wb[4] = {ub[x].x, ub[x].y, ub[x].z, ub[x].w};
-#pragma unroll
-            for (int h = 0; h < 4; ++h) {
-              const float a0 = bf16_bits_to_float(wa[h] & 0xffffu), a1 = bf16_bits_to_float(wa[h] >> 16);
-              const float b0 = bf16_bits_to_float(wb[h] & 0xffffu), b1 = bf16_bits_to_float(wb[h] >> 16);
-              na = fmaf(a0, a0, fmaf(a1, a1, na));
-              nb = fmaf(b0, b0, fmaf(b1, b1, nb));
-            }
-            bf16x8 va, vb;
-            __builtin_memcpy(&va, &ua[x], sizeof va);
-            __builtin_memcpy(&vb, &ub[x], sizeof vb);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, vb, acc, 0, 0, 0);
-          }
-        }
-      } else {
-        const float* Fa = ra < g ? static_cast<const float*>(a.feats) + size_t(perm[p0 + ra]) * a.d : nullptr;
-        const float* Fb = rb < g ? static_cast<const float*>(a.feats) + size_t(perm[p0 + rb]) * a.d : nullptr;
-        for (int k0 = 0; k0 < a.d; k0 += 16) {
-          const int kk = k0 + quad * 4;
-          float4 fa = make_float4(0.f, 0.f, 0.f, 0.f), fb = fa;
-          if (Fa && kk < a.d) fa = *reinterpret_cast<const float4*>(Fa + kk);
-          if (tb == ta) fb = fa;
-          else if (Fb && kk < a.d) fb = *reinterpret_cast<const float4*>(Fb + kk);
-          na = fmaf(fa.x, fa.x, fmaf(fa.y, fa.y, fmaf(fa.z, fa.z, fmaf(fa.w, fa.w, na))));
-          nb = fmaf(fb.x, fb.x, fmaf(fb.y, fb.y, fmaf(fb.z, fb.z, fmaf(fb.w, fb.w, nb))));
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.x, fb.x, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.y, fb.y, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.z, fb.z, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.w, fb.w, acc, 0, 0, 0);
-        }
-      }
-      // Row sums of squares: the four lanes sharing l % 16 hold its slices.
-      na += __shfl_xor(na, 16);
-      na += __shfl_xor(na, 32);
-      nb += __shfl_xor(nb, 16);
-      nb += __shfl_xor(nb, 32);
-      const int cb = tb * kTileRows + row;    // output column of this lane
-      const bool cvalid = cb < g;
-      const unsigned long long vb = cvalid ? a.vox_pos[p0 + cb] : 0ull;
-      const double wv = cvalid ? double(a.v[perm[p0 + cb]]) : 0.0;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int oa = quad * 4 + r;           // output row within tile ta
-        const float nra = __shfl(na, oa);
-        const int ca = ta * kTileRows + oa;
-        if (cvalid && ca < g && adjacent(a.vox_pos[p0 + ca], vb)) {
-          const float den = sqrtf(nra) * sqrtf(nb);
-          const float cosv = den > 0.f ? acc[r] / den : 0.f;
-          float df = fminf(fmaxf(1.f - cosv, 0.f), 2.f);
-          if (ca == cb) df = 0.f;
-          arow[r] = fma(wv, double(df), arow[r]);
-          lmax = fmaxf(lmax, df);
-        }
-      }
-    }
-    // Sum each output row over the 16 lanes (columns) that share it.
+    for (int tb = 0; tb < t.ntile; ++tb) pair_tile<BF16>(a, perm, t, tb, arow, lmax);
+    row_sums(arow);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      double x = arow[r];
-      x += __shfl_xor(x, 1);
-      x += __shfl_xor(x, 2);
-      x += __shfl_xor(x, 4);
-      x += __shfl_xor(x, 8);
-      const int ca = ta * kTileRows + quad * 4 + r;
-      if (row == 0 && ca < g) a.A[p0 + ca] = x;
+      const int ca = t.ta * kTileRows + quad * 4 + r;
+      if (row == 0 && ca < t.g) a.A[t.p0 + ca] = arow[r];
     }
   }
-  lmax = wave_max(lmax);
-  if (lane == 0) atomic_max_nonneg(a.ctrl + kCtrlMf, lmax);
+  block_max_to(a.ctrl + kCtrlMf, lmax);
 }
 
-// One thread per group: prototype = argmin of (lam_f / M_f) A + B.
+constexpr int kSplitWaves = 16;
+
+template <bool BF16>
+__global__ __launch_bounds__(kSplitWaves * 64) void lite_pair_split_kernel(LiteDev a) {
+  __shared__ double spart[kSplitWaves][kTileRows];
+  __shared__ float sm[kSplitWaves];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
+  const int units = int(a.ctrl[kCtrlTiles]);
+  const int row = lane & 15, quad = lane >> 4;
+  float lmax = 0.f;
+  for (int u = blockIdx.x; u < units; u += gridDim.x) {
+    Unit t;
+    if (!unit_of(a, u, t) || t.ntile <= kSplitTiles) continue;   // the same for the whole block
+    double arow[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int tb = w; tb < t.ntile; tb += kSplitWaves) pair_tile<BF16>(a, perm, t, tb, arow, lmax);
+    row_sums(arow);
+    if (row == 0) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) spart[w][quad * 4 + r] = arow[r];
+    }
+    __syncthreads();
+    if (threadIdx.x < kTileRows) {
+      const int ca = t.ta * kTileRows + threadIdx.x;
+      if (ca < t.g) {
+        double x = 0.0;
+#pragma unroll
+        for (int q = 0; q < kSplitWaves; ++q) x += spart[q][threadIdx.x];
+        a.A[t.p0 + ca] = x;
+      }
+    }
+    __syncthreads();
+  }
+  lmax = wave_max(lmax);
+  if (lane == 0) sm[w] = lmax;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < kSplitWaves; ++q) lmax = fmaxf(lmax, sm[q]);
+    atomic_max_nonneg(a.ctrl + kCtrlMf, lmax);
+  }
+}
+
+// One wave per group: prototype = argmin of (lam_f / M_f) A + B over the
+// group's members (lanes), ties to the smaller token index.
 __global__ __launch_bounds__(kThreads) void lite_select_kernel(LiteDev a) {
-  const int q = blockIdx.x * kThreads + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int q = blockIdx.x * kWaves + (threadIdx.x >> 6);
   if (q >= a.k) return;
   const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
   const float m_f = __uint_as_float(a.ctrl[kCtrlMf]);
   const double wf = m_f > 0.f ? double(a.lam_f) / double(m_f) : 0.0;
-  double best = 0.0;
+  double best = DBL_MAX;
   int bt = INT_MAX;
   const int i0 = clamp_range(a.gstart[q], a.n), i1 = clamp_range(a.gstart[q + 1], a.n);
-  for (int i = i0; i < i1; ++i) {
+  for (int i = i0 + lane; i < i1; i += 64) {
     const double c = fma(wf, a.A[i], a.B[i]);
     const int tk = perm[i];
-    if (bt == INT_MAX || c < best || (c == best && tk < bt)) {
+    if (c < best || (c == best && tk < bt)) {
       best = c;
       bt = tk;
     }
   }
-  a.selected[q] = bt == INT_MAX ? -1 : bt;
-  a.gcost[q] = best;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const double oc = __shfl_xor(best, o);
+    const int ot = __shfl_xor(bt, o);
+    if (oc < best || (oc == best && ot < bt)) {
+      best = oc;
+      bt = ot;
+    }
+  }
+  if (lane == 0) {
+    a.selected[q] = bt == INT_MAX ? -1 : bt;
+    a.gcost[q] = bt == INT_MAX ? 0.0 : best;
+  }
 }
 
 __global__ __launch_bounds__(kThreads) void lite_total_kernel(LiteDev a) {
@@ -737,12 +867,20 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   // over all groups, so n / 16 + k waves cover every tile.
   const int units = p.n / kTileRows + p.k;
   const int blocks = std::max(1, std::min((units + kWaves - 1) / kWaves, 65535));
-  if (p.bf16)
-    lite_pair_kernel<true><<<blocks, kThreads, 0, stream>>>(a);
-  else
-    lite_pair_kernel<false><<<blocks, kThreads, 0, stream>>>(a);
+  lite_maxima_kernel<<<std::max(1, std::min((p.n + kWaves - 1) / kWaves, 512)), kThreads, 0, stream>>>(a);
+  lite_b_kernel<<<(p.n + kWaves - 1) / kWaves, kThreads, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  lite_select_kernel<<<(p.k + kThreads - 1) / kThreads, kThreads, 0, stream>>>(a);
+  // Groups of more than kSplitTiles tiles: one block per row tile.
+  const int split_blocks = std::max(1, std::min(units, 256));
+  if (p.bf16) {
+    lite_pair_kernel<true><<<blocks, kThreads, 0, stream>>>(a);
+    lite_pair_split_kernel<true><<<split_blocks, kSplitWaves * 64, 0, stream>>>(a);
+  } else {
+    lite_pair_kernel<false><<<blocks, kThreads, 0, stream>>>(a);
+    lite_pair_split_kernel<false><<<split_blocks, kSplitWaves * 64, 0, stream>>>(a);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  lite_select_kernel<<<(p.k + kWaves - 1) / kWaves, kThreads, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (p.objective) {
     lite_total_kernel<<<1, kThreads, 0, stream>>>(a);
