@@ -10,7 +10,10 @@ in HBM: the FST cost (coverprune_fst_cost), the greedy selection of K tokens
 
 Prints one JSON line: prune latency in ms per scene, the dominant kernel's
 roofline fraction, the dense greedy sweep's HBM fraction, and the CPU oracle
-timed on the host for comparison.
+timed on the host for comparison.  Timed beside the step (never inside it):
+the local greedy on 64-nearest tables, the device capacity from 16
+neighbours, the literal greedy (entropic transport per step), and four
+6272-token scenes greedied one by one and in one batched launch.
 """
 from __future__ import annotations
 
