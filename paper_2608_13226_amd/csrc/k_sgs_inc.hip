@@ -132,12 +132,12 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
     if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
   }
 
-  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + blk, epoch_of(0), sg, si);
+  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
 
   for (int step = 0; step < a.k; ++step) {
     // Some block has a candidate while unchosen columns remain; the clamp
     // only keeps a broken slot from addressing past the matrix.
-    const int tw = read_winner(a.cand + (step & 1) * kMaxBlocks, epoch_of(step), nb, a.abort, su, &sflag);
+    const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
     if (tw < 0) break;
     if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
       __int128 L = 0;
@@ -187,7 +187,7 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
       __syncthreads();
     }
     // The barrier above completed this block's list writes.
-    if (tid == 0) put(a.lens + blk, ((unsigned long long)(step + 1) << 32) | unsigned(base));
+    if (tid == 0) put(lens_slot(a.lens, blk), ((unsigned long long)(step + 1) << 32) | unsigned(base));
 
     // The last step's changes only feed the objective, kept by block 0.
     if (step + 1 == a.k && blk != 0) break;
@@ -201,7 +201,7 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
       if (tid < nb) {
         unsigned long long x;
         const unsigned int round = unsigned(step + 1);
-        if (wait_slot(a.lens + tid, a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
+        if (wait_slot(lens_slot(a.lens, tid), a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
           c = int(x & 0xffffffffull);
         else
           slflag = 1;
@@ -299,7 +299,7 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
 
     // 4. This block's candidate for the next step.
     if (step + 1 < a.k)
-      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + ((step + 1) & 1) * kMaxBlocks + blk,
+      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
                      epoch_of(step + 1), sg, si);
   }
   __syncthreads();

@@ -113,10 +113,10 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
   };
 
   local_gains();
-  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + blk, epoch_of(0), sg, si);
+  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
 
   for (int step = 0; step < a.k; ++step) {
-    const int tw = read_winner(a.cand + (step & 1) * kMaxBlocks, epoch_of(step), nb, a.abort, su, &sflag);
+    const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
     if (tw < 0) break;
     if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
       __int128 L = 0;
@@ -164,7 +164,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
       base += tot;
       __syncthreads();
     }
-    if (tid == 0) put(a.lens + blk, ((unsigned long long)(step + 1) << 32) | unsigned(base));
+    if (tid == 0) put(lens_slot(a.lens, blk), ((unsigned long long)(step + 1) << 32) | unsigned(base));
     if (step + 1 == a.k && blk != 0) break;
 
     // 2. Every block's slice length, then every change applied to the
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
       if (tid < nb) {
         unsigned long long x;
         const unsigned int round = unsigned(step + 1);
-        if (wait_slot(a.lens + tid, a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
+        if (wait_slot(lens_slot(a.lens, tid), a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
           c = int(x & 0xffffffffull);
         else
           slflag = 1;
@@ -220,7 +220,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
     // 3. Fresh local gains and this block's candidate for the next step.
     if (step + 1 < a.k) {
       local_gains();
-      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, a.cand + ((step + 1) & 1) * kMaxBlocks + blk,
+      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
                      epoch_of(step + 1), sg, si);
     }
   }

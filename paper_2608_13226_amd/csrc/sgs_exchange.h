@@ -29,6 +29,9 @@ namespace {
 constexpr int kBlock = 512;
 constexpr int kWaves = kBlock / 64;
 constexpr int kMaxBlocks = 256;    // at most one block per compute unit
+// Exchange slots sit one per 128-byte line: packed 8 bytes apart, 16 blocks
+// on different XCDs would write into the line that every block is polling.
+constexpr int kSlotStride = 16;
 constexpr int kIndexBits = 20;     // candidate: [epoch | 43-bit gain | 20-bit inverted index]
 constexpr unsigned long long kIndexMask = (1ull << kIndexBits) - 1ull;
 constexpr unsigned long long kEpoch = 1ull << 63;
@@ -89,11 +92,20 @@ Layout layout(int64_t n, int64_t k) {
   Layout L;
   size_t o = 0;
   L.list = o; o += a256(size_t(n + kMaxBlocks) * 16);
-  L.lens = o; o += a256(size_t(kMaxBlocks) * 8);
-  L.cand = o; o += a256(size_t(2 * kMaxBlocks) * 8);
+  L.lens = o; o += a256(size_t(kMaxBlocks) * kSlotStride * 8);
+  L.cand = o; o += a256(size_t(2 * kMaxBlocks) * kSlotStride * 8);
   L.ctrl = o; o += 256;
   L.total = o;
   return L;
+}
+
+// Block b's candidate slot of slot set `set` (set = step % 2), and its
+// slice-length slot.
+__host__ __device__ __forceinline__ unsigned long long* cand_slot(unsigned long long* cand, int set, int b) {
+  return cand + (size_t(set) * kMaxBlocks + b) * kSlotStride;
+}
+__host__ __device__ __forceinline__ unsigned long long* lens_slot(unsigned long long* lens, int b) {
+  return lens + size_t(b) * kSlotStride;
 }
 
 // Nonnegative gain truncated to its top 43 bits (relative resolution 2^-31),
@@ -114,9 +126,9 @@ __device__ __forceinline__ unsigned long long epoch_of(int step) {
 __global__ void sgs_inc_init_kernel(IncDev a) {
   const int gt = blockIdx.x * blockDim.x + threadIdx.x, nt = gridDim.x * blockDim.x;
   for (int s = gt; s < kMaxBlocks; s += nt) {
-    a.lens[s] = 0ull;
-    a.cand[s] = 0ull;
-    a.cand[kMaxBlocks + s] = 0ull;
+    a.lens[size_t(s) * kSlotStride] = 0ull;
+    a.cand[size_t(s) * kSlotStride] = 0ull;
+    a.cand[size_t(kMaxBlocks + s) * kSlotStride] = 0ull;
   }
   for (int j = gt; j < a.n; j += nt)
     if (a.assign) a.assign[j] = -1;
@@ -272,7 +284,7 @@ __device__ int read_winner(const unsigned long long* slots, unsigned long long e
   __syncthreads();
   if (tid < nb) {
     unsigned long long x;
-    if (wait_slot(slots + tid, abort, [epoch](unsigned long long v) { return (v & kEpoch) == epoch; }, x))
+    if (wait_slot(slots + size_t(tid) * kSlotStride, abort, [epoch](unsigned long long v) { return (v & kEpoch) == epoch; }, x))
       best = x & ~kEpoch;
     else
       *sflag = 1;
