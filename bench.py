@@ -240,7 +240,8 @@ def main():
     cost = torch.empty((n, n), dtype=torch.float32, device=dev)
     maxima = torch.empty(3, dtype=torch.float32, device=dev)
     ws_f = torch.empty(lib.coverprune_fst_cost_workspace(n, d, dt), dtype=torch.uint8, device=dev)
-    ws_s = torch.empty(max(lib.coverprune_sgs_workspace(n, k, f) for f in (cp.CP_SGS_DENSE, cp.CP_SGS_INCREMENTAL)),
+    ws_s = torch.empty(max(lib.coverprune_sgs_workspace(n, k, f) for f in
+                           (cp.CP_SGS_DENSE, cp.CP_SGS_INCREMENTAL, cp.CP_SGS_INCREMENTAL | cp.CP_SGS_COMPACT)),
                        dtype=torch.uint8, device=dev)
     ws_l = torch.empty(lib.coverprune_lite_workspace(n, d, k, dt), dtype=torch.uint8, device=dev)
 
@@ -285,13 +286,13 @@ def main():
     # the greedy's streaming figure.  Algorithmic bytes per launch: the N x N
     # float32 cost read once per step, plus the per-target vectors (capacity
     # and best cost read, best cost written).
-    def time_sgs(incremental, reps):
+    def time_sgs(incremental, reps, compact=False):
         e0 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
         e1 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
         out = None
         for i in range(reps):
             e0[i].record()
-            out = cp.sgs_select(cost, t["capacity"], k, workspace=ws_s, incremental=incremental)
+            out = cp.sgs_select(cost, t["capacity"], k, workspace=ws_s, incremental=incremental, compact=compact)
             e1[i].record()
         torch.cuda.synchronize()
         return float(np.mean([x.elapsed_time(y) for x, y in zip(e0, e1)])), out
@@ -312,8 +313,14 @@ def main():
     # cost, one cost element per target per step (the pick's column), and one
     # row of N costs per target whose best cost the pick lowers.  The number of
     # such (step, target) pairs is replayed on the host from the cost and the
-    # picks, outside the timed region.
+    # picks, outside the timed region.  The transposed copy that the rows
+    # schedule writes in its step-0 pass is not counted.  The compact schedule
+    # (changes exchanged between blocks, no copy) is timed beside it.
+    compact = None
     if args.sgs == "incremental":
+        c_ms, rc = time_sgs(True, 1, compact=True)
+        compact = {"ms": round(c_ms, 3), "us_per_greedy_step": round(c_ms * 1e3 / k, 2),
+                   "same_picks": bool(np.array_equal(rc.selected.cpu().numpy(), sel))}
         C = cost.cpu().numpy()                     # target-major: C[j, s]
         b = np.full(n, np.float32(3.0), np.float32)       # c0: sgs_select's default, the sum of the unit weights
         changed = 0
@@ -326,8 +333,8 @@ def main():
         sgs_bytes = 4.0 * n * n + 4.0 * n * k + 4.0 * n * changed
         sgs_gbs = sgs_bytes / (s_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(sgs_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(sgs_gbs / HBM_PEAK_GBS, 4), "traffic": traffic("sgs_inc_kernel", cfg.name),
-                    "kernel": "sgs_inc_kernel", "bytes_per_launch": sgs_bytes, "ms_per_launch": round(s_ms, 3),
+                    "frac": round(sgs_gbs / HBM_PEAK_GBS, 4), "traffic": traffic("sgs_rows_kernel", cfg.name),
+                    "kernel": "sgs_rows_kernel", "bytes_per_launch": sgs_bytes, "ms_per_launch": round(s_ms, 3),
                     "changed_targets": changed, "us_per_greedy_step": round(s_ms * 1e3 / k, 2)}
     else:
         roofline = {key: dense[key] for key in ("bound", "achieved", "peak", "unit", "frac", "traffic", "kernel")}
@@ -428,7 +435,8 @@ def main():
                                for c, kk in zip(bcosts, bks)), dtype=torch.uint8, device=dev)
         ws_bb = torch.empty(lib.coverprune_sgs_batch_workspace(
             (cp._SgsScene * len(bks))(*[cp._SgsScene(0, 0, int(c.shape[0]), kk, 3.0, 0, 0, 0, 0)
-                                        for c, kk in zip(bcosts, bks)]), len(bks)), dtype=torch.uint8, device=dev)
+                                        for c, kk in zip(bcosts, bks)]), len(bks), cp.CP_SGS_INCREMENTAL),
+                            dtype=torch.uint8, device=dev)
         for _ in range(2):                      # warm-up of both forms
             one = [cp.sgs_select(c, v, kk, workspace=ws_b, incremental=True).selected
                    for c, v, kk in zip(bcosts, bcaps, bks)]
@@ -477,6 +485,7 @@ def main():
             "sgs_select_ms": round(s_ms, 3),
             "sgs_dense_sweep": dense,
             "sgs_dense_same_picks": same,
+            "sgs_compact_schedule": compact,
             "sgs_local": local,
             "fst_capacity": cap,
             "sgs_literal": lit,

@@ -73,6 +73,7 @@ typedef struct {
 /* SGS flags (the same greedy either way; see coverprune_sgs_select). */
 #define CP_SGS_DENSE 0u       /* every step re-evaluates every candidate's gain over the whole cost matrix */
 #define CP_SGS_INCREMENTAL 1u /* gains computed once, then updated from the rows whose best cost drops */
+#define CP_SGS_COMPACT 2u     /* with CP_SGS_INCREMENTAL: the schedule with the small workspace */
 
 /* ------------------------------------------------------------------------ */
 /* FST transport cost (Sec. 3.3, Eq. 7-8).
@@ -161,6 +162,14 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
  *             same float32 differences and float64 products, only the order
  *             of the float64 additions differs, so picks can differ from the
  *             dense sweep only between gains within rounding of each other.
+ *             For n <= 32768 every compute unit keeps all n best costs and
+ *             finds the targets a pick improves itself, from the pick's row
+ *             of a source-major copy of the cost that the first pass writes
+ *             into the workspace (4 n^2 bytes, 1 GiB at n = 16384); larger
+ *             scenes, or CP_SGS_INCREMENTAL | CP_SGS_COMPACT, exchange the
+ *             improved targets between the compute units instead (about 16
+ *             bytes per token, slower per step).  Both schedules sum the
+ *             same integers and return the same result.
  *   selected        [k] int32 output: tokens in the order they were chosen
  *   step_gain       [k] double output (may be NULL): gain of each step
  *   step_objective  [k] double output (may be NULL): L(S) after each step
@@ -168,9 +177,11 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
  *                   token that covers it most cheaply (the earliest chosen among
  *                   equals), or -1 if no chosen token costs less than c0
  */
-/* Workspace for one form (flags as for coverprune_sgs_select): the dense form
- * needs about 9 MB at n = 16384 (private best costs and float64 partial
- * gains of up to 64 row panels), the incremental form about 16 B per token. */
+/* Workspace for one form (flags as for coverprune_sgs_select; 0 for flags it
+ * does not accept): the dense form needs about 9 MB at n = 16384 (private
+ * best costs and float64 partial gains of up to 64 row panels), the
+ * incremental form 4 n + 16 bytes per token up to n = 32768 and about 16
+ * bytes per token beyond that or with CP_SGS_COMPACT. */
 size_t coverprune_sgs_workspace(int64_t n, int64_t k, uint32_t flags);
 cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capacity, int64_t k,
                                 float c0, uint32_t flags, int32_t* selected, double* step_gain,
@@ -195,8 +206,12 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
  *             only); each field as for coverprune_sgs_select, all device memory
  *   count     1 <= count <= CP_SGS_MAX_BATCH (and at most the number of
  *             compute units)
- *   workspace the sum of the scenes' incremental workspaces, laid out one
- *             after another; size from coverprune_sgs_batch_workspace
+ *   flags     CP_SGS_INCREMENTAL, or CP_SGS_INCREMENTAL | CP_SGS_COMPACT (as
+ *             for coverprune_sgs_select; the small-workspace schedule also
+ *             runs when any scene exceeds n = 32768)
+ *   workspace the sum of the scenes' incremental workspaces for `flags`, laid
+ *             out one after another; size from coverprune_sgs_batch_workspace
+ *             (0 for bad scenes, count or flags)
  */
 #define CP_SGS_MAX_BATCH 16
 typedef struct {
@@ -211,9 +226,9 @@ typedef struct {
   int32_t* assign;         /* [n] or NULL */
 } cp_sgs_scene;
 
-size_t coverprune_sgs_batch_workspace(const cp_sgs_scene* scenes, int32_t count);
-cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count, void* workspace,
-                                      size_t workspace_bytes, void* stream);
+size_t coverprune_sgs_batch_workspace(const cp_sgs_scene* scenes, int32_t count, uint32_t flags);
+cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count, uint32_t flags,
+                                      void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Spatially local greedy (Sec. 3.5, Eq. 13).

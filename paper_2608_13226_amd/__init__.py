@@ -26,6 +26,7 @@ DEFAULT_KAPPA = 10.0
 CP_F32, CP_BF16 = 0, 1
 CP_SGS_DENSE = 0
 CP_SGS_INCREMENTAL = 1
+CP_SGS_COMPACT = 2
 
 
 class CoverPruneError(RuntimeError):
@@ -78,9 +79,9 @@ def library() -> ctypes.CDLL:
     lib.coverprune_fst_capacity.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, i64, _CapWeights, vp, vp, vp, sz,
                                             vp]
     lib.coverprune_fst_capacity.restype = st
-    lib.coverprune_sgs_batch_workspace.argtypes = [ctypes.POINTER(_SgsScene), ctypes.c_int32]
+    lib.coverprune_sgs_batch_workspace.argtypes = [ctypes.POINTER(_SgsScene), ctypes.c_int32, ctypes.c_uint32]
     lib.coverprune_sgs_batch_workspace.restype = sz
-    lib.coverprune_sgs_select_batch.argtypes = [ctypes.POINTER(_SgsScene), ctypes.c_int32, vp, sz, vp]
+    lib.coverprune_sgs_select_batch.argtypes = [ctypes.POINTER(_SgsScene), ctypes.c_int32, ctypes.c_uint32, vp, sz, vp]
     lib.coverprune_sgs_select_batch.restype = st
     lib.coverprune_sgs_literal_workspace.argtypes = [i64, i64]
     lib.coverprune_sgs_literal_workspace.restype = sz
@@ -222,11 +223,12 @@ class SgsResult:
 
 def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[float] = None,
                weights=(1.0, 1.0, 1.0), workspace: Optional[torch.Tensor] = None,
-               stream=None, incremental: bool = False) -> SgsResult:
+               stream=None, incremental: bool = False, compact: bool = False) -> SgsResult:
     """Greedy selection of k tokens over a target-major cost (Sec. 3.5, Eq. 11-16).
     c0 defaults to the sum of the cost weights, the largest value C takes.
     incremental=True runs the same greedy with gains updated from the rows
-    whose best cost drops (CP_SGS_INCREMENTAL) instead of full sweeps."""
+    whose best cost drops (CP_SGS_INCREMENTAL) instead of full sweeps;
+    compact=True (with incremental) picks the small-workspace schedule."""
     lib = library()
     n = cost.shape[0]
     dev = cost.device
@@ -238,7 +240,9 @@ def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[
     gain = torch.empty(int(k), dtype=torch.float64, device=dev)
     obj = torch.empty(int(k), dtype=torch.float64, device=dev)
     assign = torch.empty(n, dtype=torch.int32, device=dev)
-    flags = CP_SGS_INCREMENTAL if incremental else CP_SGS_DENSE
+    if compact and not incremental:
+        raise ValueError("compact=True needs incremental=True")
+    flags = (CP_SGS_INCREMENTAL | (CP_SGS_COMPACT if compact else 0)) if incremental else CP_SGS_DENSE
     need = lib.coverprune_sgs_workspace(n, int(k), flags)
     if workspace is None:
         workspace = _workspace(need, dev)
@@ -249,9 +253,10 @@ def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[
 
 
 def sgs_select_batch(costs, capacities, ks, c0: Optional[float] = None, weights=(1.0, 1.0, 1.0),
-                     workspace: Optional[torch.Tensor] = None, stream=None):
+                     workspace: Optional[torch.Tensor] = None, stream=None, compact: bool = False):
     """The incremental greedy of several scenes (lists of target-major costs,
-    capacities and budgets) in one launch.  Returns one SgsResult per scene."""
+    capacities and budgets) in one launch.  Returns one SgsResult per scene.
+    compact=True picks the small-workspace schedule."""
     lib = library()
     count = len(costs)
     if not (len(capacities) == len(ks) == count):
@@ -272,10 +277,12 @@ def sgs_select_batch(costs, capacities, ks, c0: Optional[float] = None, weights=
         arr[s] = _SgsScene(cost.data_ptr(), cap.data_ptr(), n, int(k), float(c0), r.selected.data_ptr(),
                            r.gain.data_ptr(), r.objective.data_ptr(), r.assign.data_ptr())
         out.append(r)
-    need = lib.coverprune_sgs_batch_workspace(arr, count)
+    flags = CP_SGS_INCREMENTAL | (CP_SGS_COMPACT if compact else 0)
+    need = lib.coverprune_sgs_batch_workspace(arr, count, flags)
     if workspace is None:
         workspace = _workspace(need, costs[0].device if count else None)
-    _check(lib.coverprune_sgs_select_batch(arr, count, _ptr(workspace), workspace.numel(), _stream(stream)))
+    _check(lib.coverprune_sgs_select_batch(arr, count, flags, _ptr(workspace), workspace.numel(),
+                                           _stream(stream)))
     return out
 
 

@@ -145,8 +145,10 @@ cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int6
 // ---------------------------------------------------------------------------
 size_t coverprune_sgs_workspace(int64_t n, int64_t k, uint32_t flags) {
   if (n < 1 || k < 1) return 0;
-  if (flags == CP_SGS_INCREMENTAL) return cp::sgs_inc_workspace_bytes(n, k);
-  return cp::sgs_workspace_bytes(n, k);
+  if (flags == CP_SGS_INCREMENTAL) return cp::sgs_inc_workspace_bytes(n, k, false);
+  if (flags == (CP_SGS_INCREMENTAL | CP_SGS_COMPACT)) return cp::sgs_inc_workspace_bytes(n, k, true);
+  if (flags == CP_SGS_DENSE) return cp::sgs_workspace_bytes(n, k);
+  return 0;
 }
 
 cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capacity, int64_t k,
@@ -156,7 +158,8 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
   if (n < 1 || n > kMaxDenseN) return fail(CP_ERR_INVALID_ARG, "n = %lld outside [1, %lld]", (long long)n, (long long)kMaxDenseN);
   if (k < 1 || k > n) return fail(CP_ERR_INVALID_ARG, "k = %lld outside [1, n = %lld]", (long long)k, (long long)n);
   if (!std::isfinite(c0)) return fail(CP_ERR_INVALID_ARG, "c0 must be finite");
-  if (flags != CP_SGS_DENSE && flags != CP_SGS_INCREMENTAL) return fail(CP_ERR_UNSUPPORTED, "unknown flags 0x%x", flags);
+  if (flags != CP_SGS_DENSE && flags != CP_SGS_INCREMENTAL && flags != (CP_SGS_INCREMENTAL | CP_SGS_COMPACT))
+    return fail(CP_ERR_UNSUPPORTED, "unknown flags 0x%x", flags);
   if (!cost || !capacity || !selected) return fail(CP_ERR_INVALID_ARG, "cost, capacity and selected must be non-NULL");
   if (!aligned16(cost)) return fail(CP_ERR_INVALID_ARG, "cost is not 16-byte aligned");
   cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_workspace(n, k, flags));
@@ -174,27 +177,33 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
   p.assign = assign;
   p.workspace = workspace;
   p.workspace_bytes = workspace_bytes;
-  hipError_t e = flags == CP_SGS_INCREMENTAL ? cp::launch_sgs_incremental(p, static_cast<hipStream_t>(stream))
-                                             : cp::launch_sgs_dense(p, static_cast<hipStream_t>(stream));
+  hipError_t e = flags == CP_SGS_DENSE
+                     ? cp::launch_sgs_dense(p, static_cast<hipStream_t>(stream))
+                     : cp::launch_sgs_incremental(p, (flags & CP_SGS_COMPACT) != 0, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "sgs");
   return ok();
 }
 
 // ---------------------------------------------------------------------------
-size_t coverprune_sgs_batch_workspace(const cp_sgs_scene* scenes, int32_t count) {
-  if (!scenes || count < 1 || count > CP_SGS_MAX_BATCH) return 0;
+static bool batch_flags_ok(uint32_t flags) {
+  return flags == CP_SGS_INCREMENTAL || flags == (CP_SGS_INCREMENTAL | CP_SGS_COMPACT);
+}
+
+size_t coverprune_sgs_batch_workspace(const cp_sgs_scene* scenes, int32_t count, uint32_t flags) {
+  if (!scenes || count < 1 || count > CP_SGS_MAX_BATCH || !batch_flags_ok(flags)) return 0;
   int64_t n[CP_SGS_MAX_BATCH], k[CP_SGS_MAX_BATCH];
   for (int32_t s = 0; s < count; ++s) {
     if (scenes[s].n < 1 || scenes[s].k < 1) return 0;
     n[s] = scenes[s].n;
     k[s] = scenes[s].k;
   }
-  return cp::sgs_inc_batch_workspace_bytes(n, k, int(count));
+  return cp::sgs_inc_batch_workspace_bytes(n, k, int(count), (flags & CP_SGS_COMPACT) != 0);
 }
 
-cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count, void* workspace,
-                                      size_t workspace_bytes, void* stream) {
+cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count, uint32_t flags,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
   if (!scenes) return fail(CP_ERR_INVALID_ARG, "scenes is NULL");
+  if (!batch_flags_ok(flags)) return fail(CP_ERR_UNSUPPORTED, "unknown flags 0x%x", flags);
   if (count < 1 || count > CP_SGS_MAX_BATCH)
     return fail(CP_ERR_INVALID_ARG, "count = %d outside [1, %d]", (int)count, CP_SGS_MAX_BATCH);
   cp::SgsParams p[CP_SGS_MAX_BATCH];
@@ -220,9 +229,10 @@ cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count,
     p[s].workspace = nullptr;
     p[s].workspace_bytes = 0;
   }
-  cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_batch_workspace(scenes, count));
+  cp_status st = check_workspace(workspace, workspace_bytes, coverprune_sgs_batch_workspace(scenes, count, flags));
   if (st != CP_OK) return st;
-  hipError_t e = cp::launch_sgs_incremental_batch(p, int(count), workspace, static_cast<hipStream_t>(stream));
+  hipError_t e = cp::launch_sgs_incremental_batch(p, int(count), (flags & CP_SGS_COMPACT) != 0, workspace,
+                                                  static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "sgs batch");
   return ok();
 }

@@ -95,19 +95,34 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   for (int cc = 0; cc < cnt; cc += 64) {
     const bool colok = cc + lane < cnt;
     const int col = lo + cc + lane;
-    __int128 g = 0;
+    // The next chunk's loads are issued before the current chunk's terms
+    // are formed; two accumulators halve the chain of 128-bit additions.
+    __int128 g0 = 0, g1 = 0;
+    float xn[kInitRows], vn[kInitRows];
+    auto load = [&](int j0) {
+#pragma unroll
+      for (int u = 0; u < kInitRows; ++u) {
+        const int j = j0 + u;
+        xn[u] = (colok && j < a.n) ? __builtin_nontemporal_load(a.C + size_t(j) * a.n + col) : a.c0;
+        vn[u] = j < a.n ? a.v[j] : 0.f;
+      }
+    };
+    if (w * kInitRows < a.n) load(w * kInitRows);
     for (int j0 = w * kInitRows; j0 < a.n; j0 += kWaves * kInitRows) {
       float x[kInitRows], vj[kInitRows];
 #pragma unroll
       for (int u = 0; u < kInitRows; ++u) {
-        const int j = j0 + u;
-        x[u] = (colok && j < a.n) ? __builtin_nontemporal_load(a.C + size_t(j) * a.n + col) : a.c0;
-        vj[u] = j < a.n ? a.v[j] : 0.f;
+        x[u] = xn[u];
+        vj[u] = vn[u];
       }
+      if (j0 + kWaves * kInitRows < a.n) load(j0 + kWaves * kInitRows);
 #pragma unroll
-      for (int u = 0; u < kInitRows; ++u) g += fx(double(vj[u]) * double(fmaxf(a.c0 - x[u], 0.f)), S);
+      for (int u = 0; u < kInitRows; u += 2) {
+        g0 += fx(double(vj[u]) * double(fmaxf(a.c0 - x[u], 0.f)), S);
+        g1 += fx(double(vj[u + 1]) * double(fmaxf(a.c0 - x[u + 1], 0.f)), S);
+      }
     }
-    red[tid] = g;
+    red[tid] = g0 + g1;
     __syncthreads();
     if (tid < 64 && cc + tid < cnt) {
       __int128 s = 0;
@@ -287,12 +302,7 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
       __syncthreads();
     }
     if (blk == 0) {
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const unsigned long long olo = __shfl_xor((unsigned long long)dobj, o);
-        const long long ohi = __shfl_xor((long long)(dobj >> 64), o);
-        dobj += ((__int128)ohi << 64) | (__int128)olo;
-      }
+      dobj = wave_sum_i128(dobj);
       if (lane == 0) sLw[w] += dobj;
       obj_step = step;
     }
@@ -313,7 +323,388 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
     for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
 }
 
+// ---------------------------------------------------------------------------
+// Rows form of the same greedy, for scenes whose n best costs fit in LDS.
+//
+// The exchange form learns J_l from the owners of the rows (a pass over the
+// own rows, an exchange of slice lengths, a walk of the change list).  Here
+// every block keeps all n best costs b_j in LDS and finds J_l itself: it
+// reads the winner's costs to every target, C(t_l, j) for all j, as one
+// contiguous row of a source-major copy T of the cost (T[s][j] = C(s, j)),
+// tests each against b_j, and applies the rows that improve straight away.
+// Every block then holds the identical J_l and the identical b, a step needs
+// one exchange (the candidates) instead of two, and no block reads another's
+// list.  T is written by the step-0 pass, which reads the whole cost in
+// column strips anyway: block b writes the rows of T of its own columns.
+//
+// Per step and wave: the wave's chunks of the winner's row (256 targets a
+// load, 16 bytes a lane) are loaded together; a chunk without a hit costs one
+// LDS read and four compares; hits are compacted into the wave's list in LDS
+// (target, old b, new b) and their rows' segments over the block's columns
+// are read 16 rows at a time.  The block's columns' deltas are then summed
+// over the waves in wave order, as in the exchange form, and are the same
+// integers, so both forms take the same picks.
+constexpr int kRowsMaxN = 32768;   // 128 KB of best costs in LDS
+constexpr int kRowsMaxW = 128;     // columns per block: two per lane
+constexpr int kRowChunk = 256;     // targets per wave-load of the winner's row
+constexpr int kList = 128;         // hits a wave collects before applying them (dense steps)
+constexpr int kCap = kList * kWaves;   // hits a block lists in one step
+constexpr int kInitRowsT = 16;     // rows a wave has in flight in the transposing pass
+
+int rows_ldt(int64_t n) { return int((n + kRowChunk - 1) / kRowChunk * kRowChunk); }
+
+// Fixed-point scale, the same in every block (same sum, same order): every
+// partial gain is at most c0 sum(v) < 2^(101 - S).
+__device__ __forceinline__ int fixed_scale(const IncDev& a, double* sd) {
+  double x = 0.0;
+  for (int j = threadIdx.x; j < a.n; j += kBlock) x += double(a.v[j]);
+  const double M = double(a.c0) * block_sum_all(x, sd);
+  int S = 0;
+  if (M > 0.0) {
+    int e = 0;
+    (void)__builtin_frexp(M, &e);   // M < 2^e
+    S = 101 - e;
+  }
+  return S;
+}
+
+// NG 64-column groups per block (W <= 64 NG); RL chunk loads per wave and
+// step (n <= kRowChunk kWaves RL).
+template <int NG, int RL>
+__device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
+  extern __shared__ unsigned long long smem[];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lo = blk * a.W;
+  const int cnt = max(0, min(a.n, lo + a.W) - lo);
+  unsigned long long* sGlo = smem;                                 // [W] running gains, low words
+  long long* sGhi = reinterpret_cast<long long*>(sGlo + a.W);      // [W] high words
+  float* sball = reinterpret_cast<float*>(sGhi + a.W);             // [ldt] b_j; -inf past n (never a hit)
+  unsigned char* ssel = reinterpret_cast<unsigned char*>(sball + a.ldt);   // [W] chosen columns
+  __shared__ __int128 red[kBlock];
+  __shared__ __int128 sg[kWaves];
+  __shared__ double sd[kWaves];
+  __shared__ int si[kWaves];
+  __shared__ unsigned long long su[kWaves];
+  __shared__ int sflag;
+  __shared__ int lj[kCap];                    // hit list: target
+  __shared__ float lbo[kCap];                 // old best cost
+  __shared__ float lbn[kCap];                 // new best cost
+  __shared__ int scnt[2];                     // hits listed in steps of each parity
+  __shared__ int schunk[kRowsMaxN / kRowChunk];   // dense steps: hits per chunk, then their offsets
+  if (tid == 0) scnt[0] = scnt[1] = 0;
+
+  for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
+  for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
+  const int S = fixed_scale(a, sd);
+
+  // Step-0 gains of the own columns (every row at b = c0), and the own rows
+  // of T: lane `col` holds C_tm[j0 .. j0 + 16)[col], which is T[col][j0 ..
+  // j0 + 16), half a 128-byte line whose other half the next wave writes in
+  // the same round.  Wave w takes the 16-row chunks w, w + kWaves, ...; the
+  // waves' sums are added in wave order.
+  for (int cc = 0; cc < cnt; cc += 64) {
+    const bool colok = cc + lane < cnt;
+    const int col = lo + cc + lane;
+    f32x4* trow = reinterpret_cast<f32x4*>(a.T + size_t(colok ? col : 0) * a.ldt);
+    // The next chunk's loads are issued before the current chunk's terms
+    // are formed; two accumulators halve the chain of 128-bit additions.
+    __int128 g0 = 0, g1 = 0;
+    float xn[kInitRowsT], vn[kInitRowsT];
+    auto load = [&](int j0) {
+#pragma unroll
+      for (int u = 0; u < kInitRowsT; ++u) {
+        const int j = j0 + u;
+        xn[u] = (colok && j < a.n) ? __builtin_nontemporal_load(a.C + size_t(j) * a.n + col) : a.c0;
+        vn[u] = j < a.n ? a.v[j] : 0.f;
+      }
+    };
+    if (w * kInitRowsT < a.n) load(w * kInitRowsT);
+    for (int j0 = w * kInitRowsT; j0 < a.n; j0 += kWaves * kInitRowsT) {
+      float x[kInitRowsT], vj[kInitRowsT];
+#pragma unroll
+      for (int u = 0; u < kInitRowsT; ++u) {
+        x[u] = xn[u];
+        vj[u] = vn[u];
+      }
+      if (j0 + kWaves * kInitRowsT < a.n) load(j0 + kWaves * kInitRowsT);
+#pragma unroll
+      for (int u = 0; u < kInitRowsT; u += 2) {
+        g0 += fx(double(vj[u]) * double(fmaxf(a.c0 - x[u], 0.f)), S);
+        g1 += fx(double(vj[u + 1]) * double(fmaxf(a.c0 - x[u + 1], 0.f)), S);
+      }
+      // Ordinary (write-back) stores: the two halves of a line meet in L2.
+      if (colok) {
+#pragma unroll
+        for (int q = 0; q < kInitRowsT / 4; ++q)
+          trow[j0 / 4 + q] = f32x4{x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
+      }
+    }
+    red[tid] = g0 + g1;
+    __syncthreads();
+    if (tid < 64 && cc + tid < cnt) {
+      __int128 s = 0;
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) s += red[q * 64 + tid];
+      sGlo[cc + tid] = (unsigned long long)s;
+      sGhi[cc + tid] = (long long)(s >> 64);
+    }
+    __syncthreads();
+  }
+  // The rows of T are read by every block: each wave's writes reach memory
+  // before the block's step-0 candidate is published, and every block
+  // acquires after it has read all candidates of step 0.
+  __threadfence();
+  __syncthreads();
+
+  // Block 0 keeps the objective as one running part per wave (as in the
+  // exchange form).
+  __shared__ __int128 sLw[kWaves];
+  int obj_step = -1;
+  if (blk == 0) {
+    __int128 x = 0;
+    for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
+    const __int128 L0 = block_sum_i128(x, sg);
+    if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
+  }
+
+  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
+
+  const int nch = a.ldt / kRowChunk;
+  for (int step = 0; step < a.k; ++step) {
+    const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
+    if (tw < 0) break;
+    if (step == 0) __threadfence();
+    if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
+      __int128 L = 0;
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) L += sLw[q];
+      a.step_obj[obj_step] = fx_to_double(L, S);
+    }
+    const int t = min(tw, a.n - 1);
+    if (t >= lo && t < lo + cnt && tid == 0) {
+      ssel[t - lo] = 1;
+      a.selected[step] = t;
+      if (a.step_gain) a.step_gain[step] = fx_to_double(((__int128)sGhi[t - lo] << 64) | (__int128)sGlo[t - lo], S);
+    }
+
+    // The wave's chunks of the winner's row, all loads in flight together.
+    const f32x4* row = reinterpret_cast<const f32x4*>(a.T + size_t(t) * a.ldt);
+    f32x4 xr[RL];
+#pragma unroll
+    for (int i = 0; i < RL; ++i)
+      if (w + i * kWaves < nch) xr[i] = row[(w + i * kWaves) * (kRowChunk / 4) + lane];
+
+    __int128 g[NG];
+#pragma unroll
+    for (int q = 0; q < NG; ++q) g[q] = 0;
+    __int128 dobj = 0;
+    // Applies listed hits base .. base + m to the wave's partial gains (and,
+    // in block 0, to the objective), and records them in assign and (with
+    // setb) in b.
+    auto apply = [&](int base, int m, bool setb) {
+      // Lane u < kChunk of a batch holds entry e0 + u and its capacity; the
+      // entries are broadcast with readlane.  The next batch's entries and
+      // row reads are issued before the current batch's terms are summed.
+      int jl = 0;
+      float bol = 0.f, bnl = 0.f, vl = 0.f;
+      float xc[kChunk][NG];
+      auto fetch = [&](int e0) {
+        const int nbt = min(kChunk, base + m - e0);
+        jl = 0;
+        bol = bnl = vl = 0.f;
+        if (lane < nbt) {
+          jl = lj[e0 + lane];
+          bol = lbo[e0 + lane];
+          bnl = lbn[e0 + lane];
+          vl = a.v[jl];
+        }
+#pragma unroll
+        for (int u = 0; u < kChunk; ++u) {
+          const int j = __builtin_amdgcn_readlane(jl, u);
+#pragma unroll
+          for (int q = 0; q < NG; ++q)
+            xc[u][q] = (u < nbt && q * 64 + lane < cnt) ? a.C[size_t(j) * a.n + lo + q * 64 + lane] : 0.f;
+        }
+      };
+      if (m > 0) fetch(base);
+      for (int e0 = base; e0 < base + m; e0 += kChunk) {
+        const int nbt = min(kChunk, base + m - e0);
+        const int cj = jl;
+        const float cbo = bol, cbn = bnl, cv = vl;
+        float cx[kChunk][NG];
+#pragma unroll
+        for (int u = 0; u < kChunk; ++u)
+#pragma unroll
+          for (int q = 0; q < NG; ++q) cx[u][q] = xc[u][q];
+        if (e0 + kChunk < base + m) fetch(e0 + kChunk);
+#pragma unroll
+        for (int u = 0; u < kChunk; ++u) {
+          if (u < nbt) {
+            const float bo = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cbo), u));
+            const float bn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cbn), u));
+            const double vv = double(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(cv), u)));
+#pragma unroll
+            for (int q = 0; q < NG; ++q) {
+              // A column that cost at least the old best contributes 0
+              // before and after.
+              const float xx = cx[u][q];
+              if (q * 64 + lane < cnt && xx < bo)
+                g[q] += fx(vv * double(fmaxf(bn - xx, 0.f)), S) - fx(vv * double(bo - xx), S);
+            }
+          }
+        }
+        // The batch's targets, one lane each: objective (block 0), b and assign.
+        if (lane < nbt) {
+          if (blk == 0) dobj += fx(double(cv) * double(cbn), S) - fx(double(cv) * double(cbo), S);
+          if (setb) sball[cj] = cbn;
+          if (a.assign && unsigned(cj - lo) < unsigned(cnt)) a.assign[cj] = t;
+        }
+      }
+    };
+
+    // Fast path: the waves list the hits of their chunks in one block-wide
+    // list (a chunk's hits reserve their places with one LDS atomic), and
+    // after a barrier each wave applies an equal share of it: the targets a
+    // pick improves lie close together, in few chunks of few waves.
+    const int par = step & 1;
+#pragma unroll
+    for (int i = 0; i < RL; ++i) {
+      const int q0 = w + i * kWaves;
+      if (q0 < nch) {
+        const int j0 = q0 * kRowChunk + 4 * lane;     // this lane's four targets
+        const f32x4 bo = *reinterpret_cast<const f32x4*>(sball + j0);
+        const f32x4 x = xr[i];
+        const unsigned long long m0 = __ballot(x[0] < bo[0]), m1 = __ballot(x[1] < bo[1]);
+        const unsigned long long m2 = __ballot(x[2] < bo[2]), m3 = __ballot(x[3] < bo[3]);
+        if ((m0 | m1 | m2 | m3) != 0ull) {
+          const unsigned long long lt = (1ull << lane) - 1ull;
+          const int tot = __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+          int at = 0;
+          if (lane == 0) at = atomicAdd(&scnt[par], tot);
+          at = __builtin_amdgcn_readlane(at, 0);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const unsigned long long mk = c == 0 ? m0 : c == 1 ? m1 : c == 2 ? m2 : m3;
+            const int e = at + __popcll(mk & lt);
+            if (((mk >> lane) & 1ull) && e < kCap) {
+              lj[e] = j0 + c;
+              lbo[e] = bo[c];
+              lbn[e] = x[c];
+            }
+            at += __popcll(mk);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    const int total = scnt[par];
+    if (tid == 0) scnt[par ^ 1] = 0;   // last read in the previous step, next used in the next
+    if (total <= kCap) {
+      const int per = (total + kWaves - 1) / kWaves;
+      const int e0 = min(total, w * per);
+      apply(e0, min(total, e0 + per) - e0, true);
+    } else {
+      // Dense step (early in the greedy): the list is built and applied in
+      // rounds of kCap entries, each entry's place fixed by the hit counts
+      // of the chunks before it, and every round is shared evenly by the
+      // waves.  b keeps its old values until the last round (the hit test is
+      // repeated each round), then takes the new ones.
+      for (int q0 = w; q0 < nch; q0 += kWaves) {
+        const int j0 = q0 * kRowChunk + 4 * lane;
+        const f32x4 bo = *reinterpret_cast<const f32x4*>(sball + j0);
+        const f32x4 x = row[q0 * (kRowChunk / 4) + lane];
+        const int c = __popcll(__ballot(x[0] < bo[0])) + __popcll(__ballot(x[1] < bo[1])) +
+                      __popcll(__ballot(x[2] < bo[2])) + __popcll(__ballot(x[3] < bo[3]));
+        if (lane == 0) schunk[q0] = c;
+      }
+      __syncthreads();
+      if (w == 0) {
+        // Exclusive prefix of the chunk counts, two chunks a lane.
+        const int c0 = 2 * lane < nch ? schunk[2 * lane] : 0;
+        const int c1 = 2 * lane + 1 < nch ? schunk[2 * lane + 1] : 0;
+        const int incl = wave_scan_incl(c0 + c1);
+        if (2 * lane < nch) schunk[2 * lane] = incl - c0 - c1;
+        if (2 * lane + 1 < nch) schunk[2 * lane + 1] = incl - c1;
+      }
+      __syncthreads();
+      for (int r0 = 0; r0 < total; r0 += kCap) {
+        for (int q0 = w; q0 < nch; q0 += kWaves) {
+          const int j0 = q0 * kRowChunk + 4 * lane;
+          const f32x4 bo = *reinterpret_cast<const f32x4*>(sball + j0);
+          const f32x4 x = row[q0 * (kRowChunk / 4) + lane];
+          int at = schunk[q0] - r0;
+          for (int c = 0; c < 4; ++c) {
+            const bool hit = x[c] < bo[c];
+            const unsigned long long mk = __ballot(hit);
+            const int e = at + __popcll(mk & ((1ull << lane) - 1ull));
+            if (hit && e >= 0 && e < kCap) {
+              lj[e] = j0 + c;
+              lbo[e] = bo[c];
+              lbn[e] = x[c];
+            }
+            at += __popcll(mk);
+          }
+        }
+        __syncthreads();
+        const int m = min(kCap, total - r0);
+        const int per = (m + kWaves - 1) / kWaves;
+        const int e0 = min(m, w * per);
+        apply(e0, min(m, e0 + per) - e0, false);
+        __syncthreads();
+      }
+      for (int q0 = w; q0 < nch; q0 += kWaves) {
+        const int j0 = q0 * kRowChunk + 4 * lane;
+        f32x4 b = *reinterpret_cast<const f32x4*>(sball + j0);
+        const f32x4 x = row[q0 * (kRowChunk / 4) + lane];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) b[c] = x[c] < b[c] ? x[c] : b[c];
+        *reinterpret_cast<f32x4*>(sball + j0) = b;
+      }
+    }
+
+    // The waves' partial gains, added in wave order by wave 0.  With one
+    // column group wave 0 then publishes the candidate on its own (the next
+    // step begins with a barrier); with two the general publish reads every
+    // column after a barrier.
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+      red[tid] = g[q];
+      __syncthreads();
+      if (tid < 64 && q * 64 + tid < cnt) {
+        const int c = q * 64 + tid;
+        __int128 s = ((__int128)sGhi[c] << 64) | (__int128)sGlo[c];
+#pragma unroll
+        for (int r = 0; r < kWaves; ++r) s += red[r * 64 + tid];
+        sGlo[c] = (unsigned long long)s;
+        sGhi[c] = (long long)(s >> 64);
+      }
+      if (NG > 1) __syncthreads();
+    }
+    if (blk == 0) {
+      dobj = wave_sum_i128(dobj);
+      if (lane == 0) sLw[w] += dobj;
+      obj_step = step;
+    }
+
+    if (step + 1 < a.k)
+      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
+                     epoch_of(step + 1), sg, si);
+  }
+  __syncthreads();
+  if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
+    __int128 L = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) L += sLw[q];
+    a.step_obj[obj_step] = fx_to_double(L, S);
+  }
+  if (blk == 0 && get(a.abort))
+    for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
+}
+
 __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) { inc_body(a, blockIdx.x, gridDim.x); }
+
+template <int NG, int RL>
+__global__ __launch_bounds__(kBlock) void sgs_rows_kernel(IncDev a) { rows_body<NG, RL>(a, blockIdx.x, gridDim.x); }
 
 // Several scenes in one launch: scene s runs on blocks [g0[s], g0[s + 1])
 // with its own slots, change lists and abort flag, so the scenes' greedies
@@ -332,7 +723,39 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_batch_kernel(IncBatch b) {
   inc_body(b.scene[s], int(blockIdx.x) - b.g0[s], b.g0[s + 1] - b.g0[s]);
 }
 
-IncDev inc_dev(const SgsParams& p, char* w, int W) {
+template <int NG, int RL>
+__global__ __launch_bounds__(kBlock) void sgs_rows_batch_kernel(IncBatch b) {
+  int s = 0;
+  while (s + 1 < b.count && int(blockIdx.x) >= b.g0[s + 1]) ++s;
+  rows_body<NG, RL>(b.scene[s], int(blockIdx.x) - b.g0[s], b.g0[s + 1] - b.g0[s]);
+}
+
+// The rows form runs when the scene's best costs fit in LDS and a block has
+// at most two columns per lane; otherwise the exchange form.
+bool use_rows(int64_t n, int W) { return n <= kRowsMaxN && W <= kRowsMaxW; }
+
+// The instance for the largest n and W of a launch.
+constexpr int kRowsSmallN = kRowChunk * kWaves * 8;
+const void* rows_kernel(int64_t n, int W) {
+  if (n <= kRowsSmallN)
+    return W <= 64 ? reinterpret_cast<const void*>(sgs_rows_kernel<1, 8>)
+                   : reinterpret_cast<const void*>(sgs_rows_kernel<2, 8>);
+  return reinterpret_cast<const void*>(sgs_rows_kernel<2, 16>);
+}
+const void* rows_batch_kernel(int64_t n, int W) {
+  if (n <= kRowsSmallN)
+    return W <= 64 ? reinterpret_cast<const void*>(sgs_rows_batch_kernel<1, 8>)
+                   : reinterpret_cast<const void*>(sgs_rows_batch_kernel<2, 8>);
+  return reinterpret_cast<const void*>(sgs_rows_batch_kernel<2, 16>);
+}
+
+// Exchange slots and lists, then (when the rows form may run) T.
+size_t inc_bytes(int64_t n, int64_t k, bool compact) {
+  const size_t base = layout(n, k).total;
+  return !compact && n <= kRowsMaxN ? base + a256(size_t(n) * rows_ldt(n) * sizeof(float)) : base;
+}
+
+IncDev inc_dev(const SgsParams& p, char* w, int W, bool rows) {
   const Layout L = layout(p.n, p.k);
   IncDev a;
   a.C = p.cost;
@@ -349,44 +772,52 @@ IncDev inc_dev(const SgsParams& p, char* w, int W) {
   a.cand = reinterpret_cast<unsigned long long*>(w + L.cand);
   a.abort = reinterpret_cast<unsigned int*>(w + L.ctrl);
   a.W = W;
+  a.T = rows ? reinterpret_cast<float*>(w + L.total) : nullptr;
+  a.ldt = rows ? rows_ldt(p.n) : 0;
   return a;
 }
 
 size_t lds_for(int W) { return size_t(W) * (16 + 4 + 4 + 1) + 16; }
+size_t lds_rows(int W, int64_t n) { return size_t(W) * (16 + 1) + size_t(rows_ldt(n)) * 4 + 16; }
+
+hipError_t fits(const void* kernel, size_t lds) {
+  int per_cu = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kBlock, lds);
+  if (e != hipSuccess) return e;
+  return per_cu < 1 ? hipErrorCooperativeLaunchTooLarge : hipSuccess;
+}
 
 }  // namespace
 
-size_t sgs_inc_workspace_bytes(int64_t n, int64_t k) { return layout(n, k).total; }
+size_t sgs_inc_workspace_bytes(int64_t n, int64_t k, bool compact) { return inc_bytes(n, k, compact); }
 
-hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream) {
+hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t stream) {
   int dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
   const int nb = blocks_for(p.n, cus);
   const int W = (p.n + nb - 1) / nb;
-  const size_t lds = lds_for(W);
-  int per_cu = 0;
-  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(sgs_inc_kernel),
-                                                        kBlock, lds)) != hipSuccess)
-    return e;
-  if (per_cu < 1) return hipErrorCooperativeLaunchTooLarge;
+  const bool rows = !compact && use_rows(p.n, W);
+  const void* kernel = rows ? rows_kernel(p.n, W) : reinterpret_cast<const void*>(sgs_inc_kernel);
+  const size_t lds = rows ? lds_rows(W, p.n) : lds_for(W);
+  if ((e = fits(kernel, lds)) != hipSuccess) return e;
 
-  IncDev a = inc_dev(p, static_cast<char*>(p.workspace), W);
+  IncDev a = inc_dev(p, static_cast<char*>(p.workspace), W, rows);
   sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   void* args[] = {&a};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_inc_kernel), dim3(nb), dim3(kBlock), args,
-                                    lds, stream);
+  return hipLaunchCooperativeKernel(kernel, dim3(nb), dim3(kBlock), args, lds, stream);
 }
 
-size_t sgs_inc_batch_workspace_bytes(const int64_t* n, const int64_t* k, int count) {
+size_t sgs_inc_batch_workspace_bytes(const int64_t* n, const int64_t* k, int count, bool compact) {
   size_t total = 0;
-  for (int s = 0; s < count; ++s) total += layout(n[s], k[s]).total;
+  for (int s = 0; s < count; ++s) total += inc_bytes(n[s], k[s], compact);
   return total;
 }
 
-hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, void* workspace, hipStream_t stream) {
+hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, bool compact, void* workspace,
+                                        hipStream_t stream) {
   if (count < 1 || count > kMaxBatch) return hipErrorInvalidValue;
   int dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -417,6 +848,15 @@ hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, void* wor
     ++nb[best];
     ++used;
   }
+  // The rows form when every scene allows it (one form per launch).
+  bool rows = !compact;
+  int wmax = 0, nmax = 0;
+  for (int s = 0; s < count; ++s) {
+    const int W = (p[s].n + nb[s] - 1) / nb[s];
+    rows = rows && use_rows(p[s].n, W);
+    wmax = std::max(wmax, W);
+    nmax = std::max(nmax, p[s].n);
+  }
   IncBatch b;
   b.count = count;
   b.g0[0] = 0;
@@ -424,23 +864,19 @@ hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, void* wor
   char* w = static_cast<char*>(workspace);
   for (int s = 0; s < count; ++s) {
     const int W = (p[s].n + nb[s] - 1) / nb[s];
-    b.scene[s] = inc_dev(p[s], w + off, W);
+    b.scene[s] = inc_dev(p[s], w + off, W, rows);
     b.g0[s + 1] = b.g0[s] + nb[s];
-    lds = std::max(lds, lds_for(W));
-    off += layout(p[s].n, p[s].k).total;
+    lds = std::max(lds, rows ? lds_rows(W, p[s].n) : lds_for(W));
+    off += inc_bytes(p[s].n, p[s].k, compact);
   }
-  int per_cu = 0;
-  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(sgs_inc_batch_kernel),
-                                                        kBlock, lds)) != hipSuccess)
-    return e;
-  if (per_cu < 1) return hipErrorCooperativeLaunchTooLarge;
+  const void* kernel = rows ? rows_batch_kernel(nmax, wmax) : reinterpret_cast<const void*>(sgs_inc_batch_kernel);
+  if ((e = fits(kernel, lds)) != hipSuccess) return e;
   for (int s = 0; s < count; ++s) {
     sgs_inc_init_kernel<<<std::min(1024, (std::max(p[s].n, p[s].k) + 255) / 256), 256, 0, stream>>>(b.scene[s]);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   void* args[] = {&b};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_inc_batch_kernel), dim3(used), dim3(kBlock),
-                                    args, lds, stream);
+  return hipLaunchCooperativeKernel(kernel, dim3(used), dim3(kBlock), args, lds, stream);
 }
 
 }  // namespace cp

@@ -207,12 +207,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
       }
     }
     if (blk == 0) {
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const unsigned long long olo = __shfl_xor((unsigned long long)dobj, o);
-        const long long ohi = __shfl_xor((long long)(dobj >> 64), o);
-        dobj += ((__int128)ohi << 64) | (__int128)olo;
-      }
+      dobj = wave_sum_i128(dobj);
       if (lane == 0) sLw[w] += dobj;
       obj_step = step;
     }
@@ -238,7 +233,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
 }  // namespace
 
 
-size_t sgs_local_workspace_bytes(int64_t n, int64_t k) { return sgs_inc_workspace_bytes(n, k); }
+size_t sgs_local_workspace_bytes(int64_t n, int64_t k) { return layout(n, k).total; }
 
 hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipStream_t stream) {
   if (p.n < 1 || p.n > kLocalMaxN || g < 1 || g > p.n || g > kLocalMaxG) return hipErrorInvalidValue;

@@ -51,13 +51,17 @@ struct SgsParams {
 
 size_t sgs_workspace_bytes(int64_t n, int64_t k);
 hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream);
-size_t sgs_inc_workspace_bytes(int64_t n, int64_t k);
-hipError_t launch_sgs_incremental(const SgsParams& p, hipStream_t stream);
+// Incremental form: the rows schedule (workspace about 4 n bytes per token)
+// unless `compact` or the scene is too large for it, else the exchange
+// schedule (about 16 bytes per token).
+size_t sgs_inc_workspace_bytes(int64_t n, int64_t k, bool compact);
+hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t stream);
 // Up to 16 scenes in one cooperative launch (incremental form); the scenes'
 // workspaces lie one after another in `workspace` (each p[s].workspace is
 // ignored).
-size_t sgs_inc_batch_workspace_bytes(const int64_t* n, const int64_t* k, int count);
-hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, void* workspace, hipStream_t stream);
+size_t sgs_inc_batch_workspace_bytes(const int64_t* n, const int64_t* k, int count, bool compact);
+hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, bool compact, void* workspace,
+                                        hipStream_t stream);
 // Local form: gains over the neighbour table nbr [n, g] (g <= 128, n <= 16384).
 size_t sgs_local_workspace_bytes(int64_t n, int64_t k);
 hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipStream_t stream);

@@ -42,17 +42,23 @@ constexpr unsigned long long kNoCandidate = 1ull;   // below every real candidat
 constexpr unsigned int kSpinLimit = 1u << 22;
 
 // Fixed-point value of a nonnegative term: floor(t 2^S) in 128 bits, read
-// off the bits of the double t 2^S (exact: a power-of-two scaling) with one
-// 64-bit shift; t 2^S < 2^102.  Negative, zero and subnormal-range values
-// give 0.
+// off the bits of the double t 2^S (exact: a power-of-two scaling); t 2^S <
+// 2^102.  Negative, zero and subnormal-range values give 0.  With value
+// m 2^sh (m the 53-bit significand), the low word is m << sh or m >> -sh and
+// the high word m >> (64 - sh) for sh > 0; all three shifts are formed and
+// the right ones kept with masks, so the terms of a batch carry no branches
+// and interleave.
 __device__ __forceinline__ __int128 fx(double t, int S) {
   const unsigned long long b = (unsigned long long)__double_as_longlong(__builtin_ldexp(t, S));
   const int E = int(b >> 52) & 0x7ff;
-  if ((b >> 63) || E < 1023) return 0;                       // negative, or below 1
   const unsigned long long m = (b & ((1ull << 52) - 1ull)) | (1ull << 52);
   const int sh = E - 1075;                                    // value = m 2^sh, sh <= 49
-  if (sh <= 0) return (__int128)(m >> -sh);
-  return ((__int128)(m >> (64 - sh)) << 64) | (__int128)(m << sh);
+  const unsigned long long up = m << (sh & 63), down = m >> ((-sh) & 63), carry = m >> ((64 - sh) & 63);
+  const unsigned long long pos = 0ull - (unsigned long long)(sh > 0);
+  const unsigned long long ok = 0ull - (unsigned long long)((b >> 63) == 0 && E >= 1023);   // not negative, at least 1
+  const unsigned long long lo = ((up & pos) | (down & ~pos)) & ok;
+  const unsigned long long hi = carry & pos & ok;
+  return ((__int128)hi << 64) | (__int128)lo;
 }
 
 __device__ __forceinline__ double fx_to_double(__int128 g, int S) {
@@ -74,6 +80,8 @@ struct IncDev {
   unsigned long long* cand;   // [2][blocks] packed candidate | epoch << 63
   unsigned int* abort;        // set when a wait exceeds kSpinLimit polls
   int W;                      // rows and columns per block
+  float* T;                   // rows form only: [n][ldt] source-major copy, T[s][t] = C(s, t)
+  int ldt;                    // its row stride, n rounded up to a whole 256-row chunk
 };
 
 struct Layout {
@@ -135,14 +143,85 @@ __global__ void sgs_inc_init_kernel(IncDev a) {
   if (gt == 0) *a.abort = 0u;
 }
 
+// Wave reductions without LDS traffic: DPP moves within each row of 16
+// lanes, in the pattern swap neighbours, swap pairs, mirror halves of 8,
+// mirror the row (after each step every lane of a group of 2, 4, 8, 16 holds
+// the group's result), then the four row results read from lanes 0, 16, 32
+// and 48.  Every lane of the wave must be active.
+constexpr int kDppSteps[4] = {0xB1, 0x4E, 0x141, 0x140};   // quad_perm [1,0,3,2], [2,3,0,1], row_half_mirror, row_mirror
+
+template <int CTRL>
+__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long x) {
+  const unsigned a = __builtin_amdgcn_mov_dpp(unsigned(x), CTRL, 0xf, 0xf, false);
+  const unsigned b = __builtin_amdgcn_mov_dpp(unsigned(x >> 32), CTRL, 0xf, 0xf, false);
+  return ((unsigned long long)b << 32) | a;
+}
+__device__ __forceinline__ unsigned long long lane_u64(unsigned long long x, int r) {
+  return ((unsigned long long)__builtin_amdgcn_readlane(unsigned(x >> 32), r) << 32) |
+         unsigned(__builtin_amdgcn_readlane(unsigned(x), r));
+}
+template <int CTRL>
+__device__ __forceinline__ __int128 dpp_i128(__int128 x) {
+  return ((__int128)(long long)dpp_u64<CTRL>((unsigned long long)(x >> 64)) << 64) |
+         (__int128)dpp_u64<CTRL>((unsigned long long)x);
+}
+__device__ __forceinline__ __int128 lane_i128(__int128 x, int r) {
+  return ((__int128)(long long)lane_u64((unsigned long long)(x >> 64), r) << 64) |
+         (__int128)lane_u64((unsigned long long)x, r);
+}
+
+__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long x) {
+  unsigned long long y;
+  y = dpp_u64<kDppSteps[0]>(x); x = y > x ? y : x;
+  y = dpp_u64<kDppSteps[1]>(x); x = y > x ? y : x;
+  y = dpp_u64<kDppSteps[2]>(x); x = y > x ? y : x;
+  y = dpp_u64<kDppSteps[3]>(x); x = y > x ? y : x;
+  unsigned long long m = lane_u64(x, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    y = lane_u64(x, r);
+    m = y > m ? y : m;
+  }
+  return m;
+}
+
+__device__ __forceinline__ long long wave_max_i64(long long x) {
+  long long y;
+  y = (long long)dpp_u64<kDppSteps[0]>((unsigned long long)x); x = y > x ? y : x;
+  y = (long long)dpp_u64<kDppSteps[1]>((unsigned long long)x); x = y > x ? y : x;
+  y = (long long)dpp_u64<kDppSteps[2]>((unsigned long long)x); x = y > x ? y : x;
+  y = (long long)dpp_u64<kDppSteps[3]>((unsigned long long)x); x = y > x ? y : x;
+  long long m = (long long)lane_u64((unsigned long long)x, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    y = (long long)lane_u64((unsigned long long)x, r);
+    m = y > m ? y : m;
+  }
+  return m;
+}
+
+__device__ __forceinline__ __int128 wave_sum_i128(__int128 x) {
+  x += dpp_i128<kDppSteps[0]>(x);
+  x += dpp_i128<kDppSteps[1]>(x);
+  x += dpp_i128<kDppSteps[2]>(x);
+  x += dpp_i128<kDppSteps[3]>(x);
+  return lane_i128(x, 0) + lane_i128(x, 16) + lane_i128(x, 32) + lane_i128(x, 48);
+}
+
+// Inclusive prefix sum over the lanes of a wave (every lane active).
+__device__ __forceinline__ int wave_scan_incl(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
 // Sum over the block of 128-bit integers, result in every thread.
 __device__ __int128 block_sum_i128(__int128 x, __int128* sg) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const unsigned long long lo = __shfl_xor((unsigned long long)x, o);
-    const long long hi = __shfl_xor((long long)(x >> 64), o);
-    x += ((__int128)hi << 64) | (__int128)lo;
-  }
+  x = wave_sum_i128(x);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   __syncthreads();
   if (lane == 0) sg[w] = x;
@@ -203,15 +282,76 @@ __device__ double block_sum_all(double x, double* sd) {
   return s;
 }
 
+// (g, gi) is better than (h, hi): larger gain, or equal gain and smaller index.
+__device__ __forceinline__ bool better(__int128 g, int gi, __int128 h, int hi) {
+  return g > h || (g == h && gi < hi);
+}
+
+// One step of the wave argmax: every lane takes the better of its own pair
+// and that of the lane the DPP pattern CTRL names.
+template <int CTRL>
+__device__ __forceinline__ void argmax_dpp(__int128& g, int& gi) {
+  const __int128 og = dpp_i128<CTRL>(g);
+  const int oi = __builtin_amdgcn_mov_dpp(gi, CTRL, 0xf, 0xf, false);
+  if (better(og, oi, g, gi)) {
+    g = og;
+    gi = oi;
+  }
+}
+
+// Argmax of (g, gi) over a whole wave, in every lane, in the DPP pattern of
+// the wave reductions above.  Pairs are totally ordered, so the order of the
+// comparisons does not matter.
+__device__ __forceinline__ void wave_argmax_exact(__int128& g, int& gi) {
+  argmax_dpp<kDppSteps[0]>(g, gi);
+  argmax_dpp<kDppSteps[1]>(g, gi);
+  argmax_dpp<kDppSteps[2]>(g, gi);
+  argmax_dpp<kDppSteps[3]>(g, gi);
+  __int128 bg = lane_i128(g, 0);
+  int bi = __builtin_amdgcn_readlane(gi, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    const __int128 rg = lane_i128(g, r);
+    const int ri = __builtin_amdgcn_readlane(gi, r);
+    if (better(rg, ri, bg, bi)) {
+      bg = rg;
+      bi = ri;
+    }
+  }
+  g = bg;
+  gi = bi;
+}
+
+// The same argmax (g = -1 marks no candidate; gains are below 2^102): the
+// largest top 64 bits of the gains first; a single lane holding them holds
+// the largest gain, and only a tie in those bits takes the full comparison.
+__device__ __forceinline__ void wave_argmax(__int128& g, int& gi) {
+  const long long key = (long long)(g >> 38);
+  const long long top = wave_max_i64(key);
+  const unsigned long long c = __ballot(key == top);
+  if (__popcll(c) == 1) {
+    const int l = __ffsll((long long)c) - 1;
+    g = lane_i128(g, l);
+    gi = __builtin_amdgcn_readlane(gi, l);
+    return;
+  }
+  if (key != top) {
+    g = -1;
+    gi = INT_MAX;
+  }
+  wave_argmax_exact(g, gi);
+}
+
 // Exact argmax (ties to the smaller index) of the block's unchosen columns,
 // published as the block's candidate for the step; across blocks the gains
 // compare as doubles truncated to 43 bits.  With at most 64 columns wave 0
 // does it alone, one column per lane, and no barrier follows: the callers'
 // next step begins with one (read_winner), and the gains and chosen flags it
 // reads were last written by wave 0 itself.
-__device__ void publish_argmax(const unsigned long long* sGlo, const long long* sGhi, const unsigned char* ssel,
-                               int lo, int cnt, int S, unsigned long long* slot, unsigned long long epoch,
-                               __int128* sg, int* si) {
+__device__ __forceinline__ void publish_argmax(const unsigned long long* sGlo, const long long* sGhi,
+                                               const unsigned char* ssel, int lo, int cnt, int S,
+                                               unsigned long long* slot, unsigned long long epoch, __int128* sg,
+                                               int* si) {
   if (cnt <= 64) {
     if (threadIdx.x >= 64) return;
     const int i = threadIdx.x;
@@ -221,17 +361,7 @@ __device__ void publish_argmax(const unsigned long long* sGlo, const long long* 
       g = ((__int128)sGhi[i] << 64) | (__int128)sGlo[i];
       gi = lo + i;
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const unsigned long long olo = __shfl_xor((unsigned long long)g, o);
-      const long long ohi = __shfl_xor((long long)(g >> 64), o);
-      const int oi = __shfl_xor(gi, o);
-      const __int128 og = ((__int128)ohi << 64) | (__int128)olo;
-      if (og > g || (og == g && oi < gi)) {
-        g = og;
-        gi = oi;
-      }
-    }
+    wave_argmax(g, gi);
     if (i == 0) put(slot, (gi != INT_MAX ? pack_key(fx_to_double(g, S), gi) : kNoCandidate) | epoch);
     return;
   }
@@ -245,17 +375,7 @@ __device__ void publish_argmax(const unsigned long long* sGlo, const long long* 
         gi = lo + i;
       }
     }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const unsigned long long olo = __shfl_xor((unsigned long long)g, o);
-    const long long ohi = __shfl_xor((long long)(g >> 64), o);
-    const int oi = __shfl_xor(gi, o);
-    const __int128 og = ((__int128)ohi << 64) | (__int128)olo;
-    if (og > g || (og == g && oi < gi)) {
-      g = og;
-      gi = oi;
-    }
-  }
+  wave_argmax(g, gi);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   if (lane == 0) {
     sg[w] = g;
@@ -289,11 +409,7 @@ __device__ int read_winner(const unsigned long long* slots, unsigned long long e
     else
       *sflag = 1;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const unsigned long long y = __shfl_xor(best, o);
-    best = y > best ? y : best;
-  }
+  best = wave_max_u64(best);
   if (lane == 0) su[w] = best;
   __syncthreads();
   unsigned long long m = su[0];

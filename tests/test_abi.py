@@ -48,9 +48,16 @@ def test_workspace_queries(lib):
     assert lib.coverprune_fst_cost_workspace(16384, 3584, 1) >= 16384 * 4
     a = lib.coverprune_sgs_workspace(1024, 102, 0)
     b = lib.coverprune_sgs_workspace(16384, 1638, 0)
-    # the incremental form needs far less than the dense form's partial gains
-    c = lib.coverprune_sgs_workspace(16384, 1638, 1)
+    # the compact incremental schedule needs far less than the dense form's
+    # partial gains; the rows schedule adds the source-major copy of the cost
+    c = lib.coverprune_sgs_workspace(16384, 1638, 3)
     assert 16384 * 16 <= c < b
+    r = lib.coverprune_sgs_workspace(16384, 1638, 1)
+    assert r == c + 16384 * 16384 * 4
+    # ... up to n = 32768 (rows padded to 256 targets); beyond it the compact one
+    assert lib.coverprune_sgs_workspace(1000, 100, 1) == lib.coverprune_sgs_workspace(1000, 100, 3) + 1000 * 1024 * 4
+    assert lib.coverprune_sgs_workspace(32769, 100, 1) == lib.coverprune_sgs_workspace(32769, 100, 3)
+    assert lib.coverprune_sgs_workspace(16384, 1638, 2) == 0      # compact alone is not a form
     assert 0 < a < b
     # at least two radix key buffers, two token buffers and the packed voxel words
     assert lib.coverprune_lite_workspace(32768, 3584, 3277, 1) >= 32768 * 40
@@ -93,7 +100,9 @@ def _sgs(lib, **kw):
 
 @pytest.mark.parametrize("kw,code", [
     (dict(n=0), INVALID), (dict(k=0), INVALID), (dict(k=65), INVALID), (dict(k=-1), INVALID),
-    (dict(c0=float("inf")), INVALID), (dict(flags=7), UNSUPPORTED), (dict(cost=None), INVALID),
+    (dict(c0=float("inf")), INVALID), (dict(flags=7), UNSUPPORTED), (dict(flags=2), UNSUPPORTED),
+    (dict(flags=3, ws_bytes=100), WORKSPACE), (dict(flags=1, ws_bytes=64 * 16 + 1024), WORKSPACE),
+    (dict(cost=None), INVALID),
     (dict(v=None), INVALID), (dict(sel=None), INVALID), (dict(ws=None), WORKSPACE),
     (dict(ws_bytes=100), WORKSPACE), (dict(ws=ctypes.c_void_p(0x1008)), WORKSPACE),
 ])
@@ -237,9 +246,12 @@ def _scenes(count, **kw):
 
 
 def test_batch_workspace_is_the_sum_of_the_scenes(lib):
-    one = lib.coverprune_sgs_workspace(64, 8, 1)
-    assert lib.coverprune_sgs_batch_workspace(_scenes(3), 3) == 3 * one
-    assert lib.coverprune_sgs_batch_workspace(_scenes(3), 17) == 0
+    for flags in (1, 3):
+        one = lib.coverprune_sgs_workspace(64, 8, flags)
+        assert lib.coverprune_sgs_batch_workspace(_scenes(3), 3, flags) == 3 * one
+        assert lib.coverprune_sgs_batch_workspace(_scenes(3), 17, flags) == 0
+    assert lib.coverprune_sgs_batch_workspace(_scenes(3), 3, 0) == 0
+    assert lib.coverprune_sgs_batch_workspace(_scenes(3), 3, 2) == 0
 
 
 @pytest.mark.parametrize("count,kw,code", [
@@ -249,11 +261,16 @@ def test_batch_workspace_is_the_sum_of_the_scenes(lib):
 ])
 def test_batch_rejects(lib, count, kw, code):
     arr = _scenes(max(count, 1), **kw) if count <= 16 else _scenes(16)
-    assert lib.coverprune_sgs_select_batch(arr, count, FAKE, 1 << 30, None) == code
+    assert lib.coverprune_sgs_select_batch(arr, count, 1, FAKE, 1 << 30, None) == code
     assert lib.coverprune_last_error() != b""
 
 
 def test_batch_rejects_small_workspace(lib):
-    assert lib.coverprune_sgs_select_batch(_scenes(2), 2, FAKE, 64, None) == WORKSPACE
-    assert lib.coverprune_sgs_select_batch(_scenes(2), 2, None, 1 << 30, None) == WORKSPACE
-    assert lib.coverprune_sgs_select_batch(None, 2, FAKE, 1 << 30, None) == INVALID
+    assert lib.coverprune_sgs_select_batch(_scenes(2), 2, 1, FAKE, 64, None) == WORKSPACE
+    assert lib.coverprune_sgs_select_batch(_scenes(2), 2, 1, None, 1 << 30, None) == WORKSPACE
+    assert lib.coverprune_sgs_select_batch(None, 2, 1, FAKE, 1 << 30, None) == INVALID
+
+
+@pytest.mark.parametrize("flags", [0, 2, 4, 5, 7])
+def test_batch_rejects_flags(lib, flags):
+    assert lib.coverprune_sgs_select_batch(_scenes(2), 2, flags, FAKE, 1 << 30, None) == UNSUPPORTED

@@ -23,11 +23,17 @@ def _case(cfg, n, seed):
     return s, C32
 
 
-def _run_batch(cases, ks, c0=3.0):
+# Both schedules of the incremental form: improved targets found by every
+# block from the transposed cost ("rows") or exchanged between blocks.
+SCHEDULES = [pytest.param(False, id="rows"), pytest.param(True, id="compact")]
+
+
+def _run_batch(cases, ks, c0=3.0, compact=False):
     costs = [torch.from_numpy(np.ascontiguousarray(C.T)).cuda() for _, C in cases]
     caps = [torch.from_numpy(np.ascontiguousarray(s.capacity)).cuda() for s, _ in cases]
-    res = _cp().sgs_select_batch(costs, caps, ks, c0=c0)
-    single = [_cp().sgs_select(c, v, k, c0=c0, incremental=True) for c, v, k in zip(costs, caps, ks)]
+    res = _cp().sgs_select_batch(costs, caps, ks, c0=c0, compact=compact)
+    single = [_cp().sgs_select(c, v, k, c0=c0, incremental=True, compact=compact)
+              for c, v, k in zip(costs, caps, ks)]
     torch.cuda.synchronize()
     return res, single
 
@@ -53,13 +59,14 @@ def _check_scene(s, C32, k, got, alone, c0=3.0):
         assert np.array_equal(assign, ref["assign"])
 
 
-def test_batch_of_mixed_sizes():
+@pytest.mark.parametrize("compact", SCHEDULES)
+def test_batch_of_mixed_sizes(compact):
     specs = [("n1024_d256_f32", 300, 30, 0), ("n4096_d1152", 997, 100, 1), ("n8192_d3584", 1531, 60, 2),
              ("n4096_d1152", 64, 64, 3)]
     cases = [_case(cfg, n, seed) for cfg, n, _, seed in specs]
     ks = [k for _, _, k, _ in specs]
-    print(f"sgs batch sizes {[s.n for s, _ in cases]} ks {ks}", flush=True)
-    res, single = _run_batch(cases, ks)
+    print(f"sgs batch sizes {[s.n for s, _ in cases]} ks {ks} compact={compact}", flush=True)
+    res, single = _run_batch(cases, ks, compact=compact)
     for (s, C32), k, got, alone in zip(cases, ks, res, single):
         _check_scene(s, C32, k, got, alone)
 
@@ -71,15 +78,16 @@ def test_batch_of_one():
     _check_scene(*cases[0], 100, res[0], single[0])
 
 
-def test_batch_of_sixteen():
+@pytest.mark.parametrize("compact", SCHEDULES)
+def test_batch_of_sixteen(compact):
     # The largest batch: sixteen small scenes, including n = 1, k = 1 and k = n.
     rng = np.random.default_rng(5)
     sizes = [1, 2, 40, 64, 65, 100, 128, 129, 200, 257, 300, 333, 64, 90, 150, 400]
     cases = [_case("n4096_d1152", n, 10 + i) for i, n in enumerate(sizes)]
     ks = [max(1, min(n, int(rng.integers(1, n + 1)))) for n in sizes]
     ks[3], ks[4] = 64, 1
-    print(f"sgs batch of sixteen ks {ks}", flush=True)
-    res, single = _run_batch(cases, ks)
+    print(f"sgs batch of sixteen ks {ks} compact={compact}", flush=True)
+    res, single = _run_batch(cases, ks, compact=compact)
     for (s, C32), k, got, alone in zip(cases, ks, res, single):
         _check_scene(s, C32, k, got, alone)
 

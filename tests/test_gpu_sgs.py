@@ -20,26 +20,32 @@ def _sub(cfg, n, seed):
 
 
 # Both forms of the greedy: full sweeps (dense) and running gains updated from
-# the targets whose best cost drops (incremental).
-MODES = [pytest.param(False, id="dense"), pytest.param(True, id="incremental")]
+# the targets whose best cost drops (incremental), the latter in both
+# schedules: every block finds the improved targets from the pick's row of
+# the transposed cost ("rows"), or the blocks exchange them ("compact").
+MODES = ["dense", "rows", "compact"]
 
 
-def _gpu_select(C_tm_f32: np.ndarray, v: np.ndarray, k: int, c0: float, incremental=False):
+def _run(cost, cap, k, c0, mode):
+    return _cp().sgs_select(cost, cap, k, c0=c0, incremental=mode != "dense", compact=mode == "compact")
+
+
+def _gpu_select(C_tm_f32: np.ndarray, v: np.ndarray, k: int, c0: float, mode="dense"):
     cost = torch.from_numpy(np.ascontiguousarray(C_tm_f32)).cuda()
     cap = torch.from_numpy(np.ascontiguousarray(v, dtype=np.float32)).cuda()
-    r = _cp().sgs_select(cost, cap, k, c0=c0, incremental=incremental)
+    r = _run(cost, cap, k, c0, mode)
     torch.cuda.synchronize()
     return (r.selected.cpu().numpy(), r.gain.cpu().numpy(), r.objective.cpu().numpy(),
             r.assign.cpu().numpy())
 
 
-def _same_cost_case(s, k, c0=3.0, weights=(1.0, 1.0, 1.0), kappa=10.0, incremental=False):
+def _same_cost_case(s, k, c0=3.0, weights=(1.0, 1.0, 1.0), kappa=10.0, mode="dense"):
     """The oracle's cost, rounded once to float32, drives both greedies."""
     C_ref, _ = parity.oracle_cost(s, weights, kappa)
     C32 = C_ref.astype(np.float32)                 # source-major, float32 values
     v = s.capacity
     ref = sgs.sgs_ref(C32.astype(np.float64), v.astype(np.float64), k, c0)
-    sel, gain, obj, assign = _gpu_select(np.ascontiguousarray(C32.T), v, k, c0, incremental)
+    sel, gain, obj, assign = _gpu_select(np.ascontiguousarray(C32.T), v, k, c0, mode)
     ties, g_or, o_or = parity.replay_greedy(C32, v, c0, sel)
     assert np.allclose(gain, g_or, rtol=1e-6, atol=1e-12)
     assert np.allclose(obj, o_or, rtol=1e-9, atol=1e-12)
@@ -63,41 +69,41 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("incremental", MODES)
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("cfg,n,k,seed", CASES)
-def test_same_cost_parity(cfg, n, k, seed, incremental):
+def test_same_cost_parity(cfg, n, k, seed, mode):
     s = _sub(cfg, n, seed)
-    print(f"sgs same-cost {cfg} n={s.n} k={k} seed={seed} incremental={incremental}", flush=True)
-    ties = _same_cost_case(s, k, incremental=incremental)
+    print(f"sgs same-cost {cfg} n={s.n} k={k} seed={seed} mode={mode}", flush=True)
+    ties = _same_cost_case(s, k, mode=mode)
     assert len(ties) <= 1, f"unexpected near-ties at steps {ties}"
 
 
-@pytest.mark.parametrize("incremental", MODES)
-def test_single_token(incremental):
+@pytest.mark.parametrize("mode", MODES)
+def test_single_token(mode):
     s = _sub("n4096_d1152", 1, 0)
     s.capacity[:] = 1.0
-    print(f"sgs n=1 incremental={incremental}", flush=True)
-    sel, gain, obj, assign = _gpu_select(np.zeros((1, 1), np.float32), s.capacity, 1, 3.0, incremental)
+    print(f"sgs n=1 mode={mode}", flush=True)
+    sel, gain, obj, assign = _gpu_select(np.zeros((1, 1), np.float32), s.capacity, 1, 3.0, mode)
     assert sel.tolist() == [0] and assign.tolist() == [0]
     assert gain[0] == pytest.approx(3.0) and obj[0] == 0.0
 
 
-@pytest.mark.parametrize("incremental", MODES)
-def test_exact_ties_go_to_smaller_index(incremental):
+@pytest.mark.parametrize("mode", MODES)
+def test_exact_ties_go_to_smaller_index(mode):
     # Duplicated tokens have identical gains at every step; the smaller index wins.
     s = _sub("n4096_d1152", 200, 5)
     idx = np.concatenate([np.arange(200), np.arange(0, 200, 7)])
     d = subscene(s, idx)
-    print(f"sgs exact ties incremental={incremental}", flush=True)
+    print(f"sgs exact ties mode={mode}", flush=True)
     C_ref, _ = parity.oracle_cost(d)
     C32 = C_ref.astype(np.float32)
     ref = sgs.sgs_ref(C32.astype(np.float64), d.capacity.astype(np.float64), 40, 3.0)
-    sel, _, _, _ = _gpu_select(np.ascontiguousarray(C32.T), d.capacity, 40, 3.0, incremental)
+    sel, _, _, _ = _gpu_select(np.ascontiguousarray(C32.T), d.capacity, 40, 3.0, mode)
     assert np.array_equal(sel, ref["selected"])
 
 
-@pytest.mark.parametrize("incremental", MODES)
-def test_zero_capacity_steps_still_select(incremental):
+@pytest.mark.parametrize("mode", MODES)
+def test_zero_capacity_steps_still_select(mode):
     # Only 3 targets carry capacity: after they are covered every gain is 0 and
     # the remaining picks go to the smallest unselected indices.
     s = _sub("n4096_d1152", 120, 6)
@@ -108,23 +114,23 @@ def test_zero_capacity_steps_still_select(incremental):
     C_ref, _ = parity.oracle_cost(s)
     C32 = C_ref.astype(np.float32)
     ref = sgs.sgs_ref(C32.astype(np.float64), v.astype(np.float64), 10, 3.0)
-    sel, gain, _, _ = _gpu_select(np.ascontiguousarray(C32.T), v, 10, 3.0, incremental)
+    sel, gain, _, _ = _gpu_select(np.ascontiguousarray(C32.T), v, 10, 3.0, mode)
     assert np.array_equal(sel, ref["selected"])
     assert np.all(gain[3:] == 0.0)
 
 
-@pytest.mark.parametrize("incremental", MODES)
-def test_end_to_end_parity(incremental):
+@pytest.mark.parametrize("mode", MODES)
+def test_end_to_end_parity(mode):
     # GPU cost and GPU greedy against the oracle's cost and greedy.  A pick may
     # differ from the oracle's only where two gains are closer than the cost
     # error can resolve.
     s = _sub("n4096_d1152", 1200, 7)
     k = 120
-    print(f"sgs end-to-end n={s.n} k={k} incremental={incremental}", flush=True)
+    print(f"sgs end-to-end n={s.n} k={k} mode={mode}", flush=True)
     t = to_device(s)
     cp = _cp()
     cost, _ = cp.fst_cost(t["feats"], t["pos"], t["frame"])
-    r = cp.sgs_select(cost, t["capacity"], k, incremental=incremental)
+    r = _run(cost, t["capacity"], k, 3.0, mode)
     torch.cuda.synchronize()
     sel = r.selected.cpu().numpy()
     C_ref, _ = parity.oracle_cost(s)
@@ -136,28 +142,28 @@ def test_end_to_end_parity(incremental):
     print(f"  {len(ties)} near-tie steps", flush=True)
 
 
-@pytest.mark.parametrize("incremental", MODES)
-def test_deterministic(incremental):
+@pytest.mark.parametrize("mode", MODES)
+def test_deterministic(mode):
     s = _sub("n4096_d1152", 1000, 8)
     C_ref, _ = parity.oracle_cost(s)
     C_tm = np.ascontiguousarray(C_ref.T.astype(np.float32))
-    print(f"sgs determinism incremental={incremental}", flush=True)
-    a = _gpu_select(C_tm, s.capacity, 100, 3.0, incremental)
-    b = _gpu_select(C_tm, s.capacity, 100, 3.0, incremental)
+    print(f"sgs determinism mode={mode}", flush=True)
+    a = _gpu_select(C_tm, s.capacity, 100, 3.0, mode)
+    b = _gpu_select(C_tm, s.capacity, 100, 3.0, mode)
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("incremental", MODES)
-def test_full_size_first_steps(incremental):
+@pytest.mark.parametrize("mode", MODES)
+def test_full_size_first_steps(mode):
     # 16384 tokens, the benchmark's launch shape, first 6 steps against the
     # oracle on the same float32 cost (narrow 16-d features keep the oracle fast).
     s = make_scene("n16384_d3584", 0, dim=16)
-    print(f"sgs full size n={s.n} incremental={incremental}", flush=True)
+    print(f"sgs full size n={s.n} mode={mode}", flush=True)
     C_tm, _ = parity.oracle_cost_f32_target_major(s)
     k = 6
-    sel, gain, obj, _ = _gpu_select(C_tm, s.capacity, k, 3.0, incremental)
+    sel, gain, obj, _ = _gpu_select(C_tm, s.capacity, k, 3.0, mode)
     C32 = C_tm.T
     ties, g_or, o_or = parity.replay_greedy(C32, s.capacity, 3.0, sel)
     assert np.allclose(gain, g_or, rtol=1e-6)
@@ -166,15 +172,15 @@ def test_full_size_first_steps(incremental):
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("incremental", MODES)
-def test_full_size_trajectory_invariants(incremental):
+@pytest.mark.parametrize("mode", MODES)
+def test_full_size_trajectory_invariants(mode):
     # The full 16384-token workload as the benchmark runs it (K = 1638).
     s = make_scene("n16384_d3584", 0)
-    print(f"sgs full workload n={s.n} k={s.k} incremental={incremental}", flush=True)
+    print(f"sgs full workload n={s.n} k={s.k} mode={mode}", flush=True)
     t = to_device(s)
     cp = _cp()
     cost, _ = cp.fst_cost(t["feats"], t["pos"], t["frame"])
-    r = cp.sgs_select(cost, t["capacity"], s.k, incremental=incremental)
+    r = _run(cost, t["capacity"], s.k, 3.0, mode)
     torch.cuda.synchronize()
     sel, gain, obj, assign = (r.selected.cpu().numpy(), r.gain.cpu().numpy(),
                               r.objective.cpu().numpy(), r.assign.cpu().numpy())
@@ -228,8 +234,28 @@ def test_incremental_general_form_matches_dense():
     cp = _cp()
     a = cp.sgs_select(cost, cap, k, c0=3.0)
     b = cp.sgs_select(cost, cap, k, c0=3.0, incremental=True)
+    c = cp.sgs_select(cost, cap, k, c0=3.0, incremental=True, compact=True)
     torch.cuda.synchronize()
     assert np.array_equal(a.selected.cpu().numpy(), b.selected.cpu().numpy())
     assert np.allclose(a.gain.cpu().numpy(), b.gain.cpu().numpy(), rtol=1e-9, atol=0.0)
     assert np.allclose(a.objective.cpu().numpy(), b.objective.cpu().numpy(), rtol=1e-9, atol=0.0)
     assert np.array_equal(a.assign.cpu().numpy(), b.assign.cpu().numpy())
+    for x, y in zip((b.selected, b.gain, b.objective, b.assign), (c.selected, c.gain, c.objective, c.assign)):
+        assert torch.equal(x, y)
+
+
+@pytest.mark.slow
+def test_full_size_schedules_agree_bitwise():
+    # The two incremental schedules sum the same fixed-point terms over the
+    # same block partition, so on the full workload every output is equal bit
+    # for bit, including past near-ties.
+    s = make_scene("n16384_d3584", 0)
+    print(f"sgs rows vs compact schedule n={s.n} k={s.k}", flush=True)
+    t = to_device(s)
+    cp = _cp()
+    cost, _ = cp.fst_cost(t["feats"], t["pos"], t["frame"])
+    a = cp.sgs_select(cost, t["capacity"], s.k, incremental=True)
+    b = cp.sgs_select(cost, t["capacity"], s.k, incremental=True, compact=True)
+    torch.cuda.synchronize()
+    for x, y in zip((a.selected, a.gain, a.objective, a.assign), (b.selected, b.gain, b.objective, b.assign)):
+        assert torch.equal(x, y)
