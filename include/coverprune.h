@@ -261,7 +261,11 @@ cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count,
  *
  * Both enqueue on `stream` and return before the work is done; bad sizes or
  * NULL pointers return CP_ERR_INVALID_ARG before anything is enqueued.  The
- * workspace of the greedy is about 16 B per token.
+ * greedy keeps all n best costs on every compute unit and finds the targets
+ * a pick improves from the pick's row of a source-major copy of the cost,
+ * which it writes into the workspace first; the workspace is 4 n^2 bytes
+ * for that copy (n rounded up to 256 per row; 1 GiB at n = 16384) plus 4 KB
+ * per step of k for the objective's parts.
  */
 #define CP_SGS_LOCAL_MAX_N 16384
 #define CP_SGS_LOCAL_MAX_G 128

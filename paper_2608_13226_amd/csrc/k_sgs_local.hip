@@ -4,15 +4,25 @@
 //   gain(c) = sum_{j in M_g(c)} v_j max(0, b_j - C(c, j)),
 // while a pick still lowers the best cost b_j of every target it is cheaper
 // for (the residual of Eq. 14 is over all targets) and L(S) sums over all of
-// them.  The pick exchange and the change lists are the incremental form's.
-// Every block keeps all n best costs in LDS, updated from the whole change
-// list each step, together with its candidates' neighbour lists and costs
-// C(c, j), j in M_g(c) (read once at launch), and sums its candidates' local
-// gains afresh each step: lanes over candidates, waves over the neighbour
-// list, each term the float64 difference b_j - C(c, j) times v_j rounded onto
-// the fixed-point grid.  n <= kLocalMaxN, g <= kLocalMaxG.
+// them.  One cooperative launch of one block per compute unit; block b owns
+// candidates [b W, (b + 1) W).  Every block keeps all n best costs in LDS,
+// together with its candidates' neighbour lists, the costs C(c, j) and the
+// capacities v_j of those neighbours (read once at launch), and per step:
+//   1. reads every block's candidate and takes the same winner t;
+//   2. reads the winner's costs to every target, C(t, j) for all j, as one
+//      contiguous row of a source-major copy T of the cost (written by a
+//      transposing kernel before the launch), and lowers b_j wherever the
+//      winner is cheaper: every block holds the identical b afterwards, and
+//      no block exchanges anything but its candidate;
+//   3. sums its candidates' local gains afresh from LDS: lanes over
+//      candidates, waves over the neighbour list, each term the float64
+//      difference b_j - C(c, j) times v_j rounded onto the fixed-point grid;
+//   4. publishes the exact argmax of its unchosen candidates.
+// L(S) is kept in the same fixed point as one running part per block over
+// the block's own targets, stored for every step and added up in block order
+// by a second kernel.  n <= kLocalMaxN, g <= kLocalMaxG.
 //
-// The exchanges and the fixed point are in sgs_exchange.h.
+// The candidate exchange and the fixed point are in sgs_exchange.h.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -24,8 +34,43 @@ namespace {
 
 constexpr int kLocalMaxN = 16384;
 constexpr int kLocalMaxG = 128;
+constexpr int kChunkT = 256;                          // targets per wave-load of the winner's row
+constexpr int kLoadsT = kLocalMaxN / kChunkT / kWaves;  // such loads per wave and step
+constexpr int kTile = 64;                             // transposing kernel's tile
 
-__global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32_t* __restrict__ nbr, int g) {
+int local_ldt(int64_t n) { return int((n + kChunkT - 1) / kChunkT * kChunkT); }
+
+// T[s][j] = C_tm[j][s] through a 64 x 65 LDS tile: coalesced reads along s,
+// coalesced writes along j.  Row padding [n, ldt) is left as it is.
+__global__ __launch_bounds__(256) void transpose_kernel(const float* __restrict__ C, int n, float* __restrict__ T,
+                                                        int ldt) {
+  __shared__ float tile[kTile][kTile + 1];
+  const int tj = blockIdx.y * kTile, ts = blockIdx.x * kTile;
+  const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
+#pragma unroll 4
+  for (int r = r0; r < kTile; r += 4) {
+    const int j = tj + r, s = ts + c;
+    if (j < n && s < n) tile[r][c] = C[size_t(j) * n + s];
+  }
+  __syncthreads();
+#pragma unroll 4
+  for (int r = r0; r < kTile; r += 4) {
+    const int s = ts + r, j = tj + c;
+    if (s < n && j < n) T[size_t(s) * ldt + j] = tile[c][r];
+  }
+}
+
+struct LocalDev {
+  IncDev a;
+  const int32_t* nbr;
+  int g;
+  __int128* part;      // [k][blocks] running objective part of each block after each step
+  int* scale;          // the fixed-point exponent S, for the objective sums
+};
+
+__global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
+  const IncDev& a = L.a;
+  const int g = L.g;
   extern __shared__ unsigned long long smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int blk = blockIdx.x, nb = gridDim.x;
@@ -33,31 +78,40 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
   const int cnt = max(0, min(a.n, lo + a.W) - lo);
   unsigned long long* sGlo = smem;                                 // [W] gains, low words
   long long* sGhi = reinterpret_cast<long long*>(sGlo + a.W);      // [W] high words
-  float* sball = reinterpret_cast<float*>(sGhi + a.W);             // [n] best cost of every target
-  float* scg = sball + a.n;                                        // [W][g] C(c, j), j in M_g(c)
-  int* snb = reinterpret_cast<int*>(scg + size_t(a.W) * g);        // [W][g] M_g(c)
+  float* sball = reinterpret_cast<float*>(sGhi + a.W);             // [ldt] b_j; -inf past n (never lowered)
+  // The band, neighbour-major ([g][W]: entry q of candidate i at q W + i),
+  // so that the lanes of a wave (consecutive candidates) read consecutive
+  // words.
+  float* scg = sball + a.ldt;                                      // [g][W] C(c, j), j in M_g(c)
+  float* snv = scg + size_t(a.W) * g;                              // [g][W] v_j, j in M_g(c)
+  float* sv = snv + size_t(a.W) * g;                               // [W] v of the own targets
+  unsigned short* snb = reinterpret_cast<unsigned short*>(sv + a.W);   // [g][W] M_g(c)
   unsigned char* ssel = reinterpret_cast<unsigned char*>(snb + size_t(a.W) * g);   // [W]
   __shared__ __int128 red[kBlock];
   __shared__ __int128 sg[kWaves];
   __shared__ double sd[kWaves];
   __shared__ int si[kWaves];
-  __shared__ int swt[kWaves];
   __shared__ unsigned long long su[kWaves];
-  __shared__ int spre[kMaxBlocks + 1];
-  __shared__ int sflag;                       // abort seen while waiting for the winner
-  __shared__ int slflag;                      // ... or for the slice lengths
+  __shared__ int sflag;
+  __shared__ __int128 sLw[kWaves];            // this block's objective part, one running share per wave
 
-  for (int j = tid; j < a.n; j += kBlock) sball[j] = a.c0;
-  for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
-  // The band of the own candidates: neighbour lists and C(c, j) = C_tm[j][c]
-  // (indices clamped into range; the table is the caller's).
+  for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
+  for (int i = tid; i < cnt; i += kBlock) {
+    ssel[i] = 0;
+    sv[i] = a.v[lo + i];
+  }
+  // The band of the own candidates: neighbour lists, C(c, j) = C_tm[j][c]
+  // and v_j (indices clamped into range; the table is the caller's).
   for (int e = tid; e < cnt * g; e += kBlock) {
-    const int i = e / g;
-    const int j = min(max(nbr[size_t(lo + i) * g + (e - i * g)], 0), a.n - 1);
-    snb[e] = j;
-    scg[e] = a.C[size_t(j) * a.n + lo + i];
+    const int i = e / g, q = e - i * g;
+    const int j = min(max(L.nbr[size_t(lo + i) * g + q], 0), a.n - 1);
+    const int at = q * a.W + i;
+    snb[at] = (unsigned short)j;
+    scg[at] = a.C[size_t(j) * a.n + lo + i];
+    snv[at] = a.v[j];
   }
 
+  // Fixed-point scale, the same in every block (same sum, same order).
   double vsum;
   {
     double x = 0.0;
@@ -71,35 +125,50 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
     (void)__builtin_frexp(M, &e);
     S = 101 - e;
   }
+  if (blk == 0 && tid == 0) *L.scale = S;
 
-  // Objective in block 0, one running part per wave (as in the incremental
-  // form): step l's total is written after the next step's first barrier.
-  __shared__ __int128 sLw[kWaves];
-  int obj_step = -1;
-  if (blk == 0) {
+  // The objective part of the own targets at b = c0.
+  {
     __int128 x = 0;
-    for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
-    const __int128 L0 = block_sum_i128(x, sg);
-    if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
+    for (int i = tid; i < cnt; i += kBlock) x += fx(double(sv[i]) * double(a.c0), S);
+    const __int128 P0 = block_sum_i128(x, sg);
+    if (tid < kWaves) sLw[tid] = tid == 0 ? P0 : 0;
   }
 
   // Local gains of the own candidates from the current best costs: lane =
   // candidate within a chunk of 64, waves split the neighbour list.
   const int qper = (g + kWaves - 1) / kWaves;
   auto local_gains = [&]() {
-    __syncthreads();
     for (int cc = 0; cc < cnt; cc += 64) {
       const int i = cc + lane;
-      __int128 gsum = 0;
+      // Four neighbours at a time: their LDS reads are issued together
+      // (index, then best cost) before the terms are formed.
+      __int128 g0 = 0, g1 = 0;
       if (i < cnt) {
         const int q1 = min(g, (w + 1) * qper);
-        for (int q = w * qper; q < q1; ++q) {
-          const int j = snb[i * g + q];
-          const double d = double(sball[j]) - double(scg[i * g + q]);
-          if (d > 0.0) gsum += fx(double(a.v[j]) * d, S);
+        for (int q = w * qper; q < q1; q += 4) {
+          int jj[4];
+          float cg[4], nv[4], bj[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int e = min(q + u, q1 - 1) * a.W + i;
+            jj[u] = snb[e];
+            cg[u] = scg[e];
+            nv[u] = snv[e];
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) bj[u] = sball[jj[u]];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const double d = double(bj[u]) - double(cg[u]);
+            if (q + u < q1 && d > 0.0) {
+              if (u & 1) g1 += fx(double(nv[u]) * d, S);
+              else g0 += fx(double(nv[u]) * d, S);
+            }
+          }
         }
       }
-      red[tid] = gsum;
+      red[tid] = g0 + g1;
       __syncthreads();
       if (tid < 64 && cc + tid < cnt) {
         __int128 s = 0;
@@ -112,18 +181,14 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
     }
   };
 
+  __syncthreads();
   local_gains();
   publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
 
+  const int nch = a.ldt / kChunkT;
   for (int step = 0; step < a.k; ++step) {
     const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
     if (tw < 0) break;
-    if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
-      __int128 L = 0;
-#pragma unroll
-      for (int q = 0; q < kWaves; ++q) L += sLw[q];
-      a.step_obj[obj_step] = fx_to_double(L, S);
-    }
     const int t = min(tw, a.n - 1);
     if (t >= lo && t < lo + cnt && tid == 0) {
       ssel[t - lo] = 1;
@@ -131,88 +196,51 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
       if (a.step_gain) a.step_gain[step] = fx_to_double(((__int128)sGhi[t - lo] << 64) | (__int128)sGlo[t - lo], S);
     }
 
-    // 1. Own targets that the pick improves, into the block's slice.
-    int base = 0;
-    unsigned long long* mine = a.list + size_t(blk) * a.W * 2;
-    for (int i0 = 0; i0 < cnt; i0 += kBlock) {
-      const int i = i0 + tid;
-      float cv = 0.f, bo = 0.f;
-      bool hit = false;
-      if (i < cnt) {
-        cv = a.C[size_t(lo + i) * a.n + t];
-        bo = sball[lo + i];
-        hit = cv < bo;
-      }
-      const unsigned long long m = __ballot(hit);
-      const int rank = __popcll(m & ((1ull << lane) - 1ull));
-      if (lane == 0) swt[w] = __popcll(m);
-      __syncthreads();
-      int off = base, tot = 0;
+    // 2. The winner's row against b, the wave's chunks loaded together; each
+    // lane lowers its own four targets, and the own targets' changes enter
+    // assign and the block's objective part.
+    const f32x4* row = reinterpret_cast<const f32x4*>(a.T + size_t(t) * a.ldt);
+    f32x4 xr[kLoadsT];
 #pragma unroll
-      for (int q = 0; q < kWaves; ++q) {
-        if (q < w) off += swt[q];
-        tot += swt[q];
-      }
-      if (hit) {
-        const int slot = off + rank;
-        put(mine + size_t(slot) * 2,
-            (unsigned long long)(unsigned int)(lo + i) | ((unsigned long long)__float_as_uint(a.v[lo + i]) << 32));
-        put(mine + size_t(slot) * 2 + 1,
-            (unsigned long long)__float_as_uint(bo) | ((unsigned long long)__float_as_uint(cv) << 32));
-        if (a.assign) a.assign[lo + i] = t;
-      }
-      base += tot;
-      __syncthreads();
-    }
-    if (tid == 0) put(lens_slot(a.lens, blk), ((unsigned long long)(step + 1) << 32) | unsigned(base));
-    if (step + 1 == a.k && blk != 0) break;
-
-    // 2. Every block's slice length, then every change applied to the
-    // replicated best costs (and, in block 0, to the objective).
-    {
-      if (tid == 0) slflag = 0;
-      __syncthreads();
-      int c = 0;
-      if (tid < nb) {
-        unsigned long long x;
-        const unsigned int round = unsigned(step + 1);
-        if (wait_slot(lens_slot(a.lens, tid), a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
-          c = int(x & 0xffffffffull);
-        else
-          slflag = 1;
-      }
-      const int incl = block_inclusive_scan(c, swt);
-      if (tid < nb) spre[tid + 1] = incl;
-      if (tid == 0) spre[0] = 0;
-      __syncthreads();
-    }
-    if (slflag) break;
-    const int total = spre[nb];
+    for (int i = 0; i < kLoadsT; ++i)
+      if (w + i * kWaves < nch) xr[i] = row[(w + i * kWaves) * (kChunkT / 4) + lane];
     __int128 dobj = 0;
-    for (int e = tid; e < total; e += kBlock) {
-      int s0 = 0, s1 = nb;   // spre[s0] <= e < spre[s1]
-      while (s1 - s0 > 1) {
-        const int mid = (s0 + s1) >> 1;
-        if (spre[mid] <= e) s0 = mid;
-        else s1 = mid;
-      }
-      const unsigned long long* src = a.list + (size_t(s0) * a.W + size_t(e - spre[s0])) * 2;
-      const unsigned long long h0 = get(src), h1 = get(src + 1);
-      const int j = int(h0 & 0xffffffffull);
-      const float bn = __uint_as_float(unsigned(h1 >> 32));
-      sball[j] = bn;
-      if (blk == 0) {
-        const double vj = double(__uint_as_float(unsigned(h0 >> 32)));
-        dobj += fx(vj * double(bn), S) - fx(vj * double(__uint_as_float(unsigned(h1 & 0xffffffffull))), S);
+#pragma unroll
+    for (int i = 0; i < kLoadsT; ++i) {
+      const int q0 = w + i * kWaves;
+      if (q0 < nch) {
+        const int j0 = q0 * kChunkT + 4 * lane;
+        f32x4 b = *reinterpret_cast<const f32x4*>(sball + j0);
+        const f32x4 x = xr[i];
+        const bool any = x[0] < b[0] || x[1] < b[1] || x[2] < b[2] || x[3] < b[3];
+        if (any) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            if (x[c] < b[c]) {
+              const int j = j0 + c;
+              if (unsigned(j - lo) < unsigned(cnt)) {
+                if (a.assign) a.assign[j] = t;
+                const double vj = double(sv[j - lo]);
+                dobj += fx(vj * double(x[c]), S) - fx(vj * double(b[c]), S);
+              }
+              b[c] = x[c];
+            }
+          }
+          *reinterpret_cast<f32x4*>(sball + j0) = b;
+        }
       }
     }
-    if (blk == 0) {
-      dobj = wave_sum_i128(dobj);
-      if (lane == 0) sLw[w] += dobj;
-      obj_step = step;
+    dobj = wave_sum_i128(dobj);
+    if (lane == 0) sLw[w] += dobj;
+    __syncthreads();
+    if (tid == 0 && L.part) {
+      __int128 P = 0;
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) P += sLw[q];
+      L.part[size_t(step) * nb + blk] = P;
     }
 
-    // 3. Fresh local gains and this block's candidate for the next step.
+    // 3-4. Fresh local gains and this block's candidate for the next step.
     if (step + 1 < a.k) {
       local_gains();
       publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
@@ -220,20 +248,36 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(IncDev a, const int32
     }
   }
   __syncthreads();
-  if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
-    __int128 L = 0;
-#pragma unroll
-    for (int q = 0; q < kWaves; ++q) L += sLw[q];
-    a.step_obj[obj_step] = fx_to_double(L, S);
-  }
   if (blk == 0 && get(a.abort))
     for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
 }
 
+// L(S) after step l: the blocks' parts added in block order.
+__global__ void local_objective_kernel(const __int128* part, int nb, int k, const int* scale, double* out) {
+  const int l = blockIdx.x * blockDim.x + threadIdx.x;
+  if (l >= k) return;
+  __int128 s = 0;
+  for (int b = 0; b < nb; ++b) s += part[size_t(l) * nb + b];
+  out[l] = fx_to_double(s, *scale);
+}
+
+// Exchange slots, then the objective parts (k x kMaxBlocks), the scale, and T.
+struct LocalLayout {
+  size_t part, scale, T, total;
+};
+LocalLayout local_layout(int64_t n, int64_t k) {
+  LocalLayout L;
+  size_t o = layout(n, k).total;
+  L.part = o; o += a256(size_t(k) * kMaxBlocks * sizeof(__int128));
+  L.scale = o; o += 256;
+  L.T = o; o += a256(size_t(n) * local_ldt(n) * sizeof(float));
+  L.total = o;
+  return L;
+}
+
 }  // namespace
 
-
-size_t sgs_local_workspace_bytes(int64_t n, int64_t k) { return layout(n, k).total; }
+size_t sgs_local_workspace_bytes(int64_t n, int64_t k) { return local_layout(n, k).total; }
 
 hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipStream_t stream) {
   if (p.n < 1 || p.n > kLocalMaxN || g < 1 || g > p.n || g > kLocalMaxG) return hipErrorInvalidValue;
@@ -243,7 +287,8 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
   if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
   const int nb = blocks_for(p.n, cus);
   const int W = (p.n + nb - 1) / nb;
-  const size_t lds = size_t(W) * 16 + size_t(p.n) * 4 + size_t(W) * g * 8 + size_t(W) + 16;
+  const int ldt = local_ldt(p.n);
+  const size_t lds = size_t(W) * (16 + 4 + 1) + size_t(ldt) * 4 + size_t(W) * g * (4 + 4 + 2) + 16;
   if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(sgs_local_kernel),
                                hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
     return e;
@@ -253,9 +298,11 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
     return e;
   if (per_cu < 1) return hipErrorCooperativeLaunchTooLarge;
 
-  const Layout L = layout(p.n, p.k);
+  const Layout X = layout(p.n, p.k);
+  const LocalLayout Y = local_layout(p.n, p.k);
   char* w = static_cast<char*>(p.workspace);
-  IncDev a;
+  LocalDev d;
+  IncDev& a = d.a;
   a.C = p.cost;
   a.v = p.capacity;
   a.n = p.n;
@@ -265,17 +312,32 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
   a.step_gain = p.step_gain;
   a.step_obj = p.step_objective;
   a.assign = p.assign;
-  a.list = reinterpret_cast<unsigned long long*>(w + L.list);
-  a.lens = reinterpret_cast<unsigned long long*>(w + L.lens);
-  a.cand = reinterpret_cast<unsigned long long*>(w + L.cand);
-  a.abort = reinterpret_cast<unsigned int*>(w + L.ctrl);
+  a.list = reinterpret_cast<unsigned long long*>(w + X.list);
+  a.lens = reinterpret_cast<unsigned long long*>(w + X.lens);
+  a.cand = reinterpret_cast<unsigned long long*>(w + X.cand);
+  a.abort = reinterpret_cast<unsigned int*>(w + X.ctrl);
   a.W = W;
+  a.T = reinterpret_cast<float*>(w + Y.T);
+  a.ldt = ldt;
+  d.nbr = nbr;
+  d.g = g;
+  d.part = p.step_objective ? reinterpret_cast<__int128*>(w + Y.part) : nullptr;
+  d.scale = reinterpret_cast<int*>(w + Y.scale);
 
   sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  void* args[] = {&a, const_cast<int32_t**>(&nbr), &g};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_local_kernel), dim3(nb), dim3(kBlock), args,
-                                    lds, stream);
+  const int tiles = (p.n + kTile - 1) / kTile;
+  transpose_kernel<<<dim3(tiles, tiles), 256, 0, stream>>>(p.cost, p.n, a.T, ldt);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  void* args[] = {&d};
+  if ((e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_local_kernel), dim3(nb), dim3(kBlock), args,
+                                      lds, stream)) != hipSuccess)
+    return e;
+  if (p.step_objective) {
+    local_objective_kernel<<<(p.k + 255) / 256, 256, 0, stream>>>(d.part, nb, p.k, d.scale, p.step_objective);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace cp

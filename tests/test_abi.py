@@ -140,7 +140,10 @@ def test_binding_needs_the_library(monkeypatch, tmp_path):
 
 def test_local_workspace_query(lib):
     assert lib.coverprune_sgs_local_workspace(0, 8) == 0
-    assert 16384 * 16 <= lib.coverprune_sgs_local_workspace(16384, 1638) < lib.coverprune_sgs_workspace(16384, 1638, 0)
+    # exchange slots, one objective part per block and step, the transposed cost
+    ws = lib.coverprune_sgs_local_workspace(16384, 1638)
+    assert 16384 * 16384 * 4 + 1638 * 256 * 16 <= ws < 16384 * 16384 * 4 + 1638 * 256 * 16 + (1 << 22)
+    assert lib.coverprune_sgs_local_workspace(1000, 10) >= 1000 * 1024 * 4
 
 
 def _knn(lib, **kw):
