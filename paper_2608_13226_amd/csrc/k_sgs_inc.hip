@@ -16,10 +16,13 @@
 // dropped to zero is exactly zero), the result does not depend on the grid,
 // and equal gains go to the smaller index.
 //
-// One cooperative launch, one block of eight waves per compute unit.  Block b owns the rows
-// and the columns [b W, (b + 1) W): the best costs b_j and capacities of its
-// rows and the running gains of its columns stay in LDS for the whole launch.
-// Per step:
+// The fixed-point scale and the step-0 gains (b = c0) come from two ordinary
+// kernels ahead of the greedy (inc_scale_kernel, inc_first_pass_kernel), which
+// run with many more waves in flight than the greedy itself.  The greedy is
+// one cooperative launch, one block of eight waves per compute unit.  Block b
+// owns the rows and the columns [b W, (b + 1) W): the best costs b_j and
+// capacities of its rows and the running gains of its columns stay in LDS for
+// the whole launch.  Per step:
 //   1. every block reads all blocks' candidates for the step (each block's
 //      best unchosen column, published at the end of the previous step) and
 //      takes the same winner;
@@ -45,7 +48,6 @@ namespace {
 
 constexpr int kBatch = 64;         // change-list entries a wave fetches per round
 constexpr int kChunk = 16;         // of which the rows read together
-constexpr int kInitRows = 16;      // rows a wave has in flight in the full pass
 
 // The greedy of one scene as run by block `blk` of the scene's `nb` blocks.
 __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
@@ -60,7 +62,6 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   unsigned char* ssel = reinterpret_cast<unsigned char*>(sv + a.W);       // [W] chosen columns
   __shared__ __int128 red[kBlock];
   __shared__ __int128 sg[kWaves];
-  __shared__ double sd[kWaves];
   __shared__ int si[kWaves];
   __shared__ int swt[kWaves];
   __shared__ unsigned long long su[kWaves];
@@ -74,65 +75,17 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
     ssel[i] = 0;
   }
 
-  // Fixed-point scale, the same in every block (same sum, same order): every
-  // partial gain is at most c0 sum(v) < 2^(101 - S).
-  double vsum;
-  {
-    double x = 0.0;
-    for (int j = tid; j < a.n; j += kBlock) x += double(a.v[j]);
-    vsum = block_sum_all(x, sd);
+  // The fixed-point scale and the step-0 gains of the own columns (every row
+  // at b = c0) come from the first-pass kernels: the gains as P partial sums
+  // over row ranges, whose integer total does not depend on the split.
+  const int S = *a.scale;
+  for (int i = tid; i < cnt; i += kBlock) {
+    __int128 g = 0;
+    for (int q = 0; q < a.P; ++q) g += a.part[size_t(q) * a.n + lo + i];
+    sGlo[i] = (unsigned long long)g;
+    sGhi[i] = (long long)(g >> 64);
   }
-  const double M = double(a.c0) * vsum;
-  int S = 0;
-  if (M > 0.0) {
-    int e = 0;
-    (void)__builtin_frexp(M, &e);   // M < 2^e
-    S = 101 - e;
-  }
-
-  // Step-0 gains of the own columns: every row at b = c0.  Wave w takes the
-  // 16-row chunks w, w + kWaves, ...; the waves' sums are added in wave order.
-  for (int cc = 0; cc < cnt; cc += 64) {
-    const bool colok = cc + lane < cnt;
-    const int col = lo + cc + lane;
-    // The next chunk's loads are issued before the current chunk's terms
-    // are formed; two accumulators halve the chain of 128-bit additions.
-    __int128 g0 = 0, g1 = 0;
-    float xn[kInitRows], vn[kInitRows];
-    auto load = [&](int j0) {
-#pragma unroll
-      for (int u = 0; u < kInitRows; ++u) {
-        const int j = j0 + u;
-        xn[u] = (colok && j < a.n) ? __builtin_nontemporal_load(a.C + size_t(j) * a.n + col) : a.c0;
-        vn[u] = j < a.n ? a.v[j] : 0.f;
-      }
-    };
-    if (w * kInitRows < a.n) load(w * kInitRows);
-    for (int j0 = w * kInitRows; j0 < a.n; j0 += kWaves * kInitRows) {
-      float x[kInitRows], vj[kInitRows];
-#pragma unroll
-      for (int u = 0; u < kInitRows; ++u) {
-        x[u] = xn[u];
-        vj[u] = vn[u];
-      }
-      if (j0 + kWaves * kInitRows < a.n) load(j0 + kWaves * kInitRows);
-#pragma unroll
-      for (int u = 0; u < kInitRows; u += 2) {
-        g0 += fx(double(vj[u]) * double(fmaxf(a.c0 - x[u], 0.f)), S);
-        g1 += fx(double(vj[u + 1]) * double(fmaxf(a.c0 - x[u + 1], 0.f)), S);
-      }
-    }
-    red[tid] = g0 + g1;
-    __syncthreads();
-    if (tid < 64 && cc + tid < cnt) {
-      __int128 s = 0;
-#pragma unroll
-      for (int q = 0; q < kWaves; ++q) s += red[q * 64 + tid];
-      sGlo[cc + tid] = (unsigned long long)s;
-      sGhi[cc + tid] = (long long)(s >> 64);
-    }
-    __syncthreads();
-  }
+  __syncthreads();
 
   // Block 0 keeps the objective L = sum_j v_j b_j in the gains' fixed point,
   // starting from b = c0, as one running part per wave: a wave adds its share
@@ -334,8 +287,8 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
 // tests each against b_j, and applies the rows that improve straight away.
 // Every block then holds the identical J_l and the identical b, a step needs
 // one exchange (the candidates) instead of two, and no block reads another's
-// list.  T is written by the step-0 pass, which reads the whole cost in
-// column strips anyway: block b writes the rows of T of its own columns.
+// list.  T is written by the first-pass kernel, which reads the whole cost in
+// column strips for the step-0 gains anyway.
 //
 // Per step and wave: the wave's chunks of the winner's row (256 targets a
 // load, 16 bytes a lane) are loaded together; a chunk without a hit costs one
@@ -349,7 +302,6 @@ constexpr int kRowsMaxW = 128;     // columns per block: two per lane
 constexpr int kRowChunk = 256;     // targets per wave-load of the winner's row
 constexpr int kList = 128;         // hits a wave collects before applying them (dense steps)
 constexpr int kCap = kList * kWaves;   // hits a block lists in one step
-constexpr int kInitRowsT = 16;     // rows a wave has in flight in the transposing pass
 
 int rows_ldt(int64_t n) { return int((n + kRowChunk - 1) / kRowChunk * kRowChunk); }
 
@@ -382,7 +334,6 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   unsigned char* ssel = reinterpret_cast<unsigned char*>(sball + a.ldt);   // [W] chosen columns
   __shared__ __int128 red[kBlock];
   __shared__ __int128 sg[kWaves];
-  __shared__ double sd[kWaves];
   __shared__ int si[kWaves];
   __shared__ unsigned long long su[kWaves];
   __shared__ int sflag;
@@ -395,65 +346,15 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
 
   for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
   for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
-  const int S = fixed_scale(a, sd);
-
-  // Step-0 gains of the own columns (every row at b = c0), and the own rows
-  // of T: lane `col` holds C_tm[j0 .. j0 + 16)[col], which is T[col][j0 ..
-  // j0 + 16), half a 128-byte line whose other half the next wave writes in
-  // the same round.  Wave w takes the 16-row chunks w, w + kWaves, ...; the
-  // waves' sums are added in wave order.
-  for (int cc = 0; cc < cnt; cc += 64) {
-    const bool colok = cc + lane < cnt;
-    const int col = lo + cc + lane;
-    f32x4* trow = reinterpret_cast<f32x4*>(a.T + size_t(colok ? col : 0) * a.ldt);
-    // The next chunk's loads are issued before the current chunk's terms
-    // are formed; two accumulators halve the chain of 128-bit additions.
-    __int128 g0 = 0, g1 = 0;
-    float xn[kInitRowsT], vn[kInitRowsT];
-    auto load = [&](int j0) {
-#pragma unroll
-      for (int u = 0; u < kInitRowsT; ++u) {
-        const int j = j0 + u;
-        xn[u] = (colok && j < a.n) ? __builtin_nontemporal_load(a.C + size_t(j) * a.n + col) : a.c0;
-        vn[u] = j < a.n ? a.v[j] : 0.f;
-      }
-    };
-    if (w * kInitRowsT < a.n) load(w * kInitRowsT);
-    for (int j0 = w * kInitRowsT; j0 < a.n; j0 += kWaves * kInitRowsT) {
-      float x[kInitRowsT], vj[kInitRowsT];
-#pragma unroll
-      for (int u = 0; u < kInitRowsT; ++u) {
-        x[u] = xn[u];
-        vj[u] = vn[u];
-      }
-      if (j0 + kWaves * kInitRowsT < a.n) load(j0 + kWaves * kInitRowsT);
-#pragma unroll
-      for (int u = 0; u < kInitRowsT; u += 2) {
-        g0 += fx(double(vj[u]) * double(fmaxf(a.c0 - x[u], 0.f)), S);
-        g1 += fx(double(vj[u + 1]) * double(fmaxf(a.c0 - x[u + 1], 0.f)), S);
-      }
-      // Ordinary (write-back) stores: the two halves of a line meet in L2.
-      if (colok) {
-#pragma unroll
-        for (int q = 0; q < kInitRowsT / 4; ++q)
-          trow[j0 / 4 + q] = f32x4{x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
-      }
-    }
-    red[tid] = g0 + g1;
-    __syncthreads();
-    if (tid < 64 && cc + tid < cnt) {
-      __int128 s = 0;
-#pragma unroll
-      for (int q = 0; q < kWaves; ++q) s += red[q * 64 + tid];
-      sGlo[cc + tid] = (unsigned long long)s;
-      sGhi[cc + tid] = (long long)(s >> 64);
-    }
-    __syncthreads();
+  // The fixed-point scale, the step-0 gains (as P partial sums over row
+  // ranges) and T come from the first-pass kernels.
+  const int S = *a.scale;
+  for (int i = tid; i < cnt; i += kBlock) {
+    __int128 g = 0;
+    for (int q = 0; q < a.P; ++q) g += a.part[size_t(q) * a.n + lo + i];
+    sGlo[i] = (unsigned long long)g;
+    sGhi[i] = (long long)(g >> 64);
   }
-  // The rows of T are read by every block: each wave's writes reach memory
-  // before the block's step-0 candidate is published, and every block
-  // acquires after it has read all candidates of step 0.
-  __threadfence();
   __syncthreads();
 
   // Block 0 keeps the objective as one running part per wave (as in the
@@ -473,7 +374,6 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   for (int step = 0; step < a.k; ++step) {
     const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
     if (tw < 0) break;
-    if (step == 0) __threadfence();
     if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
       __int128 L = 0;
 #pragma unroll
@@ -706,6 +606,86 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) { inc_body(a,
 template <int NG, int RL>
 __global__ __launch_bounds__(kBlock) void sgs_rows_kernel(IncDev a) { rows_body<NG, RL>(a, blockIdx.x, gridDim.x); }
 
+// The fixed-point scale of a scene (one block; the sum in the same order as
+// every block of the greedy would take it).
+__global__ __launch_bounds__(kBlock) void inc_scale_kernel(IncDev a, int* scale) {
+  __shared__ double sd[kWaves];
+  const int S = fixed_scale(a, sd);
+  if (threadIdx.x == 0) *scale = S;
+}
+
+// Step-0 gains, every row at b = c0, split over a grid of (column strip,
+// row range) blocks so that the pass runs with many more waves in flight than
+// the greedy's one block per compute unit: block (b, p) sums rows
+// [p R, (p + 1) R) of columns [b W, (b + 1) W) into part[p][column], 128-bit
+// fixed point, four waves adding in wave order.  With WT it also writes those
+// rows of T: lane `col` holds C_tm[j0 .. j0 + 16)[col], which is T[col][j0 ..
+// j0 + 16), half a 128-byte line whose other half the next wave writes in the
+// same round (R is a multiple of 16, so no line is shared between blocks).
+constexpr int kPassThreads = 256;
+constexpr int kPassWaves = kPassThreads / 64;
+constexpr int kPassRows = 16;
+
+__host__ __device__ __forceinline__ int pass_rows(int n, int P) {
+  return ((n + P - 1) / P + kPassRows - 1) / kPassRows * kPassRows;
+}
+
+template <bool WT>
+__global__ __launch_bounds__(kPassThreads) void inc_first_pass_kernel(IncDev a, __int128* part) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lo = blockIdx.x * a.W, cnt = max(0, min(a.n, lo + a.W) - lo);
+  const int R = pass_rows(a.n, a.P), r0 = blockIdx.y * R, r1 = min(a.n, r0 + R);
+  const int S = *a.scale;
+  __shared__ __int128 red[kPassThreads];
+  for (int cc = 0; cc < cnt; cc += 64) {
+    const bool colok = cc + lane < cnt;
+    const int col = lo + cc + lane;
+    f32x4* trow = WT ? reinterpret_cast<f32x4*>(a.T + size_t(colok ? col : 0) * a.ldt) : nullptr;
+    // The next chunk's loads are issued before the current chunk's terms are
+    // formed; two accumulators halve the chain of 128-bit additions.
+    __int128 g0 = 0, g1 = 0;
+    float xn[kPassRows], vn[kPassRows];
+    auto load = [&](int j0) {
+#pragma unroll
+      for (int u = 0; u < kPassRows; ++u) {
+        const int j = j0 + u;
+        xn[u] = (colok && j < r1) ? __builtin_nontemporal_load(a.C + size_t(j) * a.n + col) : a.c0;
+        vn[u] = j < r1 ? a.v[j] : 0.f;
+      }
+    };
+    if (r0 + w * kPassRows < r1) load(r0 + w * kPassRows);
+    for (int j0 = r0 + w * kPassRows; j0 < r1; j0 += kPassWaves * kPassRows) {
+      float x[kPassRows], vj[kPassRows];
+#pragma unroll
+      for (int u = 0; u < kPassRows; ++u) {
+        x[u] = xn[u];
+        vj[u] = vn[u];
+      }
+      if (j0 + kPassWaves * kPassRows < r1) load(j0 + kPassWaves * kPassRows);
+#pragma unroll
+      for (int u = 0; u < kPassRows; u += 2) {
+        g0 += fx(double(vj[u]) * double(fmaxf(a.c0 - x[u], 0.f)), S);
+        g1 += fx(double(vj[u + 1]) * double(fmaxf(a.c0 - x[u + 1], 0.f)), S);
+      }
+      // Ordinary (write-back) stores: the two halves of a line meet in L2.
+      if (WT && colok) {
+#pragma unroll
+        for (int q = 0; q < kPassRows / 4; ++q)
+          trow[j0 / 4 + q] = f32x4{x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
+      }
+    }
+    red[threadIdx.x] = g0 + g1;
+    __syncthreads();
+    if (threadIdx.x < 64 && cc + threadIdx.x < cnt) {
+      __int128 s = 0;
+#pragma unroll
+      for (int q = 0; q < kPassWaves; ++q) s += red[q * 64 + threadIdx.x];
+      part[size_t(blockIdx.y) * a.n + lo + cc + threadIdx.x] = s;
+    }
+    __syncthreads();
+  }
+}
+
 // Several scenes in one launch: scene s runs on blocks [g0[s], g0[s + 1])
 // with its own slots, change lists and abort flag, so the scenes' greedies
 // proceed independently side by side.
@@ -749,11 +729,23 @@ const void* rows_batch_kernel(int64_t n, int W) {
   return reinterpret_cast<const void*>(sgs_rows_batch_kernel<2, 16>);
 }
 
-// Exchange slots and lists, then (when the rows form may run) T.
-size_t inc_bytes(int64_t n, int64_t k, bool compact) {
-  const size_t base = layout(n, k).total;
-  return !compact && n <= kRowsMaxN ? base + a256(size_t(n) * rows_ldt(n) * sizeof(float)) : base;
+// Exchange slots and lists, the first pass's partial gains and scale, then
+// (when the rows form may run) T.
+constexpr int kPassParts = 4;   // row ranges of the first pass
+struct IncLayout {
+  size_t part, scale, T, total;
+};
+IncLayout inc_layout(int64_t n, int64_t k, bool compact) {
+  IncLayout L;
+  size_t o = layout(n, k).total;
+  L.part = o; o += a256(size_t(kPassParts) * n * sizeof(__int128));
+  L.scale = o; o += 256;
+  L.T = o;
+  if (!compact && n <= kRowsMaxN) o += a256(size_t(n) * rows_ldt(n) * sizeof(float));
+  L.total = o;
+  return L;
 }
+size_t inc_bytes(int64_t n, int64_t k, bool compact) { return inc_layout(n, k, compact).total; }
 
 IncDev inc_dev(const SgsParams& p, char* w, int W, bool rows) {
   const Layout L = layout(p.n, p.k);
@@ -772,9 +764,26 @@ IncDev inc_dev(const SgsParams& p, char* w, int W, bool rows) {
   a.cand = reinterpret_cast<unsigned long long*>(w + L.cand);
   a.abort = reinterpret_cast<unsigned int*>(w + L.ctrl);
   a.W = W;
-  a.T = rows ? reinterpret_cast<float*>(w + L.total) : nullptr;
+  const IncLayout M = inc_layout(p.n, p.k, !rows);
+  a.T = rows ? reinterpret_cast<float*>(w + M.T) : nullptr;
   a.ldt = rows ? rows_ldt(p.n) : 0;
+  a.part = reinterpret_cast<const __int128*>(w + M.part);
+  a.P = kPassParts;
+  a.scale = reinterpret_cast<const int*>(w + M.scale);
   return a;
+}
+
+// The scale and the step-0 pass of one scene, ahead of the greedy's launch.
+hipError_t launch_first_pass(const IncDev& a, int nb, hipStream_t stream) {
+  inc_scale_kernel<<<1, kBlock, 0, stream>>>(a, const_cast<int*>(a.scale));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  __int128* part = const_cast<__int128*>(a.part);
+  if (a.T)
+    inc_first_pass_kernel<true><<<dim3(nb, a.P), kPassThreads, 0, stream>>>(a, part);
+  else
+    inc_first_pass_kernel<false><<<dim3(nb, a.P), kPassThreads, 0, stream>>>(a, part);
+  return hipGetLastError();
 }
 
 size_t lds_for(int W) { return size_t(W) * (16 + 4 + 4 + 1) + 16; }
@@ -806,6 +815,7 @@ hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t 
   IncDev a = inc_dev(p, static_cast<char*>(p.workspace), W, rows);
   sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = launch_first_pass(a, nb, stream)) != hipSuccess) return e;
   void* args[] = {&a};
   return hipLaunchCooperativeKernel(kernel, dim3(nb), dim3(kBlock), args, lds, stream);
 }
@@ -874,6 +884,7 @@ hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, bool comp
   for (int s = 0; s < count; ++s) {
     sgs_inc_init_kernel<<<std::min(1024, (std::max(p[s].n, p[s].k) + 255) / 256), 256, 0, stream>>>(b.scene[s]);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_first_pass(b.scene[s], b.g0[s + 1] - b.g0[s], stream)) != hipSuccess) return e;
   }
   void* args[] = {&b};
   return hipLaunchCooperativeKernel(kernel, dim3(used), dim3(kBlock), args, lds, stream);

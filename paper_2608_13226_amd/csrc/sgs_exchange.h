@@ -82,6 +82,9 @@ struct IncDev {
   int W;                      // rows and columns per block
   float* T;                   // rows form only: [n][ldt] source-major copy, T[s][t] = C(s, t)
   int ldt;                    // its row stride, n rounded up to a whole 256-row chunk
+  const __int128* part;       // incremental form: [P][n] step-0 gains summed over P row ranges
+  int P;
+  const int* scale;           // incremental form: the fixed-point exponent S
 };
 
 struct Layout {
