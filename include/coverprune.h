@@ -159,9 +159,11 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
  *             CP_SGS_INCREMENTAL: the gains are summed once at b = c0 and then
  *             updated, step by step, from the rows of the targets whose best
  *             cost the pick lowers (their old and new b); the terms are the
- *             same float32 differences and float64 products, only the order
- *             of the float64 additions differs, so picks can differ from the
- *             dense sweep only between gains within rounding of each other.
+ *             same float32 differences and float64 products, each rounded
+ *             down onto a grid of 2^-S (c0 * sum v < 2^(62 - S)) and summed
+ *             exactly in 64-bit integers, so picks can differ from the dense
+ *             sweep's float64 sums only between gains within rounding of
+ *             each other.
  *             For n <= 32768 every compute unit keeps all n best costs and
  *             finds the targets a pick improves itself, from the pick's row
  *             of a source-major copy of the cost that the first pass writes
@@ -239,10 +241,10 @@ cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count,
  * while a pick still lowers b_j of every target it is cheaper for (the
  * residual of Eq. 14 is over all targets) and L(S) is summed over all of
  * them.  Each term takes the float64 difference of the two float32 costs and
- * a float64 product; every gain is summed afresh each step in exact 128-bit
- * fixed point at a scale of 2^-S, S set by c0 * sum v (so only terms below
- * that resolution differ from a float64 sum).  Equal gains go to the smaller
- * index; exactly k tokens are selected.
+ * a float64 product; every gain is summed afresh each step in exact 64-bit
+ * fixed point at a scale of 2^-S with c0 * sum v < 2^(62 - S) (so only terms
+ * below that resolution differ from a float64 sum).  Equal gains go to the
+ * smaller index; exactly k tokens are selected.
  *
  * coverprune_knn writes the tables: row t lists the g tokens nearest to t,
  * ordered by (distance, index), t itself included.  Distances are compared as

@@ -10,11 +10,12 @@
 // of K full matrices.  Every term v_j max(0, b_j - C) is formed as in the
 // dense sweep (the difference in float32, the product exactly in float64) and
 // then rounded down onto a fixed-point grid of 2^-S, S chosen per launch so
-// that c0 sum(v) stays below 2^101; gains are sums of these integers in 128
+// that c0 sum(v) stays below 2^62; gains are sums of these integers in 64
 // bits.  Integer sums do not depend on their order, so the running gains are
 // bit-identical to gains summed afresh from the current b (a gain that has
-// dropped to zero is exactly zero), the result does not depend on the grid,
-// and equal gains go to the smaller index.
+// dropped to zero is exactly zero), and equal gains go to the smaller index.
+// The grid, about 2^-62 c0 sum(v), is finer than the rounding of a float64
+// sum of the same terms.
 //
 // The fixed-point scale and the step-0 gains (b = c0) come from two ordinary
 // kernels ahead of the greedy (inc_scale_kernel, inc_first_pass_kernel), which
@@ -55,13 +56,12 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lo = blk * a.W;
   const int cnt = max(0, min(a.n, lo + a.W) - lo);
-  unsigned long long* sGlo = smem;                                 // [W] running gains, low words
-  long long* sGhi = reinterpret_cast<long long*>(sGlo + a.W);      // [W] high words
-  float* sb = reinterpret_cast<float*>(sGhi + a.W);                // [W] best costs of own rows
+  long long* sG = reinterpret_cast<long long*>(smem);             // [W] running gains
+  float* sb = reinterpret_cast<float*>(sG + a.W);                  // [W] best costs of own rows
   float* sv = sb + a.W;                                            // [W] capacities of own rows
   unsigned char* ssel = reinterpret_cast<unsigned char*>(sv + a.W);       // [W] chosen columns
-  __shared__ __int128 red[kBlock];
-  __shared__ __int128 sg[kWaves];
+  __shared__ long long red[kBlock];
+  __shared__ long long sg[kWaves];
   __shared__ int si[kWaves];
   __shared__ int swt[kWaves];
   __shared__ unsigned long long su[kWaves];
@@ -80,10 +80,9 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   // over row ranges, whose integer total does not depend on the split.
   const int S = *a.scale;
   for (int i = tid; i < cnt; i += kBlock) {
-    __int128 g = 0;
+    long long g = 0;
     for (int q = 0; q < a.P; ++q) g += a.part[size_t(q) * a.n + lo + i];
-    sGlo[i] = (unsigned long long)g;
-    sGhi[i] = (long long)(g >> 64);
+    sG[i] = g;
   }
   __syncthreads();
 
@@ -91,16 +90,16 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   // starting from b = c0, as one running part per wave: a wave adds its share
   // of a step's changes without a barrier, and thread 0 totals the parts for
   // step l after the next step's first barrier (after the loop for the last).
-  __shared__ __int128 sLw[kWaves];
+  __shared__ long long sLw[kWaves];
   int obj_step = -1;
   if (blk == 0) {
-    __int128 x = 0;
+    long long x = 0;
     for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
-    const __int128 L0 = block_sum_i128(x, sg);
+    const long long L0 = block_sum_i64(x, sg);
     if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
   }
 
-  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
+  publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
 
   for (int step = 0; step < a.k; ++step) {
     // Some block has a candidate while unchosen columns remain; the clamp
@@ -108,7 +107,7 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
     const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
     if (tw < 0) break;
     if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
-      __int128 L = 0;
+      long long L = 0;
 #pragma unroll
       for (int q = 0; q < kWaves; ++q) L += sLw[q];
       a.step_obj[obj_step] = fx_to_double(L, S);
@@ -117,7 +116,7 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
     if (t >= lo && t < lo + cnt && tid == 0) {
       ssel[t - lo] = 1;
       a.selected[step] = t;
-      if (a.step_gain) a.step_gain[step] = fx_to_double(((__int128)sGhi[t - lo] << 64) | (__int128)sGlo[t - lo], S);
+      if (a.step_gain) a.step_gain[step] = fx_to_double(sG[t - lo], S);
     }
 
     // 1. Own rows that the pick improves, compacted into the block's slice.
@@ -185,11 +184,11 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
     // 3. Apply the changes to the own columns' gains.  Each lane of a round
     // locates and fetches one entry; the entries are then broadcast and every
     // lane reads its column of each entry's row.
-    __int128 dobj = 0;
+    long long dobj = 0;
     for (int cc = 0; cc < cnt; cc += 64) {
       const bool colok = cc + lane < cnt;
       const int col = lo + cc + lane;
-      __int128 g = 0;
+      long long g = 0;
       // Rounds of up to kBatch entries per wave, the list split evenly over
       // the waves.
       const int per = min(kBatch, (total + kWaves - 1) / kWaves);
@@ -246,28 +245,27 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
       red[tid] = g;
       __syncthreads();
       if (tid < 64 && cc + tid < cnt) {
-        __int128 s = ((__int128)sGhi[cc + tid] << 64) | (__int128)sGlo[cc + tid];
+        long long s = sG[cc + tid];
 #pragma unroll
         for (int q = 0; q < kWaves; ++q) s += red[q * 64 + tid];
-        sGlo[cc + tid] = (unsigned long long)s;
-        sGhi[cc + tid] = (long long)(s >> 64);
+        sG[cc + tid] = s;
       }
       __syncthreads();
     }
     if (blk == 0) {
-      dobj = wave_sum_i128(dobj);
+      dobj = wave_sum_i64(dobj);
       if (lane == 0) sLw[w] += dobj;
       obj_step = step;
     }
 
     // 4. This block's candidate for the next step.
     if (step + 1 < a.k)
-      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
+      publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
                      epoch_of(step + 1), sg, si);
   }
   __syncthreads();
   if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
-    __int128 L = 0;
+    long long L = 0;
 #pragma unroll
     for (int q = 0; q < kWaves; ++q) L += sLw[q];
     a.step_obj[obj_step] = fx_to_double(L, S);
@@ -306,7 +304,7 @@ constexpr int kCap = kList * kWaves;   // hits a block lists in one step
 int rows_ldt(int64_t n) { return int((n + kRowChunk - 1) / kRowChunk * kRowChunk); }
 
 // Fixed-point scale, the same in every block (same sum, same order): every
-// partial gain is at most c0 sum(v) < 2^(101 - S).
+// partial gain is at most c0 sum(v) < 2^(62 - S).
 __device__ __forceinline__ int fixed_scale(const IncDev& a, double* sd) {
   double x = 0.0;
   for (int j = threadIdx.x; j < a.n; j += kBlock) x += double(a.v[j]);
@@ -315,7 +313,7 @@ __device__ __forceinline__ int fixed_scale(const IncDev& a, double* sd) {
   if (M > 0.0) {
     int e = 0;
     (void)__builtin_frexp(M, &e);   // M < 2^e
-    S = 101 - e;
+    S = 62 - e;
   }
   return S;
 }
@@ -328,12 +326,11 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lo = blk * a.W;
   const int cnt = max(0, min(a.n, lo + a.W) - lo);
-  unsigned long long* sGlo = smem;                                 // [W] running gains, low words
-  long long* sGhi = reinterpret_cast<long long*>(sGlo + a.W);      // [W] high words
-  float* sball = reinterpret_cast<float*>(sGhi + a.W);             // [ldt] b_j; -inf past n (never a hit)
+  long long* sG = reinterpret_cast<long long*>(smem);             // [W] running gains (W rounded up to even)
+  float* sball = reinterpret_cast<float*>(sG + ((a.W + 1) & ~1));  // [ldt] b_j, 16-byte aligned; -inf past n
   unsigned char* ssel = reinterpret_cast<unsigned char*>(sball + a.ldt);   // [W] chosen columns
-  __shared__ __int128 red[kBlock];
-  __shared__ __int128 sg[kWaves];
+  __shared__ long long red[kBlock];
+  __shared__ long long sg[kWaves];
   __shared__ int si[kWaves];
   __shared__ unsigned long long su[kWaves];
   __shared__ int sflag;
@@ -350,32 +347,31 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   // ranges) and T come from the first-pass kernels.
   const int S = *a.scale;
   for (int i = tid; i < cnt; i += kBlock) {
-    __int128 g = 0;
+    long long g = 0;
     for (int q = 0; q < a.P; ++q) g += a.part[size_t(q) * a.n + lo + i];
-    sGlo[i] = (unsigned long long)g;
-    sGhi[i] = (long long)(g >> 64);
+    sG[i] = g;
   }
   __syncthreads();
 
   // Block 0 keeps the objective as one running part per wave (as in the
   // exchange form).
-  __shared__ __int128 sLw[kWaves];
+  __shared__ long long sLw[kWaves];
   int obj_step = -1;
   if (blk == 0) {
-    __int128 x = 0;
+    long long x = 0;
     for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
-    const __int128 L0 = block_sum_i128(x, sg);
+    const long long L0 = block_sum_i64(x, sg);
     if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
   }
 
-  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
+  publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
 
   const int nch = a.ldt / kRowChunk;
   for (int step = 0; step < a.k; ++step) {
     const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
     if (tw < 0) break;
     if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
-      __int128 L = 0;
+      long long L = 0;
 #pragma unroll
       for (int q = 0; q < kWaves; ++q) L += sLw[q];
       a.step_obj[obj_step] = fx_to_double(L, S);
@@ -384,7 +380,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     if (t >= lo && t < lo + cnt && tid == 0) {
       ssel[t - lo] = 1;
       a.selected[step] = t;
-      if (a.step_gain) a.step_gain[step] = fx_to_double(((__int128)sGhi[t - lo] << 64) | (__int128)sGlo[t - lo], S);
+      if (a.step_gain) a.step_gain[step] = fx_to_double(sG[t - lo], S);
     }
 
     // The wave's chunks of the winner's row, all loads in flight together.
@@ -394,10 +390,10 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     for (int i = 0; i < RL; ++i)
       if (w + i * kWaves < nch) xr[i] = row[(w + i * kWaves) * (kRowChunk / 4) + lane];
 
-    __int128 g[NG];
+    long long g[NG];
 #pragma unroll
     for (int q = 0; q < NG; ++q) g[q] = 0;
-    __int128 dobj = 0;
+    long long dobj = 0;
     // Applies listed hits base .. base + m to the wave's partial gains (and,
     // in block 0, to the objective), and records them in assign and (with
     // setb) in b.
@@ -572,27 +568,26 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       __syncthreads();
       if (tid < 64 && q * 64 + tid < cnt) {
         const int c = q * 64 + tid;
-        __int128 s = ((__int128)sGhi[c] << 64) | (__int128)sGlo[c];
+        long long s = sG[c];
 #pragma unroll
         for (int r = 0; r < kWaves; ++r) s += red[r * 64 + tid];
-        sGlo[c] = (unsigned long long)s;
-        sGhi[c] = (long long)(s >> 64);
+        sG[c] = s;
       }
       if (NG > 1) __syncthreads();
     }
     if (blk == 0) {
-      dobj = wave_sum_i128(dobj);
+      dobj = wave_sum_i64(dobj);
       if (lane == 0) sLw[w] += dobj;
       obj_step = step;
     }
 
     if (step + 1 < a.k)
-      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
+      publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
                      epoch_of(step + 1), sg, si);
   }
   __syncthreads();
   if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
-    __int128 L = 0;
+    long long L = 0;
 #pragma unroll
     for (int q = 0; q < kWaves; ++q) L += sLw[q];
     a.step_obj[obj_step] = fx_to_double(L, S);
@@ -617,7 +612,7 @@ __global__ __launch_bounds__(kBlock) void inc_scale_kernel(IncDev a, int* scale)
 // Step-0 gains, every row at b = c0, split over a grid of (column strip,
 // row range) blocks so that the pass runs with many more waves in flight than
 // the greedy's one block per compute unit: block (b, p) sums rows
-// [p R, (p + 1) R) of columns [b W, (b + 1) W) into part[p][column], 128-bit
+// [p R, (p + 1) R) of columns [b W, (b + 1) W) into part[p][column], 64-bit
 // fixed point, four waves adding in wave order.  With WT it also writes those
 // rows of T: lane `col` holds C_tm[j0 .. j0 + 16)[col], which is T[col][j0 ..
 // j0 + 16), half a 128-byte line whose other half the next wave writes in the
@@ -631,19 +626,19 @@ __host__ __device__ __forceinline__ int pass_rows(int n, int P) {
 }
 
 template <bool WT>
-__global__ __launch_bounds__(kPassThreads) void inc_first_pass_kernel(IncDev a, __int128* part) {
+__global__ __launch_bounds__(kPassThreads) void inc_first_pass_kernel(IncDev a, long long* part) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int lo = blockIdx.x * a.W, cnt = max(0, min(a.n, lo + a.W) - lo);
   const int R = pass_rows(a.n, a.P), r0 = blockIdx.y * R, r1 = min(a.n, r0 + R);
   const int S = *a.scale;
-  __shared__ __int128 red[kPassThreads];
+  __shared__ long long red[kPassThreads];
   for (int cc = 0; cc < cnt; cc += 64) {
     const bool colok = cc + lane < cnt;
     const int col = lo + cc + lane;
     f32x4* trow = WT ? reinterpret_cast<f32x4*>(a.T + size_t(colok ? col : 0) * a.ldt) : nullptr;
     // The next chunk's loads are issued before the current chunk's terms are
-    // formed; two accumulators halve the chain of 128-bit additions.
-    __int128 g0 = 0, g1 = 0;
+    // formed; two accumulators.
+    long long g0 = 0, g1 = 0;
     float xn[kPassRows], vn[kPassRows];
     auto load = [&](int j0) {
 #pragma unroll
@@ -677,7 +672,7 @@ __global__ __launch_bounds__(kPassThreads) void inc_first_pass_kernel(IncDev a, 
     red[threadIdx.x] = g0 + g1;
     __syncthreads();
     if (threadIdx.x < 64 && cc + threadIdx.x < cnt) {
-      __int128 s = 0;
+      long long s = 0;
 #pragma unroll
       for (int q = 0; q < kPassWaves; ++q) s += red[q * 64 + threadIdx.x];
       part[size_t(blockIdx.y) * a.n + lo + cc + threadIdx.x] = s;
@@ -738,7 +733,7 @@ struct IncLayout {
 IncLayout inc_layout(int64_t n, int64_t k, bool compact) {
   IncLayout L;
   size_t o = layout(n, k).total;
-  L.part = o; o += a256(size_t(kPassParts) * n * sizeof(__int128));
+  L.part = o; o += a256(size_t(kPassParts) * n * sizeof(long long));
   L.scale = o; o += 256;
   L.T = o;
   if (!compact && n <= kRowsMaxN) o += a256(size_t(n) * rows_ldt(n) * sizeof(float));
@@ -767,7 +762,7 @@ IncDev inc_dev(const SgsParams& p, char* w, int W, bool rows) {
   const IncLayout M = inc_layout(p.n, p.k, !rows);
   a.T = rows ? reinterpret_cast<float*>(w + M.T) : nullptr;
   a.ldt = rows ? rows_ldt(p.n) : 0;
-  a.part = reinterpret_cast<const __int128*>(w + M.part);
+  a.part = reinterpret_cast<const long long*>(w + M.part);
   a.P = kPassParts;
   a.scale = reinterpret_cast<const int*>(w + M.scale);
   return a;
@@ -778,7 +773,7 @@ hipError_t launch_first_pass(const IncDev& a, int nb, hipStream_t stream) {
   inc_scale_kernel<<<1, kBlock, 0, stream>>>(a, const_cast<int*>(a.scale));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  __int128* part = const_cast<__int128*>(a.part);
+  long long* part = const_cast<long long*>(a.part);
   if (a.T)
     inc_first_pass_kernel<true><<<dim3(nb, a.P), kPassThreads, 0, stream>>>(a, part);
   else
@@ -786,8 +781,8 @@ hipError_t launch_first_pass(const IncDev& a, int nb, hipStream_t stream) {
   return hipGetLastError();
 }
 
-size_t lds_for(int W) { return size_t(W) * (16 + 4 + 4 + 1) + 16; }
-size_t lds_rows(int W, int64_t n) { return size_t(W) * (16 + 1) + size_t(rows_ldt(n)) * 4 + 16; }
+size_t lds_for(int W) { return size_t(W) * (8 + 4 + 4 + 1) + 16; }
+size_t lds_rows(int W, int64_t n) { return size_t((W + 1) & ~1) * 8 + size_t(rows_ldt(n)) * 4 + size_t(W) + 16; }
 
 hipError_t fits(const void* kernel, size_t lds) {
   int per_cu = 0;

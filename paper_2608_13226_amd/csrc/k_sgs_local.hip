@@ -64,7 +64,7 @@ struct LocalDev {
   IncDev a;
   const int32_t* nbr;
   int g;
-  __int128* part;      // [k][blocks] running objective part of each block after each step
+  long long* part;     // [k][blocks] running objective part of each block after each step
   int* scale;          // the fixed-point exponent S, for the objective sums
 };
 
@@ -76,9 +76,8 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
   const int blk = blockIdx.x, nb = gridDim.x;
   const int lo = blk * a.W;
   const int cnt = max(0, min(a.n, lo + a.W) - lo);
-  unsigned long long* sGlo = smem;                                 // [W] gains, low words
-  long long* sGhi = reinterpret_cast<long long*>(sGlo + a.W);      // [W] high words
-  float* sball = reinterpret_cast<float*>(sGhi + a.W);             // [ldt] b_j; -inf past n (never lowered)
+  long long* sG = reinterpret_cast<long long*>(smem);             // [W] gains (W rounded up to even)
+  float* sball = reinterpret_cast<float*>(sG + ((a.W + 1) & ~1));  // [ldt] b_j, 16-byte aligned; -inf past n
   // The band, neighbour-major ([g][W]: entry q of candidate i at q W + i),
   // so that the lanes of a wave (consecutive candidates) read consecutive
   // words.
@@ -87,13 +86,13 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
   float* sv = snv + size_t(a.W) * g;                               // [W] v of the own targets
   unsigned short* snb = reinterpret_cast<unsigned short*>(sv + a.W);   // [g][W] M_g(c)
   unsigned char* ssel = reinterpret_cast<unsigned char*>(snb + size_t(a.W) * g);   // [W]
-  __shared__ __int128 red[kBlock];
-  __shared__ __int128 sg[kWaves];
+  __shared__ long long red[kBlock];
+  __shared__ long long sg[kWaves];
   __shared__ double sd[kWaves];
   __shared__ int si[kWaves];
   __shared__ unsigned long long su[kWaves];
   __shared__ int sflag;
-  __shared__ __int128 sLw[kWaves];            // this block's objective part, one running share per wave
+  __shared__ long long sLw[kWaves];            // this block's objective part, one running share per wave
 
   for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
   for (int i = tid; i < cnt; i += kBlock) {
@@ -123,15 +122,15 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
   if (M > 0.0) {
     int e = 0;
     (void)__builtin_frexp(M, &e);
-    S = 101 - e;
+    S = 62 - e;
   }
   if (blk == 0 && tid == 0) *L.scale = S;
 
   // The objective part of the own targets at b = c0.
   {
-    __int128 x = 0;
+    long long x = 0;
     for (int i = tid; i < cnt; i += kBlock) x += fx(double(sv[i]) * double(a.c0), S);
-    const __int128 P0 = block_sum_i128(x, sg);
+    const long long P0 = block_sum_i64(x, sg);
     if (tid < kWaves) sLw[tid] = tid == 0 ? P0 : 0;
   }
 
@@ -143,7 +142,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
       const int i = cc + lane;
       // Four neighbours at a time: their LDS reads are issued together
       // (index, then best cost) before the terms are formed.
-      __int128 g0 = 0, g1 = 0;
+      long long g0 = 0, g1 = 0;
       if (i < cnt) {
         const int q1 = min(g, (w + 1) * qper);
         for (int q = w * qper; q < q1; q += 4) {
@@ -171,11 +170,10 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
       red[tid] = g0 + g1;
       __syncthreads();
       if (tid < 64 && cc + tid < cnt) {
-        __int128 s = 0;
+        long long s = 0;
 #pragma unroll
         for (int q = 0; q < kWaves; ++q) s += red[q * 64 + tid];
-        sGlo[cc + tid] = (unsigned long long)s;
-        sGhi[cc + tid] = (long long)(s >> 64);
+        sG[cc + tid] = s;
       }
       __syncthreads();
     }
@@ -183,7 +181,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
 
   __syncthreads();
   local_gains();
-  publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
+  publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
 
   const int nch = a.ldt / kChunkT;
   for (int step = 0; step < a.k; ++step) {
@@ -193,7 +191,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
     if (t >= lo && t < lo + cnt && tid == 0) {
       ssel[t - lo] = 1;
       a.selected[step] = t;
-      if (a.step_gain) a.step_gain[step] = fx_to_double(((__int128)sGhi[t - lo] << 64) | (__int128)sGlo[t - lo], S);
+      if (a.step_gain) a.step_gain[step] = fx_to_double(sG[t - lo], S);
     }
 
     // 2. The winner's row against b, the wave's chunks loaded together; each
@@ -204,7 +202,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
 #pragma unroll
     for (int i = 0; i < kLoadsT; ++i)
       if (w + i * kWaves < nch) xr[i] = row[(w + i * kWaves) * (kChunkT / 4) + lane];
-    __int128 dobj = 0;
+    long long dobj = 0;
 #pragma unroll
     for (int i = 0; i < kLoadsT; ++i) {
       const int q0 = w + i * kWaves;
@@ -230,11 +228,11 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
         }
       }
     }
-    dobj = wave_sum_i128(dobj);
+    dobj = wave_sum_i64(dobj);
     if (lane == 0) sLw[w] += dobj;
     __syncthreads();
     if (tid == 0 && L.part) {
-      __int128 P = 0;
+      long long P = 0;
 #pragma unroll
       for (int q = 0; q < kWaves; ++q) P += sLw[q];
       L.part[size_t(step) * nb + blk] = P;
@@ -243,7 +241,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
     // 3-4. Fresh local gains and this block's candidate for the next step.
     if (step + 1 < a.k) {
       local_gains();
-      publish_argmax(sGlo, sGhi, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
+      publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
                      epoch_of(step + 1), sg, si);
     }
   }
@@ -253,10 +251,10 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
 }
 
 // L(S) after step l: the blocks' parts added in block order.
-__global__ void local_objective_kernel(const __int128* part, int nb, int k, const int* scale, double* out) {
+__global__ void local_objective_kernel(const long long* part, int nb, int k, const int* scale, double* out) {
   const int l = blockIdx.x * blockDim.x + threadIdx.x;
   if (l >= k) return;
-  __int128 s = 0;
+  long long s = 0;
   for (int b = 0; b < nb; ++b) s += part[size_t(l) * nb + b];
   out[l] = fx_to_double(s, *scale);
 }
@@ -268,7 +266,7 @@ struct LocalLayout {
 LocalLayout local_layout(int64_t n, int64_t k) {
   LocalLayout L;
   size_t o = layout(n, k).total;
-  L.part = o; o += a256(size_t(k) * kMaxBlocks * sizeof(__int128));
+  L.part = o; o += a256(size_t(k) * kMaxBlocks * sizeof(long long));
   L.scale = o; o += 256;
   L.T = o; o += a256(size_t(n) * local_ldt(n) * sizeof(float));
   L.total = o;
@@ -288,7 +286,7 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
   const int nb = blocks_for(p.n, cus);
   const int W = (p.n + nb - 1) / nb;
   const int ldt = local_ldt(p.n);
-  const size_t lds = size_t(W) * (16 + 4 + 1) + size_t(ldt) * 4 + size_t(W) * g * (4 + 4 + 2) + 16;
+  const size_t lds = size_t((W + 1) & ~1) * 8 + size_t(ldt) * 4 + size_t(W) * g * (4 + 4 + 2) + size_t(W) * (4 + 1) + 16;
   if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(sgs_local_kernel),
                                hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
     return e;
@@ -321,7 +319,7 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
   a.ldt = ldt;
   d.nbr = nbr;
   d.g = g;
-  d.part = p.step_objective ? reinterpret_cast<__int128*>(w + Y.part) : nullptr;
+  d.part = p.step_objective ? reinterpret_cast<long long*>(w + Y.part) : nullptr;
   d.scale = reinterpret_cast<int*>(w + Y.scale);
 
   sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);

@@ -41,30 +41,20 @@ constexpr unsigned long long kNoCandidate = 1ull;   // below every real candidat
 // its waits and returns, and selected[] is filled with -1.
 constexpr unsigned int kSpinLimit = 1u << 22;
 
-// Fixed-point value of a nonnegative term: floor(t 2^S) in 128 bits, read
-// off the bits of the double t 2^S (exact: a power-of-two scaling); t 2^S <
-// 2^102.  Negative, zero and subnormal-range values give 0.  With value
-// m 2^sh (m the 53-bit significand), the low word is m << sh or m >> -sh and
-// the high word m >> (64 - sh) for sh > 0; all three shifts are formed and
-// the right ones kept with masks, so the terms of a batch carry no branches
-// and interleave.
-__device__ __forceinline__ __int128 fx(double t, int S) {
-  const unsigned long long b = (unsigned long long)__double_as_longlong(__builtin_ldexp(t, S));
-  const int E = int(b >> 52) & 0x7ff;
-  const unsigned long long m = (b & ((1ull << 52) - 1ull)) | (1ull << 52);
-  const int sh = E - 1075;                                    // value = m 2^sh, sh <= 49
-  const unsigned long long up = m << (sh & 63), down = m >> ((-sh) & 63), carry = m >> ((64 - sh) & 63);
-  const unsigned long long pos = 0ull - (unsigned long long)(sh > 0);
-  const unsigned long long ok = 0ull - (unsigned long long)((b >> 63) == 0 && E >= 1023);   // not negative, at least 1
-  const unsigned long long lo = ((up & pos) | (down & ~pos)) & ok;
-  const unsigned long long hi = carry & pos & ok;
-  return ((__int128)hi << 64) | (__int128)lo;
+// Fixed-point value of a nonnegative term: floor(t 2^S) as a 64-bit
+// integer, for t 2^S < 2^62 (the scale S is chosen so that every gain and
+// the objective stay below 2^62).  t 2^S is exact (a power-of-two scaling);
+// its high and low 32-bit halves are taken by truncating float64 -> uint32
+// conversions, the low half from the exact remainder t 2^S - high 2^32.
+// Negative values and NaN give 0.  Float64 arithmetic only, no branches.
+__device__ __forceinline__ long long fx(double t, int S) {
+  const double y = fmax(__builtin_ldexp(t, S), 0.0);
+  const unsigned h = (unsigned)(y * 0x1p-32);
+  const unsigned l = (unsigned)__builtin_fma(-double(h), 0x1p32, y);
+  return (long long)(((unsigned long long)h << 32) | l);
 }
 
-__device__ __forceinline__ double fx_to_double(__int128 g, int S) {
-  const double x = (double)(long long)(g >> 64) * 0x1p64 + (double)(unsigned long long)g;
-  return __builtin_ldexp(x, -S);
-}
+__device__ __forceinline__ double fx_to_double(long long g, int S) { return __builtin_ldexp(double(g), -S); }
 
 struct IncDev {
   const float* C;
@@ -82,7 +72,7 @@ struct IncDev {
   int W;                      // rows and columns per block
   float* T;                   // rows form only: [n][ldt] source-major copy, T[s][t] = C(s, t)
   int ldt;                    // its row stride, n rounded up to a whole 256-row chunk
-  const __int128* part;       // incremental form: [P][n] step-0 gains summed over P row ranges
+  const long long* part;      // incremental form: [P][n] step-0 gains summed over P row ranges
   int P;
   const int* scale;           // incremental form: the fixed-point exponent S
 };
@@ -163,15 +153,7 @@ __device__ __forceinline__ unsigned long long lane_u64(unsigned long long x, int
   return ((unsigned long long)__builtin_amdgcn_readlane(unsigned(x >> 32), r) << 32) |
          unsigned(__builtin_amdgcn_readlane(unsigned(x), r));
 }
-template <int CTRL>
-__device__ __forceinline__ __int128 dpp_i128(__int128 x) {
-  return ((__int128)(long long)dpp_u64<CTRL>((unsigned long long)(x >> 64)) << 64) |
-         (__int128)dpp_u64<CTRL>((unsigned long long)x);
-}
-__device__ __forceinline__ __int128 lane_i128(__int128 x, int r) {
-  return ((__int128)(long long)lane_u64((unsigned long long)(x >> 64), r) << 64) |
-         (__int128)lane_u64((unsigned long long)x, r);
-}
+
 
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long x) {
   unsigned long long y;
@@ -203,12 +185,28 @@ __device__ __forceinline__ long long wave_max_i64(long long x) {
   return m;
 }
 
-__device__ __forceinline__ __int128 wave_sum_i128(__int128 x) {
-  x += dpp_i128<kDppSteps[0]>(x);
-  x += dpp_i128<kDppSteps[1]>(x);
-  x += dpp_i128<kDppSteps[2]>(x);
-  x += dpp_i128<kDppSteps[3]>(x);
-  return lane_i128(x, 0) + lane_i128(x, 16) + lane_i128(x, 32) + lane_i128(x, 48);
+__device__ __forceinline__ long long wave_sum_i64(long long x) {
+  x += (long long)dpp_u64<kDppSteps[0]>((unsigned long long)x);
+  x += (long long)dpp_u64<kDppSteps[1]>((unsigned long long)x);
+  x += (long long)dpp_u64<kDppSteps[2]>((unsigned long long)x);
+  x += (long long)dpp_u64<kDppSteps[3]>((unsigned long long)x);
+  return (long long)(lane_u64((unsigned long long)x, 0) + lane_u64((unsigned long long)x, 16) +
+                     lane_u64((unsigned long long)x, 32) + lane_u64((unsigned long long)x, 48));
+}
+
+__device__ __forceinline__ int wave_min_i32(int x) {
+  int y;
+  y = __builtin_amdgcn_mov_dpp(x, kDppSteps[0], 0xf, 0xf, false); x = y < x ? y : x;
+  y = __builtin_amdgcn_mov_dpp(x, kDppSteps[1], 0xf, 0xf, false); x = y < x ? y : x;
+  y = __builtin_amdgcn_mov_dpp(x, kDppSteps[2], 0xf, 0xf, false); x = y < x ? y : x;
+  y = __builtin_amdgcn_mov_dpp(x, kDppSteps[3], 0xf, 0xf, false); x = y < x ? y : x;
+  int m = __builtin_amdgcn_readlane(x, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    y = __builtin_amdgcn_readlane(x, r);
+    m = y < m ? y : m;
+  }
+  return m;
 }
 
 // Inclusive prefix sum over the lanes of a wave (every lane active).
@@ -222,14 +220,14 @@ __device__ __forceinline__ int wave_scan_incl(int x) {
   return x;
 }
 
-// Sum over the block of 128-bit integers, result in every thread.
-__device__ __int128 block_sum_i128(__int128 x, __int128* sg) {
-  x = wave_sum_i128(x);
+// Sum over the block of 64-bit integers, result in every thread.
+__device__ long long block_sum_i64(long long x, long long* sg) {
+  x = wave_sum_i64(x);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   __syncthreads();
   if (lane == 0) sg[w] = x;
   __syncthreads();
-  __int128 s = 0;
+  long long s = 0;
 #pragma unroll
   for (int q = 0; q < kWaves; ++q) s += sg[q];
   __syncthreads();
@@ -285,64 +283,13 @@ __device__ double block_sum_all(double x, double* sd) {
   return s;
 }
 
-// (g, gi) is better than (h, hi): larger gain, or equal gain and smaller index.
-__device__ __forceinline__ bool better(__int128 g, int gi, __int128 h, int hi) {
-  return g > h || (g == h && gi < hi);
-}
-
-// One step of the wave argmax: every lane takes the better of its own pair
-// and that of the lane the DPP pattern CTRL names.
-template <int CTRL>
-__device__ __forceinline__ void argmax_dpp(__int128& g, int& gi) {
-  const __int128 og = dpp_i128<CTRL>(g);
-  const int oi = __builtin_amdgcn_mov_dpp(gi, CTRL, 0xf, 0xf, false);
-  if (better(og, oi, g, gi)) {
-    g = og;
-    gi = oi;
-  }
-}
-
-// Argmax of (g, gi) over a whole wave, in every lane, in the DPP pattern of
-// the wave reductions above.  Pairs are totally ordered, so the order of the
-// comparisons does not matter.
-__device__ __forceinline__ void wave_argmax_exact(__int128& g, int& gi) {
-  argmax_dpp<kDppSteps[0]>(g, gi);
-  argmax_dpp<kDppSteps[1]>(g, gi);
-  argmax_dpp<kDppSteps[2]>(g, gi);
-  argmax_dpp<kDppSteps[3]>(g, gi);
-  __int128 bg = lane_i128(g, 0);
-  int bi = __builtin_amdgcn_readlane(gi, 0);
-#pragma unroll
-  for (int r = 16; r < 64; r += 16) {
-    const __int128 rg = lane_i128(g, r);
-    const int ri = __builtin_amdgcn_readlane(gi, r);
-    if (better(rg, ri, bg, bi)) {
-      bg = rg;
-      bi = ri;
-    }
-  }
-  g = bg;
-  gi = bi;
-}
-
-// The same argmax (g = -1 marks no candidate; gains are below 2^102): the
-// largest top 64 bits of the gains first; a single lane holding them holds
-// the largest gain, and only a tie in those bits takes the full comparison.
-__device__ __forceinline__ void wave_argmax(__int128& g, int& gi) {
-  const long long key = (long long)(g >> 38);
-  const long long top = wave_max_i64(key);
-  const unsigned long long c = __ballot(key == top);
-  if (__popcll(c) == 1) {
-    const int l = __ffsll((long long)c) - 1;
-    g = lane_i128(g, l);
-    gi = __builtin_amdgcn_readlane(gi, l);
-    return;
-  }
-  if (key != top) {
-    g = -1;
-    gi = INT_MAX;
-  }
-  wave_argmax_exact(g, gi);
+// Argmax of (g, gi) over a whole wave (every lane active), in every lane:
+// the largest gain, then the smallest index among the lanes that hold it.
+// g = -1 marks no candidate (gi = INT_MAX).
+__device__ __forceinline__ void wave_argmax(long long& g, int& gi) {
+  const long long top = wave_max_i64(g);
+  gi = wave_min_i32(g == top ? gi : INT_MAX);
+  g = top;
 }
 
 // Exact argmax (ties to the smaller index) of the block's unchosen columns,
@@ -351,32 +298,28 @@ __device__ __forceinline__ void wave_argmax(__int128& g, int& gi) {
 // does it alone, one column per lane, and no barrier follows: the callers'
 // next step begins with one (read_winner), and the gains and chosen flags it
 // reads were last written by wave 0 itself.
-__device__ __forceinline__ void publish_argmax(const unsigned long long* sGlo, const long long* sGhi,
-                                               const unsigned char* ssel, int lo, int cnt, int S,
-                                               unsigned long long* slot, unsigned long long epoch, __int128* sg,
-                                               int* si) {
+__device__ __forceinline__ void publish_argmax(const long long* sG, const unsigned char* ssel, int lo, int cnt,
+                                               int S, unsigned long long* slot, unsigned long long epoch,
+                                               long long* sg, int* si) {
   if (cnt <= 64) {
     if (threadIdx.x >= 64) return;
     const int i = threadIdx.x;
-    __int128 g = -1;
+    long long g = -1;
     int gi = INT_MAX;
     if (i < cnt && !ssel[i]) {
-      g = ((__int128)sGhi[i] << 64) | (__int128)sGlo[i];
+      g = sG[i];
       gi = lo + i;
     }
     wave_argmax(g, gi);
     if (i == 0) put(slot, (gi != INT_MAX ? pack_key(fx_to_double(g, S), gi) : kNoCandidate) | epoch);
     return;
   }
-  __int128 g = -1;
+  long long g = -1;
   int gi = INT_MAX;
   for (int i = threadIdx.x; i < cnt; i += kBlock)
-    if (!ssel[i]) {
-      const __int128 x = ((__int128)sGhi[i] << 64) | (__int128)sGlo[i];
-      if (x > g || (x == g && lo + i < gi)) {
-        g = x;
-        gi = lo + i;
-      }
+    if (!ssel[i] && sG[i] > g) {   // increasing i: ties keep the smaller index
+      g = sG[i];
+      gi = lo + i;
     }
   wave_argmax(g, gi);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;

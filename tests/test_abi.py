@@ -142,7 +142,7 @@ def test_local_workspace_query(lib):
     assert lib.coverprune_sgs_local_workspace(0, 8) == 0
     # exchange slots, one objective part per block and step, the transposed cost
     ws = lib.coverprune_sgs_local_workspace(16384, 1638)
-    assert 16384 * 16384 * 4 + 1638 * 256 * 16 <= ws < 16384 * 16384 * 4 + 1638 * 256 * 16 + (1 << 22)
+    assert 16384 * 16384 * 4 + 1638 * 256 * 8 <= ws < 16384 * 16384 * 4 + 1638 * 256 * 8 + (1 << 22)
     assert lib.coverprune_sgs_local_workspace(1000, 10) >= 1000 * 1024 * 4
 
 
