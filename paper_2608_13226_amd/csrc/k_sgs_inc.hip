@@ -613,13 +613,18 @@ __global__ __launch_bounds__(kBlock) void inc_scale_kernel(IncDev a, int* scale)
 // row range) blocks so that the pass runs with many more waves in flight than
 // the greedy's one block per compute unit: block (b, p) sums rows
 // [p R, (p + 1) R) of columns [b W, (b + 1) W) into part[p][column], 64-bit
-// fixed point, four waves adding in wave order.  With WT it also writes those
-// rows of T: lane `col` holds C_tm[j0 .. j0 + 16)[col], which is T[col][j0 ..
-// j0 + 16), half a 128-byte line whose other half the next wave writes in the
-// same round (R is a multiple of 16, so no line is shared between blocks).
+// fixed point, four waves adding in wave order.  A round covers 64 rows, 16
+// per wave.  With WT the round's 64 x 64 tile also goes to T through LDS:
+// lane `col` of a wave holds C_tm[j0 .. j0 + 16)[col], i.e. a piece of row
+// `col` of T; after a barrier each store instruction writes four rows of T,
+// 256 contiguous bytes each (16 lanes of 16 bytes), so every line written is
+// whole.  R is a multiple of 16 and rows of T are only written below the
+// range's end (n, padding aside, for the last range).
 constexpr int kPassThreads = 256;
 constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kPassRows = 16;
+constexpr int kPassTile = kPassWaves * kPassRows;   // rows per round
+constexpr int kPassLd = kPassTile + 4;               // LDS row of the tile: 16-byte aligned, banks spread
 
 __host__ __device__ __forceinline__ int pass_rows(int n, int P) {
   return ((n + P - 1) / P + kPassRows - 1) / kPassRows * kPassRows;
@@ -627,17 +632,17 @@ __host__ __device__ __forceinline__ int pass_rows(int n, int P) {
 
 template <bool WT>
 __global__ __launch_bounds__(kPassThreads) void inc_first_pass_kernel(IncDev a, long long* part) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lo = blockIdx.x * a.W, cnt = max(0, min(a.n, lo + a.W) - lo);
   const int R = pass_rows(a.n, a.P), r0 = blockIdx.y * R, r1 = min(a.n, r0 + R);
   const int S = *a.scale;
   __shared__ long long red[kPassThreads];
+  __shared__ __attribute__((aligned(16))) float tile[WT ? 64 : 1][WT ? kPassLd : 1];   // [column][row of the round]
   for (int cc = 0; cc < cnt; cc += 64) {
     const bool colok = cc + lane < cnt;
     const int col = lo + cc + lane;
-    f32x4* trow = WT ? reinterpret_cast<f32x4*>(a.T + size_t(colok ? col : 0) * a.ldt) : nullptr;
-    // The next chunk's loads are issued before the current chunk's terms are
-    // formed; two accumulators.
+    // The next round's loads are issued before the current round's terms
+    // are formed; two accumulators.
     long long g0 = 0, g1 = 0;
     float xn[kPassRows], vn[kPassRows];
     auto load = [&](int j0) {
@@ -648,34 +653,46 @@ __global__ __launch_bounds__(kPassThreads) void inc_first_pass_kernel(IncDev a, 
         vn[u] = j < r1 ? a.v[j] : 0.f;
       }
     };
-    if (r0 + w * kPassRows < r1) load(r0 + w * kPassRows);
-    for (int j0 = r0 + w * kPassRows; j0 < r1; j0 += kPassWaves * kPassRows) {
+    load(r0 + w * kPassRows);
+    for (int jr = r0; jr < r1; jr += kPassTile) {   // uniform over the block
+      const int j0 = jr + w * kPassRows;
       float x[kPassRows], vj[kPassRows];
 #pragma unroll
       for (int u = 0; u < kPassRows; ++u) {
         x[u] = xn[u];
         vj[u] = vn[u];
       }
-      if (j0 + kPassWaves * kPassRows < r1) load(j0 + kPassWaves * kPassRows);
+      if (jr + kPassTile < r1) load(j0 + kPassTile);   // rows past r1 load as zero terms
 #pragma unroll
       for (int u = 0; u < kPassRows; u += 2) {
         g0 += fx(double(vj[u]) * double(fmaxf(a.c0 - x[u], 0.f)), S);
         g1 += fx(double(vj[u + 1]) * double(fmaxf(a.c0 - x[u + 1], 0.f)), S);
       }
-      // Ordinary (write-back) stores: the two halves of a line meet in L2.
-      if (WT && colok) {
+      if (WT) {
 #pragma unroll
         for (int q = 0; q < kPassRows / 4; ++q)
-          trow[j0 / 4 + q] = f32x4{x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
+          *reinterpret_cast<f32x4*>(&tile[lane][w * kPassRows + 4 * q]) =
+              f32x4{x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
+        __syncthreads();
+        // Instruction q: columns 16 q .. 16 q + 15, lane piece (tid % 16) of
+        // four rows; a piece starting below r1 lies below ldt.
+#pragma unroll
+        for (int q = 0; q < 64 / (kPassThreads / 16); ++q) {
+          const int c = q * (kPassThreads / 16) + tid / 16, r = (tid % 16) * 4;
+          if (cc + c < cnt && jr + r < r1)
+            *reinterpret_cast<f32x4*>(a.T + size_t(lo + cc + c) * a.ldt + jr + r) =
+                *reinterpret_cast<const f32x4*>(&tile[c][r]);
+        }
+        __syncthreads();
       }
     }
-    red[threadIdx.x] = g0 + g1;
+    red[tid] = g0 + g1;
     __syncthreads();
-    if (threadIdx.x < 64 && cc + threadIdx.x < cnt) {
+    if (tid < 64 && cc + tid < cnt) {
       long long s = 0;
 #pragma unroll
-      for (int q = 0; q < kPassWaves; ++q) s += red[q * 64 + threadIdx.x];
-      part[size_t(blockIdx.y) * a.n + lo + cc + threadIdx.x] = s;
+      for (int q = 0; q < kPassWaves; ++q) s += red[q * 64 + tid];
+      part[size_t(blockIdx.y) * a.n + lo + cc + tid] = s;
     }
     __syncthreads();
   }
@@ -726,7 +743,7 @@ const void* rows_batch_kernel(int64_t n, int W) {
 
 // Exchange slots and lists, the first pass's partial gains and scale, then
 // (when the rows form may run) T.
-constexpr int kPassParts = 4;   // row ranges of the first pass
+constexpr int kPassParts = 3;   // row ranges of the first pass (three blocks per compute unit fit at once)
 struct IncLayout {
   size_t part, scale, T, total;
 };
