@@ -318,6 +318,94 @@ __device__ __forceinline__ int fixed_scale(const IncDev& a, double* sd) {
   return S;
 }
 
+// Predicting the next winner (rows schedule, at most 64 columns a block).
+// Each block publishes two words in its slot: its best key (word 0) and its
+// second-best key (word 1), each with the exchange's epoch bit.  After a
+// step's exchange every block knows, for the runner-up r (the best candidate
+// outside the winner's block), a lower bound on its fixed-point gain (from
+// its key), and an upper bound U on every other candidate's truncated gain:
+// the best keys of all blocks but the winner's and r's, and the second-best
+// keys of those two (a block's other columns gain at most its second best,
+// and gains only fall).  While applying the step's hits every block also sums
+// r's changes from the same terms, so every block holds the same lower bound
+// on r's gain after the step; if its truncated gain is strictly above U, r is
+// the next winner (whatever the indices), every block knows it, and the next
+// step runs without an exchange, on r's row of T loaded during this step.
+__device__ __forceinline__ void publish_rows(const long long* sG, const unsigned char* ssel, int lo, int cnt, int S,
+                                             unsigned long long* slot, unsigned long long epoch) {
+  if (threadIdx.x >= 64) return;
+  const int i = threadIdx.x;
+  const bool ok = i < cnt && !ssel[i];
+  long long g1 = ok ? sG[i] : -1;
+  int i1 = ok ? lo + i : INT_MAX;
+  const long long mine = g1;
+  const int mi = i1;
+  wave_argmax(g1, i1);
+  long long g2 = mi == i1 ? -1 : mine;
+  int i2 = mi == i1 ? INT_MAX : mi;
+  wave_argmax(g2, i2);
+  if (i == 0) {
+    put(slot + 1, (i2 != INT_MAX ? pack_key(fx_to_double(g2, S), i2) : kNoCandidate) | epoch);
+    put(slot, (i1 != INT_MAX ? pack_key(fx_to_double(g1, S), i1) : kNoCandidate) | epoch);
+  }
+}
+
+// A lower bound on the fixed-point gain g behind a key: the key keeps the
+// top bits of the float64 value of g 2^-S (rounded to nearest from 64 bits,
+// then truncated), so scaling it back can exceed g by at most half a unit in
+// the 53rd bit, which the bound takes off.
+__device__ __forceinline__ long long key_gain_floor(unsigned long long key, int S) {
+  const double d = __longlong_as_double((long long)((key >> kIndexBits) << (kIndexBits + 1)));
+  const long long G = (long long)__builtin_ldexp(d, S);
+  return max(0ll, G - (G >> 52) - 1);
+}
+
+// read_winner for two-word slots: thread i < nb polls both words of block
+// i's slot and stores them (epoch bits cleared) in sk1 and sk2.  Returns the
+// winner's index, -1 when the launch is aborting.
+__device__ int read_winner_rows(const unsigned long long* slots, unsigned long long epoch, int nb, unsigned int* abort,
+                                unsigned long long* su, int* sflag, unsigned long long* sk1, unsigned long long* sk2) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  unsigned long long best = 0ull;
+  if (tid == 0) *sflag = 0;
+  __syncthreads();
+  if (tid < nb) {
+    const unsigned long long* p = slots + size_t(tid) * kSlotStride;
+    bool done = false;
+    for (unsigned int spins = 0; !done; ++spins) {
+      const unsigned long long x0 = get(p), x1 = get(p + 1);
+      if ((x0 & kEpoch) == epoch && (x1 & kEpoch) == epoch) {
+        best = x0 & ~kEpoch;
+        sk1[tid] = best;
+        sk2[tid] = x1 & ~kEpoch;
+        done = true;
+      } else {
+        if ((spins & 63u) == 63u) {
+          if (get(abort)) {
+            *sflag = 1;
+            break;
+          }
+          if (spins > kSpinLimit) {
+            put(abort, 1u);
+            *sflag = 1;
+            break;
+          }
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+  }
+  best = wave_max_u64(best);
+  if (lane == 0) su[w] = best;
+  __syncthreads();
+  unsigned long long m = su[0];
+#pragma unroll
+  for (int q = 1; q < kWaves; ++q) m = su[q] > m ? su[q] : m;
+  const bool aborting = *sflag != 0;
+  __syncthreads();
+  return aborting ? -1 : int(kIndexMask - (m & kIndexMask));
+}
+
 // NG 64-column groups per block (W <= 64 NG); RL chunk loads per wave and
 // step (n <= kRowChunk kWaves RL).
 template <int NG, int RL>
@@ -340,6 +428,12 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   __shared__ int scnt[2];                     // hits listed in steps of each parity
   __shared__ int schunk[kRowsMaxN / kRowChunk];   // dense steps: hits per chunk, then their offsets
   if (tid == 0) scnt[0] = scnt[1] = 0;
+  // Prediction of the next winner (one column group only): every block's
+  // two slot words of the last exchange and the waves' parts of the
+  // runner-up's change in the step.
+  constexpr bool kSpec = NG == 1;
+  __shared__ unsigned long long sk1[kSpec ? kMaxBlocks : 1], sk2[kSpec ? kMaxBlocks : 1];
+  __shared__ long long sdr[kWaves];
 
   for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
   for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
@@ -364,11 +458,27 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
   }
 
-  publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
+  // Slot sets and epochs count exchanges, which predicted steps skip.
+  int xc = 0;
+  if (kSpec)
+    publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0));
+  else
+    publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
 
   const int nch = a.ldt / kRowChunk;
+  bool predicted = false;     // this step's winner was predicted (no exchange)
+  int tpred = -1;
+  f32x4 xr2[RL];              // the predicted winner's row, loaded during the previous step
   for (int step = 0; step < a.k; ++step) {
-    const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
+    int tw;
+    if (predicted) {
+      __syncthreads();
+      tw = tpred;
+    } else {
+      tw = kSpec ? read_winner_rows(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, su, &sflag, sk1, sk2)
+                 : read_winner(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, su, &sflag);
+      ++xc;
+    }
     if (tw < 0) break;
     if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
       long long L = 0;
@@ -383,17 +493,46 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       if (a.step_gain) a.step_gain[step] = fx_to_double(sG[t - lo], S);
     }
 
-    // The wave's chunks of the winner's row, all loads in flight together.
+    // The wave's chunks of the winner's row, all loads in flight together
+    // (already loaded when the winner was predicted).
     const f32x4* row = reinterpret_cast<const f32x4*>(a.T + size_t(t) * a.ldt);
     f32x4 xr[RL];
 #pragma unroll
     for (int i = 0; i < RL; ++i)
-      if (w + i * kWaves < nch) xr[i] = row[(w + i * kWaves) * (kRowChunk / 4) + lane];
+      if (w + i * kWaves < nch) xr[i] = predicted ? xr2[i] : row[(w + i * kWaves) * (kRowChunk / 4) + lane];
+
+    // After an exchange every wave finds the runner-up r, the lower bound on
+    // its gain and the bound on the others while the row is in flight.
+    // Blocks own W consecutive columns, so the winner's block is t / W.
+    int rr = -1;
+    long long spec_g = 0;
+    unsigned long long spec_u = 0ull;
+    if (kSpec && !predicted && step + 1 < a.k) {
+      const int bt = t / a.W;
+      unsigned long long k[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int b = lane + 64 * q;
+        k[q] = (b < nb && b != bt) ? sk1[b] : 0ull;
+      }
+      const unsigned long long kr = wave_max_u64(max(max(k[0], k[1]), max(k[2], k[3])));
+      if (kr > kNoCandidate) {
+        rr = int(kIndexMask - (kr & kIndexMask));
+        const int br = rr / a.W;
+        unsigned long long u = 0ull;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) u = max(u, (lane + 64 * q) == br ? 0ull : k[q]);
+        u = max(wave_max_u64(u), max(sk2[bt], sk2[br]));
+        spec_g = key_gain_floor(sk1[br], S);
+        spec_u = u >> kIndexBits;
+      }
+    }
 
     long long g[NG];
 #pragma unroll
     for (int q = 0; q < NG; ++q) g[q] = 0;
     long long dobj = 0;
+    long long dr = 0;           // this wave's part of the runner-up's change
     // Applies listed hits base .. base + m to the wave's partial gains (and,
     // in block 0, to the objective), and records them in assign and (with
     // setb) in b.
@@ -402,17 +541,18 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       // entries are broadcast with readlane.  The next batch's entries and
       // row reads are issued before the current batch's terms are summed.
       int jl = 0;
-      float bol = 0.f, bnl = 0.f, vl = 0.f;
+      float bol = 0.f, bnl = 0.f, vl = 0.f, rl = 0.f;
       float xc[kChunk][NG];
       auto fetch = [&](int e0) {
         const int nbt = min(kChunk, base + m - e0);
         jl = 0;
-        bol = bnl = vl = 0.f;
+        bol = bnl = vl = rl = 0.f;
         if (lane < nbt) {
           jl = lj[e0 + lane];
           bol = lbo[e0 + lane];
           bnl = lbn[e0 + lane];
           vl = a.v[jl];
+          if (rr >= 0) rl = a.C[size_t(jl) * a.n + rr];   // C(r, j): the runner-up's cost to the entry
         }
 #pragma unroll
         for (int u = 0; u < kChunk; ++u) {
@@ -426,7 +566,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       for (int e0 = base; e0 < base + m; e0 += kChunk) {
         const int nbt = min(kChunk, base + m - e0);
         const int cj = jl;
-        const float cbo = bol, cbn = bnl, cv = vl;
+        const float cbo = bol, cbn = bnl, cv = vl, cr = rl;
         float cx[kChunk][NG];
 #pragma unroll
         for (int u = 0; u < kChunk; ++u)
@@ -449,8 +589,11 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
             }
           }
         }
-        // The batch's targets, one lane each: objective (block 0), b and assign.
+        // The batch's targets, one lane each: objective (block 0), the
+        // runner-up's change, b and assign.
         if (lane < nbt) {
+          if (rr >= 0 && cr < cbo)
+            dr += fx(double(cv) * double(fmaxf(cbn - cr, 0.f)), S) - fx(double(cv) * double(cbo - cr), S);
           if (blk == 0) dobj += fx(double(cv) * double(cbn), S) - fx(double(cv) * double(cbo), S);
           if (setb) sball[cj] = cbn;
           if (a.assign && unsigned(cj - lo) < unsigned(cnt)) a.assign[cj] = t;
@@ -558,6 +701,16 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       }
     }
 
+    if (kSpec && rr >= 0) {
+      dr = wave_sum_i64(dr);
+      if (lane == 0) sdr[w] = dr;
+      // r's row, for the next step if r is confirmed: issued after the
+      // step's own loads so that none of their waits includes it.
+      const f32x4* rowr = reinterpret_cast<const f32x4*>(a.T + size_t(rr) * a.ldt);
+#pragma unroll
+      for (int i = 0; i < RL; ++i)
+        if (w + i * kWaves < nch) xr2[i] = rowr[(w + i * kWaves) * (kRowChunk / 4) + lane];
+    }
     // The waves' partial gains, added in wave order by wave 0.  With one
     // column group wave 0 then publishes the candidate on its own (the next
     // step begins with a barrier); with two the general publish reads every
@@ -581,9 +734,24 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       obj_step = step;
     }
 
-    if (step + 1 < a.k)
-      publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, (step + 1) & 1, blk),
-                     epoch_of(step + 1), sg, si);
+    // The lower bound on the runner-up's gain after the step, the same in
+    // every block: when its truncated gain beats the bound on all others, r
+    // is the next winner.
+    bool next = false;
+    if (kSpec && rr >= 0) {
+      long long gr = spec_g;
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) gr += sdr[q];
+      next = gr > 0 && (pack_key(fx_to_double(gr, S), rr) >> kIndexBits) > spec_u;
+    }
+    if (step + 1 < a.k && !next) {
+      if (kSpec)
+        publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, xc & 1, blk), epoch_of(xc));
+      else
+        publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, xc & 1, blk), epoch_of(xc), sg, si);
+    }
+    predicted = next;
+    tpred = rr;
   }
   __syncthreads();
   if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {

@@ -117,9 +117,9 @@ __device__ __forceinline__ unsigned long long pack_key(double g, int idx) {
   return (gb << kIndexBits) | (kIndexMask - (unsigned long long)idx);
 }
 
-// Epoch bit of the candidates for step l, kept in slot set l % 2: it flips
-// between consecutive uses of a set and is never the zero of a fresh
-// workspace for steps 0 and 1.
+// Epoch bit of the candidates of exchange l (the step, unless steps skip
+// their exchange), kept in slot set l % 2: it flips between consecutive uses
+// of a set and is never the zero of a fresh workspace for exchanges 0 and 1.
 __device__ __forceinline__ unsigned long long epoch_of(int step) {
   return ((step >> 1) & 1) ? 0ull : kEpoch;
 }
@@ -128,8 +128,12 @@ __global__ void sgs_inc_init_kernel(IncDev a) {
   const int gt = blockIdx.x * blockDim.x + threadIdx.x, nt = gridDim.x * blockDim.x;
   for (int s = gt; s < kMaxBlocks; s += nt) {
     a.lens[size_t(s) * kSlotStride] = 0ull;
-    a.cand[size_t(s) * kSlotStride] = 0ull;
-    a.cand[size_t(kMaxBlocks + s) * kSlotStride] = 0ull;
+    // Word 0 of a candidate slot holds the key; the rows schedule also
+    // writes word 1 (the second key).
+    for (int w = 0; w < 2; ++w) {
+      a.cand[size_t(s) * kSlotStride + w] = 0ull;
+      a.cand[size_t(kMaxBlocks + s) * kSlotStride + w] = 0ull;
+    }
   }
   for (int j = gt; j < a.n; j += nt)
     if (a.assign) a.assign[j] = -1;
