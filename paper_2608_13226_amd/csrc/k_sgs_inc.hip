@@ -331,6 +331,11 @@ __device__ __forceinline__ int fixed_scale(const IncDev& a, double* sd) {
 // on r's gain after the step; if its truncated gain is strictly above U, r is
 // the next winner (whatever the indices), every block knows it, and the next
 // step runs without an exchange, on r's row of T loaded during this step.
+// The same holds down a chain: with r_1, r_2, ... the best candidates of
+// distinct blocks in key order (the winner's block left out), r_m follows
+// r_(m-1) when its bound beats the best key of the remaining blocks, r_(m+1),
+// and the second-best keys of the winner's block and of r_1 .. r_m; every
+// block tracks the changes of all of r_1 .. r_kChain since the exchange.
 __device__ __forceinline__ void publish_rows(const long long* sG, const unsigned char* ssel, int lo, int cnt, int S,
                                              unsigned long long* slot, unsigned long long epoch) {
   if (threadIdx.x >= 64) return;
@@ -406,6 +411,9 @@ __device__ int read_winner_rows(const unsigned long long* slots, unsigned long l
   return aborting ? -1 : int(kIndexMask - (m & kIndexMask));
 }
 
+constexpr int kChain = 1;   // predicted steps in a row at most (deeper chains measured slower)
+constexpr int kTrackMax = 256;   // hits of a step that still tracks the chain
+
 // NG 64-column groups per block (W <= 64 NG); RL chunk loads per wave and
 // step (n <= kRowChunk kWaves RL).
 template <int NG, int RL>
@@ -428,12 +436,12 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   __shared__ int scnt[2];                     // hits listed in steps of each parity
   __shared__ int schunk[kRowsMaxN / kRowChunk];   // dense steps: hits per chunk, then their offsets
   if (tid == 0) scnt[0] = scnt[1] = 0;
-  // Prediction of the next winner (one column group only): every block's
-  // two slot words of the last exchange and the waves' parts of the
-  // runner-up's change in the step.
+  // Prediction of the next winners (one column group only): every block's
+  // two slot words of the last exchange and the waves' parts of the chain
+  // candidates' changes in the step.
   constexpr bool kSpec = NG == 1;
   __shared__ unsigned long long sk1[kSpec ? kMaxBlocks : 1], sk2[kSpec ? kMaxBlocks : 1];
-  __shared__ long long sdr[kWaves];
+  __shared__ long long sdr[kWaves][kChain];
 
   for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
   for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
@@ -469,6 +477,20 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   bool predicted = false;     // this step's winner was predicted (no exchange)
   int tpred = -1;
   f32x4 xr2[RL];              // the predicted winner's row, loaded during the previous step
+  // The chain since the last exchange, the same in every wave and block:
+  // candidates r_1 .. (-1 past the last), lower bounds on their gains (with
+  // their changes since the exchange), the bounds they must beat (truncated
+  // gain bits), and the position (steps predicted since the exchange).
+  int rc[kChain];
+  long long acc[kChain];
+  unsigned long long ub[kChain];
+  int chain = 0;
+#pragma unroll
+  for (int m = 0; m < kChain; ++m) {
+    rc[m] = -1;
+    acc[m] = 0;
+    ub[m] = 0ull;
+  }
   for (int step = 0; step < a.k; ++step) {
     int tw;
     if (predicted) {
@@ -501,13 +523,10 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     for (int i = 0; i < RL; ++i)
       if (w + i * kWaves < nch) xr[i] = predicted ? xr2[i] : row[(w + i * kWaves) * (kRowChunk / 4) + lane];
 
-    // After an exchange every wave finds the runner-up r, the lower bound on
-    // its gain and the bound on the others while the row is in flight.
-    // Blocks own W consecutive columns, so the winner's block is t / W.
-    int rr = -1;
-    long long spec_g = 0;
-    unsigned long long spec_u = 0ull;
-    if (kSpec && !predicted && step + 1 < a.k) {
+    // After an exchange every wave builds the chain while the row is in
+    // flight: the best keys of distinct blocks in order, each taken out in
+    // turn.  Blocks own W consecutive columns, so the winner's block is t / W.
+    if (kSpec && !predicted) {
       const int bt = t / a.W;
       unsigned long long k[4];
 #pragma unroll
@@ -515,24 +534,36 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
         const int b = lane + 64 * q;
         k[q] = (b < nb && b != bt) ? sk1[b] : 0ull;
       }
-      const unsigned long long kr = wave_max_u64(max(max(k[0], k[1]), max(k[2], k[3])));
-      if (kr > kNoCandidate) {
-        rr = int(kIndexMask - (kr & kIndexMask));
-        const int br = rr / a.W;
-        unsigned long long u = 0ull;
+      unsigned long long u2 = sk2[bt];
+      int bprev = -1;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) u = max(u, (lane + 64 * q) == br ? 0ull : k[q]);
-        u = max(wave_max_u64(u), max(sk2[bt], sk2[br]));
-        spec_g = key_gain_floor(sk1[br], S);
-        spec_u = u >> kIndexBits;
+      for (int m = 0; m <= kChain; ++m) {
+        const unsigned long long kr = wave_max_u64(max(max(k[0], k[1]), max(k[2], k[3])));
+        const bool real = kr > kNoCandidate && (m == 0 || bprev >= 0);
+        const int r = real ? int(kIndexMask - (kr & kIndexMask)) : -1;
+        const int br = real ? r / a.W : -1;
+        if (m > 0) ub[m - 1] = max(real ? kr : 0ull, u2) >> kIndexBits;
+        if (m < kChain) {
+          rc[m] = r;
+          acc[m] = real ? key_gain_floor(kr, S) : 0;
+          if (real) u2 = max(u2, sk2[br]);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) k[q] = (lane + 64 * q) == br ? 0ull : k[q];
+        }
+        bprev = br;
       }
+      chain = 0;
     }
 
     long long g[NG];
 #pragma unroll
     for (int q = 0; q < NG; ++q) g[q] = 0;
     long long dobj = 0;
-    long long dr = 0;           // this wave's part of the runner-up's change
+    long long dr[kChain];       // this wave's parts of the chain candidates' changes
+#pragma unroll
+    for (int m = 0; m < kChain; ++m) dr[m] = 0;
+    // Candidates still ahead in the chain: r_(chain+1) ..
+    auto live = [&](int m) { return kSpec && m >= chain && rc[m] >= 0; };
     // Applies listed hits base .. base + m to the wave's partial gains (and,
     // in block 0, to the objective), and records them in assign and (with
     // setb) in b.
@@ -541,18 +572,23 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       // entries are broadcast with readlane.  The next batch's entries and
       // row reads are issued before the current batch's terms are summed.
       int jl = 0;
-      float bol = 0.f, bnl = 0.f, vl = 0.f, rl = 0.f;
+      float bol = 0.f, bnl = 0.f, vl = 0.f;
+      float rl[kChain];
       float xc[kChunk][NG];
       auto fetch = [&](int e0) {
         const int nbt = min(kChunk, base + m - e0);
         jl = 0;
-        bol = bnl = vl = rl = 0.f;
+        bol = bnl = vl = 0.f;
+#pragma unroll
+        for (int c = 0; c < kChain; ++c) rl[c] = 0.f;
         if (lane < nbt) {
           jl = lj[e0 + lane];
           bol = lbo[e0 + lane];
           bnl = lbn[e0 + lane];
           vl = a.v[jl];
-          if (rr >= 0) rl = a.C[size_t(jl) * a.n + rr];   // C(r, j): the runner-up's cost to the entry
+#pragma unroll
+          for (int c = 0; c < kChain; ++c)
+            if (live(c)) rl[c] = a.C[size_t(jl) * a.n + rc[c]];   // C(r_c, j): a candidate's cost to the entry
         }
 #pragma unroll
         for (int u = 0; u < kChunk; ++u) {
@@ -566,7 +602,10 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       for (int e0 = base; e0 < base + m; e0 += kChunk) {
         const int nbt = min(kChunk, base + m - e0);
         const int cj = jl;
-        const float cbo = bol, cbn = bnl, cv = vl, cr = rl;
+        const float cbo = bol, cbn = bnl, cv = vl;
+        float cr[kChain];
+#pragma unroll
+        for (int c = 0; c < kChain; ++c) cr[c] = rl[c];
         float cx[kChunk][NG];
 #pragma unroll
         for (int u = 0; u < kChunk; ++u)
@@ -589,11 +628,13 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
             }
           }
         }
-        // The batch's targets, one lane each: objective (block 0), the
-        // runner-up's change, b and assign.
+        // The batch's targets, one lane each: objective (block 0), the chain
+        // candidates' changes, b and assign.
         if (lane < nbt) {
-          if (rr >= 0 && cr < cbo)
-            dr += fx(double(cv) * double(fmaxf(cbn - cr, 0.f)), S) - fx(double(cv) * double(cbo - cr), S);
+#pragma unroll
+          for (int c = 0; c < kChain; ++c)
+            if (live(c) && cr[c] < cbo)
+              dr[c] += fx(double(cv) * double(fmaxf(cbn - cr[c], 0.f)), S) - fx(double(cv) * double(cbo - cr[c]), S);
           if (blk == 0) dobj += fx(double(cv) * double(cbn), S) - fx(double(cv) * double(cbo), S);
           if (setb) sball[cj] = cbn;
           if (a.assign && unsigned(cj - lo) < unsigned(cnt)) a.assign[cj] = t;
@@ -637,6 +678,9 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     }
     __syncthreads();
     const int total = scnt[par];
+    // Early steps improve many targets; tracking the chain there costs more
+    // than it saves, so a step with many hits ends the chain.
+    if (total > kTrackMax) chain = kChain;
     if (tid == 0) scnt[par ^ 1] = 0;   // last read in the previous step, next used in the next
     if (total <= kCap) {
       const int per = (total + kWaves - 1) / kWaves;
@@ -701,12 +745,21 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       }
     }
 
-    if (kSpec && rr >= 0) {
-      dr = wave_sum_i64(dr);
-      if (lane == 0) sdr[w] = dr;
-      // r's row, for the next step if r is confirmed: issued after the
-      // step's own loads so that none of their waits includes it.
-      const f32x4* rowr = reinterpret_cast<const f32x4*>(a.T + size_t(rr) * a.ldt);
+    // The next candidate, r_(chain+1), and its row for the next step if it
+    // is confirmed: issued after the step's own loads so that none of their
+    // waits includes it.
+    int rn = -1;
+#pragma unroll
+    for (int c = 0; c < kChain; ++c)
+      if (c == chain) rn = rc[c];
+    if (kSpec && rn >= 0) {
+#pragma unroll
+      for (int c = 0; c < kChain; ++c)
+        if (live(c)) {
+          const long long d = wave_sum_i64(dr[c]);
+          if (lane == 0) sdr[w][c] = d;
+        }
+      const f32x4* rowr = reinterpret_cast<const f32x4*>(a.T + size_t(rn) * a.ldt);
 #pragma unroll
       for (int i = 0; i < RL; ++i)
         if (w + i * kWaves < nch) xr2[i] = rowr[(w + i * kWaves) * (kRowChunk / 4) + lane];
@@ -734,15 +787,25 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       obj_step = step;
     }
 
-    // The lower bound on the runner-up's gain after the step, the same in
-    // every block: when its truncated gain beats the bound on all others, r
-    // is the next winner.
+    // The lower bounds on the candidates' gains after the step, the same in
+    // every block: when the next candidate's truncated gain beats its bound
+    // on all others, it is the next winner.
     bool next = false;
-    if (kSpec && rr >= 0) {
-      long long gr = spec_g;
+    if (kSpec && rn >= 0) {
 #pragma unroll
-      for (int q = 0; q < kWaves; ++q) gr += sdr[q];
-      next = gr > 0 && (pack_key(fx_to_double(gr, S), rr) >> kIndexBits) > spec_u;
+      for (int c = 0; c < kChain; ++c)
+        if (live(c))
+#pragma unroll
+          for (int q = 0; q < kWaves; ++q) acc[c] += sdr[q][c];
+      long long gr = 0;
+      unsigned long long u = 0ull;
+#pragma unroll
+      for (int c = 0; c < kChain; ++c)
+        if (c == chain) {
+          gr = acc[c];
+          u = ub[c];
+        }
+      next = step + 1 < a.k && gr > 0 && (pack_key(fx_to_double(gr, S), rn) >> kIndexBits) > u;
     }
     if (step + 1 < a.k && !next) {
       if (kSpec)
@@ -751,7 +814,8 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
         publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, xc & 1, blk), epoch_of(xc), sg, si);
     }
     predicted = next;
-    tpred = rr;
+    tpred = rn;
+    chain += next ? 1 : 0;
   }
   __syncthreads();
   if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
