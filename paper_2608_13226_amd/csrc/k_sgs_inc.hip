@@ -209,8 +209,10 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
         const int m = min(per, total - e0);
         // Entry u is broadcast from lane u with readlane (u is uniform), in
         // chunks of kChunk whose row reads are in flight together.
-        const int hj = int(h0 & 0xffffffffull), hv = int(h0 >> 32);
+        const int hj = int(h0 & 0xffffffffull);
         const int hbo = int(h1 & 0xffffffffull), hbn = int(h1 >> 32);
+        // Each lane's entry capacity scaled once for fx_scaled.
+        const long long hvs = __double_as_longlong(fx_scale(double(__uint_as_float(unsigned(h0 >> 32))), S));
         for (int u0 = 0; u0 < m; u0 += kChunk) {
           float x[kChunk];
 #pragma unroll
@@ -229,8 +231,10 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
               const float bo = __int_as_float(__builtin_amdgcn_readlane(hbo, u0 + i));
               if (x[i] < bo) {
                 const float bn = __int_as_float(__builtin_amdgcn_readlane(hbn, u0 + i));
-                const double vj = double(__int_as_float(__builtin_amdgcn_readlane(hv, u0 + i)));
-                g += fx(vj * double(fmaxf(bn - x[i], 0.f)), S) - fx(vj * double(bo - x[i]), S);
+                const double vs = __longlong_as_double(
+                    (long long)(((unsigned long long)(unsigned)__builtin_amdgcn_readlane(int(hvs >> 32), u0 + i) << 32) |
+                                (unsigned)__builtin_amdgcn_readlane(int(hvs), u0 + i)));
+                g += (long long)(fx_scaled(vs, fmaxf(bn - x[i], 0.f)) - fx_scaled(vs, bo - x[i]));
               }
             }
           }
@@ -602,7 +606,11 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       for (int e0 = base; e0 < base + m; e0 += kChunk) {
         const int nbt = min(kChunk, base + m - e0);
         const int cj = jl;
-        const float cbo = bol, cbn = bnl, cv = vl;
+        const float cbo = bol, cbn = bnl;
+        // Each lane's entry capacity scaled once for fx_scaled (0 past the
+        // batch, where v was not read).
+        const double cvs = fx_scale(double(vl), S);
+        const long long cvb = __double_as_longlong(cvs);
         float cr[kChain];
 #pragma unroll
         for (int c = 0; c < kChain; ++c) cr[c] = rl[c];
@@ -617,14 +625,16 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
           if (u < nbt) {
             const float bo = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cbo), u));
             const float bn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cbn), u));
-            const double vv = double(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(cv), u)));
+            const double vs = __longlong_as_double(
+                (long long)(((unsigned long long)(unsigned)__builtin_amdgcn_readlane(int(cvb >> 32), u) << 32) |
+                            (unsigned)__builtin_amdgcn_readlane(int(cvb), u)));
 #pragma unroll
             for (int q = 0; q < NG; ++q) {
               // A column that cost at least the old best contributes 0
               // before and after.
               const float xx = cx[u][q];
               if (q * 64 + lane < cnt && xx < bo)
-                g[q] += fx(vv * double(fmaxf(bn - xx, 0.f)), S) - fx(vv * double(bo - xx), S);
+                g[q] += (long long)(fx_scaled(vs, fmaxf(bn - xx, 0.f)) - fx_scaled(vs, bo - xx));
             }
           }
         }
@@ -634,8 +644,8 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
 #pragma unroll
           for (int c = 0; c < kChain; ++c)
             if (live(c) && cr[c] < cbo)
-              dr[c] += fx(double(cv) * double(fmaxf(cbn - cr[c], 0.f)), S) - fx(double(cv) * double(cbo - cr[c]), S);
-          if (blk == 0) dobj += fx(double(cv) * double(cbn), S) - fx(double(cv) * double(cbo), S);
+              dr[c] += (long long)(fx_scaled(cvs, fmaxf(cbn - cr[c], 0.f)) - fx_scaled(cvs, cbo - cr[c]));
+          if (blk == 0) dobj += (long long)(fx_scaled(cvs, cbn) - fx_scaled(cvs, cbo));
           if (setb) sball[cj] = cbn;
           if (a.assign && unsigned(cj - lo) < unsigned(cnt)) a.assign[cj] = t;
         }

@@ -56,6 +56,19 @@ __device__ __forceinline__ long long fx(double t, int S) {
 
 __device__ __forceinline__ double fx_to_double(long long g, int S) { return __builtin_ldexp(double(g), -S); }
 
+// fx(v d, S) for many terms of one capacity v: vs = max(v 2^S, 0) is taken
+// once, and for float d >= 0 the product vs d is exact (two 24-bit
+// significands), so fx_scaled(vs, d) equals fx(v d, S) bit for bit with no
+// scaling or clamping per term.  Returned as the unsigned 64-bit pattern, so
+// that a difference of two terms is one 64-bit subtraction.
+__device__ __forceinline__ double fx_scale(double v, int S) { return fmax(__builtin_ldexp(v, S), 0.0); }
+__device__ __forceinline__ unsigned long long fx_scaled(double vs, float d) {
+  const double y = vs * double(d);
+  const unsigned h = (unsigned)(y * 0x1p-32);
+  const unsigned l = (unsigned)__builtin_fma(-double(h), 0x1p32, y);
+  return ((unsigned long long)h << 32) | l;
+}
+
 struct IncDev {
   const float* C;
   const float* v;
