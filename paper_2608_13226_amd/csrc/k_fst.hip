@@ -142,8 +142,19 @@ __global__ __launch_bounds__(256) void pos_pairmax_kernel(const float* pos, int 
 // ---------------------------------------------------------------------------
 constexpr int kEpiTile = 64;
 
+// log1p from the hardware base-2 logarithm with Goldberg's correction
+// (D. Goldberg, "What every computer scientist should know about
+// floating-point arithmetic", 1991, Thm. 4): with u = fl(1 + x), log1p(x) =
+// log(u) x / (u - 1) to within a few ulps, and x itself when u rounds to 1.
+// The library's log1pf made the epilogue bound by instruction issue.
+__device__ __forceinline__ float log1p_hw(float x) {
+  const float u = 1.f + x;
+  const float d = u - 1.f;
+  return d == 0.f ? x : __builtin_amdgcn_logf(u) * 0.69314718055994531f * (x * __builtin_amdgcn_rcpf(d));
+}
+
 __device__ __forceinline__ float phi_kappa(float z, float kappa, float inv_log1p_kappa) {
-  return kappa > 0.f ? log1pf(kappa * z) * inv_log1p_kappa : z;
+  return kappa > 0.f ? log1p_hw(kappa * z) * inv_log1p_kappa : z;
 }
 
 // Block = one upper tile pair (ti <= tj) of 64 x 64.  The upper tile holds
@@ -197,7 +208,7 @@ __global__ __launch_bounds__(256) void fst_epilogue_kernel(FstParams p, FstScrat
   // Both terms of an entry from its raw d_f; writes the mirror value to LDS.
   auto cost_at = [&](int r, int c, float df) {
     const float dx = rx[r] - cx[c], dy = ry[r] - cy[c], dz = rz[r] - cz[c];
-    const float dist = sqrtf(dx * dx + dy * dy + dz * dz);
+    const float dist = __builtin_amdgcn_sqrtf(dx * dx + dy * dy + dz * dz);   // v_sqrt_f32, 1 ulp
     const float base = wf * df + p.lambda_x * phi_kappa(dist * inv_mx, p.kappa, p.inv_log1p_kappa);
     if (mirror) tr[c][r] = base + wt * float(max(0, rf[r] - cf[c]));
     return base + wt * float(max(0, cf[c] - rf[r]));
@@ -205,7 +216,7 @@ __global__ __launch_bounds__(256) void fst_epilogue_kernel(FstParams p, FstScrat
   const bool full = (ti + 1) * kEpiTile <= n && (tj + 1) * kEpiTile <= n;
   if (VEC && full) {
     const int c4 = (t & 15) * 4;
-#pragma unroll 2
+#pragma unroll 4
     for (int r = t >> 4; r < kEpiTile; r += 16) {
       float4* at = reinterpret_cast<float4*>(p.cost + size_t(ti * kEpiTile + r) * n + tj * kEpiTile + c4);
       const float4 df = *at;

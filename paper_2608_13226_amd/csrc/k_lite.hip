@@ -11,17 +11,17 @@
 //              the mass before each position, t(p) = min(K-1, K * mass / W);
 //              a prefix-min scan of t(p) - p and the K - N + p floor give the
 //              group of every position (the walk of Eq. 17 in scan form)
-//     tiles    16-row tiles per group and their prefix (work units below)
-//   maxima   M_x, M_tau over same-group, 27-adjacent pairs (a wave per
-//            position, after the front)
-//   B(p)     sum_j v_j (lam_x phi(d_x / M_x) + lam_tau d_tau / M_tau), or
-//            v_j c0 for a non-adjacent pair: every term of the group cost that
-//            does not involve features (a wave per position, after the front)
+//     tiles    16-row tiles per group, their prefix, the group of every
+//              tile and the list of big groups' tiles (work units below)
 //   pairs    per 16-row tile of a group, the tile's rows against the whole
 //            group on the matrix cores (16 x 16 tiles over D), d_f,
-//            A(p) = sum_j v_j d_f over adjacent pairs, and the global M_f:
-//            one wave per tile for groups of at most two tiles, one block per
-//            tile (waves splitting the column tiles) for larger groups
+//            A(p) = sum_j v_j d_f over adjacent pairs, and the global M_f,
+//            M_x, M_tau over those pairs: one wave per tile for groups of at
+//            most two tiles, one block per tile (waves splitting the column
+//            tiles) for larger groups
+//   B(p)     sum_j v_j (lam_x phi(d_x / M_x) + lam_tau d_tau / M_tau), or
+//            v_j c0 for a non-adjacent pair: every term of the group cost that
+//            does not involve features (a wave per position, after the pairs)
 //   select   cost(p) = (lam_f / M_f) A(p) + B(p); per-group argmin (Eq. 18)
 //   total    fixed-order sum of the K prototype costs (Eq. 20 objective)
 #include <hip/hip_runtime.h>
@@ -66,6 +66,9 @@ struct LiteDev {
   int* gid;                     // [n] group of each sorted position
   int* gstart;                  // [k + 1]
   int* rt_start;                // [k + 1] first 16-row tile of each group
+  int* unit_group;              // [n / 16 + k] group of every 16-row tile
+  int* big_unit;                // [n / 16 + k] tiles of groups of more than kSplitTiles tiles, in order
+  unsigned long long* bsum2;    // [G]
   double* A;                    // [n]
   double* B;                    // [n]
   double* gcost;                // [k]
@@ -81,11 +84,15 @@ constexpr int kCtrlMf = 9;         // float bits of max d_f
 constexpr int kCtrlSorted = 10;    // which key/tok buffer holds the sorted order
 constexpr int kCtrlBarrier = 11;   // grid barrier counter
 constexpr int kCtrlTiles = 12;     // total number of 16-row tiles
+constexpr int kCtrlBig = 13;       // tiles of groups of more than kSplitTiles tiles
 
 struct Layout {
-  size_t key0, key1, tok0, tok1, vox_tok, vox_pos, hist, bsum, bmin, gid, gstart, rt_start, A, B, gcost,
-      ctrl, total;
+  size_t key0, key1, tok0, tok1, vox_tok, vox_pos, hist, bsum, bsum2, bmin, gid, gstart, rt_start, unit_group,
+      big_unit, A, B, gcost, ctrl, total;
 };
+
+// Groups of more than this many 16-row tiles are split over a block's waves.
+constexpr int kSplitTiles = 2;
 
 size_t a256(size_t x) { return (x + 255) / 256 * 256; }
 
@@ -100,10 +107,13 @@ Layout layout(int64_t n, int64_t k) {
   L.vox_pos = o;  o += a256(size_t(n) * 8);
   L.hist = o;     o += a256(size_t(kFrontBlocks) * kBins * 4);
   L.bsum = o;     o += a256(size_t(kFrontBlocks) * 8);
+  L.bsum2 = o;    o += a256(size_t(kFrontBlocks) * 8);
   L.bmin = o;     o += a256(size_t(kFrontBlocks) * 4);
   L.gid = o;      o += a256(size_t(n) * 4);
   L.gstart = o;   o += a256(size_t(k + 1) * 4);
   L.rt_start = o; o += a256(size_t(k + 1) * 4);
+  L.unit_group = o; o += a256(size_t(n / kTileRows + k) * 4);
+  L.big_unit = o; o += a256(size_t(n / kTileRows + k) * 4);
   L.A = o;        o += a256(size_t(n) * 8);
   L.B = o;        o += a256(size_t(n) * 8);
   L.gcost = o;    o += a256(size_t(k) * 8);
@@ -226,6 +236,7 @@ __global__ void lite_init_kernel(LiteDev a) {
     a.ctrl[kCtrlSorted] = 0u;
     a.ctrl[kCtrlBarrier] = 0u;
     a.ctrl[kCtrlTiles] = 0u;
+    a.ctrl[kCtrlBig] = 0u;
   }
 }
 
@@ -440,139 +451,68 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
   }
   grid_barrier(bar, ++round);
 
-  // ---- tiles per group (block sums)
+  // ---- tiles per group, and tiles of big groups (block sums)
   const int gtile = (K + G - 1) / G;
   const int q0 = min(K, blk * gtile), q1 = min(K, q0 + gtile);
   {
-    unsigned long long local = 0ull;
+    unsigned long long local = 0ull, lbig = 0ull;
     for (int q = q0 + t; q < q1; q += kThreads) {
       const int g = max(0, get(a.gstart + q + 1) - get(a.gstart + q));
-      local += (unsigned long long)((g + kTileRows - 1) / kTileRows);
+      const int nt = (g + kTileRows - 1) / kTileRows;
+      local += (unsigned long long)nt;
+      lbig += nt > kSplitTiles ? (unsigned long long)nt : 0ull;
     }
-    unsigned long long tot;
+    unsigned long long tot, tbig;
     block_excl_sum_u64(local, s_u64, tot);
-    if (t == 0) put(a.bsum + blk, tot);
+    block_excl_sum_u64(lbig, s_u64, tbig);
+    if (t == 0) {
+      put(a.bsum + blk, tot);
+      put(a.bsum2 + blk, tbig);
+    }
   }
   grid_barrier(bar, ++round);
 
-  // ---- tile prefix per group; B(p), the feature-free part of every group cost
+  // ---- tile prefix per group, the group of every tile and the list of big
+  // groups' tiles (work units of the pair kernels)
   {
-    unsigned long long run, tot;
+    unsigned long long run, tot, rbig, tbig;
     block_prefix_u64(a.bsum, G, blk, s_u64, run, tot);
-    if (blk == 0 && t == 0) put(a.ctrl + kCtrlTiles, unsigned(tot));
+    block_prefix_u64(a.bsum2, G, blk, s_u64, rbig, tbig);
+    if (blk == 0 && t == 0) {
+      put(a.ctrl + kCtrlTiles, unsigned(tot));
+      put(a.ctrl + kCtrlBig, unsigned(tbig));
+    }
     for (int c0 = q0; c0 < q1; c0 += kThreads) {
       const int q = c0 + t;
-      unsigned long long nt = 0ull;
+      int nt = 0;
       if (q < q1) {
         const int g = max(0, get(a.gstart + q + 1) - get(a.gstart + q));
-        nt = (unsigned long long)((g + kTileRows - 1) / kTileRows);
+        nt = (g + kTileRows - 1) / kTileRows;
       }
-      unsigned long long chunk;
-      const unsigned long long ex = block_excl_sum_u64(nt, s_u64, chunk);
-      if (q < q1) a.rt_start[q] = int(run + ex);
+      const int nb = nt > kSplitTiles ? nt : 0;
+      unsigned long long chunk, cbig;
+      const unsigned long long ex = block_excl_sum_u64((unsigned long long)nt, s_u64, chunk);
+      const unsigned long long exb = block_excl_sum_u64((unsigned long long)nb, s_u64, cbig);
+      if (q < q1) {
+        const int u0 = int(run + ex), b0 = int(rbig + exb);
+        a.rt_start[q] = u0;
+        for (int x = 0; x < nt; ++x) a.unit_group[u0 + x] = q;
+        for (int x = 0; x < nb; ++x) a.big_unit[b0 + x] = u0 + x;
+      }
       if (q == K - 1) a.rt_start[K] = int(run + ex + nt);
       run += chunk;
+      rbig += cbig;
     }
   }
   if (blk == 0 && t == 0) a.ctrl[kCtrlSorted] = unsigned(sorted);
 }
 
-// Block-wide maximum of a nonnegative float, raised into *bits with one
-// atomic (same-address atomics from many blocks serialize).
-__device__ __forceinline__ void block_max_to(unsigned int* bits, float x) {
-  __shared__ float sm[kWaves];
-  x = wave_max(x);
-  if ((threadIdx.x & 63) == 0) sm[threadIdx.x >> 6] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int q = 1; q < kWaves; ++q) x = fmaxf(x, sm[q]);
-    atomic_max_nonneg(bits, x);
-  }
-}
-
 // ---------------------------------------------------------------------------
-// M_x and M_tau over the evaluated pairs (same group, adjacent voxels): waves
-// stride over the sorted positions, lanes over each group's members; one
-// atomic maximum per block (few blocks: same-address atomics serialize).
-__global__ __launch_bounds__(kThreads) void lite_maxima_kernel(LiteDev a) {
-  __shared__ double smx[kWaves];
-  __shared__ int smt[kWaves];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
-  double mx2 = 0.0;
-  int mt = 0;
-  for (int i = blockIdx.x * kWaves + w; i < a.n; i += gridDim.x * kWaves) {
-    const int q = min(max(a.gid[i], 0), a.k - 1);
-    const int tokn = perm[i];
-    const unsigned long long vi = a.vox_pos[i];
-    const double xi = a.pos[3 * tokn], yi = a.pos[3 * tokn + 1], zi = a.pos[3 * tokn + 2];
-    const int fi = a.frame[tokn];
-    const int j0 = clamp_range(a.gstart[q], a.n), j1 = clamp_range(a.gstart[q + 1], a.n);
-    for (int j = j0 + lane; j < j1; j += 64) {
-      if (!adjacent(vi, a.vox_pos[j])) continue;
-      const int tj = perm[j];
-      mx2 = fmax(mx2, sq_dist(xi, yi, zi, a.pos[3 * tj], a.pos[3 * tj + 1], a.pos[3 * tj + 2]));
-      mt = max(mt, abs(fi - a.frame[tj]));
-    }
-  }
-  mx2 = wave_max(mx2);
-  mt = wave_max(mt);
-  if (lane == 0) {
-    smx[w] = mx2;
-    smt[w] = mt;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int q = 1; q < kWaves; ++q) {
-      mx2 = fmax(mx2, smx[q]);
-      mt = max(mt, smt[q]);
-    }
-    atomic_max_nonneg(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2), mx2);
-    atomicMax(a.ctrl + kCtrlMt, unsigned(mt));
-  }
-}
-
-// ---------------------------------------------------------------------------
-// B(p) = sum over the group of v_j (lam_x phi(d_x / M_x) + lam_tau d_tau / M_tau)
-// for adjacent pairs and v_j c0 otherwise: one wave per sorted position, lanes
-// over the group's members, summed lane-strided and then across the wave in a
-// fixed order.
-__global__ __launch_bounds__(kThreads) void lite_b_kernel(LiteDev a) {
-  const int lane = threadIdx.x & 63;
-  const int i = blockIdx.x * kWaves + (threadIdx.x >> 6);
-  if (i >= a.n) return;
-  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
-  const double m_x = sqrt(__longlong_as_double(*reinterpret_cast<const long long*>(a.ctrl + kCtrlMx2)));
-  const int m_t = int(a.ctrl[kCtrlMt]);
-  const double c0 = double(a.lam_f) + double(a.lam_x) + double(a.lam_t);
-  const int q = min(max(a.gid[i], 0), a.k - 1);
-  const int tokn = perm[i];
-  const unsigned long long vi = a.vox_pos[i];
-  const double xi = a.pos[3 * tokn], yi = a.pos[3 * tokn + 1], zi = a.pos[3 * tokn + 2];
-  const int fi = a.frame[tokn];
-  double acc = 0.0;
-  const int j0 = clamp_range(a.gstart[q], a.n), j1 = clamp_range(a.gstart[q + 1], a.n);
-  for (int j = j0 + lane; j < j1; j += 64) {
-    const int tj = perm[j];
-    const double vj = double(a.v[tj]);
-    if (!adjacent(vi, a.vox_pos[j])) {
-      acc += vj * c0;
-      continue;
-    }
-    const double dist = sqrt(sq_dist(xi, yi, zi, a.pos[3 * tj], a.pos[3 * tj + 1], a.pos[3 * tj + 2]));
-    const double z = m_x > 0.0 ? dist / m_x : 0.0;
-    const double ph = a.kappa > 0.f ? log1p(double(a.kappa) * z) * a.inv_log1p_kappa : z;
-    const double dt = m_t > 0 ? double(max(0, fi - a.frame[tj])) / double(m_t) : 0.0;
-    acc += vj * (double(a.lam_x) * ph + double(a.lam_t) * dt);
-  }
-  acc = wave_sum(acc);
-  if (lane == 0) a.B[i] = acc;
-}
-
-// ---------------------------------------------------------------------------
-// Within-group feature pass.  Work unit: one 16-row tile ta of one group,
+// Within-group pair pass.  Work unit: one 16-row tile ta of one group,
 // multiplied on the matrix cores against every 16-row tile tb of the same
-// group over the full feature width.  Lane l supplies row l % 16 and feature
+// group over the full feature width.  The same pass raises M_x and M_tau:
+// it visits every evaluated pair (same group, adjacent voxels, diagonal
+// included), which is the set those maxima range over.  Lane l supplies row l % 16 and feature
 // slice 8 (l / 16) .. +8 of each 32-wide K step (bf16), or 4 (l / 16) .. +4 of
 // each 16-wide step spread over four MFMAs (f32); the output element
 // (4 (l / 16) + r, l % 16) lands in register r of lane l.  A group of at most
@@ -580,32 +520,33 @@ __global__ __launch_bounds__(kThreads) void lite_b_kernel(LiteDev a) {
 // takes one block per unit whose waves split the column tiles and add their
 // row sums in wave order (lite_pair_split_kernel), so a big group does not
 // leave one wave working through all its tiles alone.
-constexpr int kSplitTiles = 2;
-
 struct Unit {
   int p0, g, ntile, ta;
 };
 
-// Group and row tile of unit u: the last q with rt_start[q] <= u.
+// Group and row tile of unit u, from the front's table.
 __device__ __forceinline__ bool unit_of(const LiteDev& a, int u, Unit& t) {
-  int lo = 0, hi = a.k - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.rt_start[mid] <= u) lo = mid;
-    else hi = mid - 1;
-  }
-  t.p0 = clamp_range(a.gstart[lo], a.n);
-  t.g = max(0, clamp_range(a.gstart[lo + 1], a.n) - t.p0);
+  const int q = min(max(a.unit_group[u], 0), a.k - 1);
+  t.p0 = clamp_range(a.gstart[q], a.n);
+  t.g = max(0, clamp_range(a.gstart[q + 1], a.n) - t.p0);
   t.ntile = (t.g + kTileRows - 1) / kTileRows;
-  t.ta = u - a.rt_start[lo];
+  t.ta = u - a.rt_start[q];
   return t.ta >= 0 && t.ta < t.ntile;
 }
 
+// Running maxima of one lane over the pairs it evaluates: squared distance
+// (float64) and frame gap.
+struct PairMax {
+  float df = 0.f;
+  double x2 = 0.0;
+  int tau = 0;
+};
+
 // Row tile t.ta against column tile tb: adds v_j d_f over adjacent pairs to
-// arow (the lane's four output rows) and raises lmax.
+// arow (the lane's four output rows) and raises the maxima.
 template <bool BF16>
 __device__ __forceinline__ void pair_tile(const LiteDev& a, const int* perm, const Unit& t, int tb, double* arow,
-                                          float& lmax) {
+                                          PairMax& pm) {
   const int lane = threadIdx.x & 63;
   const int row = lane & 15, quad = lane >> 4;
   const int ra = t.ta * kTileRows + row;  // operand row of this lane in tile ta
@@ -669,12 +610,21 @@ __device__ __forceinline__ void pair_tile(const LiteDev& a, const int* perm, con
   nb += __shfl_xor(nb, 32);
   const int cb = tb * kTileRows + row;    // output column of this lane
   const bool cvalid = cb < t.g;
+  const int tokb = cvalid ? perm[t.p0 + cb] : 0;
   const unsigned long long vb = cvalid ? a.vox_pos[t.p0 + cb] : 0ull;
-  const double wv = cvalid ? double(a.v[perm[t.p0 + cb]]) : 0.0;
+  const double wv = cvalid ? double(a.v[tokb]) : 0.0;
+  const float xb = a.pos[3 * tokb], yb = a.pos[3 * tokb + 1], zb = a.pos[3 * tokb + 2];
+  const int fb = a.frame[tokb];
+  // Lane l (l < 16) also holds row l of tile ta's position and frame.
+  const int toka = ra < t.g ? perm[t.p0 + ra] : 0;
+  const float xa = a.pos[3 * toka], ya = a.pos[3 * toka + 1], za = a.pos[3 * toka + 2];
+  const int fa = a.frame[toka];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int oa = quad * 4 + r;           // output row within tile ta
     const float nra = __shfl(na, oa);
+    const float xo = __shfl(xa, oa), yo = __shfl(ya, oa), zo = __shfl(za, oa);
+    const int fo = __shfl(fa, oa);
     const int ca = t.ta * kTileRows + oa;
     if (cvalid && ca < t.g && adjacent(a.vox_pos[t.p0 + ca], vb)) {
       const float den = sqrtf(nra) * sqrtf(nb);
@@ -682,8 +632,41 @@ __device__ __forceinline__ void pair_tile(const LiteDev& a, const int* perm, con
       float df = fminf(fmaxf(1.f - cosv, 0.f), 2.f);
       if (ca == cb) df = 0.f;
       arow[r] = fma(wv, double(df), arow[r]);
-      lmax = fmaxf(lmax, df);
+      pm.df = fmaxf(pm.df, df);
+      pm.x2 = fmax(pm.x2, sq_dist(xo, yo, zo, xb, yb, zb));
+      pm.tau = max(pm.tau, abs(fo - fb));
     }
+  }
+}
+
+// Folds a block's maxima into the control words.  Atomics on one cache line
+// from many blocks serialize, so a block first reads the current value (the
+// maxima only grow) and issues an atomic only where it holds a larger one.
+template <int NW>
+__device__ __forceinline__ void pair_max_to(const LiteDev& a, PairMax pm) {
+  __shared__ float sf[NW];
+  __shared__ double sx[NW];
+  __shared__ int st[NW];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  pm.df = wave_max(pm.df);
+  pm.x2 = wave_max(pm.x2);
+  pm.tau = wave_max(pm.tau);
+  if (lane == 0) {
+    sf[w] = pm.df;
+    sx[w] = pm.x2;
+    st[w] = pm.tau;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < NW; ++q) {
+      pm.df = fmaxf(pm.df, sf[q]);
+      pm.x2 = fmax(pm.x2, sx[q]);
+      pm.tau = max(pm.tau, st[q]);
+    }
+    unsigned long long* mx2 = reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2);
+    if (pm.df > __uint_as_float(get(a.ctrl + kCtrlMf))) atomic_max_nonneg(a.ctrl + kCtrlMf, pm.df);
+    if (pm.x2 > __longlong_as_double((long long)get(mx2))) atomic_max_nonneg(mx2, pm.x2);
+    if (unsigned(pm.tau) > get(a.ctrl + kCtrlMt)) atomicMax(a.ctrl + kCtrlMt, unsigned(pm.tau));
   }
 }
 
@@ -701,19 +684,19 @@ __device__ __forceinline__ void row_sums(double* arow) {
 }
 
 template <bool BF16>
-__global__ __launch_bounds__(kThreads) void lite_pair_kernel(LiteDev a) {
+__global__ __launch_bounds__(kThreads, 4) void lite_pair_kernel(LiteDev a) {
   const int lane = threadIdx.x & 63;
   const int gw = blockIdx.x * kWaves + (threadIdx.x >> 6);
   const int nw = gridDim.x * kWaves;
   const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
   const int units = int(a.ctrl[kCtrlTiles]);
   const int row = lane & 15, quad = lane >> 4;
-  float lmax = 0.f;
+  PairMax pm;
   for (int u = gw; u < units; u += nw) {
     Unit t;
     if (!unit_of(a, u, t) || t.ntile > kSplitTiles) continue;
     double arow[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int tb = 0; tb < t.ntile; ++tb) pair_tile<BF16>(a, perm, t, tb, arow, lmax);
+    for (int tb = 0; tb < t.ntile; ++tb) pair_tile<BF16>(a, perm, t, tb, arow, pm);
     row_sums(arow);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -721,7 +704,7 @@ __global__ __launch_bounds__(kThreads) void lite_pair_kernel(LiteDev a) {
       if (row == 0 && ca < t.g) a.A[t.p0 + ca] = arow[r];
     }
   }
-  block_max_to(a.ctrl + kCtrlMf, lmax);
+  pair_max_to<kWaves>(a, pm);
 }
 
 constexpr int kSplitWaves = 16;
@@ -729,17 +712,16 @@ constexpr int kSplitWaves = 16;
 template <bool BF16>
 __global__ __launch_bounds__(kSplitWaves * 64) void lite_pair_split_kernel(LiteDev a) {
   __shared__ double spart[kSplitWaves][kTileRows];
-  __shared__ float sm[kSplitWaves];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
-  const int units = int(a.ctrl[kCtrlTiles]);
+  const int nbig = int(a.ctrl[kCtrlBig]);
   const int row = lane & 15, quad = lane >> 4;
-  float lmax = 0.f;
-  for (int u = blockIdx.x; u < units; u += gridDim.x) {
+  PairMax pm;
+  for (int b = blockIdx.x; b < nbig; b += gridDim.x) {
     Unit t;
-    if (!unit_of(a, u, t) || t.ntile <= kSplitTiles) continue;   // the same for the whole block
+    if (!unit_of(a, a.big_unit[b], t)) continue;   // the same for the whole block
     double arow[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int tb = w; tb < t.ntile; tb += kSplitWaves) pair_tile<BF16>(a, perm, t, tb, arow, lmax);
+    for (int tb = w; tb < t.ntile; tb += kSplitWaves) pair_tile<BF16>(a, perm, t, tb, arow, pm);
     row_sums(arow);
     if (row == 0) {
 #pragma unroll
@@ -757,12 +739,76 @@ __global__ __launch_bounds__(kSplitWaves * 64) void lite_pair_split_kernel(LiteD
     }
     __syncthreads();
   }
-  lmax = wave_max(lmax);
-  if (lane == 0) sm[w] = lmax;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int q = 1; q < kSplitWaves; ++q) lmax = fmaxf(lmax, sm[q]);
-    atomic_max_nonneg(a.ctrl + kCtrlMf, lmax);
+  pair_max_to<kSplitWaves>(a, pm);
+}
+
+// B(p) = sum over the group of v_j (lam_x phi(d_x / M_x) + lam_tau d_tau / M_tau)
+// for adjacent pairs and v_j c0 otherwise: every term of the group cost that
+// does not involve features.  One wave per 16-row tile of a group (the pair
+// kernels' work units): lane l takes row l % 16 of the tile and every fourth
+// member of the group from l / 16 on; the four lanes of a row add their sums
+// in a fixed order.
+__global__ __launch_bounds__(kThreads) void lite_b_kernel(LiteDev a) {
+  const int lane = threadIdx.x & 63;
+  const int row = lane & 15, quad = lane >> 4;
+  const int gw = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  const int nw = gridDim.x * kWaves;
+  const int units = int(a.ctrl[kCtrlTiles]);
+  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
+  const double m_x = sqrt(__longlong_as_double(*reinterpret_cast<const long long*>(a.ctrl + kCtrlMx2)));
+  const int m_t = int(a.ctrl[kCtrlMt]);
+  const double c0 = double(a.lam_f) + double(a.lam_x) + double(a.lam_t);
+  for (int u = gw; u < units; u += nw) {
+    Unit t;
+    if (!unit_of(a, u, t)) continue;
+    const int r = t.ta * kTileRows + row;
+    const bool rvalid = r < t.g;
+    const int i = t.p0 + min(r, t.g - 1);
+    const int tokn = perm[i];
+    const unsigned long long vi = a.vox_pos[i];
+    const double xi = a.pos[3 * tokn], yi = a.pos[3 * tokn + 1], zi = a.pos[3 * tokn + 2];
+    const int fi = a.frame[tokn];
+    double acc = 0.0;
+    // Members jj, jj + 4, jj + 8, jj + 12 per round: their loads go out
+    // together, then their terms are added in member order.
+    constexpr int R = 4;
+    for (int j0 = quad; j0 < t.g; j0 += 4 * R) {
+      int tj[R];
+      unsigned long long vj[R];
+#pragma unroll
+      for (int x = 0; x < R; ++x) {
+        const int jj = min(j0 + 4 * x, t.g - 1);
+        tj[x] = perm[t.p0 + jj];
+        vj[x] = a.vox_pos[t.p0 + jj];
+      }
+      float px[R], py[R], pz[R], cv[R];
+      int fr[R];
+#pragma unroll
+      for (int x = 0; x < R; ++x) {
+        px[x] = a.pos[3 * tj[x]];
+        py[x] = a.pos[3 * tj[x] + 1];
+        pz[x] = a.pos[3 * tj[x] + 2];
+        fr[x] = a.frame[tj[x]];
+        cv[x] = a.v[tj[x]];
+      }
+#pragma unroll
+      for (int x = 0; x < R; ++x) {
+        if (j0 + 4 * x >= t.g) break;
+        const double w = double(cv[x]);
+        if (!adjacent(vi, vj[x])) {
+          acc += w * c0;
+          continue;
+        }
+        const double dist = sqrt(sq_dist(xi, yi, zi, px[x], py[x], pz[x]));
+        const double z = m_x > 0.0 ? dist / m_x : 0.0;
+        const double ph = a.kappa > 0.f ? log1p(double(a.kappa) * z) * a.inv_log1p_kappa : z;
+        const double dt = m_t > 0 ? double(max(0, fi - fr[x])) / double(m_t) : 0.0;
+        acc += w * (double(a.lam_x) * ph + double(a.lam_t) * dt);
+      }
+    }
+    acc += __shfl_xor(acc, 16);
+    acc += __shfl_xor(acc, 32);
+    if (quad == 0 && rvalid) a.B[i] = acc;
   }
 }
 
@@ -850,6 +896,9 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   a.gid = reinterpret_cast<int*>(w + L.gid);
   a.gstart = reinterpret_cast<int*>(w + L.gstart);
   a.rt_start = reinterpret_cast<int*>(w + L.rt_start);
+  a.unit_group = reinterpret_cast<int*>(w + L.unit_group);
+  a.big_unit = reinterpret_cast<int*>(w + L.big_unit);
+  a.bsum2 = reinterpret_cast<unsigned long long*>(w + L.bsum2);
   a.A = reinterpret_cast<double*>(w + L.A);
   a.B = reinterpret_cast<double*>(w + L.B);
   a.gcost = reinterpret_cast<double*>(w + L.gcost);
@@ -867,9 +916,6 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   // over all groups, so n / 16 + k waves cover every tile.
   const int units = p.n / kTileRows + p.k;
   const int blocks = std::max(1, std::min((units + kWaves - 1) / kWaves, 65535));
-  lite_maxima_kernel<<<std::max(1, std::min((p.n + kWaves - 1) / kWaves, 512)), kThreads, 0, stream>>>(a);
-  lite_b_kernel<<<(p.n + kWaves - 1) / kWaves, kThreads, 0, stream>>>(a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
   // Groups of more than kSplitTiles tiles: one block per row tile.
   const int split_blocks = std::max(1, std::min(units, 256));
   if (p.bf16) {
@@ -879,6 +925,9 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
     lite_pair_kernel<false><<<blocks, kThreads, 0, stream>>>(a);
     lite_pair_split_kernel<false><<<split_blocks, kSplitWaves * 64, 0, stream>>>(a);
   }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // B needs M_x and M_tau, which the pair kernels raise.
+  lite_b_kernel<<<blocks, kThreads, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   lite_select_kernel<<<(p.k + kWaves - 1) / kWaves, kThreads, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
