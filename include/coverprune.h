@@ -169,7 +169,7 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
  *             of a source-major copy of the cost that the first pass writes
  *             into the workspace (4 n^2 bytes, 1 GiB at n = 16384); larger
  *             scenes, or CP_SGS_INCREMENTAL | CP_SGS_COMPACT, exchange the
- *             improved targets between the compute units instead (about 16
+ *             improved targets between the compute units instead (about 45
  *             bytes per token, slower per step).  Both schedules sum the
  *             same integers and return the same result.
  *   selected        [k] int32 output: tokens in the order they were chosen
@@ -182,8 +182,9 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
 /* Workspace for one form (flags as for coverprune_sgs_select; 0 for flags it
  * does not accept): the dense form needs about 9 MB at n = 16384 (private
  * best costs and float64 partial gains of up to 64 row panels), the
- * incremental form 4 n + 16 bytes per token up to n = 32768 and about 16
- * bytes per token beyond that or with CP_SGS_COMPACT. */
+ * incremental form 4 n + 45 bytes per token up to n = 32768 and about 45
+ * bytes per token beyond that or with CP_SGS_COMPACT, each plus about
+ * 100 KB of exchange slots. */
 size_t coverprune_sgs_workspace(int64_t n, int64_t k, uint32_t flags);
 cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capacity, int64_t k,
                                 float c0, uint32_t flags, int32_t* selected, double* step_gain,
