@@ -10,7 +10,8 @@
 //     groups   V = floor(v * 2^40) in exact integers; an exclusive scan gives
 //              the mass before each position, t(p) = min(K-1, K * mass / W);
 //              a prefix-min scan of t(p) - p and the K - N + p floor give the
-//              group of every position (the walk of Eq. 17 in scan form)
+//              group of every position (the walk of Eq. 17 in scan form),
+//              and in the same pass the group starts
 //     tiles    16-row tiles per group, their prefix, the group of every
 //              tile and the list of big groups' tiles (work units below)
 //   pairs    per 16-row tile of a group, the tile's rows against the whole
@@ -427,27 +428,34 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     }
     __syncthreads();
     int run = s_minoff;
+    // Group starts, voxels by sorted position and the group output in the
+    // same pass: a position starts a group when its group differs from the
+    // one before it.  Position p0 - 1 lies in the previous block, and its
+    // group follows from the same prefix minimum (s_minoff covers every
+    // position before p0).
+    __shared__ int s_gid[kThreads];
+    int gprev = blk > 0 && p0 > 0 ? max(K - n + p0 - 1, p0 - 1 + s_minoff) : -1;
     for (int c0 = p0; c0 < p1; c0 += kThreads) {
       const int i = c0 + t;
       const int m = i < p1 ? get(a.gid + i) : INT_MAX;
       const int inc = min(block_incl_min(m, s_i32), run);
-      if (i < p1) put(a.gid + i, max(K - n + i, i + inc));
+      const int q = i < p1 ? max(K - n + i, i + inc) : -1;
+      if (i < p1) put(a.gid + i, q);
       s_i32[t] = inc;
+      s_gid[t] = q;
       __syncthreads();
       run = s_i32[kThreads - 1];
+      if (i < p1) {
+        const int qb = t > 0 ? s_gid[t - 1] : gprev;
+        if (i == 0 || qb != q) put(a.gstart + q, i);
+        if (i == n - 1) put(a.gstart + K, n);
+        const int tokn = get(perm + i);
+        put(a.vox_pos + i, get(a.vox_tok + tokn));
+        if (a.group) a.group[tokn] = q;
+      }
+      gprev = s_gid[kThreads - 1];
       __syncthreads();
     }
-  }
-  grid_barrier(bar, ++round);
-
-  // ---- group starts, voxels by sorted position, group output
-  for (int i = p0 + t; i < p1; i += kThreads) {
-    const int q = get(a.gid + i);
-    if (i == 0 || get(a.gid + i - 1) != q) put(a.gstart + q, i);
-    if (i == n - 1) put(a.gstart + K, n);
-    const int tokn = get(perm + i);
-    put(a.vox_pos + i, get(a.vox_tok + tokn));
-    if (a.group) a.group[tokn] = q;
   }
   grid_barrier(bar, ++round);
 
