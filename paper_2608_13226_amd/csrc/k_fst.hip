@@ -107,10 +107,10 @@ __device__ __forceinline__ double sq_dist(double ax, double ay, double az, doubl
 
 constexpr int kPosTile = 256;
 
-// Exact maximum squared distance over all pairs: blocks walk the upper
-// 256 x 256 tiles (grid-stride), a thread takes one row of the tile against
-// the tile's columns staged in LDS, and each block issues one atomic at the
-// end.
+// Exact maximum squared distance over all pairs: one block per upper
+// 256 x 256 tile (enough waves in flight to hide the float64 latency), a
+// thread takes one row of the tile against the tile's columns staged in LDS,
+// and a block whose maximum is larger than the running one raises it.
 __global__ __launch_bounds__(256) void pos_pairmax_kernel(const float* pos, int n, int ntiles, FstScratch s) {
   __shared__ double sx[kPosTile], sy[kPosTile], sz[kPosTile];
   __shared__ double sm[4];
@@ -136,7 +136,10 @@ __global__ __launch_bounds__(256) void pos_pairmax_kernel(const float* pos, int 
   best = wave_max(best);
   if ((threadIdx.x & 63) == 0) sm[threadIdx.x >> 6] = best;
   __syncthreads();
-  if (threadIdx.x == 0) atomic_max_nonneg(s.mx2_bits, fmax(fmax(sm[0], sm[1]), fmax(sm[2], sm[3])));
+  // Read first: the maximum only grows, and atomics from many blocks on one
+  // address serialize.
+  const double m = fmax(fmax(sm[0], sm[1]), fmax(sm[2], sm[3]));
+  if (threadIdx.x == 0 && m > __longlong_as_double((long long)get(s.mx2_bits))) atomic_max_nonneg(s.mx2_bits, m);
 }
 
 // ---------------------------------------------------------------------------
@@ -276,7 +279,7 @@ hipError_t launch_fst_prep(const FstParams& p, const FstScratch& s, hipStream_t 
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int t = tiles_of(p.n, kPosTile);
   const int tiles = t * (t + 1) / 2;
-  pos_pairmax_kernel<<<std::min(tiles, 512), 256, 0, stream>>>(p.pos, p.n, tiles, s);
+  pos_pairmax_kernel<<<tiles, 256, 0, stream>>>(p.pos, p.n, tiles, s);
   return hipGetLastError();
 }
 
