@@ -56,6 +56,13 @@ class SceneConfig:
     camera_height: float = 1.5
     voxel: Optional[float] = None   # Lite voxel size, metres
     path: str = "full"              # "full" (cost + greedy) or "lite"
+    # The workload's capacities come from the FST capacity of Eq. 9-10 with
+    # this many 3D neighbours per token (None: the generator's own recipe
+    # above is the workload's).  The generator does not compute it: that is
+    # the method's arithmetic, done by the library for the benchmark and by
+    # the oracle for the parity tests; `capacity` stays the generator's
+    # recipe for every other use of the scene.
+    fst_capacity_nn: Optional[int] = None
 
     @property
     def n(self) -> int:
@@ -64,16 +71,19 @@ class SceneConfig:
 
 # The five workloads the path is measured and checked on, named by what they
 # are.  Box extents not fixed by the workload description are chosen so that
-# the 3 m camera orbit encloses the objects.
+# the 3 m camera orbit encloses the objects.  Capacities: uniform for the
+# 8192-token scene, proportional to the token count of the token's object for
+# the 16384-token room, and the FST capacity (8 or 16 neighbours) for the
+# other three.
 CONFIGS = {
     # 1024 tokens (8 frames x 128), 256-d float32 features, K = 102 (10 %).
     "n1024_d256_f32": SceneConfig(
         "n1024_d256_f32", 8, 128, 256, "f32", 102, 12, None,
-        (0.0, 0.0, 0.0), (6.0, 6.0, 3.0), 0.05, "density", False, None, 0.0),
+        (0.0, 0.0, 0.0), (6.0, 6.0, 3.0), 0.05, "density", False, None, 0.0, fst_capacity_nn=8),
     # 4096 tokens (16 frames x 16x16 patches), 1152-d bf16, K = 410 (10 %).
     "n4096_d1152": SceneConfig(
         "n4096_d1152", 16, 256, 1152, "bf16", 410, 40, 1.2,
-        (-2.0, -2.0, 0.0), (2.0, 2.0, 2.5), 0.05, "density", True, None, 0.0),
+        (-2.0, -2.0, 0.0), (2.0, 2.0, 2.5), 0.05, "density", True, None, 0.0, fst_capacity_nn=16),
     # 8192 tokens (32 frames x 256), 3584-d bf16 (LLM width), K = 1229 (15 %).
     "n8192_d3584": SceneConfig(
         "n8192_d3584", 32, 256, 3584, "bf16", 1229, 80, 1.2,
@@ -86,7 +96,7 @@ CONFIGS = {
     "lite_n32768_d3584": SceneConfig(
         "lite_n32768_d3584", 128, 256, 3584, "bf16", 3277, 300, 1.2,
         (-8.0, -8.0, 0.0), (8.0, 8.0, 3.0), 0.05, "uniform", True, (4, 12), 0.2,
-        voxel=0.25, path="lite"),
+        voxel=0.25, path="lite", fst_capacity_nn=16),
     # The paper's own efficiency shape: 32 frames x 196 tokens = 6272 -> 628.
     "paper_n6272_d3584": SceneConfig(
         "paper_n6272_d3584", 32, 196, 3584, "bf16", 628, 80, 1.2,

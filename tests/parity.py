@@ -2,11 +2,14 @@
 from the oracle; GPU outputs are only ever the thing being checked."""
 from __future__ import annotations
 
-import numpy as np
-
 import functools
+import os
+from concurrent.futures import ThreadPoolExecutor
 
-from oracle import fst, lite, sgs
+import numpy as np
+from threadpoolctl import threadpool_limits
+
+from oracle import capacity, fst, lite, sgs
 from scenes import make_scene, subscene
 
 # Cost tolerance: bf16 inputs with float32 accumulation against float64.
@@ -31,6 +34,18 @@ def sample_scene(cfg, n, seed, salt=0):
     return subscene(s, idx)
 
 
+def workload_scene(cfg, seed):
+    """A whole workload scene with the workload's own capacities: the
+    generator's recipe, or the oracle's FST capacity (Eq. 9-10) where the
+    workload names it.  Inputs of both the library and the oracle."""
+    s = make_scene(cfg, seed)
+    nn = s.config.fst_capacity_nn
+    if nn:
+        F = fst.widen_features(s.feats, s.dtype)
+        s.capacity = capacity.capacity_ref(F, s.pos, s.frame, nn)["v"].astype(np.float32)
+    return s
+
+
 def oracle_cost(scene, weights=(1.0, 1.0, 1.0), kappa=10.0, rows=None, maxima=None):
     F = fst.widen_features(scene.feats, scene.dtype)
     return fst.fst_cost_ref(F, scene.pos, scene.frame, weights=weights, kappa=kappa, rows=rows,
@@ -49,6 +64,37 @@ def oracle_cost_f32_target_major(scene, weights=(1.0, 1.0, 1.0), kappa=10.0, blo
         C, _ = fst.fst_cost_ref(F, scene.pos, scene.frame, weights=weights, kappa=kappa, rows=rows,
                                 maxima=maxima)
         out[:, lo:lo + rows.size] = C.T.astype(np.float32)
+    return out, maxima
+
+
+def _workers():
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def oracle_cost_full(scene, weights=(1.0, 1.0, 1.0), kappa=10.0, block=256):
+    """The oracle's whole cost C[s, t] in float64, source-major, for scenes of
+    up to tens of thousands of tokens.  Each row block is one call of the
+    oracle on a thread pool (one BLAS thread per call); the normalisers are
+    the oracle's discrepancy maxima over every block, exactly what
+    ``fst.sample_maxima`` returns (a maximum does not depend on the order)."""
+    F = fst.widen_features(scene.feats, scene.dtype)
+    n = scene.n
+    blocks = [np.arange(lo, min(n, lo + block)) for lo in range(0, n, block)]
+
+    def block_max(r):
+        return (float(fst.feature_discrepancy(F, r).max()), float(fst.spatial_discrepancy(scene.pos, r).max()),
+                float(fst.temporal_discrepancy(scene.frame, r).max()))
+
+    out = np.empty((n, n), np.float64)
+
+    def block_cost(r):
+        C, _ = fst.fst_cost_ref(F, scene.pos, scene.frame, weights=weights, kappa=kappa, rows=r, maxima=maxima)
+        out[r[0]:r[-1] + 1] = C
+
+    with threadpool_limits(1), ThreadPoolExecutor(_workers()) as pool:
+        parts = list(pool.map(block_max, blocks))
+        maxima = tuple(max(p[i] for p in parts) for i in range(3))
+        list(pool.map(block_cost, blocks))
     return out, maxima
 
 
@@ -93,6 +139,98 @@ def replay_greedy(C_src: np.ndarray, v: np.ndarray, c0: float, picks, tie_atol=0
         b = np.minimum(b, C[t])
         objs.append(float(np.sum(v * b)))
     return ties, np.array(gains), np.array(objs)
+
+
+def _row_gains(C, rows, v, b):
+    """Exact float64 gains sum_j v_j max(0, b_j - C(c, j)) of the source rows
+    ``rows`` (an integer array, so indexing copies), the formula of
+    ``replay_greedy``."""
+    X = np.asarray(C[np.asarray(rows, np.int64)], np.float64)
+    if X.base is not None or X.dtype != np.float64:
+        X = np.array(X, np.float64)
+    np.subtract(b[None, :], X, out=X)
+    np.maximum(X, 0.0, out=X)
+    X *= v[None, :]
+    return X.sum(axis=1)
+
+
+def _gains(C, rows, v, b, pool, chunk=256):
+    rows = np.asarray(rows, np.int64)
+    if pool is None or rows.size <= chunk:
+        return _row_gains(C, rows, v, b)
+    return np.concatenate(list(pool.map(lambda lo: _row_gains(C, rows[lo:lo + chunk], v, b),
+                                        range(0, rows.size, chunk))))
+
+
+def lazy_replay(C, v, c0: float, picks, tie_atol=0.0, alt=None, tie_rtol=TIE_RTOL):
+    """``replay_greedy`` for full-size trajectories.
+
+    C is the source-major cost (float32 or float64; C[c, j] = C(c, j)) on
+    which the oracle evaluates exact float64 gains along the trajectory
+    ``picks``.  Every candidate keeps an upper bound on its gain, the gain it
+    had when last evaluated: gains only shrink as targets get covered (the
+    coverage function is submodular, Sec. 3.5), so a candidate whose bound is
+    below the pick's gain cannot beat or tie the pick, and only the others
+    are evaluated again.  The check is therefore the same as evaluating
+    every candidate at every step.
+
+    A competitor c beats the pick t if its gain is larger, or equal at a
+    smaller index; the pick is accepted when
+    gain(t) >= gain(c) - (tie_rtol * gain(c) + tie_atol + delta_t + delta_c)
+    for every such c.  ``alt`` is the source-major cost the picks were made
+    on, when it is not C (end-to-end runs): then delta_c = sum_j v_j (|b_j -
+    b'_j| + |C(c, j) - C'(c, j)|), with b' the best costs under ``alt``, bounds
+    how far c's gain under ``alt`` is from its gain under C; otherwise delta = 0.
+
+    Returns (ties, gains, objectives, near): the steps whose pick was not the
+    oracle's own choice, the oracle's gains of the picks, L after each step,
+    and for each tie step (step, pick, oracle choice, their gains, allowance).
+    """
+    v = np.asarray(v, np.float64)
+    n = C.shape[0]
+    b = np.full(n, float(c0))
+    b_alt = b.copy() if alt is not None else None
+    chosen = np.zeros(n, bool)
+    ties, gains, objs, near = [], [], [], []
+
+    def delta(c):
+        return float(np.sum(v * (np.abs(b - b_alt) + np.abs(np.asarray(C[c], np.float64) -
+                                                             np.asarray(alt[c], np.float64)))))
+
+    with threadpool_limits(1), ThreadPoolExecutor(_workers()) as pool:
+        ub = _gains(C, np.arange(n), v, b, pool)
+        for step, t in enumerate(int(x) for x in picks):
+            assert 0 <= t < n and not chosen[t], f"step {step}: pick {t} invalid or repeated"
+            g_t = float(_row_gains(C, [t], v, b)[0])
+            cand = np.flatnonzero(ub >= g_t)
+            cand = cand[~chosen[cand] & (cand != t)]
+            if cand.size:
+                g_c = _gains(C, cand, v, b, pool)
+                ub[cand] = g_c
+                beat = (g_c > g_t) | ((g_c == g_t) & (cand < t))
+                if beat.any():
+                    comp, g_comp = cand[beat], g_c[beat]
+                    slack = tie_rtol * np.abs(g_comp) + tie_atol
+                    if alt is not None:
+                        d_t = delta(t)
+                        slack = slack + d_t + np.array([delta(c) for c in comp])
+                    bad = g_t < g_comp - slack
+                    if bad.any():
+                        c = int(comp[bad][0])
+                        raise AssertionError(f"step {step}: picked {t} with gain {g_t!r}, but {c} has "
+                                             f"{float(g_comp[bad][0])!r} (allowance {float(slack[bad][0]):.3g})")
+                    top = np.flatnonzero(g_comp == g_comp.max())
+                    best = int(comp[top].min())
+                    ties.append(step)
+                    near.append(dict(step=step, pick=t, oracle=best, gain=g_t, oracle_gain=float(g_comp.max()),
+                                     allowance=float(np.max(slack))))
+            chosen[t] = True
+            gains.append(g_t)
+            b = np.minimum(b, np.asarray(C[t], np.float64))
+            if alt is not None:
+                b_alt = np.minimum(b_alt, np.asarray(alt[t], np.float64))
+            objs.append(float(np.sum(v * b)))
+    return ties, np.array(gains), np.array(objs), near
 
 
 def replay_greedy_local(C_tm: np.ndarray, v: np.ndarray, c0: float, neighbours, picks, tie_atol=0.0):
