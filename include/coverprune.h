@@ -38,6 +38,18 @@
  *     of the calling thread.
  *   - Results are bitwise reproducible run to run on the same GPU.  Calls on
  *     distinct workspaces and streams may run concurrently.
+ *   - Waits between the blocks of one launch are bounded.  The selection
+ *     calls (sgs_select, sgs_select_batch, sgs_local_select, lite_select) run
+ *     persistent launches whose blocks wait for each other; a wait that has
+ *     polled for about a second (far beyond any legitimate wait: a launch
+ *     starved of compute units, or a broken device) gives up, every block of
+ *     the launch leaves, and every entry of `selected` is set to -1, which is
+ *     never a token index.  The call itself has already returned CP_OK (the
+ *     host is not synchronised), so a caller that must detect this checks
+ *     selected[0] >= 0 once the stream has completed; the other outputs of
+ *     that call are then undefined.  COVERPRUNE_TEST_ABORT=1 in the
+ *     environment makes every such launch give up at its first unmet wait
+ *     (a test of this path; every kernel still ends normally).
  */
 #ifndef COVERPRUNE_H
 #define COVERPRUNE_H
@@ -74,6 +86,13 @@ typedef struct {
 #define CP_SGS_DENSE 0u       /* every step re-evaluates every candidate's gain over the whole cost matrix */
 #define CP_SGS_INCREMENTAL 1u /* gains computed once, then updated from the rows whose best cost drops */
 #define CP_SGS_COMPACT 2u     /* with CP_SGS_INCREMENTAL: the schedule with the small workspace */
+
+/* The cost of leaving a target uncovered, c0 of the greedy (Sec. 3.5): the
+ * largest value the cost of Eq. 8 can take, (lambda_f + lambda_x) +
+ * lambda_tau in float arithmetic.  The selection calls take c0 as an argument;
+ * this is the value to pass for a cost made with weights w.  Pure host
+ * arithmetic, no device work. */
+float coverprune_uncovered_cost(cp_fst_weights w);
 
 /* ------------------------------------------------------------------------ */
 /* FST transport cost (Sec. 3.3, Eq. 7-8).
@@ -152,8 +171,8 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
  *   cost      [n, n] float, target-major as written by coverprune_fst_cost
  *   capacity  [n] float target capacities v (Sec. 3.4), v >= 0
  *   k         1 <= k <= n
- *   c0        cost of leaving a target uncovered; lambda_f + lambda_x +
- *             lambda_tau (the largest value C can take) is the usual choice
+ *   c0        cost of leaving a target uncovered; coverprune_uncovered_cost(w)
+ *             (the largest value C can take) is the usual choice
  *   flags     CP_SGS_DENSE: every step sums every candidate's gain over the
  *             whole matrix (K full reads of the cost).
  *             CP_SGS_INCREMENTAL: the gains are summed once at b = c0 and then
@@ -351,18 +370,23 @@ cp_status coverprune_sgs_literal_select(const float* cost, int64_t n, const floa
  *   group       [n] int32 output (may be NULL): group of every token
  *   objective   [1] double output (may be NULL): sum over groups of the
  *               prototype's cost, the block-plan transport cost of Eq. 20
+ *   token_cost  [n] double output (may be NULL): every token t's cost to its
+ *               group, sum_{j in G_q} v_j C(t, j), the quantity Eq. 18
+ *               minimises (token order, not Morton order)
+ * The front of the call (keys, sort, groups) is one persistent launch with
+ * bounded waits; when it gives up, selected[] is -1 and the objective NaN.
  */
 size_t coverprune_lite_workspace(int64_t n, int64_t d, int64_t k, cp_dtype dtype);
 cp_status coverprune_lite_select(const void* feats, cp_dtype dtype, int64_t n, int64_t d,
                                  const float* pos, const int32_t* frame, const float* capacity,
                                  int64_t k, cp_fst_weights w, float voxel_size, int32_t* selected,
-                                 int32_t* group, double* objective, void* workspace,
+                                 int32_t* group, double* objective, double* token_cost, void* workspace,
                                  size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 const char* coverprune_status_string(cp_status status); /* static text, never NULL */
 const char* coverprune_last_error(void);                /* thread-local; "" if none */
-int coverprune_abi_version(void);                       /* 1 */
+int coverprune_abi_version(void);                       /* 2 */
 
 #ifdef __cplusplus
 }

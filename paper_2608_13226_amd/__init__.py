@@ -3,7 +3,16 @@
 Python binding of ``libcoverprune.so`` (C-ABI in include/coverprune.h).  The
 functions here only check and marshal torch tensors: every step runs in the
 library's HIP kernels.  Tensors must live on the current GPU; work is
-enqueued on torch's current stream and nothing synchronises the host.
+enqueued on torch's current stream and nothing synchronises the host, with
+two exceptions that the caller asks for:
+
+* ``check=True`` on a selection call (or ``result.check()`` later)
+  synchronises the stream and raises CoverPruneError when the launch's
+  bounded waits gave up (the library then marks ``selected`` with -1);
+* ``COVERPRUNE_DEBUG=1`` in the environment validates the data before every
+  call (finite features, positions and costs; capacities finite, >= 0, with
+  a positive sum), which the library itself does not read for validity, and
+  then checks every selection as ``check=True`` does.
 """
 from __future__ import annotations
 
@@ -14,7 +23,8 @@ from typing import Optional
 
 import torch
 
-__all__ = ["fst_cost", "fst_capacity", "sgs_select", "sgs_select_batch", "sgs_literal_select", "knn", "sgs_local_select", "lite_select", "library", "library_path", "CoverPruneError",
+__all__ = ["fst_cost", "fst_capacity", "sgs_select", "sgs_select_batch", "sgs_literal_select", "knn",
+           "sgs_local_select", "lite_select", "uncovered_cost", "library", "library_path", "CoverPruneError",
            "DEFAULT_KAPPA"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -22,6 +32,7 @@ _LIB_NAME = "libcoverprune.so"
 
 # The paper leaves kappa open (Sec. 3.3 only requires kappa > 0).
 DEFAULT_KAPPA = 10.0
+ABI_VERSION = 2
 
 CP_F32, CP_BF16 = 0, 1
 CP_SGS_DENSE = 0
@@ -31,6 +42,39 @@ CP_SGS_COMPACT = 2
 
 class CoverPruneError(RuntimeError):
     pass
+
+
+def _debug() -> bool:
+    return os.environ.get("COVERPRUNE_DEBUG", "") == "1"
+
+
+def _require(ok: bool, msg: str) -> None:
+    if not ok:
+        raise CoverPruneError(f"COVERPRUNE_DEBUG: {msg}")
+
+
+def _debug_features(feats, pos, frame) -> None:
+    _require(bool(torch.isfinite(feats).all()), "features hold NaN or infinite values")
+    _require(bool(torch.isfinite(pos).all()), "positions hold NaN or infinite values")
+
+
+def _debug_capacity(capacity) -> None:
+    _require(bool(torch.isfinite(capacity).all()), "capacities hold NaN or infinite values")
+    _require(bool((capacity >= 0).all()), "capacities must be >= 0")
+    _require(float(capacity.double().sum()) > 0.0, "capacities must have a positive sum")
+
+
+def _debug_cost(cost) -> None:
+    _require(bool(torch.isfinite(cost).all()), "the cost holds NaN or infinite values")
+
+
+def _check_selected(selected: torch.Tensor, stream, what: str) -> None:
+    """Synchronise ``stream`` and raise when the launch gave up (-1 picks)."""
+    s = torch.cuda.current_stream() if stream is None else stream
+    s.synchronize()
+    if selected.numel() and int(selected[0].item()) < 0:
+        raise CoverPruneError(f"{what}: the launch gave up waiting (bounded wait exceeded); "
+                              f"selected holds -1")
 
 
 class _Weights(ctypes.Structure):
@@ -98,7 +142,7 @@ def library() -> ctypes.CDLL:
     lib.coverprune_lite_workspace.argtypes = [i64, i64, i64, ctypes.c_int]
     lib.coverprune_lite_workspace.restype = sz
     lib.coverprune_lite_select.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, vp, i64, _Weights,
-                                           ctypes.c_float, vp, vp, vp, vp, sz, vp]
+                                           ctypes.c_float, vp, vp, vp, vp, vp, sz, vp]
     lib.coverprune_lite_select.restype = st
     lib.coverprune_status_string.argtypes = [st]
     lib.coverprune_status_string.restype = ctypes.c_char_p
@@ -106,6 +150,11 @@ def library() -> ctypes.CDLL:
     lib.coverprune_last_error.restype = ctypes.c_char_p
     lib.coverprune_abi_version.argtypes = []
     lib.coverprune_abi_version.restype = ctypes.c_int
+    lib.coverprune_uncovered_cost.argtypes = [_Weights]
+    lib.coverprune_uncovered_cost.restype = ctypes.c_float
+    if lib.coverprune_abi_version() != ABI_VERSION:
+        raise CoverPruneError(f"{path} has ABI {lib.coverprune_abi_version()}, this binding needs {ABI_VERSION}: "
+                              f"rebuild it")
     _lib = lib
     return lib
 
@@ -156,6 +205,12 @@ def _weights(weights, kappa) -> _Weights:
     return _Weights(lf, lx, lt, float(kappa))
 
 
+def uncovered_cost(weights=(1.0, 1.0, 1.0)) -> float:
+    """c0 of the greedy for a cost made with ``weights``: the largest value
+    the cost can take (coverprune_uncovered_cost)."""
+    return float(library().coverprune_uncovered_cost(_weights(weights, 0.0)))
+
+
 def fst_cost(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor,
              weights=(1.0, 1.0, 1.0), kappa: float = DEFAULT_KAPPA,
              out: Optional[torch.Tensor] = None, maxima: Optional[torch.Tensor] = None,
@@ -170,6 +225,8 @@ def fst_cost(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor,
     _need(feats, "feats", feats.dtype, (n, d), dev)
     _need(pos, "pos", torch.float32, (n, 3), dev)
     _need(frame, "frame", torch.int32, (n,), dev)
+    if _debug():
+        _debug_features(feats, pos, frame)
     if out is None:
         out = torch.empty((n, n), dtype=torch.float32, device=dev)
     _need(out, "out", torch.float32, (n, n), dev)
@@ -197,6 +254,8 @@ def fst_capacity(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor, n_
     _need(feats, "feats", feats.dtype, (n, d), dev)
     _need(pos, "pos", torch.float32, (n, 3), dev)
     _need(frame, "frame", torch.int32, (n,), dev)
+    if _debug():
+        _debug_features(feats, pos, frame)
     if out is None:
         out = torch.empty(n, dtype=torch.float32, device=dev)
     _need(out, "out", torch.float32, (n,), dev)
@@ -220,22 +279,34 @@ class SgsResult:
     objective: torch.Tensor    # [k] float64, L(S) after each step
     assign: torch.Tensor       # [n] int32
 
+    def check(self, stream=None) -> "SgsResult":
+        """Synchronise and raise CoverPruneError if the launch gave up."""
+        _check_selected(self.selected, stream, "greedy selection")
+        return self
+
+
+def _c0(c0, weights) -> float:
+    return uncovered_cost(weights) if c0 is None else float(c0)
+
 
 def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[float] = None,
                weights=(1.0, 1.0, 1.0), workspace: Optional[torch.Tensor] = None,
-               stream=None, incremental: bool = False, compact: bool = False) -> SgsResult:
+               stream=None, incremental: bool = False, compact: bool = False, check: bool = False) -> SgsResult:
     """Greedy selection of k tokens over a target-major cost (Sec. 3.5, Eq. 11-16).
-    c0 defaults to the sum of the cost weights, the largest value C takes.
-    incremental=True runs the same greedy with gains updated from the rows
-    whose best cost drops (CP_SGS_INCREMENTAL) instead of full sweeps;
-    compact=True (with incremental) picks the small-workspace schedule."""
+    c0 defaults to coverprune_uncovered_cost(weights), the largest value C
+    takes.  incremental=True runs the same greedy with gains updated from the
+    rows whose best cost drops (CP_SGS_INCREMENTAL) instead of full sweeps;
+    compact=True (with incremental) picks the small-workspace schedule.
+    check=True synchronises and raises if the launch gave up."""
     lib = library()
     n = cost.shape[0]
     dev = cost.device
     _need(cost, "cost", torch.float32, (n, n), dev)
     _need(capacity, "capacity", torch.float32, (n,), dev)
-    if c0 is None:
-        c0 = float(sum(float(w) for w in weights))
+    if _debug():
+        _debug_cost(cost)
+        _debug_capacity(capacity)
+    c0 = _c0(c0, weights)
     sel = torch.empty(int(k), dtype=torch.int32, device=dev)
     gain = torch.empty(int(k), dtype=torch.float64, device=dev)
     obj = torch.empty(int(k), dtype=torch.float64, device=dev)
@@ -249,20 +320,21 @@ def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[
     _check(lib.coverprune_sgs_select(_ptr(cost), n, _ptr(capacity), int(k), float(c0), flags,
                                      _ptr(sel), _ptr(gain), _ptr(obj), _ptr(assign), _ptr(workspace),
                                      workspace.numel(), _stream(stream)))
-    return SgsResult(sel, gain, obj, assign)
+    r = SgsResult(sel, gain, obj, assign)
+    return r.check(stream) if (check or _debug()) else r
 
 
 def sgs_select_batch(costs, capacities, ks, c0: Optional[float] = None, weights=(1.0, 1.0, 1.0),
-                     workspace: Optional[torch.Tensor] = None, stream=None, compact: bool = False):
+                     workspace: Optional[torch.Tensor] = None, stream=None, compact: bool = False,
+                     check: bool = False):
     """The incremental greedy of several scenes (lists of target-major costs,
     capacities and budgets) in one launch.  Returns one SgsResult per scene.
-    compact=True picks the small-workspace schedule."""
+    compact=True picks the small-workspace schedule; check as for sgs_select."""
     lib = library()
     count = len(costs)
     if not (len(capacities) == len(ks) == count):
         raise ValueError("costs, capacities and ks must have the same length")
-    if c0 is None:
-        c0 = float(sum(float(w) for w in weights))
+    c0 = _c0(c0, weights)
     arr = (_SgsScene * max(count, 1))()
     out = []
     for s, (cost, cap, k) in enumerate(zip(costs, capacities, ks)):
@@ -270,6 +342,9 @@ def sgs_select_batch(costs, capacities, ks, c0: Optional[float] = None, weights=
         dev = cost.device
         _need(cost, f"costs[{s}]", torch.float32, (n, n), dev)
         _need(cap, f"capacities[{s}]", torch.float32, (n,), dev)
+        if _debug():
+            _debug_cost(cost)
+            _debug_capacity(cap)
         r = SgsResult(torch.empty(int(k), dtype=torch.int32, device=dev),
                       torch.empty(int(k), dtype=torch.float64, device=dev),
                       torch.empty(int(k), dtype=torch.float64, device=dev),
@@ -283,6 +358,9 @@ def sgs_select_batch(costs, capacities, ks, c0: Optional[float] = None, weights=
         workspace = _workspace(need, costs[0].device if count else None)
     _check(lib.coverprune_sgs_select_batch(arr, count, flags, _ptr(workspace), workspace.numel(),
                                            _stream(stream)))
+    if check or _debug():
+        for r in out:
+            r.check(stream)
     return out
 
 
@@ -339,10 +417,10 @@ def knn(pos: torch.Tensor, g: int, out: Optional[torch.Tensor] = None, stream=No
 
 def sgs_local_select(cost: torch.Tensor, capacity: torch.Tensor, neighbours: torch.Tensor, k: int,
                      c0: Optional[float] = None, weights=(1.0, 1.0, 1.0),
-                     workspace: Optional[torch.Tensor] = None, stream=None) -> SgsResult:
+                     workspace: Optional[torch.Tensor] = None, stream=None, check: bool = False) -> SgsResult:
     """Greedy selection with each candidate's gain over its neighbour row only
     (Sec. 3.5, Eq. 13); neighbours is an [n, g] int32 table such as knn()
-    returns.  c0 as for sgs_select."""
+    returns.  c0 and check as for sgs_select."""
     lib = library()
     n = cost.shape[0]
     dev = cost.device
@@ -352,8 +430,10 @@ def sgs_local_select(cost: torch.Tensor, capacity: torch.Tensor, neighbours: tor
         raise ValueError("neighbours must be an [n, g] table")
     g = neighbours.shape[1]
     _need(neighbours, "neighbours", torch.int32, (n, g), dev)
-    if c0 is None:
-        c0 = float(sum(float(w) for w in weights))
+    if _debug():
+        _debug_cost(cost)
+        _debug_capacity(capacity)
+    c0 = _c0(c0, weights)
     sel = torch.empty(int(k), dtype=torch.int32, device=dev)
     gain = torch.empty(int(k), dtype=torch.float64, device=dev)
     obj = torch.empty(int(k), dtype=torch.float64, device=dev)
@@ -364,7 +444,8 @@ def sgs_local_select(cost: torch.Tensor, capacity: torch.Tensor, neighbours: tor
     _check(lib.coverprune_sgs_local_select(_ptr(cost), n, _ptr(capacity), _ptr(neighbours), g, int(k), float(c0),
                                            _ptr(sel), _ptr(gain), _ptr(obj), _ptr(assign), _ptr(workspace),
                                            workspace.numel(), _stream(stream)))
-    return SgsResult(sel, gain, obj, assign)
+    r = SgsResult(sel, gain, obj, assign)
+    return r.check(stream) if (check or _debug()) else r
 
 
 @dataclass
@@ -372,12 +453,20 @@ class LiteResult:
     selected: torch.Tensor     # [k] int32, prototype of group q at [q]
     group: torch.Tensor        # [n] int32
     objective: torch.Tensor    # [1] float64
+    token_cost: torch.Tensor   # [n] float64, each token's cost to its group (Eq. 18)
+
+    def check(self, stream=None) -> "LiteResult":
+        """Synchronise and raise CoverPruneError if the launch gave up."""
+        _check_selected(self.selected, stream, "Lite selection")
+        return self
 
 
 def lite_select(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor, capacity: torch.Tensor,
                 k: int, weights=(1.0, 1.0, 1.0), kappa: float = DEFAULT_KAPPA, voxel_size: float = 0.25,
-                workspace: Optional[torch.Tensor] = None, stream=None) -> LiteResult:
-    """CoverPrune-Lite (Sec. 4, Eq. 17-20)."""
+                workspace: Optional[torch.Tensor] = None, stream=None, token_cost: bool = False,
+                check: bool = False) -> LiteResult:
+    """CoverPrune-Lite (Sec. 4, Eq. 17-20).  token_cost=True also returns
+    every token's cost to its group; check as for sgs_select."""
     lib = library()
     n, d = feats.shape
     dev = feats.device
@@ -386,13 +475,19 @@ def lite_select(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor, cap
     _need(pos, "pos", torch.float32, (n, 3), dev)
     _need(frame, "frame", torch.int32, (n,), dev)
     _need(capacity, "capacity", torch.float32, (n,), dev)
+    if _debug():
+        _debug_features(feats, pos, frame)
+        _debug_capacity(capacity)
     sel = torch.empty(int(k), dtype=torch.int32, device=dev)
     group = torch.empty(n, dtype=torch.int32, device=dev)
     obj = torch.empty(1, dtype=torch.float64, device=dev)
+    tc = torch.empty(n if token_cost else 0, dtype=torch.float64, device=dev)
     need = lib.coverprune_lite_workspace(n, d, int(k), dt)
     if workspace is None:
         workspace = _workspace(need, dev)
     _check(lib.coverprune_lite_select(_ptr(feats), dt, n, d, _ptr(pos), _ptr(frame), _ptr(capacity), int(k),
                                       _weights(weights, kappa), float(voxel_size), _ptr(sel), _ptr(group),
-                                      _ptr(obj), _ptr(workspace), workspace.numel(), _stream(stream)))
-    return LiteResult(sel, group, obj)
+                                      _ptr(obj), _ptr(tc) if token_cost else None, _ptr(workspace),
+                                      workspace.numel(), _stream(stream)))
+    r = LiteResult(sel, group, obj, tc)
+    return r.check(stream) if (check or _debug()) else r

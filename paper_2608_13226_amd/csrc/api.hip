@@ -88,7 +88,9 @@ const char* coverprune_status_string(cp_status s) {
 
 const char* coverprune_last_error(void) { return g_last_error.c_str(); }
 
-int coverprune_abi_version(void) { return 1; }
+int coverprune_abi_version(void) { return 2; }
+
+float coverprune_uncovered_cost(cp_fst_weights w) { return (w.lambda_f + w.lambda_x) + w.lambda_tau; }
 
 // ---------------------------------------------------------------------------
 size_t coverprune_fst_cost_workspace(int64_t n, int64_t d, cp_dtype dtype) {
@@ -378,7 +380,7 @@ size_t coverprune_lite_workspace(int64_t n, int64_t d, int64_t k, cp_dtype dtype
 cp_status coverprune_lite_select(const void* feats, cp_dtype dtype, int64_t n, int64_t d,
                                  const float* pos, const int32_t* frame, const float* capacity,
                                  int64_t k, cp_fst_weights w, float voxel_size, int32_t* selected,
-                                 int32_t* group, double* objective, void* workspace,
+                                 int32_t* group, double* objective, double* token_cost, void* workspace,
                                  size_t workspace_bytes, void* stream) {
   cp_status st = check_features(feats, dtype, n, d, kMaxLiteN);
   if (st != CP_OK) return st;
@@ -407,6 +409,7 @@ cp_status coverprune_lite_select(const void* feats, cp_dtype dtype, int64_t n, i
   p.selected = selected;
   p.group = group;
   p.objective = objective;
+  p.token_cost = token_cost;
   p.workspace = workspace;
   p.workspace_bytes = workspace_bytes;
   hipError_t e = cp::launch_lite(p, static_cast<hipStream_t>(stream));

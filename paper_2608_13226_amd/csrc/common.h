@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <cstdlib>
+
 namespace cp {
 
 constexpr int kWave = 64;
@@ -97,18 +99,81 @@ __device__ __forceinline__ double get(const double* p) {
   return __longlong_as_double((long long)get(reinterpret_cast<const unsigned long long*>(p)));
 }
 
+// Bounded waits.  Every poll loop in the library reads the launch's abort
+// flag after each 64th failed poll (a device-scope load costs a round trip
+// through memory, so not after every one) and after every failed poll once
+// `limit` polls have failed; past the limit the wait raises the flag itself.
+// A wait that gives up makes its block leave the launch, every other block
+// gives up at its next unmet wait, and a kernel after the launch marks the
+// outputs (selected = -1).  kSpinLimit polls with a short sleep take about a
+// second, far beyond any legitimate wait.
+constexpr unsigned int kSpinLimit = 1u << 22;
+
+__device__ __forceinline__ bool give_up(unsigned int spins, unsigned int limit, unsigned int* abort) {
+  if ((spins & 63u) != 63u && spins < limit) return false;
+  if (get(abort)) return true;
+  if (spins >= limit) {
+    put(abort, 1u);
+    return true;
+  }
+  return false;
+}
+
+// Host side: the poll limit of the bounded waits and the abort flag's value
+// at launch.  COVERPRUNE_TEST_ABORT=1 in the environment starts every launch
+// with the flag raised and a zero limit, so that each wait gives up at its
+// first failed poll: the failure path runs, and every kernel still exits
+// normally (tests of that path; never set otherwise).
+struct WaitPolicy {
+  unsigned int limit;
+  unsigned int preset;
+};
+inline WaitPolicy wait_policy() {
+  const char* s = std::getenv("COVERPRUNE_TEST_ABORT");
+  if (s && s[0] == '1' && s[1] == 0) return {0u, 1u};
+  return {kSpinLimit, 0u};
+}
+
+// After a launch whose waits are bounded: every selected[] entry becomes -1
+// when the launch gave up.  A kernel of its own, so that it runs after every
+// block of the launch has finished and no block's late store of a pick can
+// land after the mark.
+namespace {
+__global__ void mark_aborted_kernel(const unsigned int* abort, int32_t* selected, int k) {
+  if (!*abort) return;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < k; i += gridDim.x * blockDim.x) selected[i] = -1;
+}
+hipError_t launch_mark_aborted(const unsigned int* abort, int32_t* selected, int k, hipStream_t stream) {
+  mark_aborted_kernel<<<(k + 255) / 256 < 64 ? (k + 255) / 256 : 64, 256, 0, stream>>>(abort, selected, k);
+  return hipGetLastError();
+}
+}  // namespace
+
 // Grid barrier for a cooperative launch: every block counts itself in and
 // waits until all gridDim.x blocks have arrived `round` times.  `counter`
 // must be zero at launch.  Only data written with put() before the barrier
-// may be read with get() after it.
-__device__ __forceinline__ void grid_barrier(unsigned int* counter, unsigned int round) {
+// may be read with get() after it.  Returns false, in every thread of the
+// block, when the wait gave up (see give_up): the block must then leave.
+__device__ __forceinline__ bool grid_barrier(unsigned int* counter, unsigned int round, unsigned int* abort,
+                                             unsigned int limit, int* sflag) {
   __syncthreads();
   if (threadIdx.x == 0) {
     __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const unsigned int target = round * gridDim.x;
-    while (get(counter) < target) __builtin_amdgcn_s_sleep(1);
+    int ok = 1;
+    for (unsigned int spins = 0; get(counter) < target; ++spins) {
+      if (give_up(spins, limit, abort)) {
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    *sflag = ok;
   }
   __syncthreads();
+  const bool ok = *sflag != 0;
+  __syncthreads();
+  return ok;
 }
 
 // (gain, index) pair ordering used by every argmax: larger gain first, then

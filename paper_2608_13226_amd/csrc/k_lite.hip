@@ -56,6 +56,9 @@ struct LiteDev {
   int32_t* selected;
   int32_t* group;
   double* objective;
+  double* token_cost;           // [n] or nullptr: each token's cost to its group (Eq. 18)
+  unsigned int poll_limit;      // polls before a grid barrier gives up (WaitPolicy)
+  unsigned int abort_init;      // the abort word's value at launch
   // workspace
   unsigned long long* key[2];
   int* tok[2];
@@ -86,6 +89,7 @@ constexpr int kCtrlSorted = 10;    // which key/tok buffer holds the sorted orde
 constexpr int kCtrlBarrier = 11;   // grid barrier counter
 constexpr int kCtrlTiles = 12;     // total number of 16-row tiles
 constexpr int kCtrlBig = 13;       // tiles of groups of more than kSplitTiles tiles
+constexpr int kCtrlAbort = 14;     // raised when a grid barrier of the front gives up
 
 struct Layout {
   size_t key0, key1, tok0, tok1, vox_tok, vox_pos, hist, bsum, bsum2, bmin, gid, gstart, rt_start, unit_group,
@@ -238,6 +242,7 @@ __global__ void lite_init_kernel(LiteDev a) {
     a.ctrl[kCtrlBarrier] = 0u;
     a.ctrl[kCtrlTiles] = 0u;
     a.ctrl[kCtrlBig] = 0u;
+    a.ctrl[kCtrlAbort] = a.abort_init;
   }
 }
 
@@ -248,7 +253,11 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
   const int tile = (n + G - 1) / G;
   const int p0 = min(n, blk * tile), p1 = min(n, p0 + tile);
   unsigned int* bar = a.ctrl + kCtrlBarrier;
+  unsigned int* abort = a.ctrl + kCtrlAbort;
   unsigned int round = 0;
+  // Every grid barrier is bounded; a block whose barrier gives up leaves, and
+  // the kernels after the front see the abort word and do nothing.
+  __shared__ int s_ok;
 
   __shared__ unsigned int s_u32[3][kWaves];
   __shared__ unsigned long long s_u64[kThreads + 2];
@@ -275,7 +284,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       atomicMin(a.ctrl + kCtrlBbox + t, x);
     }
   }
-  grid_barrier(bar, ++round);
+  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
 
   // ---- Morton keys
   {
@@ -303,7 +312,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     }
     if (lane == 0) atomicMax(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey), kmax);
   }
-  grid_barrier(bar, ++round);
+  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
 
   // ---- stable LSD radix sort of (key, token), 8 bits per pass
   const unsigned long long maxkey = get(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey));
@@ -320,7 +329,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     for (int i = p0 + t; i < p1; i += kThreads) atomicAdd(&s_hist[(get(ks + i) >> sh) & 0xffu], 1u);
     __syncthreads();
     put(a.hist + blk * kBins + t, s_hist[t]);
-    grid_barrier(bar, ++round);
+    if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
 
     // Base offset of digit t for this block: every smaller digit anywhere,
     // plus digit t in earlier blocks.
@@ -373,7 +382,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       s_base[t] += add;
       __syncthreads();
     }
-    grid_barrier(bar, ++round);
+    if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
   }
   const int sorted = passes & 1;
   const int* perm = sorted ? a.tok[1] : a.tok[0];
@@ -386,7 +395,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     block_excl_sum_u64(local, s_u64, tot);
     if (t == 0) put(a.bsum + blk, tot);
   }
-  grid_barrier(bar, ++round);
+  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
   {
     unsigned long long run, W;
     block_prefix_u64(a.bsum, G, blk, s_u64, run, W);
@@ -417,7 +426,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       put(a.bmin + blk, m);
     }
   }
-  grid_barrier(bar, ++round);
+  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
   {
     s_i32[t] = t < blk ? get(a.bmin + t) : INT_MAX;
     __syncthreads();
@@ -457,7 +466,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       __syncthreads();
     }
   }
-  grid_barrier(bar, ++round);
+  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
 
   // ---- tiles per group, and tiles of big groups (block sums)
   const int gtile = (K + G - 1) / G;
@@ -478,7 +487,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       put(a.bsum2 + blk, tbig);
     }
   }
-  grid_barrier(bar, ++round);
+  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
 
   // ---- tile prefix per group, the group of every tile and the list of big
   // groups' tiles (work units of the pair kernels)
@@ -693,6 +702,7 @@ __device__ __forceinline__ void row_sums(double* arow) {
 
 template <bool BF16>
 __global__ __launch_bounds__(kThreads, 4) void lite_pair_kernel(LiteDev a) {
+  if (a.ctrl[kCtrlAbort]) return;   // the front gave up: its tables are incomplete
   const int lane = threadIdx.x & 63;
   const int gw = blockIdx.x * kWaves + (threadIdx.x >> 6);
   const int nw = gridDim.x * kWaves;
@@ -719,6 +729,7 @@ constexpr int kSplitWaves = 16;
 
 template <bool BF16>
 __global__ __launch_bounds__(kSplitWaves * 64) void lite_pair_split_kernel(LiteDev a) {
+  if (a.ctrl[kCtrlAbort]) return;
   __shared__ double spart[kSplitWaves][kTileRows];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
@@ -757,6 +768,7 @@ __global__ __launch_bounds__(kSplitWaves * 64) void lite_pair_split_kernel(LiteD
 // member of the group from l / 16 on; the four lanes of a row add their sums
 // in a fixed order.
 __global__ __launch_bounds__(kThreads) void lite_b_kernel(LiteDev a) {
+  if (a.ctrl[kCtrlAbort]) return;
   const int lane = threadIdx.x & 63;
   const int row = lane & 15, quad = lane >> 4;
   const int gw = blockIdx.x * kWaves + (threadIdx.x >> 6);
@@ -826,6 +838,13 @@ __global__ __launch_bounds__(kThreads) void lite_select_kernel(LiteDev a) {
   const int lane = threadIdx.x & 63;
   const int q = blockIdx.x * kWaves + (threadIdx.x >> 6);
   if (q >= a.k) return;
+  if (a.ctrl[kCtrlAbort]) {
+    if (lane == 0) {
+      a.selected[q] = -1;
+      a.gcost[q] = __builtin_nan("");
+    }
+    return;
+  }
   const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
   const float m_f = __uint_as_float(a.ctrl[kCtrlMf]);
   const double wf = m_f > 0.f ? double(a.lam_f) / double(m_f) : 0.0;
@@ -835,6 +854,7 @@ __global__ __launch_bounds__(kThreads) void lite_select_kernel(LiteDev a) {
   for (int i = i0 + lane; i < i1; i += 64) {
     const double c = fma(wf, a.A[i], a.B[i]);
     const int tk = perm[i];
+    if (a.token_cost) a.token_cost[tk] = c;
     if (c < best || (c == best && tk < bt)) {
       best = c;
       bt = tk;
@@ -892,6 +912,10 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   a.selected = p.selected;
   a.group = p.group;
   a.objective = p.objective;
+  a.token_cost = p.token_cost;
+  const WaitPolicy wp = wait_policy();
+  a.poll_limit = wp.limit;
+  a.abort_init = wp.preset;
   a.key[0] = reinterpret_cast<unsigned long long*>(w + L.key0);
   a.key[1] = reinterpret_cast<unsigned long long*>(w + L.key1);
   a.tok[0] = reinterpret_cast<int*>(w + L.tok0);

@@ -67,6 +67,9 @@ struct SgsDev {
   unsigned int* strip_cnt;   // [S]
   unsigned int* step_cnt;
   unsigned int* fin_cnt;
+  unsigned int* abort;       // set when the step wait gives up
+  unsigned int poll_limit;   // polls before it gives up (WaitPolicy)
+  unsigned int abort_init;   // the abort flag's value at launch
   int P, S, rows;            // panels, strips, rows per panel
 };
 
@@ -150,6 +153,7 @@ __global__ void sgs_init_kernel(SgsDev a) {
   if (gt == 0) {
     *a.step_cnt = 0u;
     *a.fin_cnt = 0u;
+    *a.abort = a.abort_init;
   }
 }
 
@@ -323,26 +327,39 @@ __global__ __launch_bounds__(BT) void sgs_dense_kernel(SgsDev a) {
       }
       block_arrive<BT>(a.step_cnt, &s_prev);
     }
-    // Wait until every strip has reported, then read the winner.
+    // Wait until every strip has reported, then read the winner; -1 when the
+    // wait gave up, and the block leaves the loop.
     if (tid == 0) {
       const unsigned int target = unsigned(step + 1) * unsigned(a.S);
-      while (get(a.step_cnt) < target) __builtin_amdgcn_s_sleep(1);
-      const unsigned long long kk = __hip_atomic_load(a.key + step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int t = int(kIndexMask - (kk & kIndexMask));
-      s_t = t;
-      const int ts = t / kStrip;
-      if (int(blockIdx.x) == ts % int(gridDim.x)) put(a.mask + t, 1u);   // owner of item (0, ts)
-      if (blockIdx.x == 0) {
-        a.selected[step] = t;
-        if (a.step_gain) a.step_gain[step] = get(a.strip_g + ts);
+      bool ok = true;
+      for (unsigned int spins = 0; get(a.step_cnt) < target; ++spins) {
+        if (give_up(spins, a.poll_limit, a.abort)) {
+          ok = false;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
       }
+      int t = -1;
+      if (ok) {
+        const unsigned long long kk = __hip_atomic_load(a.key + step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        t = int(kIndexMask - (kk & kIndexMask));
+        const int ts = t / kStrip;
+        if (int(blockIdx.x) == ts % int(gridDim.x)) put(a.mask + t, 1u);   // owner of item (0, ts)
+        if (blockIdx.x == 0) {
+          a.selected[step] = t;
+          if (a.step_gain) a.step_gain[step] = get(a.strip_g + ts);
+        }
+      }
+      s_t = t;
     }
     __syncthreads();
     tprev = s_t;
+    if (tprev < 0) break;
   }
 
-  // Apply the last pick: assignment and the final objective.
-  for (int it = blockIdx.x; it < items; it += gridDim.x) {
+  // Apply the last pick: assignment and the final objective (not when the
+  // launch gave up; tprev is the same in every thread of the block).
+  for (int it = blockIdx.x; tprev >= 0 && it < items; it += gridDim.x) {
     const int panel = it / a.S, strip = it - panel * a.S;
     if (strip != 0) continue;
     const int j0 = panel * a.rows, j1 = min(a.n, j0 + a.rows);
@@ -358,7 +375,7 @@ __global__ __launch_bounds__(BT) void sgs_dense_kernel(SgsDev a) {
     if (tid == 0) put(a.obj_part + panel, s);
   }
   const unsigned int fprev = block_arrive<BT>(a.fin_cnt, &s_prev);
-  if (fprev == gridDim.x - 1u && a.step_obj) {
+  if (fprev == gridDim.x - 1u && a.step_obj && !get(a.abort)) {
     double x = 0.0;
     for (int p = tid; p < a.P; p += BT) x += get(a.obj_part + p);
     const double s = block_sum<BT>(x, sd);
@@ -420,6 +437,10 @@ hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream) {
   a.strip_cnt = reinterpret_cast<unsigned int*>(w + L.strip_cnt);
   a.step_cnt = reinterpret_cast<unsigned int*>(w + L.ctrl);
   a.fin_cnt = reinterpret_cast<unsigned int*>(w + L.ctrl + 4);
+  a.abort = reinterpret_cast<unsigned int*>(w + L.ctrl + 8);
+  const WaitPolicy wp = wait_policy();
+  a.poll_limit = wp.limit;
+  a.abort_init = wp.preset;
   a.P = P;
   a.S = S;
   a.rows = rows;
@@ -429,7 +450,8 @@ hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream) {
   void* args[] = {&a};
   const void* fn = vec4 ? reinterpret_cast<const void*>(sgs_dense_kernel<kBlock, true>)
                         : reinterpret_cast<const void*>(sgs_dense_kernel<kBlock, false>);
-  return hipLaunchCooperativeKernel(fn, dim3(grid), dim3(kBlock), args, 0, stream);
+  if ((e = hipLaunchCooperativeKernel(fn, dim3(grid), dim3(kBlock), args, 0, stream)) != hipSuccess) return e;
+  return launch_mark_aborted(a.abort, a.selected, a.k, stream);
 }
 
 }  // namespace cp

@@ -104,7 +104,7 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   for (int step = 0; step < a.k; ++step) {
     // Some block has a candidate while unchosen columns remain; the clamp
     // only keeps a broken slot from addressing past the matrix.
-    const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
+    const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, a.poll_limit, su, &sflag);
     if (tw < 0) break;
     if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
       long long L = 0;
@@ -168,7 +168,8 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
       if (tid < nb) {
         unsigned long long x;
         const unsigned int round = unsigned(step + 1);
-        if (wait_slot(lens_slot(a.lens, tid), a.abort, [round](unsigned long long v) { return (v >> 32) == round; }, x))
+        if (wait_slot(lens_slot(a.lens, tid), a.abort, a.poll_limit,
+                      [round](unsigned long long v) { return (v >> 32) == round; }, x))
           c = int(x & 0xffffffffull);
         else
           slflag = 1;
@@ -274,8 +275,6 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
     for (int q = 0; q < kWaves; ++q) L += sLw[q];
     a.step_obj[obj_step] = fx_to_double(L, S);
   }
-  if (blk == 0 && get(a.abort))
-    for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
 }
 
 // ---------------------------------------------------------------------------
@@ -373,7 +372,8 @@ __device__ __forceinline__ long long key_gain_floor(unsigned long long key, int 
 // i's slot and stores them (epoch bits cleared) in sk1 and sk2.  Returns the
 // winner's index, -1 when the launch is aborting.
 __device__ int read_winner_rows(const unsigned long long* slots, unsigned long long epoch, int nb, unsigned int* abort,
-                                unsigned long long* su, int* sflag, unsigned long long* sk1, unsigned long long* sk2) {
+                                unsigned int limit, unsigned long long* su, int* sflag, unsigned long long* sk1,
+                                unsigned long long* sk2) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   unsigned long long best = 0ull;
   if (tid == 0) *sflag = 0;
@@ -389,16 +389,9 @@ __device__ int read_winner_rows(const unsigned long long* slots, unsigned long l
         sk2[tid] = x1 & ~kEpoch;
         done = true;
       } else {
-        if ((spins & 63u) == 63u) {
-          if (get(abort)) {
-            *sflag = 1;
-            break;
-          }
-          if (spins > kSpinLimit) {
-            put(abort, 1u);
-            *sflag = 1;
-            break;
-          }
+        if (give_up(spins, limit, abort)) {
+          *sflag = 1;
+          break;
         }
         __builtin_amdgcn_s_sleep(1);
       }
@@ -501,8 +494,9 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
       __syncthreads();
       tw = tpred;
     } else {
-      tw = kSpec ? read_winner_rows(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, su, &sflag, sk1, sk2)
-                 : read_winner(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, su, &sflag);
+      tw = kSpec ? read_winner_rows(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, a.poll_limit, su,
+                                    &sflag, sk1, sk2)
+                 : read_winner(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, a.poll_limit, su, &sflag);
       ++xc;
     }
     if (tw < 0) break;
@@ -834,8 +828,6 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     for (int q = 0; q < kWaves; ++q) L += sLw[q];
     a.step_obj[obj_step] = fx_to_double(L, S);
   }
-  if (blk == 0 && get(a.abort))
-    for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
 }
 
 __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) { inc_body(a, blockIdx.x, gridDim.x); }
@@ -1017,6 +1009,9 @@ IncDev inc_dev(const SgsParams& p, char* w, int W, bool rows) {
   a.lens = reinterpret_cast<unsigned long long*>(w + L.lens);
   a.cand = reinterpret_cast<unsigned long long*>(w + L.cand);
   a.abort = reinterpret_cast<unsigned int*>(w + L.ctrl);
+  const WaitPolicy wp = wait_policy();
+  a.poll_limit = wp.limit;
+  a.abort_init = wp.preset;
   a.W = W;
   const IncLayout M = inc_layout(p.n, p.k, !rows);
   a.T = rows ? reinterpret_cast<float*>(w + M.T) : nullptr;
@@ -1071,7 +1066,8 @@ hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t 
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = launch_first_pass(a, nb, stream)) != hipSuccess) return e;
   void* args[] = {&a};
-  return hipLaunchCooperativeKernel(kernel, dim3(nb), dim3(kBlock), args, lds, stream);
+  if ((e = hipLaunchCooperativeKernel(kernel, dim3(nb), dim3(kBlock), args, lds, stream)) != hipSuccess) return e;
+  return launch_mark_aborted(a.abort, a.selected, a.k, stream);
 }
 
 size_t sgs_inc_batch_workspace_bytes(const int64_t* n, const int64_t* k, int count, bool compact) {
@@ -1141,7 +1137,10 @@ hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, bool comp
     if ((e = launch_first_pass(b.scene[s], b.g0[s + 1] - b.g0[s], stream)) != hipSuccess) return e;
   }
   void* args[] = {&b};
-  return hipLaunchCooperativeKernel(kernel, dim3(used), dim3(kBlock), args, lds, stream);
+  if ((e = hipLaunchCooperativeKernel(kernel, dim3(used), dim3(kBlock), args, lds, stream)) != hipSuccess) return e;
+  for (int s = 0; s < count; ++s)
+    if ((e = launch_mark_aborted(b.scene[s].abort, b.scene[s].selected, b.scene[s].k, stream)) != hipSuccess) return e;
+  return hipSuccess;
 }
 
 }  // namespace cp

@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
 
   const int nch = a.ldt / kChunkT;
   for (int step = 0; step < a.k; ++step) {
-    const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, su, &sflag);
+    const int tw = read_winner(cand_slot(a.cand, step & 1, 0), epoch_of(step), nb, a.abort, a.poll_limit, su, &sflag);
     if (tw < 0) break;
     const int t = min(tw, a.n - 1);
     if (t >= lo && t < lo + cnt && tid == 0) {
@@ -245,9 +245,6 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
                      epoch_of(step + 1), sg, si);
     }
   }
-  __syncthreads();
-  if (blk == 0 && get(a.abort))
-    for (int s = tid; s < a.k; s += kBlock) a.selected[s] = -1;
 }
 
 // L(S) after step l: the blocks' parts added in block order.
@@ -314,6 +311,9 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
   a.lens = reinterpret_cast<unsigned long long*>(w + X.lens);
   a.cand = reinterpret_cast<unsigned long long*>(w + X.cand);
   a.abort = reinterpret_cast<unsigned int*>(w + X.ctrl);
+  const WaitPolicy wp = wait_policy();
+  a.poll_limit = wp.limit;
+  a.abort_init = wp.preset;
   a.W = W;
   a.T = reinterpret_cast<float*>(w + Y.T);
   a.ldt = ldt;
@@ -331,6 +331,7 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
   if ((e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_local_kernel), dim3(nb), dim3(kBlock), args,
                                       lds, stream)) != hipSuccess)
     return e;
+  if ((e = launch_mark_aborted(a.abort, a.selected, a.k, stream)) != hipSuccess) return e;
   if (p.step_objective) {
     local_objective_kernel<<<(p.k + 255) / 256, 256, 0, stream>>>(d.part, nb, p.k, d.scale, p.step_objective);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -124,6 +124,7 @@ struct LiteParams {
   int32_t* selected;              // [k]
   int32_t* group;                 // [n] or nullptr
   double* objective;              // [1] or nullptr
+  double* token_cost;             // [n] or nullptr
   void* workspace;
   size_t workspace_bytes;
 };

@@ -36,10 +36,9 @@ constexpr int kIndexBits = 20;     // candidate: [epoch | 43-bit gain | 20-bit i
 constexpr unsigned long long kIndexMask = (1ull << kIndexBits) - 1ull;
 constexpr unsigned long long kEpoch = 1ull << 63;
 constexpr unsigned long long kNoCandidate = 1ull;   // below every real candidate
-// Every wait in the kernel is bounded: about a second of polling (far beyond
-// any legitimate wait) raises the abort flag, after which every block leaves
-// its waits and returns, and selected[] is filled with -1.
-constexpr unsigned int kSpinLimit = 1u << 22;
+// Every wait in the kernel is bounded (give_up in common.h): a wait that
+// gives up raises the abort flag, every block leaves its waits and returns,
+// and a kernel after the launch fills selected[] with -1.
 
 // Fixed-point value of a nonnegative term: floor(t 2^S) as a 64-bit
 // integer, for t 2^S < 2^62 (the scale S is chosen so that every gain and
@@ -81,7 +80,9 @@ struct IncDev {
   unsigned long long* list;   // [blocks][W][2]: (row | v << 32), (old b | new b << 32)
   unsigned long long* lens;   // [blocks] (step + 1) << 32 | slice length
   unsigned long long* cand;   // [2][blocks] packed candidate | epoch << 63
-  unsigned int* abort;        // set when a wait exceeds kSpinLimit polls
+  unsigned int* abort;        // set when a wait gives up
+  unsigned int poll_limit;    // polls before a wait gives up (WaitPolicy)
+  unsigned int abort_init;    // the abort flag's value at launch (WaitPolicy)
   int W;                      // rows and columns per block
   float* T;                   // rows form only: [n][ldt] source-major copy, T[s][t] = C(s, t)
   int ldt;                    // its row stride, n rounded up to a whole 256-row chunk
@@ -150,7 +151,7 @@ __global__ void sgs_inc_init_kernel(IncDev a) {
   }
   for (int j = gt; j < a.n; j += nt)
     if (a.assign) a.assign[j] = -1;
-  if (gt == 0) *a.abort = 0u;
+  if (gt == 0) *a.abort = a.abort_init;
 }
 
 // Wave reductions without LDS traffic: DPP moves within each row of 16
@@ -252,19 +253,14 @@ __device__ long long block_sum_i64(long long x, long long* sg) {
 }
 
 // Poll *p until pred(value) holds; false if the launch is aborting (this
-// wait timed out, or another one did).
+// wait gave up, or another one did).
 template <class Pred>
-__device__ bool wait_slot(const unsigned long long* p, unsigned int* abort, Pred pred, unsigned long long& x) {
+__device__ bool wait_slot(const unsigned long long* p, unsigned int* abort, unsigned int limit, Pred pred,
+                          unsigned long long& x) {
   for (unsigned int spins = 0;; ++spins) {
     x = get(p);
     if (pred(x)) return true;
-    if ((spins & 63u) == 63u) {
-      if (get(abort)) return false;
-      if (spins > kSpinLimit) {
-        put(abort, 1u);
-        return false;
-      }
-    }
+    if (give_up(spins, limit, abort)) return false;
     __builtin_amdgcn_s_sleep(1);
   }
 }
@@ -360,14 +356,15 @@ __device__ __forceinline__ void publish_argmax(const long long* sG, const unsign
 // epoch; the largest wins (the same in every block).  Returns -1 when the
 // launch is aborting.
 __device__ int read_winner(const unsigned long long* slots, unsigned long long epoch, int nb,
-                           unsigned int* abort, unsigned long long* su, int* sflag) {
+                           unsigned int* abort, unsigned int limit, unsigned long long* su, int* sflag) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   unsigned long long best = 0ull;
   if (tid == 0) *sflag = 0;
   __syncthreads();
   if (tid < nb) {
     unsigned long long x;
-    if (wait_slot(slots + size_t(tid) * kSlotStride, abort, [epoch](unsigned long long v) { return (v & kEpoch) == epoch; }, x))
+    if (wait_slot(slots + size_t(tid) * kSlotStride, abort, limit,
+                  [epoch](unsigned long long v) { return (v & kEpoch) == epoch; }, x))
       best = x & ~kEpoch;
     else
       *sflag = 1;

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.coverprune_abi_version() == 1
+    assert lib.coverprune_abi_version() == 2
     for code, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported"),
                        (3, b"workspace too small"), (4, b"HIP runtime error")]:
         assert lib.coverprune_status_string(code) == text
@@ -112,10 +112,10 @@ def test_sgs_rejects(lib, kw, code):
 
 def _lite(lib, **kw):
     a = dict(feats=FAKE, dtype=1, n=64, d=64, pos=FAKE, frame=FAKE, v=FAKE, k=8, w=_w(), h=0.25,
-             sel=FAKE, group=None, obj=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
+             sel=FAKE, group=None, obj=None, tcost=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
     a.update(kw)
     return lib.coverprune_lite_select(a["feats"], a["dtype"], a["n"], a["d"], a["pos"], a["frame"], a["v"],
-                                      a["k"], a["w"], a["h"], a["sel"], a["group"], a["obj"], a["ws"],
+                                      a["k"], a["w"], a["h"], a["sel"], a["group"], a["obj"], a["tcost"], a["ws"],
                                       a["ws_bytes"], a["stream"])
 
 
@@ -127,6 +127,26 @@ def _lite(lib, **kw):
 ])
 def test_lite_rejects(lib, kw, code):
     assert _lite(lib, **kw) == code
+
+
+def test_uncovered_cost_is_the_largest_cost(lib):
+    # c0 = (lambda_f + lambda_x) + lambda_tau in float arithmetic: every term of
+    # Eq. 8 is at most its weight once normalised.
+    import paper_2608_13226_amd as cp
+    assert lib.coverprune_uncovered_cost(cp._Weights(1.0, 1.0, 1.0, 10.0)) == 3.0
+    assert lib.coverprune_uncovered_cost(cp._Weights(0.5, 2.0, 0.25, 0.0)) == 2.75
+    x = lib.coverprune_uncovered_cost(cp._Weights(0.1, 0.2, 0.3, 1.0))
+    f = ctypes.c_float
+    assert x == f(f(f(0.1).value + f(0.2).value).value + f(0.3).value).value
+    assert cp.uncovered_cost((1.0, 1.0, 1.0)) == 3.0
+
+
+def test_binding_rejects_a_library_of_another_abi(monkeypatch):
+    import paper_2608_13226_amd as cp
+    monkeypatch.setattr(cp, "_lib", None)
+    monkeypatch.setattr(cp, "ABI_VERSION", 1)
+    with pytest.raises(cp.CoverPruneError, match="ABI"):
+        cp.library()
 
 
 def test_binding_needs_the_library(monkeypatch, tmp_path):

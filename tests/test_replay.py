@@ -92,3 +92,12 @@ def test_oracle_cost_full_is_the_oracle():
     C, m = parity.oracle_cost_full(s, block=100)
     C2, m2 = parity.oracle_cost(s)
     assert np.array_equal(C, C2) and m == m2
+
+
+def test_threaded_neighbour_table_is_the_oracle():
+    from oracle import capacity
+    from scenes import make_scene
+    s = make_scene("n1024_d256_f32", 2)
+    a = parity.oracle_neighbours_excluding_self(s.pos, 8, block=100)
+    b = capacity.neighbours_excluding_self(s.pos, 8)
+    assert np.array_equal(a, b)
