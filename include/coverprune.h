@@ -253,6 +253,32 @@ cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count,
                                       void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* The greedy without a workspace, for callers that cannot allocate memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).
+ *
+ * coverprune_sgs_select with flags CP_SGS_INCREMENTAL | CP_SGS_COMPACT (the
+ * same kernels, so the same result bit for bit), its scratch space taken
+ * from a device array inside the library instead of a workspace argument:
+ * about 1.5 MiB, one copy per GPU, held until the process ends.  The call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine).
+ * Its first call on a device looks up that device's copy of the array, with
+ * the device current.
+ *
+ *   cost, n, capacity, k, c0, selected, step_gain, step_objective, assign:
+ *             as for coverprune_sgs_select; n <= CP_SGS_NOALLOC_MAX_N (larger
+ *             scenes return CP_ERR_INVALID_ARG before anything is enqueued)
+ * Every call on one GPU uses that GPU's single scratch array, which keeps
+ * the last call's contents (each call clears what must start at zero):
+ * calls that overlap on one GPU, on different streams or from different
+ * threads, race and give undefined results.  Serialise them.
+ */
+#define CP_SGS_NOALLOC_MAX_N 32768
+cp_status coverprune_sgs_select_noalloc(const float* cost, int64_t n, const float* capacity, int64_t k, float c0,
+                                        int32_t* selected, double* step_gain, double* step_objective,
+                                        int32_t* assign, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Spatially local greedy (Sec. 3.5, Eq. 13).
  *
  * The same greedy with each candidate's gain restricted to its neighbour set

@@ -150,6 +150,8 @@ def library() -> ctypes.CDLL:
     lib.coverprune_last_error.restype = ctypes.c_char_p
     lib.coverprune_abi_version.argtypes = []
     lib.coverprune_abi_version.restype = ctypes.c_int
+    lib.coverprune_sgs_select_noalloc.argtypes = [vp, i64, vp, i64, ctypes.c_float, vp, vp, vp, vp, vp]
+    lib.coverprune_sgs_select_noalloc.restype = st
     lib.coverprune_uncovered_cost.argtypes = [_Weights]
     lib.coverprune_uncovered_cost.restype = ctypes.c_float
     if lib.coverprune_abi_version() != ABI_VERSION:

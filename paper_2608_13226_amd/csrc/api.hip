@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "../../include/coverprune.h"
@@ -236,6 +237,85 @@ cp_status coverprune_sgs_select_batch(const cp_sgs_scene* scenes, int32_t count,
   hipError_t e = cp::launch_sgs_incremental_batch(p, int(count), (flags & CP_SGS_COMPACT) != 0, workspace,
                                                   static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "sgs batch");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// The greedy without a workspace argument, for callers that cannot allocate.
+// Its scratch space is one file-scope device array: each GPU the library runs
+// on holds its own copy until the process ends.  In host code the array's
+// name is not a device address, so the address is looked up once per device
+// (hipGetSymbolAddress, with that device current) and only that address is
+// ever handed to kernels.
+
+}  // extern "C"
+
+namespace {
+
+// The compact schedule's workspace at CP_SGS_NOALLOC_MAX_N tokens is about
+// 1.35 MiB (change list, exchange slots, step-0 partial gains); the array is
+// a little larger and every call checks the exact need against it.
+constexpr size_t kNoallocBytes = size_t(3) << 19;   // 1.5 MiB
+__device__ __align__(256) unsigned char scratch[kNoallocBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up on its first use.
+cp_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(CP_ERR_UNSUPPORTED, "device %d outside the %d devices the scratch table covers", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(CP_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return CP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cp_status coverprune_sgs_select_noalloc(const float* cost, int64_t n, const float* capacity, int64_t k, float c0,
+                                        int32_t* selected, double* step_gain, double* step_objective,
+                                        int32_t* assign, void* stream) {
+  if (n < 1 || n > CP_SGS_NOALLOC_MAX_N)
+    return fail(CP_ERR_INVALID_ARG, "n = %lld outside [1, %d] (the no-allocation greedy's scratch limit)",
+                (long long)n, CP_SGS_NOALLOC_MAX_N);
+  if (k < 1 || k > n) return fail(CP_ERR_INVALID_ARG, "k = %lld outside [1, n = %lld]", (long long)k, (long long)n);
+  if (!std::isfinite(c0)) return fail(CP_ERR_INVALID_ARG, "c0 must be finite");
+  if (!cost || !capacity || !selected) return fail(CP_ERR_INVALID_ARG, "cost, capacity and selected must be non-NULL");
+  if (!aligned16(cost)) return fail(CP_ERR_INVALID_ARG, "cost is not 16-byte aligned");
+  const size_t need = cp::sgs_inc_workspace_bytes(n, k, true);
+  if (need > kNoallocBytes)
+    return fail(CP_ERR_UNSUPPORTED, "scene needs %zu bytes of scratch, %zu available", need, kNoallocBytes);
+  void* ws = nullptr;
+  cp_status st = scratch_of_current_device(&ws);
+  if (st != CP_OK) return st;
+
+  cp::SgsParams p;
+  p.cost = cost;
+  p.n = int(n);
+  p.capacity = capacity;
+  p.k = int(k);
+  p.c0 = c0;
+  p.selected = selected;
+  p.step_gain = step_gain;
+  p.step_objective = step_objective;
+  p.assign = assign;
+  p.workspace = ws;
+  p.workspace_bytes = kNoallocBytes;
+  hipError_t e = cp::launch_sgs_incremental(p, true, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sgs noalloc");
   return ok();
 }
 

@@ -129,6 +129,19 @@ def test_lite_rejects(lib, kw, code):
     assert _lite(lib, **kw) == code
 
 
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), INVALID), (dict(n=32769), INVALID), (dict(k=0), INVALID), (dict(k=65), INVALID),
+    (dict(cost=None), INVALID), (dict(cap=None), INVALID), (dict(sel=None), INVALID),
+    (dict(c0=float("nan")), INVALID), (dict(cost=ctypes.c_void_p(0x1004)), INVALID),
+])
+def test_sgs_noalloc_rejects(lib, kw, code):
+    # Host checks only: every rejection happens before the device is touched.
+    a = dict(cost=FAKE, n=64, cap=FAKE, k=8, c0=3.0, sel=FAKE)
+    a.update(kw)
+    assert lib.coverprune_sgs_select_noalloc(a["cost"], a["n"], a["cap"], a["k"], ctypes.c_float(a["c0"]), a["sel"],
+                                             None, None, None, None) == code
+
+
 def test_uncovered_cost_is_the_largest_cost(lib):
     # c0 = (lambda_f + lambda_x) + lambda_tau in float arithmetic: every term of
     # Eq. 8 is at most its weight once normalised.
