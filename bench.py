@@ -56,6 +56,9 @@ def _args():
     ap.add_argument("--batch-scenes", type=int, default=4,
                     help="scenes of the paper's 6272-token shape whose greedies are timed one by one and "
                          "batched (0 to skip)")
+    ap.add_argument("--dump-maps", default="",
+                    help="write this process's memory map (/proc/self/maps) to this file just before exit, so "
+                         "that addresses in a crash report from process teardown name their libraries")
     ap.add_argument("--ceilings", action="store_true",
                     help="only measure the achievable ceilings: a 1 GiB device-to-device copy (also the "
                          "calibration kernel for the HBM byte counters) and a 16384 x 3584 x 16384 bf16 "
@@ -182,7 +185,10 @@ def cpu_baseline(scene, lite_h):
 
 def time_lite(name, seed, reps, dev):
     """CoverPrune-Lite alone on its own workload: HIP-event time per call and
-    the feature stream's share of HBM peak (features are read once)."""
+    the feature stream's share of HBM peak (features are read once).  Timed
+    with the workload's own capacities (the FST capacity of Eq. 9-10 from
+    coverprune_fst_capacity, computed before the timed calls, where the
+    workload names it) and with the generator's uniform capacities."""
     import numpy as np
     import torch
 
@@ -195,23 +201,40 @@ def time_lite(name, seed, reps, dev):
     lib = cp.library()
     dt = cp.CP_BF16 if scene.dtype == "bf16" else cp.CP_F32
     ws = torch.empty(lib.coverprune_lite_workspace(scene.n, scene.dim, scene.k, dt), dtype=torch.uint8, device=dev)
-    run = lambda: cp.lite_select(t["feats"], t["pos"], t["frame"], t["capacity"], scene.k,
-                                 voxel_size=cfg.voxel or 0.25, workspace=ws)
-    run()
-    torch.cuda.synchronize()
-    e0 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
-    e1 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
-    for i in range(reps):
-        e0[i].record()
-        run()
-        e1[i].record()
-    torch.cuda.synchronize()
-    ms = float(np.mean([a.elapsed_time(b) for a, b in zip(e0, e1)]))
+    caps = {cfg.capacity: t["capacity"]}
+    cap_ms = None
+    if cfg.fst_capacity_nn:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        v, _ = cp.fst_capacity(t["feats"], t["pos"], t["frame"], cfg.fst_capacity_nn)
+        e1.record()
+        torch.cuda.synchronize()
+        cap_ms = e0.elapsed_time(e1)
+        caps = {f"fst{cfg.fst_capacity_nn}": v, **caps}
     feat_bytes = float(scene.n) * scene.dim * (2 if scene.dtype == "bf16" else 4)
+    runs = {}
+    for key, cap in caps.items():
+        run = lambda: cp.lite_select(t["feats"], t["pos"], t["frame"], cap, scene.k,
+                                     voxel_size=cfg.voxel or 0.25, workspace=ws)
+        r = run()
+        torch.cuda.synchronize()
+        sizes = torch.bincount(r.group.long()).cpu().numpy()
+        e0 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+        e1 = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+        for i in range(reps):
+            e0[i].record()
+            run()
+            e1[i].record()
+        torch.cuda.synchronize()
+        ms = float(np.mean([a.elapsed_time(b) for a, b in zip(e0, e1)]))
+        runs[key] = {"ms_per_scene": round(ms, 4), "group_sizes": [int(sizes.min()), int(sizes.max())],
+                     "hbm": {"achieved": round(feat_bytes / (ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                             "unit": "GB/s", "bytes": feat_bytes,
+                             "note": "features read once; whole call timed"}}
+    first = next(iter(runs))
     return {"workload": name, "n": scene.n, "d": scene.dim, "k": scene.k, "voxel_m": cfg.voxel,
-            "ms_per_scene": round(ms, 4),
-            "hbm": {"achieved": round(feat_bytes / (ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "bytes": feat_bytes, "note": "features read once; whole call timed"}}
+            "capacity": first, "ms_per_scene": runs[first]["ms_per_scene"], "hbm": runs[first]["hbm"],
+            "by_capacity": runs, "fst_capacity_ms": None if cap_ms is None else round(cap_ms, 3)}
 
 
 def main():
@@ -358,6 +381,32 @@ def main():
     else:
         roofline = {key: dense[key] for key in ("bound", "achieved", "peak", "unit", "frac", "traffic", "kernel")}
         roofline.update({"bytes_per_launch": dense_bytes, "ms_per_launch": round(dense_ms, 3)})
+
+    # The latency floor of a greedy step on this device: the candidate
+    # exchange alone, and followed by the dependent read of the row the
+    # winner names (coverprune_step_floor: the greedy's launch shape, slots,
+    # waits and loads, nothing else), over the cost's rows.  A step of the
+    # rows schedule does both (or only the read, when its winner was
+    # predicted), then applies the targets the pick improves.
+    ws_floor = torch.empty(lib.coverprune_step_floor_workspace(), dtype=torch.uint8, device=dev)
+    floor_rounds = 4096
+
+    def floor_us(read_rows):
+        cp.step_floor(cost, 64, read_rows=read_rows, workspace=ws_floor)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        cp.step_floor(cost, floor_rounds, read_rows=read_rows, workspace=ws_floor)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / floor_rounds
+
+    exch_us, step_floor_us = floor_us(False), floor_us(True)
+    roofline["latency_floor"] = {
+        "exchange_us": round(exch_us, 3), "exchange_and_row_read_us": round(step_floor_us, 3),
+        "greedy_us_per_step": round(s_ms * 1e3 / k, 3),
+        "greedy_over_floor": round(s_ms * 1e3 / k / step_floor_us, 3), "rounds": floor_rounds,
+        "note": "coverprune_step_floor: rounds of the greedy's candidate exchange (+ the dependent read of the "
+                "winner's 64 KB row); greedy_us_per_step is the whole sgs_select call over K"}
 
     # Local greedy (Eq. 13) on the same cost: the g-nearest tables, then the
     # greedy with gains over each candidate's table row.  The paper leaves g
@@ -528,4 +577,27 @@ def main():
 
 
 if __name__ == "__main__":
+    _a = _args()
+    if _a.dump_maps:
+        import atexit
+
+        def _dump_maps(path=_a.dump_maps):
+            with open("/proc/self/maps") as src, open(path, "w") as dst:
+                dst.write(src.read())
+
+        atexit.register(_dump_maps)
     main()
+    # Leave no device work or memory of ours to process teardown (the HIP
+    # runtime's and a profiler's exit handlers): every tensor of main() is
+    # gone once it returns, and torch's cache goes back to the runtime.
+    if "torch" in sys.modules:
+        import gc
+
+        import torch
+        if torch.cuda.is_initialized():
+            torch.cuda.synchronize()
+            gc.collect()
+            torch.cuda.empty_cache()
+            torch.cuda.synchronize()
+    sys.stdout.flush()
+    sys.stderr.flush()

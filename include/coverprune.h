@@ -123,7 +123,7 @@ cp_status coverprune_fst_cost(const void* feats, cp_dtype dtype, int64_t n, int6
 
 /* Largest scene and neighbour count of the 3D nearest-neighbour tables
  * (coverprune_knn, coverprune_fst_capacity). */
-#define CP_KNN_MAX_N 16384
+#define CP_KNN_MAX_N 32768
 #define CP_KNN_MAX_G 1024
 
 /* ------------------------------------------------------------------------ */
@@ -408,6 +408,29 @@ cp_status coverprune_lite_select(const void* feats, cp_dtype dtype, int64_t n, i
                                  int64_t k, cp_fst_weights w, float voxel_size, int32_t* selected,
                                  int32_t* group, double* objective, double* token_cost, void* workspace,
                                  size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Measurement: the latency floor of one greedy step on this device (Sec. 3.5).
+ *
+ * A step of coverprune_sgs_select's rows schedule cannot avoid two dependent
+ * operations: the exchange in which every block publishes its best candidate
+ * and reads every other block's, and the read of the winner's row of the
+ * source-major cost (4 n bytes) that tells every block which targets the
+ * pick improves.  This call runs `rounds` rounds of exactly those, with the
+ * greedy's launch shape for a scene of n_rows tokens and its own slots,
+ * waits and loads, and nothing else; each round's published key depends on
+ * the previous round's row.  The call's duration divided by `rounds` is a
+ * floor for a greedy step; with read_rows = 0 only the exchange runs.
+ *
+ *   rows      [n_rows, row_len] float device buffer, any contents (a cost
+ *             matrix serves); row_len % 256 == 0, 256 <= row_len <= 32768
+ *   rounds    >= 1
+ *   workspace coverprune_step_floor_workspace() bytes (exchange slots)
+ * Waits are bounded as in the greedy.
+ */
+size_t coverprune_step_floor_workspace(void);
+cp_status coverprune_step_floor(const float* rows, int64_t n_rows, int64_t row_len, int32_t rounds,
+                                int32_t read_rows, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 const char* coverprune_status_string(cp_status status); /* static text, never NULL */

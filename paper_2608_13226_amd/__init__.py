@@ -24,7 +24,7 @@ from typing import Optional
 import torch
 
 __all__ = ["fst_cost", "fst_capacity", "sgs_select", "sgs_select_batch", "sgs_literal_select", "knn",
-           "sgs_local_select", "lite_select", "uncovered_cost", "library", "library_path", "CoverPruneError",
+           "sgs_local_select", "lite_select", "uncovered_cost", "step_floor", "library", "library_path", "CoverPruneError",
            "DEFAULT_KAPPA"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -152,6 +152,10 @@ def library() -> ctypes.CDLL:
     lib.coverprune_abi_version.restype = ctypes.c_int
     lib.coverprune_sgs_select_noalloc.argtypes = [vp, i64, vp, i64, ctypes.c_float, vp, vp, vp, vp, vp]
     lib.coverprune_sgs_select_noalloc.restype = st
+    lib.coverprune_step_floor_workspace.argtypes = []
+    lib.coverprune_step_floor_workspace.restype = sz
+    lib.coverprune_step_floor.argtypes = [vp, i64, i64, ctypes.c_int32, ctypes.c_int32, vp, sz, vp]
+    lib.coverprune_step_floor.restype = st
     lib.coverprune_uncovered_cost.argtypes = [_Weights]
     lib.coverprune_uncovered_cost.restype = ctypes.c_float
     if lib.coverprune_abi_version() != ABI_VERSION:
@@ -401,6 +405,22 @@ def sgs_literal_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, epsil
                                              _ptr(resid) if keep else None, _ptr(obj), _ptr(workspace),
                                              workspace.numel(), _stream(stream)))
     return LiteralResult(sel, score, resid, obj)
+
+
+def step_floor(rows: torch.Tensor, rounds: int, read_rows: bool = True, workspace: Optional[torch.Tensor] = None,
+               stream=None) -> None:
+    """Enqueue `rounds` rounds of the greedy's candidate exchange, each
+    followed (read_rows) by the read of the row of ``rows`` [n, row_len]
+    float32 that the round's winner names: the latency floor of a greedy
+    step (coverprune_step_floor).  Time it with events on the stream."""
+    lib = library()
+    if rows.dim() != 2:
+        raise ValueError("rows must be [n, row_len]")
+    _need(rows, "rows", torch.float32, tuple(rows.shape), rows.device)
+    if workspace is None:
+        workspace = _workspace(lib.coverprune_step_floor_workspace(), rows.device)
+    _check(lib.coverprune_step_floor(_ptr(rows), rows.shape[0], rows.shape[1], int(rounds), int(bool(read_rows)),
+                                     _ptr(workspace), workspace.numel(), _stream(stream)))
 
 
 def knn(pos: torch.Tensor, g: int, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:

@@ -320,6 +320,26 @@ cp_status coverprune_sgs_select_noalloc(const float* cost, int64_t n, const floa
 }
 
 // ---------------------------------------------------------------------------
+size_t coverprune_step_floor_workspace(void) { return cp::step_floor_workspace_bytes(); }
+
+cp_status coverprune_step_floor(const float* rows, int64_t n_rows, int64_t row_len, int32_t rounds,
+                                int32_t read_rows, void* workspace, size_t workspace_bytes, void* stream) {
+  if (n_rows < 1 || n_rows > kMaxDenseN)
+    return fail(CP_ERR_INVALID_ARG, "n_rows = %lld outside [1, %lld]", (long long)n_rows, (long long)kMaxDenseN);
+  if (row_len < 256 || row_len > 32768 || row_len % 256 != 0)
+    return fail(CP_ERR_INVALID_ARG, "row_len = %lld must be a multiple of 256 in [256, 32768]", (long long)row_len);
+  if (rounds < 1) return fail(CP_ERR_INVALID_ARG, "rounds = %d must be >= 1", (int)rounds);
+  if (!rows) return fail(CP_ERR_INVALID_ARG, "rows is NULL");
+  if (!aligned16(rows)) return fail(CP_ERR_INVALID_ARG, "rows is not 16-byte aligned");
+  cp_status st = check_workspace(workspace, workspace_bytes, coverprune_step_floor_workspace());
+  if (st != CP_OK) return st;
+  hipError_t e = cp::launch_step_floor(rows, int(n_rows), int(row_len), int(rounds), read_rows != 0, workspace,
+                                       static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "step floor");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
 size_t coverprune_sgs_literal_workspace(int64_t n, int64_t k) {
   if (n < 1 || k < 1 || k > n) return 0;
   return cp::sgs_literal_workspace_bytes(n, k);

@@ -14,11 +14,13 @@
 //    <= U, which hold every member of M_g together with all keys tied with
 //    the g-th, and ranks them by (key, index).  A row whose collection
 //    overflows kCap is marked with -1 in its first entry.
-//  - knn_radix_kernel, one row at a time per block with all n keys in LDS: an
-//    8-bit radix select over the key's eight bytes finds the g-th smallest key
-//    T and how many keys equal to T belong to the answer; the tokens below T,
-//    and the first tokens equal to T in index order, are collected and ranked.
-//    It serves g > kBoundMaxG and the rows the first kernel marked.
+//  - knn_radix_kernel, one row at a time per block with all n keys in LDS
+//    (n <= kKnnLdsN; for larger n each pass recomputes the keys from the
+//    positions, which stay in L2): an 8-bit radix select over the key's eight
+//    bytes finds the g-th smallest key T and how many keys equal to T belong
+//    to the answer; the tokens below T, and the first tokens equal to T in
+//    index order, are collected and ranked.  It serves g > kBoundMaxG and the
+//    rows the first kernel marked.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -29,7 +31,8 @@
 namespace cp {
 namespace {
 
-constexpr int kKnnMaxN = 16384;   // n float64 keys fill 128 KiB of LDS
+constexpr int kKnnMaxN = 32768;
+constexpr int kKnnLdsN = 16384;   // up to here the radix select keeps n float64 keys (128 KiB) in LDS
 constexpr int kKnnMaxG = 1024;
 constexpr int kKnnBlock = 256;
 constexpr int kKnnWaves = kKnnBlock / 64;
@@ -157,11 +160,13 @@ __global__ __launch_bounds__(kKnnBlock) void knn_bound_kernel(const float* __res
   }
 }
 
-// Row c by radix select; keys is the block's dynamic LDS: n keys, then g
-// collected keys and g indices.
+// Row c by radix select; keys is the block's dynamic LDS: n keys (kLds
+// only), then g collected keys and g indices.  Without kLds every read of a
+// key recomputes it from the positions (the same float64 value).
+template <bool kLds>
 __device__ void knn_radix_row(const float* __restrict__ pos, int n, int g, int c, unsigned long long* keys,
                               int32_t* __restrict__ out) {
-  unsigned long long* ckey = keys + n;
+  unsigned long long* ckey = kLds ? keys + n : keys;
   int* cidx = reinterpret_cast<int*>(ckey + g);
   __shared__ unsigned int hist[256];
   __shared__ int swt[kKnnWaves];
@@ -169,8 +174,12 @@ __device__ void knn_radix_row(const float* __restrict__ pos, int n, int g, int c
   __shared__ int s_rank;
   const int tid = threadIdx.x;
   const float qx = pos[3 * c], qy = pos[3 * c + 1], qz = pos[3 * c + 2];
-  for (int j = tid; j < n; j += kKnnBlock)
-    keys[j] = sq_dist_key(qx, qy, qz, pos[3 * j], pos[3 * j + 1], pos[3 * j + 2]);
+  auto key = [&](int j) -> unsigned long long {
+    return kLds ? keys[j] : sq_dist_key(qx, qy, qz, pos[3 * j], pos[3 * j + 1], pos[3 * j + 2]);
+  };
+  if (kLds)
+    for (int j = tid; j < n; j += kKnnBlock)
+      keys[j] = sq_dist_key(qx, qy, qz, pos[3 * j], pos[3 * j + 1], pos[3 * j + 2]);
   if (tid == 0) {
     s_prefix = 0ull;
     s_rank = g - 1;                                     // 0-based rank of the g-th smallest
@@ -185,7 +194,7 @@ __device__ void knn_radix_row(const float* __restrict__ pos, int n, int g, int c
     __syncthreads();
     const unsigned long long prefix = s_prefix;
     for (int j = tid; j < n; j += kKnnBlock) {
-      const unsigned long long k = keys[j];
+      const unsigned long long k = key(j);
       if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
     }
     __syncthreads();
@@ -211,7 +220,7 @@ __device__ void knn_radix_row(const float* __restrict__ pos, int n, int g, int c
   const int j0 = min(n, tid * span), j1 = min(n, j0 + span);
   int n_less = 0, n_eq = 0;
   for (int j = j0; j < j1; ++j) {
-    const unsigned long long k = keys[j];
+    const unsigned long long k = key(j);
     n_less += k < T;
     n_eq += k == T;
   }
@@ -221,7 +230,7 @@ __device__ void knn_radix_row(const float* __restrict__ pos, int n, int g, int c
   (void)eq_total;
   int o_less = less_before, o_eq = eq_before;
   for (int j = j0; j < j1; ++j) {
-    const unsigned long long k = keys[j];
+    const unsigned long long k = key(j);
     if (k < T) {
       ckey[o_less] = k;
       cidx[o_less] = j;
@@ -254,6 +263,7 @@ __device__ void knn_radix_row(const float* __restrict__ pos, int n, int g, int c
 // whose first entry the bounding kernel set to -1.  Block b takes rows
 // b, b + gridDim.x, ...; it checks kKnnBlock of them at a time and selects the
 // ones it must redo one after another.
+template <bool kLds>
 __global__ __launch_bounds__(kKnnBlock) void knn_radix_kernel(const float* __restrict__ pos, int n, int g,
                                                               int marked_only, int32_t* __restrict__ out) {
   extern __shared__ unsigned long long keys[];
@@ -268,14 +278,14 @@ __global__ __launch_bounds__(kKnnBlock) void knn_radix_kernel(const float* __res
     if (c < n && (!marked_only || out[size_t(c) * g] == -1)) rows[atomicAdd(&nrows, 1)] = c;
     __syncthreads();
     const int cnt = nrows;
-    for (int r = 0; r < cnt; ++r) knn_radix_row(pos, n, g, rows[r], keys, out);
+    for (int r = 0; r < cnt; ++r) knn_radix_row<kLds>(pos, n, g, rows[r], keys, out);
     __syncthreads();
   }
 }
 
 }  // namespace
 
-static size_t knn_lds_bytes(int n, int g) { return size_t(n) * 8 + size_t(g) * 12; }
+static size_t knn_lds_bytes(int n, int g) { return (n <= kKnnLdsN ? size_t(n) * 8 : 0) + size_t(g) * 12; }
 
 hipError_t launch_knn(const float* pos, int n, int g, int32_t* out, hipStream_t stream) {
   if (n < 1 || n > kKnnMaxN || g < 1 || g > n || g > kKnnMaxG) return hipErrorInvalidValue;
@@ -286,14 +296,19 @@ hipError_t launch_knn(const float* pos, int n, int g, int32_t* out, hipStream_t 
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   const size_t lds = knn_lds_bytes(n, g);
-  if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(knn_radix_kernel),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
+  const bool in_lds = n <= kKnnLdsN;
+  const void* radix = in_lds ? reinterpret_cast<const void*>(knn_radix_kernel<true>)
+                             : reinterpret_cast<const void*>(knn_radix_kernel<false>);
+  if ((e = hipFuncSetAttribute(radix, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds))) != hipSuccess)
     return e;
   int dev = 0, cus = 0;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
   const int grid = std::max(1, std::min(n, bound ? cus : 4 * cus));
-  knn_radix_kernel<<<grid, kKnnBlock, lds, stream>>>(pos, n, g, bound ? 1 : 0, out);
+  if (in_lds)
+    knn_radix_kernel<true><<<grid, kKnnBlock, lds, stream>>>(pos, n, g, bound ? 1 : 0, out);
+  else
+    knn_radix_kernel<false><<<grid, kKnnBlock, lds, stream>>>(pos, n, g, bound ? 1 : 0, out);
   return hipGetLastError();
 }
 

@@ -66,7 +66,14 @@ hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, bool comp
 size_t sgs_local_workspace_bytes(int64_t n, int64_t k);
 hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipStream_t stream);
 
-// Nearest-neighbour tables: out [n, g], n <= 16384, g <= min(n, 1024).
+// Latency floor of a greedy step: rounds of the candidate exchange, each
+// followed (read_rows) by the read of a row of `rows` [n_rows][row_len] that
+// the exchange's winner names.  row_len is a multiple of 256, at most 32768.
+size_t step_floor_workspace_bytes();
+hipError_t launch_step_floor(const float* rows, int n_rows, int row_len, int rounds, bool read_rows, void* workspace,
+                             hipStream_t stream);
+
+// Nearest-neighbour tables: out [n, g], n <= 32768, g <= min(n, 1024).
 hipError_t launch_knn(const float* pos, int n, int g, int32_t* out, hipStream_t stream);
 
 // The greedy step solved as written: entropic semi-relaxed transport per step.

@@ -142,6 +142,18 @@ def test_sgs_noalloc_rejects(lib, kw, code):
                                              None, None, None, None) == code
 
 
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), INVALID), (dict(row_len=100), INVALID), (dict(row_len=0), INVALID),
+    (dict(row_len=32768 + 256), INVALID), (dict(rounds=0), INVALID), (dict(rows=None), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(ws_bytes=16), WORKSPACE),
+])
+def test_step_floor_rejects(lib, kw, code):
+    a = dict(rows=FAKE, n=64, row_len=256, rounds=10, read=1, ws=FAKE, ws_bytes=1 << 20)
+    a.update(kw)
+    assert lib.coverprune_step_floor(a["rows"], a["n"], a["row_len"], a["rounds"], a["read"], a["ws"], a["ws_bytes"],
+                                     None) == code
+
+
 def test_uncovered_cost_is_the_largest_cost(lib):
     # c0 = (lambda_f + lambda_x) + lambda_tau in float arithmetic: every term of
     # Eq. 8 is at most its weight once normalised.

@@ -93,6 +93,13 @@ def test_lite_full_size(capacity):
     # whose groups range from 2 to 26 tokens.
     s = parity.workload_scene("lite_n32768_d3584", 0) if capacity == "fst16" else make_scene("lite_n32768_d3584", 0)
     print(f"lite full size n={s.n} k={s.k} capacity={capacity}", flush=True)
+    if capacity == "fst16":
+        # The library's own capacity at this size against the oracle's (the
+        # input used below): within one float32 rounding.
+        t = to_device(s)
+        v_gpu, _ = _cp().fst_capacity(t["feats"], t["pos"], t["frame"], 16)
+        v_gpu = v_gpu.cpu().numpy().astype(np.float64)
+        assert np.allclose(v_gpu, s.capacity.astype(np.float64), rtol=2.0 ** -22, atol=0.0)
     sel, group, obj, tc = _gpu(s, s.k, 0.25)
     ref = parity.lite_reference(s, s.k, h=0.25)
     sizes = np.bincount(ref["group"])

@@ -117,6 +117,23 @@ def test_knn_full_size_sampled_rows():
         assert np.array_equal(got[rows], oknn.knn_ref(s.pos, g, rows=rows))
 
 
+@pytest.mark.slow
+def test_knn_beyond_keys_in_lds():
+    # 32768 tokens, more than the radix select keeps in LDS: its rows recompute
+    # their keys from the positions.  A quarter of the tokens share one point,
+    # so their rows overflow the bounding pass and take the radix select; g =
+    # 200 sends every row there.  Sampled rows against the oracle.
+    s = make_scene("lite_n32768_d3584", 0, dim=8)
+    pos = s.pos.copy()
+    pos[::4] = pos[0]
+    rng = np.random.default_rng(15)
+    rows = np.sort(np.concatenate([rng.choice(s.n, 96, replace=False), np.arange(0, 128, 4)]))
+    for g in (17, 200):
+        print(f"knn n={s.n} g={g} (keys recomputed)", flush=True)
+        got = _gpu_knn(pos, g)
+        assert np.array_equal(got[rows], oknn.knn_ref(pos, g, rows=rows))
+
+
 # ---------------------------------------------------------------------------
 # Local greedy on the oracle's cost and the oracle's neighbour tables.
 
