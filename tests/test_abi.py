@@ -198,7 +198,7 @@ def _knn(lib, **kw):
 
 
 @pytest.mark.parametrize("kw,code", [
-    (dict(n=0), INVALID), (dict(n=16385, g=8), INVALID), (dict(g=0), INVALID), (dict(g=65), INVALID),
+    (dict(n=0), INVALID), (dict(n=32769, g=8), INVALID), (dict(g=0), INVALID), (dict(g=65), INVALID),
     (dict(n=4096, g=1025), INVALID), (dict(pos=None), INVALID), (dict(out=None), INVALID),
 ])
 def test_knn_rejects(lib, kw, code):
@@ -245,7 +245,7 @@ def _cap(lib, **kw):
 
 
 @pytest.mark.parametrize("kw,code", [
-    (dict(n=1, nn=1), INVALID), (dict(n=16385), INVALID), (dict(nn=0), INVALID), (dict(nn=64), INVALID),
+    (dict(n=1, nn=1), INVALID), (dict(n=32769), INVALID), (dict(nn=0), INVALID), (dict(nn=64), INVALID),
     (dict(n=4096, nn=1024), INVALID), (dict(d=12), UNSUPPORTED), (dict(feats=None), INVALID),
     (dict(pos=None), INVALID), (dict(frame=None), INVALID), (dict(v=None), INVALID),
     (dict(alpha=_cw(af=-1.0)), INVALID), (dict(alpha=_cw(at=float("inf"))), INVALID),
