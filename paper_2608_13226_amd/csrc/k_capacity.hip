@@ -206,7 +206,7 @@ size_t capacity_workspace_bytes(int64_t n, int64_t nn) { return cap_layout(n, nn
 hipError_t launch_capacity(const CapacityParams& c, hipStream_t stream) {
   const CapLayout L = cap_layout(c.n, c.nn);
   char* w = static_cast<char*>(c.workspace);
-  CapDev p;
+  CapDev p{};
   p.feats = c.feats;
   p.n = c.n;
   p.d = c.d;

@@ -895,7 +895,7 @@ size_t lite_workspace_bytes(int64_t n, int64_t k) { return layout(n, k).total; }
 hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   const Layout L = layout(p.n, p.k);
   char* w = static_cast<char*>(p.workspace);
-  LiteDev a;
+  LiteDev a{};
   a.feats = p.feats;
   a.n = p.n;
   a.d = p.d;

@@ -92,7 +92,7 @@ hipError_t launch_step_floor(const float* rows, int n_rows, int row_len, int rou
   if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
   // The greedy's grid for a scene of n_rows tokens.
   const int nb = blocks_for(n_rows, cus);
-  ProbeDev a;
+  ProbeDev a{};
   a.rows = rows;
   a.n_rows = n_rows;
   a.ldt = row_len;

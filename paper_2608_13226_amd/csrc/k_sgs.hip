@@ -418,7 +418,7 @@ hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream) {
 
   const Layout L = layout(n, p.k);
   char* w = static_cast<char*>(p.workspace);
-  SgsDev a;
+  SgsDev a{};
   a.C = p.cost;
   a.v = p.capacity;
   a.n = n;

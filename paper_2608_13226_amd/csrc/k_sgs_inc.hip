@@ -440,35 +440,57 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   __shared__ unsigned long long sk1[kSpec ? kMaxBlocks : 1], sk2[kSpec ? kMaxBlocks : 1];
   __shared__ long long sdr[kWaves][kChain];
 
-  for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
-  for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
+  // A launch that continues another one runs only when its gate says so
+  // (the same word for every block), and then starts from the state the
+  // previous launch handed over.
+  if (a.gate && *a.gate != a.gate_val) return;
+  const bool resume = a.k_begin > 0;
+  if (resume && *a.abort) return;             // the launch before it gave up
   // The fixed-point scale, the step-0 gains (as P partial sums over row
   // ranges) and T come from the first-pass kernels.
   const int S = *a.scale;
-  for (int i = tid; i < cnt; i += kBlock) {
-    long long g = 0;
-    for (int q = 0; q < a.P; ++q) g += a.part[size_t(q) * a.n + lo + i];
-    sG[i] = g;
+  if (resume) {
+    for (int j = tid; j < a.ldt; j += kBlock) sball[j] = a.ho_b[j];
+    for (int i = tid; i < cnt; i += kBlock) {
+      ssel[i] = a.ho_sel[lo + i];
+      sG[i] = a.ho_gain[lo + i];
+    }
+  } else {
+    for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
+    for (int i = tid; i < cnt; i += kBlock) {
+      ssel[i] = 0;
+      long long g = 0;
+      for (int q = 0; q < a.P; ++q) g += a.part[size_t(q) * a.n + lo + i];
+      sG[i] = g;
+    }
   }
   __syncthreads();
 
   // Block 0 keeps the objective as one running part per wave (as in the
   // exchange form).
   __shared__ long long sLw[kWaves];
-  int obj_step = -1;
+  int obj_step = a.k_begin - 1;
   if (blk == 0) {
-    long long x = 0;
-    for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
-    const long long L0 = block_sum_i64(x, sg);
+    long long L0 = 0;
+    if (resume) {
+      L0 = a.ho_misc[0];
+    } else {
+      long long x = 0;
+      for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
+      L0 = block_sum_i64(x, sg);
+    }
     if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
   }
 
-  // Slot sets and epochs count exchanges, which predicted steps skip.
-  int xc = 0;
-  if (kSpec)
-    publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0));
-  else
-    publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
+  // Slot sets and epochs count exchanges, which predicted steps skip.  A
+  // continuing launch finds its first exchange's candidates published.
+  int xc = resume ? int(a.ho_misc[1]) : 0;
+  if (!resume) {
+    if (kSpec)
+      publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0));
+    else
+      publish_argmax(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0), sg, si);
+  }
 
   const int nch = a.ldt / kRowChunk;
   bool predicted = false;     // this step's winner was predicted (no exchange)
@@ -488,7 +510,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     acc[m] = 0;
     ub[m] = 0ull;
   }
-  for (int step = 0; step < a.k; ++step) {
+  for (int step = a.k_begin; step < a.k_end; ++step) {
     int tw;
     if (predicted) {
       __syncthreads();
@@ -809,7 +831,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
           gr = acc[c];
           u = ub[c];
         }
-      next = step + 1 < a.k && gr > 0 && (pack_key(fx_to_double(gr, S), rn) >> kIndexBits) > u;
+      next = step + 1 < a.k_end && gr > 0 && (pack_key(fx_to_double(gr, S), rn) >> kIndexBits) > u;
     }
     if (step + 1 < a.k && !next) {
       if (kSpec)
@@ -828,12 +850,270 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     for (int q = 0; q < kWaves; ++q) L += sLw[q];
     a.step_obj[obj_step] = fx_to_double(L, S);
   }
+  // Hand the state over to the launch that continues (the last step
+  // published the candidates of the next exchange).
+  if (a.k_end < a.k) {
+    for (int i = tid; i < cnt; i += kBlock) {
+      a.ho_gain[lo + i] = sG[i];
+      a.ho_sel[lo + i] = ssel[i];
+    }
+    if (blk == 0) {
+      for (int j = tid; j < a.ldt; j += kBlock) a.ho_b[j] = sball[j];
+      if (tid == 0) {
+        long long L = 0;
+#pragma unroll
+        for (int q = 0; q < kWaves; ++q) L += sLw[q];
+        a.ho_misc[0] = L;
+        a.ho_misc[1] = xc;
+      }
+    }
+  }
 }
 
 __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) { inc_body(a, blockIdx.x, gridDim.x); }
 
 template <int NG, int RL>
 __global__ __launch_bounds__(kBlock) void sgs_rows_kernel(IncDev a) { rows_body<NG, RL>(a, blockIdx.x, gridDim.x); }
+
+// ---------------------------------------------------------------------------
+// The rows schedule's later steps from candidate lists.
+//
+// Best costs only fall, so a pair (candidate c, target j) with C(c, j) >= b_j
+// never changes a gain again.  After kListStep steps few pairs are left (at
+// N = 16384, K = 1638: 44 per candidate on average, at most 5391 among one
+// block's 64 candidates).  The rows schedule then runs in two launches: the
+// first stops after kListStep steps and hands its state over (best costs,
+// running gains, chosen flags, objective, exchange count); list_build_kernel
+// writes every candidate's pairs (target, cost, the target's capacity) into
+// a list of at most kListMax entries; sgs_list_kernel runs the remaining steps
+// from the lists.  Per step a block reads the winner's list (a few KB, from
+// L2 for all but the first block of an XCD) instead of its 64 KB row of T, and
+// applies the hits from its own pairs, kept in LDS in buckets of kBucketT
+// targets, instead of reading each hit row's segment over its columns from
+// memory.  The terms are the fixed-point terms of the rows of T, so the picks
+// are the same.  When the lists do not fit (a candidate with more than
+// kListMax pairs, or a block with more than kEntMax), the build raises lfail
+// and the rows kernel continues instead (its launch is gated on lfail).
+constexpr int kListStep = 128;                        // steps before the lists
+constexpr int kListSlots = 256;                       // per candidate: a header and kListMax pairs
+constexpr int kListMax = kListSlots - 1;
+constexpr int kListMaxN = kRowChunk * kWaves * 8;     // 16384, the one-group rows kernel's reach
+constexpr int kBucketShift = 2;                       // kBucketT = 4 targets per bucket
+constexpr int kBuckets = kListMaxN >> kBucketShift;
+constexpr int kEntMax = 8192;                         // own pairs a block keeps in LDS
+
+bool lists_for(int64_t n, int64_t k, int W) { return n <= kListMaxN && W <= 64 && k > kListStep; }
+
+// One wave per candidate: its pairs from its row of T against the handed
+// over best costs.  Also counts the pairs of each block of the list kernel.
+__global__ __launch_bounds__(256) void list_build_kernel(IncDev a) {
+  if (*a.abort) return;
+  const int lane = threadIdx.x & 63;
+  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (c >= a.n) return;
+  const f32x4* row = reinterpret_cast<const f32x4*>(a.T + size_t(c) * a.ldt);
+  const f32x4* bb = reinterpret_cast<const f32x4*>(a.ho_b);
+  unsigned long long* dst = a.lists + size_t(c) * (2 * kListSlots);
+  const int nch = a.ldt / kRowChunk;
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  int m = 0;
+  for (int q0 = 0; q0 < nch; q0 += 8) {
+    f32x4 x[8], b[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (q0 + u < nch) {
+        x[u] = row[(q0 + u) * (kRowChunk / 4) + lane];
+        b[u] = bb[(q0 + u) * (kRowChunk / 4) + lane];
+      }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (q0 + u >= nch) break;
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        const bool hit = x[u][cc] < b[u][cc];         // never past n, where b = -inf
+        const unsigned long long mk = __ballot(hit);
+        if (hit) {
+          const int pos = m + __popcll(mk & lt);
+          const int j = (q0 + u) * kRowChunk + 4 * lane + cc;
+          if (pos < kListMax) {
+            dst[2 * (1 + pos)] = (unsigned long long)(unsigned)j | ((unsigned long long)__float_as_uint(x[u][cc]) << 32);
+            dst[2 * (1 + pos) + 1] = (unsigned long long)__float_as_uint(a.v[j]);
+          }
+        }
+        m += __popcll(mk);
+      }
+    }
+  }
+  if (lane == 0) {
+    dst[0] = (unsigned long long)m;
+    const unsigned int tot = atomicAdd(a.lblock + c / a.W, unsigned(m)) + unsigned(m);
+    if (m > kListMax || tot > unsigned(kEntMax)) atomicOr(a.lfail, 1u);
+  }
+}
+
+// The greedy's steps kListStep .. k - 1 from the lists (one block of eight
+// waves per compute unit, block b owning candidates [b W, (b + 1) W) as in
+// the rows kernel, W <= 64).
+__global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
+  if (*a.lfail || *a.abort) return;
+  extern __shared__ unsigned long long smem[];
+  const int blk = blockIdx.x, nb = gridDim.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lo = blk * a.W;
+  const int cnt = max(0, min(a.n, lo + a.W) - lo);
+  float* sball = reinterpret_cast<float*>(smem);                   // [ldt] best costs
+  __shared__ long long sG[64];
+  __shared__ unsigned char ssel[64];
+  __shared__ unsigned int sbk[kBuckets];                            // bucket ends
+  __shared__ unsigned short sej[kEntMax];                           // own pairs: target,
+  __shared__ unsigned char sec[kEntMax];                            //   candidate (own index),
+  __shared__ float secv[kEntMax];                                   //   cost
+  __shared__ unsigned long long sdelta[64];
+  __shared__ int lj[kListSlots];                                    // the step's hits: target,
+  __shared__ float lbo[kListSlots], lbn[kListSlots], lv[kListSlots];   // old b, new b, capacity
+  __shared__ int scnt[2];
+  __shared__ unsigned long long su[kWaves], sk1[kMaxBlocks], sk2[kMaxBlocks];
+  __shared__ int sflag;
+  __shared__ int swt[kWaves];
+  __shared__ long long sLw[kWaves];
+  const int S = *a.scale;
+
+  for (int j = tid; j < a.ldt; j += kBlock) sball[j] = a.ho_b[j];
+  if (tid < 64) {
+    ssel[tid] = tid < cnt ? a.ho_sel[lo + tid] : 1;
+    sG[tid] = tid < cnt ? a.ho_gain[lo + tid] : 0;
+    sdelta[tid] = 0ull;
+  }
+  for (int i = tid; i < kBuckets; i += kBlock) sbk[i] = 0u;
+  if (tid < kWaves) sLw[tid] = (blk == 0 && tid == 0) ? a.ho_misc[0] : 0;
+  if (tid == 0) scnt[0] = scnt[1] = 0;
+  __syncthreads();
+  // The own pairs into LDS buckets by target: counts, starts, then places
+  // (after which sbk[b] is the end of bucket b).
+  for (int ci = w; ci < cnt; ci += kWaves) {
+    const unsigned long long* src = a.lists + size_t(lo + ci) * (2 * kListSlots);
+    const int m = min(int(src[0]), kListMax);
+    for (int e = 1 + lane; e <= m; e += 64) atomicAdd(&sbk[unsigned(src[2 * e]) >> kBucketShift], 1u);
+  }
+  __syncthreads();
+  {
+    constexpr int per = kBuckets / kBlock;
+    unsigned int c[per], tot = 0u;
+#pragma unroll
+    for (int q = 0; q < per; ++q) {
+      c[q] = sbk[tid * per + q];
+      tot += c[q];
+    }
+    const int incl = block_inclusive_scan(int(tot), swt);
+    unsigned int run = unsigned(incl) - tot;
+#pragma unroll
+    for (int q = 0; q < per; ++q) {
+      sbk[tid * per + q] = run;
+      run += c[q];
+    }
+  }
+  __syncthreads();
+  for (int ci = w; ci < cnt; ci += kWaves) {
+    const unsigned long long* src = a.lists + size_t(lo + ci) * (2 * kListSlots);
+    const int m = min(int(src[0]), kListMax);
+    for (int e = 1 + lane; e <= m; e += 64) {
+      const unsigned long long w0 = src[2 * e];
+      const unsigned int slot = atomicAdd(&sbk[unsigned(w0) >> kBucketShift], 1u);
+      sej[slot] = (unsigned short)unsigned(w0);
+      sec[slot] = (unsigned char)ci;
+      secv[slot] = __uint_as_float(unsigned(w0 >> 32));
+    }
+  }
+  __syncthreads();
+
+  int xc = int(a.ho_misc[1]);
+  int obj_step = a.k_begin - 1;
+  for (int step = a.k_begin; step < a.k; ++step) {
+    const int tw = read_winner_rows(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, a.poll_limit, su,
+                                    &sflag, sk1, sk2);
+    ++xc;
+    if (tw < 0) break;
+    if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
+      long long L = 0;
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) L += sLw[q];
+      a.step_obj[obj_step] = fx_to_double(L, S);
+    }
+    const int t = min(tw, a.n - 1);
+    if (t >= lo && t < lo + cnt && tid == 0) {
+      ssel[t - lo] = 1;
+      a.selected[step] = t;
+      if (a.step_gain) a.step_gain[step] = fx_to_double(sG[t - lo], S);
+    }
+    // The winner's hits from its list: waves 0-3, lane e of the list at
+    // 1 + 64 w + lane (plain loads: the lists are fixed since the build).
+    const int par = step & 1;
+    if (w < 4) {
+      const uint4* lw = reinterpret_cast<const uint4*>(a.lists + size_t(t) * (2 * kListSlots));
+      const int e = 1 + w * 64 + lane;
+      const uint4 hv = lw[0];
+      const uint4 ev = e < kListSlots ? lw[e] : uint4{0u, 0u, 0u, 0u};
+      const int m = min(int(hv.x), kListMax);
+      const bool valid = e <= m;
+      const int j = valid ? min(int(ev.x), a.n - 1) : 0;
+      const float x = __uint_as_float(ev.y);
+      const float bo = valid ? sball[j] : 0.f;
+      const bool hit = valid && x < bo;
+      const unsigned long long mk = __ballot(hit);
+      if (mk) {
+        int at = 0;
+        if (lane == 0) at = atomicAdd(&scnt[par], __popcll(mk));
+        at = __builtin_amdgcn_readlane(at, 0);
+        if (hit) {
+          const int q = at + __popcll(mk & ((1ull << lane) - 1ull));
+          lj[q] = j;
+          lbo[q] = bo;
+          lbn[q] = x;
+          lv[q] = __uint_as_float(ev.z);
+        }
+      }
+    }
+    __syncthreads();
+    const int total = scnt[par];
+    if (tid == 0) scnt[par ^ 1] = 0;   // last read in the previous step, next used in the next
+    // Hits h = w, w + 8, ...: the lanes scan the hit's bucket for the own
+    // pairs with that target; their gain changes add up in LDS as 64-bit
+    // integers, the same terms as the rows of T give.
+    long long dobj = 0;
+    for (int h = w; h < total; h += kWaves) {
+      const int j = lj[h];
+      const float bo = lbo[h], bn = lbn[h];
+      const double vs = fx_scale(double(lv[h]), S);
+      const int bk = j >> kBucketShift;
+      const int y1 = int(sbk[bk]);
+      for (int y = (bk ? int(sbk[bk - 1]) : 0) + lane; y < y1; y += 64)
+        if (sej[y] == (unsigned short)j) {
+          const float cv = secv[y];
+          if (cv < bo) atomicAdd(&sdelta[sec[y]], fx_scaled(vs, fmaxf(bn - cv, 0.f)) - fx_scaled(vs, bo - cv));
+        }
+      if (lane == 0) {
+        if (blk == 0) dobj += (long long)(fx_scaled(vs, bn) - fx_scaled(vs, bo));
+        sball[j] = bn;
+        if (a.assign && unsigned(j - lo) < unsigned(cnt)) a.assign[j] = t;
+      }
+    }
+    if (blk == 0 && lane == 0) sLw[w] += dobj;
+    obj_step = step;
+    __syncthreads();
+    if (tid < 64) {
+      if (tid < cnt) sG[tid] += (long long)sdelta[tid];
+      sdelta[tid] = 0ull;
+    }
+    if (step + 1 < a.k) publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, xc & 1, blk), epoch_of(xc));
+  }
+  __syncthreads();
+  if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
+    long long L = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) L += sLw[q];
+    a.step_obj[obj_step] = fx_to_double(L, S);
+  }
+}
 
 // The fixed-point scale of a scene (one block; the sum in the same order as
 // every block of the greedy would take it).
@@ -979,7 +1259,7 @@ const void* rows_batch_kernel(int64_t n, int W) {
 // (when the rows form may run) T.
 constexpr int kPassParts = 3;   // row ranges of the first pass (three blocks per compute unit fit at once)
 struct IncLayout {
-  size_t part, scale, T, total;
+  size_t part, scale, T, lists, ho_gain, ho_sel, ho_b, misc, total;
 };
 IncLayout inc_layout(int64_t n, int64_t k, bool compact) {
   IncLayout L;
@@ -988,6 +1268,16 @@ IncLayout inc_layout(int64_t n, int64_t k, bool compact) {
   L.scale = o; o += 256;
   L.T = o;
   if (!compact && n <= kRowsMaxN) o += a256(size_t(n) * rows_ldt(n) * sizeof(float));
+  // The candidate lists and the hand-over between launches (rows schedule,
+  // n <= kListMaxN, more than kListStep picks).
+  L.lists = L.ho_gain = L.ho_sel = L.ho_b = L.misc = o;
+  if (!compact && n <= kListMaxN && k > kListStep) {
+    L.lists = o;   o += a256(size_t(n) * kListSlots * 16);
+    L.ho_gain = o; o += a256(size_t(n) * 8);
+    L.ho_sel = o;  o += a256(size_t(n));
+    L.ho_b = o;    o += a256(size_t(rows_ldt(n)) * 4);
+    L.misc = o;    o += a256(16 + 4 + size_t(kMaxBlocks) * 4);   // objective, exchanges; lfail; lblock
+  }
   L.total = o;
   return L;
 }
@@ -995,7 +1285,7 @@ size_t inc_bytes(int64_t n, int64_t k, bool compact) { return inc_layout(n, k, c
 
 IncDev inc_dev(const SgsParams& p, char* w, int W, bool rows) {
   const Layout L = layout(p.n, p.k);
-  IncDev a;
+  IncDev a{};
   a.C = p.cost;
   a.v = p.capacity;
   a.n = p.n;
@@ -1019,6 +1309,18 @@ IncDev inc_dev(const SgsParams& p, char* w, int W, bool rows) {
   a.part = reinterpret_cast<const long long*>(w + M.part);
   a.P = kPassParts;
   a.scale = reinterpret_cast<const int*>(w + M.scale);
+  a.k_begin = 0;
+  a.k_end = p.k;
+  a.gate = nullptr;
+  a.gate_val = 0u;
+  const bool lists = rows && lists_for(p.n, p.k, W);
+  a.lists = lists ? reinterpret_cast<unsigned long long*>(w + M.lists) : nullptr;
+  a.ho_gain = lists ? reinterpret_cast<long long*>(w + M.ho_gain) : nullptr;
+  a.ho_sel = lists ? reinterpret_cast<unsigned char*>(w + M.ho_sel) : nullptr;
+  a.ho_b = lists ? reinterpret_cast<float*>(w + M.ho_b) : nullptr;
+  a.ho_misc = lists ? reinterpret_cast<long long*>(w + M.misc) : nullptr;
+  a.lfail = lists ? reinterpret_cast<unsigned int*>(w + M.misc + 16) : nullptr;
+  a.lblock = lists ? reinterpret_cast<unsigned int*>(w + M.misc + 20) : nullptr;
   return a;
 }
 
@@ -1062,11 +1364,35 @@ hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t 
   if ((e = fits(kernel, lds)) != hipSuccess) return e;
 
   IncDev a = inc_dev(p, static_cast<char*>(p.workspace), W, rows);
+  // Scenes the list phase serves: the rows kernel stops after kListStep
+  // steps, the lists are built, and the list kernel (or, when the lists do
+  // not fit, the rows kernel again) runs the rest.
+  const bool lists = a.lists != nullptr;
+  if (lists) {
+    a.k_end = kListStep;
+    if ((e = fits(reinterpret_cast<const void*>(sgs_list_kernel), size_t(a.ldt) * 4)) != hipSuccess) return e;
+  }
   sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = launch_first_pass(a, nb, stream)) != hipSuccess) return e;
   void* args[] = {&a};
   if ((e = hipLaunchCooperativeKernel(kernel, dim3(nb), dim3(kBlock), args, lds, stream)) != hipSuccess) return e;
+  if (lists) {
+    list_build_kernel<<<(p.n + 3) / 4, 256, 0, stream>>>(a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    IncDev b = a;
+    b.k_begin = kListStep;
+    b.k_end = p.k;
+    void* bargs[] = {&b};
+    if ((e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_list_kernel), dim3(nb), dim3(kBlock), bargs,
+                                        size_t(a.ldt) * 4, stream)) != hipSuccess)
+      return e;
+    IncDev c = b;
+    c.gate = a.lfail;
+    c.gate_val = 1u;
+    void* cargs[] = {&c};
+    if ((e = hipLaunchCooperativeKernel(kernel, dim3(nb), dim3(kBlock), cargs, lds, stream)) != hipSuccess) return e;
+  }
   return launch_mark_aborted(a.abort, a.selected, a.k, stream);
 }
 
@@ -1117,7 +1443,7 @@ hipError_t launch_sgs_incremental_batch(const SgsParams* p, int count, bool comp
     wmax = std::max(wmax, W);
     nmax = std::max(nmax, p[s].n);
   }
-  IncBatch b;
+  IncBatch b{};
   b.count = count;
   b.g0[0] = 0;
   size_t lds = 0, off = 0;

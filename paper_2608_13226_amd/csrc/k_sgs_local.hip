@@ -296,7 +296,7 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
   const Layout X = layout(p.n, p.k);
   const LocalLayout Y = local_layout(p.n, p.k);
   char* w = static_cast<char*>(p.workspace);
-  LocalDev d;
+  LocalDev d{};   // value-initialised: fields this launcher does not set stay null
   IncDev& a = d.a;
   a.C = p.cost;
   a.v = p.capacity;

@@ -89,6 +89,19 @@ struct IncDev {
   const long long* part;      // incremental form: [P][n] step-0 gains summed over P row ranges
   int P;
   const int* scale;           // incremental form: the fixed-point exponent S
+  // Rows schedule in two launches with a hand-over (see k_sgs_inc.hip): the
+  // steps of this launch, the word that decides whether it runs, and the
+  // state handed from one launch to the next.
+  int k_begin, k_end;         // steps [k_begin, k_end); [0, k) for a single launch
+  const unsigned int* gate;   // the launch runs only if *gate == gate_val (null: always)
+  unsigned int gate_val;
+  long long* ho_gain;         // [n] running gains
+  unsigned char* ho_sel;      // [n] chosen flags
+  float* ho_b;                // [ldt] best costs
+  long long* ho_misc;         // [0] objective in fixed point, [1] exchanges so far
+  unsigned long long* lists;  // [n][kListSlots][2] candidate lists
+  unsigned int* lfail;        // the lists do not fit
+  unsigned int* lblock;       // [blocks] pairs of each block's candidates
 };
 
 struct Layout {
@@ -151,6 +164,10 @@ __global__ void sgs_inc_init_kernel(IncDev a) {
   }
   for (int j = gt; j < a.n; j += nt)
     if (a.assign) a.assign[j] = -1;
+  if (a.lfail) {
+    for (int s = gt; s < kMaxBlocks; s += nt) a.lblock[s] = 0u;
+    if (gt == 0) *a.lfail = 0u;
+  }
   if (gt == 0) *a.abort = a.abort_init;
 }
 

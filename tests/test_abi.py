@@ -53,7 +53,11 @@ def test_workspace_queries(lib):
     c = lib.coverprune_sgs_workspace(16384, 1638, 3)
     assert 16384 * 16 <= c < b
     r = lib.coverprune_sgs_workspace(16384, 1638, 1)
-    assert r == c + 16384 * 16384 * 4
+    # ... and, past 128 picks up to n = 16384, the candidate lists (256 pairs
+    # of 16 bytes per token) and the hand-over between the two launches
+    # (gains, chosen flags, best costs: 13 bytes per token, and 1280 bytes)
+    assert r == c + 16384 * 16384 * 4 + 16384 * 256 * 16 + 16384 * 13 + 1280
+    assert lib.coverprune_sgs_workspace(16384, 128, 1) == lib.coverprune_sgs_workspace(16384, 128, 3) + 16384 * 16384 * 4
     # ... up to n = 32768 (rows padded to 256 targets); beyond it the compact one
     assert lib.coverprune_sgs_workspace(1000, 100, 1) == lib.coverprune_sgs_workspace(1000, 100, 3) + 1000 * 1024 * 4
     assert lib.coverprune_sgs_workspace(32769, 100, 1) == lib.coverprune_sgs_workspace(32769, 100, 3)

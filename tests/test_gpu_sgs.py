@@ -143,6 +143,32 @@ def test_end_to_end_parity(mode):
 
 
 @pytest.mark.parametrize("mode", MODES)
+def test_lists_that_do_not_fit(mode):
+    # Past step 128 the rows schedule continues from candidate lists when
+    # they fit.  Here they cannot: a candidate's cost to every other target
+    # falls with its index, so once the greedy has picked candidate m, every
+    # candidate above m undercuts the best cost of nearly all targets (about
+    # five candidates keep 300 to 700 such pairs after 128 picks, above the
+    # 255 a list holds).  The rows of T then serve the remaining steps (the
+    # gated second launch), with the same result.
+    n, k = 1024, 200
+    rng = np.random.default_rng(21)
+    C_src = np.repeat((1.0 - 1e-3 * np.arange(n) / n)[:, None], n, axis=1)
+    C_src = (C_src + 1e-5 * rng.random((n, n))).astype(np.float32)
+    np.fill_diagonal(C_src, 0.0)
+    v = rng.random(n).astype(np.float32)
+    v /= v.sum()
+    print(f"sgs lists that do not fit, mode={mode}", flush=True)
+    ref = sgs.sgs_ref(C_src.astype(np.float64), v.astype(np.float64), k, 3.0)
+    sel, gain, obj, assign = _gpu_select(np.ascontiguousarray(C_src.T), v, k, 3.0, mode)
+    ties, g_or, o_or = parity.replay_greedy(C_src, v, 3.0, sel)
+    assert np.allclose(gain, g_or, rtol=1e-6, atol=1e-12)
+    assert np.allclose(obj, o_or, rtol=1e-9, atol=1e-12)
+    if not ties:
+        assert np.array_equal(sel, ref["selected"]) and np.array_equal(assign, ref["assign"])
+
+
+@pytest.mark.parametrize("mode", MODES)
 def test_deterministic(mode):
     s = _sub("n4096_d1152", 1000, 8)
     C_ref, _ = parity.oracle_cost(s)
