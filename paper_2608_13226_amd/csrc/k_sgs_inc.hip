@@ -888,8 +888,10 @@ __global__ __launch_bounds__(kBlock) void sgs_rows_kernel(IncDev a) { rows_body<
 // a list of at most kListMax entries; sgs_list_kernel runs the remaining steps
 // from the lists.  Per step a block reads the winner's list (a few KB, from
 // L2 for all but the first block of an XCD) instead of its 64 KB row of T, and
-// applies the hits from its own pairs, kept in LDS in buckets of kBucketT
-// targets, instead of reading each hit row's segment over its columns from
+// its threads hold the block's own pairs in registers (up to kOwnSets a
+// thread) with each pair's last seen best cost: a step's changes to the own
+// gains come from the pairs whose best cost fell, found by one LDS read per
+// pair, instead of reading each hit row's segment over its columns from
 // memory.  The terms are the fixed-point terms of the rows of T, so the picks
 // are the same.  When the lists do not fit (a candidate with more than
 // kListMax pairs, or a block with more than kEntMax), the build raises lfail
@@ -898,9 +900,8 @@ constexpr int kListStep = 128;                        // steps before the lists
 constexpr int kListSlots = 256;                       // per candidate: a header and kListMax pairs
 constexpr int kListMax = kListSlots - 1;
 constexpr int kListMaxN = kRowChunk * kWaves * 8;     // 16384, the one-group rows kernel's reach
-constexpr int kBucketShift = 2;                       // kBucketT = 4 targets per bucket
-constexpr int kBuckets = kListMaxN >> kBucketShift;
-constexpr int kEntMax = 8192;                         // own pairs a block keeps in LDS
+constexpr int kOwnSets = 16;                          // own pairs a thread holds
+constexpr int kEntMax = kOwnSets * kBlock;            // own pairs a block holds: 8192
 
 bool lists_for(int64_t n, int64_t k, int W) { return n <= kListMaxN && W <= 64 && k > kListStep; }
 
@@ -954,6 +955,27 @@ __global__ __launch_bounds__(256) void list_build_kernel(IncDev a) {
 // The greedy's steps kListStep .. k - 1 from the lists (one block of eight
 // waves per compute unit, block b owning candidates [b W, (b + 1) W) as in
 // the rows kernel, W <= 64).
+//
+// Predicted steps, as in the rows kernel but up to kListChain in a row: after
+// an exchange the chain r_1, r_2, ... are the best candidates of distinct
+// blocks in key order (the winner's block left out).  r_m is the next winner
+// when a lower bound on its gain (its key, plus its exact changes since the
+// exchange) beats the key of r_(m+1) and the second-best keys of the
+// winner's block and of r_1 .. r_m's blocks.  Every block holds the lists of
+// the exchange's winner and of the chain in registers, so it sums the chain's
+// changes itself (an entry's target was hit when its best cost fell in the
+// step: the same terms as the owner applies), and a predicted step finds its
+// winner's hits in registers: no exchange and no memory latency.
+//
+// A step: the waves holding the winner's list lower the best costs of its
+// hits in LDS; after a barrier every thread compares its own pairs' and its
+// chain entries' last seen best costs with LDS and sums the changes (own
+// candidates into LDS, chain candidates per wave); after a second barrier
+// every thread updates the chain bounds and decides whether the next step is
+// predicted, and wave 0 folds the gains and publishes when it is not.
+constexpr int kListChain = 3;                         // predicted steps in a row at most
+constexpr int kListSets = (kListChain + 2) / 2;      // chain list entries a thread holds
+
 __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   if (*a.lfail || *a.abort) return;
   extern __shared__ unsigned long long smem[];
@@ -964,18 +986,13 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   float* sball = reinterpret_cast<float*>(smem);                   // [ldt] best costs
   __shared__ long long sG[64];
   __shared__ unsigned char ssel[64];
-  __shared__ unsigned int sbk[kBuckets];                            // bucket ends
-  __shared__ unsigned short sej[kEntMax];                           // own pairs: target,
-  __shared__ unsigned char sec[kEntMax];                            //   candidate (own index),
-  __shared__ float secv[kEntMax];                                   //   cost
   __shared__ unsigned long long sdelta[64];
-  __shared__ int lj[kListSlots];                                    // the step's hits: target,
-  __shared__ float lbo[kListSlots], lbn[kListSlots], lv[kListSlots];   // old b, new b, capacity
-  __shared__ int scnt[2];
+  __shared__ int soff[65];                                          // own pairs: each candidate's first
+  __shared__ unsigned char sown[kEntMax];                           //   and each pair's candidate
   __shared__ unsigned long long su[kWaves], sk1[kMaxBlocks], sk2[kMaxBlocks];
   __shared__ int sflag;
-  __shared__ int swt[kWaves];
-  __shared__ long long sLw[kWaves];
+  __shared__ unsigned long long sL;                                 // objective (block 0)
+  __shared__ unsigned long long sacc[kListChain + 1];               // chain changes since the exchange
   const int S = *a.scale;
 
   for (int j = tid; j < a.ldt; j += kBlock) sball[j] = a.ho_b[j];
@@ -983,136 +1000,240 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
     ssel[tid] = tid < cnt ? a.ho_sel[lo + tid] : 1;
     sG[tid] = tid < cnt ? a.ho_gain[lo + tid] : 0;
     sdelta[tid] = 0ull;
+    // Where each own candidate's pairs start among the block's.
+    const int m = tid < cnt ? min(int(a.lists[size_t(lo + tid) * (2 * kListSlots)]), kListMax) : 0;
+    const int incl = wave_scan_incl(m);
+    soff[tid + 1] = incl;
+    if (tid == 0) soff[0] = 0;
   }
-  for (int i = tid; i < kBuckets; i += kBlock) sbk[i] = 0u;
-  if (tid < kWaves) sLw[tid] = (blk == 0 && tid == 0) ? a.ho_misc[0] : 0;
-  if (tid == 0) scnt[0] = scnt[1] = 0;
+  if (tid == 0) sL = (unsigned long long)(blk == 0 ? a.ho_misc[0] : 0);
   __syncthreads();
-  // The own pairs into LDS buckets by target: counts, starts, then places
-  // (after which sbk[b] is the end of bucket b).
-  for (int ci = w; ci < cnt; ci += kWaves) {
-    const unsigned long long* src = a.lists + size_t(lo + ci) * (2 * kListSlots);
-    const int m = min(int(src[0]), kListMax);
-    for (int e = 1 + lane; e <= m; e += 64) atomicAdd(&sbk[unsigned(src[2 * e]) >> kBucketShift], 1u);
-  }
-  __syncthreads();
-  {
-    constexpr int per = kBuckets / kBlock;
-    unsigned int c[per], tot = 0u;
-#pragma unroll
-    for (int q = 0; q < per; ++q) {
-      c[q] = sbk[tid * per + q];
-      tot += c[q];
-    }
-    const int incl = block_inclusive_scan(int(tot), swt);
-    unsigned int run = unsigned(incl) - tot;
-#pragma unroll
-    for (int q = 0; q < per; ++q) {
-      sbk[tid * per + q] = run;
-      run += c[q];
-    }
-  }
-  __syncthreads();
-  for (int ci = w; ci < cnt; ci += kWaves) {
-    const unsigned long long* src = a.lists + size_t(lo + ci) * (2 * kListSlots);
-    const int m = min(int(src[0]), kListMax);
-    for (int e = 1 + lane; e <= m; e += 64) {
-      const unsigned long long w0 = src[2 * e];
-      const unsigned int slot = atomicAdd(&sbk[unsigned(w0) >> kBucketShift], 1u);
-      sej[slot] = (unsigned short)unsigned(w0);
-      sec[slot] = (unsigned char)ci;
-      secv[slot] = __uint_as_float(unsigned(w0 >> 32));
-    }
-  }
+  const int npairs = min(soff[64], kEntMax);
+  for (int ci = w; ci < cnt; ci += kWaves)
+    for (int e = soff[ci] + lane; e < min(soff[ci + 1], npairs); e += 64) sown[e] = (unsigned char)ci;
   __syncthreads();
 
+  // Own pair p = q kBlock + tid of the block (candidates in order, each with
+  // its list's entries) in set q: target | own index << 16, cost, capacity,
+  // and the best cost as last seen (-inf for no pair, which never falls).
+  // Every step of the set-up is issued for all sets before its results are
+  // used.
+  int pj[kOwnSets];
+  float pc[kOwnSets], pv[kOwnSets], pb[kOwnSets];
+  {
+    int ci[kOwnSets], e[kOwnSets];
+#pragma unroll
+    for (int q = 0; q < kOwnSets; ++q) ci[q] = q * kBlock + tid < npairs ? int(sown[q * kBlock + tid]) : 0;
+#pragma unroll
+    for (int q = 0; q < kOwnSets; ++q) e[q] = q * kBlock + tid < npairs ? 1 + q * kBlock + tid - soff[ci[q]] : 0;
+    uint4 ev[kOwnSets];
+#pragma unroll
+    for (int q = 0; q < kOwnSets; ++q)
+      ev[q] = reinterpret_cast<const uint4*>(a.lists + size_t(min(lo + ci[q], a.n - 1)) * (2 * kListSlots))[e[q]];
+#pragma unroll
+    for (int q = 0; q < kOwnSets; ++q) {
+      const bool ok = q * kBlock + tid < npairs;
+      const int j = ok ? min(int(ev[q].x), a.n - 1) : 0;
+      pj[q] = j | (ci[q] << 16);
+      pc[q] = __uint_as_float(ev[q].y);
+      pv[q] = __uint_as_float(ev[q].z);
+      pb[q] = ok ? sball[j] : -__builtin_inff();
+    }
+  }
+
+  // Chain slots: 0 the exchange's winner, m = 1 .. kListChain the candidate
+  // r_m (-1 past the last), with lower bounds on their gains at the exchange
+  // and the key bits they must beat.  Entry set q of a thread is entry
+  // (tid & 255) of slot 2 q + (tid >> 8)'s list: target, cost, scaled
+  // capacity, and the target's best cost as last seen (entry 0 of a list is
+  // its header).
+  const int half = tid >> 8, ent = tid & (kListSlots - 1);
+  int rc[kListChain + 1];
+  long long acc[kListChain + 1];
+  unsigned long long ub[kListChain + 1];
+  int ej[kListSets];
+  float ec[kListSets], eb[kListSets];
+  double evs[kListSets];
+  bool eok[kListSets];
+#pragma unroll
+  for (int m = 0; m <= kListChain; ++m) {
+    rc[m] = -1;
+    acc[m] = 0;
+    ub[m] = 0ull;
+  }
+#pragma unroll
+  for (int q = 0; q < kListSets; ++q) {
+    ej[q] = 0;
+    ec[q] = eb[q] = 0.f;
+    evs[q] = 0.0;
+    eok[q] = false;
+  }
   int xc = int(a.ho_misc[1]);
   int obj_step = a.k_begin - 1;
+  bool predicted = false;
+  int pos = 0;                 // the step's place in the chain (0: after an exchange)
   for (int step = a.k_begin; step < a.k; ++step) {
-    const int tw = read_winner_rows(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, a.poll_limit, su,
-                                    &sflag, sk1, sk2);
-    ++xc;
-    if (tw < 0) break;
-    if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
-      long long L = 0;
+    int t = -1;
+    if (!predicted) {
+      const int tw = read_winner_rows(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, a.poll_limit, su,
+                                      &sflag, sk1, sk2);
+      ++xc;
+      if (tw < 0) break;
+      t = min(tw, a.n - 1);
+      if (tid <= kListChain) sacc[tid] = 0ull;
+      // The chain from the exchange's keys (every wave the same).
+      const int bt = t / a.W;
+      unsigned long long kq[4];
 #pragma unroll
-      for (int q = 0; q < kWaves; ++q) L += sLw[q];
-      a.step_obj[obj_step] = fx_to_double(L, S);
+      for (int q = 0; q < 4; ++q) {
+        const int bq = lane + 64 * q;
+        kq[q] = (bq < nb && bq != bt) ? sk1[bq] : 0ull;
+      }
+      unsigned long long u2 = sk2[bt];
+      rc[0] = t;
+#pragma unroll
+      for (int m = 1; m <= kListChain + 1; ++m) {
+        const unsigned long long kr = wave_max_u64(max(max(kq[0], kq[1]), max(kq[2], kq[3])));
+        const bool real = kr > kNoCandidate && (m == 1 || rc[m - 1] >= 0);
+        const int r = real ? int(kIndexMask - (kr & kIndexMask)) : -1;
+        const int br = real ? r / a.W : -1;
+        if (m >= 2) ub[m - 1] = max(real ? kr : 0ull, u2) >> kIndexBits;
+        if (m <= kListChain) {
+          rc[m] = r;
+          acc[m] = real ? key_gain_floor(kr, S) : 0;
+          if (real) u2 = max(u2, sk2[br]);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) kq[q] = (lane + 64 * q) == br ? 0ull : kq[q];
+        }
+      }
+      pos = 0;
+      // The lists of the winner and of the chain, all loads in flight
+      // together (plain loads: the lists are fixed since the build).
+      uint4 hv[kListSets], ev[kListSets];
+#pragma unroll
+      for (int q = 0; q < kListSets; ++q) {
+        const int sl = 2 * q + half;
+        int r = -1;
+#pragma unroll
+        for (int m = 0; m <= kListChain; ++m)
+          if (m == sl) r = rc[m];
+        const uint4* lw = reinterpret_cast<const uint4*>(a.lists + size_t(max(r, 0)) * (2 * kListSlots));
+        hv[q] = lw[0];
+        ev[q] = lw[ent];
+        eok[q] = r >= 0;
+      }
+#pragma unroll
+      for (int q = 0; q < kListSets; ++q) {
+        eok[q] = eok[q] && ent >= 1 && ent <= min(int(hv[q].x), kListMax);
+        ej[q] = eok[q] ? min(int(ev[q].x), a.n - 1) : 0;
+        ec[q] = __uint_as_float(ev[q].y);
+        evs[q] = fx_scale(double(__uint_as_float(ev[q].z)), S);
+      }
+      // The entries' best costs before the step's hits lower them.
+#pragma unroll
+      for (int q = 0; q < kListSets; ++q) eb[q] = eok[q] ? sball[ej[q]] : 0.f;
+      __syncthreads();
+    } else {
+#pragma unroll
+      for (int m = 1; m <= kListChain; ++m)
+        if (m == pos) t = rc[m];
     }
-    const int t = min(tw, a.n - 1);
+    if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) a.step_obj[obj_step] = fx_to_double((long long)sL, S);
     if (t >= lo && t < lo + cnt && tid == 0) {
       ssel[t - lo] = 1;
       a.selected[step] = t;
       if (a.step_gain) a.step_gain[step] = fx_to_double(sG[t - lo], S);
     }
-    // The winner's hits from its list: waves 0-3, lane e of the list at
-    // 1 + 64 w + lane (plain loads: the lists are fixed since the build).
-    const int par = step & 1;
-    if (w < 4) {
-      const uint4* lw = reinterpret_cast<const uint4*>(a.lists + size_t(t) * (2 * kListSlots));
-      const int e = 1 + w * 64 + lane;
-      const uint4 hv = lw[0];
-      const uint4 ev = e < kListSlots ? lw[e] : uint4{0u, 0u, 0u, 0u};
-      const int m = min(int(hv.x), kListMax);
-      const bool valid = e <= m;
-      const int j = valid ? min(int(ev.x), a.n - 1) : 0;
-      const float x = __uint_as_float(ev.y);
-      const float bo = valid ? sball[j] : 0.f;
-      const bool hit = valid && x < bo;
-      const unsigned long long mk = __ballot(hit);
-      if (mk) {
-        int at = 0;
-        if (lane == 0) at = atomicAdd(&scnt[par], __popcll(mk));
-        at = __builtin_amdgcn_readlane(at, 0);
-        if (hit) {
-          const int q = at + __popcll(mk & ((1ull << lane) - 1ull));
-          lj[q] = j;
-          lbo[q] = bo;
-          lbn[q] = x;
-          lv[q] = __uint_as_float(ev.z);
+    // The winner's hits, from the waves that hold its list (slot pos): each
+    // lowers its target's best cost (a target appears once in a list).
+    long long dobj = 0;
+#pragma unroll
+    for (int q = 0; q < kListSets; ++q) {
+      if (2 * q + half != pos) continue;   // uniform over the wave
+      if (eok[q]) {
+        const int j = ej[q];
+        const float x = ec[q], bo = sball[j];
+        if (x < bo) {
+          sball[j] = x;
+          if (blk == 0) dobj = (long long)(fx_scaled(evs[q], x) - fx_scaled(evs[q], bo));
+          if (a.assign && unsigned(j - lo) < unsigned(cnt)) a.assign[j] = t;
         }
       }
     }
     __syncthreads();
-    const int total = scnt[par];
-    if (tid == 0) scnt[par ^ 1] = 0;   // last read in the previous step, next used in the next
-    // Hits h = w, w + 8, ...: the lanes scan the hit's bucket for the own
-    // pairs with that target; their gain changes add up in LDS as 64-bit
-    // integers, the same terms as the rows of T give.
-    long long dobj = 0;
-    for (int h = w; h < total; h += kWaves) {
-      const int j = lj[h];
-      const float bo = lbo[h], bn = lbn[h];
-      const double vs = fx_scale(double(lv[h]), S);
-      const int bk = j >> kBucketShift;
-      const int y1 = int(sbk[bk]);
-      for (int y = (bk ? int(sbk[bk - 1]) : 0) + lane; y < y1; y += 64)
-        if (sej[y] == (unsigned short)j) {
-          const float cv = secv[y];
-          if (cv < bo) atomicAdd(&sdelta[sec[y]], fx_scaled(vs, fmaxf(bn - cv, 0.f)) - fx_scaled(vs, bo - cv));
+    if (dobj != 0) atomicAdd(&sL, (unsigned long long)dobj);
+    obj_step = step;
+    // Own pairs whose best cost fell: their candidates' gain changes, added
+    // up in LDS as 64-bit integers (all reads issued before any is used).
+    {
+      float bq[kOwnSets];
+#pragma unroll
+      for (int q = 0; q < kOwnSets; ++q) bq[q] = sball[pj[q] & 0xffff];
+      bool any = false;
+#pragma unroll
+      for (int q = 0; q < kOwnSets; ++q) any |= bq[q] < pb[q];
+      if (any) {
+#pragma unroll
+        for (int q = 0; q < kOwnSets; ++q) {
+          const float bn = bq[q], bo = pb[q];
+          if (bn < bo) {
+            const float cv = pc[q];
+            if (cv < bo) {
+              const double vs = fx_scale(double(pv[q]), S);
+              atomicAdd(&sdelta[pj[q] >> 16], fx_scaled(vs, fmaxf(bn - cv, 0.f)) - fx_scaled(vs, bo - cv));
+            }
+            pb[q] = bn;
+          }
         }
-      if (lane == 0) {
-        if (blk == 0) dobj += (long long)(fx_scaled(vs, bn) - fx_scaled(vs, bo));
-        sball[j] = bn;
-        if (a.assign && unsigned(j - lo) < unsigned(cnt)) a.assign[j] = t;
       }
     }
-    if (blk == 0 && lane == 0) sLw[w] += dobj;
-    obj_step = step;
+    // The chain candidates still ahead (slots above pos): their changes in
+    // the step, from the entries whose best cost fell, into LDS.
+#pragma unroll
+    for (int q = 0; q < kListSets; ++q) {
+      const int sl = 2 * q + half;
+      if (sl <= pos || sl > kListChain) continue;   // uniform over the wave
+      long long d = 0;
+      if (eok[q]) {
+        const float bn = sball[ej[q]], bo = eb[q];
+        if (bn < bo) {
+          const float cv = ec[q];
+          if (cv < bo) d = (long long)(fx_scaled(evs[q], fmaxf(bn - cv, 0.f)) - fx_scaled(evs[q], bo - cv));
+          eb[q] = bn;
+        }
+      }
+      if (__ballot(d != 0)) {
+        d = wave_sum_i64(d);
+        if (lane == 0) atomicAdd(&sacc[sl], (unsigned long long)d);
+      }
+    }
     __syncthreads();
     if (tid < 64) {
       if (tid < cnt) sG[tid] += (long long)sdelta[tid];
       sdelta[tid] = 0ull;
     }
-    if (step + 1 < a.k) publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, xc & 1, blk), epoch_of(xc));
+    bool next = false;
+    if (pos < kListChain && step + 1 < a.k) {
+      int rn = -1;
+      long long gr = 0;
+      unsigned long long u = 0ull;
+#pragma unroll
+      for (int m = 1; m <= kListChain; ++m)
+        if (m == pos + 1) {
+          rn = rc[m];
+          gr = acc[m];
+          u = ub[m];
+        }
+      gr += (long long)sacc[pos + 1];
+      next = rn >= 0 && gr > 0 && (pack_key(fx_to_double(gr, S), rn) >> kIndexBits) > u;
+    }
+    // Wave 0 folded the gains itself, so it publishes without a barrier.
+    if (step + 1 < a.k && !next) publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, xc & 1, blk), epoch_of(xc));
+    predicted = next;
+    pos += next ? 1 : 0;
   }
   __syncthreads();
-  if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) {
-    long long L = 0;
-#pragma unroll
-    for (int q = 0; q < kWaves; ++q) L += sLw[q];
-    a.step_obj[obj_step] = fx_to_double(L, S);
-  }
+  if (blk == 0 && tid == 0 && obj_step >= 0 && a.step_obj) a.step_obj[obj_step] = fx_to_double((long long)sL, S);
 }
 
 // The fixed-point scale of a scene (one block; the sum in the same order as
