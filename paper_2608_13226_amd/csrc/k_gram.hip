@@ -188,18 +188,12 @@ constexpr int kBigK = 64;
 // groups.
 __device__ __forceinline__ int swz(int row, int chunk) { return row * 8 + (chunk ^ ((row >> 1) & 7)); }
 
-// Map a linear block index to an upper tile.  Blocks are dealt to the 8 XCDs
-// round-robin, so each XCD gets a contiguous range of the linear order; that
-// order walks the upper triangle in bands of kBand tile rows, column by
-// column, so the ~32 tiles resident on one XCD span about 4 row and 8 column
-// panels and share their K slabs through the XCD's L2.  Each band starts with
-// a triangle (column r0 + j holds j + 1 tiles, j < rows - 1) followed by full
-// columns of `rows` tiles.  Returns false for padding blocks.
+// The upper tile at position `lin` of the band order: the triangle is walked
+// in bands of kBand tile rows, column by column.  Each band starts with a
+// triangle (column r0 + j holds j + 1 tiles, j < rows - 1) followed by full
+// columns of `rows` tiles.
 constexpr int kBand = 8;
-__device__ __forceinline__ bool big_tile(int b, int nb, int T, int& ti, int& tj) {
-  const int per = (nb + 7) / 8;
-  int lin = (b % 8) * per + b / 8;
-  if (lin >= nb) return false;
+__device__ __forceinline__ bool band_tile(int lin, int T, int& ti, int& tj) {
   for (int r0 = 0; r0 < T; r0 += kBand) {
     const int rows = min(kBand, T - r0);
     const int tri = rows * (rows - 1) / 2;
@@ -222,17 +216,30 @@ __device__ __forceinline__ bool big_tile(int b, int nb, int T, int& ti, int& tj)
   return false;
 }
 
-// Slab loader: instruction i of wave w (eight waves) fills LDS slots
-// (4 w + i) * 64 + lane of one operand (slot = row * 8 + physical chunk), i.e.
-// row 32 w + 8 i + lane / 8 at physical chunk lane % 8, holding logical chunk
-// (lane % 8) ^ (lane / 16) ^ (4 (i % 2)).  `voff_even` / `voff_odd` are the
-// lane's byte offsets for i = 0 / 1 at k = 0; rows past the feature matrix
-// read as zero (buffer range check).
+// Map block b of the `nb` full-tile blocks to an upper tile.  Blocks are
+// dealt to the 8 XCDs round-robin, so each XCD gets a contiguous range of
+// the band order: the ~32 tiles resident on one XCD span about 4 row and 8
+// column panels and share their K slabs through the XCD's L2.  Returns false
+// for padding blocks.
+__device__ __forceinline__ bool big_tile(int b, int nb, int T, int& ti, int& tj) {
+  const int per = (nb + 7) / 8;
+  const int lin = (b % 8) * per + b / 8;
+  if (lin >= nb) return false;
+  return band_tile(lin, T, ti, tj);
+}
+
+// Slab loader for R-row operands: instruction i < R / 64 of wave w (eight
+// waves) fills LDS slots (R / 64 w + i) * 64 + lane of one operand (slot =
+// row * 8 + physical chunk), i.e. row R / 8 w + 8 i + lane / 8 at physical
+// chunk lane % 8, holding logical chunk (lane % 8) ^ (lane / 16) ^ (4 (i %
+// 2)).  `voff_even` / `voff_odd` are the lane's byte offsets for i = 0 / 1 at
+// k = 0; rows past the feature matrix read as zero (buffer range check).
+template <int R>
 __device__ __forceinline__ void load_slab(uint4* dst, __amdgpu_buffer_rsrc_t rsrc, int voff_even, int voff_odd,
                                           int row_step, int k0, int wave) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst + (wave * 4 + i) * 64, 16,
+  for (int i = 0; i < R / 64; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst + (wave * (R / 64) + i) * 64, 16,
                                              ((i & 1) ? voff_odd : voff_even) + (i >> 1) * row_step, k0 * 2, 0, 0);
 }
 
@@ -311,44 +318,40 @@ __device__ __forceinline__ void interleave_step() {
   {                                                                                      \
     __builtin_amdgcn_s_waitcnt(0xF70); /* vmcnt(0) */                                    \
     slab_barrier();                                                                      \
-    load_frags(fa[0], fb[0], ST, ST + kBig * 8, offa[0], offb[0]);                       \
+    load_frags(fa[0], fb[0], ST, ST + R * 8, offa[0], offb[0]);                          \
     __builtin_amdgcn_sched_barrier(0);                                                   \
     _Pragma("unroll") for (int kk = 0; kk < 4; ++kk) {                                   \
-      if (kk < 3) load_frags(fa[(kk + 1) & 1], fb[(kk + 1) & 1], ST, ST + kBig * 8,      \
+      if (kk < 3) load_frags(fa[(kk + 1) & 1], fb[(kk + 1) & 1], ST, ST + R * 8,         \
                              offa[kk + 1], offb[kk + 1]);                                \
       if (kk == 0 && LOAD >= 0) {                                                        \
-        load_slab(NX, rsrc, voff_a0, voff_a1, row_step, (LOAD) * kBigK, wave);           \
-        load_slab(NX + kBig * 8, rsrc, voff_b0, voff_b1, row_step, (LOAD) * kBigK, wave); \
+        load_slab<R>(NX, rsrc, voff_a0, voff_a1, row_step, (LOAD) * kBigK, wave);        \
+        load_slab<R>(NX + R * 8, rsrc, voff_b0, voff_b1, row_step, (LOAD) * kBigK, wave); \
       }                                                                                  \
       mma_step(acc, fa[kk & 1], fb[kk & 1]);                                             \
-      if (kk == 0) interleave_first();                                                   \
-      else if (kk < 3) interleave_step();                                                \
+      if (R == kBig && kk == 0) interleave_first();                                      \
+      else if (R == kBig && kk < 3) interleave_step();                                   \
       __builtin_amdgcn_sched_barrier(0);                                                 \
     }                                                                                    \
   }
 
-// Eight waves in a 2 x 4 arrangement of 128 x 64 wave tiles (4 x 2 MFMA 32 x
-// 32 tiles, 128 accumulators per lane), two waves per SIMD: while one waits
-// on LDS or a barrier the other keeps the matrix core busy.  Loads into one
-// stage stay in flight while the other is read.  Requires d % (2 * kBigK) == 0.
-__global__ __launch_bounds__(512) void gram_bf16_big_kernel(const uint16_t* __restrict__ F, int n, int d,
-                                                            const float* __restrict__ inv_norm,
-                                                            float* __restrict__ out, unsigned int* mf_bits,
-                                                            int ntiles, int T) {
-  int ti, tj;
-  if (!big_tile(blockIdx.x, ntiles, T, ti, tj)) return;
-  const int row0 = ti * kBig, col0 = tj * kBig;
-  // One LDS object per stage (A rows, then B rows), so the compiler can tell
-  // which stage each in-flight load targets.
-  __shared__ uint4 st0[2 * kBig * 8], st1[2 * kBig * 8];
+// Eight waves in a 2 x 4 arrangement of (R / 2) x (R / 4) wave tiles (R / 64
+// x R / 128 MFMA 32 x 32 tiles; at R = 256, 128 accumulators per lane), two
+// waves per SIMD: while one waits on LDS or a barrier the other keeps the
+// matrix core busy.  Loads into one stage stay in flight while the other is
+// read.  Requires d % (2 * kBigK) == 0.
+template <int R>
+__device__ __forceinline__ void gram_big_tile(const uint16_t* __restrict__ F, int n, int d,
+                                              const float* __restrict__ inv_norm, float* __restrict__ out,
+                                              unsigned int* mf_bits, int row0, int col0, uint4* st0, uint4* st1) {
+  constexpr int MT = R / 64, NT = R / 128;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;
 
-  f32x16 acc[4][2];
+  f32x16 acc[MT][NT];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < MT; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NT; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
@@ -357,7 +360,7 @@ __global__ __launch_bounds__(512) void gram_bf16_big_kernel(const uint16_t* __re
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(F), 0, n * d * 2, 0x00020000);
   const int lrow = lane >> 3, lc_even = (lane & 7) ^ (lane >> 4), lc_odd = lc_even ^ 4;
-  const int ra = row0 + wave * 32 + lrow, rb = col0 + wave * 32 + lrow;
+  const int ra = row0 + wave * (R / 8) + lrow, rb = col0 + wave * (R / 8) + lrow;
   const int voff_a0 = (ra * d + lc_even * 8) * 2, voff_a1 = ((ra + 8) * d + lc_odd * 8) * 2;
   const int voff_b0 = (rb * d + lc_even * 8) * 2, voff_b1 = ((rb + 8) * d + lc_odd * 8) * 2;
   const int row_step = 32 * d;    // 16 rows, in bytes
@@ -367,14 +370,14 @@ __global__ __launch_bounds__(512) void gram_bf16_big_kernel(const uint16_t* __re
   int offa[4], offb[4];
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) {
-    offa[kk] = swz(wm * 128 + (lane & 31), kk * 2 + (lane >> 5));
-    offb[kk] = swz(wn * 64 + (lane & 31), kk * 2 + (lane >> 5));
+    offa[kk] = swz(wm * (R / 2) + (lane & 31), kk * 2 + (lane >> 5));
+    offb[kk] = swz(wn * (R / 4) + (lane & 31), kk * 2 + (lane >> 5));
   }
 
-  bf16x8 fa[2][4], fb[2][2];
+  bf16x8 fa[2][MT], fb[2][NT];
   const int nslabs = d / kBigK;   // even, at least 2
-  load_slab(st0, rsrc, voff_a0, voff_a1, row_step, 0, wave);
-  load_slab(st0 + kBig * 8, rsrc, voff_b0, voff_b1, row_step, 0, wave);
+  load_slab<R>(st0, rsrc, voff_a0, voff_a1, row_step, 0, wave);
+  load_slab<R>(st0 + R * 8, rsrc, voff_b0, voff_b1, row_step, 0, wave);
   int s = 0;
   for (; s + 2 < nslabs; s += 2) {
     CP_BIG_SLAB(st0, st1, s + 1)
@@ -382,8 +385,35 @@ __global__ __launch_bounds__(512) void gram_bf16_big_kernel(const uint16_t* __re
   }
   CP_BIG_SLAB(st0, st1, s + 1)
   CP_BIG_SLAB(st1, st0, -1)
+  store_df(acc, row0 + wm * (R / 2), col0 + wn * (R / 4), lane, n, inv_norm, out, mf_bits);
+}
 #undef CP_BIG_SLAB
-  store_df(acc, row0 + wm * 128, col0 + wn * 64, lane, n, inv_norm, out, mf_bits);
+
+// Blocks [0, nfull) take full 256 x 256 tiles (band order, XCD-aware); the
+// tiles after them, which would fill only part of a last round of the
+// device's compute units, are split into four 128 x 128 quarters, block
+// nfull + 4 t + q taking quarter q (row half q / 2, column half q % 2) of
+// tile nfull + t in band order.  A diagonal tile's lower-left quarter lies
+// below the diagonal and is left out.
+__global__ __launch_bounds__(512) void gram_bf16_big_kernel(const uint16_t* __restrict__ F, int n, int d,
+                                                            const float* __restrict__ inv_norm,
+                                                            float* __restrict__ out, unsigned int* mf_bits,
+                                                            int nfull, int ntiles, int T) {
+  // One LDS object per stage (A rows, then B rows), so the compiler can tell
+  // which stage each in-flight load targets.
+  __shared__ uint4 st0[2 * kBig * 8], st1[2 * kBig * 8];
+  int ti, tj;
+  const int b = blockIdx.x;
+  if (b < nfull) {
+    if (!big_tile(b, nfull, T, ti, tj)) return;
+    gram_big_tile<kBig>(F, n, d, inv_norm, out, mf_bits, ti * kBig, tj * kBig, st0, st1);
+    return;
+  }
+  const int lin = nfull + (b - nfull) / 4, q = (b - nfull) % 4;
+  if (lin >= ntiles || !band_tile(lin, T, ti, tj)) return;
+  if (ti == tj && q == 2) return;
+  gram_big_tile<kBig / 2>(F, n, d, inv_norm, out, mf_bits, ti * kBig + (q >> 1) * (kBig / 2),
+                          tj * kBig + (q & 1) * (kBig / 2), st0, st1);
 }
 
 // ---------------------------------------------------------------------------
@@ -472,9 +502,16 @@ hipError_t launch_gram(const FstParams& p, const FstScratch& s, hipStream_t stre
   if (p.bf16 && p.d % (2 * kBigK) == 0 && p.n >= 4096 && int64_t(p.n) * p.d < (int64_t(1) << 30)) {
     const int t = (p.n + kBig - 1) / kBig;
     const int tiles = t * (t + 1) / 2;
-    const int blocks = (tiles + 7) / 8 * 8;
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    // Whole rounds of full tiles (a multiple of 8 blocks, for the XCD
+    // dealing), the rest as quarter tiles.
+    const int nfull = cus > 0 ? tiles / cus * cus / 8 * 8 : tiles / 8 * 8;
+    const int blocks = nfull + 4 * (tiles - nfull);
     gram_bf16_big_kernel<<<blocks, 512, 0, stream>>>(static_cast<const uint16_t*>(p.feats), p.n, p.d,
-                                                       s.inv_norm, p.cost, s.mf_bits, tiles, t);
+                                                       s.inv_norm, p.cost, s.mf_bits, nfull, tiles, t);
     return hipGetLastError();
   }
   const int t = (p.n + kTile - 1) / kTile;
