@@ -356,8 +356,12 @@ def main():
     # row of N costs per target whose best cost the pick lowers.  The number of
     # such (step, target) pairs is replayed on the host from the cost and the
     # picks, outside the timed region.  The transposed copy that the rows
-    # schedule writes in its step-0 pass is not counted.  The compact schedule
-    # (changes exchanged between blocks, no copy) is timed beside it.
+    # schedule writes in its step-0 pass and the candidate lists of its later
+    # steps are not counted.  The unit is the whole sgs_select call (its
+    # kernels run back to back on one stream: slot clearing, scale, first
+    # pass, rows kernel for the first 128 steps, list build, list kernel), so
+    # one pair of events brackets it.  The compact schedule (changes exchanged
+    # between blocks, no copy) is timed beside it.
     compact = None
     if args.sgs == "incremental":
         c_ms, rc = time_sgs(True, 1, compact=True)
@@ -375,8 +379,10 @@ def main():
         sgs_bytes = 4.0 * n * n + 4.0 * n * k + 4.0 * n * changed
         sgs_gbs = sgs_bytes / (s_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(sgs_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(sgs_gbs / HBM_PEAK_GBS, 4), "traffic": traffic("sgs_rows_kernel", cfg.name),
-                    "kernel": "sgs_rows_kernel", "bytes_per_launch": sgs_bytes, "ms_per_launch": round(s_ms, 3),
+                    "frac": round(sgs_gbs / HBM_PEAK_GBS, 4), "traffic": traffic("sgs_select", cfg.name),
+                    "kernel": "sgs_select (inc_first_pass_kernel, sgs_rows_kernel, list_build_kernel, "
+                              "sgs_list_kernel)",
+                    "bytes_per_launch": sgs_bytes, "ms_per_launch": round(s_ms, 3),
                     "changed_targets": changed, "us_per_greedy_step": round(s_ms * 1e3 / k, 2)}
     else:
         roofline = {key: dense[key] for key in ("bound", "achieved", "peak", "unit", "frac", "traffic", "kernel")}
@@ -406,7 +412,8 @@ def main():
         "greedy_us_per_step": round(s_ms * 1e3 / k, 3),
         "greedy_over_floor": round(s_ms * 1e3 / k / step_floor_us, 3), "rounds": floor_rounds,
         "note": "coverprune_step_floor: rounds of the greedy's candidate exchange (+ the dependent read of the "
-                "winner's 64 KB row); greedy_us_per_step is the whole sgs_select call over K"}
+                "winner's 64 KB row); greedy_us_per_step is the whole sgs_select call over K, whose steps "
+                "after the 128th skip the exchange when the winner is predicted"}
 
     # Local greedy (Eq. 13) on the same cost: the g-nearest tables, then the
     # greedy with gains over each candidate's table row.  The paper leaves g
