@@ -186,11 +186,17 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
  *             For n <= 32768 every compute unit keeps all n best costs and
  *             finds the targets a pick improves itself, from the pick's row
  *             of a source-major copy of the cost that the first pass writes
- *             into the workspace (4 n^2 bytes, 1 GiB at n = 16384); larger
- *             scenes, or CP_SGS_INCREMENTAL | CP_SGS_COMPACT, exchange the
- *             improved targets between the compute units instead (about 45
- *             bytes per token, slower per step).  Both schedules sum the
- *             same integers and return the same result.
+ *             into the workspace (4 n^2 bytes, 1 GiB at n = 16384).  For
+ *             n <= 16384 and k > 128 the steps after the 128th run from
+ *             per-candidate lists of the targets each candidate can still
+ *             improve (4 KB per token in the workspace), with the next
+ *             winner predicted without an exchange when bounds that every
+ *             compute unit computes identically prove it; the same
+ *             integers, so the same picks.  Larger scenes, or
+ *             CP_SGS_INCREMENTAL | CP_SGS_COMPACT, exchange the improved
+ *             targets between the compute units instead (about 45 bytes
+ *             per token, slower per step).  Both schedules sum the same
+ *             integers and return the same result.
  *   selected        [k] int32 output: tokens in the order they were chosen
  *   step_gain       [k] double output (may be NULL): gain of each step
  *   step_objective  [k] double output (may be NULL): L(S) after each step
@@ -201,7 +207,8 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
 /* Workspace for one form (flags as for coverprune_sgs_select; 0 for flags it
  * does not accept): the dense form needs about 9 MB at n = 16384 (private
  * best costs and float64 partial gains of up to 64 row panels), the
- * incremental form 4 n + 45 bytes per token up to n = 32768 and about 45
+ * incremental form 4 n + 45 bytes per token up to n = 32768 (plus 4 KB per
+ * token for the candidate lists when n <= 16384 and k > 128) and about 45
  * bytes per token beyond that or with CP_SGS_COMPACT, each plus about
  * 100 KB of exchange slots. */
 size_t coverprune_sgs_workspace(int64_t n, int64_t k, uint32_t flags);
