@@ -151,11 +151,15 @@ hipError_t launch_mark_aborted(const unsigned int* abort, int32_t* selected, int
 
 // Grid barrier for a cooperative launch: every block counts itself in and
 // waits until all gridDim.x blocks have arrived `round` times.  `counter`
-// must be zero at launch.  Only data written with put() before the barrier
-// may be read with get() after it.  Returns false, in every thread of the
-// block, when the wait gave up (see give_up): the block must then leave.
+// must be zero at launch.  Only data written with put() (or device-scope
+// atomics) before the barrier may be read with get() after it: every wave
+// first waits until its own such writes are acknowledged, then the block's
+// waves meet, and only then does the block count itself in.  Returns false,
+// in every thread of the block, when the wait gave up (see give_up): the
+// block must then leave.
 __device__ __forceinline__ bool grid_barrier(unsigned int* counter, unsigned int round, unsigned int* abort,
                                              unsigned int limit, int* sflag) {
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's stores and atomics are done
   __syncthreads();
   if (threadIdx.x == 0) {
     __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

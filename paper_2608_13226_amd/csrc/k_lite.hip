@@ -6,7 +6,10 @@
 //     keys     q = floor((x - min) * 256 / h) in float64, clamped to 21 bits;
 //              key = 3-way bit interleave; voxel = q >> 8
 //     sort     stable LSD radix sort of (key, token) in 8-bit digits over the
-//              key bits in use; equal keys stay in token order
+//              key bits in use; equal keys stay in token order.  A pass's
+//              digit counts per block range are added up while the pass
+//              before it places its elements (by the range that receives
+//              each), so a pass needs one grid barrier
 //     groups   V = floor(v * 2^40) in exact integers; an exclusive scan gives
 //              the mass before each position, t(p) = min(K-1, K * mass / W);
 //              a prefix-min scan of t(p) - p and the K - N + p floor give the
@@ -40,6 +43,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kFrontBlocks = 64;
+constexpr int kMaxPasses = 8;          // 8-bit digits of a key of at most 63 bits
 constexpr int kBins = 256;
 constexpr int kAxisBits = 21;
 constexpr int kSubBits = 8;
@@ -64,7 +68,7 @@ struct LiteDev {
   int* tok[2];
   unsigned long long* vox_tok;  // [n] packed voxel of each token
   unsigned long long* vox_pos;  // [n] packed voxel of each sorted position
-  unsigned int* hist;           // [G][256]
+  unsigned int* hist;           // [kMaxPasses][G][256]: digit counts of each pass's ranges
   unsigned long long* bsum;     // [G]
   int* bmin;                    // [G]
   int* gid;                     // [n] group of each sorted position
@@ -110,7 +114,7 @@ Layout layout(int64_t n, int64_t k) {
   L.tok1 = o;     o += a256(size_t(n) * 4);
   L.vox_tok = o;  o += a256(size_t(n) * 8);
   L.vox_pos = o;  o += a256(size_t(n) * 8);
-  L.hist = o;     o += a256(size_t(kFrontBlocks) * kBins * 4);
+  L.hist = o;     o += a256(size_t(kMaxPasses) * kFrontBlocks * kBins * 4);
   L.bsum = o;     o += a256(size_t(kFrontBlocks) * 8);
   L.bsum2 = o;    o += a256(size_t(kFrontBlocks) * 8);
   L.bmin = o;     o += a256(size_t(kFrontBlocks) * 4);
@@ -267,7 +271,9 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
   __shared__ unsigned int s_wcnt[kWaves][kBins];
   __shared__ int s_minoff;
 
-  // ---- bbox minimum per axis
+  // ---- this block's rows of every pass's digit counts start at zero (the
+  // first additions come after the next barrier); bbox minimum per axis
+  for (int q = t; q < kMaxPasses * kBins; q += kThreads) put(a.hist + (size_t(q / kBins) * G + blk) * kBins + q % kBins, 0u);
   {
     unsigned int m[3] = {0xffffffffu, 0xffffffffu, 0xffffffffu};
     for (int i = p0 + t; i < p1; i += kThreads)
@@ -293,6 +299,8 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
                            double(float_from_order_key(get(a.ctrl + kCtrlBbox + 2)))};
     const double top = double((1 << kAxisBits) - 1);
     unsigned long long kmax = 0ull;
+    s_hist[t] = 0u;
+    __syncthreads();
     for (int i = p0 + t; i < p1; i += kThreads) {
       unsigned int q[3];
       for (int ax = 0; ax < 3; ++ax) {
@@ -304,6 +312,7 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       put(a.key[0] + i, key);
       put(a.tok[0] + i, i);
       put(a.vox_tok + i, pack_vox(q[0] >> kSubBits, q[1] >> kSubBits, q[2] >> kSubBits));
+      atomicAdd(&s_hist[unsigned(key & 0xffu)], 1u);
       kmax = max(kmax, key);
     }
     for (int o = 32; o > 0; o >>= 1) {
@@ -311,6 +320,8 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       kmax = max(kmax, y);
     }
     if (lane == 0) atomicMax(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey), kmax);
+    __syncthreads();
+    put(a.hist + size_t(blk) * kBins + t, s_hist[t]);   // pass 0: the block's own range, in token order
   }
   if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
 
@@ -324,26 +335,18 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     const int* ts = src ? a.tok[1] : a.tok[0];
     unsigned long long* kd = src ? a.key[0] : a.key[1];
     int* td = src ? a.tok[0] : a.tok[1];
-    s_hist[t] = 0u;
-    __syncthreads();
-    for (int i = p0 + t; i < p1; i += kThreads) atomicAdd(&s_hist[(get(ks + i) >> sh) & 0xffu], 1u);
-    __syncthreads();
-    put(a.hist + blk * kBins + t, s_hist[t]);
-    if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-
+    const unsigned int* hist = a.hist + size_t(pass) * G * kBins;
     // Base offset of digit t for this block: every smaller digit anywhere,
-    // plus digit t in earlier blocks.
+    // plus digit t in earlier blocks (all G counts read in one round trip).
     {
       unsigned int tot = 0u, pre = 0u;
-      for (int b0 = 0; b0 < G; b0 += 16) {
-        unsigned int h[16];
+      unsigned int h[kFrontBlocks];
 #pragma unroll
-        for (int x = 0; x < 16; ++x) h[x] = b0 + x < G ? get(a.hist + (b0 + x) * kBins + t) : 0u;
+      for (int x = 0; x < kFrontBlocks; ++x) h[x] = x < G ? get(hist + x * kBins + t) : 0u;
 #pragma unroll
-        for (int x = 0; x < 16; ++x) {
-          tot += h[x];
-          if (b0 + x < blk) pre += h[x];
-        }
+      for (int x = 0; x < kFrontBlocks; ++x) {
+        tot += h[x];
+        if (x < blk) pre += h[x];
       }
       unsigned long long total;
       const unsigned long long ex = block_excl_sum_u64(tot, s_u64, total);
@@ -352,12 +355,19 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     __syncthreads();
 
     // Stable scatter, 256 items per round: rank among equal digits inside a
-    // wave from ballots, then across the block's waves through LDS.
+    // wave from ballots, then across the block's waves through LDS.  The
+    // next round's element is loaded while this one is placed.
+    unsigned long long kn = p0 + t < p1 ? get(ks + p0 + t) : 0ull;
+    int tn = p0 + t < p1 ? get(ts + p0 + t) : 0;
     for (int c0 = p0; c0 < p1; c0 += kThreads) {
       const int i = c0 + t;
       const bool live = i < p1;
-      const unsigned long long kv = live ? get(ks + i) : 0ull;
-      const int tv = live ? get(ts + i) : 0;
+      const unsigned long long kv = kn;
+      const int tv = tn;
+      if (i + kThreads < p1) {
+        kn = get(ks + i + kThreads);
+        tn = get(ts + i + kThreads);
+      }
       const unsigned int dig = unsigned((kv >> sh) & 0xffu);
       unsigned long long same = __ballot(live);
       for (int bit = 0; bit < 8; ++bit) {
@@ -375,6 +385,12 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
         for (int q = 0; q < w; ++q) off += s_wcnt[q][dig];
         put(kd + off + rank, kv);
         put(td + off + rank, tv);
+        // The next pass's digit of this element, counted for the range
+        // that receives it.
+        if (pass + 1 < passes)
+          __hip_atomic_fetch_add(a.hist + (size_t(pass + 1) * G + (off + rank) / tile) * kBins +
+                                     unsigned((kv >> (sh + 8)) & 0xffu),
+                                 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       __syncthreads();
       unsigned int add = 0u;

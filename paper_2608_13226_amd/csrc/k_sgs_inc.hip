@@ -974,7 +974,8 @@ __global__ __launch_bounds__(256) void list_build_kernel(IncDev a) {
 // every thread updates the chain bounds and decides whether the next step is
 // predicted, and wave 0 folds the gains and publishes when it is not.
 constexpr int kListChain = 3;                         // predicted steps in a row at most
-constexpr int kListSets = (kListChain + 2) / 2;      // chain list entries a thread holds
+constexpr int kSlotsPerSet = kBlock / kListSlots;    // lists the block's threads hold side by side
+constexpr int kListSets = (kListChain + kSlotsPerSet) / kSlotsPerSet;   // chain list entries a thread holds
 
 __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   if (*a.lfail || *a.abort) return;
@@ -1044,10 +1045,10 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   // Chain slots: 0 the exchange's winner, m = 1 .. kListChain the candidate
   // r_m (-1 past the last), with lower bounds on their gains at the exchange
   // and the key bits they must beat.  Entry set q of a thread is entry
-  // (tid & 255) of slot 2 q + (tid >> 8)'s list: target, cost, scaled
-  // capacity, and the target's best cost as last seen (entry 0 of a list is
-  // its header).
-  const int half = tid >> 8, ent = tid & (kListSlots - 1);
+  // tid % kListSlots of slot q kSlotsPerSet + tid / kListSlots's list:
+  // target, cost, scaled capacity, and the target's best cost as last seen
+  // (entry 0 of a list is its header).
+  const int half = tid / kListSlots, ent = tid % kListSlots;
   int rc[kListChain + 1];
   long long acc[kListChain + 1];
   unsigned long long ub[kListChain + 1];
@@ -1112,7 +1113,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
       uint4 hv[kListSets], ev[kListSets];
 #pragma unroll
       for (int q = 0; q < kListSets; ++q) {
-        const int sl = 2 * q + half;
+        const int sl = q * kSlotsPerSet + half;
         int r = -1;
 #pragma unroll
         for (int m = 0; m <= kListChain; ++m)
@@ -1149,7 +1150,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
     long long dobj = 0;
 #pragma unroll
     for (int q = 0; q < kListSets; ++q) {
-      if (2 * q + half != pos) continue;   // uniform over the wave
+      if (q * kSlotsPerSet + half != pos) continue;   // uniform over the wave
       if (eok[q]) {
         const int j = ej[q];
         const float x = ec[q], bo = sball[j];
@@ -1191,7 +1192,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
     // the step, from the entries whose best cost fell, into LDS.
 #pragma unroll
     for (int q = 0; q < kListSets; ++q) {
-      const int sl = 2 * q + half;
+      const int sl = q * kSlotsPerSet + half;
       if (sl <= pos || sl > kListChain) continue;   // uniform over the wave
       long long d = 0;
       if (eok[q]) {
