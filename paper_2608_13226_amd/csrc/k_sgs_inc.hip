@@ -416,6 +416,11 @@ constexpr int kTrackMax = 256;   // hits of a step that still tracks the chain
 template <int NG, int RL>
 __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   extern __shared__ unsigned long long smem[];
+  // Hits a block lists in one step: with one column group the list is four
+  // times kCap (48 KB of LDS beside the 64 KB of best costs), which puts all
+  // but the first dense steps in one round; two groups keep 128 KB of best
+  // costs and the short list.
+  constexpr int kCapR = (NG == 1 ? 4 : 1) * kCap;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lo = blk * a.W;
   const int cnt = max(0, min(a.n, lo + a.W) - lo);
@@ -427,9 +432,9 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   __shared__ int si[kWaves];
   __shared__ unsigned long long su[kWaves];
   __shared__ int sflag;
-  __shared__ int lj[kCap];                    // hit list: target
-  __shared__ float lbo[kCap];                 // old best cost
-  __shared__ float lbn[kCap];                 // new best cost
+  __shared__ int lj[kCapR];                    // hit list: target
+  __shared__ float lbo[kCapR];                 // old best cost
+  __shared__ float lbn[kCapR];                 // new best cost
   __shared__ int scnt[2];                     // hits listed in steps of each parity
   __shared__ int schunk[kRowsMaxN / kRowChunk];   // dense steps: hits per chunk, then their offsets
   if (tid == 0) scnt[0] = scnt[1] = 0;
@@ -692,7 +697,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
           for (int c = 0; c < 4; ++c) {
             const unsigned long long mk = c == 0 ? m0 : c == 1 ? m1 : c == 2 ? m2 : m3;
             const int e = at + __popcll(mk & lt);
-            if (((mk >> lane) & 1ull) && e < kCap) {
+            if (((mk >> lane) & 1ull) && e < kCapR) {
               lj[e] = j0 + c;
               lbo[e] = bo[c];
               lbn[e] = x[c];
@@ -708,13 +713,13 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     // than it saves, so a step with many hits ends the chain.
     if (total > kTrackMax) chain = kChain;
     if (tid == 0) scnt[par ^ 1] = 0;   // last read in the previous step, next used in the next
-    if (total <= kCap) {
+    if (total <= kCapR) {
       const int per = (total + kWaves - 1) / kWaves;
       const int e0 = min(total, w * per);
       apply(e0, min(total, e0 + per) - e0, true);
     } else {
       // Dense step (early in the greedy): the list is built and applied in
-      // rounds of kCap entries, each entry's place fixed by the hit counts
+      // rounds of kCapR entries, each entry's place fixed by the hit counts
       // of the chunks before it, and every round is shared evenly by the
       // waves.  b keeps its old values until the last round (the hit test is
       // repeated each round), then takes the new ones.
@@ -736,7 +741,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
         if (2 * lane + 1 < nch) schunk[2 * lane + 1] = incl - c1;
       }
       __syncthreads();
-      for (int r0 = 0; r0 < total; r0 += kCap) {
+      for (int r0 = 0; r0 < total; r0 += kCapR) {
         for (int q0 = w; q0 < nch; q0 += kWaves) {
           const int j0 = q0 * kRowChunk + 4 * lane;
           const f32x4 bo = *reinterpret_cast<const f32x4*>(sball + j0);
@@ -746,7 +751,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
             const bool hit = x[c] < bo[c];
             const unsigned long long mk = __ballot(hit);
             const int e = at + __popcll(mk & ((1ull << lane) - 1ull));
-            if (hit && e >= 0 && e < kCap) {
+            if (hit && e >= 0 && e < kCapR) {
               lj[e] = j0 + c;
               lbo[e] = bo[c];
               lbn[e] = x[c];
@@ -755,7 +760,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
           }
         }
         __syncthreads();
-        const int m = min(kCap, total - r0);
+        const int m = min(kCapR, total - r0);
         const int per = (m + kWaves - 1) / kWaves;
         const int e0 = min(m, w * per);
         apply(e0, min(m, e0 + per) - e0, false);
