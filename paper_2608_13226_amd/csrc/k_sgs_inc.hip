@@ -307,16 +307,24 @@ constexpr int kCap = kList * kWaves;   // hits a block lists in one step
 int rows_ldt(int64_t n) { return int((n + kRowChunk - 1) / kRowChunk * kRowChunk); }
 
 // Fixed-point scale, the same in every block (same sum, same order): every
-// partial gain is at most c0 sum(v) < 2^(62 - S).
+// partial gain is at most c0 sum(v) < 2^(62 - S), and every single term
+// v_j d 2^S (0 <= d <= c0) at most c0 max(v) 2^S < 2^52, which fx_diff
+// needs.
 __device__ __forceinline__ int fixed_scale(const IncDev& a, double* sd) {
-  double x = 0.0;
-  for (int j = threadIdx.x; j < a.n; j += kBlock) x += double(a.v[j]);
+  double x = 0.0, m = 0.0;
+  for (int j = threadIdx.x; j < a.n; j += kBlock) {
+    x += double(a.v[j]);
+    m = fmax(m, double(a.v[j]));
+  }
   const double M = double(a.c0) * block_sum_all(x, sd);
+  const double Mt = double(a.c0) * block_max_all(m, sd);
   int S = 0;
   if (M > 0.0) {
     int e = 0;
     (void)__builtin_frexp(M, &e);   // M < 2^e
     S = 62 - e;
+    (void)__builtin_frexp(Mt, &e);  // 0 < Mt <= M
+    S = min(S, 52 - e);
   }
   return S;
 }
@@ -449,7 +457,10 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   // (the same word for every block), and then starts from the state the
   // previous launch handed over.
   if (a.gate && *a.gate != a.gate_val) return;
-  const bool resume = a.k_begin > 0;
+  // After the early kernel the first step is the one it stopped before.
+  if (a.start && *a.abort) return;
+  const int k_begin = a.start ? int(*a.start) : a.k_begin;
+  const bool resume = k_begin > 0;
   if (resume && *a.abort) return;             // the launch before it gave up
   // The fixed-point scale, the step-0 gains (as P partial sums over row
   // ranges) and T come from the first-pass kernels.
@@ -474,7 +485,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
   // Block 0 keeps the objective as one running part per wave (as in the
   // exchange form).
   __shared__ long long sLw[kWaves];
-  int obj_step = a.k_begin - 1;
+  int obj_step = k_begin - 1;
   if (blk == 0) {
     long long L0 = 0;
     if (resume) {
@@ -515,7 +526,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     acc[m] = 0;
     ub[m] = 0ull;
   }
-  for (int step = a.k_begin; step < a.k_end; ++step) {
+  for (int step = k_begin; step < a.k_end; ++step) {
     int tw;
     if (predicted) {
       __syncthreads();
@@ -628,7 +639,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
         const int nbt = min(kChunk, base + m - e0);
         const int cj = jl;
         const float cbo = bol, cbn = bnl;
-        // Each lane's entry capacity scaled once for fx_scaled (0 past the
+        // Each lane's entry capacity scaled once for fx_diff (0 past the
         // batch, where v was not read).
         const double cvs = fx_scale(double(vl), S);
         const long long cvb = __double_as_longlong(cvs);
@@ -654,8 +665,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
               // A column that cost at least the old best contributes 0
               // before and after.
               const float xx = cx[u][q];
-              if (q * 64 + lane < cnt && xx < bo)
-                g[q] += (long long)(fx_scaled(vs, fmaxf(bn - xx, 0.f)) - fx_scaled(vs, bo - xx));
+              if (q * 64 + lane < cnt && xx < bo) g[q] += fx_diff(vs, fmaxf(bn - xx, 0.f), bo - xx);
             }
           }
         }
@@ -665,8 +675,8 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
 #pragma unroll
           for (int c = 0; c < kChain; ++c)
             if (live(c) && cr[c] < cbo)
-              dr[c] += (long long)(fx_scaled(cvs, fmaxf(cbn - cr[c], 0.f)) - fx_scaled(cvs, cbo - cr[c]));
-          if (blk == 0) dobj += (long long)(fx_scaled(cvs, cbn) - fx_scaled(cvs, cbo));
+              dr[c] += fx_diff(cvs, fmaxf(cbn - cr[c], 0.f), cbo - cr[c]);
+          if (blk == 0) dobj += fx_diff(cvs, cbn, cbo);
           if (setb) sball[cj] = cbn;
           if (a.assign && unsigned(cj - lo) < unsigned(cnt)) a.assign[cj] = t;
         }
@@ -879,6 +889,293 @@ __global__ __launch_bounds__(kBlock) void sgs_inc_kernel(IncDev a) { inc_body(a,
 
 template <int NG, int RL>
 __global__ __launch_bounds__(kBlock) void sgs_rows_kernel(IncDev a) { rows_body<NG, RL>(a, blockIdx.x, gridDim.x); }
+
+// ---------------------------------------------------------------------------
+// The rows schedule's early steps.
+//
+// A pick early in the greedy lowers the best cost of thousands of targets
+// (about a fifth of all targets in each of the first 16 steps at N = 16384),
+// and the rows kernel has every block read its own 64 columns of each such
+// target's row of the cost: a 256-byte piece of thousands of rows per block
+// and step, which the memory system serves at well under half its streaming
+// rate.  Here the step's hits are split instead.  Every block still finds all
+// of them from the winner's row of T (each block keeps every best cost);
+// block b then takes the b-th equal share of the hit list (in target order),
+// reads its targets' whole rows of the cost (contiguous, 64 KB each at
+// N = 16384) and sums the gain changes of all n columns, the same 64-bit
+// fixed-point terms as the rows kernel, into registers.  It writes the sums
+// to its row of a [blocks] x [n] table, with the objective's change of its
+// share after them, and raises its flag for the step; every block then adds,
+// for its own columns, the rows of all blocks whose share was not empty.  The
+// gains are the same integers as in the rows kernel (integer sums do not
+// depend on their order), so the picks are the same.
+//
+// The kernel runs while a step improves at least kEarlyMinHits targets, and
+// at most until the lists take over (or to the end), then hands its state
+// to the rows kernel as the rows kernel hands it to the list kernel, with the
+// next step in ho_misc[2].  One column group only (n <= kEarlyMaxN): a
+// thread holds the changes of n / kBlock columns.
+constexpr int kEarlyMaxN = kRowChunk * kWaves * 8;    // 16384, the one-group rows kernel's reach
+constexpr int kEarlyCols = kEarlyMaxN / kBlock;       // columns per thread: 32
+constexpr int kEarlyPass = 8;                         // of which one pass over the share sums
+constexpr int kEarlyDepth = 4;                        // rows whose loads are in flight
+constexpr int kEarlyShare = 64;                       // hits a block takes per step at most (W <= 64)
+constexpr int kEarlyMinHits = 512;                    // steps with fewer hits go back to the rows kernel
+
+int early_ldp(int64_t n) { return int((n + 1 + 63) / 64 * 64); }
+bool early_for(int64_t n, int W) { return n <= kEarlyMaxN && W <= 64; }
+
+__global__ __launch_bounds__(kBlock) void sgs_early_kernel(IncDev a) {
+  extern __shared__ unsigned long long smem[];
+  constexpr int RL = 8;                               // chunk loads per wave: n <= kRowChunk kWaves RL
+  const int blk = blockIdx.x, nb = gridDim.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lo = blk * a.W;
+  const int cnt = max(0, min(a.n, lo + a.W) - lo);
+  long long* sG = reinterpret_cast<long long*>(smem);             // [W] running gains (W rounded up to even)
+  float* sball = reinterpret_cast<float*>(sG + ((a.W + 1) & ~1));  // [ldt] b_j; -inf past n
+  unsigned char* ssel = reinterpret_cast<unsigned char*>(sball + a.ldt);   // [W] chosen columns
+  __shared__ long long red[kBlock];
+  __shared__ unsigned long long su[kWaves];
+  __shared__ unsigned long long sk1[kMaxBlocks], sk2[kMaxBlocks];
+  __shared__ int sflag;
+  __shared__ int schunk[kEarlyMaxN / kRowChunk];     // hits per chunk of the winner's row, then their offsets
+  __shared__ int stot;
+  __shared__ int sj[kEarlyShare];                     // the block's share: target, old and new best cost,
+  __shared__ float sbo[kEarlyShare], sbn[kEarlyShare];
+  __shared__ double svs[kEarlyShare];                 // and its capacity scaled for fx_diff
+
+  const int S = *a.scale;
+  for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
+  for (int i = tid; i < cnt; i += kBlock) {
+    ssel[i] = 0;
+    long long g = 0;
+    for (int q = 0; q < a.P; ++q) g += a.part[size_t(q) * a.n + lo + i];
+    sG[i] = g;
+  }
+  __syncthreads();
+  // Block 0 keeps the objective (in wave 1 after the start).
+  long long L = 0;
+  if (blk == 0) {
+    long long x = 0;
+    for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
+    L = block_sum_i64(x, red);
+  }
+  publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0));
+
+  const int nch = a.ldt / kRowChunk;
+  const int k_stop = a.k_end;                         // steps [0, k_stop) at most
+  long long* mine = a.epart + size_t(blk) * a.ldp;
+  int xc = 0;
+  for (int step = 0; step < k_stop; ++step) {
+    const int tw = read_winner_rows(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, a.poll_limit, su,
+                                    &sflag, sk1, sk2);
+    ++xc;
+    if (tw < 0) return;
+    const int t = min(tw, a.n - 1);
+    if (t >= lo && t < lo + cnt && tid == 0) {
+      ssel[t - lo] = 1;
+      a.selected[step] = t;
+      if (a.step_gain) a.step_gain[step] = fx_to_double(sG[t - lo], S);
+    }
+
+    // The winner's row of T: every wave its chunks, all loads in flight.
+    const f32x4* row = reinterpret_cast<const f32x4*>(a.T + size_t(t) * a.ldt);
+    f32x4 xr[RL];
+#pragma unroll
+    for (int i = 0; i < RL; ++i)
+      if (w + i * kWaves < nch) xr[i] = row[(w + i * kWaves) * (kRowChunk / 4) + lane];
+    // Hits per chunk, their offsets in target order, and the total.
+#pragma unroll
+    for (int i = 0; i < RL; ++i) {
+      const int q0 = w + i * kWaves;
+      if (q0 < nch) {
+        const f32x4 bo = *reinterpret_cast<const f32x4*>(sball + q0 * kRowChunk + 4 * lane);
+        const f32x4 x = xr[i];
+        const int c = __popcll(__ballot(x[0] < bo[0])) + __popcll(__ballot(x[1] < bo[1])) +
+                      __popcll(__ballot(x[2] < bo[2])) + __popcll(__ballot(x[3] < bo[3]));
+        if (lane == 0) schunk[q0] = c;
+      }
+    }
+    __syncthreads();
+    if (w == 0) {
+      const int c0 = 2 * lane < nch ? schunk[2 * lane] : 0;
+      const int c1 = 2 * lane + 1 < nch ? schunk[2 * lane + 1] : 0;
+      const int incl = wave_scan_incl(c0 + c1);
+      if (2 * lane < nch) schunk[2 * lane] = incl - c0 - c1;
+      if (2 * lane + 1 < nch) schunk[2 * lane + 1] = incl - c1;
+      if (lane == 63) stot = incl;
+    }
+    __syncthreads();
+    const int H = stot;
+    const int per = (H + nb - 1) / nb;                // at most ceil(n / nb) <= W
+    const int e_lo = min(H, blk * per), e_hi = min(H, e_lo + per);
+    const int nshare = per > 0 ? (H + per - 1) / per : 0;   // blocks with a share
+    // The block's share of the list; every target's new best cost; assign
+    // for the own targets.
+#pragma unroll
+    for (int i = 0; i < RL; ++i) {
+      const int q0 = w + i * kWaves;
+      if (q0 < nch) {
+        const int j0 = q0 * kRowChunk + 4 * lane;
+        f32x4 bo = *reinterpret_cast<const f32x4*>(sball + j0);
+        const f32x4 x = xr[i];
+        int at = schunk[q0];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const bool hit = x[c] < bo[c];
+          const unsigned long long mk = __ballot(hit);
+          const int e = at + __popcll(mk & ((1ull << lane) - 1ull));
+          if (hit) {
+            const int j = j0 + c;
+            if (e >= e_lo && e < e_hi) {
+              sj[e - e_lo] = j;
+              sbo[e - e_lo] = bo[c];
+              sbn[e - e_lo] = x[c];
+              svs[e - e_lo] = fx_scale(double(a.v[j]), S);
+            }
+            if (a.assign && unsigned(j - lo) < unsigned(cnt)) a.assign[j] = t;
+            bo[c] = x[c];
+          }
+          at += __popcll(mk);
+        }
+        *reinterpret_cast<f32x4*>(sball + j0) = bo;
+      }
+    }
+    __syncthreads();
+
+    // The share's rows of the cost, in passes over kEarlyPass of the
+    // thread's columns at a time, with the next kEarlyDepth rows' loads in
+    // flight while a row is summed.  Loads past the share repeat its last
+    // row and columns past n read column n - 1, so that every load is issued
+    // unconditionally (the waits then count them exactly); such values are
+    // never summed.
+    const int nsh = e_hi - e_lo;
+    if (nsh > 0) {
+#pragma unroll 1
+      for (int h = 0; h < kEarlyCols; h += kEarlyPass) {
+        long long acc[kEarlyPass];
+        float buf[kEarlyDepth][kEarlyPass];
+#pragma unroll
+        for (int q = 0; q < kEarlyPass; ++q) acc[q] = 0;
+        auto load = [&](float* dst, int e) {
+          const float* r = a.C + size_t(sj[min(e, nsh - 1)]) * a.n;
+#pragma unroll
+          for (int q = 0; q < kEarlyPass; ++q)
+            dst[q] = __builtin_nontemporal_load(r + min(tid + kBlock * (h + q), a.n - 1));
+        };
+#pragma unroll
+        for (int d = 0; d < kEarlyDepth; ++d) load(buf[d], d);
+        for (int e = 0; e < nsh; e += kEarlyDepth) {
+#pragma unroll
+          for (int d = 0; d < kEarlyDepth; ++d) {
+            float x[kEarlyPass];
+#pragma unroll
+            for (int q = 0; q < kEarlyPass; ++q) x[q] = buf[d][q];
+            load(buf[d], e + d + kEarlyDepth);
+            if (e + d < nsh) {
+              const float bo = sbo[e + d], bn = sbn[e + d];
+              const double vs = svs[e + d];
+#pragma unroll
+              for (int q = 0; q < kEarlyPass; ++q) {
+                // A column that cost at least the old best contributes 0
+                // before and after.
+                if (tid + kBlock * (h + q) < a.n && x[q] < bo)
+                  acc[q] += fx_diff(vs, fmaxf(bn - x[q], 0.f), bo - x[q]);
+              }
+            }
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < kEarlyPass; ++q) {
+          const int c = tid + kBlock * (h + q);
+          if (c < a.n) put(reinterpret_cast<unsigned long long*>(mine + c), (unsigned long long)acc[q]);
+        }
+      }
+      if (w == 0) {
+        long long d = 0;
+        if (lane < nsh) d = fx_diff(svs[lane], sbn[lane], sbo[lane]);
+        d = wave_sum_i64(d);
+        if (lane == 0) put(reinterpret_cast<unsigned long long*>(mine + a.n), (unsigned long long)d);
+      }
+      __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's stores are done
+    }
+    __syncthreads();
+    if (nsh > 0 && tid == 0) put(lens_slot(a.lens, blk), (unsigned long long)(step + 1));
+
+    // Every share's sums, once its block has raised its flag for the step.
+    if (tid == 0) sflag = 0;
+    __syncthreads();
+    if (tid < nshare) {
+      unsigned long long f;
+      const unsigned long long want = (unsigned long long)(step + 1);
+      if (!wait_slot(lens_slot(a.lens, tid), a.abort, a.poll_limit, [want](unsigned long long v) { return v == want; },
+                     f))
+        sflag = 1;
+    }
+    __syncthreads();
+    if (sflag) return;
+    {
+      // All of a thread's loads are issued before any is used (a row past
+      // nshare, or a column past cnt, is read from a valid address and not
+      // summed).
+      constexpr int kRead = 16;                       // loads in flight: two rounds for 256 blocks
+      const int col = min(lo + min(lane, max(cnt - 1, 0)), a.n - 1);
+      long long s = 0;
+      for (int b0 = 0; b0 < nshare; b0 += kRead * kWaves) {
+        unsigned long long x[kRead];
+#pragma unroll
+        for (int m = 0; m < kRead; ++m)
+          x[m] = get(reinterpret_cast<const unsigned long long*>(
+              a.epart + size_t(min(b0 + w + kWaves * m, nb - 1)) * a.ldp + col));
+#pragma unroll
+        for (int m = 0; m < kRead; ++m)
+          if (lane < cnt && b0 + w + kWaves * m < nshare) s += (long long)x[m];
+      }
+      red[tid] = s;
+    }
+    if (blk == 0 && w == 1) {
+      constexpr int kRead = kMaxBlocks / 64;
+      unsigned long long x[kRead];
+#pragma unroll
+      for (int m = 0; m < kRead; ++m)
+        x[m] = get(reinterpret_cast<const unsigned long long*>(a.epart + size_t(min(lane + 64 * m, nb - 1)) * a.ldp + a.n));
+      long long s = 0;
+#pragma unroll
+      for (int m = 0; m < kRead; ++m)
+        if (lane + 64 * m < nshare) s += (long long)x[m];
+      L += wave_sum_i64(s);
+      if (lane == 0 && a.step_obj) a.step_obj[step] = fx_to_double(L, S);
+    }
+    __syncthreads();
+    if (tid < 64 && tid < cnt) {
+      long long s = sG[tid];
+#pragma unroll
+      for (int r = 0; r < kWaves; ++r) s += red[r * 64 + tid];
+      sG[tid] = s;
+    }
+    // The next exchange's candidates (wave 0, which also wrote the gains),
+    // unless this was the last step.
+    if (step + 1 < a.k) publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, xc & 1, blk), epoch_of(xc));
+    if (step + 1 == k_stop || H < kEarlyMinHits) {
+      // Hand over before step + 1.
+      __syncthreads();
+      for (int i = tid; i < cnt; i += kBlock) {
+        a.ho_gain[lo + i] = sG[i];
+        a.ho_sel[lo + i] = ssel[i];
+      }
+      if (blk == 0) {
+        for (int j = tid; j < a.ldt; j += kBlock) a.ho_b[j] = sball[j];
+        if (tid == 64) {
+          a.ho_misc[0] = L;
+          a.ho_misc[1] = xc;
+          a.ho_misc[2] = step + 1;
+        }
+      }
+      return;
+    }
+  }
+}
 
 // ---------------------------------------------------------------------------
 // The rows schedule's later steps from candidate lists.
@@ -1161,7 +1458,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
         const float x = ec[q], bo = sball[j];
         if (x < bo) {
           sball[j] = x;
-          if (blk == 0) dobj = (long long)(fx_scaled(evs[q], x) - fx_scaled(evs[q], bo));
+          if (blk == 0) dobj = fx_diff(evs[q], x, bo);
           if (a.assign && unsigned(j - lo) < unsigned(cnt)) a.assign[j] = t;
         }
       }
@@ -1186,7 +1483,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
             const float cv = pc[q];
             if (cv < bo) {
               const double vs = fx_scale(double(pv[q]), S);
-              atomicAdd(&sdelta[pj[q] >> 16], fx_scaled(vs, fmaxf(bn - cv, 0.f)) - fx_scaled(vs, bo - cv));
+              atomicAdd(&sdelta[pj[q] >> 16], (unsigned long long)fx_diff(vs, fmaxf(bn - cv, 0.f), bo - cv));
             }
             pb[q] = bn;
           }
@@ -1204,7 +1501,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
         const float bn = sball[ej[q]], bo = eb[q];
         if (bn < bo) {
           const float cv = ec[q];
-          if (cv < bo) d = (long long)(fx_scaled(evs[q], fmaxf(bn - cv, 0.f)) - fx_scaled(evs[q], bo - cv));
+          if (cv < bo) d = fx_diff(evs[q], fmaxf(bn - cv, 0.f), bo - cv);
           eb[q] = bn;
         }
       }
@@ -1386,7 +1683,7 @@ const void* rows_batch_kernel(int64_t n, int W) {
 // (when the rows form may run) T.
 constexpr int kPassParts = 3;   // row ranges of the first pass (three blocks per compute unit fit at once)
 struct IncLayout {
-  size_t part, scale, T, lists, ho_gain, ho_sel, ho_b, misc, total;
+  size_t part, scale, T, epart, lists, ho_gain, ho_sel, ho_b, misc, total;
 };
 IncLayout inc_layout(int64_t n, int64_t k, bool compact) {
   IncLayout L;
@@ -1395,15 +1692,23 @@ IncLayout inc_layout(int64_t n, int64_t k, bool compact) {
   L.scale = o; o += 256;
   L.T = o;
   if (!compact && n <= kRowsMaxN) o += a256(size_t(n) * rows_ldt(n) * sizeof(float));
-  // The candidate lists and the hand-over between launches (rows schedule,
-  // n <= kListMaxN, more than kListStep picks).
+  // The early kernel's partial sums (rows schedule, n <= kEarlyMaxN), for
+  // as many blocks as the scene can have.
+  L.epart = o;
+  const bool early = !compact && n <= kEarlyMaxN;
+  if (early) o += a256(size_t(std::min<int64_t>(kMaxBlocks, (n + 63) / 64)) * early_ldp(n) * 8);
+  // The candidate lists (n <= kListMaxN, more than kListStep picks) and the
+  // hand-over between launches (lists or the early kernel).
   L.lists = L.ho_gain = L.ho_sel = L.ho_b = L.misc = o;
-  if (!compact && n <= kListMaxN && k > kListStep) {
+  const bool lists = !compact && n <= kListMaxN && k > kListStep;
+  if (lists) {
     L.lists = o;   o += a256(size_t(n) * kListSlots * 16);
+  }
+  if (lists || early) {
     L.ho_gain = o; o += a256(size_t(n) * 8);
     L.ho_sel = o;  o += a256(size_t(n));
     L.ho_b = o;    o += a256(size_t(rows_ldt(n)) * 4);
-    L.misc = o;    o += a256(16 + 4 + size_t(kMaxBlocks) * 4);   // objective, exchanges; lfail; lblock
+    L.misc = o;    o += a256(24 + 4 + size_t(kMaxBlocks) * 4);   // objective, exchanges, next step; lfail; lblock
   }
   L.total = o;
   return L;
@@ -1441,13 +1746,18 @@ IncDev inc_dev(const SgsParams& p, char* w, int W, bool rows) {
   a.gate = nullptr;
   a.gate_val = 0u;
   const bool lists = rows && lists_for(p.n, p.k, W);
+  const bool early = rows && early_for(p.n, W);
+  const bool ho = lists || early;
   a.lists = lists ? reinterpret_cast<unsigned long long*>(w + M.lists) : nullptr;
-  a.ho_gain = lists ? reinterpret_cast<long long*>(w + M.ho_gain) : nullptr;
-  a.ho_sel = lists ? reinterpret_cast<unsigned char*>(w + M.ho_sel) : nullptr;
-  a.ho_b = lists ? reinterpret_cast<float*>(w + M.ho_b) : nullptr;
-  a.ho_misc = lists ? reinterpret_cast<long long*>(w + M.misc) : nullptr;
-  a.lfail = lists ? reinterpret_cast<unsigned int*>(w + M.misc + 16) : nullptr;
-  a.lblock = lists ? reinterpret_cast<unsigned int*>(w + M.misc + 20) : nullptr;
+  a.ho_gain = ho ? reinterpret_cast<long long*>(w + M.ho_gain) : nullptr;
+  a.ho_sel = ho ? reinterpret_cast<unsigned char*>(w + M.ho_sel) : nullptr;
+  a.ho_b = ho ? reinterpret_cast<float*>(w + M.ho_b) : nullptr;
+  a.ho_misc = ho ? reinterpret_cast<long long*>(w + M.misc) : nullptr;
+  a.lfail = lists ? reinterpret_cast<unsigned int*>(w + M.misc + 24) : nullptr;
+  a.lblock = lists ? reinterpret_cast<unsigned int*>(w + M.misc + 28) : nullptr;
+  a.epart = early ? reinterpret_cast<long long*>(w + M.epart) : nullptr;
+  a.ldp = early ? early_ldp(p.n) : 0;
+  a.start = nullptr;
   return a;
 }
 
@@ -1499,15 +1809,27 @@ hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t 
     a.k_end = kListStep;
     if ((e = fits(reinterpret_cast<const void*>(sgs_list_kernel), size_t(a.ldt) * 4)) != hipSuccess) return e;
   }
+  // The early kernel runs the first steps, while they improve many targets;
+  // the rows kernel continues from the step it stopped before.
+  const bool early = a.epart != nullptr;
+  if (early && (e = fits(reinterpret_cast<const void*>(sgs_early_kernel), lds)) != hipSuccess) return e;
   sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = launch_first_pass(a, nb, stream)) != hipSuccess) return e;
+  if (early) {
+    void* eargs[] = {&a};
+    if ((e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_early_kernel), dim3(nb), dim3(kBlock), eargs,
+                                        lds, stream)) != hipSuccess)
+      return e;
+    a.start = a.ho_misc + 2;
+  }
   void* args[] = {&a};
   if ((e = hipLaunchCooperativeKernel(kernel, dim3(nb), dim3(kBlock), args, lds, stream)) != hipSuccess) return e;
   if (lists) {
     list_build_kernel<<<(p.n + 3) / 4, 256, 0, stream>>>(a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     IncDev b = a;
+    b.start = nullptr;
     b.k_begin = kListStep;
     b.k_end = p.k;
     void* bargs[] = {&b};

@@ -68,6 +68,18 @@ __device__ __forceinline__ unsigned long long fx_scaled(double vs, float d) {
   return ((unsigned long long)h << 32) | l;
 }
 
+// fx_scaled(vs, d1) - fx_scaled(vs, d2) when both products are below 2^52
+// (the incremental form's scale guarantees it for every term): floor(y) +
+// 2^52 is then exact and lies in [2^52, 2^53), where the float64 bit
+// pattern is that of 2^52 plus the integer floor(y), so the difference of
+// the two patterns is the difference of the floors.  Four float64
+// operations a term instead of seven.
+__device__ __forceinline__ long long fx_diff(double vs, float d1, float d2) {
+  const double a = __builtin_floor(vs * double(d1)) + 0x1p52;
+  const double b = __builtin_floor(vs * double(d2)) + 0x1p52;
+  return __double_as_longlong(a) - __double_as_longlong(b);
+}
+
 struct IncDev {
   const float* C;
   const float* v;
@@ -98,10 +110,16 @@ struct IncDev {
   long long* ho_gain;         // [n] running gains
   unsigned char* ho_sel;      // [n] chosen flags
   float* ho_b;                // [ldt] best costs
-  long long* ho_misc;         // [0] objective in fixed point, [1] exchanges so far
+  long long* ho_misc;         // [0] objective in fixed point, [1] exchanges so far, [2] next step
   unsigned long long* lists;  // [n][kListSlots][2] candidate lists
   unsigned int* lfail;        // the lists do not fit
   unsigned int* lblock;       // [blocks] pairs of each block's candidates
+  // Early steps of the rows schedule (sgs_early_kernel): each block's partial
+  // gain changes of every column, and the step a launch after it starts from
+  // (null: k_begin).
+  long long* epart;           // [blocks][ldp]: columns 0 .. n - 1, then the objective's change
+  int ldp;
+  const long long* start;
 };
 
 struct Layout {
@@ -309,6 +327,20 @@ __device__ double block_sum_all(double x, double* sd) {
   double s = 0.0;
 #pragma unroll
   for (int q = 0; q < kWaves; ++q) s += sd[q];
+  __syncthreads();
+  return s;
+}
+
+// Block maximum, result in every thread.
+__device__ double block_max_all(double x, double* sd) {
+  x = wave_max(x);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sd[w] = x;
+  __syncthreads();
+  double s = sd[0];
+#pragma unroll
+  for (int q = 1; q < kWaves; ++q) s = fmax(s, sd[q]);
   __syncthreads();
   return s;
 }

@@ -53,13 +53,21 @@ def test_workspace_queries(lib):
     c = lib.coverprune_sgs_workspace(16384, 1638, 3)
     assert 16384 * 16 <= c < b
     r = lib.coverprune_sgs_workspace(16384, 1638, 1)
-    # ... and, past 128 picks up to n = 16384, the candidate lists (256 pairs
-    # of 16 bytes per token) and the hand-over between the two launches
-    # (gains, chosen flags, best costs: 13 bytes per token, and 1280 bytes)
-    assert r == c + 16384 * 16384 * 4 + 16384 * 256 * 16 + 16384 * 13 + 1280
-    assert lib.coverprune_sgs_workspace(16384, 128, 1) == lib.coverprune_sgs_workspace(16384, 128, 3) + 16384 * 16384 * 4
-    # ... up to n = 32768 (rows padded to 256 targets); beyond it the compact one
-    assert lib.coverprune_sgs_workspace(1000, 100, 1) == lib.coverprune_sgs_workspace(1000, 100, 3) + 1000 * 1024 * 4
+    # ... and, up to n = 16384, the early steps' per-block partial sums
+    # (256 blocks of n + 1 columns rounded up to 64, 8 bytes each) and the
+    # hand-over between launches (gains, chosen flags, best costs: 13 bytes
+    # per token, and 1280 bytes); past 128 picks also the candidate lists
+    # (256 pairs of 16 bytes per token)
+    early = 256 * 16448 * 8
+    ho = 16384 * 13 + 1280
+    assert r == c + 16384 * 16384 * 4 + early + 16384 * 256 * 16 + ho
+    assert lib.coverprune_sgs_workspace(16384, 128, 1) == (lib.coverprune_sgs_workspace(16384, 128, 3)
+                                                           + 16384 * 16384 * 4 + early + ho)
+    # ... up to n = 32768 (rows padded to 256 targets; 16 blocks at n = 1000);
+    # beyond it the compact one
+    assert lib.coverprune_sgs_workspace(1000, 100, 1) == (lib.coverprune_sgs_workspace(1000, 100, 3)
+                                                          + 1000 * 1024 * 4 + 16 * 1024 * 8
+                                                          + 8192 + 1024 + 4096 + 1280)
     assert lib.coverprune_sgs_workspace(32769, 100, 1) == lib.coverprune_sgs_workspace(32769, 100, 3)
     assert lib.coverprune_sgs_workspace(16384, 1638, 2) == 0      # compact alone is not a form
     assert 0 < a < b
