@@ -179,7 +179,8 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
  *             updated, step by step, from the rows of the targets whose best
  *             cost the pick lowers (their old and new b); the terms are the
  *             same float32 differences and float64 products, each rounded
- *             down onto a grid of 2^-S (c0 * sum v < 2^(62 - S)) and summed
+ *             down onto a grid of 2^-S (c0 * sum v < 2^(62 - S) and
+ *             c0 * max v < 2^(52 - S); costs are taken in [0, c0]) and summed
  *             exactly in 64-bit integers, so picks can differ from the dense
  *             sweep's float64 sums only between gains within rounding of
  *             each other.
@@ -187,6 +188,11 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
  *             finds the targets a pick improves itself, from the pick's row
  *             of a source-major copy of the cost that the first pass writes
  *             into the workspace (4 n^2 bytes, 1 GiB at n = 16384).  For
+ *             n <= 16384 the first steps, while a pick lowers at least 512
+ *             best costs, split each step's improved targets between the
+ *             compute units, which read those targets' whole rows and
+ *             exchange per-column sums through the workspace (8 bytes per
+ *             column and compute unit, up to 2 KB per token).  For
  *             n <= 16384 and k > 128 the steps after the 128th run from
  *             per-candidate lists of the targets each candidate can still
  *             improve (4 KB per token in the workspace), with the next
@@ -207,7 +213,8 @@ cp_status coverprune_fst_capacity(const void* feats, cp_dtype dtype, int64_t n, 
 /* Workspace for one form (flags as for coverprune_sgs_select; 0 for flags it
  * does not accept): the dense form needs about 9 MB at n = 16384 (private
  * best costs and float64 partial gains of up to 64 row panels), the
- * incremental form 4 n + 45 bytes per token up to n = 32768 (plus 4 KB per
+ * incremental form 4 n + 45 bytes per token up to n = 32768 (plus up to
+ * 2 KB per token for the early steps' sums when n <= 16384, and 4 KB per
  * token for the candidate lists when n <= 16384 and k > 128) and about 45
  * bytes per token beyond that or with CP_SGS_COMPACT, each plus about
  * 100 KB of exchange slots. */
