@@ -208,19 +208,22 @@ __device__ __forceinline__ unsigned long long lane_u64(unsigned long long x, int
 }
 
 
+__device__ __forceinline__ unsigned wave_max_u32(unsigned x) {
+  x = max(x, unsigned(__builtin_amdgcn_mov_dpp(int(x), kDppSteps[0], 0xf, 0xf, false)));
+  x = max(x, unsigned(__builtin_amdgcn_mov_dpp(int(x), kDppSteps[1], 0xf, 0xf, false)));
+  x = max(x, unsigned(__builtin_amdgcn_mov_dpp(int(x), kDppSteps[2], 0xf, 0xf, false)));
+  x = max(x, unsigned(__builtin_amdgcn_mov_dpp(int(x), kDppSteps[3], 0xf, 0xf, false)));
+  return max(max(unsigned(__builtin_amdgcn_readlane(int(x), 0)), unsigned(__builtin_amdgcn_readlane(int(x), 16))),
+             max(unsigned(__builtin_amdgcn_readlane(int(x), 32)), unsigned(__builtin_amdgcn_readlane(int(x), 48))));
+}
+
+// The 64-bit maximum as two 32-bit ones: the largest high word, then the
+// largest low word among the lanes that hold it (32-bit steps take one
+// compare-select where a 64-bit step takes three).
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long x) {
-  unsigned long long y;
-  y = dpp_u64<kDppSteps[0]>(x); x = y > x ? y : x;
-  y = dpp_u64<kDppSteps[1]>(x); x = y > x ? y : x;
-  y = dpp_u64<kDppSteps[2]>(x); x = y > x ? y : x;
-  y = dpp_u64<kDppSteps[3]>(x); x = y > x ? y : x;
-  unsigned long long m = lane_u64(x, 0);
-#pragma unroll
-  for (int r = 16; r < 64; r += 16) {
-    y = lane_u64(x, r);
-    m = y > m ? y : m;
-  }
-  return m;
+  const unsigned hm = wave_max_u32(unsigned(x >> 32));
+  const unsigned lm = wave_max_u32(unsigned(x >> 32) == hm ? unsigned(x) : 0u);
+  return ((unsigned long long)hm << 32) | lm;
 }
 
 __device__ __forceinline__ long long wave_max_i64(long long x) {
