@@ -217,12 +217,19 @@ __device__ __forceinline__ unsigned wave_max_u32(unsigned x) {
              max(unsigned(__builtin_amdgcn_readlane(int(x), 32)), unsigned(__builtin_amdgcn_readlane(int(x), 48))));
 }
 
-// The 64-bit maximum as two 32-bit ones: the largest high word, then the
-// largest low word among the lanes that hold it (32-bit steps take one
-// compare-select where a 64-bit step takes three).
+// The 64-bit maximum as 32-bit ones: the largest high word, then the low
+// word of the one lane that holds it, or, when several do, the largest of
+// their low words (32-bit steps take one compare-select where a 64-bit step
+// takes three).
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long x) {
-  const unsigned hm = wave_max_u32(unsigned(x >> 32));
-  const unsigned lm = wave_max_u32(unsigned(x >> 32) == hm ? unsigned(x) : 0u);
+  const unsigned hi = unsigned(x >> 32);
+  const unsigned hm = wave_max_u32(hi);
+  const unsigned long long tie = __ballot(hi == hm);
+  unsigned lm;
+  if (__popcll(tie) == 1)
+    lm = unsigned(__builtin_amdgcn_readlane(int(unsigned(x)), __builtin_ctzll(tie)));
+  else
+    lm = wave_max_u32(hi == hm ? unsigned(x) : 0u);
   return ((unsigned long long)hm << 32) | lm;
 }
 
