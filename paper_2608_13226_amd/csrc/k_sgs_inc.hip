@@ -1190,11 +1190,10 @@ __global__ __launch_bounds__(kBlock) void sgs_early_kernel(IncDev a) {
 // a list of at most kListMax entries; sgs_list_kernel runs the remaining steps
 // from the lists.  Per step a block reads the winner's list (a few KB, from
 // L2 for all but the first block of an XCD) instead of its 64 KB row of T, and
-// its threads hold the block's own pairs in registers (up to kOwnSets a
-// thread) with each pair's last seen best cost: a step's changes to the own
-// gains come from the pairs whose best cost fell, found by one LDS read per
-// pair, instead of reading each hit row's segment over its columns from
-// memory.  The terms are the fixed-point terms of the rows of T, so the picks
+// keeps the block's own pairs (up to kEntMax) in LDS indexed by target: the
+// thread that lowers a target's best cost from the winner's list also adds
+// the changes of the own candidates paired with that target, instead of
+// reading each hit row's segment over its columns from memory.  The terms are the fixed-point terms of the rows of T, so the picks
 // are the same.  When the lists do not fit (a candidate with more than
 // kListMax pairs, or a block with more than kEntMax), the build raises lfail
 // and the rows kernel continues instead (its launch is gated on lfail).
@@ -1202,10 +1201,17 @@ constexpr int kListStep = 128;                        // steps before the lists
 constexpr int kListSlots = 256;                       // per candidate: a header and kListMax pairs
 constexpr int kListMax = kListSlots - 1;
 constexpr int kListMaxN = kRowChunk * kWaves * 8;     // 16384, the one-group rows kernel's reach
-constexpr int kOwnSets = 16;                          // own pairs a thread holds
+constexpr int kOwnSets = 16;                          // own pairs a thread places at the start
 constexpr int kEntMax = kOwnSets * kBlock;            // own pairs a block holds: 8192
 
 bool lists_for(int64_t n, int64_t k, int W) { return n <= kListMaxN && W <= 64 && k > kListStep; }
+
+// The list kernel's LDS: the best costs, the own pairs' first index per
+// target (16 bits each, targets 0 .. n), their costs and candidates.
+__host__ __device__ __forceinline__ int list_off_words(int n) { return (n + 2) / 2; }
+size_t list_lds(int64_t n) {
+  return size_t(rows_ldt(n)) * 4 + size_t(list_off_words(int(n))) * 4 + size_t(kEntMax) * 5;
+}
 
 // One wave per candidate: its pairs from its row of T against the handed
 // over best costs.  Also counts the pairs of each block of the list kernel.
@@ -1287,11 +1293,18 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   const int lo = blk * a.W;
   const int cnt = max(0, min(a.n, lo + a.W) - lo);
   float* sball = reinterpret_cast<float*>(smem);                   // [ldt] best costs
+  // The block's own pairs by target: pairs [off(j), off(j + 1)) have target
+  // j, each with its cost and its candidate (own index); off as 16-bit
+  // values, two to a word.
+  unsigned int* soffw = reinterpret_cast<unsigned int*>(sball + a.ldt);   // [n / 2 + 1]
+  float* spc = reinterpret_cast<float*>(soffw + list_off_words(a.n));     // [kEntMax]
+  unsigned char* spk = reinterpret_cast<unsigned char*>(spc + kEntMax);   // [kEntMax]
+  auto off = [&](int j) { return int((soffw[j >> 1] >> ((j & 1) * 16)) & 0xffffu); };
   __shared__ long long sG[64];
   __shared__ unsigned char ssel[64];
   __shared__ unsigned long long sdelta[64];
-  __shared__ int soff[65];                                          // own pairs: each candidate's first
-  __shared__ unsigned char sown[kEntMax];                           //   and each pair's candidate
+  __shared__ int soff[65];                                          // each own candidate's first pair
+  __shared__ int swt[kWaves];
   __shared__ unsigned long long su[kWaves], sk1[kMaxBlocks], sk2[kMaxBlocks];
   __shared__ int sflag;
   __shared__ unsigned long long sL;                                 // objective (block 0)
@@ -1299,6 +1312,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   const int S = *a.scale;
 
   for (int j = tid; j < a.ldt; j += kBlock) sball[j] = a.ho_b[j];
+  for (int i = tid; i < list_off_words(a.n); i += kBlock) soffw[i] = 0u;
   if (tid < 64) {
     ssel[tid] = tid < cnt ? a.ho_sel[lo + tid] : 1;
     sG[tid] = tid < cnt ? a.ho_gain[lo + tid] : 0;
@@ -1312,36 +1326,58 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   if (tid == 0) sL = (unsigned long long)(blk == 0 ? a.ho_misc[0] : 0);
   __syncthreads();
   const int npairs = min(soff[64], kEntMax);
-  for (int ci = w; ci < cnt; ci += kWaves)
-    for (int e = soff[ci] + lane; e < min(soff[ci + 1], npairs); e += 64) sown[e] = (unsigned char)ci;
-  __syncthreads();
-
-  // Own pair p = q kBlock + tid of the block (candidates in order, each with
-  // its list's entries) in set q: target | own index << 16, cost, capacity,
-  // and the best cost as last seen (-inf for no pair, which never falls).
-  // Every step of the set-up is issued for all sets before its results are
-  // used.
-  int pj[kOwnSets];
-  float pc[kOwnSets], pv[kOwnSets], pb[kOwnSets];
   {
+    // Pair p = q kBlock + tid of the block (candidates in order, each with
+    // its list's entries): its candidate by a search of soff, its entry from
+    // the list; all loads issued before any is used.
     int ci[kOwnSets], e[kOwnSets];
 #pragma unroll
-    for (int q = 0; q < kOwnSets; ++q) ci[q] = q * kBlock + tid < npairs ? int(sown[q * kBlock + tid]) : 0;
+    for (int q = 0; q < kOwnSets; ++q) {
+      const int pq = q * kBlock + tid;
+      int c = 0;
 #pragma unroll
-    for (int q = 0; q < kOwnSets; ++q) e[q] = q * kBlock + tid < npairs ? 1 + q * kBlock + tid - soff[ci[q]] : 0;
-    uint4 ev[kOwnSets];
+      for (int st = 32; st > 0; st >>= 1)
+        if (c + st < 64 && soff[c + st] <= pq) c += st;
+      ci[q] = c;
+      e[q] = pq < npairs ? 1 + pq - soff[c] : 0;
+    }
+    uint2 ev[kOwnSets];
 #pragma unroll
     for (int q = 0; q < kOwnSets; ++q)
-      ev[q] = reinterpret_cast<const uint4*>(a.lists + size_t(min(lo + ci[q], a.n - 1)) * (2 * kListSlots))[e[q]];
+      ev[q] = reinterpret_cast<const uint2*>(a.lists + size_t(min(lo + ci[q], a.n - 1)) * (2 * kListSlots))[2 * e[q]];
+    // Pairs per target (16-bit counts, two to a word), their inclusive
+    // prefix over the targets, then each pair placed at its target's end,
+    // which moves down to the target's first pair.
 #pragma unroll
-    for (int q = 0; q < kOwnSets; ++q) {
-      const bool ok = q * kBlock + tid < npairs;
-      const int j = ok ? min(int(ev[q].x), a.n - 1) : 0;
-      pj[q] = j | (ci[q] << 16);
-      pc[q] = __uint_as_float(ev[q].y);
-      pv[q] = __uint_as_float(ev[q].z);
-      pb[q] = ok ? sball[j] : -__builtin_inff();
+    for (int q = 0; q < kOwnSets; ++q)
+      if (q * kBlock + tid < npairs) {
+        const int j = min(int(ev[q].x), a.n - 1);
+        atomicAdd(&soffw[j >> 1], 1u << ((j & 1) * 16));
+      }
+    __syncthreads();
+    const int per = (list_off_words(a.n) + kBlock - 1) / kBlock;   // words a thread scans
+    int sum = 0;
+    for (int i = tid * per; i < min((tid + 1) * per, list_off_words(a.n)); ++i)
+      sum += int(soffw[i] & 0xffffu) + int(soffw[i] >> 16);
+    int run = block_inclusive_scan(sum, swt) - sum;
+    for (int i = tid * per; i < min((tid + 1) * per, list_off_words(a.n)); ++i) {
+      const unsigned int wv = soffw[i];
+      const int lo16 = run + int(wv & 0xffffu);
+      const int hi16 = lo16 + int(wv >> 16);
+      soffw[i] = unsigned(lo16) | (unsigned(hi16) << 16);
+      run = hi16;
     }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kOwnSets; ++q)
+      if (q * kBlock + tid < npairs) {
+        const int j = min(int(ev[q].x), a.n - 1);
+        const unsigned int sh = (j & 1) * 16;
+        const int pos = int((atomicSub(&soffw[j >> 1], 1u << sh) >> sh) & 0xffffu) - 1;
+        spc[pos] = __uint_as_float(ev[q].y);
+        spk[pos] = (unsigned char)ci[q];
+      }
+    __syncthreads();
   }
 
   // Chain slots: 0 the exchange's winner, m = 1 .. kListChain the candidate
@@ -1460,36 +1496,19 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
           sball[j] = x;
           if (blk == 0) dobj = fx_diff(evs[q], x, bo);
           if (a.assign && unsigned(j - lo) < unsigned(cnt)) a.assign[j] = t;
+          // The own candidates with a pair on j: their gain changes, added
+          // up in LDS as 64-bit integers.
+          const int p1 = off(j + 1);
+          for (int p = off(j); p < p1; ++p) {
+            const float cv = spc[p];
+            if (cv < bo) atomicAdd(&sdelta[spk[p]], (unsigned long long)fx_diff(evs[q], fmaxf(x - cv, 0.f), bo - cv));
+          }
         }
       }
     }
     __syncthreads();
     if (dobj != 0) atomicAdd(&sL, (unsigned long long)dobj);
     obj_step = step;
-    // Own pairs whose best cost fell: their candidates' gain changes, added
-    // up in LDS as 64-bit integers (all reads issued before any is used).
-    {
-      float bq[kOwnSets];
-#pragma unroll
-      for (int q = 0; q < kOwnSets; ++q) bq[q] = sball[pj[q] & 0xffff];
-      bool any = false;
-#pragma unroll
-      for (int q = 0; q < kOwnSets; ++q) any |= bq[q] < pb[q];
-      if (any) {
-#pragma unroll
-        for (int q = 0; q < kOwnSets; ++q) {
-          const float bn = bq[q], bo = pb[q];
-          if (bn < bo) {
-            const float cv = pc[q];
-            if (cv < bo) {
-              const double vs = fx_scale(double(pv[q]), S);
-              atomicAdd(&sdelta[pj[q] >> 16], (unsigned long long)fx_diff(vs, fmaxf(bn - cv, 0.f), bo - cv));
-            }
-            pb[q] = bn;
-          }
-        }
-      }
-    }
     // The chain candidates still ahead (slots above pos): their changes in
     // the step, from the entries whose best cost fell, into LDS.
 #pragma unroll
@@ -1807,7 +1826,7 @@ hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t 
   const bool lists = a.lists != nullptr;
   if (lists) {
     a.k_end = kListStep;
-    if ((e = fits(reinterpret_cast<const void*>(sgs_list_kernel), size_t(a.ldt) * 4)) != hipSuccess) return e;
+    if ((e = fits(reinterpret_cast<const void*>(sgs_list_kernel), list_lds(p.n))) != hipSuccess) return e;
   }
   // The early kernel runs the first steps, while they improve many targets;
   // the rows kernel continues from the step it stopped before.
@@ -1834,7 +1853,7 @@ hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t 
     b.k_end = p.k;
     void* bargs[] = {&b};
     if ((e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_list_kernel), dim3(nb), dim3(kBlock), bargs,
-                                        size_t(a.ldt) * 4, stream)) != hipSuccess)
+                                        list_lds(p.n), stream)) != hipSuccess)
       return e;
     IncDev c = b;
     c.gate = a.lfail;
