@@ -2,9 +2,11 @@
 """Benchmark of CoverPrune's hot path on one MI355X.
 
 One step = one pass of the hot path over one synthetic scene resident in
-HBM: the FST cost (coverprune_fst_cost) and the greedy selection of K tokens
-over it (coverprune_sgs_select, incremental form by default): CoverPrune's
-prune latency.  The default workload is the 16384-token, 3584-wide bfloat16
+HBM: the FST cost and the greedy selection of K tokens over it in one call
+(coverprune_prune, whose cost epilogue also writes the greedy's first gains):
+CoverPrune's prune latency.  The same two parts as separate calls
+(coverprune_fst_cost, then coverprune_sgs_select) are timed beside the step,
+with the same result.  The default workload is the 16384-token, 3584-wide bfloat16
 scene whose 1 GiB float32 cost matrix stays in HBM (K = 1638).
 CoverPrune-Lite (coverprune_lite_select), the alternative method of Sec. 4,
 is timed on its own beside the step, on this scene and on its 32768-token
@@ -48,7 +50,8 @@ def _args():
                     help="also time CoverPrune-Lite alone on this workload ('' to skip)")
     ap.add_argument("--sgs", choices=("incremental", "dense"), default="incremental",
                     help="form of the greedy inside the timed step (the same greedy; picks can differ "
-                         "only between gains within rounding of each other)")
+                         "only between gains within rounding of each other); dense times the two calls "
+                         "as the step")
     ap.add_argument("--literal-rounds", type=int, default=50,
                     help="scaling rounds per step of the literal greedy timed beside the step (0 to skip)")
     ap.add_argument("--literal-eps", type=float, default=0.05,
@@ -267,23 +270,26 @@ def main():
     cost = torch.empty((n, n), dtype=torch.float32, device=dev)
     maxima = torch.empty(3, dtype=torch.float32, device=dev)
     ws_f = torch.empty(lib.coverprune_fst_cost_workspace(n, d, dt), dtype=torch.uint8, device=dev)
+    ws_p = torch.empty(lib.coverprune_prune_workspace(n, d, k, dt), dtype=torch.uint8, device=dev)
     ws_s = torch.empty(max(lib.coverprune_sgs_workspace(n, k, f) for f in
                            (cp.CP_SGS_DENSE, cp.CP_SGS_INCREMENTAL, cp.CP_SGS_INCREMENTAL | cp.CP_SGS_COMPACT)),
                        dtype=torch.uint8, device=dev)
     ws_l = torch.empty(lib.coverprune_lite_workspace(n, d, k, dt), dtype=torch.uint8, device=dev)
 
+    run_f = lambda: cp.fst_cost(t["feats"], t["pos"], t["frame"], out=cost, maxima=maxima, workspace=ws_f)
+    run_s = lambda: cp.sgs_select(cost, t["capacity"], k, workspace=ws_s, incremental=args.sgs == "incremental")
+    fused = args.sgs == "incremental"
+
     def step(i=None, ev=None):
-        run_f = lambda: cp.fst_cost(t["feats"], t["pos"], t["frame"], out=cost, maxima=maxima, workspace=ws_f)
-        run_s = lambda: cp.sgs_select(cost, t["capacity"], k, workspace=ws_s,
-                                      incremental=args.sgs == "incremental")
-        run_l = lambda: cp.lite_select(t["feats"], t["pos"], t["frame"], t["capacity"], k,
-                                       voxel_size=lite_h, workspace=ws_l)
+        if fused:
+            run = lambda: cp.prune(t["feats"], t["pos"], t["frame"], t["capacity"], k, out=cost, maxima=maxima,
+                                   workspace=ws_p)[2]
+            return run() if ev is None else _timed(run, ev["p0"], ev["p1"], i)
         if ev is None:
-            run_f(); r = run_s()
-        else:
-            _timed(run_f, ev["f0"], ev["f1"], i)
-            r = _timed(run_s, ev["s0"], ev["s1"], i)
-        return r
+            run_f()
+            return run_s()
+        _timed(run_f, ev["f0"], ev["f1"], i)
+        return _timed(run_s, ev["s0"], ev["s1"], i)
 
     for _ in range(args.warmup):
         step()
@@ -291,19 +297,30 @@ def main():
 
     K = args.steps
     ev = {key: [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-          for key in ("f0", "f1", "s0", "s1")}
+          for key in ("p0", "p1", "f0", "f1", "s0", "s1")}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
         r = step(i, ev)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / K
 
     def avg(a, b):
         return float(np.mean([ev[a][i].elapsed_time(ev[b][i]) for i in range(K)]))
 
+    # The step's two parts as separate calls, timed beside the step (the
+    # cost's epilogue and the greedy's own first pass instead of the fused
+    # epilogue): the same cost and picks.
+    p_ms = avg("p0", "p1") if fused else None
+    if fused:
+        sel_step = r.selected.clone()
+        for i in range(K):
+            _timed(run_f, ev["f0"], ev["f1"], i)
+            rs = _timed(run_s, ev["s0"], ev["s1"], i)
+        torch.cuda.synchronize()
+        assert torch.equal(rs.selected, sel_step), "coverprune_prune and the two calls picked differently"
     f_ms, s_ms = avg("f0", "f1"), avg("s0", "s1")
-    ms_per_step = wall * 1e3 / K
 
     # CoverPrune-Lite on the same scene, outside the step (an alternative to
     # the cost and greedy, not a part of them).
@@ -359,8 +376,10 @@ def main():
     # schedule writes in its step-0 pass and the candidate lists of its later
     # steps are not counted.  The unit is the whole sgs_select call (its
     # kernels run back to back on one stream: slot clearing, scale, first
-    # pass, rows kernel for the first 128 steps, list build, list kernel), so
-    # one pair of events brackets it.  The compact schedule (changes exchanged
+    # pass, the early kernel while steps lower many targets, the rows kernel
+    # to step 128, list build, list kernel), so one pair of events brackets
+    # it; inside coverprune_prune the same kernels run without the first
+    # pass.  The compact schedule (changes exchanged
     # between blocks, no copy) is timed beside it.
     compact = None
     if args.sgs == "incremental":
@@ -380,8 +399,8 @@ def main():
         sgs_gbs = sgs_bytes / (s_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(sgs_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(sgs_gbs / HBM_PEAK_GBS, 4), "traffic": traffic("sgs_select", cfg.name),
-                    "kernel": "sgs_select (inc_first_pass_kernel, sgs_rows_kernel, list_build_kernel, "
-                              "sgs_list_kernel)",
+                    "kernel": "sgs_select (inc_first_pass_kernel, sgs_early_kernel, sgs_rows_kernel, "
+                              "list_build_kernel, sgs_list_kernel)",
                     "bytes_per_launch": sgs_bytes, "ms_per_launch": round(s_ms, 3),
                     "changed_targets": changed, "us_per_greedy_step": round(s_ms * 1e3 / k, 2)}
     else:
@@ -556,6 +575,7 @@ def main():
                    "lite_voxel_m": lite_h, "seed": args.seed, "sgs": args.sgs},
         "roofline": roofline,
         "breakdown": {
+            "prune_ms": round(p_ms, 3) if fused else None,
             "fst_cost_ms": round(f_ms, 3),
             "sgs_select_ms": round(s_ms, 3),
             "sgs_dense_sweep": dense,
@@ -566,7 +586,7 @@ def main():
             "fst_capacity": cap,
             "sgs_literal": lit,
             "sgs_batch": batch,
-            "coverprune_ms_per_scene": round(f_ms + s_ms, 3),
+            "two_calls_ms_per_scene": round(f_ms + s_ms, 3),
             "lite_select_ms_same_scene": round(l_ms, 3),
             "fst_cost_mfma": {"bound": "mfma", "achieved": round(f_tflops, 1), "peak": peak,
                               "unit": "TFLOP/s", "frac": round(f_tflops / peak, 4),

@@ -225,6 +225,42 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
                                 size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* The whole prune of one scene (Sec. 3): the FST cost (Sec. 3.3, Eq. 7-8)
+ * and the incremental greedy (Sec. 3.5, Eq. 11-16) in one call.
+ *
+ * The result is that of coverprune_fst_cost followed by coverprune_sgs_select
+ * with CP_SGS_INCREMENTAL on the same arguments: the same cost in `cost`, the
+ * same picks, gains, objective and assignment.  When n is a multiple of 64
+ * and the greedy's rows schedule serves n (n <= 32768 on a device of 256
+ * compute units), the cost's epilogue also writes the greedy's source-major
+ * copy of the cost and its step-0 gains (as fixed-point partial sums over
+ * blocks of 64 targets), so the greedy starts without a pass of its own over
+ * the cost; otherwise the two calls' kernels run one after the other.
+ *
+ *   feats .. w       as for coverprune_fst_cost
+ *   capacity .. c0   as for coverprune_sgs_select (c0 >= every cost value,
+ *                    e.g. coverprune_uncovered_cost(w))
+ *   cost             [n, n] float output, target-major (16-byte aligned)
+ *   maxima           [3] float output (may be NULL), as for coverprune_fst_cost
+ *   selected .. assign  outputs as for coverprune_sgs_select
+ *   workspace        device memory of coverprune_prune_workspace bytes (0 for
+ *                    bad sizes): the FST workspace, then the greedy's
+ *                    incremental workspace, plus, when n is a multiple of 64,
+ *                    the partial gains (8 bytes per column and block of 64
+ *                    targets: 32 MB at n = 16384)
+ * Errors: CP_ERR_INVALID_ARG / CP_ERR_UNSUPPORTED for bad arguments (checked
+ * before anything is enqueued), CP_ERR_HIP when a launch fails.  A greedy
+ * whose bounded waits give up writes -1 into every selected[] entry, as for
+ * coverprune_sgs_select.
+ */
+size_t coverprune_prune_workspace(int64_t n, int64_t d, int64_t k, cp_dtype dtype);
+cp_status coverprune_prune(const void* feats, cp_dtype dtype, int64_t n, int64_t d, const float* pos,
+                           const int32_t* frame, cp_fst_weights w, const float* capacity, int64_t k, float c0,
+                           float* cost, float* maxima, int32_t* selected, double* step_gain,
+                           double* step_objective, int32_t* assign, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Several scenes' greedies in one launch (the incremental form).
  *
  * Pruning runs once per request before the language model's prefill

@@ -23,7 +23,7 @@ from typing import Optional
 
 import torch
 
-__all__ = ["fst_cost", "fst_capacity", "sgs_select", "sgs_select_batch", "sgs_literal_select", "knn",
+__all__ = ["fst_cost", "fst_capacity", "prune", "sgs_select", "sgs_select_batch", "sgs_literal_select", "knn",
            "sgs_local_select", "lite_select", "uncovered_cost", "step_floor", "library", "library_path", "CoverPruneError",
            "DEFAULT_KAPPA"]
 
@@ -116,6 +116,11 @@ def library() -> ctypes.CDLL:
     lib.coverprune_fst_cost.restype = st
     lib.coverprune_sgs_workspace.argtypes = [i64, i64, ctypes.c_uint32]
     lib.coverprune_sgs_workspace.restype = sz
+    lib.coverprune_prune_workspace.argtypes = [i64, i64, i64, ctypes.c_int]
+    lib.coverprune_prune_workspace.restype = sz
+    lib.coverprune_prune.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, _Weights, vp, i64, ctypes.c_float,
+                                     vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.coverprune_prune.restype = st
     lib.coverprune_sgs_select.argtypes = [vp, i64, vp, i64, ctypes.c_float, u32, vp, vp, vp, vp, vp, sz, vp]
     lib.coverprune_sgs_select.restype = st
     lib.coverprune_fst_capacity_workspace.argtypes = [i64, i64]
@@ -328,6 +333,46 @@ def sgs_select(cost: torch.Tensor, capacity: torch.Tensor, k: int, c0: Optional[
                                      workspace.numel(), _stream(stream)))
     r = SgsResult(sel, gain, obj, assign)
     return r.check(stream) if (check or _debug()) else r
+
+
+def prune(feats: torch.Tensor, pos: torch.Tensor, frame: torch.Tensor, capacity: torch.Tensor, k: int,
+          c0: Optional[float] = None, weights=(1.0, 1.0, 1.0), kappa: float = DEFAULT_KAPPA,
+          out: Optional[torch.Tensor] = None, maxima: Optional[torch.Tensor] = None,
+          workspace: Optional[torch.Tensor] = None, stream=None, check: bool = False):
+    """The whole prune of one scene (Sec. 3): the FST cost and the
+    incremental greedy in one call (coverprune_prune), the same result as
+    fst_cost followed by sgs_select(incremental=True).  c0 defaults to
+    coverprune_uncovered_cost(weights).  Returns (cost, maxima, SgsResult)."""
+    lib = library()
+    n, d = feats.shape
+    dev = feats.device
+    dt = _feature_dtype(feats)
+    _need(feats, "feats", feats.dtype, (n, d), dev)
+    _need(pos, "pos", torch.float32, (n, 3), dev)
+    _need(frame, "frame", torch.int32, (n,), dev)
+    _need(capacity, "capacity", torch.float32, (n,), dev)
+    if _debug():
+        _debug_features(feats, pos, frame)
+        _debug_capacity(capacity)
+    if out is None:
+        out = torch.empty((n, n), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, (n, n), dev)
+    if maxima is None:
+        maxima = torch.empty(3, dtype=torch.float32, device=dev)
+    _need(maxima, "maxima", torch.float32, (3,), dev)
+    c0 = _c0(c0, weights)
+    sel = torch.empty(int(k), dtype=torch.int32, device=dev)
+    gain = torch.empty(int(k), dtype=torch.float64, device=dev)
+    obj = torch.empty(int(k), dtype=torch.float64, device=dev)
+    assign = torch.empty(n, dtype=torch.int32, device=dev)
+    need = lib.coverprune_prune_workspace(n, d, int(k), dt)
+    if workspace is None:
+        workspace = _workspace(need, dev)
+    _check(lib.coverprune_prune(_ptr(feats), dt, n, d, _ptr(pos), _ptr(frame), _weights(weights, kappa),
+                                _ptr(capacity), int(k), float(c0), _ptr(out), _ptr(maxima), _ptr(sel), _ptr(gain),
+                                _ptr(obj), _ptr(assign), _ptr(workspace), workspace.numel(), _stream(stream)))
+    r = SgsResult(sel, gain, obj, assign)
+    return out, maxima, (r.check(stream) if (check or _debug()) else r)
 
 
 def sgs_select_batch(costs, capacities, ks, c0: Optional[float] = None, weights=(1.0, 1.0, 1.0),

@@ -188,6 +188,97 @@ cp_status coverprune_sgs_select(const float* cost, int64_t n, const float* capac
 }
 
 // ---------------------------------------------------------------------------
+// The greedy's part of the prune workspace: the fused form's (the rows
+// schedule and the epilogue's partial gains) for n a multiple of 64, the
+// incremental form's otherwise.
+static size_t prune_sgs_bytes(int64_t n, int64_t k) {
+  return n % 64 == 0 ? cp::sgs_fused_workspace_bytes(n, k) : cp::sgs_inc_workspace_bytes(n, k, false);
+}
+
+size_t coverprune_prune_workspace(int64_t n, int64_t d, int64_t k, cp_dtype dtype) {
+  if (n < 1 || k < 1 || k > n) return 0;
+  return align_up(coverprune_fst_cost_workspace(n, d, dtype)) + prune_sgs_bytes(n, k);
+}
+
+cp_status coverprune_prune(const void* feats, cp_dtype dtype, int64_t n, int64_t d, const float* pos,
+                           const int32_t* frame, cp_fst_weights w, const float* capacity, int64_t k, float c0,
+                           float* cost, float* maxima, int32_t* selected, double* step_gain,
+                           double* step_objective, int32_t* assign, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  cp_status st = check_features(feats, dtype, n, d, kMaxDenseN);
+  if (st != CP_OK) return st;
+  if (k < 1 || k > n) return fail(CP_ERR_INVALID_ARG, "k = %lld outside [1, n = %lld]", (long long)k, (long long)n);
+  if (!std::isfinite(c0)) return fail(CP_ERR_INVALID_ARG, "c0 must be finite");
+  if (!pos || !frame || !cost || !capacity || !selected)
+    return fail(CP_ERR_INVALID_ARG, "pos, frame, cost, capacity and selected must be non-NULL");
+  if (!aligned16(cost)) return fail(CP_ERR_INVALID_ARG, "cost is not 16-byte aligned");
+  if ((st = check_weights(w)) != CP_OK) return st;
+  if ((st = check_workspace(workspace, workspace_bytes, coverprune_prune_workspace(n, d, k, dtype))) != CP_OK)
+    return st;
+
+  const size_t fst_bytes = align_up(coverprune_fst_cost_workspace(n, d, dtype));
+  char* base = static_cast<char*>(workspace);
+  cp::FstScratch s;
+  s.inv_norm = reinterpret_cast<float*>(base);
+  char* tail = base + align_up(size_t(n) * sizeof(float));
+  s.mf_bits = reinterpret_cast<unsigned int*>(tail);
+  s.tau_min = reinterpret_cast<int*>(tail + 4);
+  s.tau_max = reinterpret_cast<int*>(tail + 8);
+  s.mx2_bits = reinterpret_cast<unsigned long long*>(tail + 16);
+
+  cp::FstParams p;
+  p.feats = feats;
+  p.bf16 = dtype == CP_BF16;
+  p.n = int(n);
+  p.d = int(d);
+  p.pos = pos;
+  p.frame = frame;
+  p.lambda_f = w.lambda_f;
+  p.lambda_x = w.lambda_x;
+  p.lambda_tau = w.lambda_tau;
+  p.kappa = w.kappa;
+  p.inv_log1p_kappa = inv_log1p(w.kappa);
+  p.cost = cost;
+  p.maxima = maxima;
+
+  cp::SgsParams q;
+  q.cost = cost;
+  q.n = int(n);
+  q.capacity = capacity;
+  q.k = int(k);
+  q.c0 = c0;
+  q.selected = selected;
+  q.step_gain = step_gain;
+  q.step_objective = step_objective;
+  q.assign = assign;
+  q.workspace = base + fst_bytes;
+  q.workspace_bytes = workspace_bytes - fst_bytes;
+
+  hipStream_t s_ = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if ((e = cp::launch_fst_prep(p, s, s_)) != hipSuccess) return hip_fail(e, "fst prep");
+  if ((e = cp::launch_gram(p, s, s_)) != hipSuccess) return hip_fail(e, "gram");
+  if (!cp::sgs_fused_fits(n)) {
+    // The two calls' kernels one after the other.
+    if ((e = cp::launch_fst_epilogue(p, s, s_)) != hipSuccess) return hip_fail(e, "fst epilogue");
+    if ((e = cp::launch_sgs_incremental(q, false, s_)) != hipSuccess) return hip_fail(e, "sgs");
+    return ok();
+  }
+  cp::SgsFused f;
+  if ((e = cp::sgs_fused_prepare(q, &f, s_)) != hipSuccess) return hip_fail(e, "sgs scale");
+  cp::EpiSgs g;
+  g.T = f.T;
+  g.ldt = f.ldt;
+  g.part = f.part;
+  g.v = capacity;
+  g.c0 = c0;
+  g.scale = f.scale;
+  if ((e = cp::launch_fst_epilogue_sgs(p, s, g, s_)) != hipSuccess) return hip_fail(e, "fst epilogue");
+  if ((e = cp::launch_sgs_fused(q, f, s_)) != hipSuccess) return hip_fail(e, "sgs");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
 static bool batch_flags_ok(uint32_t flags) {
   return flags == CP_SGS_INCREMENTAL || flags == (CP_SGS_INCREMENTAL | CP_SGS_COMPACT);
 }

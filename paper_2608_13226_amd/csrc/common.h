@@ -49,6 +49,15 @@ __device__ __forceinline__ int wave_min(int x) {
   return x;
 }
 
+// A 64-bit value moved between lanes by a DPP pattern (both halves).  Every
+// lane of the wave must be active.
+template <int CTRL>
+__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long x) {
+  const unsigned a = __builtin_amdgcn_mov_dpp(unsigned(x), CTRL, 0xf, 0xf, false);
+  const unsigned b = __builtin_amdgcn_mov_dpp(unsigned(x >> 32), CTRL, 0xf, 0xf, false);
+  return ((unsigned long long)b << 32) | a;
+}
+
 // For x >= 0 the IEEE bit pattern orders like the value, so an unsigned
 // integer atomicMax on the bits is an exact, order-independent float max.
 __device__ __forceinline__ void atomic_max_nonneg(unsigned int* bits, float x) {

@@ -10,6 +10,7 @@
 #include <climits>
 
 #include "common.h"
+#include "fixed_point.h"
 #include "launch.h"
 
 namespace cp {
@@ -263,6 +264,149 @@ __global__ __launch_bounds__(256) void fst_epilogue_kernel(FstParams p, FstScrat
   }
 }
 
+// The epilogue of coverprune_prune (n a multiple of 64): the cost as above,
+// and for the greedy that follows it the source-major copy T and the step-0
+// gains, so that the greedy needs no pass of its own over the cost.  For the
+// upper tile pair (ti, tj), with X[r][c] = C(s = j_c, t = i_r) (the tile's
+// own entries) and Y[r][c] = C(s = i_r, t = j_c) (its mirror's, transposed):
+//   C_tm tile (ti, tj) = X and, off the diagonal, C_tm tile (tj, ti) = Y^T;
+//   T tile (tj, ti) = X^T and, off the diagonal, T tile (ti, tj) = Y;
+//   part[ti][j_c] = sum_r fx(v_{i_r} max(0, c0 - X[r][c])) and, off the
+//   diagonal, part[tj][i_r] = sum_c fx(v_{j_c} max(0, c0 - Y[r][c])).
+// Every (64-target block, column) partial is written exactly once, and the
+// greedy adds the n / 64 partials of a column in 64-bit integers, so the
+// gains do not depend on the split.  A thread holds 4 rows x 4 columns of
+// both X and Y; the two transposed tiles go through LDS one after the other.
+__global__ __launch_bounds__(256) void fst_epilogue_sgs_kernel(FstParams p, FstScratch s, EpiSgs g) {
+  int ti, tj;
+  upper_tile(blockIdx.x, ti, tj);
+  const int n = p.n;
+  __shared__ float rx[kEpiTile], ry[kEpiTile], rz[kEpiTile], cx[kEpiTile], cy[kEpiTile], cz[kEpiTile];
+  __shared__ int rf[kEpiTile], cf[kEpiTile];
+  __shared__ double rvs[kEpiTile], cvs[kEpiTile];
+  __shared__ float tr[kEpiTile][kEpiTile + 1];
+  __shared__ long long red[4][kEpiTile];
+
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int S = *g.scale;
+  if (t < kEpiTile) {
+    const int i = ti * kEpiTile + t;
+    rx[t] = p.pos[3 * i];
+    ry[t] = p.pos[3 * i + 1];
+    rz[t] = p.pos[3 * i + 2];
+    rf[t] = p.frame[i];
+    rvs[t] = fx_scale(double(g.v[i]), S);
+  } else if (t < 2 * kEpiTile) {
+    const int c = t - kEpiTile, j = tj * kEpiTile + c;
+    cx[c] = p.pos[3 * j];
+    cy[c] = p.pos[3 * j + 1];
+    cz[c] = p.pos[3 * j + 2];
+    cf[c] = p.frame[j];
+    cvs[c] = fx_scale(double(g.v[j]), S);
+  }
+  const float m_f = __uint_as_float(*s.mf_bits);
+  const float m_x = float(sqrt(__longlong_as_double((long long)*s.mx2_bits)));
+  const int m_t = *s.tau_max - *s.tau_min;
+  if (blockIdx.x == 0 && t == 0 && p.maxima) {
+    p.maxima[0] = m_f;
+    p.maxima[1] = m_x;
+    p.maxima[2] = float(m_t);
+  }
+  const float wf = m_f > 0.f ? p.lambda_f / m_f : 0.f;
+  const float inv_mx = m_x > 0.f ? 1.f / m_x : 0.f;
+  const float wt = m_t > 0 ? p.lambda_tau / float(m_t) : 0.f;
+  __syncthreads();
+
+  const bool mirror = ti != tj;
+  const int c4 = (t & 15) * 4, r0 = t >> 4;
+  float X[4][4], Y[4][4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int r = r0 + 16 * k;
+    float4* at = reinterpret_cast<float4*>(p.cost + size_t(ti * kEpiTile + r) * n + tj * kEpiTile + c4);
+    const float4 df4 = *at;
+    const float df[4] = {df4.x, df4.y, df4.z, df4.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = c4 + u;
+      const float dx = rx[r] - cx[c], dy = ry[r] - cy[c], dz = rz[r] - cz[c];
+      const float dist = __builtin_amdgcn_sqrtf(dx * dx + dy * dy + dz * dz);
+      const float base = wf * df[u] + p.lambda_x * phi_kappa(dist * inv_mx, p.kappa, p.inv_log1p_kappa);
+      X[k][u] = base + wt * float(max(0, cf[c] - rf[r]));
+      Y[k][u] = base + wt * float(max(0, rf[r] - cf[c]));
+    }
+    *at = make_float4(X[k][0], X[k][1], X[k][2], X[k][3]);
+    if (mirror)
+      *reinterpret_cast<float4*>(g.T + size_t(ti * kEpiTile + r) * g.ldt + tj * kEpiTile + c4) =
+          make_float4(Y[k][0], Y[k][1], Y[k][2], Y[k][3]);
+  }
+
+  // Step-0 partial gains.  Column sums of X: a thread's four rows, then the
+  // lanes 16 and 32 apart (same columns, other rows), then the four waves.
+  unsigned long long xs[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    long long a = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) a += fx_term(rvs[r0 + 16 * k], fmaxf(g.c0 - X[k][u], 0.f));
+    xs[u] = (unsigned long long)a;
+#pragma unroll
+    for (int o = 16; o < 64; o <<= 1) xs[u] += __shfl_xor(xs[u], o);
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) red[w][c4 + u] = (long long)xs[u];
+  }
+  // Row sums of Y (mirror tiles): a thread's four columns, then the 16 lanes
+  // of its row (a DPP row).
+  if (mirror) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      long long a = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) a += fx_term(cvs[c4 + u], fmaxf(g.c0 - Y[k][u], 0.f));
+      unsigned long long y = (unsigned long long)a;
+      y += dpp_u64<0xB1>(y);    // quad_perm [1,0,3,2]
+      y += dpp_u64<0x4E>(y);    // quad_perm [2,3,0,1]
+      y += dpp_u64<0x141>(y);   // row_half_mirror
+      y += dpp_u64<0x140>(y);   // row_mirror
+      if ((t & 15) == 0) g.part[size_t(tj) * n + ti * kEpiTile + r0 + 16 * k] = (long long)y;
+    }
+  }
+  __syncthreads();
+  if (t < kEpiTile)
+    g.part[size_t(ti) * n + tj * kEpiTile + t] = red[0][t] + red[1][t] + red[2][t] + red[3][t];
+
+  // Off the diagonal, C_tm tile (tj, ti) = Y^T; then T tile (tj, ti) = X^T
+  // (on the diagonal too: there the Gram's two triangles can differ in the
+  // last bit, so T is the cost's own transpose rather than Y), through LDS.
+  if (mirror) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) tr[c4 + u][r0 + 16 * k] = Y[k][u];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int r = r0 + 16 * k;
+      *reinterpret_cast<float4*>(p.cost + size_t(tj * kEpiTile + r) * n + ti * kEpiTile + c4) =
+          make_float4(tr[r][c4], tr[r][c4 + 1], tr[r][c4 + 2], tr[r][c4 + 3]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) tr[c4 + u][r0 + 16 * k] = X[k][u];
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int r = r0 + 16 * k;
+    *reinterpret_cast<float4*>(g.T + size_t(tj * kEpiTile + r) * g.ldt + ti * kEpiTile + c4) =
+        make_float4(tr[r][c4], tr[r][c4 + 1], tr[r][c4 + 2], tr[r][c4 + 3]);
+  }
+}
+
 int tiles_of(int n, int tile) { return (n + tile - 1) / tile; }
 
 }  // namespace
@@ -280,6 +424,13 @@ hipError_t launch_fst_prep(const FstParams& p, const FstScratch& s, hipStream_t 
   const int t = tiles_of(p.n, kPosTile);
   const int tiles = t * (t + 1) / 2;
   pos_pairmax_kernel<<<tiles, 256, 0, stream>>>(p.pos, p.n, tiles, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_fst_epilogue_sgs(const FstParams& p, const FstScratch& s, const EpiSgs& g, hipStream_t stream) {
+  if (p.n % kEpiTile != 0) return hipErrorInvalidValue;
+  const int t = p.n / kEpiTile;
+  fst_epilogue_sgs_kernel<<<t * (t + 1) / 2, 256, 0, stream>>>(p, s, g);
   return hipGetLastError();
 }
 

@@ -419,6 +419,37 @@ __device__ int read_winner_rows(const unsigned long long* slots, unsigned long l
 constexpr int kChain = 1;   // predicted steps in a row at most (deeper chains measured slower)
 constexpr int kTrackMax = 256;   // hits of a step that still tracks the chain
 
+// The step-0 gains of a block's columns [lo, lo + cnt) from the P partial
+// sums part[q][column] (64-bit integers, so the split does not matter):
+// thread (column tid % 64, group tid / 64) adds partials group, group +
+// kWaves, ..., eight loads in flight, then the groups' sums are added in
+// LDS.  P is 3 after the first pass, n / 64 after the fused epilogue.
+__device__ __forceinline__ void init_gains(const IncDev& a, long long* sG, int lo, int cnt, long long* red) {
+  const int tid = threadIdx.x, g = tid >> 6;
+  for (int i0 = 0; i0 < cnt; i0 += 64) {
+    const int i = i0 + (tid & 63);
+    const int col = lo + min(i, cnt - 1);
+    long long x = 0;
+    for (int q0 = g; q0 < a.P; q0 += 8 * kWaves) {
+      long long v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = a.part[size_t(min(q0 + u * kWaves, a.P - 1)) * a.n + col];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (q0 + u * kWaves < a.P) x += v[u];
+    }
+    red[tid] = x;
+    __syncthreads();
+    if (tid < 64 && i0 + tid < cnt) {
+      long long t = 0;
+#pragma unroll
+      for (int r = 0; r < kWaves; ++r) t += red[r * 64 + tid];
+      sG[i0 + tid] = t;
+    }
+    __syncthreads();
+  }
+}
+
 // NG 64-column groups per block (W <= 64 NG); RL chunk loads per wave and
 // step (n <= kRowChunk kWaves RL).
 template <int NG, int RL>
@@ -473,12 +504,8 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     }
   } else {
     for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
-    for (int i = tid; i < cnt; i += kBlock) {
-      ssel[i] = 0;
-      long long g = 0;
-      for (int q = 0; q < a.P; ++q) g += a.part[size_t(q) * a.n + lo + i];
-      sG[i] = g;
-    }
+    for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
+    init_gains(a, sG, lo, cnt, red);
   }
   __syncthreads();
 
@@ -947,13 +974,8 @@ __global__ __launch_bounds__(kBlock) void sgs_early_kernel(IncDev a) {
 
   const int S = *a.scale;
   for (int j = tid; j < a.ldt; j += kBlock) sball[j] = j < a.n ? a.c0 : -__builtin_inff();
-  for (int i = tid; i < cnt; i += kBlock) {
-    ssel[i] = 0;
-    long long g = 0;
-    for (int q = 0; q < a.P; ++q) g += a.part[size_t(q) * a.n + lo + i];
-    sG[i] = g;
-  }
-  __syncthreads();
+  for (int i = tid; i < cnt; i += kBlock) ssel[i] = 0;
+  init_gains(a, sG, lo, cnt, red);
   // Block 0 keeps the objective (in wave 1 after the start).
   long long L = 0;
   if (blk == 0) {
@@ -1289,7 +1311,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   if (*a.lfail || *a.abort) return;
   extern __shared__ unsigned long long smem[];
   const int blk = blockIdx.x, nb = gridDim.x;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int lo = blk * a.W;
   const int cnt = max(0, min(a.n, lo + a.W) - lo);
   float* sball = reinterpret_cast<float*>(smem);                   // [ldt] best costs
@@ -1803,23 +1825,33 @@ hipError_t fits(const void* kernel, size_t lds) {
   return per_cu < 1 ? hipErrorCooperativeLaunchTooLarge : hipSuccess;
 }
 
-}  // namespace
-
-size_t sgs_inc_workspace_bytes(int64_t n, int64_t k, bool compact) { return inc_bytes(n, k, compact); }
-
-hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t stream) {
-  int dev = 0, cus = 0;
+int device_cus(int* cus) {
+  int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  return hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev);
+}
+
+// The greedy's launches; with `fused` the step-0 gains and T were written by
+// fst_epilogue_sgs_kernel (and the scale before it), so the first pass is
+// skipped and the gains come from its partial sums.
+hipError_t run_incremental(const SgsParams& p, bool compact, const SgsFused* fused, hipStream_t stream) {
+  int cus = 0;
+  hipError_t e = hipError_t(device_cus(&cus));
+  if (e != hipSuccess) return e;
   const int nb = blocks_for(p.n, cus);
   const int W = (p.n + nb - 1) / nb;
   const bool rows = !compact && use_rows(p.n, W);
+  if (fused && !rows) return hipErrorInvalidValue;
   const void* kernel = rows ? rows_kernel(p.n, W) : reinterpret_cast<const void*>(sgs_inc_kernel);
   const size_t lds = rows ? lds_rows(W, p.n) : lds_for(W);
   if ((e = fits(kernel, lds)) != hipSuccess) return e;
 
   IncDev a = inc_dev(p, static_cast<char*>(p.workspace), W, rows);
+  if (fused) {
+    a.part = fused->part;
+    a.P = fused->P;
+  }
   // Scenes the list phase serves: the rows kernel stops after kListStep
   // steps, the lists are built, and the list kernel (or, when the lists do
   // not fit, the rows kernel again) runs the rest.
@@ -1834,7 +1866,7 @@ hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t 
   if (early && (e = fits(reinterpret_cast<const void*>(sgs_early_kernel), lds)) != hipSuccess) return e;
   sgs_inc_init_kernel<<<std::min(1024, (std::max(p.n, p.k) + 255) / 256), 256, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if ((e = launch_first_pass(a, nb, stream)) != hipSuccess) return e;
+  if (!fused && (e = launch_first_pass(a, nb, stream)) != hipSuccess) return e;
   if (early) {
     void* eargs[] = {&a};
     if ((e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(sgs_early_kernel), dim3(nb), dim3(kBlock), eargs,
@@ -1862,6 +1894,46 @@ hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t 
     if ((e = hipLaunchCooperativeKernel(kernel, dim3(nb), dim3(kBlock), cargs, lds, stream)) != hipSuccess) return e;
   }
   return launch_mark_aborted(a.abort, a.selected, a.k, stream);
+}
+
+}  // namespace
+
+size_t sgs_inc_workspace_bytes(int64_t n, int64_t k, bool compact) { return inc_bytes(n, k, compact); }
+
+hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t stream) {
+  return run_incremental(p, compact, nullptr, stream);
+}
+
+// coverprune_prune: the rows schedule's workspace, then the epilogue's
+// partial gains, [n / 64][n] 64-bit integers.
+bool sgs_fused_fits(int64_t n) {
+  int cus = 0;
+  if (device_cus(&cus) != hipSuccess || n < 64 || n % 64 != 0) return false;
+  const int nb = blocks_for(n, cus);
+  return use_rows(n, int((n + nb - 1) / nb));
+}
+
+size_t sgs_fused_workspace_bytes(int64_t n, int64_t k) {
+  return inc_bytes(n, k, false) + a256(size_t(n / 64) * size_t(n) * 8);
+}
+
+hipError_t sgs_fused_prepare(const SgsParams& p, SgsFused* f, hipStream_t stream) {
+  int cus = 0;
+  hipError_t e = hipError_t(device_cus(&cus));
+  if (e != hipSuccess) return e;
+  const int nb = blocks_for(p.n, cus);
+  IncDev a = inc_dev(p, static_cast<char*>(p.workspace), (p.n + nb - 1) / nb, true);
+  f->T = a.T;
+  f->ldt = a.ldt;
+  f->part = reinterpret_cast<long long*>(static_cast<char*>(p.workspace) + inc_bytes(p.n, p.k, false));
+  f->P = p.n / 64;
+  f->scale = const_cast<int*>(a.scale);
+  inc_scale_kernel<<<1, kBlock, 0, stream>>>(a, f->scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_sgs_fused(const SgsParams& p, const SgsFused& f, hipStream_t stream) {
+  return run_incremental(p, false, &f, stream);
 }
 
 size_t sgs_inc_batch_workspace_bytes(const int64_t* n, const int64_t* k, int count, bool compact) {

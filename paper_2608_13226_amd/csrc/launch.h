@@ -34,6 +34,19 @@ hipError_t launch_fst_prep(const FstParams& p, const FstScratch& s, hipStream_t 
 hipError_t launch_gram(const FstParams& p, const FstScratch& s, hipStream_t stream);
 hipError_t launch_fst_epilogue(const FstParams& p, const FstScratch& s, hipStream_t stream);
 
+// The epilogue of coverprune_prune (n a multiple of 64): the cost, and for
+// the incremental greedy that follows, its source-major copy T and the
+// step-0 gains as partial sums over 64-target blocks.
+struct EpiSgs {
+  float* T;                       // [n][ldt] T[s][t] = C(s, t)
+  int ldt;
+  long long* part;                // [n / 64][n] fixed-point partial gains
+  const float* v;                 // [n] capacities
+  float c0;
+  const int* scale;               // the greedy's fixed-point exponent, set before the launch
+};
+hipError_t launch_fst_epilogue_sgs(const FstParams& p, const FstScratch& s, const EpiSgs& g, hipStream_t stream);
+
 // Greedy selection.
 struct SgsParams {
   const float* cost;              // [n, n] target-major
@@ -56,6 +69,23 @@ hipError_t launch_sgs_dense(const SgsParams& p, hipStream_t stream);
 // schedule (about 16 bytes per token).
 size_t sgs_inc_workspace_bytes(int64_t n, int64_t k, bool compact);
 hipError_t launch_sgs_incremental(const SgsParams& p, bool compact, hipStream_t stream);
+// The incremental greedy after launch_fst_epilogue_sgs (coverprune_prune):
+// the rows schedule, whose T and step-0 partial gains that epilogue writes.
+// sgs_fused_fits: n a multiple of 64 that the rows schedule serves on this
+// device.  sgs_fused_prepare points f into p.workspace (sized by
+// sgs_fused_workspace_bytes) and enqueues the scale the epilogue needs;
+// launch_sgs_fused runs the greedy itself.
+struct SgsFused {
+  float* T;
+  int ldt;
+  long long* part;
+  int P;
+  int* scale;
+};
+bool sgs_fused_fits(int64_t n);
+size_t sgs_fused_workspace_bytes(int64_t n, int64_t k);
+hipError_t sgs_fused_prepare(const SgsParams& p, SgsFused* f, hipStream_t stream);
+hipError_t launch_sgs_fused(const SgsParams& p, const SgsFused& f, hipStream_t stream);
 // Up to 16 scenes in one cooperative launch (incremental form); the scenes'
 // workspaces lie one after another in `workspace` (each p[s].workspace is
 // ignored).
