@@ -590,7 +590,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     // flight: the best keys of distinct blocks in order, each taken out in
     // turn.  Blocks own W consecutive columns, so the winner's block is t / W.
     if (kSpec && !predicted) {
-      const int bt = t / a.W;
+      const int bt = block_of(a, t);
       unsigned long long k[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -604,7 +604,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
         const unsigned long long kr = wave_max_u64(max(max(k[0], k[1]), max(k[2], k[3])));
         const bool real = kr > kNoCandidate && (m == 0 || bprev >= 0);
         const int r = real ? int(kIndexMask - (kr & kIndexMask)) : -1;
-        const int br = real ? r / a.W : -1;
+        const int br = real ? block_of(a, r) : -1;
         if (m > 0) ub[m - 1] = max(real ? kr : 0ull, u2) >> kIndexBits;
         if (m < kChain) {
           rc[m] = r;
@@ -1443,7 +1443,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
       t = min(tw, a.n - 1);
       if (tid <= kListChain) sacc[tid] = 0ull;
       // The chain from the exchange's keys (every wave the same).
-      const int bt = t / a.W;
+      const int bt = block_of(a, t);
       unsigned long long kq[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -1457,7 +1457,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
         const unsigned long long kr = wave_max_u64(max(max(kq[0], kq[1]), max(kq[2], kq[3])));
         const bool real = kr > kNoCandidate && (m == 1 || rc[m - 1] >= 0);
         const int r = real ? int(kIndexMask - (kr & kIndexMask)) : -1;
-        const int br = real ? r / a.W : -1;
+        const int br = real ? block_of(a, r) : -1;
         if (m >= 2) ub[m - 1] = max(real ? kr : 0ull, u2) >> kIndexBits;
         if (m <= kListChain) {
           rc[m] = r;
@@ -1776,6 +1776,7 @@ IncDev inc_dev(const SgsParams& p, char* w, int W, bool rows) {
   a.poll_limit = wp.limit;
   a.abort_init = wp.preset;
   a.W = W;
+  a.w_magic = w_magic_of(W);
   const IncLayout M = inc_layout(p.n, p.k, !rows);
   a.T = rows ? reinterpret_cast<float*>(w + M.T) : nullptr;
   a.ldt = rows ? rows_ldt(p.n) : 0;

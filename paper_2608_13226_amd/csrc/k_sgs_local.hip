@@ -315,6 +315,7 @@ hipError_t launch_sgs_local(const SgsParams& p, const int32_t* nbr, int g, hipSt
   a.poll_limit = wp.limit;
   a.abort_init = wp.preset;
   a.W = W;
+  a.w_magic = w_magic_of(W);
   a.T = reinterpret_cast<float*>(w + Y.T);
   a.ldt = ldt;
   d.nbr = nbr;

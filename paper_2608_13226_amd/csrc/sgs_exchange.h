@@ -57,6 +57,7 @@ struct IncDev {
   unsigned int poll_limit;    // polls before a wait gives up (WaitPolicy)
   unsigned int abort_init;    // the abort flag's value at launch (WaitPolicy)
   int W;                      // rows and columns per block
+  unsigned int w_magic;       // floor(2^32 / W) + 1: block_of(c) = c / W by one high multiply
   float* T;                   // rows form only: [n][ldt] source-major copy, T[s][t] = C(s, t)
   int ldt;                    // its row stride, n rounded up to a whole 256-row chunk
   const long long* part;      // incremental form: [P][n] step-0 gains summed over P row ranges
@@ -82,6 +83,15 @@ struct IncDev {
   int ldp;
   const long long* start;
 };
+
+// The block that owns column c: c / W as the high word of c times
+// floor(2^32 / W) + 1, exact for c < 2^18 and 2 <= W <= 2^13 (the product
+// exceeds 2^32 c / W by less than c, which moves c / W by less than 2^-14,
+// below the gap 1 / W to the next integer).  W = 1 only with n = 1 (the
+// grid has one block per 64 tokens at most), where the multiplier wraps to
+// 0 and column 0's block is 0.
+__device__ __forceinline__ int block_of(const IncDev& a, int c) { return int(__umulhi(unsigned(c), a.w_magic)); }
+inline unsigned int w_magic_of(int W) { return unsigned(0xffffffffu / unsigned(W)) + 1u; }
 
 struct Layout {
   size_t list, lens, cand, ctrl, total;
