@@ -1324,7 +1324,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   auto off = [&](int j) { return int((soffw[j >> 1] >> ((j & 1) * 16)) & 0xffffu); };
   __shared__ long long sG[64];
   __shared__ unsigned char ssel[64];
-  __shared__ unsigned long long sdelta[64];
+  __shared__ unsigned long long sdelta[2][64];                      // own gain changes, by step parity
   __shared__ int soff[65];                                          // each own candidate's first pair
   __shared__ int swt[kWaves];
   __shared__ unsigned long long su[kWaves], sk1[kMaxBlocks], sk2[kMaxBlocks];
@@ -1338,7 +1338,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   if (tid < 64) {
     ssel[tid] = tid < cnt ? a.ho_sel[lo + tid] : 1;
     sG[tid] = tid < cnt ? a.ho_gain[lo + tid] : 0;
-    sdelta[tid] = 0ull;
+    sdelta[0][tid] = sdelta[1][tid] = 0ull;
     // Where each own candidate's pairs start among the block's.
     const int m = tid < cnt ? min(int(a.lists[size_t(lo + tid) * (2 * kListSlots)]), kListMax) : 0;
     const int incl = wave_scan_incl(m);
@@ -1435,6 +1435,7 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
   int pos = 0;                 // the step's place in the chain (0: after an exchange)
   for (int step = a.k_begin; step < a.k; ++step) {
     int t = -1;
+    const int par = step & 1;
     if (!predicted) {
       const int tw = read_winner_rows(cand_slot(a.cand, xc & 1, 0), epoch_of(xc), nb, a.abort, a.poll_limit, su,
                                       &sflag, sk1, sk2);
@@ -1523,7 +1524,8 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
           const int p1 = off(j + 1);
           for (int p = off(j); p < p1; ++p) {
             const float cv = spc[p];
-            if (cv < bo) atomicAdd(&sdelta[spk[p]], (unsigned long long)fx_diff(evs[q], fmaxf(x - cv, 0.f), bo - cv));
+            if (cv < bo)
+              atomicAdd(&sdelta[par][spk[p]], (unsigned long long)fx_diff(evs[q], fmaxf(x - cv, 0.f), bo - cv));
           }
         }
       }
@@ -1552,9 +1554,12 @@ __global__ __launch_bounds__(kBlock) void sgs_list_kernel(IncDev a) {
       }
     }
     __syncthreads();
+    // Wave 0 folds the step's own changes.  A predicted next step starts
+    // without a barrier, so its hits add into the other parity's buffer
+    // while this one is read and cleared.
     if (tid < 64) {
-      if (tid < cnt) sG[tid] += (long long)sdelta[tid];
-      sdelta[tid] = 0ull;
+      if (tid < cnt) sG[tid] += (long long)sdelta[par][tid];
+      sdelta[par][tid] = 0ull;
     }
     bool next = false;
     if (pos < kListChain && step + 1 < a.k) {
