@@ -575,8 +575,50 @@ struct PairMax {
   int tau = 0;
 };
 
-// Row tile t.ta against column tile tb: adds v_j d_f over adjacent pairs to
-// arow (the lane's four output rows) and raises the maxima.
+// The epilogue of a tile product: acc holds row tile t.ta against column
+// tile tb (output element (4 (l / 16) + r, l % 16) in register r of lane l),
+// na the squared norm of the lane's row l % 16 of tile ta and nb that of
+// column tile tb's row l % 16.  Adds v_j d_f over adjacent pairs to arow
+// (the lane's four output rows) and raises the maxima.
+__device__ __forceinline__ void pair_epilogue(const LiteDev& a, const int* perm, const Unit& t, int tb,
+                                              const f32x4& acc, float na, float nb, double* arow, PairMax& pm) {
+  const int lane = threadIdx.x & 63;
+  const int row = lane & 15, quad = lane >> 4;
+  const int ra = t.ta * kTileRows + row;
+  const int cb = tb * kTileRows + row;    // output column of this lane
+  const bool cvalid = cb < t.g;
+  const int tokb = cvalid ? perm[t.p0 + cb] : 0;
+  const unsigned long long vb = cvalid ? a.vox_pos[t.p0 + cb] : 0ull;
+  const double wv = cvalid ? double(a.v[tokb]) : 0.0;
+  const float xb = a.pos[3 * tokb], yb = a.pos[3 * tokb + 1], zb = a.pos[3 * tokb + 2];
+  const int fb = a.frame[tokb];
+  // Lane l (l < 16) also holds row l of tile ta's position and frame.
+  const int toka = ra < t.g ? perm[t.p0 + ra] : 0;
+  const float xa = a.pos[3 * toka], ya = a.pos[3 * toka + 1], za = a.pos[3 * toka + 2];
+  const int fa = a.frame[toka];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int oa = quad * 4 + r;           // output row within tile ta
+    const float nra = __shfl(na, oa);
+    const float xo = __shfl(xa, oa), yo = __shfl(ya, oa), zo = __shfl(za, oa);
+    const int fo = __shfl(fa, oa);
+    const int ca = t.ta * kTileRows + oa;
+    if (cvalid && ca < t.g && adjacent(a.vox_pos[t.p0 + ca], vb)) {
+      const float den = sqrtf(nra) * sqrtf(nb);
+      const float cosv = den > 0.f ? acc[r] / den : 0.f;
+      float df = fminf(fmaxf(1.f - cosv, 0.f), 2.f);
+      if (ca == cb) df = 0.f;
+      arow[r] = fma(wv, double(df), arow[r]);
+      pm.df = fmaxf(pm.df, df);
+      pm.x2 = fmax(pm.x2, sq_dist(xo, yo, zo, xb, yb, zb));
+      pm.tau = max(pm.tau, abs(fo - fb));
+    }
+  }
+}
+
+
+// Row tile t.ta against column tile tb: the product over the feature width,
+// then pair_epilogue.
 template <bool BF16>
 __device__ __forceinline__ void pair_tile(const LiteDev& a, const int* perm, const Unit& t, int tb, double* arow,
                                           PairMax& pm) {
@@ -641,34 +683,63 @@ __device__ __forceinline__ void pair_tile(const LiteDev& a, const int* perm, con
   na += __shfl_xor(na, 32);
   nb += __shfl_xor(nb, 16);
   nb += __shfl_xor(nb, 32);
-  const int cb = tb * kTileRows + row;    // output column of this lane
-  const bool cvalid = cb < t.g;
-  const int tokb = cvalid ? perm[t.p0 + cb] : 0;
-  const unsigned long long vb = cvalid ? a.vox_pos[t.p0 + cb] : 0ull;
-  const double wv = cvalid ? double(a.v[tokb]) : 0.0;
-  const float xb = a.pos[3 * tokb], yb = a.pos[3 * tokb + 1], zb = a.pos[3 * tokb + 2];
-  const int fb = a.frame[tokb];
-  // Lane l (l < 16) also holds row l of tile ta's position and frame.
-  const int toka = ra < t.g ? perm[t.p0 + ra] : 0;
-  const float xa = a.pos[3 * toka], ya = a.pos[3 * toka + 1], za = a.pos[3 * toka + 2];
-  const int fa = a.frame[toka];
+  pair_epilogue(a, perm, t, tb, acc, na, nb, arow, pm);
+}
+
+// Row tile t.ta of a group of two tiles against both column tiles, with
+// bfloat16 features: the lane's rows of both tiles are read once per K step
+// and feed the products ta x ta and ta x tb, which then go through
+// pair_epilogue in column-tile order, as the two pair_tile calls they
+// replace (the same products and sums, so the same values).  Those calls
+// read tile ta's rows twice.
+__device__ __forceinline__ void pair_tile_both(const LiteDev& a, const int* perm, const Unit& t, double* arow,
+                                               PairMax& pm) {
+  const int lane = threadIdx.x & 63;
+  const int row = lane & 15, quad = lane >> 4;
+  const int tb = 1 - t.ta;
+  const int ra = t.ta * kTileRows + row, rb = tb * kTileRows + row;
+  const uint16_t* Fa = ra < t.g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[t.p0 + ra]) * a.d : nullptr;
+  const uint16_t* Fb = rb < t.g ? static_cast<const uint16_t*>(a.feats) + size_t(perm[t.p0 + rb]) * a.d : nullptr;
+  f32x4 caa = {0.f, 0.f, 0.f, 0.f}, cab = caa;
+  float na = 0.f, nb = 0.f;
+  constexpr int U = 8;
+  for (int k0 = 0; k0 < a.d; k0 += 32 * U) {
+    uint4 ua[U], ub[U];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int oa = quad * 4 + r;           // output row within tile ta
-    const float nra = __shfl(na, oa);
-    const float xo = __shfl(xa, oa), yo = __shfl(ya, oa), zo = __shfl(za, oa);
-    const int fo = __shfl(fa, oa);
-    const int ca = t.ta * kTileRows + oa;
-    if (cvalid && ca < t.g && adjacent(a.vox_pos[t.p0 + ca], vb)) {
-      const float den = sqrtf(nra) * sqrtf(nb);
-      const float cosv = den > 0.f ? acc[r] / den : 0.f;
-      float df = fminf(fmaxf(1.f - cosv, 0.f), 2.f);
-      if (ca == cb) df = 0.f;
-      arow[r] = fma(wv, double(df), arow[r]);
-      pm.df = fmaxf(pm.df, df);
-      pm.x2 = fmax(pm.x2, sq_dist(xo, yo, zo, xb, yb, zb));
-      pm.tau = max(pm.tau, abs(fo - fb));
+    for (int x = 0; x < U; ++x) {
+      const int kk = k0 + 32 * x + quad * 8;
+      ua[x] = uint4{0u, 0u, 0u, 0u};
+      ub[x] = uint4{0u, 0u, 0u, 0u};
+      if (Fa && kk < a.d) ua[x] = *reinterpret_cast<const uint4*>(Fa + kk);
+      if (Fb && kk < a.d) ub[x] = *reinterpret_cast<const uint4*>(Fb + kk);
     }
+#pragma unroll
+    for (int x = 0; x < U; ++x) {
+      const uint32_t wa[4] = {ua[x].x, ua[x].y, ua[x].z, ua[x].w}, wb[4] = {ub[x].x, ub[x].y, ub[x].z, ub[x].w};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const float a0 = bf16_bits_to_float(wa[h] & 0xffffu), a1 = bf16_bits_to_float(wa[h] >> 16);
+        const float b0 = bf16_bits_to_float(wb[h] & 0xffffu), b1 = bf16_bits_to_float(wb[h] >> 16);
+        na = fmaf(a0, a0, fmaf(a1, a1, na));
+        nb = fmaf(b0, b0, fmaf(b1, b1, nb));
+      }
+      bf16x8 va, vb;
+      __builtin_memcpy(&va, &ua[x], sizeof va);
+      __builtin_memcpy(&vb, &ub[x], sizeof vb);
+      caa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, va, caa, 0, 0, 0);
+      cab = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, vb, cab, 0, 0, 0);
+    }
+  }
+  na += __shfl_xor(na, 16);
+  na += __shfl_xor(na, 32);
+  nb += __shfl_xor(nb, 16);
+  nb += __shfl_xor(nb, 32);
+  if (t.ta == 0) {
+    pair_epilogue(a, perm, t, 0, caa, na, na, arow, pm);
+    pair_epilogue(a, perm, t, 1, cab, na, nb, arow, pm);
+  } else {
+    pair_epilogue(a, perm, t, 0, cab, na, nb, arow, pm);
+    pair_epilogue(a, perm, t, 1, caa, na, na, arow, pm);
   }
 }
 
@@ -730,7 +801,10 @@ __global__ __launch_bounds__(kThreads, 4) void lite_pair_kernel(LiteDev a) {
     Unit t;
     if (!unit_of(a, u, t) || t.ntile > kSplitTiles) continue;
     double arow[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int tb = 0; tb < t.ntile; ++tb) pair_tile<BF16>(a, perm, t, tb, arow, pm);
+    if (BF16 && t.ntile == 2)
+      pair_tile_both(a, perm, t, arow, pm);
+    else
+      for (int tb = 0; tb < t.ntile; ++tb) pair_tile<BF16>(a, perm, t, tb, arow, pm);
     row_sums(arow);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
