@@ -2,14 +2,19 @@
 //
 //   front (one cooperative launch; phases separated by fence-free grid
 //          barriers, data between phases exchanged with device-scope atomics)
-//     bbox     per-axis minimum of the positions (the Morton origin)
+//     bbox     per-axis minimum (the Morton origin) and maximum (which bounds
+//              the key bits in use) of the positions
 //     keys     q = floor((x - min) * 256 / h) in float64, clamped to 21 bits;
 //              key = 3-way bit interleave; voxel = q >> 8
-//     sort     stable LSD radix sort of (key, token) in 8-bit digits over the
-//              key bits in use; equal keys stay in token order.  A pass's
-//              digit counts per block range are added up while the pass
-//              before it places its elements (by the range that receives
-//              each), so a pass needs one grid barrier
+//     sort     by (key, token): the top 12 key bits in use pick a bucket
+//              (counts and capacity sums per bucket by atomics); each block
+//              owns the whole buckets that start in its range, every element
+//              goes straight to its bucket, and each block sorts its span in
+//              LDS (bitonic, on key and token packed into 64 bits).  When a
+//              span would not fit in LDS, a stable LSD radix sort in 8-bit
+//              digits over the key bits in use runs instead (a pass's digit
+//              counts per block range are added up while the pass before it
+//              places its elements, so a pass needs one grid barrier)
 //     groups   V = floor(v * 2^40) in exact integers; an exclusive scan gives
 //              the mass before each position, t(p) = min(K-1, K * mass / W);
 //              a prefix-min scan of t(p) - p and the K - N + p floor give the
@@ -48,6 +53,14 @@ constexpr int kBins = 256;
 constexpr int kAxisBits = 21;
 constexpr int kSubBits = 8;
 constexpr int kTileRows = 16;
+// Bucket pass of the sort: the top kBucketBits key bits in use pick one of
+// kBuckets buckets; every block then sorts its span of whole buckets in LDS
+// when no span holds more than kSortCap elements.
+constexpr int kBucketBits = 12;
+constexpr int kBuckets = 1 << kBucketBits;
+constexpr int kPerThread = kBuckets / kThreads;
+constexpr int kSortCap = 4096;
+static_assert(kSortCap >= kBuckets && kBuckets % kThreads == 0, "bucket tables share LDS with the sort");
 
 struct LiteDev {
   const void* feats;
@@ -69,6 +82,8 @@ struct LiteDev {
   unsigned long long* vox_tok;  // [n] packed voxel of each token
   unsigned long long* vox_pos;  // [n] packed voxel of each sorted position
   unsigned int* hist;           // [kMaxPasses][G][256]: digit counts of each pass's ranges
+  unsigned int* bcnt;           // [kBuckets] elements per bucket
+  unsigned long long* bval;     // [kBuckets] capacity units per bucket
   unsigned long long* bsum;     // [G]
   int* bmin;                    // [G]
   int* gid;                     // [n] group of each sorted position
@@ -94,10 +109,11 @@ constexpr int kCtrlBarrier = 11;   // grid barrier counter
 constexpr int kCtrlTiles = 12;     // total number of 16-row tiles
 constexpr int kCtrlBig = 13;       // tiles of groups of more than kSplitTiles tiles
 constexpr int kCtrlAbort = 14;     // raised when a grid barrier of the front gives up
+constexpr int kCtrlBboxMax = 15;   // 3 x order key of the per-axis maximum (words 15-17)
 
 struct Layout {
-  size_t key0, key1, tok0, tok1, vox_tok, vox_pos, hist, bsum, bsum2, bmin, gid, gstart, rt_start, unit_group,
-      big_unit, A, B, gcost, ctrl, total;
+  size_t key0, key1, tok0, tok1, vox_tok, vox_pos, hist, bcnt, bval, bsum, bsum2, bmin, gid, gstart, rt_start,
+      unit_group, big_unit, A, B, gcost, ctrl, total;
 };
 
 // Groups of more than this many 16-row tiles are split over a block's waves.
@@ -115,6 +131,8 @@ Layout layout(int64_t n, int64_t k) {
   L.vox_tok = o;  o += a256(size_t(n) * 8);
   L.vox_pos = o;  o += a256(size_t(n) * 8);
   L.hist = o;     o += a256(size_t(kMaxPasses) * kFrontBlocks * kBins * 4);
+  L.bcnt = o;     o += a256(size_t(kBuckets) * 4);
+  L.bval = o;     o += a256(size_t(kBuckets) * 8);
   L.bsum = o;     o += a256(size_t(kFrontBlocks) * 8);
   L.bsum2 = o;    o += a256(size_t(kFrontBlocks) * 8);
   L.bmin = o;     o += a256(size_t(kFrontBlocks) * 4);
@@ -155,23 +173,24 @@ __device__ __forceinline__ double sq_dist(double ax, double ay, double az, doubl
   return (dx * dx + dy * dy) + dz * dz;
 }
 
-// floor(K * before / W), capped at K - 1, in exact 128-bit integer arithmetic:
-// a float64 estimate corrected against the exact products.
+// floor(K * before / W), capped at K - 1, in exact 128-bit integer arithmetic.
+// The float64 estimate before * kw (kw = K / W) carries a relative error of a
+// few units in the last place on a value below K < 2^31, so it is off by less
+// than 1e-5 and its floor by at most one: one exact correction each way
+// gives the result.
 __device__ __forceinline__ bool ge128(unsigned long long ah, unsigned long long al,
                                       unsigned long long bh, unsigned long long bl) {
   return ah > bh || (ah == bh && al >= bl);
 }
-__device__ long long thresholds_crossed(unsigned long long K, unsigned long long before,
-                                        unsigned long long W) {
+__device__ __forceinline__ long long thresholds_crossed(unsigned long long K, unsigned long long before,
+                                                       unsigned long long W, double kw) {
   const unsigned long long ph = __umul64hi(K, before), pl = K * before;
-  double est = floor(double(K) * double(before) / double(W));
+  double est = floor(double(before) * kw);
   est = fmin(fmax(est, 0.0), double(K - 1));
-  long long tq = (long long)est;
-  while (tq > 0 && !ge128(ph, pl, __umul64hi((unsigned long long)tq, W), (unsigned long long)tq * W)) --tq;
-  while (tq < (long long)K - 1 &&
-         ge128(ph, pl, __umul64hi((unsigned long long)(tq + 1), W), (unsigned long long)(tq + 1) * W))
-    ++tq;
-  return tq;
+  unsigned long long tq = (unsigned long long)(unsigned int)est;
+  if (tq > 0 && !ge128(ph, pl, __umul64hi(tq, W), tq * W)) --tq;
+  if (tq + 1 < K && ge128(ph, pl, __umul64hi(tq + 1, W), (tq + 1) * W)) ++tq;
+  return (long long)tq;
 }
 
 __device__ __forceinline__ unsigned long long capacity_units(float v) {
@@ -238,6 +257,7 @@ __device__ void block_prefix_u64(const unsigned long long* vals, int G, int blk,
 __global__ void lite_init_kernel(LiteDev a) {
   if (threadIdx.x == 0) {
     a.ctrl[kCtrlBbox + 0] = a.ctrl[kCtrlBbox + 1] = a.ctrl[kCtrlBbox + 2] = 0xffffffffu;
+    a.ctrl[kCtrlBboxMax + 0] = a.ctrl[kCtrlBboxMax + 1] = a.ctrl[kCtrlBboxMax + 2] = 0u;
     *reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey) = 0ull;
     *reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2) = 0ull;
     a.ctrl[kCtrlMt] = 0u;
@@ -248,6 +268,252 @@ __global__ void lite_init_kernel(LiteDev a) {
     a.ctrl[kCtrlBig] = 0u;
     a.ctrl[kCtrlAbort] = a.abort_init;
   }
+}
+
+// Grid coordinate of one position component (Morton cell of 1 / 256 voxel).
+__device__ __forceinline__ unsigned int grid_coord(float x, double org, double scale) {
+  double g = floor((double(x) - org) * scale);
+  g = fmin(fmax(g, 0.0), double((1 << kAxisBits) - 1));
+  return (unsigned int)g;
+}
+
+__device__ __forceinline__ unsigned long long morton3(unsigned int x, unsigned int y, unsigned int z) {
+  return spread3(x) | (spread3(y) << 1) | (spread3(z) << 2);
+}
+
+// Bucket of a key.  The bit-length bound makes the clamp a no-op for finite
+// positions; a key above the bound (non-finite input) still lands in a
+// bucket of the tables, so no slot leaves the key array.
+__device__ __forceinline__ int bucket_of(unsigned long long key, int bshift) {
+  return int(min(key >> bshift, (unsigned long long)(kBuckets - 1)));
+}
+
+// Sum over the block's threads, valid in every thread.
+__device__ unsigned long long block_sum_u64(unsigned long long x, unsigned long long* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = x;
+  __syncthreads();
+  unsigned long long r = 0ull;
+  for (int q = 0; q < kWaves; ++q) r += sh[q];
+  __syncthreads();
+  return r;
+}
+
+// Compare-exchange of x[r] and x[r ^ J] inside one thread, for the
+// bitonic stage of block size k (element index t R + r).
+template <int R, int J>
+__device__ __forceinline__ void cx_in_thread(unsigned long long (&x)[R], int t, int k) {
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+    if ((r ^ J) > r) {
+      const unsigned long long lo = x[r], hi = x[r ^ J];
+      const bool up = ((t * R + r) & k) == 0;
+      const bool sw = (lo > hi) == up;
+      x[r] = sw ? hi : lo;
+      x[r ^ J] = sw ? lo : hi;
+    }
+}
+
+// The value of lane (lane ^ M) of the wave, M in {1, 2, 4, 8, 16, 32}; every
+// lane must be active.  Quad permutations give 1 and 2; a lane mirror within
+// 8 (or 16) after a quad reversal (or an 8-mirror) gives 4 (or 8); a swizzle
+// within 32 lanes gives 16, a permute 32.
+template <int M>
+__device__ __forceinline__ unsigned long long lane_xor_u64(unsigned long long x) {
+  if constexpr (M == 1) return dpp_u64<0xB1>(x);                   // quad [1, 0, 3, 2]
+  else if constexpr (M == 2) return dpp_u64<0x4E>(x);              // quad [2, 3, 0, 1]
+  else if constexpr (M == 4) return dpp_u64<0x141>(dpp_u64<0x1B>(x));   // half-row mirror of quad [3, 2, 1, 0]
+  else if constexpr (M == 8) return dpp_u64<0x140>(dpp_u64<0x141>(x));  // row mirror of half-row mirror
+  else if constexpr (M == 16) {
+    constexpr int kXor16 = 0x1f | (0x10 << 10);   // bit-mask swizzle: and 31, xor 16
+    const unsigned lo = unsigned(__builtin_amdgcn_ds_swizzle(int(unsigned(x)), kXor16));
+    const unsigned hi = unsigned(__builtin_amdgcn_ds_swizzle(int(unsigned(x >> 32)), kXor16));
+    return ((unsigned long long)hi << 32) | lo;
+  } else {
+    static_assert(M == 32, "lane distance");
+    return __shfl_xor(x, 32);
+  }
+}
+
+// One bitonic stage whose partner of element t R + r is (t ^ M) R + r, a lane
+// M away in the same wave.
+template <int R, int M>
+__device__ __forceinline__ void cx_lanes(unsigned long long (&x)[R], bool keep_min) {
+  unsigned long long y[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) y[r] = lane_xor_u64<M>(x[r]);
+#pragma unroll
+  for (int r = 0; r < R; ++r) x[r] = keep_min ? min(x[r], y[r]) : max(x[r], y[r]);
+}
+
+// Ascending bitonic sort of the block's kThreads * R values, thread t
+// holding elements t R .. t R + R - 1 in x.  Stages whose partner is in the
+// same thread run in registers, those whose partner is in the same wave by
+// lane exchanges; for the rest (partner in another wave) every thread stores
+// its R values to LDS and reads its partner's, alternating between two
+// buffers (lds0, lds1: kThreads * R values each) so that one barrier per
+// stage suffices.  Value r of thread t sits at r kThreads + t, so that a
+// wave's 8-byte accesses fall on consecutive banks.  On return thread t holds
+// the sorted elements t R .. t R + R - 1.
+template <int R>
+__device__ void bitonic_regs(unsigned long long (&x)[R], unsigned long long* lds0, unsigned long long* lds1) {
+  const int t = threadIdx.x;
+  constexpr int P = kThreads * R;
+  int flip = 0;
+  for (int k = 2; k <= P; k <<= 1)
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (j < R) {
+        if constexpr (R > 1) if (j == 1) cx_in_thread<R, 1>(x, t, k);
+        if constexpr (R > 2) if (j == 2) cx_in_thread<R, 2>(x, t, k);
+        if constexpr (R > 4) if (j == 4) cx_in_thread<R, 4>(x, t, k);
+        if constexpr (R > 8) if (j == 8) cx_in_thread<R, 8>(x, t, k);
+        continue;
+      }
+      const int tj = j / R;                          // partner thread t ^ tj
+      const bool keep_min = ((t & tj) == 0) == (((t * R) & k) == 0);
+      switch (tj) {
+        case 1: cx_lanes<R, 1>(x, keep_min); continue;
+        case 2: cx_lanes<R, 2>(x, keep_min); continue;
+        case 4: cx_lanes<R, 4>(x, keep_min); continue;
+        case 8: cx_lanes<R, 8>(x, keep_min); continue;
+        case 16: cx_lanes<R, 16>(x, keep_min); continue;
+        case 32: cx_lanes<R, 32>(x, keep_min); continue;
+        default: break;
+      }
+      unsigned long long* buf = flip ? lds1 : lds0;
+      flip ^= 1;
+#pragma unroll
+      for (int r = 0; r < R; ++r) buf[r * kThreads + t] = x[r];
+      __syncthreads();
+      unsigned long long y[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) y[r] = buf[r * kThreads + (t ^ tj)];
+#pragma unroll
+      for (int r = 0; r < R; ++r) x[r] = keep_min ? min(x[r], y[r]) : max(x[r], y[r]);
+    }
+}
+
+// The same network with every stage's sizes known at compile time (no loop
+// or branch between stages), for R <= 8; the loop above serves R = 16.
+template <int R, int K, int J>
+__device__ __forceinline__ void bitonic_stage(unsigned long long (&x)[R], unsigned long long* lds0,
+                                              unsigned long long* lds1, int& flip) {
+  const int t = threadIdx.x;
+  if constexpr (J < R) {
+    cx_in_thread<R, J>(x, t, K);
+  } else {
+    constexpr int TJ = J / R;
+    const bool keep_min = ((t & TJ) == 0) == (((t * R) & K) == 0);
+    if constexpr (TJ < 64) {
+      cx_lanes<R, TJ>(x, keep_min);
+    } else {
+      unsigned long long* buf = flip ? lds1 : lds0;
+      flip ^= 1;
+#pragma unroll
+      for (int r = 0; r < R; ++r) buf[r * kThreads + t] = x[r];
+      __syncthreads();
+      unsigned long long y[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) y[r] = buf[r * kThreads + (t ^ TJ)];
+#pragma unroll
+      for (int r = 0; r < R; ++r) x[r] = keep_min ? min(x[r], y[r]) : max(x[r], y[r]);
+    }
+  }
+  if constexpr (J > 1) bitonic_stage<R, K, J / 2>(x, lds0, lds1, flip);
+}
+
+template <int R, int K>
+__device__ __forceinline__ void bitonic_merges(unsigned long long (&x)[R], unsigned long long* lds0,
+                                               unsigned long long* lds1, int& flip) {
+  bitonic_stage<R, K, K / 2>(x, lds0, lds1, flip);
+  if constexpr (K < kThreads * R) bitonic_merges<R, 2 * K>(x, lds0, lds1, flip);
+}
+
+template <int R>
+__device__ void bitonic_unrolled(unsigned long long (&x)[R], unsigned long long* lds0, unsigned long long* lds1) {
+  int flip = 0;
+  bitonic_merges<R, 2>(x, lds0, lds1, flip);
+}
+
+// After the span sort (s_sorted: the span's packed (key, token) values in
+// order, m >= 1 of them): thread t's positions i in [i0, i1) of the span, at
+// most R of them.  Writes the permutation and the voxels by position, scans
+// the capacity units over the span (run: units before it, W: all units) and
+// leaves (tp - p, token) of each position in s_out (Eq. 17 in scan form).
+// Work on absent positions reads position m - 1 and is dropped, so that the
+// R positions' loads and arithmetic overlap.  Returns the thread's minimum
+// tp - p (INT_MAX without positions).
+template <int R>
+__device__ int span_offsets(const LiteDev& a, int r0, int m, int i0, int i1, unsigned long long tmask,
+                            const double (&org)[3], unsigned long long run, unsigned long long W,
+                            const unsigned long long* s_sorted, unsigned long long* s_out,
+                            unsigned long long* s_u64) {
+  int tk[R];
+  unsigned long long vx[R], V[R];
+#pragma unroll
+  for (int u = 0; u < R; ++u) {
+    tk[u] = int(s_sorted[min(i0 + u, m - 1)] & tmask);
+    vx[u] = pack_vox(grid_coord(a.pos[3 * tk[u]], org[0], a.grid_scale) >> kSubBits,
+                     grid_coord(a.pos[3 * tk[u] + 1], org[1], a.grid_scale) >> kSubBits,
+                     grid_coord(a.pos[3 * tk[u] + 2], org[2], a.grid_scale) >> kSubBits);
+    V[u] = capacity_units(a.v[tk[u]]);
+  }
+  unsigned long long loc = 0ull;
+#pragma unroll
+  for (int u = 0; u < R; ++u)
+    if (i0 + u < i1) {
+      loc += V[u];
+      put(a.tok[1] + r0 + i0 + u, tk[u]);
+      put(a.vox_pos + r0 + i0 + u, vx[u]);
+    }
+  unsigned long long span_tot;
+  unsigned long long before = run + block_excl_sum_u64(loc, s_u64, span_tot);
+  const double kw = W ? double(a.k) / double(W) : 0.0;
+  long long tp[R];
+#pragma unroll
+  for (int u = 0; u < R; ++u) {
+    const int pos = r0 + i0 + u;
+    tp[u] = pos == 0 ? 0 : (W == 0ull ? a.k - 1 : thresholds_crossed((unsigned long long)a.k, before, W, kw));
+    before += V[u];
+  }
+  int bmin = INT_MAX;
+#pragma unroll
+  for (int u = 0; u < R; ++u)
+    if (i0 + u < i1) {
+      const int mm = int(tp[u] - (r0 + i0 + u));
+      s_out[i0 + u] = ((unsigned long long)(unsigned int)mm << 32) | (unsigned int)tk[u];
+      bmin = min(bmin, mm);
+    }
+  return bmin;
+}
+
+// Loads src[0, m) (m <= kThreads * R; the rest padded with the largest
+// value), sorts it and leaves the sorted values in dst[0, kThreads * R)
+// (tmp: LDS of the same size, clobbered).
+template <int R>
+__device__ void span_sort(const unsigned long long* src, int m, unsigned long long* dst, unsigned long long* tmp) {
+  const int t = threadIdx.x;
+  unsigned long long x[R];
+  // Every load is issued before any is used (a device-scope load under a
+  // condition waits for itself): indices past m read element m - 1 and are
+  // then replaced by the padding.
+  if (m > 0) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) x[r] = get(src + min(t * R + r, m - 1));
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (t * R + r >= m) x[r] = ~0ull;
+  } else {
+#pragma unroll
+    for (int r = 0; r < R; ++r) x[r] = ~0ull;
+  }
+  if constexpr (R <= 8) bitonic_unrolled<R>(x, dst, tmp);
+  else bitonic_regs<R>(x, dst, tmp);
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < R; ++r) dst[t * R + r] = x[r];
+  __syncthreads();
 }
 
 __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
@@ -263,57 +529,95 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
   // the kernels after the front see the abort word and do nothing.
   __shared__ int s_ok;
 
-  __shared__ unsigned int s_u32[3][kWaves];
+  __shared__ unsigned int s_u32[6][kWaves];
   __shared__ unsigned long long s_u64[kThreads + 2];
   __shared__ int s_i32[kThreads];
   __shared__ unsigned int s_hist[kBins];
   __shared__ unsigned int s_base[kBins];
   __shared__ unsigned int s_wcnt[kWaves][kBins];
   __shared__ int s_minoff;
+  // bucket pass: per-bucket counts (then this block's base in each bucket),
+  // one wide array used in turn for per-bucket capacity sums, bucket starts
+  // and the span being sorted, and the block's keys with their ranks
+  __shared__ unsigned int s_cnt[kBuckets];
+  __shared__ unsigned long long s_wide[kSortCap];
+  __shared__ unsigned long long s_key[kSortCap];
+  __shared__ uint16_t s_rank[kSortCap];
+  __shared__ int s_span[kFrontBlocks + 1], s_first[kFrontBlocks + 1];
+  __shared__ int s_fast;
 
-  // ---- this block's rows of every pass's digit counts start at zero (the
-  // first additions come after the next barrier); bbox minimum per axis
+  // ---- this block's rows of every pass's digit counts and its slice of the
+  // bucket tables start at zero (the first additions come after the next
+  // barrier); bbox minimum and maximum per axis
   for (int q = t; q < kMaxPasses * kBins; q += kThreads) put(a.hist + (size_t(q / kBins) * G + blk) * kBins + q % kBins, 0u);
+  for (int q = blk * kThreads + t; q < kBuckets; q += G * kThreads) {
+    put(a.bcnt + q, 0u);
+    put(a.bval + q, 0ull);
+  }
   {
-    unsigned int m[3] = {0xffffffffu, 0xffffffffu, 0xffffffffu};
+    unsigned int m[6] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0u, 0u, 0u};
     for (int i = p0 + t; i < p1; i += kThreads)
-      for (int ax = 0; ax < 3; ++ax) m[ax] = min(m[ax], float_order_key(a.pos[3 * i + ax]));
-    for (int ax = 0; ax < 3; ++ax) {
-      unsigned int x = m[ax];
-      for (int o = 32; o > 0; o >>= 1) x = min(x, (unsigned int)__shfl_xor((int)x, o));
-      if (lane == 0) s_u32[ax][w] = x;
+      for (int ax = 0; ax < 3; ++ax) {
+        const unsigned int o = float_order_key(a.pos[3 * i + ax]);
+        m[ax] = min(m[ax], o);
+        m[3 + ax] = max(m[3 + ax], o);
+      }
+    for (int e = 0; e < 6; ++e) {
+      unsigned int x = m[e];
+      for (int o = 32; o > 0; o >>= 1) {
+        const unsigned int y = (unsigned int)__shfl_xor((int)x, o);
+        x = e < 3 ? min(x, y) : max(x, y);
+      }
+      if (lane == 0) s_u32[e][w] = x;
     }
     __syncthreads();
-    if (t < 3) {
+    if (t < 6) {
       unsigned int x = s_u32[t][0];
-      for (int q = 1; q < kWaves; ++q) x = min(x, s_u32[t][q]);
-      atomicMin(a.ctrl + kCtrlBbox + t, x);
+      for (int q = 1; q < kWaves; ++q) x = t < 3 ? min(x, s_u32[t][q]) : max(x, s_u32[t][q]);
+      if (t < 3) atomicMin(a.ctrl + kCtrlBbox + t, x);
+      else atomicMax(a.ctrl + kCtrlBboxMax + t - 3, x);
     }
   }
   if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
 
-  // ---- Morton keys
+  // ---- Morton keys.  The grid coordinates of the bbox maximum bound every
+  // coordinate, so their Morton code bounds the bit length of every key.
+  double org[3];
+  for (int ax = 0; ax < 3; ++ax) org[ax] = double(float_from_order_key(get(a.ctrl + kCtrlBbox + ax)));
+  unsigned int qmax[3];
+  for (int ax = 0; ax < 3; ++ax)
+    qmax[ax] = grid_coord(float_from_order_key(get(a.ctrl + kCtrlBboxMax + ax)), org[ax], a.grid_scale);
+  const unsigned long long kbound = morton3(qmax[0], qmax[1], qmax[2]);
+  const int kbits = kbound ? 64 - __clzll((long long)kbound) : 0;
+  const int tokbits = n > 1 ? 32 - __clz(n - 1) : 0;
+  const int bshift = kbits - min(kBucketBits, kbits);
+  // The bucket pass packs (key, token) into one 64-bit sort value.
+  const bool bucket_ok = kbits + tokbits <= 64 && tile <= kSortCap;
   {
-    const double org[3] = {double(float_from_order_key(get(a.ctrl + kCtrlBbox + 0))),
-                           double(float_from_order_key(get(a.ctrl + kCtrlBbox + 1))),
-                           double(float_from_order_key(get(a.ctrl + kCtrlBbox + 2)))};
-    const double top = double((1 << kAxisBits) - 1);
     unsigned long long kmax = 0ull;
     s_hist[t] = 0u;
+    if (bucket_ok)
+      for (int q = t; q < kBuckets; q += kThreads) {
+        s_cnt[q] = 0u;
+        s_wide[q] = 0ull;
+      }
     __syncthreads();
     for (int i = p0 + t; i < p1; i += kThreads) {
-      unsigned int q[3];
-      for (int ax = 0; ax < 3; ++ax) {
-        double g = floor((double(a.pos[3 * i + ax]) - org[ax]) * a.grid_scale);
-        g = fmin(fmax(g, 0.0), top);
-        q[ax] = (unsigned int)g;
-      }
-      const unsigned long long key = spread3(q[0]) | (spread3(q[1]) << 1) | (spread3(q[2]) << 2);
+      const unsigned int q0 = grid_coord(a.pos[3 * i], org[0], a.grid_scale);
+      const unsigned int q1 = grid_coord(a.pos[3 * i + 1], org[1], a.grid_scale);
+      const unsigned int q2 = grid_coord(a.pos[3 * i + 2], org[2], a.grid_scale);
+      const unsigned long long key = morton3(q0, q1, q2);
       put(a.key[0] + i, key);
       put(a.tok[0] + i, i);
-      put(a.vox_tok + i, pack_vox(q[0] >> kSubBits, q[1] >> kSubBits, q[2] >> kSubBits));
+      put(a.vox_tok + i, pack_vox(q0 >> kSubBits, q1 >> kSubBits, q2 >> kSubBits));
       atomicAdd(&s_hist[unsigned(key & 0xffu)], 1u);
       kmax = max(kmax, key);
+      if (bucket_ok) {
+        const int bk = bucket_of(key, bshift);
+        s_key[i - p0] = key;
+        s_rank[i - p0] = uint16_t(atomicAdd(&s_cnt[bk], 1u));
+        atomicAdd(&s_wide[bk], capacity_units(a.v[i]));
+      }
     }
     for (int o = 32; o > 0; o >>= 1) {
       const unsigned long long y = __shfl_xor(kmax, o);
@@ -322,126 +626,254 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     if (lane == 0) atomicMax(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey), kmax);
     __syncthreads();
     put(a.hist + size_t(blk) * kBins + t, s_hist[t]);   // pass 0: the block's own range, in token order
+    // Bucket counts and capacity sums; each block takes its base inside a
+    // bucket from the returned count (blocks land in any order within a
+    // bucket, which the span sort below puts right).
+    if (bucket_ok)
+      for (int q = t; q < kBuckets; q += kThreads) {
+        const unsigned int c = s_cnt[q];
+        if (c) {
+          s_cnt[q] = __hip_atomic_fetch_add(a.bcnt + q, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_fetch_add(a.bval + q, s_wide[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
   }
   if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
 
-  // ---- stable LSD radix sort of (key, token), 8 bits per pass
-  const unsigned long long maxkey = get(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey));
-  const int bits = maxkey ? 64 - __clzll((long long)maxkey) : 0;
-  const int passes = (bits + 7) / 8;
-  for (int pass = 0; pass < passes; ++pass) {
-    const int src = pass & 1, sh = 8 * pass;
-    const unsigned long long* ks = src ? a.key[1] : a.key[0];
-    const int* ts = src ? a.tok[1] : a.tok[0];
-    unsigned long long* kd = src ? a.key[0] : a.key[1];
-    int* td = src ? a.tok[0] : a.tok[1];
-    const unsigned int* hist = a.hist + size_t(pass) * G * kBins;
-    // Base offset of digit t for this block: every smaller digit anywhere,
-    // plus digit t in earlier blocks (all G counts read in one round trip).
-    {
-      unsigned int tot = 0u, pre = 0u;
-      unsigned int h[kFrontBlocks];
+  // ---- bucket starts and every block's span of whole buckets: the buckets
+  // that start in [b * tile, (b + 1) * tile).  When every span fits in LDS,
+  // each element goes straight to its bucket slot and each block sorts its
+  // span; otherwise the LSD radix sort below runs.
+  bool fast = false;
+  int r0 = p0, r1 = p1;            // the positions this block owns from here on
+  unsigned long long run = 0ull;   // capacity units before position r0
+  unsigned long long W = 0ull;     // all capacity units
+  if (bucket_ok) {
+    unsigned int c[kPerThread];
+    unsigned long long vb[kPerThread];
 #pragma unroll
-      for (int x = 0; x < kFrontBlocks; ++x) h[x] = x < G ? get(hist + x * kBins + t) : 0u;
+    for (int j = 0; j < kPerThread; ++j) {
+      c[j] = get(a.bcnt + t * kPerThread + j);
+      vb[j] = get(a.bval + t * kPerThread + j);
+    }
+    unsigned long long csum = 0ull;
 #pragma unroll
-      for (int x = 0; x < kFrontBlocks; ++x) {
-        tot += h[x];
-        if (x < blk) pre += h[x];
-      }
-      unsigned long long total;
-      const unsigned long long ex = block_excl_sum_u64(tot, s_u64, total);
-      s_base[t] = unsigned(ex) + pre;
+    for (int j = 0; j < kPerThread; ++j) csum += c[j];
+    unsigned long long ctot;
+    unsigned int st = unsigned(block_excl_sum_u64(csum, s_u64, ctot));
+    unsigned int* s_start = reinterpret_cast<unsigned int*>(s_wide);
+#pragma unroll
+    for (int j = 0; j < kPerThread; ++j) {
+      s_start[t * kPerThread + j] = st;
+      st += c[j];
     }
     __syncthreads();
-
-    // Stable scatter, 256 items per round: rank among equal digits inside a
-    // wave from ballots, then across the block's waves through LDS.  The
-    // next round's element is loaded while this one is placed.
-    unsigned long long kn = p0 + t < p1 ? get(ks + p0 + t) : 0ull;
-    int tn = p0 + t < p1 ? get(ts + p0 + t) : 0;
-    for (int c0 = p0; c0 < p1; c0 += kThreads) {
-      const int i = c0 + t;
-      const bool live = i < p1;
-      const unsigned long long kv = kn;
-      const int tv = tn;
-      if (i + kThreads < p1) {
-        kn = get(ks + i + kThreads);
-        tn = get(ts + i + kThreads);
+    if (t <= G) {
+      const unsigned int target = unsigned(min(n, t * tile));
+      int lo = 0, hi = kBuckets;   // first bucket starting at or after target
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (s_start[mid] < target) lo = mid + 1;
+        else hi = mid;
       }
-      const unsigned int dig = unsigned((kv >> sh) & 0xffu);
-      unsigned long long same = __ballot(live);
-      for (int bit = 0; bit < 8; ++bit) {
-        const unsigned long long m = __ballot(live && ((dig >> bit) & 1u));
-        same &= ((dig >> bit) & 1u) ? m : ~m;
-      }
-      const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-      const int rank = __popcll(same & below);
-      for (int q = t; q < kWaves * kBins; q += kThreads) (&s_wcnt[0][0])[q] = 0u;
-      __syncthreads();
-      if (live && rank == 0) s_wcnt[w][dig] = unsigned(__popcll(same));
-      __syncthreads();
-      if (live) {
-        unsigned int off = s_base[dig];
-        for (int q = 0; q < w; ++q) off += s_wcnt[q][dig];
-        put(kd + off + rank, kv);
-        put(td + off + rank, tv);
-        // The next pass's digit of this element, counted for the range
-        // that receives it.
-        if (pass + 1 < passes)
-          __hip_atomic_fetch_add(a.hist + (size_t(pass + 1) * G + (off + rank) / tile) * kBins +
-                                     unsigned((kv >> (sh + 8)) & 0xffu),
-                                 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-      __syncthreads();
-      unsigned int add = 0u;
-      for (int q = 0; q < kWaves; ++q) add += s_wcnt[q][t];
-      s_base[t] += add;
-      __syncthreads();
+      s_span[t] = lo < kBuckets ? int(s_start[lo]) : n;
+      s_first[t] = lo;
     }
-    if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-  }
-  const int sorted = passes & 1;
-  const int* perm = sorted ? a.tok[1] : a.tok[0];
-
-  // ---- groups: exclusive scan of V over sorted positions
-  {
-    unsigned long long local = 0ull;
-    for (int i = p0 + t; i < p1; i += kThreads) local += capacity_units(a.v[get(perm + i)]);
-    unsigned long long tot;
-    block_excl_sum_u64(local, s_u64, tot);
-    if (t == 0) put(a.bsum + blk, tot);
-  }
-  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-  {
-    unsigned long long run, W;
-    block_prefix_u64(a.bsum, G, blk, s_u64, run, W);
-    const unsigned long long KK = (unsigned long long)K;
-    int bmin = INT_MAX;
-    for (int c0 = p0; c0 < p1; c0 += kThreads) {
-      const int i = c0 + t;
-      const unsigned long long V = i < p1 ? capacity_units(a.v[get(perm + i)]) : 0ull;
-      unsigned long long chunk;
-      const unsigned long long ex = block_excl_sum_u64(V, s_u64, chunk);
-      if (i < p1) {
-        long long tp;
-        if (i == 0) tp = 0;
-        else if (W == 0ull) tp = K - 1;
-        else tp = thresholds_crossed(KK, run + ex, W);
-        const int m = int(tp - i);
-        put(a.gid + i, m);
-        bmin = min(bmin, m);
+    __syncthreads();
+    if (t == 0) {
+      int big = 0;
+      for (int b = 0; b < G; ++b) big = max(big, s_span[b + 1] - s_span[b]);
+      s_fast = big <= kSortCap;
+    }
+    __syncthreads();
+    fast = s_fast != 0;
+    if (fast) {
+      for (int i = p0 + t; i < p1; i += kThreads) {
+        const unsigned long long key = s_key[i - p0];
+        const int bk = bucket_of(key, bshift);
+        put(a.key[1] + s_start[bk] + s_cnt[bk] + s_rank[i - p0], (key << tokbits) | (unsigned long long)i);
       }
-      run += chunk;
+      const int fb = s_first[blk];
+      unsigned long long below = 0ull, all = 0ull;
+#pragma unroll
+      for (int j = 0; j < kPerThread; ++j) {
+        if (t * kPerThread + j < fb) below += vb[j];
+        all += vb[j];
+      }
+      run = block_sum_u64(below, s_u64);
+      W = block_sum_u64(all, s_u64);
+      r0 = s_span[blk];
+      r1 = s_span[blk + 1];
+    }
+  }
+
+  int sorted;
+  // Positions r0 + i of a sorted span, thread t taking i in [t per, t per + per).
+  const int span_m = r1 - r0;
+  int per = 1;
+  while (kThreads * per < span_m) per <<= 1;
+  const int i0 = min(span_m, t * per), i1 = min(span_m, t * per + per);
+  if (fast) {
+    if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
+    // ---- sort the span by (key, token), write the permutation and the
+    // voxels by position, and the group offsets tp - p of its positions
+    // (Eq. 17 in scan form), kept in LDS with the tokens for the next phase
+    const unsigned long long tmask = tokbits ? (~0ull >> (64 - tokbits)) : 0ull;
+    int bmin = INT_MAX;
+    if (span_m > 0) {
+      const unsigned long long* src = a.key[1] + r0;
+      switch (per) {
+        case 1:
+          span_sort<1>(src, span_m, s_wide, s_key);
+          bmin = span_offsets<1>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          break;
+        case 2:
+          span_sort<2>(src, span_m, s_wide, s_key);
+          bmin = span_offsets<2>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          break;
+        case 4:
+          span_sort<4>(src, span_m, s_wide, s_key);
+          bmin = span_offsets<4>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          break;
+        case 8:
+          span_sort<8>(src, span_m, s_wide, s_key);
+          bmin = span_offsets<8>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          break;
+        default:
+          span_sort<16>(src, span_m, s_wide, s_key);
+          bmin = span_offsets<16>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          break;
+      }
     }
     bmin = wave_min(bmin);
     if (lane == 0) s_i32[w] = bmin;
     __syncthreads();
     if (t == 0) {
-      int m = s_i32[0];
-      for (int q = 1; q < kWaves; ++q) m = min(m, s_i32[q]);
-      put(a.bmin + blk, m);
+      int mm = s_i32[0];
+      for (int q = 1; q < kWaves; ++q) mm = min(mm, s_i32[q]);
+      put(a.bmin + blk, mm);
+    }
+    sorted = 1;
+  } else {
+    // ---- stable LSD radix sort of (key, token), 8 bits per pass
+    const unsigned long long maxkey = get(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey));
+    const int bits = maxkey ? 64 - __clzll((long long)maxkey) : 0;
+    const int passes = (bits + 7) / 8;
+    for (int pass = 0; pass < passes; ++pass) {
+      const int src = pass & 1, sh = 8 * pass;
+      const unsigned long long* ks = src ? a.key[1] : a.key[0];
+      const int* ts = src ? a.tok[1] : a.tok[0];
+      unsigned long long* kd = src ? a.key[0] : a.key[1];
+      int* td = src ? a.tok[0] : a.tok[1];
+      const unsigned int* hist = a.hist + size_t(pass) * G * kBins;
+      // Base offset of digit t for this block: every smaller digit anywhere,
+      // plus digit t in earlier blocks (all G counts read in one round trip).
+      {
+        unsigned int tot = 0u, pre = 0u;
+        unsigned int h[kFrontBlocks];
+#pragma unroll
+        for (int x = 0; x < kFrontBlocks; ++x) h[x] = x < G ? get(hist + x * kBins + t) : 0u;
+#pragma unroll
+        for (int x = 0; x < kFrontBlocks; ++x) {
+          tot += h[x];
+          if (x < blk) pre += h[x];
+        }
+        unsigned long long total;
+        const unsigned long long ex = block_excl_sum_u64(tot, s_u64, total);
+        s_base[t] = unsigned(ex) + pre;
+      }
+      __syncthreads();
+
+      // Stable scatter, 256 items per round: rank among equal digits inside a
+      // wave from ballots, then across the block's waves through LDS.  The
+      // next round's element is loaded while this one is placed.
+      unsigned long long kn = p0 + t < p1 ? get(ks + p0 + t) : 0ull;
+      int tn = p0 + t < p1 ? get(ts + p0 + t) : 0;
+      for (int c0 = p0; c0 < p1; c0 += kThreads) {
+        const int i = c0 + t;
+        const bool live = i < p1;
+        const unsigned long long kv = kn;
+        const int tv = tn;
+        if (i + kThreads < p1) {
+          kn = get(ks + i + kThreads);
+          tn = get(ts + i + kThreads);
+        }
+        const unsigned int dig = unsigned((kv >> sh) & 0xffu);
+        unsigned long long same = __ballot(live);
+        for (int bit = 0; bit < 8; ++bit) {
+          const unsigned long long mb = __ballot(live && ((dig >> bit) & 1u));
+          same &= ((dig >> bit) & 1u) ? mb : ~mb;
+        }
+        const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+        const int rank = __popcll(same & below);
+        for (int q = t; q < kWaves * kBins; q += kThreads) (&s_wcnt[0][0])[q] = 0u;
+        __syncthreads();
+        if (live && rank == 0) s_wcnt[w][dig] = unsigned(__popcll(same));
+        __syncthreads();
+        if (live) {
+          unsigned int off = s_base[dig];
+          for (int q = 0; q < w; ++q) off += s_wcnt[q][dig];
+          put(kd + off + rank, kv);
+          put(td + off + rank, tv);
+          // The next pass's digit of this element, counted for the range
+          // that receives it.
+          if (pass + 1 < passes)
+            __hip_atomic_fetch_add(a.hist + (size_t(pass + 1) * G + (off + rank) / tile) * kBins +
+                                       unsigned((kv >> (sh + 8)) & 0xffu),
+                                   1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        __syncthreads();
+        unsigned int add = 0u;
+        for (int q = 0; q < kWaves; ++q) add += s_wcnt[q][t];
+        s_base[t] += add;
+        __syncthreads();
+      }
+      if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
+    }
+    sorted = passes & 1;
+    const int* perm = sorted ? a.tok[1] : a.tok[0];
+
+    // ---- groups: exclusive scan of V over sorted positions
+    {
+      unsigned long long local = 0ull;
+      for (int i = p0 + t; i < p1; i += kThreads) local += capacity_units(a.v[get(perm + i)]);
+      unsigned long long tot;
+      block_excl_sum_u64(local, s_u64, tot);
+      if (t == 0) put(a.bsum + blk, tot);
+    }
+    if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
+    {
+      block_prefix_u64(a.bsum, G, blk, s_u64, run, W);
+      const unsigned long long KK = (unsigned long long)K;
+      const double kw = W ? double(K) / double(W) : 0.0;
+      int bmin = INT_MAX;
+      for (int c0 = p0; c0 < p1; c0 += kThreads) {
+        const int i = c0 + t;
+        const unsigned long long V = i < p1 ? capacity_units(a.v[get(perm + i)]) : 0ull;
+        unsigned long long chunk;
+        const unsigned long long ex = block_excl_sum_u64(V, s_u64, chunk);
+        if (i < p1) {
+          long long tp;
+          if (i == 0) tp = 0;
+          else if (W == 0ull) tp = K - 1;
+          else tp = thresholds_crossed(KK, run + ex, W, kw);
+          const int m = int(tp - i);
+          put(a.gid + i, m);
+          bmin = min(bmin, m);
+        }
+        run += chunk;
+      }
+      bmin = wave_min(bmin);
+      if (lane == 0) s_i32[w] = bmin;
+      __syncthreads();
+      if (t == 0) {
+        int m = s_i32[0];
+        for (int q = 1; q < kWaves; ++q) m = min(m, s_i32[q]);
+        put(a.bmin + blk, m);
+      }
     }
   }
+  const int* perm = sorted ? a.tok[1] : a.tok[0];
   if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
   {
     s_i32[t] = t < blk ? get(a.bmin + t) : INT_MAX;
@@ -452,25 +884,50 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
       s_minoff = m;
     }
     __syncthreads();
-    int run = s_minoff;
+  }
+  if (fast) {
+    // ---- groups of the span's positions: prefix minimum of the offsets
+    // (earlier blocks, earlier threads, then this thread's positions in
+    // order), group starts where the group changes, the group output
+    int lmin = INT_MAX;
+    for (int i = i0; i < i1; ++i) lmin = min(lmin, int(unsigned(s_key[i] >> 32)));
+    const int incl = block_incl_min(lmin, s_i32);
+    s_i32[t] = incl;
+    __syncthreads();
+    int cur = min(s_minoff, t > 0 ? s_i32[t - 1] : INT_MAX);   // prefix minimum before position r0 + i0
+    __syncthreads();
+    int qprev = r0 + i0 > 0 ? max(K - n + r0 + i0 - 1, r0 + i0 - 1 + cur) : -1;
+    for (int i = i0; i < i1; ++i) {
+      const int pos = r0 + i;
+      const unsigned long long e = s_key[i];
+      cur = min(cur, int(unsigned(e >> 32)));
+      const int q = max(K - n + pos, pos + cur);
+      if (q != qprev) put(a.gstart + q, pos);
+      if (pos == n - 1) put(a.gstart + K, n);
+      put(a.gid + pos, q);
+      if (a.group) a.group[int(unsigned(e))] = q;
+      qprev = q;
+    }
+  } else {
+    int run_min = s_minoff;
     // Group starts, voxels by sorted position and the group output in the
     // same pass: a position starts a group when its group differs from the
-    // one before it.  Position p0 - 1 lies in the previous block, and its
-    // group follows from the same prefix minimum (s_minoff covers every
-    // position before p0).
+    // one before it.  Position r0 - 1 lies in an earlier block's range, and
+    // its group follows from the same prefix minimum (s_minoff covers every
+    // position before r0).
     __shared__ int s_gid[kThreads];
-    int gprev = blk > 0 && p0 > 0 ? max(K - n + p0 - 1, p0 - 1 + s_minoff) : -1;
-    for (int c0 = p0; c0 < p1; c0 += kThreads) {
+    int gprev = blk > 0 && r0 > 0 ? max(K - n + r0 - 1, r0 - 1 + s_minoff) : -1;
+    for (int c0 = r0; c0 < r1; c0 += kThreads) {
       const int i = c0 + t;
-      const int m = i < p1 ? get(a.gid + i) : INT_MAX;
-      const int inc = min(block_incl_min(m, s_i32), run);
-      const int q = i < p1 ? max(K - n + i, i + inc) : -1;
-      if (i < p1) put(a.gid + i, q);
+      const int m = i < r1 ? get(a.gid + i) : INT_MAX;
+      const int inc = min(block_incl_min(m, s_i32), run_min);
+      const int q = i < r1 ? max(K - n + i, i + inc) : -1;
+      if (i < r1) put(a.gid + i, q);
       s_i32[t] = inc;
       s_gid[t] = q;
       __syncthreads();
-      run = s_i32[kThreads - 1];
-      if (i < p1) {
+      run_min = s_i32[kThreads - 1];
+      if (i < r1) {
         const int qb = t > 0 ? s_gid[t - 1] : gprev;
         if (i == 0 || qb != q) put(a.gstart + q, i);
         if (i == n - 1) put(a.gstart + K, n);
@@ -483,7 +940,6 @@ __global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
     }
   }
   if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-
   // ---- tiles per group, and tiles of big groups (block sums)
   const int gtile = (K + G - 1) / G;
   const int q0 = min(K, blk * gtile), q1 = min(K, q0 + gtile);
@@ -1013,6 +1469,8 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   a.vox_tok = reinterpret_cast<unsigned long long*>(w + L.vox_tok);
   a.vox_pos = reinterpret_cast<unsigned long long*>(w + L.vox_pos);
   a.hist = reinterpret_cast<unsigned int*>(w + L.hist);
+  a.bcnt = reinterpret_cast<unsigned int*>(w + L.bcnt);
+  a.bval = reinterpret_cast<unsigned long long*>(w + L.bval);
   a.bsum = reinterpret_cast<unsigned long long*>(w + L.bsum);
   a.bmin = reinterpret_cast<int*>(w + L.bmin);
   a.gid = reinterpret_cast<int*>(w + L.gid);
