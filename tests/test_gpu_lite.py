@@ -75,6 +75,33 @@ def test_lite_skewed_capacity():
     parity.assert_lite_close(sel, group, obj, ref, tc)
 
 
+@pytest.mark.parametrize("cluster", [3000, 5000])
+def test_lite_dense_cluster(cluster):
+    # Most of 5200 tokens packed around one point: with 3000 there, one block's
+    # span of whole buckets holds about 3100 tokens (the largest span the
+    # front sorts in LDS, 16 per thread); with 5000 no span fits and the
+    # stable radix sort orders the keys instead.
+    s = _sub("n8192_d3584", 5200, 9)
+    rng = np.random.default_rng(9)
+    idx = rng.choice(s.n, size=cluster, replace=False)
+    s.pos[idx] = (s.pos.mean(0) + rng.normal(scale=1e-4, size=(cluster, 3))).astype(np.float32)
+    print(f"lite dense cluster of {cluster} in n={s.n}", flush=True)
+    ref = parity.lite_reference(s, 520, h=0.25)
+    sel, group, obj, tc = _gpu(s, 520, 0.25)
+    parity.assert_lite_close(sel, group, obj, ref, tc)
+
+
+def test_lite_keys_wider_than_the_bucket_pass():
+    # A voxel of 1e-6 m puts every coordinate at the 21-bit clamp range: keys
+    # of 63 bits do not pack with a token index into 64 bits, so the radix
+    # sort runs; clamped keys tie and stay in token order.
+    s = _sub("n4096_d1152", 1000, 10)
+    print("lite tiny voxel", flush=True)
+    ref = parity.lite_reference(s, 100, h=1e-6)
+    sel, group, obj, tc = _gpu(s, 100, 1e-6)
+    parity.assert_lite_close(sel, group, obj, ref, tc)
+
+
 def test_lite_deterministic():
     s = _sub("n4096_d1152", 1000, 8)
     print("lite determinism", flush=True)
