@@ -23,17 +23,20 @@ __global__ void fst_init_kernel(FstScratch s) {
   *s.tau_max = INT_MIN;
 }
 
-// Inverse feature norms: each wave walks rows blockIdx.x * 8 + w, + 8 *
-// gridDim.x, ..., with a row's 16-byte loads (up to 8 per lane) in flight
-// together.  Frame indices fold into a per-block range first, so the grid
-// issues only two atomics per block.
+constexpr int kPrepThreads = 256;
+constexpr int kPrepWaves = kPrepThreads / 64;
+
+// Inverse feature norms, as block blk of nblk: each wave walks rows
+// blk * 4 + w, + 4 * nblk, ..., with a row's 16-byte loads (up to 8 per lane)
+// in flight together.  Frame indices fold into a per-block range first, so
+// the grid issues only two atomics per block.
 template <bool BF16>
-__global__ __launch_bounds__(512) void row_norm_kernel(const void* feats, int n, int d,
-                                                       const int32_t* frame, FstScratch s) {
+__device__ void row_norms(const void* feats, int n, int d, const int32_t* frame, FstScratch s, int blk,
+                          int nblk) {
   const int lane = threadIdx.x & 63, wib = threadIdx.x >> 6;
   int fmin = INT_MAX, fmax = INT_MIN;
   const int m = BF16 ? d / 8 : d / 4;   // 16-byte chunks per row
-  for (int row = blockIdx.x * 8 + wib; row < n; row += gridDim.x * 8) {
+  for (int row = blk * kPrepWaves + wib; row < n; row += nblk * kPrepWaves) {
     const uint4* p = reinterpret_cast<const uint4*>(static_cast<const char*>(feats) +
                                                     size_t(row) * d * (BF16 ? 2 : 4));
     float acc = 0.f;
@@ -69,7 +72,7 @@ __global__ __launch_bounds__(512) void row_norm_kernel(const void* feats, int n,
       fmax = max(fmax, f);
     }
   }
-  __shared__ int smin[8], smax[8];
+  __shared__ int smin[kPrepWaves], smax[kPrepWaves];
   if (lane == 0) {
     smin[wib] = fmin;
     smax[wib] = fmax;
@@ -77,7 +80,7 @@ __global__ __launch_bounds__(512) void row_norm_kernel(const void* feats, int n,
   __syncthreads();
   if (threadIdx.x == 0) {
     int lo = smin[0], hi = smax[0];
-    for (int w = 1; w < 8; ++w) {
+    for (int w = 1; w < kPrepWaves; ++w) {
       lo = min(lo, smin[w]);
       hi = max(hi, smax[w]);
     }
@@ -109,14 +112,16 @@ __device__ __forceinline__ double sq_dist(double ax, double ay, double az, doubl
 constexpr int kPosTile = 256;
 
 // Exact maximum squared distance over all pairs: one block per upper
-// 256 x 256 tile (enough waves in flight to hide the float64 latency), a
-// thread takes one row of the tile against the tile's columns staged in LDS,
-// and a block whose maximum is larger than the running one raises it.
-__global__ __launch_bounds__(256) void pos_pairmax_kernel(const float* pos, int n, int ntiles, FstScratch s) {
+// 256 x 256 tile (enough waves in flight to hide the float64 latency; this
+// is block b of the tiles), a thread takes one row of the tile against the
+// tile's columns staged in LDS, and a block whose maximum is larger than the
+// running one raises it.
+__device__ void pos_pairmax(const float* pos, int n, int b, FstScratch s) {
+  static_assert(kPosTile == kPrepThreads, "one tile row per thread");
   __shared__ double sx[kPosTile], sy[kPosTile], sz[kPosTile];
-  __shared__ double sm[4];
+  __shared__ double sm[kPrepWaves];
   double best = 0.0;
-  for (int b = blockIdx.x; b < ntiles; b += gridDim.x) {
+  {
     int ti, tj;
     upper_tile(b, ti, tj);
     const int j = tj * kPosTile + threadIdx.x;
@@ -141,6 +146,16 @@ __global__ __launch_bounds__(256) void pos_pairmax_kernel(const float* pos, int 
   // address serialize.
   const double m = fmax(fmax(sm[0], sm[1]), fmax(sm[2], sm[3]));
   if (threadIdx.x == 0 && m > __longlong_as_double((long long)get(s.mx2_bits))) atomic_max_nonneg(s.mx2_bits, m);
+}
+
+// The prep in one launch: the compute-bound pair maxima (blocks [0, tiles))
+// run beside the memory-bound row norms (the nr blocks after them).
+template <bool BF16>
+__global__ __launch_bounds__(kPrepThreads) void fst_prep_kernel(const void* feats, int n, int d,
+                                                                const int32_t* frame, const float* pos,
+                                                                int tiles, int nr, FstScratch s) {
+  if (int(blockIdx.x) < tiles) pos_pairmax(pos, n, blockIdx.x, s);
+  else row_norms<BF16>(feats, n, d, frame, s, blockIdx.x - tiles, nr);
 }
 
 // ---------------------------------------------------------------------------
@@ -415,15 +430,13 @@ hipError_t launch_fst_prep(const FstParams& p, const FstScratch& s, hipStream_t 
   fst_init_kernel<<<1, 1, 0, stream>>>(s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nb = std::min((p.n + 7) / 8, 512);
-  if (p.bf16)
-    row_norm_kernel<true><<<nb, 512, 0, stream>>>(p.feats, p.n, p.d, p.frame, s);
-  else
-    row_norm_kernel<false><<<nb, 512, 0, stream>>>(p.feats, p.n, p.d, p.frame, s);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int nr = std::min((p.n + kPrepWaves - 1) / kPrepWaves, 1024);
   const int t = tiles_of(p.n, kPosTile);
   const int tiles = t * (t + 1) / 2;
-  pos_pairmax_kernel<<<tiles, 256, 0, stream>>>(p.pos, p.n, tiles, s);
+  if (p.bf16)
+    fst_prep_kernel<true><<<tiles + nr, kPrepThreads, 0, stream>>>(p.feats, p.n, p.d, p.frame, p.pos, tiles, nr, s);
+  else
+    fst_prep_kernel<false><<<tiles + nr, kPrepThreads, 0, stream>>>(p.feats, p.n, p.d, p.frame, p.pos, tiles, nr, s);
   return hipGetLastError();
 }
 
