@@ -1253,7 +1253,7 @@ __global__ __launch_bounds__(256) void list_build_kernel(IncDev a) {
 #pragma unroll
     for (int u = 0; u < 8; ++u)
       if (q0 + u < nch) {
-        x[u] = row[(q0 + u) * (kRowChunk / 4) + lane];
+        x[u] = __builtin_nontemporal_load(row + (q0 + u) * (kRowChunk / 4) + lane);   // T is read once here
         b[u] = bb[(q0 + u) * (kRowChunk / 4) + lane];
       }
 #pragma unroll
