@@ -102,6 +102,28 @@ def test_lite_keys_wider_than_the_bucket_pass():
     parity.assert_lite_close(sel, group, obj, ref, tc)
 
 
+@pytest.mark.parametrize("n,k", [(1, 1), (2, 1), (2, 2), (3, 2), (17, 5), (257, 30)])
+def test_lite_tiny_scenes(n, k):
+    # One front block (two at 257 tokens), a token field of 0-9 bits, spans of
+    # a single bucket and groups of one token.
+    s = _sub("n4096_d1152", n, 11)
+    print(f"lite tiny n={n} k={k}", flush=True)
+    ref = parity.lite_reference(s, k, h=0.25)
+    sel, group, obj, tc = _gpu(s, k, 0.25)
+    parity.assert_lite_close(sel, group, obj, ref, tc)
+
+
+def test_lite_identical_positions():
+    # Every key is zero (a zero-width bucket field: one bucket holds every
+    # token, sorted by index alone) and M_x is zero.
+    s = _sub("n4096_d1152", 600, 12)
+    s.pos[:] = s.pos[0]
+    print("lite identical positions", flush=True)
+    ref = parity.lite_reference(s, 60, h=0.25)
+    sel, group, obj, tc = _gpu(s, 60, 0.25)
+    parity.assert_lite_close(sel, group, obj, ref, tc)
+
+
 def test_lite_deterministic():
     s = _sub("n4096_d1152", 1000, 8)
     print("lite determinism", flush=True)
