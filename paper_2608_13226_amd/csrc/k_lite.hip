@@ -96,14 +96,12 @@ struct LiteDev {
   double* B;                    // [n]
   double* gcost;                // [k]
   unsigned int* ctrl;           // see kCtrl* offsets
+  unsigned int* pmax;           // [kMaxSlots][kSlotWords]: maxima over evaluated pairs, see kSlot*
 };
 
 // ctrl words
 constexpr int kCtrlBbox = 0;       // 3 x order key of the per-axis minimum
 constexpr int kCtrlMaxKey = 4;     // u64 (words 4, 5)
-constexpr int kCtrlMx2 = 6;        // u64 bits of max squared distance (words 6, 7)
-constexpr int kCtrlMt = 8;         // max |d tau| over evaluated pairs
-constexpr int kCtrlMf = 9;         // float bits of max d_f
 constexpr int kCtrlSorted = 10;    // which key/tok buffer holds the sorted order
 constexpr int kCtrlBarrier = 11;   // grid barrier counter
 constexpr int kCtrlTiles = 12;     // total number of 16-row tiles
@@ -111,9 +109,19 @@ constexpr int kCtrlBig = 13;       // tiles of groups of more than kSplitTiles t
 constexpr int kCtrlAbort = 14;     // raised when a grid barrier of the front gives up
 constexpr int kCtrlBboxMax = 15;   // 3 x order key of the per-axis maximum (words 15-17)
 
+// The maxima over evaluated pairs (M_f, M_x, M_tau) are raised by every pair
+// block; block b raises those of slot b % kMaxSlots, each slot on a cache
+// line of its own (one line for all of them serialized a thousand blocks),
+// and the kernels that use them take the maximum over the slots.
+constexpr int kMaxSlots = 32;
+constexpr int kSlotWords = 32;      // 128 bytes
+constexpr int kSlotMf = 0;          // float bits of max d_f
+constexpr int kSlotMt = 1;          // max |d tau|
+constexpr int kSlotMx2 = 2;         // u64 bits of max squared distance (words 2, 3)
+
 struct Layout {
   size_t key0, key1, tok0, tok1, vox_tok, vox_pos, hist, bcnt, bval, bsum, bsum2, bmin, gid, gstart, rt_start,
-      unit_group, big_unit, A, B, gcost, ctrl, total;
+      unit_group, big_unit, A, B, gcost, ctrl, pmax, total;
 };
 
 // Groups of more than this many 16-row tiles are split over a block's waves.
@@ -145,6 +153,7 @@ Layout layout(int64_t n, int64_t k) {
   L.B = o;        o += a256(size_t(n) * 8);
   L.gcost = o;    o += a256(size_t(k) * 8);
   L.ctrl = o;     o += 256;
+  L.pmax = o;     o += a256(size_t(kMaxSlots) * kSlotWords * 4);
   L.total = o;
   return L;
 }
@@ -259,15 +268,13 @@ __global__ void lite_init_kernel(LiteDev a) {
     a.ctrl[kCtrlBbox + 0] = a.ctrl[kCtrlBbox + 1] = a.ctrl[kCtrlBbox + 2] = 0xffffffffu;
     a.ctrl[kCtrlBboxMax + 0] = a.ctrl[kCtrlBboxMax + 1] = a.ctrl[kCtrlBboxMax + 2] = 0u;
     *reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey) = 0ull;
-    *reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2) = 0ull;
-    a.ctrl[kCtrlMt] = 0u;
-    a.ctrl[kCtrlMf] = 0u;
     a.ctrl[kCtrlSorted] = 0u;
     a.ctrl[kCtrlBarrier] = 0u;
     a.ctrl[kCtrlTiles] = 0u;
     a.ctrl[kCtrlBig] = 0u;
     a.ctrl[kCtrlAbort] = a.abort_init;
   }
+  for (int q = threadIdx.x; q < kMaxSlots * 4; q += blockDim.x) a.pmax[(q / 4) * kSlotWords + q % 4] = 0u;
 }
 
 // Grid coordinate of one position component (Morton cell of 1 / 256 voxel).
@@ -1031,6 +1038,29 @@ struct PairMax {
   int tau = 0;
 };
 
+// The maxima over all slots, in a kernel after the pair kernels: lane q of
+// the wave reads slot q, then maxima across the wave (every lane active).
+struct PairMaxima {
+  float df;
+  double x2;
+  int tau;
+};
+__device__ __forceinline__ PairMaxima pair_maxima(const LiteDev& a) {
+  static_assert(kMaxSlots <= 64, "one slot per lane");
+  const int lane = threadIdx.x & 63;
+  PairMaxima m{0.f, 0.0, 0};
+  if (lane < kMaxSlots) {
+    const unsigned int* slot = a.pmax + lane * kSlotWords;
+    m.df = __uint_as_float(slot[kSlotMf]);
+    m.tau = int(slot[kSlotMt]);
+    m.x2 = __longlong_as_double(*reinterpret_cast<const long long*>(slot + kSlotMx2));
+  }
+  m.df = wave_max(m.df);
+  m.x2 = wave_max(m.x2);
+  m.tau = wave_max(m.tau);
+  return m;
+}
+
 // The epilogue of a tile product: acc holds row tile t.ta against column
 // tile tb (output element (4 (l / 16) + r, l % 16) in register r of lane l),
 // na the squared norm of the lane's row l % 16 of tile ta and nb that of
@@ -1223,10 +1253,11 @@ __device__ __forceinline__ void pair_max_to(const LiteDev& a, PairMax pm) {
       pm.x2 = fmax(pm.x2, sx[q]);
       pm.tau = max(pm.tau, st[q]);
     }
-    unsigned long long* mx2 = reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMx2);
-    if (pm.df > __uint_as_float(get(a.ctrl + kCtrlMf))) atomic_max_nonneg(a.ctrl + kCtrlMf, pm.df);
+    unsigned int* slot = a.pmax + (blockIdx.x % kMaxSlots) * kSlotWords;
+    unsigned long long* mx2 = reinterpret_cast<unsigned long long*>(slot + kSlotMx2);
+    if (pm.df > __uint_as_float(get(slot + kSlotMf))) atomic_max_nonneg(slot + kSlotMf, pm.df);
     if (pm.x2 > __longlong_as_double((long long)get(mx2))) atomic_max_nonneg(mx2, pm.x2);
-    if (unsigned(pm.tau) > get(a.ctrl + kCtrlMt)) atomicMax(a.ctrl + kCtrlMt, unsigned(pm.tau));
+    if (unsigned(pm.tau) > get(slot + kSlotMt)) atomicMax(slot + kSlotMt, unsigned(pm.tau));
   }
 }
 
@@ -1321,8 +1352,9 @@ __global__ __launch_bounds__(kThreads) void lite_b_kernel(LiteDev a) {
   const int nw = gridDim.x * kWaves;
   const int units = int(a.ctrl[kCtrlTiles]);
   const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
-  const double m_x = sqrt(__longlong_as_double(*reinterpret_cast<const long long*>(a.ctrl + kCtrlMx2)));
-  const int m_t = int(a.ctrl[kCtrlMt]);
+  const PairMaxima mm = pair_maxima(a);
+  const double m_x = sqrt(mm.x2);
+  const int m_t = mm.tau;
   const double c0 = double(a.lam_f) + double(a.lam_x) + double(a.lam_t);
   for (int u = gw; u < units; u += nw) {
     Unit t;
@@ -1392,7 +1424,7 @@ __global__ __launch_bounds__(kThreads) void lite_select_kernel(LiteDev a) {
     return;
   }
   const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
-  const float m_f = __uint_as_float(a.ctrl[kCtrlMf]);
+  const float m_f = pair_maxima(a).df;
   const double wf = m_f > 0.f ? double(a.lam_f) / double(m_f) : 0.0;
   double best = DBL_MAX;
   int bt = INT_MAX;
@@ -1483,6 +1515,7 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   a.B = reinterpret_cast<double*>(w + L.B);
   a.gcost = reinterpret_cast<double*>(w + L.gcost);
   a.ctrl = reinterpret_cast<unsigned int*>(w + L.ctrl);
+  a.pmax = reinterpret_cast<unsigned int*>(w + L.pmax);
 
   lite_init_kernel<<<1, 64, 0, stream>>>(a);
   hipError_t e = hipGetLastError();
