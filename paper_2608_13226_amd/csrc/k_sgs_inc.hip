@@ -312,9 +312,19 @@ int rows_ldt(int64_t n) { return int((n + kRowChunk - 1) / kRowChunk * kRowChunk
 // needs.
 __device__ __forceinline__ int fixed_scale(const IncDev& a, double* sd) {
   double x = 0.0, m = 0.0;
-  for (int j = threadIdx.x; j < a.n; j += kBlock) {
-    x += double(a.v[j]);
-    m = fmax(m, double(a.v[j]));
+  // Thread t adds v[t], v[t + kBlock], ... in that order; the loads of
+  // eight of them go out together (indices past n read v[n - 1], unused).
+  constexpr int U = 8;
+  for (int j0 = threadIdx.x; j0 < a.n; j0 += kBlock * U) {
+    float vv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) vv[u] = a.v[min(j0 + u * kBlock, a.n - 1)];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (j0 + u * kBlock < a.n) {
+        x += double(vv[u]);
+        m = fmax(m, double(vv[u]));
+      }
   }
   const double M = double(a.c0) * block_sum_all(x, sd);
   const double Mt = double(a.c0) * block_max_all(m, sd);
