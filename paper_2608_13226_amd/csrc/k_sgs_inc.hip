@@ -93,8 +93,7 @@ __device__ __forceinline__ void inc_body(const IncDev& a, int blk, int nb) {
   __shared__ long long sLw[kWaves];
   int obj_step = -1;
   if (blk == 0) {
-    long long x = 0;
-    for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
+    const long long x = fx_capacity_part(a.v, a.n, a.c0, S);
     const long long L0 = block_sum_i64(x, sg);
     if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
   }
@@ -528,8 +527,7 @@ __device__ __forceinline__ void rows_body(const IncDev& a, int blk, int nb) {
     if (resume) {
       L0 = a.ho_misc[0];
     } else {
-      long long x = 0;
-      for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
+      const long long x = fx_capacity_part(a.v, a.n, a.c0, S);
       L0 = block_sum_i64(x, sg);
     }
     if (tid < kWaves) sLw[tid] = tid == 0 ? L0 : 0;
@@ -989,8 +987,7 @@ __global__ __launch_bounds__(kBlock) void sgs_early_kernel(IncDev a) {
   // Block 0 keeps the objective (in wave 1 after the start).
   long long L = 0;
   if (blk == 0) {
-    long long x = 0;
-    for (int j = tid; j < a.n; j += kBlock) x += fx(double(a.v[j]) * double(a.c0), S);
+    const long long x = fx_capacity_part(a.v, a.n, a.c0, S);
     L = block_sum_i64(x, red);
   }
   publish_rows(sG, ssel, lo, cnt, S, cand_slot(a.cand, 0, blk), epoch_of(0));

@@ -113,8 +113,18 @@ __global__ __launch_bounds__(kBlock) void sgs_local_kernel(LocalDev L) {
   // Fixed-point scale, the same in every block (same sum, same order).
   double vsum;
   {
+    // Thread t adds v[t], v[t + kBlock], ... in that order, eight loads in
+    // flight at a time.
     double x = 0.0;
-    for (int j = tid; j < a.n; j += kBlock) x += double(a.v[j]);
+    constexpr int U = 8;
+    for (int j0 = tid; j0 < a.n; j0 += kBlock * U) {
+      float vv[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) vv[u] = a.v[min(j0 + u * kBlock, a.n - 1)];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (j0 + u * kBlock < a.n) x += double(vv[u]);
+    }
     vsum = block_sum_all(x, sd);
   }
   const double M = double(a.c0) * vsum;

@@ -306,6 +306,24 @@ __device__ double block_sum_all(double x, double* sd) {
   return s;
 }
 
+// Thread t's part of sum_j fx(v_j c0, S), the objective at b = c0 (exact
+// integers, so the parts and their total do not depend on the order): j = t,
+// t + kBlock, ..., eight loads in flight at a time (a load whose result the
+// next iteration needs waits for itself otherwise).
+__device__ __forceinline__ long long fx_capacity_part(const float* v, int n, float c0, int S) {
+  long long x = 0;
+  constexpr int U = 8;
+  for (int j0 = threadIdx.x; j0 < n; j0 += kBlock * U) {
+    float vv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) vv[u] = v[min(j0 + u * kBlock, n - 1)];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (j0 + u * kBlock < n) x += fx(double(vv[u]) * double(c0), S);
+  }
+  return x;
+}
+
 // Block maximum, result in every thread.
 __device__ double block_max_all(double x, double* sd) {
   x = wave_max(x);
