@@ -38,10 +38,11 @@
  *     of the calling thread.
  *   - Results are bitwise reproducible run to run on the same GPU.  Calls on
  *     distinct workspaces and streams may run concurrently.
- *   - Waits between the blocks of one launch are bounded.  The selection
- *     calls (sgs_select, sgs_select_batch, sgs_local_select, lite_select) run
- *     persistent launches whose blocks wait for each other; a wait that has
- *     polled for about a second (far beyond any legitimate wait: a launch
+ *   - Waits between the blocks of one launch are bounded.  The greedy
+ *     selection calls (sgs_select, sgs_select_batch, sgs_local_select, and the
+ *     greedy of prune) run persistent launches whose blocks wait for each
+ *     other (lite_select has no such waits: ordinary launches only).  A wait
+ *     that has polled for about a second (far beyond any legitimate wait: a launch
  *     starved of compute units, or a broken device) gives up, every block of
  *     the launch leaves, and every entry of `selected` is set to -1, which is
  *     never a token index.  The call itself has already returned CP_OK (the
@@ -449,8 +450,8 @@ cp_status coverprune_sgs_literal_select(const float* cost, int64_t n, const floa
  *   token_cost  [n] double output (may be NULL): every token t's cost to its
  *               group, sum_{j in G_q} v_j C(t, j), the quantity Eq. 18
  *               minimises (token order, not Morton order)
- * The front of the call (keys, sort, groups) is one persistent launch with
- * bounded waits; when it gives up, selected[] is -1 and the objective NaN.
+ * Every kernel of the call is an ordinary launch and no block waits for
+ * another, so the call never gives up (COVERPRUNE_TEST_ABORT does not apply).
  */
 size_t coverprune_lite_workspace(int64_t n, int64_t d, int64_t k, cp_dtype dtype);
 cp_status coverprune_lite_select(const void* feats, cp_dtype dtype, int64_t n, int64_t d,

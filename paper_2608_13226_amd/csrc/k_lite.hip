@@ -1,25 +1,25 @@
 // CoverPrune-Lite (Sec. 4, Eq. 17-20) on one GPU.
 //
-//   front (one cooperative launch; phases separated by fence-free grid
-//          barriers, data between phases exchanged with device-scope atomics)
-//     bbox     per-axis minimum (the Morton origin) and maximum (which bounds
-//              the key bits in use) of the positions
+//   front (seven ordinary launches; each hands its results to the next
+//          through the workspace, so no block waits for another)
+//     bbox     per-block partials of the per-axis minimum (the Morton origin)
+//              and maximum (which bounds the key bits in use)
 //     keys     q = floor((x - min) * 256 / h) in float64, clamped to 21 bits;
-//              key = 3-way bit interleave; voxel = q >> 8
-//     sort     by (key, token): the top 12 key bits in use pick a bucket
-//              (counts and capacity sums per bucket by atomics); each block
-//              owns the whole buckets that start in its range, every element
-//              goes straight to its bucket, and each block sorts its span in
-//              LDS (bitonic, on key and token packed into 64 bits).  When a
-//              span would not fit in LDS, a stable LSD radix sort in 8-bit
-//              digits over the key bits in use runs instead (a pass's digit
-//              counts per block range are added up while the pass before it
-//              places its elements, so a pass needs one grid barrier)
-//     groups   V = floor(v * 2^40) in exact integers; an exclusive scan gives
-//              the mass before each position, t(p) = min(K-1, K * mass / W);
-//              a prefix-min scan of t(p) - p and the K - N + p floor give the
+//              key = 3-way bit interleave; voxel = q >> 8.  The top 12 key
+//              bits in use pick a bucket: counts and capacity sums per bucket
+//              by atomics, and every token's place in its bucket
+//     place    bucket starts; each block owns the whole buckets that start in
+//              its range of positions (its span); every token goes straight
+//              to its bucket
+//     sort     each block sorts its span by (key, token): in registers (a
+//              bitonic network on key and token packed into 64 bits) when it
+//              fits, else by a stable LSD radix sort inside the block; then
+//              the permutation, the voxels by position and, with V =
+//              floor(v * 2^40) in exact integers and the mass before each
+//              position, t(p) = min(K-1, K * mass / W) and the offset t(p) - p
+//     groups   a prefix minimum of t(p) - p and the K - N + p floor give the
 //              group of every position (the walk of Eq. 17 in scan form),
-//              and in the same pass the group starts
+//              and the group starts
 //     tiles    16-row tiles per group, their prefix, the group of every
 //              tile and the list of big groups' tiles (work units below)
 //   pairs    per 16-row tile of a group, the tile's rows against the whole
@@ -48,8 +48,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kFrontBlocks = 64;
-constexpr int kMaxPasses = 8;          // 8-bit digits of a key of at most 63 bits
-constexpr int kBins = 256;
+constexpr int kBins = 256;             // 8-bit digits of the radix sort of long spans
 constexpr int kAxisBits = 21;
 constexpr int kSubBits = 8;
 constexpr int kTileRows = 16;
@@ -74,14 +73,15 @@ struct LiteDev {
   int32_t* group;
   double* objective;
   double* token_cost;           // [n] or nullptr: each token's cost to its group (Eq. 18)
-  unsigned int poll_limit;      // polls before a grid barrier gives up (WaitPolicy)
-  unsigned int abort_init;      // the abort word's value at launch
   // workspace
   unsigned long long* key[2];
   int* tok[2];
-  unsigned long long* vox_tok;  // [n] packed voxel of each token
   unsigned long long* vox_pos;  // [n] packed voxel of each sorted position
-  unsigned int* hist;           // [kMaxPasses][G][256]: digit counts of each pass's ranges
+  unsigned int* bbox_part;      // [G][6]: order keys of each front block's per-axis minima, then maxima
+  unsigned int* within;         // [n] a token's place in its bucket
+  int* span;                    // [G + 1]: the front blocks' spans of sorted positions
+  unsigned long long* span_run; // [G]: capacity units before each span
+  double* geom;                 // [4]: the Morton origin (3 axes) and the key bits in use
   unsigned int* bcnt;           // [kBuckets] elements per bucket
   unsigned long long* bval;     // [kBuckets] capacity units per bucket
   unsigned long long* bsum;     // [G]
@@ -100,14 +100,9 @@ struct LiteDev {
 };
 
 // ctrl words
-constexpr int kCtrlBbox = 0;       // 3 x order key of the per-axis minimum
-constexpr int kCtrlMaxKey = 4;     // u64 (words 4, 5)
-constexpr int kCtrlSorted = 10;    // which key/tok buffer holds the sorted order
-constexpr int kCtrlBarrier = 11;   // grid barrier counter
+constexpr int kCtrlW = 4;          // u64 (words 4, 5): all capacity units
 constexpr int kCtrlTiles = 12;     // total number of 16-row tiles
 constexpr int kCtrlBig = 13;       // tiles of groups of more than kSplitTiles tiles
-constexpr int kCtrlAbort = 14;     // raised when a grid barrier of the front gives up
-constexpr int kCtrlBboxMax = 15;   // 3 x order key of the per-axis maximum (words 15-17)
 
 // The maxima over evaluated pairs (M_f, M_x, M_tau) are raised by every pair
 // block; block b raises those of slot b % kMaxSlots, each slot on a cache
@@ -120,8 +115,8 @@ constexpr int kSlotMt = 1;          // max |d tau|
 constexpr int kSlotMx2 = 2;         // u64 bits of max squared distance (words 2, 3)
 
 struct Layout {
-  size_t key0, key1, tok0, tok1, vox_tok, vox_pos, hist, bcnt, bval, bsum, bsum2, bmin, gid, gstart, rt_start,
-      unit_group, big_unit, A, B, gcost, ctrl, pmax, total;
+  size_t key0, key1, tok0, tok1, vox_pos, bbox_part, within, span, span_run, geom, bcnt, bval, bsum, bsum2, bmin,
+      gid, gstart, rt_start, unit_group, big_unit, A, B, gcost, ctrl, pmax, total;
 };
 
 // Groups of more than this many 16-row tiles are split over a block's waves.
@@ -136,9 +131,12 @@ Layout layout(int64_t n, int64_t k) {
   L.key1 = o;     o += a256(size_t(n) * 8);
   L.tok0 = o;     o += a256(size_t(n) * 4);
   L.tok1 = o;     o += a256(size_t(n) * 4);
-  L.vox_tok = o;  o += a256(size_t(n) * 8);
   L.vox_pos = o;  o += a256(size_t(n) * 8);
-  L.hist = o;     o += a256(size_t(kMaxPasses) * kFrontBlocks * kBins * 4);
+  L.bbox_part = o; o += a256(size_t(kFrontBlocks) * 6 * 4);
+  L.within = o;   o += a256(size_t(n) * 4);
+  L.span = o;     o += a256(size_t(kFrontBlocks + 1) * 4);
+  L.span_run = o; o += a256(size_t(kFrontBlocks) * 8);
+  L.geom = o;     o += a256(4 * 8);
   L.bcnt = o;     o += a256(size_t(kBuckets) * 4);
   L.bval = o;     o += a256(size_t(kBuckets) * 8);
   L.bsum = o;     o += a256(size_t(kFrontBlocks) * 8);
@@ -261,20 +259,6 @@ __device__ void block_prefix_u64(const unsigned long long* vals, int G, int blk,
   before = sh[kThreads];
   total = sh[kThreads + 1];
   __syncthreads();
-}
-
-__global__ void lite_init_kernel(LiteDev a) {
-  if (threadIdx.x == 0) {
-    a.ctrl[kCtrlBbox + 0] = a.ctrl[kCtrlBbox + 1] = a.ctrl[kCtrlBbox + 2] = 0xffffffffu;
-    a.ctrl[kCtrlBboxMax + 0] = a.ctrl[kCtrlBboxMax + 1] = a.ctrl[kCtrlBboxMax + 2] = 0u;
-    *reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey) = 0ull;
-    a.ctrl[kCtrlSorted] = 0u;
-    a.ctrl[kCtrlBarrier] = 0u;
-    a.ctrl[kCtrlTiles] = 0u;
-    a.ctrl[kCtrlBig] = 0u;
-    a.ctrl[kCtrlAbort] = a.abort_init;
-  }
-  for (int q = threadIdx.x; q < kMaxSlots * 4; q += blockDim.x) a.pmax[(q / 4) * kSlotWords + q % 4] = 0u;
 }
 
 // Grid coordinate of one position component (Morton cell of 1 / 256 voxel).
@@ -447,15 +431,14 @@ __device__ void bitonic_unrolled(unsigned long long (&x)[R], unsigned long long*
 // order, m >= 1 of them): thread t's positions i in [i0, i1) of the span, at
 // most R of them.  Writes the permutation and the voxels by position, scans
 // the capacity units over the span (run: units before it, W: all units) and
-// leaves (tp - p, token) of each position in s_out (Eq. 17 in scan form).
-// Work on absent positions reads position m - 1 and is dropped, so that the
-// R positions' loads and arithmetic overlap.  Returns the thread's minimum
+// writes tp - p of each position to gid (Eq. 17 in scan form).  Work on
+// absent positions reads position m - 1 and is dropped, so that the R
+// positions' loads and arithmetic overlap.  Returns the thread's minimum
 // tp - p (INT_MAX without positions).
 template <int R>
 __device__ int span_offsets(const LiteDev& a, int r0, int m, int i0, int i1, unsigned long long tmask,
                             const double (&org)[3], unsigned long long run, unsigned long long W,
-                            const unsigned long long* s_sorted, unsigned long long* s_out,
-                            unsigned long long* s_u64) {
+                            const unsigned long long* s_sorted, unsigned long long* s_u64) {
   int tk[R];
   unsigned long long vx[R], V[R];
 #pragma unroll
@@ -471,8 +454,8 @@ __device__ int span_offsets(const LiteDev& a, int r0, int m, int i0, int i1, uns
   for (int u = 0; u < R; ++u)
     if (i0 + u < i1) {
       loc += V[u];
-      put(a.tok[1] + r0 + i0 + u, tk[u]);
-      put(a.vox_pos + r0 + i0 + u, vx[u]);
+      a.tok[1][r0 + i0 + u] = tk[u];
+      a.vox_pos[r0 + i0 + u] = vx[u];
     }
   unsigned long long span_tot;
   unsigned long long before = run + block_excl_sum_u64(loc, s_u64, span_tot);
@@ -489,25 +472,29 @@ __device__ int span_offsets(const LiteDev& a, int r0, int m, int i0, int i1, uns
   for (int u = 0; u < R; ++u)
     if (i0 + u < i1) {
       const int mm = int(tp[u] - (r0 + i0 + u));
-      s_out[i0 + u] = ((unsigned long long)(unsigned int)mm << 32) | (unsigned int)tk[u];
+      a.gid[r0 + i0 + u] = mm;
       bmin = min(bmin, mm);
     }
   return bmin;
 }
 
-// Loads src[0, m) (m <= kThreads * R; the rest padded with the largest
-// value), sorts it and leaves the sorted values in dst[0, kThreads * R)
-// (tmp: LDS of the same size, clobbered).
+// Packs keys[0, m) and toks[0, m) as key * 2^tokbits + token (m <= kThreads
+// * R; the rest padded with the largest value), sorts them and leaves the
+// sorted values in dst[0, kThreads * R) (tmp: LDS of the same size,
+// clobbered).
 template <int R>
-__device__ void span_sort(const unsigned long long* src, int m, unsigned long long* dst, unsigned long long* tmp) {
+__device__ void span_sort(const unsigned long long* keys, const int* toks, int tokbits, int m,
+                          unsigned long long* dst, unsigned long long* tmp) {
   const int t = threadIdx.x;
   unsigned long long x[R];
-  // Every load is issued before any is used (a device-scope load under a
-  // condition waits for itself): indices past m read element m - 1 and are
-  // then replaced by the padding.
+  // Every load is issued before any is used: indices past m read element
+  // m - 1 and are then replaced by the padding.
   if (m > 0) {
 #pragma unroll
-    for (int r = 0; r < R; ++r) x[r] = get(src + min(t * R + r, m - 1));
+    for (int r = 0; r < R; ++r) {
+      const int i = min(t * R + r, m - 1);
+      x[r] = (keys[i] << tokbits) | (unsigned long long)(unsigned int)toks[i];
+    }
 #pragma unroll
     for (int r = 0; r < R; ++r)
       if (t * R + r >= m) x[r] = ~0ull;
@@ -523,484 +510,452 @@ __device__ void span_sort(const unsigned long long* src, int m, unsigned long lo
   __syncthreads();
 }
 
-__global__ __launch_bounds__(kThreads) void lite_front_kernel(LiteDev a) {
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int G = gridDim.x, blk = blockIdx.x;
-  const int n = a.n, K = a.k;
-  const int tile = (n + G - 1) / G;
-  const int p0 = min(n, blk * tile), p1 = min(n, p0 + tile);
-  unsigned int* bar = a.ctrl + kCtrlBarrier;
-  unsigned int* abort = a.ctrl + kCtrlAbort;
-  unsigned int round = 0;
-  // Every grid barrier is bounded; a block whose barrier gives up leaves, and
-  // the kernels after the front see the abort word and do nothing.
-  __shared__ int s_ok;
+// ---------------------------------------------------------------------------
+// The front: seven ordinary launches of G blocks.  Each hands its results to
+// the next through the workspace (the launch boundary orders them), so no
+// block ever waits for another.  Block b owns positions [b tile, (b + 1)
+// tile) up to the placement and its span of whole buckets from the sort on.
+struct FrontRange {
+  int tile, p0, p1;
+};
+__device__ __forceinline__ FrontRange front_range(int n) {
+  const int tile = (n + int(gridDim.x) - 1) / int(gridDim.x);
+  const int p0 = min(n, int(blockIdx.x) * tile);
+  return {tile, p0, min(n, p0 + tile)};
+}
 
-  __shared__ unsigned int s_u32[6][kWaves];
-  __shared__ unsigned long long s_u64[kThreads + 2];
-  __shared__ int s_i32[kThreads];
-  __shared__ unsigned int s_hist[kBins];
-  __shared__ unsigned int s_base[kBins];
-  __shared__ unsigned int s_wcnt[kWaves][kBins];
-  __shared__ int s_minoff;
-  // bucket pass: per-bucket counts (then this block's base in each bucket),
-  // one wide array used in turn for per-bucket capacity sums, bucket starts
-  // and the span being sorted, and the block's keys with their ranks
-  __shared__ unsigned int s_cnt[kBuckets];
-  __shared__ unsigned long long s_wide[kSortCap];
-  __shared__ unsigned long long s_key[kSortCap];
-  __shared__ uint16_t s_rank[kSortCap];
-  __shared__ int s_span[kFrontBlocks + 1], s_first[kFrontBlocks + 1];
-  __shared__ int s_fast;
+// The key geometry of the scene from the bbox: the Morton origin and the
+// bit length of every key (the Morton code of the grid coordinates of the
+// bbox maximum bounds it).
+__device__ __forceinline__ int tok_bits(int n) { return n > 1 ? 32 - __clz(n - 1) : 0; }
+__device__ __forceinline__ int bucket_shift(int kbits) { return kbits - min(kBucketBits, kbits); }
 
-  // ---- this block's rows of every pass's digit counts and its slice of the
-  // bucket tables start at zero (the first additions come after the next
-  // barrier); bbox minimum and maximum per axis
-  for (int q = t; q < kMaxPasses * kBins; q += kThreads) put(a.hist + (size_t(q / kBins) * G + blk) * kBins + q % kBins, 0u);
-  for (int q = blk * kThreads + t; q < kBuckets; q += G * kThreads) {
-    put(a.bcnt + q, 0u);
-    put(a.bval + q, 0ull);
+// 1. Per-block bbox partials (order keys of the per-axis minima and maxima).
+// The call's tile counts, the pair maxima's slots and the bucket tables start
+// at zero here.
+__global__ __launch_bounds__(kThreads) void lite_bbox_kernel(LiteDev a) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6, blk = blockIdx.x;
+  if (blk == 0) {
+    if (t == 0) {
+      a.ctrl[kCtrlTiles] = 0u;
+      a.ctrl[kCtrlBig] = 0u;
+    }
+    for (int q = t; q < kMaxSlots * 4; q += kThreads) a.pmax[(q / 4) * kSlotWords + q % 4] = 0u;
   }
-  {
-    unsigned int m[6] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0u, 0u, 0u};
-    for (int i = p0 + t; i < p1; i += kThreads)
-      for (int ax = 0; ax < 3; ++ax) {
-        const unsigned int o = float_order_key(a.pos[3 * i + ax]);
-        m[ax] = min(m[ax], o);
-        m[3 + ax] = max(m[3 + ax], o);
-      }
+  for (int q = blk * kThreads + t; q < kBuckets; q += int(gridDim.x) * kThreads) {
+    a.bcnt[q] = 0u;
+    a.bval[q] = 0ull;
+  }
+  const FrontRange r = front_range(a.n);
+  __shared__ unsigned int s_u32[6][kWaves];
+  unsigned int m[6] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0u, 0u, 0u};
+  for (int i = r.p0 + t; i < r.p1; i += kThreads)
+    for (int ax = 0; ax < 3; ++ax) {
+      const unsigned int o = float_order_key(a.pos[3 * i + ax]);
+      m[ax] = min(m[ax], o);
+      m[3 + ax] = max(m[3 + ax], o);
+    }
+  for (int e = 0; e < 6; ++e) {
+    unsigned int x = m[e];
+    for (int o = 32; o > 0; o >>= 1) {
+      const unsigned int y = (unsigned int)__shfl_xor((int)x, o);
+      x = e < 3 ? min(x, y) : max(x, y);
+    }
+    if (lane == 0) s_u32[e][w] = x;
+  }
+  __syncthreads();
+  if (t < 6) {
+    unsigned int x = s_u32[t][0];
+    for (int q = 1; q < kWaves; ++q) x = t < 3 ? min(x, s_u32[t][q]) : max(x, s_u32[t][q]);
+    a.bbox_part[blk * 6 + t] = x;
+  }
+}
+
+// 2. Morton keys, bucket counts and capacity sums.  Each block counts its
+// keys per bucket in LDS (a key's rank among the block's keys of its
+// bucket), adds its counts and capacity units to the bucket tables with one
+// returning atomic per non-empty bucket (the return is the block's base in
+// that bucket, blocks landing in any order) and stores every token's place
+// in its bucket, base plus rank.
+__global__ __launch_bounds__(kThreads) void lite_keys_kernel(LiteDev a) {
+  const int t = threadIdx.x, lane = t & 63, blk = blockIdx.x, G = gridDim.x;
+  const FrontRange r = front_range(a.n);
+  __shared__ unsigned int s_bb[6];
+  __shared__ unsigned int s_cnt[kBuckets];
+  __shared__ unsigned long long s_vb[kBuckets];
+  if (t < 64) {
+    // lane b reads block b's partials (blocks past G repeat the last one)
+#pragma unroll
     for (int e = 0; e < 6; ++e) {
-      unsigned int x = m[e];
+      unsigned int x = a.bbox_part[min(lane, G - 1) * 6 + e];
       for (int o = 32; o > 0; o >>= 1) {
         const unsigned int y = (unsigned int)__shfl_xor((int)x, o);
         x = e < 3 ? min(x, y) : max(x, y);
       }
-      if (lane == 0) s_u32[e][w] = x;
-    }
-    __syncthreads();
-    if (t < 6) {
-      unsigned int x = s_u32[t][0];
-      for (int q = 1; q < kWaves; ++q) x = t < 3 ? min(x, s_u32[t][q]) : max(x, s_u32[t][q]);
-      if (t < 3) atomicMin(a.ctrl + kCtrlBbox + t, x);
-      else atomicMax(a.ctrl + kCtrlBboxMax + t - 3, x);
+      if (lane == 0) s_bb[e] = x;
     }
   }
-  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-
-  // ---- Morton keys.  The grid coordinates of the bbox maximum bound every
-  // coordinate, so their Morton code bounds the bit length of every key.
+  for (int q = t; q < kBuckets; q += kThreads) {
+    s_cnt[q] = 0u;
+    s_vb[q] = 0ull;
+  }
+  __syncthreads();
   double org[3];
-  for (int ax = 0; ax < 3; ++ax) org[ax] = double(float_from_order_key(get(a.ctrl + kCtrlBbox + ax)));
   unsigned int qmax[3];
-  for (int ax = 0; ax < 3; ++ax)
-    qmax[ax] = grid_coord(float_from_order_key(get(a.ctrl + kCtrlBboxMax + ax)), org[ax], a.grid_scale);
+  for (int ax = 0; ax < 3; ++ax) {
+    org[ax] = double(float_from_order_key(s_bb[ax]));
+    qmax[ax] = grid_coord(float_from_order_key(s_bb[3 + ax]), org[ax], a.grid_scale);
+  }
   const unsigned long long kbound = morton3(qmax[0], qmax[1], qmax[2]);
   const int kbits = kbound ? 64 - __clzll((long long)kbound) : 0;
-  const int tokbits = n > 1 ? 32 - __clz(n - 1) : 0;
-  const int bshift = kbits - min(kBucketBits, kbits);
-  // The bucket pass packs (key, token) into one 64-bit sort value.
-  const bool bucket_ok = kbits + tokbits <= 64 && tile <= kSortCap;
-  {
-    unsigned long long kmax = 0ull;
-    s_hist[t] = 0u;
-    if (bucket_ok)
-      for (int q = t; q < kBuckets; q += kThreads) {
-        s_cnt[q] = 0u;
-        s_wide[q] = 0ull;
-      }
-    __syncthreads();
-    for (int i = p0 + t; i < p1; i += kThreads) {
-      const unsigned int q0 = grid_coord(a.pos[3 * i], org[0], a.grid_scale);
-      const unsigned int q1 = grid_coord(a.pos[3 * i + 1], org[1], a.grid_scale);
-      const unsigned int q2 = grid_coord(a.pos[3 * i + 2], org[2], a.grid_scale);
-      const unsigned long long key = morton3(q0, q1, q2);
-      put(a.key[0] + i, key);
-      put(a.tok[0] + i, i);
-      put(a.vox_tok + i, pack_vox(q0 >> kSubBits, q1 >> kSubBits, q2 >> kSubBits));
-      atomicAdd(&s_hist[unsigned(key & 0xffu)], 1u);
-      kmax = max(kmax, key);
-      if (bucket_ok) {
-        const int bk = bucket_of(key, bshift);
-        s_key[i - p0] = key;
-        s_rank[i - p0] = uint16_t(atomicAdd(&s_cnt[bk], 1u));
-        atomicAdd(&s_wide[bk], capacity_units(a.v[i]));
-      }
-    }
-    for (int o = 32; o > 0; o >>= 1) {
-      const unsigned long long y = __shfl_xor(kmax, o);
-      kmax = max(kmax, y);
-    }
-    if (lane == 0) atomicMax(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey), kmax);
-    __syncthreads();
-    put(a.hist + size_t(blk) * kBins + t, s_hist[t]);   // pass 0: the block's own range, in token order
-    // Bucket counts and capacity sums; each block takes its base inside a
-    // bucket from the returned count (blocks land in any order within a
-    // bucket, which the span sort below puts right).
-    if (bucket_ok)
-      for (int q = t; q < kBuckets; q += kThreads) {
-        const unsigned int c = s_cnt[q];
-        if (c) {
-          s_cnt[q] = __hip_atomic_fetch_add(a.bcnt + q, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          __hip_atomic_fetch_add(a.bval + q, s_wide[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-      }
+  const int bshift = bucket_shift(kbits);
+  if (blk == 0 && t == 0) {
+    a.geom[0] = org[0];
+    a.geom[1] = org[1];
+    a.geom[2] = org[2];
+    a.geom[3] = double(kbits);
   }
-  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-
-  // ---- bucket starts and every block's span of whole buckets: the buckets
-  // that start in [b * tile, (b + 1) * tile).  When every span fits in LDS,
-  // each element goes straight to its bucket slot and each block sorts its
-  // span; otherwise the LSD radix sort below runs.
-  bool fast = false;
-  int r0 = p0, r1 = p1;            // the positions this block owns from here on
-  unsigned long long run = 0ull;   // capacity units before position r0
-  unsigned long long W = 0ull;     // all capacity units
-  if (bucket_ok) {
-    unsigned int c[kPerThread];
-    unsigned long long vb[kPerThread];
-#pragma unroll
-    for (int j = 0; j < kPerThread; ++j) {
-      c[j] = get(a.bcnt + t * kPerThread + j);
-      vb[j] = get(a.bval + t * kPerThread + j);
-    }
-    unsigned long long csum = 0ull;
-#pragma unroll
-    for (int j = 0; j < kPerThread; ++j) csum += c[j];
-    unsigned long long ctot;
-    unsigned int st = unsigned(block_excl_sum_u64(csum, s_u64, ctot));
-    unsigned int* s_start = reinterpret_cast<unsigned int*>(s_wide);
-#pragma unroll
-    for (int j = 0; j < kPerThread; ++j) {
-      s_start[t * kPerThread + j] = st;
-      st += c[j];
-    }
-    __syncthreads();
-    if (t <= G) {
-      const unsigned int target = unsigned(min(n, t * tile));
-      int lo = 0, hi = kBuckets;   // first bucket starting at or after target
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (s_start[mid] < target) lo = mid + 1;
-        else hi = mid;
-      }
-      s_span[t] = lo < kBuckets ? int(s_start[lo]) : n;
-      s_first[t] = lo;
-    }
-    __syncthreads();
-    if (t == 0) {
-      int big = 0;
-      for (int b = 0; b < G; ++b) big = max(big, s_span[b + 1] - s_span[b]);
-      s_fast = big <= kSortCap;
-    }
-    __syncthreads();
-    fast = s_fast != 0;
-    if (fast) {
-      for (int i = p0 + t; i < p1; i += kThreads) {
-        const unsigned long long key = s_key[i - p0];
-        const int bk = bucket_of(key, bshift);
-        put(a.key[1] + s_start[bk] + s_cnt[bk] + s_rank[i - p0], (key << tokbits) | (unsigned long long)i);
-      }
-      const int fb = s_first[blk];
-      unsigned long long below = 0ull, all = 0ull;
-#pragma unroll
-      for (int j = 0; j < kPerThread; ++j) {
-        if (t * kPerThread + j < fb) below += vb[j];
-        all += vb[j];
-      }
-      run = block_sum_u64(below, s_u64);
-      W = block_sum_u64(all, s_u64);
-      r0 = s_span[blk];
-      r1 = s_span[blk + 1];
+  for (int i = r.p0 + t; i < r.p1; i += kThreads) {
+    const unsigned long long key = morton3(grid_coord(a.pos[3 * i], org[0], a.grid_scale),
+                                           grid_coord(a.pos[3 * i + 1], org[1], a.grid_scale),
+                                           grid_coord(a.pos[3 * i + 2], org[2], a.grid_scale));
+    a.key[0][i] = key;
+    const int bk = bucket_of(key, bshift);
+    a.within[i] = atomicAdd(&s_cnt[bk], 1u);
+    atomicAdd(&s_vb[bk], capacity_units(a.v[i]));
+  }
+  __syncthreads();
+  for (int q = t; q < kBuckets; q += kThreads) {
+    const unsigned int c = s_cnt[q];
+    if (c) {
+      s_cnt[q] = __hip_atomic_fetch_add(a.bcnt + q, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_add(a.bval + q, s_vb[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
+  __syncthreads();
+  // Each thread revisits its own tokens (its own stores, read back).
+  for (int i = r.p0 + t; i < r.p1; i += kThreads) a.within[i] += s_cnt[bucket_of(a.key[0][i], bshift)];
+}
 
-  int sorted;
-  // Positions r0 + i of a sorted span, thread t taking i in [t per, t per + per).
-  const int span_m = r1 - r0;
-  int per = 1;
-  while (kThreads * per < span_m) per <<= 1;
-  const int i0 = min(span_m, t * per), i1 = min(span_m, t * per + per);
-  if (fast) {
-    if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-    // ---- sort the span by (key, token), write the permutation and the
-    // voxels by position, and the group offsets tp - p of its positions
-    // (Eq. 17 in scan form), kept in LDS with the tokens for the next phase
-    const unsigned long long tmask = tokbits ? (~0ull >> (64 - tokbits)) : 0ull;
-    int bmin = INT_MAX;
-    if (span_m > 0) {
-      const unsigned long long* src = a.key[1] + r0;
+// 3. Bucket starts (an exclusive scan of the counts), the spans (block b
+// owns the whole buckets that start in [b tile, (b + 1) tile)), the capacity
+// units before each span (from the bucket sums), and every token placed in
+// its bucket: key[1] / tok[0] at bucket start + place.
+__global__ __launch_bounds__(kThreads) void lite_place_kernel(LiteDev a) {
+  const int t = threadIdx.x, blk = blockIdx.x, G = gridDim.x, n = a.n;
+  const FrontRange r = front_range(n);
+  __shared__ unsigned int s_start[kBuckets];
+  __shared__ unsigned long long s_u64[kThreads + 2];
+  __shared__ int s_first;
+  const int bshift = bucket_shift(int(a.geom[3]));
+  unsigned int c[kPerThread];
+  unsigned long long vb[kPerThread];
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    c[j] = a.bcnt[t * kPerThread + j];
+    vb[j] = a.bval[t * kPerThread + j];
+  }
+  unsigned long long csum = 0ull;
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) csum += c[j];
+  unsigned long long ctot;
+  unsigned int st = unsigned(block_excl_sum_u64(csum, s_u64, ctot));
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    s_start[t * kPerThread + j] = st;
+    st += c[j];
+  }
+  __syncthreads();
+  if (t <= G) {
+    const unsigned int target = unsigned(min(n, t * r.tile));
+    int lo = 0, hi = kBuckets;   // first bucket starting at or after target
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (s_start[mid] < target) lo = mid + 1;
+      else hi = mid;
+    }
+    if (blk == 0) a.span[t] = lo < kBuckets ? int(s_start[lo]) : n;
+    if (t == blk) s_first = lo;
+  }
+  __syncthreads();
+  const int fb = s_first;
+  unsigned long long below = 0ull, all = 0ull;
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    if (t * kPerThread + j < fb) below += vb[j];
+    all += vb[j];
+  }
+  const unsigned long long run = block_sum_u64(below, s_u64);
+  const unsigned long long W = block_sum_u64(all, s_u64);
+  if (t == 0) {
+    a.span_run[blk] = run;
+    if (blk == 0) *reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlW) = W;
+  }
+  for (int i = r.p0 + t; i < r.p1; i += kThreads) {
+    const unsigned long long key = a.key[0][i];
+    const unsigned int slot = s_start[bucket_of(key, bshift)] + a.within[i];
+    a.key[1][slot] = key;
+    a.tok[0][slot] = i;
+  }
+}
+
+// A span too long for the register sort, or whose keys do not pack with a
+// token index: a stable LSD radix sort of its (key, token) pairs in 8-bit
+// digits, the token's digits first, inside the block, then the positions'
+// tokens, voxels and group offsets chunk by chunk (the same terms as
+// span_offsets).  Data moves between (key[1], tok[0]) and (key[0], tok[1])
+// over the span's positions, which no other block touches; it ends in
+// tok[1].  Returns the thread's minimum tp - p.
+__device__ int span_radix(const LiteDev& a, int r0, int m, int kbits, int tokbits, const double (&org)[3],
+                          unsigned long long run, unsigned long long W, unsigned long long* s_u64,
+                          unsigned int* s_base, unsigned int (*s_wcnt)[kBins]) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int tpass = (tokbits + 7) / 8, passes = tpass + (kbits + 7) / 8;
+  for (int pass = 0; pass < passes; ++pass) {
+    const int src = pass & 1;
+    const unsigned long long* ks = (src ? a.key[0] : a.key[1]) + r0;
+    const int* ts = (src ? a.tok[1] : a.tok[0]) + r0;
+    unsigned long long* kd = (src ? a.key[1] : a.key[0]) + r0;
+    int* td = (src ? a.tok[0] : a.tok[1]) + r0;
+    auto digit = [&](unsigned long long k, int tk) {
+      return pass < tpass ? unsigned(tk >> (8 * pass)) & 0xffu : unsigned(k >> (8 * (pass - tpass))) & 0xffu;
+    };
+    // Digit counts over the span, then every digit's first slot.
+    s_base[t] = 0u;
+    __syncthreads();
+    for (int i = t; i < m; i += kThreads) atomicAdd(&s_base[digit(get(ks + i), get(ts + i))], 1u);
+    __syncthreads();
+    {
+      const unsigned int cnt = s_base[t];
+      unsigned long long total;
+      const unsigned long long ex = block_excl_sum_u64(cnt, s_u64, total);
+      s_base[t] = unsigned(ex);
+    }
+    __syncthreads();
+    // Stable scatter, 256 items per round: rank among equal digits inside a
+    // wave from ballots, then across the block's waves through LDS.
+    for (int c0 = 0; c0 < m; c0 += kThreads) {
+      const int i = c0 + t;
+      const bool live = i < m;
+      const unsigned long long kv = live ? get(ks + i) : 0ull;
+      const int tv = live ? get(ts + i) : 0;
+      const unsigned int dig = digit(kv, tv);
+      unsigned long long same = __ballot(live);
+      for (int bit = 0; bit < 8; ++bit) {
+        const unsigned long long mb = __ballot(live && ((dig >> bit) & 1u));
+        same &= ((dig >> bit) & 1u) ? mb : ~mb;
+      }
+      const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+      const int rank = __popcll(same & below);
+      for (int q = t; q < kWaves * kBins; q += kThreads) (&s_wcnt[0][0])[q] = 0u;
+      __syncthreads();
+      if (live && rank == 0) s_wcnt[w][dig] = unsigned(__popcll(same));
+      __syncthreads();
+      if (live) {
+        unsigned int off = s_base[dig];
+        for (int q = 0; q < w; ++q) off += s_wcnt[q][dig];
+        put(kd + off + rank, kv);
+        put(td + off + rank, tv);
+      }
+      __syncthreads();
+      unsigned int add = 0u;
+      for (int q = 0; q < kWaves; ++q) add += s_wcnt[q][t];
+      s_base[t] += add;
+      __syncthreads();
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this pass's stores are done before the next reads them
+    __syncthreads();
+  }
+  // An even number of passes left the tokens in tok[0]: move them.
+  if ((passes & 1) == 0) {
+    for (int i = t; i < m; i += kThreads) put(a.tok[1] + r0 + i, get(a.tok[0] + r0 + i));
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
+  }
+  const unsigned long long KK = (unsigned long long)a.k;
+  const double kw = W ? double(a.k) / double(W) : 0.0;
+  int bmin = INT_MAX;
+  for (int c0 = 0; c0 < m; c0 += kThreads) {
+    const int i = c0 + t;
+    const int pos = r0 + i;
+    const int tk = i < m ? get(a.tok[1] + pos) : 0;
+    const unsigned long long V = i < m ? capacity_units(a.v[tk]) : 0ull;
+    unsigned long long chunk;
+    const unsigned long long ex = block_excl_sum_u64(V, s_u64, chunk);
+    if (i < m) {
+      a.vox_pos[pos] = pack_vox(grid_coord(a.pos[3 * tk], org[0], a.grid_scale) >> kSubBits,
+                                grid_coord(a.pos[3 * tk + 1], org[1], a.grid_scale) >> kSubBits,
+                                grid_coord(a.pos[3 * tk + 2], org[2], a.grid_scale) >> kSubBits);
+      long long tp;
+      if (pos == 0) tp = 0;
+      else if (W == 0ull) tp = a.k - 1;
+      else tp = thresholds_crossed(KK, run + ex, W, kw);
+      const int mm = int(tp - pos);
+      a.gid[pos] = mm;
+      bmin = min(bmin, mm);
+    }
+    run += chunk;
+  }
+  return bmin;
+}
+
+// 4. Each block sorts its span by (key, token) -- in registers when it holds
+// at most kSortCap tokens and key and token pack into 64 bits, else with
+// span_radix -- and writes the permutation, the voxels by position and the
+// group offsets tp - p of its positions (Eq. 17 in scan form), and its
+// minimum offset.
+__global__ __launch_bounds__(kThreads) void lite_sort_kernel(LiteDev a) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6, blk = blockIdx.x;
+  __shared__ unsigned long long s_a[kSortCap], s_b[kSortCap];
+  __shared__ unsigned long long s_u64[kThreads + 2];
+  __shared__ unsigned int s_base[kBins];
+  __shared__ unsigned int s_wcnt[kWaves][kBins];
+  __shared__ int s_i32[kWaves];
+  const int r0 = a.span[blk], m = a.span[blk + 1] - r0;
+  const unsigned long long run = a.span_run[blk];
+  const unsigned long long W = *reinterpret_cast<const unsigned long long*>(a.ctrl + kCtrlW);
+  const double org[3] = {a.geom[0], a.geom[1], a.geom[2]};
+  const int kbits = int(a.geom[3]), tokbits = tok_bits(a.n);
+  int bmin = INT_MAX;
+  if (m > 0) {
+    if (m <= kSortCap && kbits + tokbits <= 64) {
+      int per = 1;
+      while (kThreads * per < m) per <<= 1;
+      const int i0 = min(m, t * per), i1 = min(m, t * per + per);
+      const unsigned long long tmask = tokbits ? (~0ull >> (64 - tokbits)) : 0ull;
+      const unsigned long long* ks = a.key[1] + r0;
+      const int* ts = a.tok[0] + r0;
       switch (per) {
         case 1:
-          span_sort<1>(src, span_m, s_wide, s_key);
-          bmin = span_offsets<1>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          span_sort<1>(ks, ts, tokbits, m, s_a, s_b);
+          bmin = span_offsets<1>(a, r0, m, i0, i1, tmask, org, run, W, s_a, s_u64);
           break;
         case 2:
-          span_sort<2>(src, span_m, s_wide, s_key);
-          bmin = span_offsets<2>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          span_sort<2>(ks, ts, tokbits, m, s_a, s_b);
+          bmin = span_offsets<2>(a, r0, m, i0, i1, tmask, org, run, W, s_a, s_u64);
           break;
         case 4:
-          span_sort<4>(src, span_m, s_wide, s_key);
-          bmin = span_offsets<4>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          span_sort<4>(ks, ts, tokbits, m, s_a, s_b);
+          bmin = span_offsets<4>(a, r0, m, i0, i1, tmask, org, run, W, s_a, s_u64);
           break;
         case 8:
-          span_sort<8>(src, span_m, s_wide, s_key);
-          bmin = span_offsets<8>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          span_sort<8>(ks, ts, tokbits, m, s_a, s_b);
+          bmin = span_offsets<8>(a, r0, m, i0, i1, tmask, org, run, W, s_a, s_u64);
           break;
         default:
-          span_sort<16>(src, span_m, s_wide, s_key);
-          bmin = span_offsets<16>(a, r0, span_m, i0, i1, tmask, org, run, W, s_wide, s_key, s_u64);
+          span_sort<16>(ks, ts, tokbits, m, s_a, s_b);
+          bmin = span_offsets<16>(a, r0, m, i0, i1, tmask, org, run, W, s_a, s_u64);
           break;
       }
+    } else {
+      bmin = span_radix(a, r0, m, kbits, tokbits, org, run, W, s_u64, s_base, s_wcnt);
     }
-    bmin = wave_min(bmin);
-    if (lane == 0) s_i32[w] = bmin;
-    __syncthreads();
-    if (t == 0) {
-      int mm = s_i32[0];
-      for (int q = 1; q < kWaves; ++q) mm = min(mm, s_i32[q]);
-      put(a.bmin + blk, mm);
-    }
-    sorted = 1;
-  } else {
-    // ---- stable LSD radix sort of (key, token), 8 bits per pass
-    const unsigned long long maxkey = get(reinterpret_cast<unsigned long long*>(a.ctrl + kCtrlMaxKey));
-    const int bits = maxkey ? 64 - __clzll((long long)maxkey) : 0;
-    const int passes = (bits + 7) / 8;
-    for (int pass = 0; pass < passes; ++pass) {
-      const int src = pass & 1, sh = 8 * pass;
-      const unsigned long long* ks = src ? a.key[1] : a.key[0];
-      const int* ts = src ? a.tok[1] : a.tok[0];
-      unsigned long long* kd = src ? a.key[0] : a.key[1];
-      int* td = src ? a.tok[0] : a.tok[1];
-      const unsigned int* hist = a.hist + size_t(pass) * G * kBins;
-      // Base offset of digit t for this block: every smaller digit anywhere,
-      // plus digit t in earlier blocks (all G counts read in one round trip).
-      {
-        unsigned int tot = 0u, pre = 0u;
-        unsigned int h[kFrontBlocks];
-#pragma unroll
-        for (int x = 0; x < kFrontBlocks; ++x) h[x] = x < G ? get(hist + x * kBins + t) : 0u;
-#pragma unroll
-        for (int x = 0; x < kFrontBlocks; ++x) {
-          tot += h[x];
-          if (x < blk) pre += h[x];
-        }
-        unsigned long long total;
-        const unsigned long long ex = block_excl_sum_u64(tot, s_u64, total);
-        s_base[t] = unsigned(ex) + pre;
-      }
-      __syncthreads();
+  }
+  bmin = wave_min(bmin);
+  if (lane == 0) s_i32[w] = bmin;
+  __syncthreads();
+  if (t == 0) {
+    int mm = s_i32[0];
+    for (int q = 1; q < kWaves; ++q) mm = min(mm, s_i32[q]);
+    a.bmin[blk] = mm;
+  }
+}
 
-      // Stable scatter, 256 items per round: rank among equal digits inside a
-      // wave from ballots, then across the block's waves through LDS.  The
-      // next round's element is loaded while this one is placed.
-      unsigned long long kn = p0 + t < p1 ? get(ks + p0 + t) : 0ull;
-      int tn = p0 + t < p1 ? get(ts + p0 + t) : 0;
-      for (int c0 = p0; c0 < p1; c0 += kThreads) {
-        const int i = c0 + t;
-        const bool live = i < p1;
-        const unsigned long long kv = kn;
-        const int tv = tn;
-        if (i + kThreads < p1) {
-          kn = get(ks + i + kThreads);
-          tn = get(ts + i + kThreads);
-        }
-        const unsigned int dig = unsigned((kv >> sh) & 0xffu);
-        unsigned long long same = __ballot(live);
-        for (int bit = 0; bit < 8; ++bit) {
-          const unsigned long long mb = __ballot(live && ((dig >> bit) & 1u));
-          same &= ((dig >> bit) & 1u) ? mb : ~mb;
-        }
-        const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-        const int rank = __popcll(same & below);
-        for (int q = t; q < kWaves * kBins; q += kThreads) (&s_wcnt[0][0])[q] = 0u;
-        __syncthreads();
-        if (live && rank == 0) s_wcnt[w][dig] = unsigned(__popcll(same));
-        __syncthreads();
-        if (live) {
-          unsigned int off = s_base[dig];
-          for (int q = 0; q < w; ++q) off += s_wcnt[q][dig];
-          put(kd + off + rank, kv);
-          put(td + off + rank, tv);
-          // The next pass's digit of this element, counted for the range
-          // that receives it.
-          if (pass + 1 < passes)
-            __hip_atomic_fetch_add(a.hist + (size_t(pass + 1) * G + (off + rank) / tile) * kBins +
-                                       unsigned((kv >> (sh + 8)) & 0xffu),
-                                   1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        __syncthreads();
-        unsigned int add = 0u;
-        for (int q = 0; q < kWaves; ++q) add += s_wcnt[q][t];
-        s_base[t] += add;
-        __syncthreads();
-      }
-      if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-    }
-    sorted = passes & 1;
-    const int* perm = sorted ? a.tok[1] : a.tok[0];
+// 5. Groups of the span's positions: the prefix minimum of the offsets
+// (earlier blocks, earlier threads, then this thread's positions in order)
+// gives each position's group (the walk of Eq. 17 in scan form); group
+// starts where the group changes; the group output.
+__global__ __launch_bounds__(kThreads) void lite_groups_kernel(LiteDev a) {
+  const int t = threadIdx.x, blk = blockIdx.x, n = a.n, K = a.k;
+  __shared__ int s_i32[kThreads];
+  __shared__ int s_minoff;
+  const int r0 = a.span[blk], m = a.span[blk + 1] - r0;
+  s_i32[t] = t < blk ? a.bmin[t] : INT_MAX;
+  __syncthreads();
+  if (t == 0) {
+    int mm = INT_MAX;
+    for (int b = 0; b < blk; ++b) mm = min(mm, s_i32[b]);
+    s_minoff = mm;
+  }
+  __syncthreads();
+  if (m <= 0) return;
+  const int per = (m + kThreads - 1) / kThreads;
+  const int i0 = min(m, t * per), i1 = min(m, t * per + per);
+  int lmin = INT_MAX;
+  for (int i = i0; i < i1; ++i) lmin = min(lmin, a.gid[r0 + i]);
+  const int incl = block_incl_min(lmin, s_i32);
+  s_i32[t] = incl;
+  __syncthreads();
+  int cur = min(s_minoff, t > 0 ? s_i32[t - 1] : INT_MAX);   // prefix minimum before position r0 + i0
+  int qprev = r0 + i0 > 0 ? max(K - n + r0 + i0 - 1, r0 + i0 - 1 + cur) : -1;
+  for (int i = i0; i < i1; ++i) {
+    const int pos = r0 + i;
+    cur = min(cur, a.gid[pos]);
+    const int q = max(K - n + pos, pos + cur);
+    if (q != qprev) a.gstart[q] = pos;
+    if (pos == n - 1) a.gstart[K] = n;
+    if (a.group) a.group[a.tok[1][pos]] = q;
+    qprev = q;
+  }
+}
 
-    // ---- groups: exclusive scan of V over sorted positions
-    {
-      unsigned long long local = 0ull;
-      for (int i = p0 + t; i < p1; i += kThreads) local += capacity_units(a.v[get(perm + i)]);
-      unsigned long long tot;
-      block_excl_sum_u64(local, s_u64, tot);
-      if (t == 0) put(a.bsum + blk, tot);
-    }
-    if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-    {
-      block_prefix_u64(a.bsum, G, blk, s_u64, run, W);
-      const unsigned long long KK = (unsigned long long)K;
-      const double kw = W ? double(K) / double(W) : 0.0;
-      int bmin = INT_MAX;
-      for (int c0 = p0; c0 < p1; c0 += kThreads) {
-        const int i = c0 + t;
-        const unsigned long long V = i < p1 ? capacity_units(a.v[get(perm + i)]) : 0ull;
-        unsigned long long chunk;
-        const unsigned long long ex = block_excl_sum_u64(V, s_u64, chunk);
-        if (i < p1) {
-          long long tp;
-          if (i == 0) tp = 0;
-          else if (W == 0ull) tp = K - 1;
-          else tp = thresholds_crossed(KK, run + ex, W, kw);
-          const int m = int(tp - i);
-          put(a.gid + i, m);
-          bmin = min(bmin, m);
-        }
-        run += chunk;
-      }
-      bmin = wave_min(bmin);
-      if (lane == 0) s_i32[w] = bmin;
-      __syncthreads();
-      if (t == 0) {
-        int m = s_i32[0];
-        for (int q = 1; q < kWaves; ++q) m = min(m, s_i32[q]);
-        put(a.bmin + blk, m);
-      }
-    }
-  }
-  const int* perm = sorted ? a.tok[1] : a.tok[0];
-  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-  {
-    s_i32[t] = t < blk ? get(a.bmin + t) : INT_MAX;
-    __syncthreads();
-    if (t == 0) {
-      int m = INT_MAX;
-      for (int b = 0; b < blk; ++b) m = min(m, s_i32[b]);
-      s_minoff = m;
-    }
-    __syncthreads();
-  }
-  if (fast) {
-    // ---- groups of the span's positions: prefix minimum of the offsets
-    // (earlier blocks, earlier threads, then this thread's positions in
-    // order), group starts where the group changes, the group output
-    int lmin = INT_MAX;
-    for (int i = i0; i < i1; ++i) lmin = min(lmin, int(unsigned(s_key[i] >> 32)));
-    const int incl = block_incl_min(lmin, s_i32);
-    s_i32[t] = incl;
-    __syncthreads();
-    int cur = min(s_minoff, t > 0 ? s_i32[t - 1] : INT_MAX);   // prefix minimum before position r0 + i0
-    __syncthreads();
-    int qprev = r0 + i0 > 0 ? max(K - n + r0 + i0 - 1, r0 + i0 - 1 + cur) : -1;
-    for (int i = i0; i < i1; ++i) {
-      const int pos = r0 + i;
-      const unsigned long long e = s_key[i];
-      cur = min(cur, int(unsigned(e >> 32)));
-      const int q = max(K - n + pos, pos + cur);
-      if (q != qprev) put(a.gstart + q, pos);
-      if (pos == n - 1) put(a.gstart + K, n);
-      put(a.gid + pos, q);
-      if (a.group) a.group[int(unsigned(e))] = q;
-      qprev = q;
-    }
-  } else {
-    int run_min = s_minoff;
-    // Group starts, voxels by sorted position and the group output in the
-    // same pass: a position starts a group when its group differs from the
-    // one before it.  Position r0 - 1 lies in an earlier block's range, and
-    // its group follows from the same prefix minimum (s_minoff covers every
-    // position before r0).
-    __shared__ int s_gid[kThreads];
-    int gprev = blk > 0 && r0 > 0 ? max(K - n + r0 - 1, r0 - 1 + s_minoff) : -1;
-    for (int c0 = r0; c0 < r1; c0 += kThreads) {
-      const int i = c0 + t;
-      const int m = i < r1 ? get(a.gid + i) : INT_MAX;
-      const int inc = min(block_incl_min(m, s_i32), run_min);
-      const int q = i < r1 ? max(K - n + i, i + inc) : -1;
-      if (i < r1) put(a.gid + i, q);
-      s_i32[t] = inc;
-      s_gid[t] = q;
-      __syncthreads();
-      run_min = s_i32[kThreads - 1];
-      if (i < r1) {
-        const int qb = t > 0 ? s_gid[t - 1] : gprev;
-        if (i == 0 || qb != q) put(a.gstart + q, i);
-        if (i == n - 1) put(a.gstart + K, n);
-        const int tokn = get(perm + i);
-        put(a.vox_pos + i, get(a.vox_tok + tokn));
-        if (a.group) a.group[tokn] = q;
-      }
-      gprev = s_gid[kThreads - 1];
-      __syncthreads();
-    }
-  }
-  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
-  // ---- tiles per group, and tiles of big groups (block sums)
+// 6. Tiles per group and tiles of big groups, summed per block of groups.
+__global__ __launch_bounds__(kThreads) void lite_tile_sums_kernel(LiteDev a) {
+  const int t = threadIdx.x, blk = blockIdx.x, G = gridDim.x, K = a.k;
+  __shared__ unsigned long long s_u64[kThreads + 2];
   const int gtile = (K + G - 1) / G;
   const int q0 = min(K, blk * gtile), q1 = min(K, q0 + gtile);
-  {
-    unsigned long long local = 0ull, lbig = 0ull;
-    for (int q = q0 + t; q < q1; q += kThreads) {
-      const int g = max(0, get(a.gstart + q + 1) - get(a.gstart + q));
-      const int nt = (g + kTileRows - 1) / kTileRows;
-      local += (unsigned long long)nt;
-      lbig += nt > kSplitTiles ? (unsigned long long)nt : 0ull;
-    }
-    unsigned long long tot, tbig;
-    block_excl_sum_u64(local, s_u64, tot);
-    block_excl_sum_u64(lbig, s_u64, tbig);
-    if (t == 0) {
-      put(a.bsum + blk, tot);
-      put(a.bsum2 + blk, tbig);
-    }
+  unsigned long long local = 0ull, lbig = 0ull;
+  for (int q = q0 + t; q < q1; q += kThreads) {
+    const int g = max(0, a.gstart[q + 1] - a.gstart[q]);
+    const int nt = (g + kTileRows - 1) / kTileRows;
+    local += (unsigned long long)nt;
+    lbig += nt > kSplitTiles ? (unsigned long long)nt : 0ull;
   }
-  if (!grid_barrier(bar, ++round, abort, a.poll_limit, &s_ok)) return;
+  unsigned long long tot, tbig;
+  block_excl_sum_u64(local, s_u64, tot);
+  block_excl_sum_u64(lbig, s_u64, tbig);
+  if (t == 0) {
+    a.bsum[blk] = tot;
+    a.bsum2[blk] = tbig;
+  }
+}
 
-  // ---- tile prefix per group, the group of every tile and the list of big
-  // groups' tiles (work units of the pair kernels)
-  {
-    unsigned long long run, tot, rbig, tbig;
-    block_prefix_u64(a.bsum, G, blk, s_u64, run, tot);
-    block_prefix_u64(a.bsum2, G, blk, s_u64, rbig, tbig);
-    if (blk == 0 && t == 0) {
-      put(a.ctrl + kCtrlTiles, unsigned(tot));
-      put(a.ctrl + kCtrlBig, unsigned(tbig));
-    }
-    for (int c0 = q0; c0 < q1; c0 += kThreads) {
-      const int q = c0 + t;
-      int nt = 0;
-      if (q < q1) {
-        const int g = max(0, get(a.gstart + q + 1) - get(a.gstart + q));
-        nt = (g + kTileRows - 1) / kTileRows;
-      }
-      const int nb = nt > kSplitTiles ? nt : 0;
-      unsigned long long chunk, cbig;
-      const unsigned long long ex = block_excl_sum_u64((unsigned long long)nt, s_u64, chunk);
-      const unsigned long long exb = block_excl_sum_u64((unsigned long long)nb, s_u64, cbig);
-      if (q < q1) {
-        const int u0 = int(run + ex), b0 = int(rbig + exb);
-        a.rt_start[q] = u0;
-        for (int x = 0; x < nt; ++x) a.unit_group[u0 + x] = q;
-        for (int x = 0; x < nb; ++x) a.big_unit[b0 + x] = u0 + x;
-      }
-      if (q == K - 1) a.rt_start[K] = int(run + ex + nt);
-      run += chunk;
-      rbig += cbig;
-    }
+// 7. The tile prefix per group, the group of every tile and the list of big
+// groups' tiles (work units of the pair kernels).
+__global__ __launch_bounds__(kThreads) void lite_tiles_kernel(LiteDev a) {
+  const int t = threadIdx.x, blk = blockIdx.x, G = gridDim.x, K = a.k;
+  __shared__ unsigned long long s_u64[kThreads + 2];
+  const int gtile = (K + G - 1) / G;
+  const int q0 = min(K, blk * gtile), q1 = min(K, q0 + gtile);
+  unsigned long long run, tot, rbig, tbig;
+  block_prefix_u64(a.bsum, G, blk, s_u64, run, tot);
+  block_prefix_u64(a.bsum2, G, blk, s_u64, rbig, tbig);
+  if (blk == 0 && t == 0) {
+    a.ctrl[kCtrlTiles] = unsigned(tot);
+    a.ctrl[kCtrlBig] = unsigned(tbig);
   }
-  if (blk == 0 && t == 0) a.ctrl[kCtrlSorted] = unsigned(sorted);
+  for (int c0 = q0; c0 < q1; c0 += kThreads) {
+    const int q = c0 + t;
+    int nt = 0;
+    if (q < q1) {
+      const int g = max(0, a.gstart[q + 1] - a.gstart[q]);
+      nt = (g + kTileRows - 1) / kTileRows;
+    }
+    const int nb = nt > kSplitTiles ? nt : 0;
+    unsigned long long chunk, cbig;
+    const unsigned long long ex = block_excl_sum_u64((unsigned long long)nt, s_u64, chunk);
+    const unsigned long long exb = block_excl_sum_u64((unsigned long long)nb, s_u64, cbig);
+    if (q < q1) {
+      const int u0 = int(run + ex), b0 = int(rbig + exb);
+      a.rt_start[q] = u0;
+      for (int x = 0; x < nt; ++x) a.unit_group[u0 + x] = q;
+      for (int x = 0; x < nb; ++x) a.big_unit[b0 + x] = u0 + x;
+    }
+    if (q == K - 1) a.rt_start[K] = int(run + ex + nt);
+    run += chunk;
+    rbig += cbig;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1276,11 +1231,10 @@ __device__ __forceinline__ void row_sums(double* arow) {
 
 template <bool BF16>
 __global__ __launch_bounds__(kThreads, 4) void lite_pair_kernel(LiteDev a) {
-  if (a.ctrl[kCtrlAbort]) return;   // the front gave up: its tables are incomplete
   const int lane = threadIdx.x & 63;
   const int gw = blockIdx.x * kWaves + (threadIdx.x >> 6);
   const int nw = gridDim.x * kWaves;
-  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
+  const int* perm = a.tok[1];
   const int units = int(a.ctrl[kCtrlTiles]);
   const int row = lane & 15, quad = lane >> 4;
   PairMax pm;
@@ -1306,10 +1260,9 @@ constexpr int kSplitWaves = 16;
 
 template <bool BF16>
 __global__ __launch_bounds__(kSplitWaves * 64) void lite_pair_split_kernel(LiteDev a) {
-  if (a.ctrl[kCtrlAbort]) return;
   __shared__ double spart[kSplitWaves][kTileRows];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
+  const int* perm = a.tok[1];
   const int nbig = int(a.ctrl[kCtrlBig]);
   const int row = lane & 15, quad = lane >> 4;
   PairMax pm;
@@ -1345,13 +1298,12 @@ __global__ __launch_bounds__(kSplitWaves * 64) void lite_pair_split_kernel(LiteD
 // member of the group from l / 16 on; the four lanes of a row add their sums
 // in a fixed order.
 __global__ __launch_bounds__(kThreads) void lite_b_kernel(LiteDev a) {
-  if (a.ctrl[kCtrlAbort]) return;
   const int lane = threadIdx.x & 63;
   const int row = lane & 15, quad = lane >> 4;
   const int gw = blockIdx.x * kWaves + (threadIdx.x >> 6);
   const int nw = gridDim.x * kWaves;
   const int units = int(a.ctrl[kCtrlTiles]);
-  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
+  const int* perm = a.tok[1];
   const PairMaxima mm = pair_maxima(a);
   const double m_x = sqrt(mm.x2);
   const int m_t = mm.tau;
@@ -1416,14 +1368,7 @@ __global__ __launch_bounds__(kThreads) void lite_select_kernel(LiteDev a) {
   const int lane = threadIdx.x & 63;
   const int q = blockIdx.x * kWaves + (threadIdx.x >> 6);
   if (q >= a.k) return;
-  if (a.ctrl[kCtrlAbort]) {
-    if (lane == 0) {
-      a.selected[q] = -1;
-      a.gcost[q] = __builtin_nan("");
-    }
-    return;
-  }
-  const int* perm = a.ctrl[kCtrlSorted] ? a.tok[1] : a.tok[0];
+  const int* perm = a.tok[1];
   const float m_f = pair_maxima(a).df;
   const double wf = m_f > 0.f ? double(a.lam_f) / double(m_f) : 0.0;
   double best = DBL_MAX;
@@ -1491,16 +1436,16 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   a.group = p.group;
   a.objective = p.objective;
   a.token_cost = p.token_cost;
-  const WaitPolicy wp = wait_policy();
-  a.poll_limit = wp.limit;
-  a.abort_init = wp.preset;
   a.key[0] = reinterpret_cast<unsigned long long*>(w + L.key0);
   a.key[1] = reinterpret_cast<unsigned long long*>(w + L.key1);
   a.tok[0] = reinterpret_cast<int*>(w + L.tok0);
   a.tok[1] = reinterpret_cast<int*>(w + L.tok1);
-  a.vox_tok = reinterpret_cast<unsigned long long*>(w + L.vox_tok);
   a.vox_pos = reinterpret_cast<unsigned long long*>(w + L.vox_pos);
-  a.hist = reinterpret_cast<unsigned int*>(w + L.hist);
+  a.bbox_part = reinterpret_cast<unsigned int*>(w + L.bbox_part);
+  a.within = reinterpret_cast<unsigned int*>(w + L.within);
+  a.span = reinterpret_cast<int*>(w + L.span);
+  a.span_run = reinterpret_cast<unsigned long long*>(w + L.span_run);
+  a.geom = reinterpret_cast<double*>(w + L.geom);
   a.bcnt = reinterpret_cast<unsigned int*>(w + L.bcnt);
   a.bval = reinterpret_cast<unsigned long long*>(w + L.bval);
   a.bsum = reinterpret_cast<unsigned long long*>(w + L.bsum);
@@ -1517,13 +1462,18 @@ hipError_t launch_lite(const LiteParams& p, hipStream_t stream) {
   a.ctrl = reinterpret_cast<unsigned int*>(w + L.ctrl);
   a.pmax = reinterpret_cast<unsigned int*>(w + L.pmax);
 
-  lite_init_kernel<<<1, 64, 0, stream>>>(a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  // The front: seven ordinary launches (a cooperative launch costs about
+  // 20 us more than an ordinary one, and no block of the front waits for
+  // another).
   const int G = std::max(1, std::min(kFrontBlocks, (p.n + kThreads - 1) / kThreads));
-  void* args[] = {&a};
-  e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(lite_front_kernel), dim3(G), dim3(kThreads),
-                                 args, 0, stream);
+  lite_bbox_kernel<<<G, kThreads, 0, stream>>>(a);
+  lite_keys_kernel<<<G, kThreads, 0, stream>>>(a);
+  lite_place_kernel<<<G, kThreads, 0, stream>>>(a);
+  lite_sort_kernel<<<G, kThreads, 0, stream>>>(a);
+  lite_groups_kernel<<<G, kThreads, 0, stream>>>(a);
+  lite_tile_sums_kernel<<<G, kThreads, 0, stream>>>(a);
+  lite_tiles_kernel<<<G, kThreads, 0, stream>>>(a);
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // One wave per 16-row tile; a group has at most n / 16 + 1 tiles in total
   // over all groups, so n / 16 + k waves cover every tile.
